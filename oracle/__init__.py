@@ -1,0 +1,173 @@
+"""CPU oracle of the predict -> route -> prioritize step (ctypes wrapper over liboracle.so).
+
+TEST INFRASTRUCTURE ONLY: the test-suite, the smoke check and the benchmark's CPU-baseline
+leg may use it; the product path (``paper_2606_12950_amd``) never imports it. It shares no
+code with the HIP library. See ``maestro_oracle.c`` for what each function computes and
+which passage of the paper it follows.
+
+Parity status of each function (what pins it, see tests/test_oracle_pins.py):
+  predict    - pinned: closed forms (zero weights -> mean of bin centres, one-hot bias ->
+               that bin's centre), convexity, centre-shift equivariance, Eq. 3 exactly, and a
+               float64 PyTorch forward pass with the same rounding points on small shapes.
+  route      - pinned: brute force via numpy lexsort on tiny inputs, invariants (feasible,
+               sorted, nothing better left out), degenerate cases, node-permutation
+               equivariance.
+  prioritize - pinned: closed forms (unit latencies), numpy stable argsort, O(len^2) suffix
+               sums, half-even rounding cases, int32 clamping, non-finite latency handling.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "maestro_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(verbose: bool = False) -> str:
+    """Compile liboracle.so with gcc (no fast-math, no FMA contraction)."""
+    cmd = ["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.oracle_predict.argtypes = [i32, P, i32, P, P, P, i64, P, P, P, P, i32, P, P, i32]
+    lib.oracle_predict.restype = ctypes.c_int
+    lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
+    lib.oracle_route.restype = ctypes.c_int
+    lib.oracle_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P]
+    lib.oracle_prioritize.restype = ctypes.c_int
+    lib.oracle_round_bf16.argtypes = [f64]
+    lib.oracle_round_bf16.restype = f64
+    lib.oracle_latency_us.argtypes = [ctypes.c_float]
+    lib.oracle_latency_us.restype = ctypes.c_int64
+    lib.oracle_max_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def round_bf16(v: float) -> float:
+    return float(_load().oracle_round_bf16(float(v)))
+
+
+def latency_us(lat_s: float) -> int:
+    return int(_load().oracle_latency_us(float(lat_s)))
+
+
+def predict(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequence[np.ndarray],
+            bin_centre: np.ndarray, prompt_len: np.ndarray, model_id: np.ndarray,
+            kv_bytes_per_token: np.ndarray, dtype: str, n_threads: int = 0):
+    """Returns (pred_len float32 [N], kv_bytes float64 [N]).
+
+    ``x``/``weights`` are float32 arrays (dtype "f32") or uint16 bf16 bit patterns ("bf16")."""
+    lib = _load()
+    dt = 0 if dtype == "f32" else 1
+    store = np.float32 if dt == 0 else np.uint16
+    x = _c(x, store)
+    n = x.shape[0]
+    ws = [_c(w, store) for w in weights]
+    bs = [_c(b, np.float32) for b in biases]
+    L = len(ws)
+    dims = np.array([x.shape[1]] + [w.shape[0] for w in ws], dtype=np.int32)
+    for l, w in enumerate(ws):
+        assert w.shape == (dims[l + 1], dims[l]), "weight shapes must chain [out][in]"
+    wptr = (ctypes.c_void_p * L)(*[w.ctypes.data for w in ws])
+    bptr = (ctypes.c_void_p * L)(*[b.ctypes.data for b in bs])
+    bc = _c(bin_centre, np.float32)
+    pl, mi = _c(prompt_len, np.int32), _c(model_id, np.int32)
+    alpha = _c(kv_bytes_per_token, np.float32)
+    pred = np.empty(n, np.float32)
+    kv = np.empty(n, np.float64)
+    st = lib.oracle_predict(L, _ptr(dims), dt, ctypes.cast(wptr, ctypes.c_void_p),
+                            ctypes.cast(bptr, ctypes.c_void_p), _ptr(bc), n, _ptr(x), _ptr(pl),
+                            _ptr(mi), _ptr(alpha), alpha.shape[0], _ptr(pred), _ptr(kv),
+                            n_threads or max_threads())
+    if st != 0:
+        raise RuntimeError(f"oracle_predict failed with status {st}")
+    return pred, kv
+
+
+def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s, cold_s,
+          resident_mask, k: int = 1, rho: float = 0.0, n_threads: int = 0):
+    """Returns (node_idx int32 [N][k], score float32 [N][k])."""
+    lib = _load()
+    mi = _c(model_id, np.int32)
+    n = mi.shape[0]
+    pr, kv = _c(pred_len, np.float32), _c(kv_bytes, np.float64)
+    dec = _c(decode_s_per_token, np.float32)
+    fr, q, cd = _c(free_bytes, np.float64), _c(queue_s, np.float32), _c(cold_s, np.float32)
+    rm = _c(resident_mask, np.uint64)
+    idx = np.empty((n, k), np.int32)
+    sc = np.empty((n, k), np.float32)
+    st = lib.oracle_route(n, _ptr(mi), _ptr(pr), _ptr(kv), _ptr(dec), dec.shape[0], fr.shape[0],
+                          _ptr(fr), _ptr(q), _ptr(cd), _ptr(rm), float(rho), int(k), _ptr(idx),
+                          _ptr(sc), n_threads or max_threads())
+    if st != 0:
+        raise RuntimeError(f"oracle_route failed with status {st}")
+    return idx, sc
+
+
+def prioritize(chain_offset, stage_latency_s, deadline_us, now_us: int, cursor=None):
+    """Returns (remaining_us int64 [S], slack_key int32 [W], order int32 [W])."""
+    lib = _load()
+    off = _c(chain_offset, np.int64)
+    W = off.shape[0] - 1
+    lat = _c(stage_latency_s, np.float32)
+    S = lat.shape[0]
+    dl = _c(deadline_us, np.int64)
+    cur = None if cursor is None else _c(cursor, np.int32)
+    rem = np.empty(S, np.int64)
+    key = np.empty(W, np.int32)
+    order = np.empty(W, np.int32)
+    st = lib.oracle_prioritize(W, S, _ptr(off), _ptr(lat), _ptr(cur), _ptr(dl), int(now_us),
+                               _ptr(rem), _ptr(key), _ptr(order))
+    if st != 0:
+        raise RuntimeError(f"oracle_prioritize failed with status {st}")
+    return rem, key, order
+
+
+def predict_workload(wl, rows: Optional[np.ndarray] = None, n_threads: int = 0):
+    """Oracle predict over a Workload (optionally only the stage indices ``rows``)."""
+    sel = slice(None) if rows is None else rows
+    return predict(wl.x[sel], wl.weights, wl.biases, wl.bin_centre, wl.prompt_len[sel],
+                   wl.model_id[sel], wl.kv_bytes_per_token, wl.spec.dtype, n_threads)
+
+
+def route_workload(wl, pred_len, kv_bytes, rows: Optional[np.ndarray] = None, n_threads: int = 0):
+    """Oracle route of a Workload's stages given their predictions (``pred_len``/``kv_bytes``
+    indexed like ``rows`` when given)."""
+    mi = wl.model_id if rows is None else wl.model_id[rows]
+    return route(mi, pred_len, kv_bytes, wl.decode_s_per_token, wl.free_bytes, wl.queue_s,
+                 wl.cold_s, wl.resident_mask, k=wl.spec.k, rho=wl.spec.rho, n_threads=n_threads)

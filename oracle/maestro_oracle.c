@@ -1,0 +1,293 @@
+/*
+ * CPU oracle for the batched predict -> route -> prioritize step of Maestro
+ * (cost prediction, Sec. III-B; cross-cluster routing, Sec. III-D and Alg. 3;
+ * remaining-time queue ordering, Sec. III-D, Eq. 7).
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE. Only the test-suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library. It shares no code, header, table or
+ * helper with the HIP library: it is a second, independent statement of what the hot path
+ * computes, written to be read against the paper rather than to be fast.
+ *
+ * Plain definitions, no blocking, fusion or reordering of arithmetic:
+ *   predict    : fp64 forward pass of the stand-in length predictor (a Linear/ReLU MLP over
+ *                length bins), fp64 softmax, expected length = sum_b p_b * centre_b, then
+ *                Eq. 3: R_kv = alpha(M) * (P + L). Hidden activations are rounded to the
+ *                storage type (float32, or bfloat16 round-to-nearest-even) after bias and ReLU,
+ *                as a network that stores its hidden layers in that type does.
+ *   route      : the definition of "best feasible node" in Alg. 3, batched: keep nodes whose
+ *                free bytes admit R_need = (1 + rho) * R_kv (FilterByPolicyAndFeasibility),
+ *                score each with the expected completion latency T_q + T_act + t_dec * L
+ *                (Eq. 6 plus the decode term of Eq. 2, RTT = eta = 0), and return the k
+ *                smallest (score, node index) pairs in lexicographic order. The strict ">" of
+ *                Alg. 3 keeps the first of equal scores, i.e. the lowest index.
+ *   prioritize : per-stage latency quantised to integer microseconds, suffix sums along each
+ *                workflow chain (Eq. 7 with the future term taken as the sum of the later
+ *                stages' predicted latencies), slack = deadline - now - remaining, clamped to
+ *                int32, then a stable ascending sort of workflows by slack.
+ *
+ * Parallelism: OpenMP over independent stages only (predict, route); every stage's
+ * arithmetic is the same sequential code whatever the thread count. prioritize is sequential.
+ *
+ * Build: gcc -O2 -fPIC -shared -fopenmp -ffp-contract=off (no fast-math), x86-64 SSE math.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <omp.h>
+
+#define ORACLE_OK 0
+#define ORACLE_BAD_ARG 1
+#define ORACLE_NO_MEM 2
+
+/* Largest |latency| in microseconds a stage may carry (about 12.7 days); larger finite values
+ * are clamped so that suffix sums of chains up to 2^22 stages stay exact in int64. */
+#define LAT_US_LIMIT ((int64_t)1 << 40)
+/* Marker of a non-finite (unroutable, infinitely late) latency; absorbing under addition. */
+#define LAT_SAT INT64_MAX
+
+/* ------------------------------------------------------------------------------------------ */
+/* value conversions                                                                          */
+/* ------------------------------------------------------------------------------------------ */
+
+static double bf16_bits_to_double(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* Round a double to the nearest bfloat16 value (8 significant bits, exponent range of
+ * float32), ties to even, returned as a double. Written from the format's definition. */
+double oracle_round_bf16(double v) {
+  if (v == 0.0 || isnan(v) || isinf(v)) return v;
+  double a = fabs(v);
+  int e;
+  frexp(a, &e);                    /* a = m * 2^e, m in [0.5, 1) */
+  int q = e - 8;                   /* quantum 2^q keeps 8 significant bits */
+  if (q < -133) q = -133;          /* subnormal bfloat16 quantum */
+  double r = nearbyint(ldexp(a, -q)); /* default rounding mode: to nearest, ties to even */
+  double out = ldexp(r, q);
+  const double max_bf16 = ldexp(255.0, 120); /* (2 - 2^-7) * 2^127 */
+  if (out > max_bf16) out = INFINITY;
+  return v < 0 ? -out : out;
+}
+
+static double round_hidden(double v, int32_t dtype) {
+  return dtype == 0 ? (double)(float)v : oracle_round_bf16(v);
+}
+
+static double stored_value(const void* base, int32_t dtype, int64_t idx) {
+  if (dtype == 0) return (double)((const float*)base)[idx];
+  return bf16_bits_to_double(((const uint16_t*)base)[idx]);
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* predict: Sec. III-B (length predictor stand-in), Eq. 3 (KV demand)                        */
+/* ------------------------------------------------------------------------------------------ */
+
+int oracle_predict(int32_t n_layers, const int32_t* dims, int32_t dtype,
+                   const void* const* weight, const float* const* bias,
+                   const float* bin_centre, int64_t n, const void* x,
+                   const int32_t* prompt_len, const int32_t* model_id,
+                   const float* kv_bytes_per_token, int32_t n_models,
+                   float* pred_len, double* kv_bytes, int32_t n_threads) {
+  if (n_layers < 1 || n_layers > 4 || (dtype != 0 && dtype != 1) || n < 0 || n_models < 1)
+    return ORACLE_BAD_ARG;
+  int32_t widest = 0;
+  for (int l = 0; l <= n_layers; ++l) {
+    if (dims[l] < 1) return ORACLE_BAD_ARG;
+    if (dims[l] > widest) widest = dims[l];
+  }
+  const int32_t D = dims[0], B = dims[n_layers];
+  int status = ORACLE_OK;
+  if (n_threads < 1) n_threads = 1;
+
+#pragma omp parallel num_threads(n_threads)
+  {
+    double* h = (double*)malloc(sizeof(double) * (size_t)widest);
+    double* z = (double*)malloc(sizeof(double) * (size_t)widest);
+    if (!h || !z) {
+#pragma omp atomic write
+      status = ORACLE_NO_MEM;
+    } else {
+#pragma omp for schedule(static)
+      for (int64_t i = 0; i < n; ++i) {
+        /* input features, converted exactly */
+        for (int32_t k = 0; k < D; ++k) h[k] = stored_value(x, dtype, i * (int64_t)D + k);
+        /* Linear layers: z_j = b_j + sum_k W[j][k] h_k, k ascending */
+        for (int l = 0; l < n_layers; ++l) {
+          const int32_t din = dims[l], dout = dims[l + 1];
+          for (int32_t j = 0; j < dout; ++j) {
+            double acc = (double)bias[l][j];
+            for (int32_t k = 0; k < din; ++k)
+              acc += stored_value(weight[l], dtype, (int64_t)j * din + k) * h[k];
+            z[j] = acc;
+          }
+          if (l + 1 < n_layers) {          /* hidden layer: ReLU, stored in dtype */
+            for (int32_t j = 0; j < dout; ++j) h[j] = round_hidden(z[j] > 0.0 ? z[j] : 0.0, dtype);
+          }
+        }
+        /* softmax over bins (max-subtracted), expected length */
+        double mu = z[0];
+        for (int32_t b = 1; b < B; ++b) if (z[b] > mu) mu = z[b];
+        double sum = 0.0;
+        for (int32_t b = 0; b < B; ++b) sum += exp(z[b] - mu);
+        double expect = 0.0;
+        for (int32_t b = 0; b < B; ++b) expect += (exp(z[b] - mu) / sum) * (double)bin_centre[b];
+        float pred = (float)expect;
+        pred_len[i] = pred;
+        /* Eq. 3: R_kv = alpha(M(T)) * (P(T) + L(T)) */
+        int32_t m = model_id[i];
+        double alpha = (m >= 0 && m < n_models) ? (double)kv_bytes_per_token[m] : NAN;
+        kv_bytes[i] = ((double)prompt_len[i] + (double)pred) * alpha;
+      }
+    }
+    free(h);
+    free(z);
+  }
+  return status;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* route: Alg. 3 (filter + best node), Eq. 6 (T_ready), Eq. 2 decode term                    */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct { float s; int32_t n; } cand_t;
+
+static int cand_less(cand_t a, cand_t b) { return a.s < b.s || (a.s == b.s && a.n < b.n); }
+
+int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                 const double* kv_bytes, const float* decode_s_per_token, int32_t n_models,
+                 int32_t n_nodes, const double* free_bytes, const float* queue_s,
+                 const float* cold_s, const uint64_t* resident_mask, double rho, int32_t k,
+                 int32_t* node_idx, float* score, int32_t n_threads) {
+  if (n < 0 || n_nodes < 1 || n_models < 1 || n_models > 64 || k < 1 || rho < 0.0)
+    return ORACLE_BAD_ARG;
+  int status = ORACLE_OK;
+  if (n_threads < 1) n_threads = 1;
+
+#pragma omp parallel num_threads(n_threads)
+  {
+    cand_t* c = (cand_t*)malloc(sizeof(cand_t) * (size_t)n_nodes);
+    unsigned char* taken = (unsigned char*)malloc((size_t)n_nodes);
+    if (!c || !taken) {
+#pragma omp atomic write
+      status = ORACLE_NO_MEM;
+    } else {
+#pragma omp for schedule(static)
+      for (int64_t i = 0; i < n; ++i) {
+        const int32_t m = model_id[i];
+        /* R_need = (1 + rho) * R_kv */
+        const double need = (rho == 0.0) ? kv_bytes[i] : kv_bytes[i] * (1.0 + rho);
+        /* decode term of Eq. 2: t_dec(M) * L, in float32 */
+        const float exec_s = pred_len[i] * decode_s_per_token[m];
+        int32_t nc = 0;
+        for (int32_t nd = 0; nd < n_nodes; ++nd) {
+          if (need > free_bytes[nd]) continue;              /* infeasible: not enough headroom */
+          const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
+          const float act = resident ? 0.0f : cold_s[nd];  /* T_act: cold start unless resident */
+          const float ready = queue_s[nd] + act;            /* Eq. 6: T_ready = T_q + T_act */
+          const float s = ready + exec_s;                   /* expected completion latency */
+          c[nc].s = s;
+          c[nc].n = nd;
+          ++nc;
+        }
+        /* the k smallest (score, index) pairs in lexicographic order */
+        memset(taken, 0, (size_t)nc);
+        for (int32_t r = 0; r < k; ++r) {
+          int32_t best = -1;
+          for (int32_t j = 0; j < nc; ++j)
+            if (!taken[j] && (best < 0 || cand_less(c[j], c[best]))) best = j;
+          if (best >= 0) {
+            taken[best] = 1;
+            node_idx[i * k + r] = c[best].n;
+            score[i * k + r] = c[best].s;
+          } else {
+            node_idx[i * k + r] = -1;
+            score[i * k + r] = INFINITY;
+          }
+        }
+      }
+    }
+    free(c);
+    free(taken);
+  }
+  return status;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* prioritize: Eq. 7 remaining time along a chain, slack against the workflow deadline        */
+/* ------------------------------------------------------------------------------------------ */
+
+/* seconds (float32) -> integer microseconds, round half to even; non-finite -> LAT_SAT */
+int64_t oracle_latency_us(float lat_s) {
+  if (!isfinite(lat_s)) return LAT_SAT;
+  double us = nearbyint((double)lat_s * 1.0e6);
+  if (us > (double)LAT_US_LIMIT) us = (double)LAT_US_LIMIT;
+  if (us < -(double)LAT_US_LIMIT) us = -(double)LAT_US_LIMIT;
+  return (int64_t)us;
+}
+
+static int64_t sat_add(int64_t a, int64_t b) {
+  return (a == LAT_SAT || b == LAT_SAT) ? LAT_SAT : a + b;
+}
+
+typedef struct { int32_t key; int32_t idx; } keyed_t;
+
+static int keyed_cmp(const void* pa, const void* pb) {
+  const keyed_t* a = (const keyed_t*)pa;
+  const keyed_t* b = (const keyed_t*)pb;
+  if (a->key != b->key) return a->key < b->key ? -1 : 1;
+  return (a->idx > b->idx) - (a->idx < b->idx);  /* equal keys keep workflow order */
+}
+
+int oracle_prioritize(int32_t n_workflows, int64_t n_stages, const int64_t* chain_offset,
+                      const float* stage_latency_s, const int32_t* cursor,
+                      const int64_t* deadline_us, int64_t now_us, int64_t* remaining_us,
+                      int32_t* slack_key, int32_t* order) {
+  if (n_workflows < 0 || n_stages < 0) return ORACLE_BAD_ARG;
+  if (n_workflows == 0) return ORACLE_OK;
+  if (chain_offset[0] != 0 || chain_offset[n_workflows] != n_stages) return ORACLE_BAD_ARG;
+  for (int32_t w = 0; w < n_workflows; ++w)
+    if (chain_offset[w + 1] < chain_offset[w]) return ORACLE_BAD_ARG;
+
+  int64_t* rem = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_stages > 0 ? n_stages : 1));
+  keyed_t* kv = (keyed_t*)malloc(sizeof(keyed_t) * (size_t)n_workflows);
+  if (!rem || !kv) { free(rem); free(kv); return ORACLE_NO_MEM; }
+
+  for (int32_t w = 0; w < n_workflows; ++w) {
+    const int64_t first = chain_offset[w], end = chain_offset[w + 1];
+    /* remaining time from stage j to the end of its chain: this stage plus every later one */
+    int64_t suffix = 0;
+    for (int64_t j = end - 1; j >= first; --j) {
+      suffix = sat_add(oracle_latency_us(stage_latency_s[j]), suffix);
+      rem[j] = suffix;
+    }
+    int64_t cur = cursor ? (int64_t)cursor[w] : 0;
+    if (cur < 0) cur = 0;
+    const int64_t r = (first + cur < end) ? rem[first + cur] : 0;  /* finished chain: 0 */
+    int32_t key;
+    if (r == LAT_SAT) {
+      key = INT32_MIN;                              /* unroutable: most urgent */
+    } else {
+      __int128 slack = (__int128)deadline_us[w] - (__int128)now_us - (__int128)r;
+      if (slack > (__int128)INT32_MAX) key = INT32_MAX;
+      else if (slack < (__int128)INT32_MIN) key = INT32_MIN;
+      else key = (int32_t)slack;
+    }
+    slack_key[w] = key;
+    kv[w].key = key;
+    kv[w].idx = w;
+  }
+  if (remaining_us) memcpy(remaining_us, rem, sizeof(int64_t) * (size_t)n_stages);
+
+  qsort(kv, (size_t)n_workflows, sizeof(keyed_t), keyed_cmp);
+  for (int32_t w = 0; w < n_workflows; ++w) order[w] = kv[w].idx;
+
+  free(rem);
+  free(kv);
+  return ORACLE_OK;
+}
+
+int oracle_max_threads(void) { return omp_get_max_threads(); }

@@ -1,0 +1,296 @@
+"""Seeded synthetic workloads for the batched predict -> route -> prioritize step.
+
+This module only *draws inputs*. It holds none of the method's arithmetic (no MLP, no
+softmax, no scoring, no scan, no sort), so both the HIP path and the CPU oracle can be fed
+from it without sharing any of the computation under test.
+
+The five named workloads follow the paper's workload structure:
+  * skewed (Zipf) model popularity (Sec. II, Observation-2 and its long-tail figure),
+  * KV demand that grows with prompt + output length (Sec. II, KV cache memory pressure;
+    Eq. 3),
+  * sequential agent chains of a few stages each (Sec. IV-A, Table I: 144,524 stages over
+    46,769 jobs, about 3.1 stages per job),
+  * mixed deadlines (Sec. IV-A, SLOs).
+The paper's own trace, its Chatbot-Arena popularity data and its trained predictor are not
+available, so these seeded draws stand in for them.
+
+Random streams: ``numpy.random.Generator(PCG64(child))`` where the children come from
+``SeedSequence(seed).spawn(len(STREAMS))`` in the fixed order of ``STREAMS``; every array is
+drawn from its own stream, so changing one size never perturbs another array.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+from dataclasses import dataclass, field
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+STREAMS = ("x", "role", "prompt", "model", "W1", "W2", "W3", "free", "resident",
+           "cold", "queue", "alpha", "dec", "half", "chain_len", "arrival", "slo")
+
+GB = 1.0e9  # free HBM is drawn in SI gigabytes and passed as a byte count
+
+# Rows of feature matrix drawn per call to the normal generator; fixed so that the drawn
+# matrix is a pure function of (seed, N, D).
+_X_CHUNK_ROWS = 1 << 16
+
+
+@dataclass(frozen=True)
+class WorkloadSpec:
+    """Shape and distribution parameters of one synthetic scheduling batch."""
+    name: str
+    seed: int
+    n_stages: int                       # ignored when n_workflows > 0 (derived from chains)
+    n_nodes: int
+    n_models: int
+    zipf_s: Optional[float]             # None -> uniform model ids
+    dims: Tuple[int, ...]               # (D, H1, [H2,] B): Linear layer widths
+    dtype: str                          # "f32" or "bf16" (features, weights, hidden)
+    prompt_lognormal: Tuple[float, float, int, int]   # (mu, sigma, lo, hi)
+    free_gb: Tuple                      # ("uniform", lo, hi) | ("bimodal", lo1, hi1, lo2, hi2)
+    resident_p: float
+    alpha: Tuple                        # ("const", v) | ("choice", v0, v1, ...)
+    dec: Tuple                          # ("const", v) | ("uniform", lo, hi)
+    k: int = 1                          # route width (top-k)
+    rho: float = 0.0                    # KV safety margin
+    n_workflows: int = 0                # > 0 -> chains of stages (prioritize input)
+    chain_len: Tuple[int, int] = (3, 8)
+    arrival_s: Tuple[float, float] = (0.0, 600.0)
+    slo_s: Tuple[float, float] = (10.0, 120.0)
+    now_s: float = 600.0
+    bin_start: float = 32.0             # bin centre of bin b = bin_start + bin_width * b
+    bin_width: float = 64.0
+    cold_s: Tuple[float, float] = (2.0, 20.0)
+    queue_s: Tuple[float, float] = (0.0, 5.0)
+
+    @property
+    def n_bins(self) -> int:
+        return self.dims[-1]
+
+    @property
+    def n_layers(self) -> int:
+        return len(self.dims) - 1
+
+
+_ALPHA_CHOICES = ("choice", 65536.0, 131072.0, 327680.0)
+
+SPECS: Dict[str, WorkloadSpec] = {
+    # Tiny predict-and-route case.
+    "c0": WorkloadSpec(
+        name="c0", seed=0, n_stages=4096, n_nodes=64, n_models=8, zipf_s=None,
+        dims=(64, 128, 32), dtype="f32", prompt_lognormal=(6.0, 1.0, 16, 8192),
+        free_gb=("uniform", 0.0, 288.0), resident_p=0.3,
+        alpha=("const", 131072.0), dec=("const", 0.02), k=1),
+    # Mid batch.
+    "c1": WorkloadSpec(
+        name="c1", seed=1, n_stages=65536, n_nodes=512, n_models=16, zipf_s=1.1,
+        dims=(256, 512, 512, 64), dtype="bf16", prompt_lognormal=(6.0, 1.0, 16, 8192),
+        free_gb=("uniform", 0.0, 288.0), resident_p=0.3,
+        alpha=_ALPHA_CHOICES, dec=("uniform", 0.010, 0.040), k=1),
+    # Large routing sweep: bimodal free HBM, long prompts.
+    "c2": WorkloadSpec(
+        name="c2", seed=2, n_stages=1048576, n_nodes=1024, n_models=32, zipf_s=1.1,
+        dims=(256, 512, 512, 64), dtype="bf16", prompt_lognormal=(6.5, 1.2, 16, 32768),
+        free_gb=("bimodal", 0.0, 40.0, 150.0, 288.0), resident_p=0.25,
+        alpha=_ALPHA_CHOICES, dec=("uniform", 0.010, 0.040), k=1),
+    # Workflow prioritisation: the mid-batch predictor/route setup over chained stages.
+    "c3": WorkloadSpec(
+        name="c3", seed=3, n_stages=0, n_nodes=512, n_models=16, zipf_s=1.1,
+        dims=(256, 512, 512, 64), dtype="bf16", prompt_lognormal=(6.0, 1.0, 16, 8192),
+        free_gb=("uniform", 0.0, 288.0), resident_p=0.3,
+        alpha=_ALPHA_CHOICES, dec=("uniform", 0.010, 0.040), k=1,
+        n_workflows=131072),
+    # High contention: top-4 routing, wide predictor.
+    "c4": WorkloadSpec(
+        name="c4", seed=4, n_stages=4194304, n_nodes=4096, n_models=64, zipf_s=1.3,
+        dims=(256, 1024, 1024, 64), dtype="bf16", prompt_lognormal=(6.0, 1.0, 16, 8192),
+        free_gb=("uniform", 0.0, 30.0), resident_p=0.3,
+        alpha=_ALPHA_CHOICES, dec=("uniform", 0.010, 0.040), k=4),
+}
+
+DESCRIPTIONS = {
+    "c0": "tiny predict+route: N=4096 stages, M=64 nodes, 8 models, MLP 64-128-32 fp32",
+    "c1": "mid batch: N=65536, M=512, 16 models Zipf(1.1), MLP 256-512-512-64 bf16",
+    "c2": "large routing sweep: N=1048576, M=1024, 32 models, bimodal free HBM",
+    "c3": "workflow prioritisation: W=131072 chains of 3..8 stages, M=512, "
+          "MLP 256-512-512-64 bf16, then slack ordering",
+    "c4": "high contention: N=4194304, M=4096, 64 models Zipf(1.3), top-4, "
+          "MLP 256-1024-1024-64 bf16",
+}
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round finite float32 values to bfloat16 (round to nearest, ties to even).
+
+    This is a storage cast of drawn data, returned as the raw uint16 bit patterns.
+    """
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns to float32."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@dataclass
+class Workload:
+    """All inputs of one batch. Array layouts match the C-ABI (row-major, one row per stage
+    or node). bf16 arrays are stored as uint16 bit patterns."""
+    spec: WorkloadSpec
+    # stages
+    x: Optional[np.ndarray]             # [N][D] float32, or uint16 (bf16 bits)
+    role: np.ndarray                    # [N] int32 (metadata, not read by the predictor)
+    prompt_len: np.ndarray              # [N] int32
+    model_id: np.ndarray                # [N] int32
+    # predictor
+    weights: list                       # per layer [out][in]: float32 or uint16 (bf16 bits)
+    biases: list                        # per layer [out] float32
+    bin_centre: np.ndarray              # [B] float32
+    # per model
+    kv_bytes_per_token: np.ndarray      # [K] float32 (alpha)
+    decode_s_per_token: np.ndarray      # [K] float32
+    # nodes
+    free_bytes: np.ndarray              # [M] float64
+    queue_s: np.ndarray                 # [M] float32
+    cold_s: np.ndarray                  # [M] float32
+    resident_mask: np.ndarray           # [M] uint64, bit m set <=> model m resident
+    # workflows (prioritize); empty when the batch has no chains
+    chain_offset: np.ndarray = field(default_factory=lambda: np.zeros(1, np.int64))
+    deadline_us: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    now_us: int = 0
+
+    @property
+    def n(self) -> int:
+        return int(self.model_id.shape[0])
+
+    @property
+    def n_workflows(self) -> int:
+        return int(self.chain_offset.shape[0] - 1)
+
+    def sha256(self) -> Dict[str, str]:
+        out = {}
+        for f in dataclasses.fields(self):
+            v = getattr(self, f.name)
+            if isinstance(v, np.ndarray):
+                out[f.name] = hashlib.sha256(np.ascontiguousarray(v).tobytes()).hexdigest()
+            elif isinstance(v, list):
+                h = hashlib.sha256()
+                for a in v:
+                    h.update(np.ascontiguousarray(a).tobytes())
+                out[f.name] = h.hexdigest()
+        return out
+
+
+def _streams(seed: int) -> Dict[str, np.random.Generator]:
+    children = np.random.SeedSequence(seed).spawn(len(STREAMS))
+    return {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(STREAMS, children)}
+
+
+def _model_ids(rng: np.random.Generator, n: int, k: int, zipf_s: Optional[float]) -> np.ndarray:
+    if zipf_s is None:
+        return rng.integers(0, k, size=n, dtype=np.int64).astype(np.int32)
+    # truncated Zipf over ids 0..k-1, id 0 the most popular
+    p = np.arange(1, k + 1, dtype=np.float64) ** (-zipf_s)
+    p /= p.sum()
+    return rng.choice(k, size=n, p=p).astype(np.int32)
+
+
+def draw_features(rng: np.random.Generator, n: int, d: int, dtype: str) -> np.ndarray:
+    out = np.empty((n, d), dtype=np.float32 if dtype == "f32" else np.uint16)
+    for r0 in range(0, n, _X_CHUNK_ROWS):
+        r1 = min(n, r0 + _X_CHUNK_ROWS)
+        block = rng.standard_normal((r1 - r0, d), dtype=np.float32)
+        out[r0:r1] = block if dtype == "f32" else f32_to_bf16_bits(block)
+    return out
+
+
+def generate(spec: WorkloadSpec, with_x: bool = True) -> Workload:
+    """Draw every input of ``spec``. ``with_x=False`` skips the (large) feature matrix."""
+    rs = _streams(spec.seed)
+    K, M = spec.n_models, spec.n_nodes
+
+    # workflows first: they fix the number of stages
+    if spec.n_workflows > 0:
+        W = spec.n_workflows
+        lo, hi = spec.chain_len
+        lens = rs["chain_len"].integers(lo, hi + 1, size=W, dtype=np.int64)
+        chain_offset = np.zeros(W + 1, dtype=np.int64)
+        np.cumsum(lens, out=chain_offset[1:])
+        n = int(chain_offset[-1])
+        arrival = rs["arrival"].uniform(spec.arrival_s[0], spec.arrival_s[1], size=W)
+        slo = rs["slo"].uniform(spec.slo_s[0], spec.slo_s[1], size=W)
+        deadline_us = np.rint((arrival + slo) * 1.0e6).astype(np.int64)
+        now_us = int(round(spec.now_s * 1.0e6))
+        # role id cycles along each chain (planner/solver/critic-style); metadata only
+        pos = np.arange(n, dtype=np.int64) - np.repeat(chain_offset[:-1], lens)
+        role = (pos % 5).astype(np.int32)
+    else:
+        n = spec.n_stages
+        chain_offset = np.zeros(1, dtype=np.int64)
+        deadline_us = np.zeros(0, dtype=np.int64)
+        now_us = 0
+        role = rs["role"].integers(0, 5, size=n, dtype=np.int64).astype(np.int32)
+
+    D = spec.dims[0]
+    x = draw_features(rs["x"], n, D, spec.dtype) if with_x else None
+
+    mu, sigma, plo, phi = spec.prompt_lognormal
+    prompt = np.clip(np.rint(rs["prompt"].lognormal(mu, sigma, size=n)), plo, phi).astype(np.int32)
+    model = _model_ids(rs["model"], n, K, spec.zipf_s)
+
+    weights, biases = [], []
+    for li in range(spec.n_layers):
+        fan_in, fan_out = spec.dims[li], spec.dims[li + 1]
+        w = rs[("W1", "W2", "W3")[li]].normal(0.0, fan_in ** -0.5, size=(fan_out, fan_in))
+        w32 = w.astype(np.float32)
+        weights.append(w32 if spec.dtype == "f32" else f32_to_bf16_bits(w32))
+        biases.append(np.zeros(fan_out, dtype=np.float32))
+    B = spec.n_bins
+    bin_centre = (spec.bin_start + spec.bin_width * np.arange(B, dtype=np.float64)).astype(np.float32)
+
+    if spec.alpha[0] == "const":
+        alpha = np.full(K, spec.alpha[1], dtype=np.float32)
+    else:
+        alpha = rs["alpha"].choice(np.asarray(spec.alpha[1:], dtype=np.float64), size=K).astype(np.float32)
+    if spec.dec[0] == "const":
+        dec = np.full(K, spec.dec[1], dtype=np.float32)
+    else:
+        dec = rs["dec"].uniform(spec.dec[1], spec.dec[2], size=K).astype(np.float32)
+
+    if spec.free_gb[0] == "uniform":
+        free = rs["free"].uniform(spec.free_gb[1], spec.free_gb[2], size=M) * GB
+    else:
+        _, lo1, hi1, lo2, hi2 = spec.free_gb
+        low_half = np.zeros(M, dtype=bool)
+        low_half[rs["half"].permutation(M)[: M // 2]] = True
+        u = rs["free"].random(size=M)
+        free = np.where(low_half, lo1 + u * (hi1 - lo1), lo2 + u * (hi2 - lo2)) * GB
+    free = free.astype(np.float64)
+
+    bits = rs["resident"].random(size=(M, K)) < spec.resident_p
+    mask = np.zeros(M, dtype=np.uint64)
+    for m in range(K):
+        mask |= bits[:, m].astype(np.uint64) << np.uint64(m)
+
+    cold = rs["cold"].uniform(spec.cold_s[0], spec.cold_s[1], size=M).astype(np.float32)
+    queue = rs["queue"].uniform(spec.queue_s[0], spec.queue_s[1], size=M).astype(np.float32)
+
+    return Workload(spec=spec, x=x, role=role, prompt_len=prompt, model_id=model,
+                    weights=weights, biases=biases, bin_centre=bin_centre,
+                    kv_bytes_per_token=alpha, decode_s_per_token=dec,
+                    free_bytes=free, queue_s=queue, cold_s=cold, resident_mask=mask,
+                    chain_offset=chain_offset, deadline_us=deadline_us, now_us=now_us)
+
+
+def workload(name: str, with_x: bool = True, **overrides) -> Workload:
+    """Named workload, optionally with fields of its spec replaced (e.g. ``n_stages=5000``)."""
+    spec = SPECS[name]
+    if overrides:
+        spec = dataclasses.replace(spec, **overrides)
+    return generate(spec, with_x=with_x)
