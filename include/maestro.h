@@ -1,0 +1,160 @@
+/*
+ * maestro.h -- C-ABI of the MI355X (gfx950) hot path of Maestro's scheduler:
+ * the batched predict -> route -> prioritize step.
+ *
+ *   maestro_predict    cost prediction (Sec. III-B): predicted output length L of every stage
+ *                      from a feature MLP over length bins (stand-in for the paper's trained
+ *                      regressor), and its KV demand R_kv = alpha(M) * (P + L) (Eq. 3).
+ *   maestro_route      cross-cluster routing (Sec. III-D, Alg. 3): drop nodes whose free KV
+ *                      headroom cannot admit R_need = (1 + rho) * R_kv, score the rest by
+ *                      expected completion latency T_q + T_act + t_dec(M) * L (Eq. 6 and the
+ *                      decode term of Eq. 2), keep the best k (lowest index on equal scores).
+ *   maestro_prioritize remaining-time queue ordering (Sec. III-D, Eq. 7): remaining
+ *                      predicted latency along each workflow chain, slack against the
+ *                      workflow deadline, stable ascending order of workflows by slack.
+ *
+ * Conventions shared by every entry point
+ *   - Every array argument is a DEVICE pointer owned by the caller. The library never
+ *     allocates, frees or synchronises, and keeps no pointer after it returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream). All work is
+ *     enqueued asynchronously on it; outputs are valid once the stream has been synchronised.
+ *   - `workspace` is caller-owned, 16-byte aligned device scratch of at least the size the
+ *     matching maestro_*_workspace() returns (NULL is allowed when that size is 0). Its
+ *     contents on entry do not matter. Calls that share a workspace must not overlap in time.
+ *   - Host-side checks only (scalars, pointers, alignment, sizes) happen before anything is
+ *     enqueued; on failure the call returns MAESTRO_ERR_INVALID_ARG / _UNSUPPORTED /
+ *     _WORKSPACE and has no effect. A failed launch returns MAESTRO_ERR_LAUNCH.
+ *   - Per-element device data is a precondition, not checked: model ids in [0, n_models),
+ *     finite inputs (stage latency excepted), monotone chain offsets.
+ *   - Empty inputs (n = 0, n_workflows = 0) are valid no-ops that return MAESTRO_OK.
+ *   - Entry points are re-entrant: the library has no mutable global state.
+ */
+#ifndef MAESTRO_H
+#define MAESTRO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define MAESTRO_API __attribute__((visibility("default")))
+#else
+#define MAESTRO_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum maestro_status {
+  MAESTRO_OK = 0,
+  MAESTRO_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, out-of-range scalar */
+  MAESTRO_ERR_UNSUPPORTED = 2,   /* valid shape the kernels are not built for */
+  MAESTRO_ERR_WORKSPACE = 3,     /* workspace smaller than maestro_*_workspace() */
+  MAESTRO_ERR_LAUNCH = 4         /* the HIP runtime rejected a launch */
+} maestro_status;
+
+typedef enum maestro_dtype {
+  MAESTRO_F32 = 0,               /* features, weights and hidden layers in float32 */
+  MAESTRO_BF16 = 1               /* bfloat16 storage, float32 accumulation */
+} maestro_dtype;
+
+/* The length predictor: n_layers Linear layers, ReLU between them, softmax over B length
+ * bins at the end; the predicted length is the softmax-weighted mean of the bin centres.
+ * Layer l maps dims[l] -> dims[l+1]: y = x * W_l^T + b_l with W_l stored [dims[l+1]][dims[l]]
+ * row-major (out x in, device, element type `dtype`, 16-byte aligned) and b_l float32
+ * [dims[l+1]] (device, 16-byte aligned). Hidden activations are stored in `dtype` after
+ * bias + ReLU (round to nearest even for bfloat16); logits, softmax and the expected length
+ * are float32.
+ * Built shapes (others return MAESTRO_ERR_UNSUPPORTED):
+ *   MAESTRO_F32,  2 layers: 64 -> 128 -> 32
+ *   MAESTRO_BF16, 3 layers: 256 -> 512 -> 512 -> 64 and 256 -> 1024 -> 1024 -> 64 */
+typedef struct maestro_predictor {
+  int32_t n_layers;            /* number of Linear layers */
+  int32_t dims[5];             /* dims[0] = D features, ..., dims[n_layers] = B bins */
+  int32_t dtype;               /* maestro_dtype */
+  const void* weight[4];       /* [dims[l+1]][dims[l]] per layer */
+  const float* bias[4];        /* [dims[l+1]] per layer */
+  const float* bin_centre;     /* [B] float32, 16-byte aligned: token count each bin stands for */
+} maestro_predictor;
+
+/* Cost prediction for n stages (Sec. III-B; Eq. 3).
+ *   x                   [n][D] row-major, element type p->dtype, 16-byte aligned
+ *   prompt_len          [n] int32: prompt tokens P of each stage
+ *   model_id            [n] int32 in [0, n_models): the stage's model M(T)
+ *   kv_bytes_per_token  [n_models] float32: alpha(M), KV bytes per token of each model
+ *   pred_len  (out)     [n] float32: predicted output length L (tokens)
+ *   kv_bytes  (out)     [n] float64: R_kv = ((double)P + (double)L) * (double)alpha(M);
+ *                       exact in float64 for P < 2^16 and alpha < 2^19.
+ * Needs no workspace (maestro_predict_workspace returns 0). */
+MAESTRO_API maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void* x,
+                               const int32_t* prompt_len, const int32_t* model_id,
+                               const float* kv_bytes_per_token, int32_t n_models,
+                               float* pred_len, double* kv_bytes,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Routing of n stages over n_nodes nodes (Sec. III-D; Alg. 3; Eq. 6; Eq. 2 decode term).
+ * Per stage i with model m = model_id[i]:
+ *   need  = rho == 0 ? kv_bytes[i] : kv_bytes[i] * (1 + rho)       (float64)
+ *   node j is feasible iff need <= free_bytes[j]                     (equality admits)
+ *   score = fl32( fl32(queue_s[j] + act) + fl32(pred_len[i] * decode_s_per_token[m]) )
+ *           with act = 0 if bit m of resident_mask[j] is set, else cold_s[j]
+ *   output the k feasible nodes with the smallest (score, j) in lexicographic order, i.e.
+ *   ties go to the lowest node index; when fewer than k nodes are feasible the tail is
+ *   padded with node -1 and score +inf.
+ *   model_id            [n] int32 in [0, n_models), 1 <= n_models <= 64
+ *   pred_len, kv_bytes  [n] float32 / float64 (from maestro_predict)
+ *   decode_s_per_token  [n_models] float32: t_dec(M), seconds per output token
+ *   free_bytes          [n_nodes] float64: KV admission headroom R_head (bytes)
+ *   queue_s, cold_s     [n_nodes] float32: queueing delay T_q, cold-start latency T_act
+ *   resident_mask       [n_nodes] uint64: bit m set <=> model m is warm on the node
+ *   rho >= 0            safety margin;  1 <= k <= 16 route width
+ *   node_idx  (out)     [n][k] int32;  score (out) [n][k] float32
+ * Scores must be finite (finite inputs whose sums do not overflow float32). */
+MAESTRO_API maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* cold_s,
+                             const uint64_t* resident_mask, double rho, int32_t k,
+                             int32_t* node_idx, float* score,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Slack ordering of n_workflows workflow chains over n_stages stages (Sec. III-D, Eq. 7).
+ *   chain_offset        [n_workflows + 1] int64, chain_offset[0] = 0, non-decreasing,
+ *                       chain_offset[W] = n_stages: stages of workflow w are
+ *                       [chain_offset[w], chain_offset[w+1]) in chain order; a chain holds
+ *                       at most 2^22 stages.
+ *   stage_latency_s     [n_stages] float32 predicted latency of each stage (e.g. the routed
+ *                       score); quantised to integer microseconds, round half to even,
+ *                       clamped to +-2^40 us; a non-finite latency marks the stage (and every
+ *                       earlier stage of its chain) as infinitely late.
+ *   cursor              [n_workflows] int32 index of the next pending stage within each chain,
+ *                       or NULL for all zero; negative counts as 0, >= chain length means
+ *                       nothing remains.
+ *   deadline_us         [n_workflows] int64;  now_us: current time (microseconds)
+ *   remaining_us (out)  [n_stages] int64 or NULL: sum of the quantised latencies from the stage
+ *                       to the end of its chain (INT64_MAX if infinitely late)
+ *   slack_key (out)     [n_workflows] int32: deadline - now - remaining(head), exact, clamped
+ *                       to int32; INT32_MIN when the remaining time is infinite
+ *   order (out)         [n_workflows] int32: workflows sorted by ascending slack_key, equal keys
+ *                       in increasing workflow index (stable).
+ * Needs maestro_prioritize_workspace(n_workflows, n_stages) bytes of workspace. */
+MAESTRO_API maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,
+                                  const int64_t* chain_offset, const float* stage_latency_s,
+                                  const int32_t* cursor, const int64_t* deadline_us,
+                                  int64_t now_us, int64_t* remaining_us, int32_t* slack_key,
+                                  int32_t* order, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/* Workspace sizes in bytes (0 = none needed). */
+MAESTRO_API size_t maestro_predict_workspace(const maestro_predictor* p, int64_t n);
+MAESTRO_API size_t maestro_route_workspace(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);
+MAESTRO_API size_t maestro_prioritize_workspace(int32_t n_workflows, int64_t n_stages);
+
+/* Static description of a status code. */
+MAESTRO_API const char* maestro_status_string(maestro_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAESTRO_H */

@@ -1,0 +1,13 @@
+"""MI355X (gfx950) hot path of Maestro's scheduler: batched predict -> route -> prioritize.
+
+The computation lives in libmaestro.so (hand-written HIP kernels behind the C-ABI of
+include/maestro.h); this package is its thin Python binding plus the seeded workload
+generator. PyTorch supplies device memory and streams only.
+"""
+from ._native import (LIBRARY_PATH, MaestroError, Predictor, load, make_predictor, predict,
+                      prioritize, prioritize_workspace_bytes, route)
+from .pipeline import DeviceBatch, StepOutputs, run_step, to_device
+
+__all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "load", "make_predictor", "predict",
+           "prioritize", "prioritize_workspace_bytes", "route", "DeviceBatch", "StepOutputs",
+           "run_step", "to_device"]

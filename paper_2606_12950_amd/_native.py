@@ -1,0 +1,229 @@
+"""Thin ctypes binding of libmaestro's C-ABI (include/maestro.h).
+
+Argument marshalling only: every step of predict / route / prioritize runs in the HIP
+kernels of libmaestro.so. PyTorch provides device memory (tensors, workspaces) and the
+stream (the current torch stream). There is no fallback: if the library is not built or no
+GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY_PATH = os.path.join(_PKG, "libmaestro.so")
+
+MAESTRO_F32, MAESTRO_BF16 = 0, 1
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace too small",
+           4: "kernel launch failed"}
+
+# Every function declared in include/maestro.h.
+EXPORTS = ("maestro_predict", "maestro_route", "maestro_prioritize", "maestro_predict_workspace",
+           "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
+
+
+class MaestroError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {_STATUS.get(status, status)} (status {status})")
+        self.status = status
+
+
+class Predictor(ctypes.Structure):
+    """Mirror of ``maestro_predictor``."""
+    _fields_ = [("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 5),
+                ("dtype", ctypes.c_int32), ("weight", ctypes.c_void_p * 4),
+                ("bias", ctypes.c_void_p * 4), ("bin_centre", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load():
+    """Load libmaestro.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIBRARY_PATH):
+        raise RuntimeError(f"{LIBRARY_PATH} is missing: build it first "
+                           "(python -m paper_2606_12950_amd.build)")
+    lib = ctypes.CDLL(LIBRARY_PATH)
+    P, i32, i64, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
+    lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
+    lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
+    lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
+    for f in ("maestro_predict", "maestro_route", "maestro_prioritize"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.maestro_predict_workspace.argtypes = [ctypes.POINTER(Predictor), i64]
+    lib.maestro_route_workspace.argtypes = [i64, i32, i32, i32]
+    lib.maestro_prioritize_workspace.argtypes = [i32, i64]
+    for f in ("maestro_predict_workspace", "maestro_route_workspace", "maestro_prioritize_workspace"):
+        getattr(lib, f).restype = sz
+    lib.maestro_status_string.argtypes = [ctypes.c_int]
+    lib.maestro_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise MaestroError(fn, status)
+
+
+def make_predictor(weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor],
+                   bin_centre: torch.Tensor) -> Predictor:
+    """Describe a predictor held in device tensors (weights [out][in], bf16 or fp32)."""
+    L = len(weights)
+    if not 1 <= L <= 4 or len(biases) != L:
+        raise ValueError("1..4 Linear layers with one bias each")
+    dt = weights[0].dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("weights must be float32 or bfloat16")
+    p = Predictor()
+    p.n_layers = L
+    p.dtype = MAESTRO_F32 if dt == torch.float32 else MAESTRO_BF16
+    p.dims[0] = weights[0].shape[1]
+    for l, (w, b) in enumerate(zip(weights, biases)):
+        _dev(w, f"weight[{l}]", dt)
+        _dev(b, f"bias[{l}]", torch.float32)
+        if w.dim() != 2 or w.shape[1] != p.dims[l] or b.shape != (w.shape[0],):
+            raise ValueError(f"layer {l}: weight must be [out][in] chaining the previous layer")
+        p.dims[l + 1] = w.shape[0]
+        p.weight[l] = w.data_ptr()
+        p.bias[l] = b.data_ptr()
+    _dev(bin_centre, "bin_centre", torch.float32)
+    if bin_centre.shape != (p.dims[L],):
+        raise ValueError("bin_centre must have one entry per output bin")
+    p.bin_centre = bin_centre.data_ptr()
+    return p
+
+
+def predict(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor],
+            bin_centre: torch.Tensor, prompt_len: torch.Tensor, model_id: torch.Tensor,
+            kv_bytes_per_token: torch.Tensor, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+            stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_predict: returns (pred_len float32 [N], kv_bytes float64 [N])."""
+    lib = load()
+    p = make_predictor(weights, biases, bin_centre)
+    _dev(x, "x", weights[0].dtype)
+    n = x.shape[0]
+    if x.dim() != 2 or x.shape[1] != p.dims[0]:
+        raise ValueError("x must be [N][D]")
+    _dev(prompt_len, "prompt_len", torch.int32)
+    _dev(model_id, "model_id", torch.int32)
+    _dev(kv_bytes_per_token, "kv_bytes_per_token", torch.float32)
+    if out is None:
+        out = (torch.empty(n, dtype=torch.float32, device=x.device),
+               torch.empty(n, dtype=torch.float64, device=x.device))
+    pred, kv = out
+    _dev(pred, "pred_len", torch.float32)
+    _dev(kv, "kv_bytes", torch.float64)
+    ws_bytes = lib.maestro_predict_workspace(ctypes.byref(p), n)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device) if ws_bytes else None
+    st = lib.maestro_predict(ctypes.byref(p), n, _ptr(x), _ptr(prompt_len), _ptr(model_id),
+                             _ptr(kv_bytes_per_token), kv_bytes_per_token.shape[0], _ptr(pred),
+                             _ptr(kv), _ptr(ws), ws_bytes, _stream(stream))
+    _check("maestro_predict", st)
+    return pred, kv
+
+
+def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,
+          decode_s_per_token: torch.Tensor, free_bytes: torch.Tensor, queue_s: torch.Tensor,
+          cold_s: torch.Tensor, resident_mask: torch.Tensor, k: int = 1, rho: float = 0.0,
+          out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, workspace: Optional[torch.Tensor] = None,
+          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_route: returns (node_idx int32 [N][k], score float32 [N][k]).
+
+    ``resident_mask`` is int64 on the torch side (same bits as the C-ABI's uint64)."""
+    lib = load()
+    _dev(model_id, "model_id", torch.int32)
+    n = model_id.shape[0]
+    _dev(pred_len, "pred_len", torch.float32)
+    _dev(kv_bytes, "kv_bytes", torch.float64)
+    _dev(decode_s_per_token, "decode_s_per_token", torch.float32)
+    _dev(free_bytes, "free_bytes", torch.float64)
+    _dev(queue_s, "queue_s", torch.float32)
+    _dev(cold_s, "cold_s", torch.float32)
+    _dev(resident_mask, "resident_mask", torch.int64)
+    M = free_bytes.shape[0]
+    if pred_len.shape[0] != n or kv_bytes.shape[0] != n:
+        raise ValueError("per-stage inputs must have the same length")
+    if queue_s.shape[0] != M or cold_s.shape[0] != M or resident_mask.shape[0] != M:
+        raise ValueError("per-node inputs must have the same length")
+    if out is None:
+        out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
+               torch.empty((n, k), dtype=torch.float32, device=model_id.device))
+    idx, sc = out
+    _dev(idx, "node_idx", torch.int32)
+    _dev(sc, "score", torch.float32)
+    ws_bytes = lib.maestro_route_workspace(n, decode_s_per_token.shape[0], M, k)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=model_id.device)
+    st = lib.maestro_route(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes),
+                           _ptr(decode_s_per_token), decode_s_per_token.shape[0], M,
+                           _ptr(free_bytes), _ptr(queue_s), _ptr(cold_s), _ptr(resident_mask),
+                           float(rho), int(k), _ptr(idx), _ptr(sc),
+                           _ptr(workspace) if ws_bytes else None,
+                           workspace.numel() if (ws_bytes and workspace is not None) else 0,
+                           _stream(stream))
+    _check("maestro_route", st)
+    return idx, sc
+
+
+def prioritize_workspace_bytes(n_workflows: int, n_stages: int) -> int:
+    return int(load().maestro_prioritize_workspace(n_workflows, n_stages))
+
+
+def prioritize(chain_offset: torch.Tensor, stage_latency_s: torch.Tensor, deadline_us: torch.Tensor,
+               now_us: int, cursor: Optional[torch.Tensor] = None, want_remaining: bool = True,
+               out: Optional[Tuple[Optional[torch.Tensor], torch.Tensor, torch.Tensor]] = None,
+               workspace: Optional[torch.Tensor] = None, stream=None):
+    """maestro_prioritize: returns (remaining_us int64 [S] or None, slack_key int32 [W],
+    order int32 [W])."""
+    lib = load()
+    _dev(chain_offset, "chain_offset", torch.int64)
+    _dev(stage_latency_s, "stage_latency_s", torch.float32)
+    _dev(deadline_us, "deadline_us", torch.int64)
+    W = chain_offset.shape[0] - 1
+    S = stage_latency_s.shape[0]
+    if deadline_us.shape[0] != W:
+        raise ValueError("one deadline per workflow")
+    if cursor is not None:
+        _dev(cursor, "cursor", torch.int32)
+        if cursor.shape[0] != W:
+            raise ValueError("one cursor per workflow")
+    dev = chain_offset.device
+    if out is None:
+        out = (torch.empty(S, dtype=torch.int64, device=dev) if want_remaining else None,
+               torch.empty(W, dtype=torch.int32, device=dev),
+               torch.empty(W, dtype=torch.int32, device=dev))
+    rem, key, order = out
+    ws_bytes = prioritize_workspace_bytes(W, S)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    st = lib.maestro_prioritize(W, S, _ptr(chain_offset), _ptr(stage_latency_s), _ptr(cursor),
+                                _ptr(deadline_us), int(now_us), _ptr(rem), _ptr(key), _ptr(order),
+                                _ptr(workspace), workspace.numel(), _stream(stream))
+    _check("maestro_prioritize", st)
+    return rem, key, order

@@ -1,0 +1,116 @@
+// C-ABI entry points of libmaestro: host-side argument checks, then the kernel launchers.
+// Nothing here touches device memory; every check happens before the first launch.
+#include "internal.h"
+
+namespace {
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* maestro_status_string(maestro_status s) {
+  switch (s) {
+    case MAESTRO_OK: return "ok";
+    case MAESTRO_ERR_INVALID_ARG: return "invalid argument";
+    case MAESTRO_ERR_UNSUPPORTED: return "unsupported shape";
+    case MAESTRO_ERR_WORKSPACE: return "workspace too small";
+    case MAESTRO_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+size_t maestro_predict_workspace(const maestro_predictor*, int64_t) { return 0; }
+
+size_t maestro_route_workspace(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k) {
+  return maestro::route_workspace_bytes(n, n_models, n_nodes, k);
+}
+
+size_t maestro_prioritize_workspace(int32_t n_workflows, int64_t n_stages) {
+  if (n_workflows < 0 || n_stages < 0) return 0;
+  return maestro::prioritize_workspace_bytes(n_workflows, n_stages);
+}
+
+maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void* x,
+                               const int32_t* prompt_len, const int32_t* model_id,
+                               const float* kv_bytes_per_token, int32_t n_models,
+                               float* pred_len, double* kv_bytes, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!p || n < 0 || n_models < 1) return MAESTRO_ERR_INVALID_ARG;
+  if (p->n_layers < 1 || p->n_layers > 4) return MAESTRO_ERR_INVALID_ARG;
+  if (p->dtype != MAESTRO_F32 && p->dtype != MAESTRO_BF16) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l <= p->n_layers; ++l)
+    if (p->dims[l] < 1) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l < p->n_layers; ++l)
+    if (!p->weight[l] || !p->bias[l] || !aligned(p->weight[l], 16) || !aligned(p->bias[l], 16))
+      return MAESTRO_ERR_INVALID_ARG;
+  if (!p->bin_centre || !aligned(p->bin_centre, 16)) return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!x || !prompt_len || !model_id || !kv_bytes_per_token || !pred_len || !kv_bytes)
+      return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(prompt_len, 4) || !aligned(model_id, 4) ||
+        !aligned(kv_bytes_per_token, 4) || !aligned(pred_len, 4) || !aligned(kv_bytes, 8))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (!maestro::predict_shape_supported(*p)) return MAESTRO_ERR_UNSUPPORTED;
+  if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;  // grid limit: 2^30 blocks of 128 rows
+  return maestro::launch_predict(*p, n, x, prompt_len, model_id, kv_bytes_per_token, pred_len,
+                                 kv_bytes, as_stream(stream));
+}
+
+maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* cold_s,
+                             const uint64_t* resident_mask, double rho, int32_t k,
+                             int32_t* node_idx, float* score, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  if (n < 0 || n_models < 1 || n_models > 64 || n_nodes < 1 || k < 1 || k > 16)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
+  if (!decode_s_per_token || !free_bytes || !queue_s || !cold_s || !resident_mask)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(decode_s_per_token, 4) || !aligned(free_bytes, 8) || !aligned(queue_s, 4) ||
+      !aligned(cold_s, 4) || !aligned(resident_mask, 8))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!model_id || !pred_len || !kv_bytes || !node_idx || !score) return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(model_id, 4) || !aligned(pred_len, 4) || !aligned(kv_bytes, 8) ||
+        !aligned(node_idx, 4) || !aligned(score, 4))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
+  const size_t need = maestro::route_workspace_bytes(n, n_models, n_nodes, k);
+  if (workspace_bytes < need || (need > 0 && !workspace)) return MAESTRO_ERR_WORKSPACE;
+  return maestro::launch_route(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models,
+                               n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k,
+                               node_idx, score, workspace, workspace_bytes, as_stream(stream));
+}
+
+maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,
+                                  const int64_t* chain_offset, const float* stage_latency_s,
+                                  const int32_t* cursor, const int64_t* deadline_us,
+                                  int64_t now_us, int64_t* remaining_us, int32_t* slack_key,
+                                  int32_t* order, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  if (n_workflows < 0 || n_stages < 0) return MAESTRO_ERR_INVALID_ARG;
+  if (n_workflows == 0) return MAESTRO_OK;
+  if (!chain_offset || !deadline_us || !slack_key || !order) return MAESTRO_ERR_INVALID_ARG;
+  if (n_stages > 0 && !stage_latency_s) return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(chain_offset, 8) || !aligned(deadline_us, 8) || !aligned(slack_key, 4) ||
+      !aligned(order, 4) || !aligned(stage_latency_s, 4) || !aligned(cursor, 4) ||
+      !aligned(remaining_us, 8))
+    return MAESTRO_ERR_INVALID_ARG;
+  const size_t need = maestro::prioritize_workspace_bytes(n_workflows, n_stages);
+  if (workspace_bytes < need || !workspace || !aligned(workspace, 16)) return MAESTRO_ERR_WORKSPACE;
+  return maestro::launch_prioritize(n_workflows, n_stages, chain_offset, stage_latency_s, cursor,
+                                    deadline_us, now_us, remaining_us, slack_key, order,
+                                    workspace, workspace_bytes, as_stream(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// Internal launch interface of libmaestro (not part of the C-ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "maestro.h"
+
+namespace maestro {
+
+// Cost prediction: fused MLP + softmax + expected length + KV bytes.
+maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void* x,
+                              const int32_t* prompt_len, const int32_t* model_id,
+                              const float* kv_bytes_per_token, float* pred_len,
+                              double* kv_bytes, hipStream_t stream);
+bool predict_shape_supported(const maestro_predictor& p);
+
+// Routing: feasibility mask, pair scores, lexicographic top-k.
+maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                            const double* kv_bytes, const float* decode_s_per_token,
+                            int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                            const float* queue_s, const float* cold_s,
+                            const uint64_t* resident_mask, double rho, int32_t k,
+                            int32_t* node_idx, float* score, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);
+
+// Prioritisation: chain suffix sums, slack keys, stable radix sort.
+maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
+                                 const int64_t* chain_offset, const float* stage_latency_s,
+                                 const int32_t* cursor, const int64_t* deadline_us,
+                                 int64_t now_us, int64_t* remaining_us, int32_t* slack_key,
+                                 int32_t* order, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+size_t prioritize_workspace_bytes(int32_t n_workflows, int64_t n_stages);
+
+inline maestro_status launch_status() {
+  return hipGetLastError() == hipSuccess ? MAESTRO_OK : MAESTRO_ERR_LAUNCH;
+}
+
+}  // namespace maestro

@@ -1,0 +1,195 @@
+// Routing of a batch of stages (Sec. III-D; Alg. 3; Eq. 6; decode term of Eq. 2).
+//
+// The (stage x node) score matrix is evaluated tile by tile and never stored: a workgroup
+// takes 256/G stages, stages node state chunk by chunk in LDS (structure of arrays: both
+// possible ready times, free bytes, residency mask), and each of the G lanes that share a
+// stage walks every G-th node of the chunk, keeping a sorted list of its best KT
+// (score, node) pairs. The G lists are then merged across lanes with xor-shuffles
+// (lexicographic on (score, node)), and the first lane writes the stage's k results.
+// G grows when the batch has too few stages to fill the chip.
+//
+// Arithmetic is the same expression, in the same order and precision, as the definition:
+// score = fl32(fl32(T_q + T_act) + fl32(L * t_dec)), with T_act in {0, cold}. The library is
+// compiled with -ffp-contract=off and the products/sums below use explicit round-to-nearest
+// intrinsics, so nothing is fused or reassociated.
+#include <type_traits>
+
+#include "internal.h"
+
+namespace maestro {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kNodeChunk = 1024;
+constexpr int32_t kNoNode = INT32_MAX;  // internal "empty slot" index, reported as -1
+
+template <int KT>
+struct TopK {
+  float s[KT];
+  int32_t n[KT];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int i = 0; i < KT; ++i) { s[i] = INFINITY; n[i] = kNoNode; }
+  }
+  // Insert a candidate whose node index is larger than every node already held (nodes are
+  // visited in increasing order within a lane): equal scores stay behind, so comparing
+  // scores strictly gives the lexicographic order.
+  __device__ __forceinline__ void push_increasing(float sc, int32_t node) {
+#pragma unroll
+    for (int i = KT - 1; i >= 0; --i) {
+      const int p = i > 0 ? i - 1 : 0;
+      const bool lt_prev = (i > 0) && sc < s[p];
+      if (sc < s[i]) {
+        if (lt_prev) { s[i] = s[p]; n[i] = n[p]; }
+        else { s[i] = sc; n[i] = node; }
+      }
+    }
+  }
+  // General lexicographic insertion, used when merging lists from other lanes.
+  __device__ __forceinline__ void push_lex(float sc, int32_t node) {
+#pragma unroll
+    for (int i = KT - 1; i >= 0; --i) {
+      const int p = i > 0 ? i - 1 : 0;
+      const bool lt_this = sc < s[i] || (sc == s[i] && node < n[i]);
+      const bool lt_prev = (i > 0) && (sc < s[p] || (sc == s[p] && node < n[p]));
+      if (lt_this) {
+        if (lt_prev) { s[i] = s[p]; n[i] = n[p]; }
+        else { s[i] = sc; n[i] = node; }
+      }
+    }
+  }
+};
+
+template <>
+__device__ __forceinline__ void TopK<1>::push_increasing(float sc, int32_t node) {
+  if (sc < s[0]) { s[0] = sc; n[0] = node; }
+}
+
+template <int KT, bool kMask64>
+__global__ __launch_bounds__(kThreads) void route_kernel(
+    int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
+    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token,
+    int32_t n_nodes, const double* __restrict__ free_bytes, const float* __restrict__ queue_s,
+    const float* __restrict__ cold_s, const uint64_t* __restrict__ resident_mask, double rho,
+    int32_t k, int g_log2, int32_t* __restrict__ node_idx, float* __restrict__ score) {
+  typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
+  __shared__ float s_warm[kNodeChunk];     // fl32(T_q + 0): ready time when the model is resident
+  __shared__ float s_cold[kNodeChunk];     // fl32(T_q + cold): ready time after a cold start
+  __shared__ double s_free[kNodeChunk];    // KV admission headroom
+  __shared__ mask_t s_mask[kNodeChunk];    // residency bits
+
+  const int tid = threadIdx.x;
+  const int G = 1 << g_log2;
+  const int64_t stage = (int64_t)blockIdx.x * (kThreads >> g_log2) + (tid >> g_log2);
+  const int g = tid & (G - 1);
+  const bool valid = stage < n;
+
+  double need = INFINITY;   // an invalid lane admits nothing
+  float exec_s = 0.0f;
+  mask_t mbit = 0;
+  if (valid) {
+    const int32_t m = model_id[stage];
+    need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
+    exec_s = __fmul_rn(pred_len[stage], decode_s_per_token[m]);
+    mbit = (mask_t)1 << m;
+  }
+
+  TopK<KT> best;
+  best.init();
+  for (int32_t c0 = 0; c0 < n_nodes; c0 += kNodeChunk) {
+    const int cn = min(kNodeChunk, n_nodes - c0);
+    __syncthreads();  // every lane is done with the previous chunk
+    for (int i = tid; i < cn; i += kThreads) {
+      const int32_t j = c0 + i;
+      const float q = queue_s[j];
+      s_warm[i] = __fadd_rn(q, 0.0f);
+      s_cold[i] = __fadd_rn(q, cold_s[j]);
+      s_free[i] = free_bytes[j];
+      s_mask[i] = (mask_t)resident_mask[j];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int i = g; i < cn; i += G) {
+      const float ready = (s_mask[i] & mbit) ? s_warm[i] : s_cold[i];
+      const float sc = __fadd_rn(ready, exec_s);
+      if (need <= s_free[i]) best.push_increasing(sc, c0 + i);
+    }
+  }
+
+  // merge the G lane lists of a stage (lanes g and g ^ o exchange and merge)
+  for (int o = 1; o < G; o <<= 1) {
+    float ps[KT];
+    int32_t pn[KT];
+#pragma unroll
+    for (int i = 0; i < KT; ++i) {
+      ps[i] = __shfl_xor(best.s[i], o);
+      pn[i] = __shfl_xor(best.n[i], o);
+    }
+#pragma unroll
+    for (int i = 0; i < KT; ++i) best.push_lex(ps[i], pn[i]);
+  }
+
+  if (valid && g == 0) {
+#pragma unroll
+    for (int i = 0; i < KT; ++i) {
+      if (i < k) {
+        const bool some = best.n[i] != kNoNode;
+        node_idx[stage * k + i] = some ? best.n[i] : -1;
+        score[stage * k + i] = some ? best.s[i] : INFINITY;
+      }
+    }
+  }
+}
+
+template <int KT>
+void launch_kt(bool mask64, dim3 grid, hipStream_t stream, int64_t n, const int32_t* model_id,
+               const float* pred_len, const double* kv_bytes, const float* dec, int32_t n_nodes,
+               const double* free_bytes, const float* queue_s, const float* cold_s,
+               const uint64_t* mask, double rho, int32_t k, int g_log2, int32_t* node_idx,
+               float* score) {
+  if (mask64)
+    route_kernel<KT, true><<<grid, dim3(kThreads), 0, stream>>>(
+        n, model_id, pred_len, kv_bytes, dec, n_nodes, free_bytes, queue_s, cold_s, mask, rho, k,
+        g_log2, node_idx, score);
+  else
+    route_kernel<KT, false><<<grid, dim3(kThreads), 0, stream>>>(
+        n, model_id, pred_len, kv_bytes, dec, n_nodes, free_bytes, queue_s, cold_s, mask, rho, k,
+        g_log2, node_idx, score);
+}
+
+// Lanes per stage: enough threads to fill the chip (about 2^18), at least 4 nodes per lane.
+int choose_g_log2(int64_t n, int32_t n_nodes) {
+  int gl = 0;
+  while (gl < 6 && n * (int64_t(1) << gl) < (int64_t(1) << 18) && (int64_t(4) << (gl + 1)) <= n_nodes) ++gl;
+  return gl;
+}
+
+}  // namespace
+
+size_t route_workspace_bytes(int64_t, int32_t, int32_t, int32_t) { return 0; }
+
+maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                            const double* kv_bytes, const float* decode_s_per_token,
+                            int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                            const float* queue_s, const float* cold_s,
+                            const uint64_t* resident_mask, double rho, int32_t k,
+                            int32_t* node_idx, float* score, void*, size_t, hipStream_t stream) {
+  if (n == 0) return MAESTRO_OK;
+  const int gl = choose_g_log2(n, n_nodes);
+  const int64_t stages_per_block = kThreads >> gl;
+  const dim3 grid((unsigned)((n + stages_per_block - 1) / stages_per_block));
+  const bool mask64 = n_models > 32;
+#define MAESTRO_ROUTE_KT(KT)                                                                   \
+  launch_kt<KT>(mask64, grid, stream, n, model_id, pred_len, kv_bytes, decode_s_per_token,     \
+                n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k, gl, node_idx, score)
+  if (k <= 1) MAESTRO_ROUTE_KT(1);
+  else if (k <= 2) MAESTRO_ROUTE_KT(2);
+  else if (k <= 4) MAESTRO_ROUTE_KT(4);
+  else if (k <= 8) MAESTRO_ROUTE_KT(8);
+  else MAESTRO_ROUTE_KT(16);
+#undef MAESTRO_ROUTE_KT
+  return launch_status();
+}
+
+}  // namespace maestro

@@ -16,12 +16,14 @@ available, so these seeded draws stand in for them.
 
 Random streams: ``numpy.random.Generator(PCG64(child))`` where the children come from
 ``SeedSequence(seed).spawn(len(STREAMS))`` in the fixed order of ``STREAMS``; every array is
-drawn from its own stream, so changing one size never perturbs another array.
+drawn from its own stream, so changing one size never perturbs another array. The feature
+matrix is drawn in chunks of 65,536 rows, chunk c from the c-th child of the "x" stream.
 """
 from __future__ import annotations
 
 import dataclasses
 import hashlib
+import os
 from dataclasses import dataclass, field
 from typing import Dict, Optional, Tuple
 
@@ -187,9 +189,13 @@ class Workload:
         return out
 
 
-def _streams(seed: int) -> Dict[str, np.random.Generator]:
+def _seeds(seed: int) -> Dict[str, np.random.SeedSequence]:
     children = np.random.SeedSequence(seed).spawn(len(STREAMS))
-    return {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(STREAMS, children)}
+    return dict(zip(STREAMS, children))
+
+
+def _streams(seed: int) -> Dict[str, np.random.Generator]:
+    return {name: np.random.Generator(np.random.PCG64(c)) for name, c in _seeds(seed).items()}
 
 
 def _model_ids(rng: np.random.Generator, n: int, k: int, zipf_s: Optional[float]) -> np.ndarray:
@@ -201,18 +207,41 @@ def _model_ids(rng: np.random.Generator, n: int, k: int, zipf_s: Optional[float]
     return rng.choice(k, size=n, p=p).astype(np.int32)
 
 
-def draw_features(rng: np.random.Generator, n: int, d: int, dtype: str) -> np.ndarray:
+def _bf16_bits_fast(block: np.ndarray) -> np.ndarray:
+    """Same rounding as f32_to_bf16_bits (nearest, ties to even), via PyTorch's multithreaded
+    CPU cast; used only for the large feature matrices."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(block, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def draw_features(seq: np.random.SeedSequence, n: int, d: int, dtype: str) -> np.ndarray:
+    """N(0, 1) features, row chunk c drawn from its own child stream seq.spawn(...)[c] so that
+    chunks can be drawn in parallel threads (numpy releases the GIL while drawing)."""
     out = np.empty((n, d), dtype=np.float32 if dtype == "f32" else np.uint16)
-    for r0 in range(0, n, _X_CHUNK_ROWS):
+    starts = list(range(0, n, _X_CHUNK_ROWS))
+    kids = seq.spawn(len(starts))
+
+    def fill(c):
+        r0 = starts[c]
         r1 = min(n, r0 + _X_CHUNK_ROWS)
-        block = rng.standard_normal((r1 - r0, d), dtype=np.float32)
-        out[r0:r1] = block if dtype == "f32" else f32_to_bf16_bits(block)
+        block = np.random.Generator(np.random.PCG64(kids[c])).standard_normal((r1 - r0, d), dtype=np.float32)
+        out[r0:r1] = block if dtype == "f32" else _bf16_bits_fast(block)
+
+    if len(starts) <= 1:
+        for c in range(len(starts)):
+            fill(c)
+    else:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(fill, range(len(starts))))
     return out
 
 
 def generate(spec: WorkloadSpec, with_x: bool = True) -> Workload:
     """Draw every input of ``spec``. ``with_x=False`` skips the (large) feature matrix."""
-    rs = _streams(spec.seed)
+    seeds = _seeds(spec.seed)
+    rs = {name: np.random.Generator(np.random.PCG64(c)) for name, c in seeds.items()}
     K, M = spec.n_models, spec.n_nodes
 
     # workflows first: they fix the number of stages
@@ -238,7 +267,7 @@ def generate(spec: WorkloadSpec, with_x: bool = True) -> Workload:
         role = rs["role"].integers(0, 5, size=n, dtype=np.int64).astype(np.int32)
 
     D = spec.dims[0]
-    x = draw_features(rs["x"], n, D, spec.dtype) if with_x else None
+    x = draw_features(seeds["x"], n, D, spec.dtype) if with_x else None
 
     mu, sigma, plo, phi = spec.prompt_lognormal
     prompt = np.clip(np.rint(rs["prompt"].lognormal(mu, sigma, size=n)), plo, phi).astype(np.int32)

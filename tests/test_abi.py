@@ -1,0 +1,120 @@
+"""The C-ABI library loads, exports every symbol the header declares, and rejects bad
+arguments on the host before anything is launched (no GPU needed: none of these calls reach
+a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_12950_amd as M
+from paper_2606_12950_amd import _native
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "maestro.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MAESTRO_API\s+[\w\s\*]+?\b(maestro_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(M.LIBRARY_PATH):
+        pytest.fail("libmaestro.so is not built (python -m paper_2606_12950_amd.build)")
+    return M.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) == 7
+    assert sorted(_native.EXPORTS) == names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    assert lib.maestro_status_string(0) == b"ok"
+    assert lib.maestro_status_string(2) == b"unsupported shape"
+    assert lib.maestro_status_string(99) == b"unknown status"
+
+
+# Host addresses that are valid-looking (non-null, aligned) but never dereferenced: every call
+# below fails validation before any launch.
+_buf = (ctypes.c_double * 64)()
+FAKE = ctypes.c_void_p(ctypes.addressof(_buf))
+MISALIGNED = ctypes.c_void_p(ctypes.addressof(_buf) + 4)
+
+
+def _pred(dims, dtype, layers):
+    p = M.Predictor()
+    p.n_layers = layers
+    for i, d in enumerate(dims):
+        p.dims[i] = d
+    p.dtype = dtype
+    for l in range(layers):
+        p.weight[l] = FAKE.value
+        p.bias[l] = FAKE.value
+    p.bin_centre = FAKE.value
+    return p
+
+
+def test_predict_validation(lib):
+    call = lambda p, n=10, x=FAKE: lib.maestro_predict(ctypes.byref(p) if p is not None else None, n, x,
+                                                       FAKE, FAKE, FAKE, 4, FAKE, FAKE, None, 0, None)
+    assert call(None) == INVALID
+    assert call(_pred((256, 512, 512, 64), 1, 3), n=-1) == INVALID
+    assert call(_pred((256, 512, 512, 64), 7, 3)) == INVALID                   # bad dtype
+    assert call(_pred((256, 512, 512, 64), 1, 3), x=None) == INVALID          # null features
+    assert call(_pred((256, 512, 512, 64), 1, 3), x=MISALIGNED) == INVALID    # misaligned
+    p = _pred((256, 512, 512, 64), 1, 3)
+    p.weight[1] = None
+    assert call(p) == INVALID                                                 # missing layer
+    assert call(_pred((256, 512, 0, 64), 1, 3)) == INVALID                    # zero width
+    assert call(_pred((256, 384, 512, 64), 1, 3)) == UNSUPPORTED              # not built
+    assert call(_pred((64, 128, 32), 1, 2)) == UNSUPPORTED                    # wrong dtype
+    assert lib.maestro_predict_workspace(ctypes.byref(_pred((64, 128, 32), 0, 2)), 100) == 0
+
+
+def test_route_validation(lib):
+    def call(n=10, n_models=8, n_nodes=16, k=1, rho=0.0, model=FAKE, free=FAKE):
+        return lib.maestro_route(n, model, FAKE, FAKE, FAKE, n_models, n_nodes, free, FAKE, FAKE, FAKE,
+                                 rho, k, FAKE, FAKE, None, 0, None)
+    assert call(n=-1) == INVALID
+    assert call(n_models=0) == INVALID
+    assert call(n_models=65) == INVALID
+    assert call(n_nodes=0) == INVALID
+    assert call(k=0) == INVALID
+    assert call(k=17) == INVALID
+    assert call(rho=-0.1) == INVALID
+    assert call(rho=float("nan")) == INVALID
+    assert call(rho=float("inf")) == INVALID
+    assert call(model=None) == INVALID
+    assert call(free=MISALIGNED) == INVALID
+
+
+def test_prioritize_validation_and_workspace(lib):
+    ws = lib.maestro_prioritize_workspace(131072, 720000)
+    # four key/value arrays padded to 4096-key tiles plus a 256-entry count table per tile
+    tiles = 131072 // 4096
+    assert ws == 4 * 4 * tiles * 4096 + 4 * 256 * tiles
+    assert lib.maestro_prioritize_workspace(0, 0) == 0
+    assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 4096 + 4 * 256
+    call = lambda W=4, S=8, off=FAKE, ws=FAKE, ws_bytes=1 << 20: lib.maestro_prioritize(
+        W, S, off, FAKE, None, FAKE, 0, None, FAKE, FAKE, ws, ws_bytes, None)
+    assert call(W=-1) == INVALID
+    assert call(S=-1) == INVALID
+    assert call(off=None) == INVALID
+    assert call(ws_bytes=100) == WORKSPACE
+    assert call(ws=None) == WORKSPACE
+    assert call(W=0) == OK                                                   # empty: no-op
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_native, "_lib", None)
+    monkeypatch.setattr(_native, "LIBRARY_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        _native.load()

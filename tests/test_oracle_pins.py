@@ -408,3 +408,22 @@ def test_prioritize_empty_and_validation():
     assert key.size == 0 and order.size == 0
     with pytest.raises(RuntimeError):
         oracle.prioritize(np.array([0, 3, 2], np.int64), np.zeros(2, np.float32), np.zeros(2, np.int64), 0)
+
+
+def test_generator_bf16_casts_agree():
+    # the fast cast used for large feature matrices rounds exactly like the reference cast
+    rng = np.random.default_rng(30)
+    v = (rng.standard_normal(200000) * 10.0 ** rng.integers(-20, 20, 200000)).astype(np.float32)
+    v[:4] = [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 0.0]
+    assert np.array_equal(W._bf16_bits_fast(v), W.f32_to_bf16_bits(v))
+
+
+def test_generator_is_deterministic():
+    a = W.workload("c3", n_workflows=500)
+    b = W.workload("c3", n_workflows=500)
+    assert a.sha256() == b.sha256()
+    assert a.n == int(a.chain_offset[-1]) and 3 * 500 <= a.n <= 8 * 500
+    assert np.all(np.diff(a.chain_offset) >= 3) and np.all(np.diff(a.chain_offset) <= 8)
+    c = W.workload("c1", n_stages=100)
+    assert c.x.dtype == np.uint16 and c.x.shape == (100, 256)
+    assert set(np.unique(c.kv_bytes_per_token)) <= {65536.0, 131072.0, 327680.0}
