@@ -80,7 +80,7 @@ typedef struct maestro_predictor {
 /* Cost prediction for n stages (Sec. III-B; Eq. 3).
  *   x                   [n][D] row-major, element type p->dtype, 16-byte aligned
  *   prompt_len          [n] int32: prompt tokens P of each stage
- *   model_id            [n] int32 in [0, n_models): the stage's model M(T)
+ *   model_id            [n] int32 in [0, n_models): the stage's model M(T), 1 <= n_models <= 64
  *   kv_bytes_per_token  [n_models] float32: alpha(M), KV bytes per token of each model
  *   pred_len  (out)     [n] float32: predicted output length L (tokens)
  *   kv_bytes  (out)     [n] float64: R_kv = ((double)P + (double)L) * (double)alpha(M);

@@ -41,7 +41,7 @@ maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void
                                size_t workspace_bytes, void* stream) {
   (void)workspace;
   (void)workspace_bytes;
-  if (!p || n < 0 || n_models < 1) return MAESTRO_ERR_INVALID_ARG;
+  if (!p || n < 0 || n_models < 1 || n_models > 64) return MAESTRO_ERR_INVALID_ARG;
   if (p->n_layers < 1 || p->n_layers > 4) return MAESTRO_ERR_INVALID_ARG;
   if (p->dtype != MAESTRO_F32 && p->dtype != MAESTRO_BF16) return MAESTRO_ERR_INVALID_ARG;
   for (int l = 0; l <= p->n_layers; ++l)
@@ -59,8 +59,8 @@ maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void
   }
   if (!maestro::predict_shape_supported(*p)) return MAESTRO_ERR_UNSUPPORTED;
   if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;  // grid limit: 2^30 blocks of 128 rows
-  return maestro::launch_predict(*p, n, x, prompt_len, model_id, kv_bytes_per_token, pred_len,
-                                 kv_bytes, as_stream(stream));
+  return maestro::launch_predict(*p, n, x, prompt_len, model_id, kv_bytes_per_token, n_models,
+                                 pred_len, kv_bytes, as_stream(stream));
 }
 
 maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,

@@ -12,7 +12,7 @@ namespace maestro {
 // Cost prediction: fused MLP + softmax + expected length + KV bytes.
 maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void* x,
                               const int32_t* prompt_len, const int32_t* model_id,
-                              const float* kv_bytes_per_token, float* pred_len,
+                              const float* kv_bytes_per_token, int32_t n_models, float* pred_len,
                               double* kv_bytes, hipStream_t stream);
 bool predict_shape_supported(const maestro_predictor& p);
 

@@ -13,9 +13,11 @@
 // consumed block by block into the logit accumulators without ever being stored whole.
 //
 // Weights stream through LDS: each 32-neuron block of a layer (plus, for the last hidden
-// layer, the matching 32 columns of the logit layer) is staged once per workgroup in a
-// double buffer and read by the four wavefronts; rows are padded by 8 bytes so that the 32
-// rows a wavefront reads at one column fall in distinct LDS banks.
+// layer, the matching 32 columns of the logit layer) is copied once per workgroup into a
+// double buffer by direct global->LDS loads (no staging registers) while the previous block
+// is being multiplied, and read by all four wavefronts with 16-byte LDS reads. Weight rows
+// are padded by 16 bytes in LDS so that the 16 rows a half-wavefront reads at one column
+// fall in distinct banks.
 #include "internal.h"
 
 namespace maestro {
@@ -31,14 +33,10 @@ constexpr int kThreads = kWaves * 64;
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
+
 // Output row (neuron or bin) of a 32x32 MFMA result held in accumulator register v by
 // lane-half h (lanes 0-31: h = 0, lanes 32-63: h = 1); the column is the lane's row r.
 __device__ __forceinline__ int acc_row(int v, int h) { return (v >> 2) * 8 + h * 4 + (v & 3); }
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint2 lo, uint2 hi) {
-  uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-  return __builtin_bit_cast(bf16x8, u);
-}
 
 // 16 consecutive floats of a 32-wide slice as seen by accumulator registers of lane-half h:
 // out[v] = src[acc_row(v, h)].
@@ -55,9 +53,7 @@ __device__ __forceinline__ void load_acc_layout(const float* __restrict__ src, i
 template <int BT>
 __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const float* __restrict__ b_last,
                                                 const float* __restrict__ centre, int h, int64_t row, int64_t n,
-                                                const int32_t* __restrict__ prompt_len,
-                                                const int32_t* __restrict__ model_id,
-                                                const float* __restrict__ alpha,
+                                                int32_t prompt, int32_t model, const float* __restrict__ alpha,
                                                 float* __restrict__ pred_len, double* __restrict__ kv_bytes) {
   float z[BT][16], c[BT][16];
   float mx = -INFINITY;
@@ -88,190 +84,347 @@ __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const
   if (h == 0 && row < n) {
     const float pred = sc / se;
     pred_len[row] = pred;
-    const int m = model_id[row];
-    kv_bytes[row] = ((double)prompt_len[row] + (double)pred) * (double)alpha[m];
+    kv_bytes[row] = ((double)prompt + (double)pred) * (double)alpha[model];
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// bfloat16, three Linear layers: D -> H1 -> H2 -> B
+// bfloat16, three Linear layers: D -> H1 -> H2 -> B   (D = 256)
 // ---------------------------------------------------------------------------------------------
+//
+// Persistent workgroups (one per compute unit) walk 128-row tiles. Everything a tile reads
+// from global memory arrives as a fixed sequence of LDS "chunks":
+//   feature chunk j (j = 0, 1) : features of tile rows 64j .. 64j+63 (and, with chunk 0, the
+//                                tile's prompt lengths and model ids)
+//   layer-1 chunk j            : W1 rows 64j .. 64j+63 (two 32-neuron blocks), all D columns
+//   layer-2 chunk (b, p)       : W2 rows 32b .. 32b+31, columns 512p .. 512p+511, plus, for
+//                                the last p, W3 columns 32b .. 32b+31 of every bin row
+// Chunks rotate through kBufs LDS buffers and are fetched kBufs-1 chunks ahead (across tile
+// boundaries) by direct global->LDS loads, so every fetch overlaps the multiplication of
+// earlier chunks. Each wavefront waits only for the loads of the chunk needed next (counted
+// vmcnt), then the workgroup barrier publishes it. No other global load is in flight, so no
+// wait ever drains the prefetch.
+//
+// LDS layouts (all 16-byte reads are free of bank conflicts per quarter-wavefront):
+//   feature chunk: 64 rows of 512 bytes, the 16-byte units of row r stored at unit ^ (r % 16)
+//   layer-1 chunk: row pairs (2i, 2i+1) stored contiguously (1 KB), 16-byte pad per pair; in
+//                  odd rows the 16-byte units are stored with index bit 3 flipped
+//   layer-2 chunk: 32 rows of 1 KB, 16-byte pad per row; then the W3 slice, B rows x 64 bytes
+//                  with the four units of row r rotated by (r / 4) % 4
+
+// Output neuron (within a 32-neuron block) computed by row i of a weight tile. With this order
+// the 16 results that lane-half h holds after a 32x32 MFMA (register v -> tile row
+// (v/4)*8 + 4h + v%4) are the neurons 16*(v/8) + 8h + v%8: two runs of 8 consecutive
+// neurons, which the next layer consumes in natural column order.
+__device__ __forceinline__ int tile_row_neuron(int i) {
+  const int q = i >> 3;
+  return 16 * (q >> 1) + 8 * ((i >> 2) & 1) + 4 * (q & 1) + (i & 3);
+}
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// acc += sum_k A_k * B[k0 + k], A_k the 16-byte LDS fragment at (k & 4 ? pb : pa) + 32k (the
+// two bases absorb the layer-1 unit swizzle; pass pa == pb elsewhere). Fragments are read
+// kLookahead steps ahead of their MFMA, and side(k) -- a slice of the previous block's
+// epilogue -- is issued right after MFMA k so that it runs while the matrix core is busy.
+// The scheduling barriers keep exactly this order.
+constexpr int kLookahead = 3;
+template <int KS, int NBREG, typename Side>
+__device__ __forceinline__ void mfma_chain(f32x16& acc, const unsigned char* pa, const unsigned char* pb,
+                                           const bf16x8 (&b)[NBREG], int k0, Side&& side) {
+  bf16x8 fr[KS];
+#pragma unroll
+  for (int k = 0; k < kLookahead && k < KS; ++k)
+    fr[k] = *reinterpret_cast<const bf16x8*>(((k & 4) ? pb : pa) + k * 32);
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if (k + kLookahead < KS) {
+      const int kk = k + kLookahead;
+      fr[kk] = *reinterpret_cast<const bf16x8*>(((kk & 4) ? pb : pa) + kk * 32);
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[k], b[k0 + k], acc, 0, 0, 0);
+    side(k);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// relu(acc[8*half + j] + bias[j]) for j = 0..7, rounded to bfloat16 (nearest even) and packed
+// as the 8 K-slots of a B operand.
+__device__ __forceinline__ bf16x8 bias_relu_bf16(const f32x16& acc, int half, const float* __restrict__ bias) {
+  const float4 b0 = *reinterpret_cast<const float4*>(bias);
+  const float4 b1 = *reinterpret_cast<const float4*>(bias + 4);
+  const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+  uint32_t w[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    f32x2 f = {fmaxf(acc[8 * half + 2 * p] + bb[2 * p], 0.0f),
+               fmaxf(acc[8 * half + 2 * p + 1] + bb[2 * p + 1], 0.0f)};
+    w[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+  }
+  return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+}
+
+// Pipelined "relu(acc + bias) -> bfloat16" of one finished 32-neuron block, in slices:
+// step 0 reads the 16 biases of the lane's neurons, steps 1..8 convert one pair of values
+// each; the result is the B-operand pair out[0] (neurons 16*0 + 8h + 0..7) and out[1].
+struct BlockEpilogue {
+  float bias[16];
+  uint32_t w[8];
+  __device__ __forceinline__ void step(int k, const f32x16& acc, const float* __restrict__ b32, int h) {
+    if (k == 0) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const float4 b0 = *reinterpret_cast<const float4*>(b32 + half * 16 + h * 8);
+        const float4 b1 = *reinterpret_cast<const float4*>(b32 + half * 16 + h * 8 + 4);
+        bias[8 * half + 0] = b0.x; bias[8 * half + 1] = b0.y; bias[8 * half + 2] = b0.z;
+        bias[8 * half + 3] = b0.w; bias[8 * half + 4] = b1.x; bias[8 * half + 5] = b1.y;
+        bias[8 * half + 6] = b1.z; bias[8 * half + 7] = b1.w;
+      }
+    } else if (k <= 8) {
+      const int p = k - 1;
+      f32x2 f = {fmaxf(acc[2 * p] + bias[2 * p], 0.0f), fmaxf(acc[2 * p + 1] + bias[2 * p + 1], 0.0f)};
+      w[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+    }
+  }
+  __device__ __forceinline__ bf16x8 out(int half) const {
+    return __builtin_bit_cast(bf16x8, make_uint4(w[4 * half], w[4 * half + 1], w[4 * half + 2], w[4 * half + 3]));
+  }
+};
+
+constexpr int kBufs = 4;                 // LDS chunk buffers (prefetch distance kBufs - 1)
+constexpr int kDmaPerChunk = 8;          // direct loads per wavefront per chunk (at least)
+
+// Direct global->LDS loads: lane l's 16 (or 4) bytes at gbase + voff land at LDS byte address
+// lds_dst + 16 l (or 4 l). Issued as inline assembly so that the compiler's automatic wait
+// insertion, which would conservatively drain every such load before any LDS read, does not
+// see them; the kernel waits for them itself (wait_chunk). gbase must be uniform.
+typedef __attribute__((address_space(3))) unsigned char lds_uchar;
+__device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, const unsigned char* lds_dst) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_uchar*)(lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(gbase) : "m0");
+}
+__device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, const unsigned char* lds_dst) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_uchar*)(lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(m0), "v"(voff), "s"(gbase) : "m0");
+}
+
+// Wait until at most N vector-memory operations of this wavefront are outstanding and all of
+// its LDS operations are done (gfx9 s_waitcnt encoding), then the workgroup barrier. The
+// empty asm statements keep the compiler from moving LDS accesses across.
+template <int N>
+__device__ __forceinline__ void wait_chunk() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+constexpr int kMaxModels = 64;           // per-model KV bytes staged in LDS
+
 template <int D, int H1, int H2, int B>
-__global__ __launch_bounds__(kThreads) void mlp3_bf16_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void mlp3_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w1, const uint16_t* __restrict__ w2,
     const uint16_t* __restrict__ w3, const float* __restrict__ b1, const float* __restrict__ b2,
-    const float* __restrict__ b3, const float* __restrict__ centre, int64_t n,
+    const float* __restrict__ b3, const float* __restrict__ centre, int64_t n, int64_t n_tiles,
     const int32_t* __restrict__ prompt_len, const int32_t* __restrict__ model_id,
-    const float* __restrict__ alpha, float* __restrict__ pred_len, double* __restrict__ kv_bytes) {
-  static_assert(D % 16 == 0 && H1 % 32 == 0 && H2 % 32 == 0 && B % 32 == 0, "tile shape");
-  constexpr int KS1 = D / 16;        // K-steps of layer 1 (32x32x16 MFMA)
-  constexpr int NB1 = H1 / 32;       // neuron blocks of layer 1
-  constexpr int KS2 = H1 / 16;       // K-steps of layer 2
-  constexpr int NB2 = H2 / 32;       // neuron blocks of layer 2
-  constexpr int BT = B / 32;         // bin tiles of the logit layer
-  constexpr int ROW1 = 2 * D + 8;    // LDS row strides in bytes (8-byte pad)
-  constexpr int ROW2 = 2 * H1 + 8;
-  constexpr int ROW3 = 2 * 32 + 8;
+    const float* __restrict__ alpha, int32_t n_models, float* __restrict__ pred_len,
+    double* __restrict__ kv_bytes) {
+  static_assert(D == 256, "feature and layer-1 chunk layouts assume 512-byte rows");
+  static_assert(H1 % 512 == 0 && H2 % 32 == 0 && B % 64 == 0, "tile shape");
+  constexpr int KS1 = D / 16;             // K-steps of layer 1 (32x32x16 MFMA)
+  constexpr int NX = 2;                   // feature chunks per tile
+  constexpr int NC1 = H1 / 64;            // layer-1 chunks (two neuron blocks each)
+  constexpr int KP = H1 / 512;            // column parts of a layer-2 block
+  constexpr int NB2 = H2 / 32;            // layer-2 neuron blocks
+  constexpr int NC = NX + NC1 + NB2 * KP; // chunks per tile
+  constexpr int BT = B / 32;              // bin tiles
+  constexpr int PAIR = 1024 + 16;         // layer-1 chunk: bytes per row pair
+  constexpr int ROW2 = 1024 + 16;         // layer-2 chunk: bytes per row
   constexpr int W3OFF = 32 * ROW2;
-  constexpr int CHUNK = cmax(32 * ROW1, 32 * ROW2 + B * ROW3);
-  constexpr int P1 = 32 * D / 8;     // 16-byte pieces per staged chunk part
-  constexpr int P2 = 32 * H1 / 8;
-  constexpr int P3 = B * 32 / 8;
-  constexpr int R1 = (P1 + kThreads - 1) / kThreads;
-  constexpr int R2 = (P2 + kThreads - 1) / kThreads;
-  constexpr int R3 = (P3 + kThreads - 1) / kThreads;
-  constexpr int RP = cmax(R1, R2 + R3);
+  constexpr int CHUNK = cmax(cmax(64 * 512, 32 * PAIR), W3OFF + B * 64);
+  static_assert(NC >= kBufs - 1, "prologue fetches whole chunks of the first tile");
 
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][CHUNK];
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kBufs * CHUNK];
+  __shared__ __attribute__((aligned(16))) float s_b1[H1];
+  __shared__ __attribute__((aligned(16))) float s_b2[H2];
+  __shared__ __attribute__((aligned(16))) float s_b3[B];
+  __shared__ __attribute__((aligned(16))) float s_c[B];
+  __shared__ __attribute__((aligned(16))) float s_alpha[kMaxModels];
+  __shared__ __attribute__((aligned(16))) int32_t s_meta[2][2][kRowsPerBlock];  // [tile parity][prompt, model][row]
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, r32 = lane & 31;
-  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + wave * kRowsPerWave + r32;
-  const int64_t xrow = row < n ? row : n - 1;
+  // wave index as a scalar: keeps every DMA source row address and LDS destination in SGPRs
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, h = lane >> 5, r32 = lane & 31;
+  const int64_t first_tile = blockIdx.x, stride = gridDim.x;
 
-  uint4 pre[RP];
-  // layer-1 chunk nb: W1 rows nb*32 .. nb*32+31
-  auto fetch1 = [&](int nb) {
-#pragma unroll
-    for (int i = 0; i < R1; ++i) {
-      const int p = tid + i * kThreads;
-      if (P1 % kThreads == 0 || p < P1) {
-        const int r = p / (D / 8), c8 = p % (D / 8);
-        pre[i] = *reinterpret_cast<const uint4*>(w1 + (size_t)(nb * 32 + r) * D + c8 * 8);
+  // ---- fetch of chunk c of tile t into LDS buffer dst, one load instruction per call:
+  // q = 0 .. kDmaPerChunk-1 are always issued; q = kDmaPerChunk adds the tile's prompt
+  // lengths / model ids (feature chunk 0) or the W3 slice (last part of a layer-2 block)
+  const uint32_t voff1 = (uint32_t)(((lane >> 5) * D + (((lane & 31) ^ ((lane >> 5) << 3)) * 8)) * 2);
+  const uint32_t voff2 = (uint32_t)(lane * 16);
+  const uint32_t voff3 = (uint32_t)(((lane >> 2) * H2 + (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
+  auto fetch_one = [&](int64_t t, int c, unsigned char* dst, int q) {
+    if (c < NX) {
+      // tile rows 64c + 2i + (lane / 32), i = wave + 4q, clamped to the last stage; a fetch
+      // past the last tile re-reads the last tile (never consumed)
+      const int64_t tt = t < n_tiles ? t : n_tiles - 1;
+      if (q < kDmaPerChunk) {
+        const int64_t row0 = tt * kRowsPerBlock + 64 * c;
+        const int i = wave + q * kWaves;
+        const int rho = 2 * i + (lane >> 5);                  // row within the chunk
+        const int64_t base = min(row0 + 2 * i, n - 1);
+        const int64_t rw = min(row0 + rho, n - 1);
+        const uint32_t unit = (uint32_t)((lane & 31) ^ (rho & 15));
+        dma16(x + base * D, (uint32_t)(rw - base) * (D * 2) + unit * 16, dst + i * 1024);
+      } else if (q == kDmaPerChunk && c == 0) {
+        // prompt lengths (waves 0, 1) and model ids (waves 2, 3) of the tile, 64 rows each
+        const int64_t r0 = tt * kRowsPerBlock + 64 * (wave & 1);
+        const int64_t base = min(r0, n - 1);
+        const int64_t rw = min(r0 + lane, n - 1);
+        const int32_t* src = (wave < 2) ? prompt_len : model_id;
+        const int parity = (int)(((t - first_tile) / stride) & 1);
+        dma4(src + base, (uint32_t)(rw - base) * 4,
+             reinterpret_cast<const unsigned char*>(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
+      }
+    } else if (c < NX + NC1) {
+      // rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units with bit 3 flipped)
+      if (q < kDmaPerChunk) {
+        const int j = c - NX, i = wave + q * kWaves;
+        dma16(w1 + (size_t)(64 * j + 2 * i) * D, voff1, dst + i * PAIR);
+      }
+    } else {
+      const int b = (c - NX - NC1) / KP, part = (c - NX - NC1) % KP;
+      if (q < kDmaPerChunk) {
+        const int r = wave + q * kWaves;
+        dma16(w2 + (size_t)(32 * b + r) * H1 + part * 512, voff2, dst + r * ROW2);
+      } else if (q == kDmaPerChunk && part == KP - 1) {
+        // W3 rows 16i .. 16i+15 (i = wave), columns 32b .. 32b+31: lane -> row 16i + lane/4,
+        // unit (lane % 4) rotated by (row / 4) % 4
+        static_assert(B / 16 == kWaves, "one W3 slice load per wavefront");
+        dma16(w3 + (size_t)(16 * wave) * H2 + 32 * b, voff3, dst + W3OFF + wave * 1024);
       }
     }
   };
-  auto store1 = [&](unsigned char* buf) {
+  auto fetch = [&](int64_t t, int c, unsigned char* dst) {
 #pragma unroll
-    for (int i = 0; i < R1; ++i) {
-      const int p = tid + i * kThreads;
-      if (P1 % kThreads == 0 || p < P1) {
-        const int r = p / (D / 8), c8 = p % (D / 8);
-        uint2* d = reinterpret_cast<uint2*>(buf + r * ROW1 + c8 * 16);
-        d[0] = make_uint2(pre[i].x, pre[i].y);
-        d[1] = make_uint2(pre[i].z, pre[i].w);
-      }
-    }
-  };
-  // layer-2 chunk nb2: W2 rows nb2*32 .. +31, and W3 columns nb2*32 .. +31 (all B rows)
-  auto fetch2 = [&](int nb2) {
-#pragma unroll
-    for (int i = 0; i < R2; ++i) {
-      const int p = tid + i * kThreads;
-      if (P2 % kThreads == 0 || p < P2) {
-        const int r = p / (H1 / 8), c8 = p % (H1 / 8);
-        pre[i] = *reinterpret_cast<const uint4*>(w2 + (size_t)(nb2 * 32 + r) * H1 + c8 * 8);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < R3; ++i) {
-      const int p = tid + i * kThreads;
-      if (P3 % kThreads == 0 || p < P3) {
-        const int r = p / 4, c8 = p % 4;
-        pre[R2 + i] = *reinterpret_cast<const uint4*>(w3 + (size_t)r * H2 + nb2 * 32 + c8 * 8);
-      }
-    }
-  };
-  auto store2 = [&](unsigned char* buf) {
-#pragma unroll
-    for (int i = 0; i < R2; ++i) {
-      const int p = tid + i * kThreads;
-      if (P2 % kThreads == 0 || p < P2) {
-        const int r = p / (H1 / 8), c8 = p % (H1 / 8);
-        uint2* d = reinterpret_cast<uint2*>(buf + r * ROW2 + c8 * 16);
-        d[0] = make_uint2(pre[i].x, pre[i].y);
-        d[1] = make_uint2(pre[i].z, pre[i].w);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < R3; ++i) {
-      const int p = tid + i * kThreads;
-      if (P3 % kThreads == 0 || p < P3) {
-        const int r = p / 4, c8 = p % 4;
-        uint2* d = reinterpret_cast<uint2*>(buf + W3OFF + r * ROW3 + c8 * 16);
-        d[0] = make_uint2(pre[R2 + i].x, pre[R2 + i].y);
-        d[1] = make_uint2(pre[R2 + i].z, pre[R2 + i].w);
-      }
-    }
-  };
-  // A operand, natural K order: columns col + 8h .. col + 8h + 7 of the lane's row
-  auto frag_nat = [&](const unsigned char* base, int stride, int col) -> bf16x8 {
-    const unsigned char* p = base + r32 * stride + (col + h * 8) * 2;
-    return as_bf16x8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 8));
-  };
-  // A operand, chained K order: columns col + 4h .. +3 and col + 8 + 4h .. +3, matching the
-  // neurons a 32x32 result tile leaves in registers 8*half .. 8*half + 7 (col = 16 * step)
-  auto frag_chain = [&](const unsigned char* base, int stride, int col) -> bf16x8 {
-    const unsigned char* p = base + r32 * stride + (col + h * 4) * 2;
-    return as_bf16x8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 16));
+    for (int q = 0; q <= kDmaPerChunk; ++q) fetch_one(t, c, dst, q);
   };
 
-  // B operand of layer 1: row xrow, natural K order
-  bf16x8 xf[KS1];
-  {
-    const uint16_t* xp = x + xrow * D + h * 8;
+  // per-lane LDS offsets of the A operands
+  const int prow = tile_row_neuron(r32);
+  int l1a[2], l1b[2];                     // layer-1 chunk, neuron block lb (rows 32lb + prow)
 #pragma unroll
-    for (int ks = 0; ks < KS1; ++ks) xf[ks] = *reinterpret_cast<const bf16x8*>(xp + ks * 16);
+  for (int lb = 0; lb < 2; ++lb) {
+    const int rho = 32 * lb + prow, odd = rho & 1;
+    const int base = (rho >> 1) * PAIR + odd * 512 + h * 16;
+    l1a[lb] = base + odd * 128;           // K-steps with bit 2 clear: unit bit 3 set for odd rows
+    l1b[lb] = base - odd * 128;           // K-steps with bit 2 set: unit bit 3 cleared
   }
+  const int l2 = prow * ROW2 + h * 16;
+  const int sw3 = (r32 >> 2) & 3;
+  const int xrow = 32 * (wave & 1) + r32; // this lane's row within its feature chunk
 
-  fetch1(0);
-  store1(lds[0]);
+  for (int i = tid; i < H1; i += kThreads) s_b1[i] = b1[i];
+  for (int i = tid; i < H2; i += kThreads) s_b2[i] = b2[i];
+  for (int i = tid; i < B; i += kThreads) { s_b3[i] = b3[i]; s_c[i] = centre[i]; }
+  for (int i = tid; i < kMaxModels; i += kThreads) s_alpha[i] = i < n_models ? alpha[i] : 0.0f;
   __syncthreads();
 
-  // ---- layer 1: H1 = relu(W1 x + b1), kept as the B operand of layer 2 -----------------
-  bf16x8 h1[KS2];
+  // chunk g of this workgroup's stream lives in buffer g % kBufs
+  int g = 0;
 #pragma unroll
-  for (int nb = 0; nb < NB1; ++nb) {
-    const unsigned char* buf = lds[nb & 1];
-    if (nb + 1 < NB1) fetch1(nb + 1); else fetch2(0);
-    f32x16 acc = {};
-#pragma unroll
-    for (int ks = 0; ks < KS1; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_nat(buf, ROW1, ks * 16), xf[ks], acc, 0, 0, 0);
-    float bias[16];
-    load_acc_layout(b1 + nb * 32, h, bias);
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        h1[2 * nb + half][j] = (__bf16)fmaxf(acc[8 * half + j] + bias[8 * half + j], 0.0f);
-    }
-    if (nb + 1 < NB1) store1(lds[(nb + 1) & 1]); else store2(lds[(nb + 1) & 1]);
-    __syncthreads();
-  }
+  for (int c = 0; c < kBufs - 1; ++c) fetch(first_tile, c, lds + c * CHUNK);
+  wait_chunk<kDmaPerChunk * (kBufs - 2)>();
 
-  // ---- layer 2 block by block, each block folded straight into the logits ---------------
-  f32x16 logit[BT];
-#pragma unroll
-  for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
-  for (int nb2 = 0; nb2 < NB2; ++nb2) {
-    const unsigned char* buf = lds[(NB1 + nb2) & 1];
-    if (nb2 + 1 < NB2) fetch2(nb2 + 1);
-    f32x16 acc = {};
-#pragma unroll
-    for (int t = 0; t < KS2; ++t)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_chain(buf, ROW2, t * 16), h1[t], acc, 0, 0, 0);
-    float bias[16];
-    load_acc_layout(b2 + nb2 * 32, h, bias);
-    bf16x8 h2[2];
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        h2[half][j] = (__bf16)fmaxf(acc[8 * half + j] + bias[8 * half + j], 0.0f);
-    }
-#pragma unroll
-    for (int bt = 0; bt < BT; ++bt) {
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-        logit[bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            frag_chain(buf + W3OFF + bt * 32 * ROW3, ROW3, tt * 16), h2[tt], logit[bt], 0, 0, 0);
-    }
-    if (nb2 + 1 < NB2) store2(lds[(NB1 + nb2 + 1) & 1]);
-    __syncthreads();
-  }
+  // fetch the chunk kBufs - 1 ahead of chunk c of tile t (possibly in the next tile)
+  auto prefetch = [&](int64_t t, int c) {
+    int pc = c + kBufs - 1;
+    int64_t pt = t;
+    if (pc >= NC) { pc -= NC; pt += stride; }
+    fetch(pt, pc, lds + ((g + kBufs - 1) % kBufs) * CHUNK);
+  };
+  auto advance = [&]() {
+    wait_chunk<kDmaPerChunk * (kBufs - 2)>();
+    ++g;
+  };
 
-  length_epilogue<BT>(logit, b3, centre, h, row, n, prompt_len, model_id, alpha, pred_len, kv_bytes);
+  for (int64_t tile = first_tile; tile < n_tiles; tile += stride) {
+    const int parity = (int)(((tile - first_tile) / stride) & 1);
+
+    // ---- features of this tile: B operand of layer 1, natural K order -------------------
+    bf16x8 xf[KS1];
+#pragma unroll
+    for (int c = 0; c < NX; ++c) {
+      const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+      prefetch(tile, c);
+      if ((wave >> 1) == c) {
+#pragma unroll
+        for (int ks = 0; ks < KS1; ++ks)
+          xf[ks] = *reinterpret_cast<const bf16x8*>(buf + xrow * 512 + (((2 * ks + h) ^ (xrow & 15)) << 4));
+      }
+      advance();
+    }
+
+    // ---- layer 1: H1 = relu(W1 x + b1), kept as the B operand of layer 2 ---------------
+    bf16x8 h1[H1 / 16];
+#pragma unroll
+    for (int c = 0; c < NC1; ++c) {
+      const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+      prefetch(tile, NX + c);
+#pragma unroll
+      for (int lb = 0; lb < 2; ++lb) {
+        f32x16 acc = {};
+        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [](int) {});
+        const int nb = 2 * c + lb;
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+          h1[2 * nb + half] = bias_relu_bf16(acc, half, s_b1 + nb * 32 + half * 16 + h * 8);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      advance();
+    }
+
+    // ---- layer 2 block by block, each block folded straight into the logits -----------
+    f32x16 logit[BT];
+#pragma unroll
+    for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
+    for (int b = 0; b < NB2; ++b) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int part = 0; part < KP; ++part) {
+        const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+        prefetch(tile, NX + NC1 + b * KP + part);
+        mfma_chain<32, H1 / 16>(acc, buf + l2, buf + l2, h1, part * 32, [](int) {});
+        if (part == KP - 1) {
+          bf16x8 h2[2];
+#pragma unroll
+          for (int half = 0; half < 2; ++half)
+            h2[half] = bias_relu_bf16(acc, half, s_b2 + b * 32 + half * 16 + h * 8);
+#pragma unroll
+          for (int bt = 0; bt < BT; ++bt) {
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+              const int off = W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4);
+              logit[bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  *reinterpret_cast<const bf16x8*>(buf + off), h2[tt], logit[bt], 0, 0, 0);
+            }
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        advance();
+      }
+    }
+
+    const int local = wave * kRowsPerWave + r32;
+    const int64_t row = tile * kRowsPerBlock + local;
+    length_epilogue<BT>(logit, s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
+                        s_alpha, pred_len, kv_bytes);
+  }
+  wait_chunk<0>();                        // no load into LDS outlives the workgroup
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -338,7 +491,9 @@ __global__ __launch_bounds__(kThreads) void mlp2_f32_kernel(
     logit[bt] = acc;
   }
 
-  length_epilogue<BT>(logit, b2, centre, h, row, n, prompt_len, model_id, alpha, pred_len, kv_bytes);
+  const int32_t prompt = row < n ? prompt_len[row] : 0;
+  const int32_t model = row < n ? model_id[row] : 0;
+  length_epilogue<BT>(logit, b2, centre, h, row, n, prompt, model, alpha, pred_len, kv_bytes);
 }
 
 bool dims_are(const maestro_predictor& p, int32_t layers, int32_t dtype, const int32_t* d) {
@@ -361,7 +516,7 @@ bool predict_shape_supported(const maestro_predictor& p) {
 
 maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void* x,
                               const int32_t* prompt_len, const int32_t* model_id,
-                              const float* kv_bytes_per_token, float* pred_len,
+                              const float* kv_bytes_per_token, int32_t n_models, float* pred_len,
                               double* kv_bytes, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   const dim3 grid((unsigned)((n + kRowsPerBlock - 1) / kRowsPerBlock)), block(kThreads);
@@ -370,18 +525,22 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
         static_cast<const float*>(x), static_cast<const float*>(p.weight[0]),
         static_cast<const float*>(p.weight[1]), p.bias[0], p.bias[1], p.bin_centre, n, prompt_len,
         model_id, kv_bytes_per_token, pred_len, kv_bytes);
-  } else if (dims_are(p, 3, MAESTRO_BF16, kBf16Mid)) {
-    mlp3_bf16_kernel<256, 512, 512, 64><<<grid, block, 0, stream>>>(
-        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
-        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
-        p.bias[0], p.bias[1], p.bias[2], p.bin_centre, n, prompt_len, model_id,
-        kv_bytes_per_token, pred_len, kv_bytes);
-  } else if (dims_are(p, 3, MAESTRO_BF16, kBf16Wide)) {
-    mlp3_bf16_kernel<256, 1024, 1024, 64><<<grid, block, 0, stream>>>(
-        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
-        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
-        p.bias[0], p.bias[1], p.bias[2], p.bin_centre, n, prompt_len, model_id,
-        kv_bytes_per_token, pred_len, kv_bytes);
+  } else if (dims_are(p, 3, MAESTRO_BF16, kBf16Mid) || dims_are(p, 3, MAESTRO_BF16, kBf16Wide)) {
+    const int64_t n_tiles = (n + kRowsPerBlock - 1) / kRowsPerBlock;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+      return MAESTRO_ERR_LAUNCH;
+    const dim3 pgrid((unsigned)(n_tiles < cus ? n_tiles : cus));
+    auto args = [&](auto kernel) {
+      kernel<<<pgrid, block, 0, stream>>>(
+          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
+          static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
+          p.bias[0], p.bias[1], p.bias[2], p.bin_centre, n, n_tiles, prompt_len, model_id,
+          kv_bytes_per_token, n_models, pred_len, kv_bytes);
+    };
+    if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64>);
+    else args(mlp3_bf16_kernel<256, 1024, 1024, 64>);
   } else {
     return MAESTRO_ERR_UNSUPPORTED;
   }
