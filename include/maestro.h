@@ -53,6 +53,13 @@ typedef enum maestro_status {
   MAESTRO_ERR_LAUNCH = 4         /* the HIP runtime rejected a launch */
 } maestro_status;
 
+typedef enum maestro_route_algo {
+  MAESTRO_ROUTE_AUTO = 0,        /* SORTED when it applies and pays off, else SCAN */
+  MAESTRO_ROUTE_SCAN = 1,        /* score every (stage, node) pair */
+  MAESTRO_ROUTE_SORTED = 2       /* per-model node lists by ready time, early-exit walk;
+                                    n_nodes <= 8192; needs maestro_route_workspace() bytes */
+} maestro_route_algo;
+
 typedef enum maestro_dtype {
   MAESTRO_F32 = 0,               /* features, weights and hidden layers in float32 */
   MAESTRO_BF16 = 1               /* bfloat16 storage, float32 accumulation */
@@ -109,12 +116,23 @@ MAESTRO_API maestro_status maestro_predict(const maestro_predictor* p, int64_t n
  *   resident_mask       [n_nodes] uint64: bit m set <=> model m is warm on the node
  *   rho >= 0            safety margin;  1 <= k <= 16 route width
  *   node_idx  (out)     [n][k] int32;  score (out) [n][k] float32
- * Scores must be finite (finite inputs whose sums do not overflow float32). */
+ * Scores must be finite (finite inputs whose sums do not overflow float32).
+ * Both algorithms return identical results. Workspace: maestro_route_workspace() bytes. */
 MAESTRO_API maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
                              const double* kv_bytes, const float* decode_s_per_token,
                              int32_t n_models, int32_t n_nodes, const double* free_bytes,
                              const float* queue_s, const float* cold_s,
                              const uint64_t* resident_mask, double rho, int32_t k,
+                             int32_t* node_idx, float* score,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* maestro_route with an explicit algorithm (maestro_route_algo); SORTED with n_nodes > 8192
+ * returns MAESTRO_ERR_UNSUPPORTED. */
+MAESTRO_API maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* cold_s,
+                             const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
                              int32_t* node_idx, float* score,
                              void* workspace, size_t workspace_bytes, void* stream);
 

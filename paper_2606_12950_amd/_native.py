@@ -21,8 +21,11 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
            4: "kernel launch failed"}
 
 # Every function declared in include/maestro.h.
-EXPORTS = ("maestro_predict", "maestro_route", "maestro_prioritize", "maestro_predict_workspace",
-           "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
+EXPORTS = ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize",
+           "maestro_predict_workspace", "maestro_route_workspace", "maestro_prioritize_workspace",
+           "maestro_status_string")
+
+ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
 
 
 class MaestroError(RuntimeError):
@@ -53,8 +56,9 @@ def load():
     P, i32, i64, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
     lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
+    lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
-    for f in ("maestro_predict", "maestro_route", "maestro_prioritize"):
+    for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize"):
         getattr(lib, f).restype = ctypes.c_int
     lib.maestro_predict_workspace.argtypes = [ctypes.POINTER(Predictor), i64]
     lib.maestro_route_workspace.argtypes = [i64, i32, i32, i32]
@@ -151,9 +155,9 @@ def predict(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[t
 def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,
           decode_s_per_token: torch.Tensor, free_bytes: torch.Tensor, queue_s: torch.Tensor,
           cold_s: torch.Tensor, resident_mask: torch.Tensor, k: int = 1, rho: float = 0.0,
-          out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, workspace: Optional[torch.Tensor] = None,
-          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """maestro_route: returns (node_idx int32 [N][k], score float32 [N][k]).
+          algo: int = ROUTE_AUTO, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+          workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_route_ex: returns (node_idx int32 [N][k], score float32 [N][k]).
 
     ``resident_mask`` is int64 on the torch side (same bits as the C-ABI's uint64)."""
     lib = load()
@@ -177,18 +181,22 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
     idx, sc = out
     _dev(idx, "node_idx", torch.int32)
     _dev(sc, "score", torch.float32)
-    ws_bytes = lib.maestro_route_workspace(n, decode_s_per_token.shape[0], M, k)
+    ws_bytes = route_workspace_bytes(n, decode_s_per_token.shape[0], M, k)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=model_id.device)
-    st = lib.maestro_route(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes),
-                           _ptr(decode_s_per_token), decode_s_per_token.shape[0], M,
-                           _ptr(free_bytes), _ptr(queue_s), _ptr(cold_s), _ptr(resident_mask),
-                           float(rho), int(k), _ptr(idx), _ptr(sc),
-                           _ptr(workspace) if ws_bytes else None,
-                           workspace.numel() if (ws_bytes and workspace is not None) else 0,
-                           _stream(stream))
-    _check("maestro_route", st)
+    st = lib.maestro_route_ex(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes),
+                              _ptr(decode_s_per_token), decode_s_per_token.shape[0], M,
+                              _ptr(free_bytes), _ptr(queue_s), _ptr(cold_s), _ptr(resident_mask),
+                              float(rho), int(k), int(algo), _ptr(idx), _ptr(sc),
+                              _ptr(workspace) if workspace is not None else None,
+                              workspace.numel() if workspace is not None else 0,
+                              _stream(stream))
+    _check("maestro_route_ex", st)
     return idx, sc
+
+
+def route_workspace_bytes(n: int, n_models: int, n_nodes: int, k: int) -> int:
+    return int(load().maestro_route_workspace(n, n_models, n_nodes, k))
 
 
 def prioritize_workspace_bytes(n_workflows: int, n_stages: int) -> int:

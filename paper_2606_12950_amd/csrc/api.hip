@@ -63,14 +63,16 @@ maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void
                                  pred_len, kv_bytes, as_stream(stream));
 }
 
-maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
-                             const double* kv_bytes, const float* decode_s_per_token,
-                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
-                             const float* queue_s, const float* cold_s,
-                             const uint64_t* resident_mask, double rho, int32_t k,
-                             int32_t* node_idx, float* score, void* workspace,
-                             size_t workspace_bytes, void* stream) {
+maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float* pred_len,
+                                const double* kv_bytes, const float* decode_s_per_token,
+                                int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                                const float* queue_s, const float* cold_s,
+                                const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
+                                int32_t* node_idx, float* score, void* workspace,
+                                size_t workspace_bytes, void* stream) {
   if (n < 0 || n_models < 1 || n_models > 64 || n_nodes < 1 || k < 1 || k > 16)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (algo != MAESTRO_ROUTE_AUTO && algo != MAESTRO_ROUTE_SCAN && algo != MAESTRO_ROUTE_SORTED)
     return MAESTRO_ERR_INVALID_ARG;
   if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
   if (!decode_s_per_token || !free_bytes || !queue_s || !cold_s || !resident_mask)
@@ -86,10 +88,23 @@ maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pr
   }
   if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
   const size_t need = maestro::route_workspace_bytes(n, n_models, n_nodes, k);
-  if (workspace_bytes < need || (need > 0 && !workspace)) return MAESTRO_ERR_WORKSPACE;
+  if (algo != MAESTRO_ROUTE_SCAN && (workspace_bytes < need || (need > 0 && !aligned(workspace, 16))))
+    return MAESTRO_ERR_WORKSPACE;
   return maestro::launch_route(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models,
-                               n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k,
+                               n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k, algo,
                                node_idx, score, workspace, workspace_bytes, as_stream(stream));
+}
+
+maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* cold_s,
+                             const uint64_t* resident_mask, double rho, int32_t k,
+                             int32_t* node_idx, float* score, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return maestro_route_ex(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes,
+                          free_bytes, queue_s, cold_s, resident_mask, rho, k, MAESTRO_ROUTE_AUTO,
+                          node_idx, score, workspace, workspace_bytes, stream);
 }
 
 maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,

@@ -21,7 +21,7 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
                             const double* kv_bytes, const float* decode_s_per_token,
                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
                             const float* queue_s, const float* cold_s,
-                            const uint64_t* resident_mask, double rho, int32_t k,
+                            const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
                             int32_t* node_idx, float* score, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
 size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);

@@ -7,10 +7,11 @@
 //     slack = deadline - now - remaining, clamped to int32. Integer sums are exact, so the
 //     result does not depend on the summation order.
 //  2. stable LSD radix sort of the (slack, workflow) pairs, 4 passes of 8-bit digits over the
-//     order-preserving unsigned image of the key. Each pass: per-tile digit counts, one
-//     exclusive scan over the digit-major count table (global offset of every (digit, tile)),
-//     and a scatter in which each wavefront ranks its items digit by digit with ballots
-//     (wave multisplit) in input order, so equal digits keep their relative order.
+//     order-preserving unsigned image of the key. Each pass: per-tile digit counts, the
+//     exclusive scan of the digit-major count table (global offset of every (digit, tile);
+//     done inside the scatter blocks when there are few tiles), and a scatter in which each
+//     wavefront ranks its items digit by digit with ballots (wave multisplit) in input order,
+//     so equal digits keep their relative order.
 //     The key array is padded to whole tiles with all-ones keys, which always sort last and
 //     never reach the caller's output.
 #include "internal.h"
@@ -125,6 +126,10 @@ __global__ __launch_bounds__(1024) void radix_scan_kernel(uint32_t* __restrict__
 // Stable scatter of one tile by the digit at `shift`. Items of the tile are taken in input
 // order: wavefront w owns positions [w*1024, (w+1)*1024), step i covers 64 consecutive ones.
 // out_keys may be null (last pass); positions >= out_limit are padding and are dropped.
+// With kFusedScan the tile derives its digit offsets from the raw count table itself
+// (digit totals over all tiles, exclusive-scanned, plus the counts of the earlier tiles);
+// otherwise `offsets` holds the scanned table.
+template <bool kFusedScan>
 __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, int shift, int n_tiles,
     const uint32_t* __restrict__ offsets, uint32_t* __restrict__ out_keys,
@@ -135,7 +140,29 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
   const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) wcount[w][tid] = 0;
-  base[tid] = offsets[(int64_t)tid * n_tiles + tile];
+  if (kFusedScan) {
+    // thread d: total of digit d over all tiles, and over the tiles before this one
+    const uint32_t* row = offsets + (int64_t)tid * n_tiles;
+    uint32_t before = 0, total = 0;
+    for (int t = 0; t < n_tiles; ++t) {
+      const uint32_t c = row[t];
+      before += (t < tile) ? c : 0u;
+      total += c;
+    }
+    base[tid] = total;
+    __syncthreads();
+    for (int off = 1; off < kBuckets; off <<= 1) {   // inclusive scan of the digit totals
+      const uint32_t v = tid >= off ? base[tid - off] : 0u;
+      __syncthreads();
+      base[tid] += v;
+      __syncthreads();
+    }
+    const uint32_t excl = base[tid] - total;
+    __syncthreads();
+    base[tid] = excl + before;
+  } else {
+    base[tid] = offsets[(int64_t)tid * n_tiles + tile];
+  }
   __syncthreads();
 
   const int64_t t0 = (int64_t)tile * kTile + wave * (kTile / kWaves);
@@ -181,6 +208,9 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
   }
 }
+
+// up to this many tiles each scatter block scans the count table itself
+constexpr int kFusedScanMaxTiles = 64;
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
@@ -231,10 +261,17 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
     const int shift = pass * kRadixBits;
     const bool last = pass + 1 == kPasses;
     radix_count_kernel<<<dim3(nt), dim3(kThreads), 0, stream>>>(keys[src], shift, nt, counts);
-    radix_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(counts, (int64_t)kBuckets * nt);
-    radix_scatter_kernel<<<dim3(nt), dim3(kThreads), 0, stream>>>(
-        keys[src], vals[src], shift, nt, counts, last ? nullptr : keys[dst],
-        last ? reinterpret_cast<uint32_t*>(order) : vals[dst], last ? (int64_t)n_workflows : L.padded);
+    uint32_t* out_k = last ? nullptr : keys[dst];
+    uint32_t* out_v = last ? reinterpret_cast<uint32_t*>(order) : vals[dst];
+    const int64_t limit = last ? (int64_t)n_workflows : L.padded;
+    if (nt <= kFusedScanMaxTiles) {
+      radix_scatter_kernel<true><<<dim3(nt), dim3(kThreads), 0, stream>>>(
+          keys[src], vals[src], shift, nt, counts, out_k, out_v, limit);
+    } else {
+      radix_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(counts, (int64_t)kBuckets * nt);
+      radix_scatter_kernel<false><<<dim3(nt), dim3(kThreads), 0, stream>>>(
+          keys[src], vals[src], shift, nt, counts, out_k, out_v, limit);
+    }
   }
   return launch_status();
 }

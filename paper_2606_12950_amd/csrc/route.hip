@@ -8,6 +8,15 @@
 // (lexicographic on (score, node)), and the first lane writes the stage's k results.
 // G grows when the batch has too few stages to fill the chip.
 //
+// A second, exact algorithm avoids the full score matrix. For a fixed model, a node's score
+// is fl32(ready + t_exec) with t_exec common to every node, and round-to-nearest addition is
+// monotone, so ordering a model's nodes by (ready time, index) orders their scores (equal
+// scores may come from different ready times, hence the lexicographic insertion below). One
+// workgroup per model sorts the nodes by that key in LDS (bitonic sort); then each stage walks
+// its model's list, skipping nodes that cannot admit its KV demand, and stops at the first
+// node whose score exceeds its current k-th best. The result is identical to the scan; the
+// walk is short unless many nodes are infeasible, and never longer than the node count.
+//
 // Arithmetic is the same expression, in the same order and precision, as the definition:
 // score = fl32(fl32(T_q + T_act) + fl32(L * t_dec)), with T_act in {0, cold}. The library is
 // compiled with -ffp-contract=off and the products/sums below use explicit round-to-nearest
@@ -165,17 +174,147 @@ int choose_g_log2(int64_t n, int32_t n_nodes) {
   return gl;
 }
 
+// ---------------------------------------------------------------------------------------------
+// sorted per-model node lists + early-exit walk
+// ---------------------------------------------------------------------------------------------
+
+constexpr int kSortMax = 8192;            // nodes sortable in one workgroup's LDS (64 KB of keys)
+constexpr int kSortThreads = 1024;
+
+struct NodeEntry {                        // 16 bytes: one node in a model's ready-time order
+  float ready;                            // fl32(T_q + T_act) for this model
+  int32_t node;
+  double free;                            // KV admission headroom
+};
+
+// order-preserving map of float bits to unsigned (a < b <=> map(a) < map(b), -0 < +0)
+__device__ __forceinline__ uint32_t float_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+__global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
+    int32_t n_nodes, int32_t padded, const float* __restrict__ queue_s, const float* __restrict__ cold_s,
+    const uint64_t* __restrict__ resident_mask, const double* __restrict__ free_bytes,
+    NodeEntry* __restrict__ lists) {
+  __shared__ uint64_t key[kSortMax];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  for (int i = tid; i < padded; i += kSortThreads) {
+    if (i < n_nodes) {
+      const bool res = (resident_mask[i] >> m) & 1u;
+      const float q = queue_s[i];
+      const float ready = res ? __fadd_rn(q, 0.0f) : __fadd_rn(q, cold_s[i]);
+      key[i] = ((uint64_t)float_key(ready) << 32) | (uint32_t)i;
+    } else {
+      key[i] = ~0ull;                     // padding sorts last
+    }
+  }
+  __syncthreads();
+  // bitonic sort, ascending
+  for (int size = 2; size <= padded; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < padded / 2; i += kSortThreads) {
+        const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const uint64_t a = key[lo], b = key[hi];
+        if ((a > b) == up) { key[lo] = b; key[hi] = a; }
+      }
+      __syncthreads();
+    }
+  }
+  NodeEntry* out = lists + (size_t)m * n_nodes;
+  for (int j = tid; j < n_nodes; j += kSortThreads) {
+    const uint64_t k = key[j];
+    NodeEntry e;
+    e.ready = key_float((uint32_t)(k >> 32));
+    e.node = (int32_t)(uint32_t)k;
+    e.free = free_bytes[e.node];
+    out[j] = e;
+  }
+}
+
+template <int KT>
+__global__ __launch_bounds__(kThreads) void walk_route_kernel(
+    int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
+    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_nodes,
+    const NodeEntry* __restrict__ lists, double rho, int32_t k, int32_t* __restrict__ node_idx,
+    float* __restrict__ score) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const int32_t m = model_id[i];
+  const double need = (rho == 0.0) ? kv_bytes[i] : __dmul_rn(kv_bytes[i], 1.0 + rho);
+  const float exec_s = __fmul_rn(pred_len[i], decode_s_per_token[m]);
+  const NodeEntry* list = lists + (size_t)m * n_nodes;
+  TopK<KT> best;
+  best.init();
+  for (int32_t j = 0; j < n_nodes; ++j) {
+    const NodeEntry e = list[j];
+    if (!(need <= e.free)) continue;                       // infeasible: skip, keep walking
+    const float sc = __fadd_rn(e.ready, exec_s);
+    if (best.n[KT - 1] != kNoNode && sc > best.s[KT - 1]) break;   // no later node can enter
+    best.push_lex(sc, e.node);
+  }
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    if (t < k) {
+      const bool some = best.n[t] != kNoNode;
+      node_idx[i * k + t] = some ? best.n[t] : -1;
+      score[i * k + t] = some ? best.s[t] : INFINITY;
+    }
+  }
+}
+
+size_t sorted_lists_bytes(int32_t n_models, int32_t n_nodes) {
+  return (size_t)n_models * (size_t)n_nodes * sizeof(NodeEntry);
+}
+
+bool sorted_possible(int32_t n_nodes) { return n_nodes <= kSortMax; }
+
+// the scan wins when there are too few stages to amortise the per-model sorts
+bool prefer_sorted(int64_t n, int32_t n_models, int32_t n_nodes) {
+  return sorted_possible(n_nodes) && n >= 4 * (int64_t)n_models;
+}
+
 }  // namespace
 
-size_t route_workspace_bytes(int64_t, int32_t, int32_t, int32_t) { return 0; }
+size_t route_workspace_bytes(int64_t, int32_t n_models, int32_t n_nodes, int32_t) {
+  return sorted_possible(n_nodes) ? sorted_lists_bytes(n_models, n_nodes) : 0;
+}
 
 maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pred_len,
                             const double* kv_bytes, const float* decode_s_per_token,
                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
                             const float* queue_s, const float* cold_s,
-                            const uint64_t* resident_mask, double rho, int32_t k,
-                            int32_t* node_idx, float* score, void*, size_t, hipStream_t stream) {
+                            const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
+                            int32_t* node_idx, float* score, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
+  bool sorted;
+  if (algo == MAESTRO_ROUTE_SCAN) sorted = false;
+  else if (algo == MAESTRO_ROUTE_SORTED) sorted = true;
+  else sorted = prefer_sorted(n, n_models, n_nodes);
+  if (sorted) {
+    if (!sorted_possible(n_nodes)) return MAESTRO_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < sorted_lists_bytes(n_models, n_nodes)) return MAESTRO_ERR_WORKSPACE;
+    NodeEntry* lists = static_cast<NodeEntry*>(workspace);
+    int padded = 1;
+    while (padded < n_nodes) padded <<= 1;
+    sort_nodes_kernel<<<dim3(n_models), dim3(kSortThreads), 0, stream>>>(
+        n_nodes, padded, queue_s, cold_s, resident_mask, free_bytes, lists);
+    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
+#define MAESTRO_WALK_KT(KT)                                                                          walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,                                                                  decode_s_per_token, n_nodes, lists, rho,                                                             k, node_idx, score)
+    if (k == 1) MAESTRO_WALK_KT(1);
+    else if (k == 2) MAESTRO_WALK_KT(2);
+    else if (k == 3) MAESTRO_WALK_KT(3);
+    else if (k == 4) MAESTRO_WALK_KT(4);
+    else if (k <= 8) MAESTRO_WALK_KT(8);
+    else MAESTRO_WALK_KT(16);
+#undef MAESTRO_WALK_KT
+    return launch_status();
+  }
   const int gl = choose_g_log2(n, n_nodes);
   const int64_t stages_per_block = kThreads >> gl;
   const dim3 grid((unsigned)((n + stages_per_block - 1) / stages_per_block));

@@ -49,6 +49,7 @@ class StepOutputs:
     slack_key: Optional[torch.Tensor]
     order: Optional[torch.Tensor]
     prio_workspace: Optional[torch.Tensor]
+    route_workspace: Optional[torch.Tensor]
 
 
 def _t(a: np.ndarray, device) -> torch.Tensor:
@@ -82,6 +83,8 @@ def allocate_outputs(b: DeviceBatch) -> StepOutputs:
     ws = None
     if chained:
         ws = torch.empty(max(_native.prioritize_workspace_bytes(W, n), 256), dtype=torch.uint8, device=dev)
+    rws_bytes = _native.route_workspace_bytes(n, b.decode_s_per_token.shape[0], b.free_bytes.shape[0], b.k)
+    rws = torch.empty(rws_bytes, dtype=torch.uint8, device=dev) if rws_bytes else None
     return StepOutputs(
         pred_len=torch.empty(n, dtype=torch.float32, device=dev),
         kv_bytes=torch.empty(n, dtype=torch.float64, device=dev),
@@ -90,7 +93,7 @@ def allocate_outputs(b: DeviceBatch) -> StepOutputs:
         remaining_us=torch.empty(n, dtype=torch.int64, device=dev) if chained else None,
         slack_key=torch.empty(W, dtype=torch.int32, device=dev) if chained else None,
         order=torch.empty(W, dtype=torch.int32, device=dev) if chained else None,
-        prio_workspace=ws)
+        prio_workspace=ws, route_workspace=rws)
 
 
 def run_predict(b: DeviceBatch, o: StepOutputs, stream=None):
@@ -98,9 +101,10 @@ def run_predict(b: DeviceBatch, o: StepOutputs, stream=None):
                     b.kv_bytes_per_token, out=(o.pred_len, o.kv_bytes), stream=stream)
 
 
-def run_route(b: DeviceBatch, o: StepOutputs, stream=None):
+def run_route(b: DeviceBatch, o: StepOutputs, stream=None, algo: int = _native.ROUTE_AUTO):
     _native.route(b.model_id, o.pred_len, o.kv_bytes, b.decode_s_per_token, b.free_bytes, b.queue_s,
-                  b.cold_s, b.resident_mask, k=b.k, rho=b.rho, out=(o.node_idx, o.score), stream=stream)
+                  b.cold_s, b.resident_mask, k=b.k, rho=b.rho, algo=algo, out=(o.node_idx, o.score),
+                  workspace=o.route_workspace, stream=stream)
 
 
 def run_prioritize(b: DeviceBatch, o: StepOutputs, stream=None):

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 7
+    assert len(names) == 8
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -83,6 +83,15 @@ def test_route_validation(lib):
     def call(n=10, n_models=8, n_nodes=16, k=1, rho=0.0, model=FAKE, free=FAKE):
         return lib.maestro_route(n, model, FAKE, FAKE, FAKE, n_models, n_nodes, free, FAKE, FAKE, FAKE,
                                  rho, k, FAKE, FAKE, None, 0, None)
+    def call_ex(algo, n_nodes=16, ws=None, ws_bytes=0):
+        return lib.maestro_route_ex(10, FAKE, FAKE, FAKE, FAKE, 8, n_nodes, FAKE, FAKE, FAKE, FAKE, 0.0, 1,
+                                    algo, FAKE, FAKE, ws, ws_bytes, None)
+    assert call_ex(3) == INVALID                                              # unknown algorithm
+    assert call_ex(-1) == INVALID
+    assert call_ex(2) == WORKSPACE                                            # sorted lists need space
+    # sorted lists: one 16-byte entry per (model, node); none beyond 8192 nodes
+    assert lib.maestro_route_workspace(10, 8, 16, 1) == 8 * 16 * 16
+    assert lib.maestro_route_workspace(10, 8, 8193, 1) == 0
     assert call(n=-1) == INVALID
     assert call(n_models=0) == INVALID
     assert call(n_models=65) == INVALID

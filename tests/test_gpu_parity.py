@@ -135,8 +135,11 @@ def test_predict_rejects_unsupported_and_bad_args():
 # route (bit-exact given identical inputs)
 # ----------------------------------------------------------------------------------------------
 
+ALGOS = {"scan": M._native.ROUTE_SCAN, "sorted": M._native.ROUTE_SORTED}
+
+
 def gpu_route(w, pred, kv, free=None, queue=None, cold=None, mask=None, dec=None, k=None, rho=None,
-              model=None):
+              model=None, algo=0):
     t = lambda a: pipeline._t(a, "cuda")
     model = w.model_id if model is None else model
     args = dict(free=w.free_bytes if free is None else free, queue=w.queue_s if queue is None else queue,
@@ -145,7 +148,7 @@ def gpu_route(w, pred, kv, free=None, queue=None, cold=None, mask=None, dec=None
     k = w.spec.k if k is None else k
     rho = w.spec.rho if rho is None else rho
     idx, sc = M.route(t(model), t(pred), t(kv), t(args["dec"]), t(args["free"]), t(args["queue"]),
-                      t(args["cold"]), t(args["mask"]), k=k, rho=rho)
+                      t(args["cold"]), t(args["mask"]), k=k, rho=rho, algo=algo)
     torch.cuda.synchronize()
     ref = oracle.route(model, pred, kv, args["dec"], args["free"], args["queue"], args["cold"],
                        args["mask"], k=k, rho=rho)
@@ -160,21 +163,23 @@ def assert_route_equal(got, ref):
                           f"oracle {ri[bad[:3]]} {rs[bad[:3]]}"
 
 
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
 @pytest.mark.parametrize("name", ["c0", "c1", "c2", "c3"])
-def test_route_matches_oracle_full(name):
+def test_route_matches_oracle_full(name, algo):
     w = wl(name)
     pred, kv, _, _ = gpu_predict(w)
-    got, ref = gpu_route(w, pred, kv)
+    got, ref = gpu_route(w, pred, kv, algo=ALGOS[algo])
     assert_route_equal(got, ref)
     infeasible = float(np.mean(ref[0][:, 0] < 0))
     print(f"{name}: {w.n} stages x {w.spec.n_nodes} nodes, routes identical; unroutable {infeasible:.4%}")
 
 
-def test_route_c4_top4_sampled_stages():
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
+def test_route_c4_top4_sampled_stages(algo):
     # full c4 on the GPU (4,194,304 stages x 4,096 nodes, top-4); oracle on a stage sample
     w = wl("c4")
     pred, kv, b, o = gpu_predict(w)
-    pipeline.run_route(b, o)
+    pipeline.run_route(b, o, algo=ALGOS[algo])
     torch.cuda.synchronize()
     gi, gs = _np(o.node_idx), _np(o.score)
     rows = np.sort(np.random.default_rng(7).choice(w.n, 20000, replace=False))
@@ -184,19 +189,21 @@ def test_route_c4_top4_sampled_stages():
     assert_route_equal((gi[rows], gs[rows]), ref)
 
 
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
 @pytest.mark.parametrize("k", [1, 3, 4, 16])
-@pytest.mark.parametrize("n,M_", [(1, 1), (7, 3), (300, 64), (2500, 1500), (40000, 37)])
-def test_route_shapes_and_widths(n, M_, k):
+@pytest.mark.parametrize("n,M_", [(1, 1), (7, 3), (300, 64), (2500, 1500), (40000, 37), (3000, 8192)])
+def test_route_shapes_and_widths(n, M_, k, algo):
     # ragged stage tiles, node chunks that do not divide, several lanes per stage, k > #nodes
     w = wl("c1", n_stages=n, n_nodes=M_, with_x=False)
     rng = np.random.default_rng(n * 31 + M_)
     pred = rng.uniform(32, 4064, n).astype(np.float32)
     kv = (w.prompt_len + pred.astype(np.float64)) * w.kv_bytes_per_token[w.model_id].astype(np.float64)
-    got, ref = gpu_route(w, pred, kv, free=w.free_bytes / 60.0, k=k)
+    got, ref = gpu_route(w, pred, kv, free=w.free_bytes / 60.0, k=k, algo=ALGOS[algo])
     assert_route_equal(got, ref)
 
 
-def test_route_ties_and_boundaries():
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
+def test_route_ties_and_boundaries(algo):
     # coarse value grids: many exactly equal scores and free == need boundaries
     rng = np.random.default_rng(5)
     n, M_, K = 5000, 700, 64
@@ -212,23 +219,24 @@ def test_route_ties_and_boundaries():
     dec = rng.choice(np.array([0.015625, 0.03125], np.float32), K)
     for k, rho in [(1, 0.0), (4, 0.0), (5, 0.25)]:
         got, ref = gpu_route(w, pred, kv, free=free, queue=q, cold=cold, mask=mask, dec=dec, k=k,
-                             rho=rho, model=model)
+                             rho=rho, model=model, algo=ALGOS[algo])
         assert_route_equal(got, ref)
         if k == 1:
             assert np.any(ref[0][:, 0] < 0) and np.any(ref[0][:, 0] >= 0)
 
 
-def test_route_all_infeasible_and_equal_scores():
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
+def test_route_all_infeasible_and_equal_scores(algo):
     w = wl("c0", n_stages=100, with_x=False)
     pred = np.full(100, 500.0, np.float32)
     kv = np.full(100, 1e12)   # more than any node has
-    got, ref = gpu_route(w, pred, kv, k=4)
+    got, ref = gpu_route(w, pred, kv, k=4, algo=ALGOS[algo])
     assert np.all(got[0] == -1) and np.all(np.isinf(got[1]))
     assert_route_equal(got, ref)
     # identical nodes: lowest feasible index first
     M_ = w.spec.n_nodes
     got, ref = gpu_route(w, pred, np.full(100, 1e9), free=np.full(M_, 1e9), queue=np.ones(M_, np.float32),
-                         cold=np.ones(M_, np.float32), mask=np.zeros(M_, np.uint64), k=4)
+                         cold=np.ones(M_, np.float32), mask=np.zeros(M_, np.uint64), k=4, algo=ALGOS[algo])
     assert np.all(got[0] == np.arange(4)[None, :])
     assert_route_equal(got, ref)
 
@@ -305,6 +313,17 @@ def test_prioritize_adversarial_keys():
         assert_prio_equal(got, ref)
         if name == "all_equal":
             assert np.array_equal(got[2], np.arange(W_))
+
+
+def test_route_sorted_rejects_too_many_nodes():
+    w = wl("c1", n_stages=10, n_nodes=8193, with_x=False)
+    pred = np.full(10, 100.0, np.float32)
+    kv = np.full(10, 1e9)
+    with pytest.raises(M.MaestroError) as e:
+        gpu_route(w, pred, kv, algo=ALGOS["sorted"])
+    assert e.value.status == 2
+    got, ref = gpu_route(w, pred, kv)            # auto falls back to the scan
+    assert_route_equal(got, ref)
 
 
 def test_prioritize_long_chain_and_empty():
