@@ -1,6 +1,7 @@
 """Throughput of the batched predict -> route -> prioritize step on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
+python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for counter calibration)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -11,6 +12,7 @@ batch: 131,072 workflows of 3..8 stages (719,712 stages), 512 nodes, 16 models, 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -25,6 +27,38 @@ METRIC = "stages predicted+routed/sec on 1 MI355X; % of HBM/MFMA roofline"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "predict_traffic.json")
+PREDICT_SOURCE = os.path.join(ROOT, "paper_2606_12950_amd", "csrc", "predict.hip")
+
+
+def predict_source_hash() -> str:
+    return hashlib.sha256(open(PREDICT_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per predictor launch from the committed counter runs, if they were taken on
+    the current kernel source for this workload; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("predict_source_sha256_16") != predict_source_hash() or rec.get("workload") != workload:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def calibrate_copy(mib: int, reps: int = 5):
+    import torch
+    src = torch.empty(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes": mib << 20, "reps": reps}), flush=True)
 
 
 def mlp_flop_per_stage(dims):
@@ -62,7 +96,12 @@ def main():
     ap.add_argument("--workload", default="c3", choices=["c0", "c1", "c2", "c3", "c4"])
     ap.add_argument("--cpu-sample-workflows", type=int, default=65536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     args = ap.parse_args()
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the batched scheduling step runs on a single "
@@ -135,7 +174,7 @@ def main():
         "roofline": {
             "bound": "mfma", "kernel": "predict (fused MLP + length epilogue)",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "frac": round(achieved / peak, 4), "traffic": measured_traffic(spec.name),
             "flop_per_launch": flop, "avg_ms": round(ms_predict, 4),
         },
         "step_ms": {"predict": round(ms_predict, 4), "route": round(ms_route, 4),
