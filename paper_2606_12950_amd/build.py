@@ -31,11 +31,15 @@ FLAGS = [
     "-Wall", "-Wno-unused-function",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
+# per-source additions: the predictor converts its MFMA accumulators with vector ALU
+# instructions, which read only architectural VGPRs; keeping MFMA results there avoids a copy
+# out of the accumulation registers for every converted value
+EXTRA = {"predict.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str, outdir: str, verbose: bool) -> str:
     obj = os.path.join(outdir, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -149,64 +149,68 @@ __device__ __forceinline__ void mfma_chain(f32x16& acc, const unsigned char* pa,
   }
 }
 
-// relu(acc[8*half + j] + bias[j]) for j = 0..7, rounded to bfloat16 (nearest even) and packed
-// as the 8 K-slots of a B operand.
-__device__ __forceinline__ bf16x8 bias_relu_bf16(const f32x16& acc, int half, const float* __restrict__ bias) {
-  const float4 b0 = *reinterpret_cast<const float4*>(bias);
-  const float4 b1 = *reinterpret_cast<const float4*>(bias + 4);
-  const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+// Accumulator of a 32-neuron block initialised with the biases of the neurons lane-half h holds
+// (registers 0-7: neurons 8h .. 8h+7, registers 8-15: neurons 16+8h .. 16+8h+7).
+__device__ __forceinline__ f32x16 bias_acc(const float* __restrict__ b32, int h) {
+  const float4 q0 = *reinterpret_cast<const float4*>(b32 + 8 * h);
+  const float4 q1 = *reinterpret_cast<const float4*>(b32 + 8 * h + 4);
+  const float4 q2 = *reinterpret_cast<const float4*>(b32 + 16 + 8 * h);
+  const float4 q3 = *reinterpret_cast<const float4*>(b32 + 16 + 8 * h + 4);
+  return f32x16{q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w,
+                q2.x, q2.y, q2.z, q2.w, q3.x, q3.y, q3.z, q3.w};
+}
+
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+// acc[8*half + j] (biases included), j = 0..7, rounded to bfloat16 (nearest even) and packed as
+// the 8 K-slots of a B operand, then rectified on the packed values: a bfloat16 is below zero
+// exactly when its bit pattern is a negative int16, so a packed int16 max with 0 is the ReLU
+// (rounding to nearest and ReLU commute; -0 becomes +0).
+__device__ __forceinline__ bf16x8 relu_bf16(const f32x16& acc, int half) {
   uint32_t w[4];
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
-    f32x2 f = {fmaxf(acc[8 * half + 2 * p] + bb[2 * p], 0.0f),
-               fmaxf(acc[8 * half + 2 * p + 1] + bb[2 * p + 1], 0.0f)};
-    w[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+    const f32x2 f = {acc[8 * half + 2 * p], acc[8 * half + 2 * p + 1]};
+    const s16x2 v = __builtin_bit_cast(s16x2, __builtin_convertvector(f, bf16x2));
+    w[p] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, s16x2{0, 0}));
   }
   return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
 }
 
-// Pipelined "relu(acc + bias) -> bfloat16" of one finished 32-neuron block, in slices:
-// step 0 reads the 16 biases of the lane's neurons, steps 1..8 convert one pair of values
-// each; the result is the B-operand pair out[0] (neurons 16*0 + 8h + 0..7) and out[1].
-struct BlockEpilogue {
-  float bias[16];
-  uint32_t w[8];
-  __device__ __forceinline__ void step(int k, const f32x16& acc, const float* __restrict__ b32, int h) {
-    if (k == 0) {
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const float4 b0 = *reinterpret_cast<const float4*>(b32 + half * 16 + h * 8);
-        const float4 b1 = *reinterpret_cast<const float4*>(b32 + half * 16 + h * 8 + 4);
-        bias[8 * half + 0] = b0.x; bias[8 * half + 1] = b0.y; bias[8 * half + 2] = b0.z;
-        bias[8 * half + 3] = b0.w; bias[8 * half + 4] = b1.x; bias[8 * half + 5] = b1.y;
-        bias[8 * half + 6] = b1.z; bias[8 * half + 7] = b1.w;
-      }
-    } else if (k <= 8) {
-      const int p = k - 1;
-      f32x2 f = {fmaxf(acc[2 * p] + bias[2 * p], 0.0f), fmaxf(acc[2 * p + 1] + bias[2 * p + 1], 0.0f)};
-      w[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
-    }
-  }
-  __device__ __forceinline__ bf16x8 out(int half) const {
-    return __builtin_bit_cast(bf16x8, make_uint4(w[4 * half], w[4 * half + 1], w[4 * half + 2], w[4 * half + 3]));
-  }
-};
-
 constexpr int kBufs = 4;                 // LDS chunk buffers (prefetch distance kBufs - 1)
 constexpr int kDmaPerChunk = 8;          // direct loads per wavefront per chunk (at least)
 
-// Direct global->LDS loads: lane l's 16 (or 4) bytes at gbase + voff land at LDS byte address
-// lds_dst + 16 l (or 4 l). Issued as inline assembly so that the compiler's automatic wait
-// insertion, which would conservatively drain every such load before any LDS read, does not
-// see them; the kernel waits for them itself (wait_chunk). gbase must be uniform.
+// Direct global->LDS loads through a raw buffer resource: lane l's 16 (or 4) bytes at byte offset
+// voff + soff of the buffer land at LDS byte address lds_base + lds_off + 16 l (or 4 l); lanes
+// whose voff is at or past the buffer's size read zeros and touch no memory. Issued as inline
+// assembly so that the compiler's automatic wait insertion, which would conservatively drain
+// every such load before any LDS read, does not see them; the kernel waits for them itself
+// (wait_chunk). rsrc, soff and lds_base are wavefront-uniform; lds_off is a compile-time constant.
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) unsigned char lds_uchar;
-__device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, const unsigned char* lds_dst) {
-  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_uchar*)(lds_dst);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(gbase) : "m0");
+
+// Raw (unstrided) buffer resource over `bytes` bytes at `base` (gfx9 descriptor: 48-bit base,
+// stride 0, byte-granular range check, 32-bit data format).
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int32_t)((a >> 32) & 0xFFFF));
+  r[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
+  r[3] = 0x00020000;
+  return r;
 }
-__device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, const unsigned char* lds_dst) {
-  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_uchar*)(lds_dst);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(m0), "v"(voff), "s"(gbase) : "m0");
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_uchar*)(p);
+}
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t soff, uint32_t lds_base,
+                                      int lds_off) {
+  asm volatile("s_add_u32 m0, %0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
+               ::"s"(lds_base), "i"(lds_off), "v"(voff), "s"(rsrc), "s"(soff) : "m0", "scc");
+}
+__device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               ::"s"(lds_base), "v"(voff), "s"(rsrc) : "m0");
 }
 
 // Wait until at most N vector-memory operations of this wavefront are outstanding and all of
@@ -246,6 +250,8 @@ void mlp3_bf16_kernel(
   constexpr int W3OFF = 32 * ROW2;
   constexpr int CHUNK = cmax(cmax(64 * 512, 32 * PAIR), W3OFF + B * 64);
   static_assert(NC >= kBufs - 1, "prologue fetches whole chunks of the first tile");
+  static_assert(NX + NC1 + kBufs - 1 <= NC, "feature and layer-1 prefetches stay within the tile");
+  static_assert(NB2 * KP >= kBufs - 1, "the peeled layer-2 blocks cover every wrapping prefetch");
 
   __shared__ __attribute__((aligned(16))) unsigned char lds[kBufs * CHUNK];
   __shared__ __attribute__((aligned(16))) float s_b1[H1];
@@ -261,57 +267,68 @@ void mlp3_bf16_kernel(
   const int lane = tid & 63, h = lane >> 5, r32 = lane & 31;
   const int64_t first_tile = blockIdx.x, stride = gridDim.x;
 
-  // ---- fetch of chunk c of tile t into LDS buffer dst, one load instruction per call:
-  // q = 0 .. kDmaPerChunk-1 are always issued; q = kDmaPerChunk adds the tile's prompt
-  // lengths / model ids (feature chunk 0) or the W3 slice (last part of a layer-2 block)
+  // ---- chunk fetchers, each issuing at least kDmaPerChunk direct loads per wavefront
+  const i32x4 rs_w1 = buffer_rsrc(w1, (uint32_t)(H1 * D * 2));
+  const i32x4 rs_w2 = buffer_rsrc(w2, (uint32_t)(H2 * H1 * 2));
+  const i32x4 rs_w3 = buffer_rsrc(w3, (uint32_t)(B * H2 * 2));
   const uint32_t voff1 = (uint32_t)(((lane >> 5) * D + (((lane & 31) ^ ((lane >> 5) << 3)) * 8)) * 2);
   const uint32_t voff2 = (uint32_t)(lane * 16);
   const uint32_t voff3 = (uint32_t)(((lane >> 2) * H2 + (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
-  auto fetch_one = [&](int64_t t, int c, unsigned char* dst, int q) {
-    if (c < NX) {
-      // tile rows 64c + 2i + (lane / 32), i = wave + 4q, clamped to the last stage; a fetch
-      // past the last tile re-reads the last tile (never consumed)
-      const int64_t tt = t < n_tiles ? t : n_tiles - 1;
-      if (q < kDmaPerChunk) {
-        const int64_t row0 = tt * kRowsPerBlock + 64 * c;
-        const int i = wave + q * kWaves;
-        const int rho = 2 * i + (lane >> 5);                  // row within the chunk
-        const int64_t base = min(row0 + 2 * i, n - 1);
-        const int64_t rw = min(row0 + rho, n - 1);
-        const uint32_t unit = (uint32_t)((lane & 31) ^ (rho & 15));
-        dma16(x + base * D, (uint32_t)(rw - base) * (D * 2) + unit * 16, dst + i * 1024);
-      } else if (q == kDmaPerChunk && c == 0) {
-        // prompt lengths (waves 0, 1) and model ids (waves 2, 3) of the tile, 64 rows each
-        const int64_t r0 = tt * kRowsPerBlock + 64 * (wave & 1);
-        const int64_t base = min(r0, n - 1);
-        const int64_t rw = min(r0 + lane, n - 1);
-        const int32_t* src = (wave < 2) ? prompt_len : model_id;
-        const int parity = (int)(((t - first_tile) / stride) & 1);
-        dma4(src + base, (uint32_t)(rw - base) * 4,
-             reinterpret_cast<const unsigned char*>(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
-      }
-    } else if (c < NX + NC1) {
-      // rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units with bit 3 flipped)
-      if (q < kDmaPerChunk) {
-        const int j = c - NX, i = wave + q * kWaves;
-        dma16(w1 + (size_t)(64 * j + 2 * i) * D, voff1, dst + i * PAIR);
-      }
-    } else {
-      const int b = (c - NX - NC1) / KP, part = (c - NX - NC1) % KP;
-      if (q < kDmaPerChunk) {
-        const int r = wave + q * kWaves;
-        dma16(w2 + (size_t)(32 * b + r) * H1 + part * 512, voff2, dst + r * ROW2);
-      } else if (q == kDmaPerChunk && part == KP - 1) {
-        // W3 rows 16i .. 16i+15 (i = wave), columns 32b .. 32b+31: lane -> row 16i + lane/4,
-        // unit (lane % 4) rotated by (row / 4) % 4
-        static_assert(B / 16 == kWaves, "one W3 slice load per wavefront");
-        dma16(w3 + (size_t)(16 * wave) * H2 + 32 * b, voff3, dst + W3OFF + wave * 1024);
-      }
+  // feature load q of a chunk: tile row rho = 64j + 2i + (lane / 32), i = wave + 4q, 16-byte unit
+  // (lane % 32) ^ (rho % 16); rho % 16 depends on q only through q % 2
+  uint32_t voffx[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int rho = 2 * wave + h + 8 * p;
+    voffx[p] = (uint32_t)((2 * wave + h) * D * 2 + (((lane & 31) ^ (rho & 15)) << 4));
+  }
+  const uint32_t voffm = (uint32_t)((64 * (wave & 1) + lane) * 4);
+  // feature chunk j of tile t (rows of a partial tile past the last stage, and every row of a
+  // tile past the last, read as zeros and are never stored). Chunk 0 also brings the tile's
+  // prompt lengths (waves 0, 1) and model ids (waves 2, 3), 64 rows each.
+  auto fetch_x = [&](int64_t t, int j, const unsigned char* dst) {
+    const bool live = t < n_tiles;
+    const int64_t row0 = live ? t * kRowsPerBlock : 0;
+    const uint32_t rows = live ? (uint32_t)min<int64_t>(kRowsPerBlock, n - row0) : 0u;
+    const i32x4 rs = buffer_rsrc(x + row0 * D, rows * (D * 2));
+    const uint32_t base = lds_addr(dst) + wave * 1024;
+#pragma unroll
+    for (int q = 0; q < kDmaPerChunk; ++q)
+      dma16(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
+    if (j == 0) {
+      const int32_t* src = (wave < 2) ? prompt_len : model_id;
+      const int parity = (int)(((t - first_tile) / stride) & 1);
+      dma4(buffer_rsrc(src + row0, rows * 4), voffm, lds_addr(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
     }
   };
-  auto fetch = [&](int64_t t, int c, unsigned char* dst) {
+  // layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units with bit
+  // 3 flipped), i = wave + 4q
+  auto fetch_l1 = [&](int j, const unsigned char* dst) {
+    const uint32_t base = lds_addr(dst) + wave * PAIR;
+    const uint32_t s0 = (uint32_t)((64 * j + 2 * wave) * D * 2);
 #pragma unroll
-    for (int q = 0; q <= kDmaPerChunk; ++q) fetch_one(t, c, dst, q);
+    for (int q = 0; q < kDmaPerChunk; ++q)
+      dma16(rs_w1, voff1, s0 + (uint32_t)(8 * q * D * 2), base, q * kWaves * PAIR);
+  };
+  // layer-2 chunk (b, part): W2 rows 32b + r, r = wave + 4q; the last part also brings W3 rows
+  // 16i .. 16i+15 (i = wave), columns 32b .. 32b+31: lane -> row 16i + lane/4, unit (lane % 4)
+  // rotated by (row / 4) % 4
+  auto fetch_l2 = [&](int b, int part, const unsigned char* dst) {
+    const uint32_t base = lds_addr(dst) + wave * ROW2;
+    const uint32_t s0 = (uint32_t)((32 * b + wave) * H1 * 2 + part * 1024);
+#pragma unroll
+    for (int q = 0; q < kDmaPerChunk; ++q)
+      dma16(rs_w2, voff2, s0 + (uint32_t)(4 * q * H1 * 2), base, q * kWaves * ROW2);
+    if (part == KP - 1) {
+      static_assert(B / 16 == kWaves, "one W3 slice load per wavefront");
+      dma16(rs_w3, voff3, (uint32_t)(16 * wave * H2 * 2 + 64 * b), lds_addr(dst) + W3OFF + wave * 1024, 0);
+    }
+  };
+  // chunk c of tile t; c is a compile-time constant at every call site
+  auto fetch = [&](int64_t t, int c, const unsigned char* dst) {
+    if (c < NX) fetch_x(t, c, dst);
+    else if (c < NX + NC1) fetch_l1(c - NX, dst);
+    else fetch_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, dst);
   };
 
   // per-lane LDS offsets of the A operands
@@ -340,13 +357,7 @@ void mlp3_bf16_kernel(
   for (int c = 0; c < kBufs - 1; ++c) fetch(first_tile, c, lds + c * CHUNK);
   wait_chunk<kDmaPerChunk * (kBufs - 2)>();
 
-  // fetch the chunk kBufs - 1 ahead of chunk c of tile t (possibly in the next tile)
-  auto prefetch = [&](int64_t t, int c) {
-    int pc = c + kBufs - 1;
-    int64_t pt = t;
-    if (pc >= NC) { pc -= NC; pt += stride; }
-    fetch(pt, pc, lds + ((g + kBufs - 1) % kBufs) * CHUNK);
-  };
+  auto ahead = [&]() { return lds + ((g + kBufs - 1) % kBufs) * CHUNK; };
   auto advance = [&]() {
     wait_chunk<kDmaPerChunk * (kBufs - 2)>();
     ++g;
@@ -360,7 +371,7 @@ void mlp3_bf16_kernel(
 #pragma unroll
     for (int c = 0; c < NX; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      prefetch(tile, c);
+      fetch(tile, c + kBufs - 1, ahead());
       if ((wave >> 1) == c) {
 #pragma unroll
         for (int ks = 0; ks < KS1; ++ks)
@@ -374,36 +385,36 @@ void mlp3_bf16_kernel(
 #pragma unroll
     for (int c = 0; c < NC1; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      prefetch(tile, NX + c);
+      fetch(tile, NX + c + kBufs - 1, ahead());
 #pragma unroll
       for (int lb = 0; lb < 2; ++lb) {
-        f32x16 acc = {};
-        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [](int) {});
         const int nb = 2 * c + lb;
+        f32x16 acc = bias_acc(s_b1 + nb * 32, h);
+        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [](int) {});
 #pragma unroll
-        for (int half = 0; half < 2; ++half)
-          h1[2 * nb + half] = bias_relu_bf16(acc, half, s_b1 + nb * 32 + half * 16 + h * 8);
+        for (int half = 0; half < 2; ++half) h1[2 * nb + half] = relu_bf16(acc, half);
         __builtin_amdgcn_sched_barrier(0);
       }
       advance();
     }
 
-    // ---- layer 2 block by block, each block folded straight into the logits -----------
+    // ---- layer 2 block by block, each block folded straight into the logits. The last
+    // blocks, whose prefetches reach into the next tile, are peeled off the loop so that its
+    // body only ever fetches layer-2 chunks ---------------------------------------------------
     f32x16 logit[BT];
 #pragma unroll
     for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
-    for (int b = 0; b < NB2; ++b) {
-      f32x16 acc = {};
+    auto l2_block = [&](int b, auto&& fetch_ahead) {
+      f32x16 acc = bias_acc(s_b2 + b * 32, h);
 #pragma unroll
       for (int part = 0; part < KP; ++part) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-        prefetch(tile, NX + NC1 + b * KP + part);
+        fetch_ahead(b * KP + part + kBufs - 1);
         mfma_chain<32, H1 / 16>(acc, buf + l2, buf + l2, h1, part * 32, [](int) {});
         if (part == KP - 1) {
           bf16x8 h2[2];
 #pragma unroll
-          for (int half = 0; half < 2; ++half)
-            h2[half] = bias_relu_bf16(acc, half, s_b2 + b * 32 + half * 16 + h * 8);
+          for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(acc, half);
 #pragma unroll
           for (int bt = 0; bt < BT; ++bt) {
 #pragma unroll
@@ -417,7 +428,18 @@ void mlp3_bf16_kernel(
         __builtin_amdgcn_sched_barrier(0);
         advance();
       }
-    }
+    };
+    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied
+    constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
+    static_assert(NB2 > kPeel, "at least one block in the steady-state loop");
+    for (int b = 0; b < NB2 - kPeel; ++b)
+      l2_block(b, [&](int j) { fetch_l2(j / KP, j % KP, ahead()); });
+#pragma unroll
+    for (int b = NB2 - kPeel; b < NB2; ++b)
+      l2_block(b, [&](int j) {
+        if (j < NB2 * KP) fetch_l2(j / KP, j % KP, ahead());
+        else fetch(tile + stride, j - NB2 * KP, ahead());
+      });
 
     const int local = wave * kRowsPerWave + r32;
     const int64_t row = tile * kRowsPerBlock + local;
