@@ -251,6 +251,7 @@ void mlp3_bf16_kernel(
   constexpr int CHUNK = cmax(cmax(64 * 512, 32 * PAIR), W3OFF + B * 64);
   static_assert(NC >= kBufs - 1, "prologue fetches whole chunks of the first tile");
   static_assert(NX + NC1 + kBufs - 1 <= NC, "feature and layer-1 prefetches stay within the tile");
+  static_assert(2 * KS1 == 32, "a layer-1 chunk is 32 MFMA steps");
   static_assert(NB2 * KP >= kBufs - 1, "the peeled layer-2 blocks cover every wrapping prefetch");
 
   __shared__ __attribute__((aligned(16))) unsigned char lds[kBufs * CHUNK];
@@ -301,34 +302,49 @@ void mlp3_bf16_kernel(
       dma4(buffer_rsrc(src + row0, rows * 4), voffm, lds_addr(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
     }
   };
-  // layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units with bit
-  // 3 flipped), i = wave + 4q
-  auto fetch_l1 = [&](int j, const unsigned char* dst) {
-    const uint32_t base = lds_addr(dst) + wave * PAIR;
-    const uint32_t s0 = (uint32_t)((64 * j + 2 * wave) * D * 2);
-#pragma unroll
-    for (int q = 0; q < kDmaPerChunk; ++q)
-      dma16(rs_w1, voff1, s0 + (uint32_t)(8 * q * D * 2), base, q * kWaves * PAIR);
+  // load q of layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units
+  // with bit 3 flipped), i = wave + 4q; q = kDmaPerChunk issues nothing
+  auto load_l1 = [&](int j, int q, const unsigned char* dst) {
+    if (q < kDmaPerChunk)
+      dma16(rs_w1, voff1, (uint32_t)((64 * j + 2 * wave + 8 * q) * D * 2), lds_addr(dst) + wave * PAIR,
+            q * kWaves * PAIR);
   };
-  // layer-2 chunk (b, part): W2 rows 32b + r, r = wave + 4q; the last part also brings W3 rows
-  // 16i .. 16i+15 (i = wave), columns 32b .. 32b+31: lane -> row 16i + lane/4, unit (lane % 4)
-  // rotated by (row / 4) % 4
-  auto fetch_l2 = [&](int b, int part, const unsigned char* dst) {
-    const uint32_t base = lds_addr(dst) + wave * ROW2;
-    const uint32_t s0 = (uint32_t)((32 * b + wave) * H1 * 2 + part * 1024);
-#pragma unroll
-    for (int q = 0; q < kDmaPerChunk; ++q)
-      dma16(rs_w2, voff2, s0 + (uint32_t)(4 * q * H1 * 2), base, q * kWaves * ROW2);
-    if (part == KP - 1) {
+  // load q of layer-2 chunk (b, part): W2 rows 32b + r, r = wave + 4q; load kDmaPerChunk of the
+  // last part brings W3 rows 16i .. 16i+15 (i = wave), columns 32b .. 32b+31: lane -> row
+  // 16i + lane/4, unit (lane % 4) rotated by (row / 4) % 4
+  auto load_l2 = [&](int b, int part, int q, const unsigned char* dst) {
+    if (q < kDmaPerChunk) {
+      dma16(rs_w2, voff2, (uint32_t)((32 * b + wave + 4 * q) * H1 * 2 + part * 1024), lds_addr(dst) + wave * ROW2,
+            q * kWaves * ROW2);
+    } else if (part == KP - 1) {
       static_assert(B / 16 == kWaves, "one W3 slice load per wavefront");
       dma16(rs_w3, voff3, (uint32_t)(16 * wave * H2 * 2 + 64 * b), lds_addr(dst) + W3OFF + wave * 1024, 0);
     }
   };
-  // chunk c of tile t; c is a compile-time constant at every call site
+  // chunk c of tile t, all loads at once; c is a compile-time constant at every call site
   auto fetch = [&](int64_t t, int c, const unsigned char* dst) {
-    if (c < NX) fetch_x(t, c, dst);
-    else if (c < NX + NC1) fetch_l1(c - NX, dst);
-    else fetch_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, dst);
+    if (c < NX) {
+      fetch_x(t, c, dst);
+    } else {
+#pragma unroll
+      for (int q = 0; q <= kDmaPerChunk; ++q) {
+        if (c < NX + NC1) load_l1(c - NX, q, dst);
+        else load_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, q, dst);
+      }
+    }
+  };
+  // The same loads spread over the 32 MFMA steps of the chunk being multiplied meanwhile: load q
+  // goes out after step 3q, so no wavefront stalls behind a burst of memory instructions. A
+  // feature chunk (no multiplications of its own to hide behind) goes out whole at step 0.
+  constexpr int kSpread = 3;
+  static_assert(kSpread * kDmaPerChunk < 32, "every load of a chunk issues within its 32 steps");
+  auto spread = [&](int64_t t, int c, const unsigned char* dst, int step) {
+    if (c < NX) {
+      if (step == 0) fetch_x(t, c, dst);
+    } else if (step % kSpread == 0 && step / kSpread <= kDmaPerChunk) {
+      if (c < NX + NC1) load_l1(c - NX, step / kSpread, dst);
+      else load_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, step / kSpread, dst);
+    }
   };
 
   // per-lane LDS offsets of the A operands
@@ -385,12 +401,13 @@ void mlp3_bf16_kernel(
 #pragma unroll
     for (int c = 0; c < NC1; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      fetch(tile, NX + c + kBufs - 1, ahead());
+      const unsigned char* dst = ahead();
 #pragma unroll
       for (int lb = 0; lb < 2; ++lb) {
         const int nb = 2 * c + lb;
         f32x16 acc = bias_acc(s_b1 + nb * 32, h);
-        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [](int) {});
+        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0,
+                             [&](int k) { spread(tile, NX + c + kBufs - 1, dst, KS1 * lb + k); });
 #pragma unroll
         for (int half = 0; half < 2; ++half) h1[2 * nb + half] = relu_bf16(acc, half);
         __builtin_amdgcn_sched_barrier(0);
@@ -404,13 +421,14 @@ void mlp3_bf16_kernel(
     f32x16 logit[BT];
 #pragma unroll
     for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
-    auto l2_block = [&](int b, auto&& fetch_ahead) {
+    auto l2_block = [&](int b, auto&& load_ahead) {
       f32x16 acc = bias_acc(s_b2 + b * 32, h);
 #pragma unroll
       for (int part = 0; part < KP; ++part) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-        fetch_ahead(b * KP + part + kBufs - 1);
-        mfma_chain<32, H1 / 16>(acc, buf + l2, buf + l2, h1, part * 32, [](int) {});
+        const unsigned char* dst = ahead();
+        mfma_chain<32, H1 / 16>(acc, buf + l2, buf + l2, h1, part * 32,
+                                [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
         if (part == KP - 1) {
           bf16x8 h2[2];
 #pragma unroll
@@ -433,12 +451,12 @@ void mlp3_bf16_kernel(
     constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
     static_assert(NB2 > kPeel, "at least one block in the steady-state loop");
     for (int b = 0; b < NB2 - kPeel; ++b)
-      l2_block(b, [&](int j) { fetch_l2(j / KP, j % KP, ahead()); });
+      l2_block(b, [&](int j, const unsigned char* dst, int k) { spread(tile, NX + NC1 + j, dst, k); });
 #pragma unroll
     for (int b = NB2 - kPeel; b < NB2; ++b)
-      l2_block(b, [&](int j) {
-        if (j < NB2 * KP) fetch_l2(j / KP, j % KP, ahead());
-        else fetch(tile + stride, j - NB2 * KP, ahead());
+      l2_block(b, [&](int j, const unsigned char* dst, int k) {
+        if (j < NB2 * KP) spread(tile, NX + NC1 + j, dst, k);
+        else spread(tile + stride, j - NB2 * KP, dst, k);
       });
 
     const int local = wave * kRowsPerWave + r32;
