@@ -186,6 +186,8 @@ constexpr int kDmaPerChunk = 8;          // direct loads per wavefront per chunk
 // assembly so that the compiler's automatic wait insertion, which would conservatively drain
 // every such load before any LDS read, does not see them; the kernel waits for them itself
 // (wait_chunk). rsrc, soff and lds_base are wavefront-uniform; lds_off is a compile-time constant.
+// An LDS-DMA load reads M0 and needs one wait state after the scalar write of M0 (a hazard the
+// compiler resolves only for instructions it generates itself), hence the s_nop.
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) unsigned char lds_uchar;
 
@@ -205,11 +207,11 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 __device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t soff, uint32_t lds_base,
                                       int lds_off) {
-  asm volatile("s_add_u32 m0, %0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
+  asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
                ::"s"(lds_base), "i"(lds_off), "v"(voff), "s"(rsrc), "s"(soff) : "m0", "scc");
 }
 __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
                ::"s"(lds_base), "v"(voff), "s"(rsrc) : "m0");
 }
 

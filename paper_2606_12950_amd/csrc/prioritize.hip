@@ -1,17 +1,22 @@
 // Slack ordering of workflows (Sec. III-D, remaining-time queueing; Eq. 7).
 //
-//  1. chain kernel, one thread per workflow: walks its chain from the last stage backwards,
-//     quantising every stage latency to integer microseconds (round half to even) and
-//     accumulating the suffix sums in int64 -- the remaining predicted time from each stage to
-//     the end of the chain. The remaining time at the workflow's cursor gives
-//     slack = deadline - now - remaining, clamped to int32. Integer sums are exact, so the
-//     result does not depend on the summation order.
+//  1. chain kernel, one thread per workflow and one 1024-thread block per sort tile: walks the
+//     workflow's chain from the last stage backwards, quantising every stage latency to integer
+//     microseconds (round half to even) and accumulating the suffix sums in int64 -- the
+//     remaining predicted time from each stage to the end of the chain. The stage latencies
+//     are loaded eight at a time, so a chain costs one memory round trip per eight stages. The
+//     remaining time at the workflow's cursor gives slack = deadline - now - remaining,
+//     clamped to int32. Integer sums are exact, so the result does not depend on the
+//     summation order. The block also counts the first radix digit of its tile.
 //  2. stable LSD radix sort of the (slack, workflow) pairs, 4 passes of 8-bit digits over the
-//     order-preserving unsigned image of the key. Each pass: per-tile digit counts, the
-//     exclusive scan of the digit-major count table (global offset of every (digit, tile);
-//     done inside the scatter blocks when there are few tiles), and a scatter in which each
-//     wavefront ranks its items digit by digit with ballots (wave multisplit) in input order,
-//     so equal digits keep their relative order.
+//     order-preserving unsigned image of the key, on 1024-key tiles, one key per thread of a
+//     1024-thread block. Each pass: per-tile digit counts (for the first pass, from the chain
+//     kernel); the global offset of every (digit, tile), i.e. the exclusive scan of the count
+//     table in digit-major order, which each scatter block derives itself from the table when
+//     there are few tiles (four threads per digit read it, one memory round trip) and a
+//     separate one-block scan writes otherwise; and a scatter in which each wavefront ranks
+//     its keys digit by digit with ballots (wave multisplit) in input order, so equal digits
+//     keep their relative order.
 //     The key array is padded to whole tiles with all-ones keys, which always sort last and
 //     never reach the caller's output.
 #include "internal.h"
@@ -19,13 +24,12 @@
 namespace maestro {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kItems = 16;                         // items per thread in a sort tile
-constexpr int kTile = kThreads * kItems;           // 4096 keys per tile
-constexpr int kWaves = kThreads / 64;
+constexpr int kTile = 1024;                        // keys per sort tile = threads per block
+constexpr int kWaves = kTile / 64;
 constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr int kPasses = 32 / kRadixBits;
+// count table: counts[t * kBuckets + d] = keys of tile t with digit d (tile-major)
 
 constexpr int64_t kLatSat = INT64_MAX;             // infinitely late (absorbing)
 constexpr double kLatUsLimit = 1099511627776.0;    // 2^40 microseconds
@@ -48,65 +52,86 @@ __device__ __forceinline__ int64_t sat_sub(int64_t a, int64_t b) {
   return r;
 }
 
-__global__ __launch_bounds__(kThreads) void chain_kernel(
-    int32_t n_workflows, int64_t padded, const int64_t* __restrict__ chain_offset,
+constexpr int kChainBatch = 8;                     // stage latencies loaded per round trip
+
+// One block per sort tile, one workflow per thread; also writes the tile's counts of the
+// first digit.
+__global__ __launch_bounds__(kTile) void chain_kernel(
+    int32_t n_workflows, const int64_t* __restrict__ chain_offset,
     const float* __restrict__ stage_latency_s, const int32_t* __restrict__ cursor,
     const int64_t* __restrict__ deadline_us, int64_t now_us, int64_t* __restrict__ remaining_us,
-    int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
-  const int64_t w = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (w >= padded) return;
-  if (w >= n_workflows) {  // tile padding: largest key, sorts after every real workflow
-    keys[w] = 0xFFFFFFFFu;
-    vals[w] = (uint32_t)w;
-    return;
-  }
-  const int64_t first = chain_offset[w], end = chain_offset[w + 1];
-  int64_t cur = cursor ? (int64_t)cursor[w] : 0;
-  if (cur < 0) cur = 0;
-  const int64_t head = first + cur;
-  int64_t suffix = 0, rem_head = 0;
-  for (int64_t j = end - 1; j >= first; --j) {
-    suffix = sat_add(latency_us(stage_latency_s[j]), suffix);
-    if (remaining_us) remaining_us[j] = suffix;
-    if (j == head) rem_head = suffix;
-  }
-  int32_t key;
-  if (rem_head == kLatSat) {
-    key = INT32_MIN;
-  } else {
-    // |rem_head| <= 2^62, so saturating the two differences keeps the int32 clamp exact
-    const int64_t slack = sat_sub(sat_sub(deadline_us[w], now_us), rem_head);
-    key = slack > INT32_MAX ? INT32_MAX : (slack < INT32_MIN ? INT32_MIN : (int32_t)slack);
-  }
-  slack_key[w] = key;
-  keys[w] = (uint32_t)key ^ 0x80000000u;   // order-preserving unsigned image
-  vals[w] = (uint32_t)w;
-}
-
-// Per-tile digit counts, digit-major: counts[d * n_tiles + t].
-__global__ __launch_bounds__(kThreads) void radix_count_kernel(const uint32_t* __restrict__ keys,
-                                                               int shift, int n_tiles,
-                                                               uint32_t* __restrict__ counts) {
+    int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+    uint32_t* __restrict__ counts) {
   __shared__ uint32_t hist[kBuckets];
   const int tid = threadIdx.x, tile = blockIdx.x;
-  hist[tid] = 0;
+  if (tid < kBuckets) hist[tid] = 0;
   __syncthreads();
-  const uint32_t* k = keys + (int64_t)tile * kTile;
+  const int64_t w = (int64_t)tile * kTile + tid;
+  uint32_t ukey = 0xFFFFFFFFu;   // tile padding: largest key, sorts after every real workflow
+  if (w < n_workflows) {
+    const int64_t first = chain_offset[w], end = chain_offset[w + 1];
+    int64_t cur = cursor ? (int64_t)cursor[w] : 0;
+    if (cur < 0) cur = 0;
+    const int64_t head = first + cur;
+    int64_t suffix = 0, rem_head = 0;
+    for (int64_t top = end - 1; top >= first; top -= kChainBatch) {
+      float lat[kChainBatch];
 #pragma unroll
-  for (int i = 0; i < kItems; ++i) atomicAdd(&hist[(k[i * kThreads + tid] >> shift) & (kBuckets - 1)], 1u);
+      for (int u = 0; u < kChainBatch; ++u) lat[u] = (top - u >= first) ? stage_latency_s[top - u] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < kChainBatch; ++u) {
+        const int64_t j = top - u;
+        if (j >= first) {
+          suffix = sat_add(latency_us(lat[u]), suffix);
+          if (remaining_us) remaining_us[j] = suffix;
+          if (j == head) rem_head = suffix;
+        }
+      }
+    }
+    int32_t key;
+    if (rem_head == kLatSat) {
+      key = INT32_MIN;
+    } else {
+      // |rem_head| <= 2^62, so saturating the two differences keeps the int32 clamp exact
+      const int64_t slack = sat_sub(sat_sub(deadline_us[w], now_us), rem_head);
+      key = slack > INT32_MAX ? INT32_MAX : (slack < INT32_MIN ? INT32_MIN : (int32_t)slack);
+    }
+    slack_key[w] = key;
+    ukey = (uint32_t)key ^ 0x80000000u;   // order-preserving unsigned image
+  }
+  keys[w] = ukey;
+  vals[w] = (uint32_t)w;
+  atomicAdd(&hist[ukey & (kBuckets - 1)], 1u);
   __syncthreads();
-  counts[(int64_t)tid * n_tiles + tile] = hist[tid];
+  if (tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
 }
 
-// Exclusive scan of the count table in place (one workgroup; the table is small next to the
-// keys: 256 entries per 4096-key tile).
-__global__ __launch_bounds__(1024) void radix_scan_kernel(uint32_t* __restrict__ counts, int64_t total) {
+// Per-tile digit counts of the digit at `shift`.
+__global__ __launch_bounds__(kTile) void radix_count_kernel(const uint32_t* __restrict__ keys, int shift,
+                                                            uint32_t* __restrict__ counts) {
+  __shared__ uint32_t hist[kBuckets];
+  const int tid = threadIdx.x, tile = blockIdx.x;
+  if (tid < kBuckets) hist[tid] = 0;
+  __syncthreads();
+  atomicAdd(&hist[(keys[(int64_t)tile * kTile + tid] >> shift) & (kBuckets - 1)], 1u);
+  __syncthreads();
+  if (tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
+}
+
+// Global offsets for many tiles (one workgroup): offsets[t * kBuckets + d] = keys with a
+// smaller digit anywhere, plus keys with digit d in tiles before t -- the exclusive scan of
+// the count table taken in digit-major order.
+__global__ __launch_bounds__(1024) void radix_scan_kernel(const uint32_t* __restrict__ counts, int n_tiles,
+                                                          uint32_t* __restrict__ offsets) {
   __shared__ uint32_t part[1024];
   const int tid = threadIdx.x;
+  const int64_t total = (int64_t)kBuckets * n_tiles;
   const int64_t per = (total + 1023) / 1024;
   const int64_t lo = min(total, tid * per), hi = min(total, lo + per);
+  // logical index i = d * n_tiles + t lives at t * kBuckets + d
+  auto at = [&](int64_t i) { return (i % n_tiles) * kBuckets + i / n_tiles; };
   uint32_t s = 0;
-  for (int64_t i = lo; i < hi; ++i) s += counts[i];
+  for (int64_t i = lo; i < hi; ++i) s += counts[at(i)];
   part[tid] = s;
   __syncthreads();
   for (int off = 1; off < 1024; off <<= 1) {   // Hillis-Steele inclusive scan
@@ -117,78 +142,85 @@ __global__ __launch_bounds__(1024) void radix_scan_kernel(uint32_t* __restrict__
   }
   uint32_t run = tid ? part[tid - 1] : 0u;
   for (int64_t i = lo; i < hi; ++i) {
-    const uint32_t c = counts[i];
-    counts[i] = run;
+    const int64_t a = at(i);
+    const uint32_t c = counts[a];
+    offsets[a] = run;
     run += c;
   }
 }
 
-// Stable scatter of one tile by the digit at `shift`. Items of the tile are taken in input
-// order: wavefront w owns positions [w*1024, (w+1)*1024), step i covers 64 consecutive ones.
-// out_keys may be null (last pass); positions >= out_limit are padding and are dropped.
-// With kFusedScan the tile derives its digit offsets from the raw count table itself
-// (digit totals over all tiles, exclusive-scanned, plus the counts of the earlier tiles);
-// otherwise `offsets` holds the scanned table.
+// Stable scatter of one tile by the digit at `shift`, one key per thread: wavefront w holds
+// tile positions [64w, 64w + 64). out_keys may be null (last pass); positions >= out_limit are
+// padding and are dropped. With kFusedScan the block derives its digit offsets from the count
+// table (digit totals over all tiles, exclusive-scanned, plus the counts of the earlier
+// tiles); otherwise `table` holds the offsets written by radix_scan_kernel.
+constexpr int kFusedScanMaxTiles = 128;
 template <bool kFusedScan>
-__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+__global__ __launch_bounds__(kTile) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, int shift, int n_tiles,
-    const uint32_t* __restrict__ offsets, uint32_t* __restrict__ out_keys,
-    uint32_t* __restrict__ out_vals, int64_t out_limit) {
+    const uint32_t* __restrict__ table, uint32_t* __restrict__ out_keys, uint32_t* __restrict__ out_vals,
+    int64_t out_limit) {
   __shared__ uint32_t wcount[kWaves][kBuckets];
   __shared__ uint32_t base[kBuckets];
+  __shared__ uint32_t part_before[4][kBuckets], part_total[4][kBuckets];
   const int tid = threadIdx.x, tile = blockIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) wcount[w][tid] = 0;
+  const int64_t pos_in = (int64_t)tile * kTile + tid;
+  const uint32_t key = keys[pos_in], val = vals[pos_in];
+  for (int i = tid; i < kWaves * kBuckets; i += kTile) (&wcount[0][0])[i] = 0;
+
   if (kFusedScan) {
-    // thread d: total of digit d over all tiles, and over the tiles before this one
-    const uint32_t* row = offsets + (int64_t)tid * n_tiles;
+    // thread (q, d), q = tid / 256: digit d over tiles q, q + 4, q + 8, ...: all loads of a
+    // thread are independent and go out together
+    const int d = tid & (kBuckets - 1), q = tid >> 8;
     uint32_t before = 0, total = 0;
-    for (int t = 0; t < n_tiles; ++t) {
-      const uint32_t c = row[t];
-      before += (t < tile) ? c : 0u;
+    constexpr int kUnroll = kFusedScanMaxTiles / 4;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int t = q + 4 * u;
+      const uint32_t c = t < n_tiles ? table[(int64_t)t * kBuckets + d] : 0u;
       total += c;
+      before += t < tile ? c : 0u;
     }
-    base[tid] = total;
+    part_before[q][d] = before;
+    part_total[q][d] = total;
+    __syncthreads();
+    if (tid < kBuckets) {
+      base[tid] = part_total[0][tid] + part_total[1][tid] + part_total[2][tid] + part_total[3][tid];
+      part_before[0][tid] += part_before[1][tid] + part_before[2][tid] + part_before[3][tid];
+    }
     __syncthreads();
     for (int off = 1; off < kBuckets; off <<= 1) {   // inclusive scan of the digit totals
-      const uint32_t v = tid >= off ? base[tid - off] : 0u;
+      uint32_t v = 0;
+      if (tid < kBuckets && tid >= off) v = base[tid - off];
       __syncthreads();
-      base[tid] += v;
+      if (tid < kBuckets) base[tid] += v;
       __syncthreads();
     }
-    const uint32_t excl = base[tid] - total;
-    __syncthreads();
-    base[tid] = excl + before;
+    if (tid < kBuckets) {
+      const uint32_t incl = base[tid];
+      const uint32_t own = part_total[0][tid] + part_total[1][tid] + part_total[2][tid] + part_total[3][tid];
+      base[tid] = incl - own + part_before[0][tid];
+    }
   } else {
-    base[tid] = offsets[(int64_t)tid * n_tiles + tile];
+    if (tid < kBuckets) base[tid] = table[(int64_t)tile * kBuckets + tid];
   }
   __syncthreads();
 
-  const int64_t t0 = (int64_t)tile * kTile + wave * (kTile / kWaves);
+  // rank among the lanes of this wavefront with the same digit, in lane order
+  const uint32_t d = (key >> shift) & (kBuckets - 1);
+  uint64_t same = ~0ull;
+#pragma unroll
+  for (int b = 0; b < kRadixBits; ++b) {
+    const bool bit = (d >> b) & 1u;
+    const uint64_t ones = __ballot(bit);
+    same &= bit ? ones : ~ones;
+  }
   const uint64_t lanes_below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  uint32_t key[kItems], val[kItems], rank[kItems];
-#pragma unroll
-  for (int i = 0; i < kItems; ++i) {
-    key[i] = keys[t0 + i * 64 + lane];
-    val[i] = vals[t0 + i * 64 + lane];
-  }
-#pragma unroll
-  for (int i = 0; i < kItems; ++i) {
-    const uint32_t d = (key[i] >> shift) & (kBuckets - 1);
-    uint64_t same = ~0ull;                     // lanes whose digit equals this lane's
-#pragma unroll
-    for (int b = 0; b < kRadixBits; ++b) {
-      const bool bit = (d >> b) & 1u;
-      const uint64_t ones = __ballot(bit);
-      same &= bit ? ones : ~ones;
-    }
-    const uint32_t before = wcount[wave][d];
-    rank[i] = before + (uint32_t)__popcll(same & lanes_below);
-    if ((same & lanes_below) == 0ull) wcount[wave][d] = before + (uint32_t)__popcll(same);
-  }
+  const uint32_t rank = (uint32_t)__popcll(same & lanes_below);
+  if ((same & lanes_below) == 0ull) wcount[wave][d] = (uint32_t)__popcll(same);   // first lane of the digit
   __syncthreads();
-  {  // offsets of each wavefront inside the tile's digit groups
+  if (tid < kBuckets) {   // offsets of each wavefront inside the tile's digit groups
     uint32_t run = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
@@ -198,25 +230,18 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
   }
   __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kItems; ++i) {
-    const uint32_t d = (key[i] >> shift) & (kBuckets - 1);
-    const int64_t pos = (int64_t)base[d] + wcount[wave][d] + rank[i];
-    if (pos < out_limit) {
-      if (out_keys) out_keys[pos] = key[i];
-      out_vals[pos] = val[i];
-    }
+  const int64_t pos = (int64_t)base[d] + wcount[wave][d] + rank;
+  if (pos < out_limit) {
+    if (out_keys) out_keys[pos] = key;
+    out_vals[pos] = val;
   }
 }
-
-// up to this many tiles each scatter block scans the count table itself
-constexpr int kFusedScanMaxTiles = 64;
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct PrioLayout {
   int64_t n_tiles, padded;
-  size_t keys_a, vals_a, keys_b, vals_b, counts, total;
+  size_t keys_a, vals_a, keys_b, vals_b, counts, offsets, total;
 };
 
 PrioLayout prio_layout(int32_t n_workflows) {
@@ -224,12 +249,14 @@ PrioLayout prio_layout(int32_t n_workflows) {
   L.n_tiles = ((int64_t)n_workflows + kTile - 1) / kTile;
   L.padded = L.n_tiles * kTile;
   const size_t kb = align256(sizeof(uint32_t) * (size_t)L.padded);
+  const size_t cb = align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_tiles);
   L.keys_a = 0;
   L.vals_a = L.keys_a + kb;
   L.keys_b = L.vals_a + kb;
   L.vals_b = L.keys_b + kb;
   L.counts = L.vals_b + kb;
-  L.total = L.counts + align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_tiles);
+  L.offsets = L.counts + cb;
+  L.total = L.offsets + (L.n_tiles > kFusedScanMaxTiles ? cb : 0);
   return L;
 }
 
@@ -251,26 +278,29 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
   uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(ws + L.keys_a), reinterpret_cast<uint32_t*>(ws + L.keys_b)};
   uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(ws + L.vals_a), reinterpret_cast<uint32_t*>(ws + L.vals_b)};
   uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.counts);
+  uint32_t* offsets = reinterpret_cast<uint32_t*>(ws + L.offsets);
 
-  chain_kernel<<<dim3((unsigned)((L.padded + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream>>>(
-      n_workflows, L.padded, chain_offset, stage_latency_s, cursor, deadline_us, now_us,
-      remaining_us, slack_key, keys[0], vals[0]);
   const int nt = (int)L.n_tiles;
+  const bool fused = nt <= kFusedScanMaxTiles;
+  chain_kernel<<<dim3((unsigned)nt), dim3(kTile), 0, stream>>>(
+      n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us,
+      slack_key, keys[0], vals[0], counts);
   for (int pass = 0; pass < kPasses; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     const int shift = pass * kRadixBits;
     const bool last = pass + 1 == kPasses;
-    radix_count_kernel<<<dim3(nt), dim3(kThreads), 0, stream>>>(keys[src], shift, nt, counts);
+    if (pass > 0)   // the chain kernel counted the first digit
+      radix_count_kernel<<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
     uint32_t* out_k = last ? nullptr : keys[dst];
     uint32_t* out_v = last ? reinterpret_cast<uint32_t*>(order) : vals[dst];
     const int64_t limit = last ? (int64_t)n_workflows : L.padded;
-    if (nt <= kFusedScanMaxTiles) {
-      radix_scatter_kernel<true><<<dim3(nt), dim3(kThreads), 0, stream>>>(
+    if (fused) {
+      radix_scatter_kernel<true><<<dim3(nt), dim3(kTile), 0, stream>>>(
           keys[src], vals[src], shift, nt, counts, out_k, out_v, limit);
     } else {
-      radix_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(counts, (int64_t)kBuckets * nt);
-      radix_scatter_kernel<false><<<dim3(nt), dim3(kThreads), 0, stream>>>(
-          keys[src], vals[src], shift, nt, counts, out_k, out_v, limit);
+      radix_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(counts, nt, offsets);
+      radix_scatter_kernel<false><<<dim3(nt), dim3(kTile), 0, stream>>>(
+          keys[src], vals[src], shift, nt, offsets, out_k, out_v, limit);
     }
   }
   return launch_status();

@@ -107,11 +107,14 @@ def test_route_validation(lib):
 
 def test_prioritize_validation_and_workspace(lib):
     ws = lib.maestro_prioritize_workspace(131072, 720000)
-    # four key/value arrays padded to 4096-key tiles plus a 256-entry count table per tile
-    tiles = 131072 // 4096
-    assert ws == 4 * 4 * tiles * 4096 + 4 * 256 * tiles
+    # four key/value arrays padded to 1024-key tiles plus a 256-entry count table per tile
+    tiles = 131072 // 1024
+    assert ws == 4 * 4 * tiles * 1024 + 4 * 256 * tiles
     assert lib.maestro_prioritize_workspace(0, 0) == 0
-    assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 4096 + 4 * 256
+    assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 1024 + 4 * 256
+    # beyond 128 tiles the scatter reads a separately scanned offset table of the same size
+    tiles = (200000 + 1023) // 1024
+    assert lib.maestro_prioritize_workspace(200000, 10**6) == 4 * 4 * tiles * 1024 + 2 * 4 * 256 * tiles
     call = lambda W=4, S=8, off=FAKE, ws=FAKE, ws_bytes=1 << 20: lib.maestro_prioritize(
         W, S, off, FAKE, None, FAKE, 0, None, FAKE, FAKE, ws, ws_bytes, None)
     assert call(W=-1) == INVALID

@@ -276,7 +276,7 @@ def test_c3_full_step_matches_oracle():
     print(f"c3: W={w.n_workflows} S={w.n}: route + order identical")
 
 
-@pytest.mark.parametrize("W_", [1, 5, 4095, 4096, 4097, 131072, 1 << 20])
+@pytest.mark.parametrize("W_", [1, 5, 1023, 1024, 1025, 4097, 131072, 131073, 1 << 20])
 def test_prioritize_random_chains(W_):
     rng = np.random.default_rng(W_)
     lens = rng.integers(0, 9, W_)
