@@ -126,17 +126,21 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // acc += sum_k A_k * B[k0 + k], A_k the 16-byte LDS fragment at (k & 4 ? pb : pa) + 32k (the
 // two bases absorb the layer-1 unit swizzle; pass pa == pb elsewhere). Fragments are read
-// kLookahead steps ahead of their MFMA, and side(k) -- a slice of the previous block's
-// epilogue -- is issued right after MFMA k so that it runs while the matrix core is busy.
-// The scheduling barriers keep exactly this order.
+// kLookahead steps ahead of their MFMA. pre() -- the deferred epilogue of the previous block --
+// runs after the first fragment reads are issued, so that it fills their latency; side(k) is
+// issued right after MFMA k, while the matrix core is busy. The scheduling barriers keep
+// exactly this order.
 constexpr int kLookahead = 3;
-template <int KS, int NBREG, typename Side>
+template <int KS, int NBREG, typename Pre, typename Side>
 __device__ __forceinline__ void mfma_chain(f32x16& acc, const unsigned char* pa, const unsigned char* pb,
-                                           const bf16x8 (&b)[NBREG], int k0, Side&& side) {
+                                           const bf16x8 (&b)[NBREG], int k0, Pre&& pre, Side&& side) {
   bf16x8 fr[KS];
 #pragma unroll
   for (int k = 0; k < kLookahead && k < KS; ++k)
     fr[k] = *reinterpret_cast<const bf16x8*>(((k & 4) ? pb : pa) + k * 32);
+  __builtin_amdgcn_sched_barrier(0);
+  pre();
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int k = 0; k < KS; ++k) {
     if (k + kLookahead < KS) {
@@ -399,7 +403,18 @@ void mlp3_bf16_kernel(
     }
 
     // ---- layer 1: H1 = relu(W1 x + b1), kept as the B operand of layer 2 ---------------
+    // Each block's ReLU is deferred into the next block's chain (the last one into the first
+    // layer-2 block). The activations live in the accumulation registers, which MFMA reads as
+    // its B operand directly, leaving the architectural registers to everything else.
     bf16x8 h1[H1 / 16];
+    f32x16 acc_prev;                      // finished accumulator of the previous block
+    auto l1_relu = [&](int nb, const f32x16& acc) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        h1[2 * nb + half] = relu_bf16(acc, half);
+        asm volatile("" : "+a"(h1[2 * nb + half]));
+      }
+    };
 #pragma unroll
     for (int c = 0; c < NC1; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
@@ -408,10 +423,10 @@ void mlp3_bf16_kernel(
       for (int lb = 0; lb < 2; ++lb) {
         const int nb = 2 * c + lb;
         f32x16 acc = bias_acc(s_b1 + nb * 32, h);
-        mfma_chain<KS1, KS1>(acc, buf + l1a[lb], buf + l1b[lb], xf, 0,
-                             [&](int k) { spread(tile, NX + c + kBufs - 1, dst, KS1 * lb + k); });
-#pragma unroll
-        for (int half = 0; half < 2; ++half) h1[2 * nb + half] = relu_bf16(acc, half);
+        mfma_chain<KS1, KS1>(
+            acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [&]() { if (nb > 0) l1_relu(nb - 1, acc_prev); },
+            [&](int k) { spread(tile, NX + c + kBufs - 1, dst, KS1 * lb + k); });
+        acc_prev = acc;
         __builtin_amdgcn_sched_barrier(0);
       }
       advance();
@@ -420,46 +435,68 @@ void mlp3_bf16_kernel(
     // ---- layer 2 block by block, each block folded straight into the logits. The last
     // blocks, whose prefetches reach into the next tile, are peeled off the loop so that its
     // body only ever fetches layer-2 chunks ---------------------------------------------------
+    // The epilogue of each block -- ReLU and the 2 BT MFMAs that fold its 32 neurons into the
+    // logits -- is deferred into the start of the next block's chain, where it covers the
+    // latency of that chain's first fragment reads; the block's W3 fragments are read into
+    // registers before the barrier that lets its buffer be refilled.
     f32x16 logit[BT];
 #pragma unroll
     for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
-    auto l2_block = [&](int b, auto&& load_ahead) {
+    bf16x8 w3f[BT][2];                    // W3 fragments of the previous block
+    auto l2_epilogue = [&](const f32x16& prev) {
+      bf16x8 h2[2];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(prev, half);
+#pragma unroll
+      for (int bt = 0; bt < BT; ++bt)
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+          logit[bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[bt], 0, 0, 0);
+    };
+    // block b; pre(prev) is the deferred epilogue of the block before it
+    auto l2_block = [&](int b, const f32x16& prev, auto&& pre, auto&& load_ahead) {
       f32x16 acc = bias_acc(s_b2 + b * 32, h);
 #pragma unroll
       for (int part = 0; part < KP; ++part) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
         const unsigned char* dst = ahead();
-        mfma_chain<32, H1 / 16>(acc, buf + l2, buf + l2, h1, part * 32,
-                                [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
+        mfma_chain<32, H1 / 16>(
+            acc, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(prev); },
+            [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
         if (part == KP - 1) {
-          bf16x8 h2[2];
 #pragma unroll
-          for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(acc, half);
+          for (int bt = 0; bt < BT; ++bt)
 #pragma unroll
-          for (int bt = 0; bt < BT; ++bt) {
-#pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-              const int off = W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4);
-              logit[bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  *reinterpret_cast<const bf16x8*>(buf + off), h2[tt], logit[bt], 0, 0, 0);
-            }
-          }
+            for (int tt = 0; tt < 2; ++tt)
+              w3f[bt][tt] = *reinterpret_cast<const bf16x8*>(
+                  buf + W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4));
         }
         __builtin_amdgcn_sched_barrier(0);
         advance();
       }
+      return acc;
     };
-    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied
+    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied.
+    // Block 0 finishes layer 1; blocks 1 .. NB2-kPeel-1 run in a loop over pairs, so that the
+    // two accumulators alternate roles without copies; the last kPeel blocks, whose prefetches
+    // reach into the next tile, are peeled.
     constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
-    static_assert(NB2 > kPeel, "at least one block in the steady-state loop");
-    for (int b = 0; b < NB2 - kPeel; ++b)
-      l2_block(b, [&](int j, const unsigned char* dst, int k) { spread(tile, NX + NC1 + j, dst, k); });
+    constexpr int kSteady = NB2 - kPeel - 1;
+    static_assert(kSteady >= 2, "at least one pair of blocks in the steady-state loop");
+    auto in_tile = [&](int j, const unsigned char* dst, int k) { spread(tile, NX + NC1 + j, dst, k); };
+    f32x16 carry = l2_block(0, acc_prev, [&](const f32x16& p) { l1_relu(H1 / 32 - 1, p); }, in_tile);
+    for (int b = 1; b + 1 <= kSteady; b += 2) {
+      const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile);
+      carry = l2_block(b + 1, a, l2_epilogue, in_tile);
+    }
+    if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
 #pragma unroll
     for (int b = NB2 - kPeel; b < NB2; ++b)
-      l2_block(b, [&](int j, const unsigned char* dst, int k) {
+      carry = l2_block(b, carry, l2_epilogue, [&](int j, const unsigned char* dst, int k) {
         if (j < NB2 * KP) spread(tile, NX + NC1 + j, dst, k);
         else spread(tile + stride, j - NB2 * KP, dst, k);
       });
+    l2_epilogue(carry);
 
     const int local = wave * kRowsPerWave + r32;
     const int64_t row = tile * kRowsPerBlock + local;
