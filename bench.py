@@ -2,6 +2,7 @@
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
 python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for counter calibration)
+python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -65,6 +66,36 @@ def mlp_flop_per_stage(dims):
     return 2 * sum(dims[i] * dims[i + 1] for i in range(len(dims) - 1))
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def percentiles(ms):
+    a = np.asarray(ms)
+    return {"p10": round(float(np.percentile(a, 10)), 4), "p50": round(float(np.median(a)), 4),
+            "p90": round(float(np.percentile(a, 90)), 4), "mean": round(float(a.mean()), 4)}
+
+
+def route_bytes(n, m, k):
+    """Algorithmic HBM bytes of routing: per stage model id, predicted length and KV bytes in
+    (16 B) and k (node, score) pairs out (8k B); node state once (queue, cold, residency, free:
+    24 B per node)."""
+    return n * (16 + 8 * k) + 24 * m
+
+
+def prioritize_bytes(n_stages, n_workflows, passes=4):
+    """Algorithmic HBM bytes of the slack ordering: per stage the latency in (4 B) and the
+    remaining time out (8 B); per workflow chain offsets, deadline in and key out (16 + 4 B),
+    then per radix pass keys and indices read and written (16 B) and the final order (4 B)."""
+    return n_stages * 12 + n_workflows * (20 + passes * 16 + 4)
+
+
 def cpu_baseline(wl, n_workflows_sample: int):
     """Oracle (C, OpenMP over stages) on the first workflows of the batch: predict -> route ->
     prioritize, timed on the host cores."""
@@ -85,7 +116,50 @@ def cpu_baseline(wl, n_workflows_sample: int):
     sample = (f"first {W_} workflows ({S} stages) of the same batch: oracle predict + route + prioritize"
               if W_ else f"first {S} stages of the same batch: oracle predict + route")
     return {"value": S / dt, "unit": "stages/s", "cores": int(threads), "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 3)}
+            "sample": sample, "seconds": round(dt, 3), "cpu_model": cpu_model()}
+
+
+def sweep_prioritize(log2_lo: int, log2_hi: int, steps: int, warmup: int):
+    """Slack ordering alone (chain suffix sums, slack keys, stable sort) at growing batch sizes,
+    inputs resident on the GPU, one JSON line per size. The chains follow the chained batch's
+    recipe: lengths uniform in 3..8 stages, arrival U[0, 600] s, SLO U[10, 120] s, now = 600 s;
+    stage latencies are uniform in [0, 60) s (the range of the routed scores)."""
+    import torch
+    from paper_2606_12950_amd import _native
+    torch.cuda.set_device(0)
+    gen = torch.Generator(device="cuda")
+    for lg in range(log2_lo, log2_hi + 1):
+        W_ = 1 << lg
+        gen.manual_seed(1000 + lg)
+        lens = torch.randint(3, 9, (W_,), generator=gen, device="cuda", dtype=torch.int64)
+        off = torch.zeros(W_ + 1, dtype=torch.int64, device="cuda")
+        torch.cumsum(lens, 0, out=off[1:])
+        S = int(off[-1].item())
+        lat = torch.rand(S, generator=gen, device="cuda", dtype=torch.float32) * 60.0
+        arrival = torch.randint(0, 600_000_001, (W_,), generator=gen, device="cuda", dtype=torch.int64)
+        slo = torch.randint(10_000_000, 120_000_001, (W_,), generator=gen, device="cuda", dtype=torch.int64)
+        deadline = arrival + slo
+        now_us = 600_000_000
+        out = (torch.empty(S, dtype=torch.int64, device="cuda"), torch.empty(W_, dtype=torch.int32, device="cuda"),
+               torch.empty(W_, dtype=torch.int32, device="cuda"))
+        ws = torch.empty(max(1, _native.prioritize_workspace_bytes(W_, S)), dtype=torch.uint8, device="cuda")
+        for _ in range(warmup):
+            _native.prioritize(off, lat, deadline, now_us, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            _native.prioritize(off, lat, deadline, now_us, out=out, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        pb = prioritize_bytes(S, W_)
+        print(json.dumps({"sweep": "prioritize", "n_workflows": W_, "n_stages": S, "ms": round(ms, 4),
+                          "workflows_per_s": W_ / (ms * 1e-3), "algorithmic_bytes": pb,
+                          "achieved_gbs": round(pb / (ms * 1e-3) / 1e9, 2),
+                          "hbm_frac": round(pb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}), flush=True)
+        del lens, off, lat, arrival, slo, deadline, out, ws
+        torch.cuda.empty_cache()
 
 
 def main():
@@ -97,10 +171,16 @@ def main():
     ap.add_argument("--cpu-sample-workflows", type=int, default=65536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--sweep-prioritize", nargs="?", const="17:26", default=None, metavar="LO:HI",
+                    help="time the slack ordering alone for W = 2^LO .. 2^HI workflows")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.sweep_prioritize:
+        lo, hi = (int(v) for v in args.sweep_prioritize.split(":"))
+        sweep_prioritize(lo, hi, steps=max(1, min(args.steps, 20)), warmup=max(1, min(args.warmup, 3)))
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -145,9 +225,12 @@ def main():
     t1 = time.perf_counter()
 
     wall = t1 - t0
-    ms_predict = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    ms_route = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    ms_prio = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    d_predict = [e[0].elapsed_time(e[1]) for e in ev]
+    d_route = [e[1].elapsed_time(e[2]) for e in ev]
+    d_prio = [e[2].elapsed_time(e[3]) for e in ev]
+    ms_predict = float(np.mean(d_predict))
+    ms_route = float(np.mean(d_route))
+    ms_prio = float(np.mean(d_prio))
 
     n = wl.n
     flop = mlp_flop_per_stage(spec.dims) * n
@@ -179,7 +262,22 @@ def main():
         },
         "step_ms": {"predict": round(ms_predict, 4), "route": round(ms_route, 4),
                     "prioritize": round(ms_prio, 4)},
+        "phase_ms": {"predict": percentiles(d_predict), "route": percentiles(d_route)},
     }
+    rb = route_bytes(n, spec.n_nodes, spec.k)
+    line["route"] = {
+        "algorithm": "sorted walk" if spec.n_nodes <= 8192 and n >= 4 * spec.n_models else "scan",
+        "stages_per_s": n / (ms_route * 1e-3), "algorithmic_bytes": rb,
+        "achieved_gbs": round(rb / (ms_route * 1e-3) / 1e9, 2), "hbm_frac": round(rb / (ms_route * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "pairs_per_s": n * spec.n_nodes / (ms_route * 1e-3),
+    }
+    if chained:
+        pb = prioritize_bytes(n, wl.n_workflows)
+        line["phase_ms"]["prioritize"] = percentiles(d_prio)
+        line["prioritize"] = {
+            "workflows_per_s": wl.n_workflows / (ms_prio * 1e-3), "algorithmic_bytes": pb,
+            "achieved_gbs": round(pb / (ms_prio * 1e-3) / 1e9, 2), "hbm_frac": round(pb / (ms_prio * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_workflows)
     print(json.dumps(line), flush=True)

@@ -13,10 +13,12 @@
 //     1024-thread block. Each pass: per-tile digit counts (for the first pass, from the chain
 //     kernel); the global offset of every (digit, tile), i.e. the exclusive scan of the count
 //     table in digit-major order, which each scatter block derives itself from the table when
-//     there are few tiles (four threads per digit read it, one memory round trip) and a
-//     separate one-block scan writes otherwise; and a scatter in which each wavefront ranks
-//     its keys digit by digit with ballots (wave multisplit) in input order, so equal digits
-//     keep their relative order.
+//     there are few tiles (four threads per digit read it, one memory round trip); with many
+//     tiles a group scan (prefix of each digit within groups of 256 tiles, in place, plus the
+//     group totals) and a one-block scan over the group totals and the digits prepare it, and
+//     the scatter adds two table entries; and a scatter in which each wavefront ranks its keys
+//     digit by digit with ballots (wave multisplit) in input order, so equal digits keep their
+//     relative order.
 //     The key array is padded to whole tiles with all-ones keys, which always sort last and
 //     never reach the caller's output.
 #include "internal.h"
@@ -24,8 +26,9 @@
 namespace maestro {
 namespace {
 
-constexpr int kTile = 1024;                        // keys per sort tile = threads per block
+constexpr int kTile = 1024;                        // threads per block (and keys per small tile)
 constexpr int kWaves = kTile / 64;
+constexpr int kBigItems = 4;                       // keys per thread in the tiles of large batches
 constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr int kPasses = 32 / kRadixBits;
@@ -55,7 +58,11 @@ __device__ __forceinline__ int64_t sat_sub(int64_t a, int64_t b) {
 constexpr int kChainBatch = 8;                     // stage latencies loaded per round trip
 
 // One block per sort tile, one workflow per thread; also writes the tile's counts of the
-// first digit.
+// first digit. When the block's workflows span at most kStageCap stages (the usual case), the
+// stage latencies pass through LDS: quantised by a coalesced sweep over the block's stage
+// range, summed per chain from LDS, and the remaining times written back by a second coalesced
+// sweep. Longer ranges walk the chains in global memory directly.
+constexpr int kStageCap = 8192;
 __global__ __launch_bounds__(kTile) void chain_kernel(
     int32_t n_workflows, const int64_t* __restrict__ chain_offset,
     const float* __restrict__ stage_latency_s, const int32_t* __restrict__ cursor,
@@ -63,10 +70,19 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
     int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
     uint32_t* __restrict__ counts) {
   __shared__ uint32_t hist[kBuckets];
+  __shared__ int64_t stage_us[kStageCap];
   const int tid = threadIdx.x, tile = blockIdx.x;
   if (tid < kBuckets) hist[tid] = 0;
-  __syncthreads();
   const int64_t w = (int64_t)tile * kTile + tid;
+  // blocks past the last workflow (padding of large batches) have an empty stage range
+  const int64_t w_lo = min((int64_t)n_workflows, (int64_t)tile * kTile);
+  const int64_t w_hi = min((int64_t)n_workflows, (int64_t)tile * kTile + kTile);
+  const int64_t s_lo = chain_offset[w_lo], s_hi = chain_offset[w_hi];   // block-uniform
+  const bool staged = s_hi - s_lo <= kStageCap;
+  if (staged) {
+    for (int64_t j = s_lo + tid; j < s_hi; j += kTile) stage_us[j - s_lo] = latency_us(stage_latency_s[j]);
+  }
+  __syncthreads();
   uint32_t ukey = 0xFFFFFFFFu;   // tile padding: largest key, sorts after every real workflow
   if (w < n_workflows) {
     const int64_t first = chain_offset[w], end = chain_offset[w + 1];
@@ -74,17 +90,25 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
     if (cur < 0) cur = 0;
     const int64_t head = first + cur;
     int64_t suffix = 0, rem_head = 0;
-    for (int64_t top = end - 1; top >= first; top -= kChainBatch) {
-      float lat[kChainBatch];
+    if (staged) {
+      for (int64_t j = end - 1; j >= first; --j) {
+        suffix = sat_add(stage_us[j - s_lo], suffix);
+        stage_us[j - s_lo] = suffix;
+        if (j == head) rem_head = suffix;
+      }
+    } else {
+      for (int64_t top = end - 1; top >= first; top -= kChainBatch) {
+        float lat[kChainBatch];
 #pragma unroll
-      for (int u = 0; u < kChainBatch; ++u) lat[u] = (top - u >= first) ? stage_latency_s[top - u] : 0.0f;
+        for (int u = 0; u < kChainBatch; ++u) lat[u] = (top - u >= first) ? stage_latency_s[top - u] : 0.0f;
 #pragma unroll
-      for (int u = 0; u < kChainBatch; ++u) {
-        const int64_t j = top - u;
-        if (j >= first) {
-          suffix = sat_add(latency_us(lat[u]), suffix);
-          if (remaining_us) remaining_us[j] = suffix;
-          if (j == head) rem_head = suffix;
+        for (int u = 0; u < kChainBatch; ++u) {
+          const int64_t j = top - u;
+          if (j >= first) {
+            suffix = sat_add(latency_us(lat[u]), suffix);
+            if (remaining_us) remaining_us[j] = suffix;
+            if (j == head) rem_head = suffix;
+          }
         }
       }
     }
@@ -103,70 +127,138 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
   vals[w] = (uint32_t)w;
   atomicAdd(&hist[ukey & (kBuckets - 1)], 1u);
   __syncthreads();
-  if (tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
+  if (counts && tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
+  if (staged && remaining_us) {
+    for (int64_t j = s_lo + tid; j < s_hi; j += kTile) remaining_us[j] = stage_us[j - s_lo];
+  }
 }
 
-// Per-tile digit counts of the digit at `shift`.
+// Per-tile digit counts of the digit at `shift`; tiles of kTile * ITEMS keys.
+template <int ITEMS>
 __global__ __launch_bounds__(kTile) void radix_count_kernel(const uint32_t* __restrict__ keys, int shift,
                                                             uint32_t* __restrict__ counts) {
   __shared__ uint32_t hist[kBuckets];
   const int tid = threadIdx.x, tile = blockIdx.x;
   if (tid < kBuckets) hist[tid] = 0;
   __syncthreads();
-  atomicAdd(&hist[(keys[(int64_t)tile * kTile + tid] >> shift) & (kBuckets - 1)], 1u);
+  uint32_t k[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) k[i] = keys[(int64_t)tile * (kTile * ITEMS) + i * kTile + tid];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) atomicAdd(&hist[(k[i] >> shift) & (kBuckets - 1)], 1u);
   __syncthreads();
   if (tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
 }
 
-// Global offsets for many tiles (one workgroup): offsets[t * kBuckets + d] = keys with a
-// smaller digit anywhere, plus keys with digit d in tiles before t -- the exclusive scan of
-// the count table taken in digit-major order.
-__global__ __launch_bounds__(1024) void radix_scan_kernel(const uint32_t* __restrict__ counts, int n_tiles,
-                                                          uint32_t* __restrict__ offsets) {
-  __shared__ uint32_t part[1024];
-  const int tid = threadIdx.x;
-  const int64_t total = (int64_t)kBuckets * n_tiles;
-  const int64_t per = (total + 1023) / 1024;
-  const int64_t lo = min(total, tid * per), hi = min(total, lo + per);
-  // logical index i = d * n_tiles + t lives at t * kBuckets + d
-  auto at = [&](int64_t i) { return (i % n_tiles) * kBuckets + i / n_tiles; };
-  uint32_t s = 0;
-  for (int64_t i = lo; i < hi; ++i) s += counts[at(i)];
-  part[tid] = s;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {   // Hillis-Steele inclusive scan
-    uint32_t v = tid >= off ? part[tid - off] : 0u;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
+// Many tiles, step 1: one block per group of kGroup tiles. In place, counts[t][d] becomes the
+// number of keys with digit d in the tiles of t's group before t; gsum[group][d] gets the
+// group's total. Thread (q, d) runs over the tiles q*kGroup/4 .. of the group for digit d (for
+// a fixed tile, a wavefront's 64 digits are consecutive words).
+constexpr int kGroup = 256;
+constexpr int kBatch = 16;                         // independent loads in flight per thread
+
+// Exclusive prefix, in place, of the column entries t0 .. t1-1 (row stride kBuckets words) of a
+// digit; returns the column total. Loads go out kBatch at a time.
+__device__ __forceinline__ uint32_t column_prefix(uint32_t* __restrict__ table, int64_t t0, int64_t t1, int d,
+                                                  uint32_t start) {
+  uint32_t run = start;
+  for (int64_t t = t0; t < t1; t += kBatch) {
+    uint32_t c[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) c[u] = (t + u < t1) ? table[(t + u) * kBuckets + d] : 0u;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (t + u < t1) {
+        table[(t + u) * kBuckets + d] = run;
+        run += c[u];
+      }
   }
-  uint32_t run = tid ? part[tid - 1] : 0u;
-  for (int64_t i = lo; i < hi; ++i) {
-    const int64_t a = at(i);
-    const uint32_t c = counts[a];
-    offsets[a] = run;
-    run += c;
-  }
+  return run - start;
 }
 
-// Stable scatter of one tile by the digit at `shift`, one key per thread: wavefront w holds
-// tile positions [64w, 64w + 64). out_keys may be null (last pass); positions >= out_limit are
-// padding and are dropped. With kFusedScan the block derives its digit offsets from the count
-// table (digit totals over all tiles, exclusive-scanned, plus the counts of the earlier
-// tiles); otherwise `table` holds the offsets written by radix_scan_kernel.
+__device__ __forceinline__ uint32_t column_sum(const uint32_t* __restrict__ table, int64_t t0, int64_t t1, int d) {
+  uint32_t run = 0;
+  for (int64_t t = t0; t < t1; t += kBatch) {
+    uint32_t c[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) c[u] = (t + u < t1) ? table[(t + u) * kBuckets + d] : 0u;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) run += c[u];
+  }
+  return run;
+}
+
+__global__ __launch_bounds__(1024) void radix_group_scan_kernel(uint32_t* __restrict__ counts, int n_tiles,
+                                                                uint32_t* __restrict__ gsum) {
+  __shared__ uint32_t part[4][kBuckets];
+  const int tid = threadIdx.x, d = tid & (kBuckets - 1), q = tid >> 8;
+  const int t0 = min(n_tiles, blockIdx.x * kGroup + q * (kGroup / 4));
+  const int t1 = min(n_tiles, t0 + kGroup / 4);
+  part[q][d] = column_sum(counts, t0, t1, d);
+  __syncthreads();
+  uint32_t before = 0;
+  for (int i = 0; i < q; ++i) before += part[i][d];
+  column_prefix(counts, t0, t1, d, before);
+  if (q == 0) gsum[(int64_t)blockIdx.x * kBuckets + d] = part[0][d] + part[1][d] + part[2][d] + part[3][d];
+}
+
+// Many tiles, step 2 (one workgroup): gsum[group][d] becomes the global offset of the group's
+// first key with digit d -- keys with a smaller digit anywhere plus keys with digit d in
+// earlier groups.
+__global__ __launch_bounds__(1024) void radix_top_scan_kernel(uint32_t* __restrict__ gsum, int n_groups) {
+  __shared__ uint32_t part[4][kBuckets];
+  __shared__ uint32_t base[kBuckets];
+  const int tid = threadIdx.x, d = tid & (kBuckets - 1), q = tid >> 8;
+  const int per = (n_groups + 3) / 4;
+  const int g0 = min(n_groups, q * per), g1 = min(n_groups, g0 + per);
+  part[q][d] = column_sum(gsum, g0, g1, d);
+  __syncthreads();
+  if (tid < kBuckets) base[tid] = part[0][tid] + part[1][tid] + part[2][tid] + part[3][tid];
+  __syncthreads();
+  for (int off = 1; off < kBuckets; off <<= 1) {   // inclusive scan of the digit totals
+    uint32_t v = 0;
+    if (tid < kBuckets && tid >= off) v = base[tid - off];
+    __syncthreads();
+    if (tid < kBuckets) base[tid] += v;
+    __syncthreads();
+  }
+  const uint32_t total_d = part[0][d] + part[1][d] + part[2][d] + part[3][d];
+  uint32_t off = base[d] - total_d;               // exclusive over digits
+  for (int i = 0; i < q; ++i) off += part[i][d];
+  column_prefix(gsum, g0, g1, d, off);
+}
+
+// Stable scatter of one tile of kTile * ITEMS keys by the digit at `shift`: wavefront w holds
+// tile positions [64 ITEMS w, 64 ITEMS (w + 1)), item i the 64 of them from 64 (ITEMS w + i).
+// out_keys may be null (last pass); positions >= out_limit are padding and are dropped. With
+// kFusedScan (few tiles, one key per thread) the block derives its digit offsets from the count
+// table (digit totals over all tiles, exclusive-scanned, plus the counts of the earlier tiles)
+// and writes each key straight to its place; otherwise `table` holds the in-group prefixes of
+// the group scan and `gtable` the group offsets of the top scan, and the tile is first placed
+// in digit order in LDS so that consecutive threads write consecutive addresses.
 constexpr int kFusedScanMaxTiles = 128;
-template <bool kFusedScan>
+template <bool kFusedScan, int ITEMS>
 __global__ __launch_bounds__(kTile) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, int shift, int n_tiles,
-    const uint32_t* __restrict__ table, uint32_t* __restrict__ out_keys, uint32_t* __restrict__ out_vals,
-    int64_t out_limit) {
+    const uint32_t* __restrict__ table, const uint32_t* __restrict__ gtable, uint32_t* __restrict__ out_keys,
+    uint32_t* __restrict__ out_vals, int64_t out_limit) {
+  static_assert(!kFusedScan || ITEMS == 1, "the fused offsets path handles one key per thread");
+  constexpr int TK = kTile * ITEMS;
+  constexpr int kStage = kFusedScan ? 1 : TK;
   __shared__ uint32_t wcount[kWaves][kBuckets];
   __shared__ uint32_t base[kBuckets];
   __shared__ uint32_t part_before[4][kBuckets], part_total[4][kBuckets];
+  __shared__ uint32_t lbase[kBuckets];                  // tile-local digit counts, then their scan
+  __shared__ uint32_t s_key[kStage], s_val[kStage];     // the tile in digit order
   const int tid = threadIdx.x, tile = blockIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int64_t pos_in = (int64_t)tile * kTile + tid;
-  const uint32_t key = keys[pos_in], val = vals[pos_in];
+  const int64_t t0 = (int64_t)tile * TK + wave * (64 * ITEMS) + lane;
+  uint32_t key[ITEMS], val[ITEMS], dig[ITEMS], rank[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    key[i] = keys[t0 + i * 64];
+    val[i] = vals[t0 + i * 64];
+  }
   for (int i = tid; i < kWaves * kBuckets; i += kTile) (&wcount[0][0])[i] = 0;
 
   if (kFusedScan) {
@@ -203,22 +295,29 @@ __global__ __launch_bounds__(kTile) void radix_scatter_kernel(
       base[tid] = incl - own + part_before[0][tid];
     }
   } else {
-    if (tid < kBuckets) base[tid] = table[(int64_t)tile * kBuckets + tid];
+    if (tid < kBuckets)
+      base[tid] = gtable[(int64_t)(tile / kGroup) * kBuckets + tid] + table[(int64_t)tile * kBuckets + tid];
   }
   __syncthreads();
 
-  // rank among the lanes of this wavefront with the same digit, in lane order
-  const uint32_t d = (key >> shift) & (kBuckets - 1);
-  uint64_t same = ~0ull;
-#pragma unroll
-  for (int b = 0; b < kRadixBits; ++b) {
-    const bool bit = (d >> b) & 1u;
-    const uint64_t ones = __ballot(bit);
-    same &= bit ? ones : ~ones;
-  }
+  // rank among this wavefront's keys with the same digit, in position order: items in order,
+  // lanes in order within an item (the wavefront's own LDS accesses stay in program order)
   const uint64_t lanes_below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const uint32_t rank = (uint32_t)__popcll(same & lanes_below);
-  if ((same & lanes_below) == 0ull) wcount[wave][d] = (uint32_t)__popcll(same);   // first lane of the digit
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const uint32_t d = (key[i] >> shift) & (kBuckets - 1);
+    uint64_t same = ~0ull;
+#pragma unroll
+    for (int b = 0; b < kRadixBits; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t ones = __ballot(bit);
+      same &= bit ? ones : ~ones;
+    }
+    const uint32_t before = wcount[wave][d];
+    dig[i] = d;
+    rank[i] = before + (uint32_t)__popcll(same & lanes_below);
+    if ((same & lanes_below) == 0ull) wcount[wave][d] = before + (uint32_t)__popcll(same);   // first lane of the digit
+  }
   __syncthreads();
   if (tid < kBuckets) {   // offsets of each wavefront inside the tile's digit groups
     uint32_t run = 0;
@@ -228,35 +327,76 @@ __global__ __launch_bounds__(kTile) void radix_scatter_kernel(
       wcount[w][tid] = run;
       run += c;
     }
+    lbase[tid] = run;                       // the tile's count of digit tid, scanned below
   }
   __syncthreads();
-  const int64_t pos = (int64_t)base[d] + wcount[wave][d] + rank;
-  if (pos < out_limit) {
-    if (out_keys) out_keys[pos] = key;
-    out_vals[pos] = val;
+  if (kFusedScan) {   // few tiles: latency-bound, write straight from the ranks
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int64_t pos = (int64_t)base[dig[i]] + wcount[wave][dig[i]] + rank[i];
+      if (pos < out_limit) {
+        if (out_keys) out_keys[pos] = key[i];
+        out_vals[pos] = val[i];
+      }
+    }
+    return;
+  }
+  for (int off = 1; off < kBuckets; off <<= 1) {   // inclusive scan of the tile's digit counts
+    uint32_t v = 0;
+    if (tid < kBuckets && tid >= off) v = lbase[tid - off];
+    __syncthreads();
+    if (tid < kBuckets) lbase[tid] += v;
+    __syncthreads();
+  }
+  // place the tile in digit order in LDS (lbase is now inclusive: digit d starts at
+  // lbase[d - 1]), then write it out
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const uint32_t d = dig[i];
+    const uint32_t lp = (d == 0 ? 0u : lbase[d - 1]) + wcount[wave][d] + rank[i];
+    s_key[lp] = key[i];
+    s_val[lp] = val[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int e = i * kTile + tid;
+    const uint32_t k2 = s_key[e], v2 = s_val[e];
+    const uint32_t d2 = (k2 >> shift) & (kBuckets - 1);
+    const int64_t pos = (int64_t)base[d2] + (e - (d2 == 0 ? 0u : lbase[d2 - 1]));
+    if (pos < out_limit) {
+      if (out_keys) out_keys[pos] = k2;
+      out_vals[pos] = v2;
+    }
   }
 }
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
+// Few workflows (up to kFusedScanMaxTiles tiles of kTile keys): one key per thread, offsets
+// fused into the scatter. More: tiles of kTile * kBigItems keys and the group/top scans.
 struct PrioLayout {
-  int64_t n_tiles, padded;
-  size_t keys_a, vals_a, keys_b, vals_b, counts, offsets, total;
+  bool fused;
+  int64_t tile_keys, n_tiles, n_groups, padded;
+  size_t keys_a, vals_a, keys_b, vals_b, counts, gsum, total;
 };
 
 PrioLayout prio_layout(int32_t n_workflows) {
   PrioLayout L{};
-  L.n_tiles = ((int64_t)n_workflows + kTile - 1) / kTile;
-  L.padded = L.n_tiles * kTile;
+  L.fused = ((int64_t)n_workflows + kTile - 1) / kTile <= kFusedScanMaxTiles;
+  L.tile_keys = L.fused ? kTile : (int64_t)kTile * kBigItems;
+  L.n_tiles = ((int64_t)n_workflows + L.tile_keys - 1) / L.tile_keys;
+  L.padded = L.n_tiles * L.tile_keys;
   const size_t kb = align256(sizeof(uint32_t) * (size_t)L.padded);
   const size_t cb = align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_tiles);
+  L.n_groups = (L.n_tiles + kGroup - 1) / kGroup;
   L.keys_a = 0;
   L.vals_a = L.keys_a + kb;
   L.keys_b = L.vals_a + kb;
   L.vals_b = L.keys_b + kb;
   L.counts = L.vals_b + kb;
-  L.offsets = L.counts + cb;
-  L.total = L.offsets + (L.n_tiles > kFusedScanMaxTiles ? cb : 0);
+  L.gsum = L.counts + cb;
+  L.total = L.gsum + (L.fused ? 0 : align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_groups));
   return L;
 }
 
@@ -278,29 +418,33 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
   uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(ws + L.keys_a), reinterpret_cast<uint32_t*>(ws + L.keys_b)};
   uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(ws + L.vals_a), reinterpret_cast<uint32_t*>(ws + L.vals_b)};
   uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.counts);
-  uint32_t* offsets = reinterpret_cast<uint32_t*>(ws + L.offsets);
+  uint32_t* gsum = reinterpret_cast<uint32_t*>(ws + L.gsum);
 
   const int nt = (int)L.n_tiles;
-  const bool fused = nt <= kFusedScanMaxTiles;
-  chain_kernel<<<dim3((unsigned)nt), dim3(kTile), 0, stream>>>(
+  // the chain kernel covers the padded range in blocks of kTile workflows; with small tiles
+  // (block = tile) it also counts the first digit
+  chain_kernel<<<dim3((unsigned)(L.padded / kTile)), dim3(kTile), 0, stream>>>(
       n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us,
-      slack_key, keys[0], vals[0], counts);
+      slack_key, keys[0], vals[0], L.fused ? counts : nullptr);
   for (int pass = 0; pass < kPasses; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     const int shift = pass * kRadixBits;
     const bool last = pass + 1 == kPasses;
-    if (pass > 0)   // the chain kernel counted the first digit
-      radix_count_kernel<<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
     uint32_t* out_k = last ? nullptr : keys[dst];
     uint32_t* out_v = last ? reinterpret_cast<uint32_t*>(order) : vals[dst];
     const int64_t limit = last ? (int64_t)n_workflows : L.padded;
-    if (fused) {
-      radix_scatter_kernel<true><<<dim3(nt), dim3(kTile), 0, stream>>>(
-          keys[src], vals[src], shift, nt, counts, out_k, out_v, limit);
+    if (L.fused) {
+      if (pass > 0)
+        radix_count_kernel<1><<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
+      radix_scatter_kernel<true, 1><<<dim3(nt), dim3(kTile), 0, stream>>>(
+          keys[src], vals[src], shift, nt, counts, nullptr, out_k, out_v, limit);
     } else {
-      radix_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(counts, nt, offsets);
-      radix_scatter_kernel<false><<<dim3(nt), dim3(kTile), 0, stream>>>(
-          keys[src], vals[src], shift, nt, offsets, out_k, out_v, limit);
+      const int ng = (int)L.n_groups;
+      radix_count_kernel<kBigItems><<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
+      radix_group_scan_kernel<<<dim3(ng), dim3(1024), 0, stream>>>(counts, nt, gsum);
+      radix_top_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(gsum, ng);
+      radix_scatter_kernel<false, kBigItems><<<dim3(nt), dim3(kTile), 0, stream>>>(
+          keys[src], vals[src], shift, nt, counts, gsum, out_k, out_v, limit);
     }
   }
   return launch_status();

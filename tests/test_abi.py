@@ -112,9 +112,11 @@ def test_prioritize_validation_and_workspace(lib):
     assert ws == 4 * 4 * tiles * 1024 + 4 * 256 * tiles
     assert lib.maestro_prioritize_workspace(0, 0) == 0
     assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 1024 + 4 * 256
-    # beyond 128 tiles the scatter reads a separately scanned offset table of the same size
-    tiles = (200000 + 1023) // 1024
-    assert lib.maestro_prioritize_workspace(200000, 10**6) == 4 * 4 * tiles * 1024 + 2 * 4 * 256 * tiles
+    # beyond 128 such tiles: 4096-key tiles, plus a 256-entry offset table per group of 256 tiles
+    tiles = (200000 + 4095) // 4096
+    assert lib.maestro_prioritize_workspace(200000, 10**6) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256
+    tiles = (1 << 26) // 4096
+    assert lib.maestro_prioritize_workspace(1 << 26, 0) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256 * (tiles // 256)
     call = lambda W=4, S=8, off=FAKE, ws=FAKE, ws_bytes=1 << 20: lib.maestro_prioritize(
         W, S, off, FAKE, None, FAKE, 0, None, FAKE, FAKE, ws, ws_bytes, None)
     assert call(W=-1) == INVALID

@@ -276,7 +276,7 @@ def test_c3_full_step_matches_oracle():
     print(f"c3: W={w.n_workflows} S={w.n}: route + order identical")
 
 
-@pytest.mark.parametrize("W_", [1, 5, 1023, 1024, 1025, 4097, 131072, 131073, 1 << 20])
+@pytest.mark.parametrize("W_", [1, 5, 1023, 1024, 1025, 4097, 131072, 131073, 300001, 1 << 20, (1 << 22) + 3])
 def test_prioritize_random_chains(W_):
     rng = np.random.default_rng(W_)
     lens = rng.integers(0, 9, W_)
@@ -324,6 +324,29 @@ def test_route_sorted_rejects_too_many_nodes():
     assert e.value.status == 2
     got, ref = gpu_route(w, pred, kv)            # auto falls back to the scan
     assert_route_equal(got, ref)
+
+
+def test_prioritize_mixed_staging():
+    # 1024-workflow blocks whose stage ranges sit exactly at, below and above the 8192-stage
+    # LDS staging capacity, in one batch: blocks walk their chains through LDS or in global
+    # memory independently
+    rng = np.random.default_rng(17)
+    lens = np.concatenate([
+        np.full(1024, 8),                                     # 8192 stages: at the capacity
+        np.concatenate([[5000], np.full(1023, 3)]),          # 8069: below
+        np.concatenate([[9000], np.zeros(1023, np.int64)]),  # 9000: above, one long chain
+        rng.integers(0, 9, 777),                              # partial last block
+    ]).astype(np.int64)
+    W_ = lens.size
+    off = np.zeros(W_ + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    S = int(off[-1])
+    lat = rng.uniform(0.0, 30.0, S).astype(np.float32)
+    lat[rng.random(S) < 0.002] = np.inf
+    dl = rng.integers(0, 720 * 10 ** 6, W_).astype(np.int64)
+    cur = rng.integers(0, 4, W_).astype(np.int32)
+    got = gpu_prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur)
+    assert_prio_equal(got, oracle.prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur))
 
 
 def test_prioritize_long_chain_and_empty():
