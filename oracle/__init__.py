@@ -12,6 +12,12 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
   route      - pinned: brute force via numpy lexsort on tiny inputs, invariants (feasible,
                sorted, nothing better left out), degenerate cases, node-permutation
                equivariance.
+  route_fitness - pinned (tests/test_oracle_fitness_pins.py): limiting weights reduce Eq. 5 to
+               one metric whose argmax is a plain argmin (nearest node by RTT, best-fit packing,
+               minimum time-to-start, minimum disruption), clipping at the window bounds and
+               degenerate windows, infeasible padding, top-k order and tie-break, per-class
+               weights, node-permutation equivariance.
+  quantiles  - pinned: numpy's percentile selection ("lower" / "higher" methods).
   prioritize - pinned: closed forms (unit latencies), numpy stable argsort, O(len^2) suffix
                sums, half-even rounding cases, int32 clamping, non-finite latency handling.
 """
@@ -55,6 +61,11 @@ def _load():
     lib.oracle_predict.restype = ctypes.c_int
     lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
+    lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
+                                         f64, i32, P, P, i32]
+    lib.oracle_route_fitness.restype = ctypes.c_int
+    lib.oracle_quantiles.argtypes = [P, i64, f64, f64, P]
+    lib.oracle_quantiles.restype = ctypes.c_int
     lib.oracle_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P]
     lib.oracle_prioritize.restype = ctypes.c_int
     lib.oracle_round_bf16.argtypes = [f64]
@@ -137,6 +148,44 @@ def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s,
     if st != 0:
         raise RuntimeError(f"oracle_route failed with status {st}")
     return idx, sc
+
+
+def route_fitness(model_id, src_id, class_id, kv_bytes, free_bytes, queue_ms, act_ms, resident_mask,
+                  deg_ms, rtt_ms, class_weights, bounds, k: int = 1, rho: float = 0.0, n_models: int = 0,
+                  n_threads: int = 0):
+    """Alg. 3 with the fitness of Eq. 5. rtt_ms [n_src][M]; class_weights [n_classes][3] =
+    (gamma, lambda, mu); bounds [6] = window bounds (lo, hi) of RTT, T_ready, C_deg. Returns
+    (node_idx int32 [N][k], fitness float32 [N][k])."""
+    lib = _load()
+    mi = _c(model_id, np.int32)
+    n = mi.shape[0]
+    si, ci = _c(src_id, np.int32), _c(class_id, np.int32)
+    kv = _c(kv_bytes, np.float64)
+    fr, q, act = _c(free_bytes, np.float64), _c(queue_ms, np.float32), _c(act_ms, np.float32)
+    rm, dg = _c(resident_mask, np.uint64), _c(deg_ms, np.float32)
+    rtt = _c(rtt_ms, np.float32)
+    cw, bd = _c(class_weights, np.float32), _c(bounds, np.float32)
+    M = fr.shape[0]
+    idx = np.empty((n, k), np.int32)
+    fit = np.empty((n, k), np.float32)
+    st = lib.oracle_route_fitness(n, _ptr(mi), _ptr(si), _ptr(ci), _ptr(kv), n_models or 64, M,
+                                  rtt.shape[0], cw.shape[0], _ptr(fr), _ptr(q), _ptr(act), _ptr(rm),
+                                  _ptr(dg), _ptr(rtt), _ptr(cw), _ptr(bd), float(rho), int(k),
+                                  _ptr(idx), _ptr(fit), n_threads or max_threads())
+    if st != 0:
+        raise RuntimeError(f"oracle_route_fitness failed with status {st}")
+    return idx, fit
+
+
+def quantiles(values, q_lo: float = 0.05, q_hi: float = 0.95):
+    """Window bounds: the order statistics of rank floor(q_lo (m-1)) and ceil(q_hi (m-1))."""
+    lib = _load()
+    v = _c(values, np.float32).reshape(-1)
+    out = np.empty(2, np.float32)
+    st = lib.oracle_quantiles(_ptr(v), v.shape[0], float(q_lo), float(q_hi), _ptr(out))
+    if st != 0:
+        raise RuntimeError(f"oracle_quantiles failed with status {st}")
+    return out
 
 
 def prioritize(chain_offset, stage_latency_s, deadline_us, now_us: int, cursor=None):

@@ -20,6 +20,12 @@
  *                (Eq. 6 plus the decode term of Eq. 2, RTT = eta = 0), and return the k
  *                smallest (score, node index) pairs in lexicographic order. The strict ">" of
  *                Alg. 3 keeps the first of equal scores, i.e. the lowest index.
+ *   fitness    : Alg. 3 with the fitness of Eq. 5: among the feasible nodes, the largest
+ *                S = A - lambda T_ready - mu C_deg, A = gamma (1 - norm RTT) + (1 - gamma) fit,
+ *                fit = R_need / headroom (best fit), T_ready = T_q + T_act (Eq. 6), each metric
+ *                min-max normalised onto [0, 1] with window bounds and clipped; float32 in a
+ *                fixed operation order; k best (fitness, lowest index).
+ *   quantiles  : the window bounds, as exact order statistics of a sample.
  *   prioritize : per-stage latency quantised to integer microseconds, suffix sums along each
  *                workflow chain (Eq. 7 with the future term taken as the sum of the later
  *                stages' predicted latencies), slack = deadline - now - remaining, clamped to
@@ -214,6 +220,126 @@ int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
     free(taken);
   }
   return status;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* route by fitness: Eq. 5 over the feasible nodes, Alg. 3 (argmax with strict ">")            */
+/* ------------------------------------------------------------------------------------------ */
+
+/* robust min-max normalisation onto [0, 1] with window bounds lo, hi (values outside the
+ * bounds clip); a degenerate window (hi <= lo) maps everything to 0. float32 throughout. */
+static float norm_inv(float lo, float hi) { return hi > lo ? 1.0f / (hi - lo) : 0.0f; }
+static float norm01(float x, float lo, float inv) {
+  float t = (x - lo) * inv;
+  if (t < 0.0f) t = 0.0f;
+  if (t > 1.0f) t = 1.0f;
+  return t;
+}
+
+typedef struct { float s; int32_t n; } fcand_t;
+/* larger fitness first; equal fitness: lower node index first (the strict ">" of Alg. 3) */
+static int fcand_better(fcand_t a, fcand_t b) { return a.s > b.s || (a.s == b.s && a.n < b.n); }
+
+int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
+                         const int32_t* class_id, const double* kv_bytes, int32_t n_models,
+                         int32_t n_nodes, int32_t n_src, int32_t n_classes,
+                         const double* free_bytes, const float* queue_ms, const float* act_ms,
+                         const uint64_t* resident_mask, const float* deg_ms, const float* rtt_ms,
+                         const float* class_weights, const float* bounds, double rho, int32_t k,
+                         int32_t* node_idx, float* fitness, int32_t n_threads) {
+  if (n < 0 || n_nodes < 1 || n_models < 1 || n_models > 64 || n_src < 1 || n_classes < 1 ||
+      k < 1 || rho < 0.0)
+    return ORACLE_BAD_ARG;
+  int status = ORACLE_OK;
+  if (n_threads < 1) n_threads = 1;
+  /* window bounds of the three normalised metrics: RTT, T_ready, C_deg (milliseconds) */
+  const float inv_rtt = norm_inv(bounds[0], bounds[1]);
+  const float inv_ready = norm_inv(bounds[2], bounds[3]);
+  const float inv_deg = norm_inv(bounds[4], bounds[5]);
+
+#pragma omp parallel num_threads(n_threads)
+  {
+    fcand_t* c = (fcand_t*)malloc(sizeof(fcand_t) * (size_t)n_nodes);
+    unsigned char* taken = (unsigned char*)malloc((size_t)n_nodes);
+    if (!c || !taken) {
+#pragma omp atomic write
+      status = ORACLE_NO_MEM;
+    } else {
+#pragma omp for schedule(static)
+      for (int64_t i = 0; i < n; ++i) {
+        const int32_t m = model_id[i];
+        /* R_need = (1 + rho) * R_kv */
+        const double need = (rho == 0.0) ? kv_bytes[i] : kv_bytes[i] * (1.0 + rho);
+        /* GetWeights(T.class): network weight gamma, lambda (T_ready), mu (C_deg) */
+        const float* wt = class_weights + 3 * (size_t)class_id[i];
+        const float gamma = wt[0], lambda = wt[1], mu = wt[2];
+        const float* rtt_row = rtt_ms + (size_t)src_id[i] * (size_t)n_nodes;
+        const float needf = (float)need;
+        int32_t nc = 0;
+        for (int32_t nd = 0; nd < n_nodes; ++nd) {
+          if (need > free_bytes[nd]) continue;              /* FilterByPolicyAndFeasibility */
+          /* Affinity: network proximity (decreasing in the normalised RTT) and best fit of
+           * R_need to the node's headroom (1 when the stage fills the headroom exactly) */
+          const float prox = 1.0f - norm01(rtt_row[nd], bounds[0], inv_rtt);
+          const float freef = (float)free_bytes[nd];
+          float fit = freef > 0.0f ? needf * (1.0f / freef) : 1.0f;
+          if (fit > 1.0f) fit = 1.0f;
+          const float a = gamma * prox + (1.0f - gamma) * fit;
+          /* RuntimeEstimate: T_ready = T_q + T_act (Eq. 6), C_deg as reported */
+          const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
+          const float ready = queue_ms[nd] + (resident ? 0.0f : act_ms[nd]);
+          /* Eq. 5: S = A - lambda * T_ready - mu * C_deg, on normalised metrics */
+          const float s = (a - lambda * norm01(ready, bounds[2], inv_ready)) - mu * norm01(deg_ms[nd], bounds[4], inv_deg);
+          c[nc].s = s;
+          c[nc].n = nd;
+          ++nc;
+        }
+        /* the k best (fitness, index) pairs: largest fitness, then lowest index */
+        memset(taken, 0, (size_t)nc);
+        for (int32_t r = 0; r < k; ++r) {
+          int32_t best = -1;
+          for (int32_t j = 0; j < nc; ++j)
+            if (!taken[j] && (best < 0 || fcand_better(c[j], c[best]))) best = j;
+          if (best >= 0) {
+            taken[best] = 1;
+            node_idx[i * k + r] = c[best].n;
+            fitness[i * k + r] = c[best].s;
+          } else {
+            node_idx[i * k + r] = -1;
+            fitness[i * k + r] = -INFINITY;
+          }
+        }
+      }
+    }
+    free(c);
+    free(taken);
+  }
+  return status;
+}
+
+/* Window bounds of the robust normalisation: the order statistics of rank floor(q_lo (m-1))
+ * and ceil(q_hi (m-1)) of m finite values (no interpolation). */
+static int float_cmp(const void* pa, const void* pb) {
+  const float a = *(const float*)pa, b = *(const float*)pb;
+  if (a < b) return -1;
+  if (a > b) return 1;
+  /* -0 before +0, so that the order is total on bit patterns */
+  const int sa = signbit(a) ? 1 : 0, sb = signbit(b) ? 1 : 0;
+  return sb - sa;
+}
+
+int oracle_quantiles(const float* values, int64_t m, double q_lo, double q_hi, float* out) {
+  if (m < 1 || !(q_lo >= 0.0 && q_lo <= q_hi && q_hi <= 1.0)) return ORACLE_BAD_ARG;
+  float* v = (float*)malloc(sizeof(float) * (size_t)m);
+  if (!v) return ORACLE_NO_MEM;
+  memcpy(v, values, sizeof(float) * (size_t)m);
+  qsort(v, (size_t)m, sizeof(float), float_cmp);
+  const int64_t i_lo = (int64_t)floor(q_lo * (double)(m - 1));
+  const int64_t i_hi = (int64_t)ceil(q_hi * (double)(m - 1));
+  out[0] = v[i_lo];
+  out[1] = v[i_hi];
+  free(v);
+  return ORACLE_OK;
 }
 
 /* ------------------------------------------------------------------------------------------ */
