@@ -9,6 +9,10 @@
  *                      headroom cannot admit R_need = (1 + rho) * R_kv, score the rest by
  *                      expected completion latency T_q + T_act + t_dec(M) * L (Eq. 6 and the
  *                      decode term of Eq. 2), keep the best k (lowest index on equal scores).
+ *   maestro_route_fitness  the same filter, then the node of largest fitness S = A - lambda
+ *                      T_ready - mu C_deg (Eq. 5): affinity from network proximity and best fit
+ *                      of R_need to the headroom, each metric normalised with window bounds
+ *                      (maestro_quantiles computes them).
  *   maestro_prioritize remaining-time queue ordering (Sec. III-D, Eq. 7): remaining
  *                      predicted latency along each workflow chain, slack against the
  *                      workflow deadline, stable ascending order of workflows by slack.
@@ -135,6 +139,52 @@ MAESTRO_API maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, 
                              const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
                              int32_t* node_idx, float* score,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Routing by fitness (Sec. III-D: Eq. 5 with T_ready of Eq. 6; Alg. 3). Per stage i with
+ * model m = model_id[i], source s = src_id[i] and weights (gamma, lambda, mu) =
+ * class_weights[class_id[i]] (GetWeights of Alg. 3):
+ *   need  = rho == 0 ? kv_bytes[i] : kv_bytes[i] * (1 + rho)       (float64)
+ *   node j is feasible iff need <= free_bytes[j]                     (equality admits)
+ *   norm_X(x) = clamp((x - lo_X) * inv_X, 0, 1), inv_X = hi_X > lo_X ? 1 / (hi_X - lo_X) : 0,
+ *               with (lo_X, hi_X) the window bounds of metric X (see maestro_quantiles)
+ *   prox  = 1 - norm_RTT(rtt_ms[s][j])                    network proximity
+ *   fit   = min(1, fl32(need) * (1 / fl32(free_bytes[j])))   best fit of R_need to the headroom
+ *           (1 when fl32(free_bytes[j]) == 0)
+ *   A     = gamma * prox + (1 - gamma) * fit               affinity
+ *   T_ready = queue_ms[j] + (bit m of resident_mask[j] ? 0 : act_ms[j])
+ *   S     = (A - lambda * norm_READY(T_ready)) - mu * norm_DEG(deg_ms[j])
+ *   every operation float32 round-to-nearest, in exactly this order; output the k feasible
+ *   nodes with the largest S, the lower node index first on equal S (the strict ">" of Alg.
+ *   3); when fewer than k nodes are feasible the tail is padded with node -1 and -inf.
+ *   model_id, src_id, class_id [n] int32: in [0, n_models), [0, n_src), [0, n_classes);
+ *                              1 <= n_models <= 64, 1 <= n_src <= 16, 1 <= n_classes <= 16
+ *   kv_bytes            [n] float64 R_kv (from maestro_predict)
+ *   free_bytes          [n_nodes] float64: KV admission headroom R_head (bytes)
+ *   queue_ms, act_ms    [n_nodes] float32: queueing delay T_q, activation latency T_act (ms)
+ *   resident_mask       [n_nodes] uint64: bit m set <=> model m is warm on the node
+ *   deg_ms              [n_nodes] float32: disruption penalty C_deg reported by the runtime (ms)
+ *   rtt_ms              [n_src][n_nodes] float32: round-trip time from each source (ms)
+ *   class_weights       [n_classes][3] float32: (gamma, lambda, mu) per stage class
+ *   bounds              [6] float32: (lo, hi) of RTT, T_ready, C_deg, in that order
+ *   rho >= 0            safety margin;  1 <= k <= 16 route width
+ *   node_idx  (out)     [n][k] int32;  fitness (out) [n][k] float32
+ * All device arrays; inputs finite. No workspace. */
+MAESTRO_API maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
+                             const int32_t* class_id, const double* kv_bytes, int32_t n_models,
+                             int32_t n_nodes, int32_t n_src, int32_t n_classes,
+                             const double* free_bytes, const float* queue_ms, const float* act_ms,
+                             const uint64_t* resident_mask, const float* deg_ms, const float* rtt_ms,
+                             const float* class_weights, const float* bounds, double rho, int32_t k,
+                             int32_t* node_idx, float* fitness, void* stream);
+
+/* Window bounds of the robust normalisation in Eq. 5 (per-metric 5th/95th percentiles of a
+ * recent window): out[0] and out[1] (device, float32) receive the values of rank
+ * floor(q_lo * (m - 1)) and ceil(q_hi * (m - 1)) of values[0 .. m-1] (device, finite), ranks
+ * counted from 0 in ascending order of the float values (-0 before +0); no interpolation.
+ * 0 <= q_lo <= q_hi <= 1, 1 <= m < 2^32. One workgroup; meant for windows of up to a few
+ * million values. No workspace. */
+MAESTRO_API maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi,
+                             float* out, void* stream);
 
 /* Slack ordering of n_workflows workflow chains over n_stages stages (Sec. III-D, Eq. 7).
  *   chain_offset        [n_workflows + 1] int64, chain_offset[0] = 0, non-decreasing,

@@ -21,9 +21,9 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
            4: "kernel launch failed"}
 
 # Every function declared in include/maestro.h.
-EXPORTS = ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize",
-           "maestro_predict_workspace", "maestro_route_workspace", "maestro_prioritize_workspace",
-           "maestro_status_string")
+EXPORTS = ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
+           "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
+           "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
 
@@ -57,6 +57,9 @@ def load():
     lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
+    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
+                                          f64, i32, P, P, P]
+    lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
     for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize"):
         getattr(lib, f).restype = ctypes.c_int
@@ -193,6 +196,68 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
                               _stream(stream))
     _check("maestro_route_ex", st)
     return idx, sc
+
+
+def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.Tensor,
+                  kv_bytes: torch.Tensor, free_bytes: torch.Tensor, queue_ms: torch.Tensor,
+                  act_ms: torch.Tensor, resident_mask: torch.Tensor, deg_ms: torch.Tensor,
+                  rtt_ms: torch.Tensor, class_weights: torch.Tensor, bounds: torch.Tensor,
+                  n_models: int, k: int = 1, rho: float = 0.0,
+                  out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                  stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_route_fitness: returns (node_idx int32 [N][k], fitness float32 [N][k]).
+
+    ``rtt_ms`` is [n_src][n_nodes], ``class_weights`` [n_classes][3] = (gamma, lambda, mu),
+    ``bounds`` [6] = (lo, hi) of RTT, T_ready, C_deg; ``resident_mask`` is int64 on the torch
+    side (same bits as the C-ABI's uint64)."""
+    lib = load()
+    _dev(model_id, "model_id", torch.int32)
+    n = model_id.shape[0]
+    _dev(src_id, "src_id", torch.int32)
+    _dev(class_id, "class_id", torch.int32)
+    _dev(kv_bytes, "kv_bytes", torch.float64)
+    _dev(free_bytes, "free_bytes", torch.float64)
+    for t, name in ((queue_ms, "queue_ms"), (act_ms, "act_ms"), (deg_ms, "deg_ms"), (rtt_ms, "rtt_ms"),
+                    (class_weights, "class_weights"), (bounds, "bounds")):
+        _dev(t, name, torch.float32)
+    _dev(resident_mask, "resident_mask", torch.int64)
+    M = free_bytes.shape[0]
+    if src_id.shape[0] != n or class_id.shape[0] != n or kv_bytes.shape[0] != n:
+        raise ValueError("per-stage inputs must have the same length")
+    if queue_ms.shape[0] != M or act_ms.shape[0] != M or resident_mask.shape[0] != M or deg_ms.shape[0] != M:
+        raise ValueError("per-node inputs must have the same length")
+    if rtt_ms.dim() != 2 or rtt_ms.shape[1] != M:
+        raise ValueError("rtt_ms must be [n_src][n_nodes]")
+    if class_weights.dim() != 2 or class_weights.shape[1] != 3 or bounds.numel() != 6:
+        raise ValueError("class_weights must be [n_classes][3] and bounds hold 6 values")
+    if out is None:
+        out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
+               torch.empty((n, k), dtype=torch.float32, device=model_id.device))
+    idx, fit = out
+    _dev(idx, "node_idx", torch.int32)
+    _dev(fit, "fitness", torch.float32)
+    st = lib.maestro_route_fitness(n, _ptr(model_id), _ptr(src_id), _ptr(class_id), _ptr(kv_bytes),
+                                   int(n_models), M, rtt_ms.shape[0], class_weights.shape[0],
+                                   _ptr(free_bytes), _ptr(queue_ms), _ptr(act_ms), _ptr(resident_mask),
+                                   _ptr(deg_ms), _ptr(rtt_ms), _ptr(class_weights), _ptr(bounds),
+                                   float(rho), int(k), _ptr(idx), _ptr(fit), _stream(stream))
+    _check("maestro_route_fitness", st)
+    return idx, fit
+
+
+def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,
+              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """maestro_quantiles: float32 [2] on the device = the order statistics of rank
+    floor(q_lo (m-1)) and ceil(q_hi (m-1)) of ``values``."""
+    lib = load()
+    _dev(values, "values", torch.float32)
+    if out is None:
+        out = torch.empty(2, dtype=torch.float32, device=values.device)
+    _dev(out, "out", torch.float32)
+    st = lib.maestro_quantiles(_ptr(values), values.numel(), float(q_lo), float(q_hi), _ptr(out),
+                               _stream(stream))
+    _check("maestro_quantiles", st)
+    return out
 
 
 def route_workspace_bytes(n: int, n_models: int, n_nodes: int, k: int) -> int:

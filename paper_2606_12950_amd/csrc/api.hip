@@ -1,5 +1,7 @@
 // C-ABI entry points of libmaestro: host-side argument checks, then the kernel launchers.
 // Nothing here touches device memory; every check happens before the first launch.
+#include <math.h>
+
 #include "internal.h"
 
 namespace {
@@ -105,6 +107,52 @@ maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pr
   return maestro_route_ex(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes,
                           free_bytes, queue_s, cold_s, resident_mask, rho, k, MAESTRO_ROUTE_AUTO,
                           node_idx, score, workspace, workspace_bytes, stream);
+}
+
+maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
+                                     const int32_t* class_id, const double* kv_bytes,
+                                     int32_t n_models, int32_t n_nodes, int32_t n_src,
+                                     int32_t n_classes, const double* free_bytes,
+                                     const float* queue_ms, const float* act_ms,
+                                     const uint64_t* resident_mask, const float* deg_ms,
+                                     const float* rtt_ms, const float* class_weights,
+                                     const float* bounds, double rho, int32_t k, int32_t* node_idx,
+                                     float* fitness, void* stream) {
+  if (n < 0 || n_models < 1 || n_models > 64 || n_nodes < 1 || k < 1 || k > 16)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n_src < 1 || n_src > maestro::kMaxFitnessSources || n_classes < 1 ||
+      n_classes > maestro::kMaxFitnessClasses)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
+  if (!free_bytes || !queue_ms || !act_ms || !resident_mask || !deg_ms || !rtt_ms || !class_weights ||
+      !bounds)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(free_bytes, 8) || !aligned(queue_ms, 4) || !aligned(act_ms, 4) ||
+      !aligned(resident_mask, 8) || !aligned(deg_ms, 4) || !aligned(rtt_ms, 4) ||
+      !aligned(class_weights, 4) || !aligned(bounds, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!model_id || !src_id || !class_id || !kv_bytes || !node_idx || !fitness)
+      return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(model_id, 4) || !aligned(src_id, 4) || !aligned(class_id, 4) ||
+        !aligned(kv_bytes, 8) || !aligned(node_idx, 4) || !aligned(fitness, 4))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
+  return maestro::launch_route_fitness(n, model_id, src_id, class_id, kv_bytes, n_nodes, n_src,
+                                       free_bytes, queue_ms, act_ms, resident_mask, deg_ms, rtt_ms,
+                                       class_weights, bounds, rho, k, node_idx, fitness,
+                                       as_stream(stream));
+}
+
+maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi, float* out,
+                                 void* stream) {
+  if (m < 1 || !(q_lo >= 0.0) || !(q_lo <= q_hi) || !(q_hi <= 1.0)) return MAESTRO_ERR_INVALID_ARG;
+  if (!values || !out || !aligned(values, 4) || !aligned(out, 4)) return MAESTRO_ERR_INVALID_ARG;
+  if (m > (int64_t)UINT32_MAX) return MAESTRO_ERR_UNSUPPORTED;
+  const int64_t r_lo = (int64_t)floor(q_lo * (double)(m - 1));
+  const int64_t r_hi = (int64_t)ceil(q_hi * (double)(m - 1));
+  return maestro::launch_quantiles(values, m, r_lo, r_hi, out, as_stream(stream));
 }
 
 maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,

@@ -1,0 +1,208 @@
+// Routing by fitness (Sec. III-D, Eq. 5 with Eq. 6; Alg. 3) and the window bounds of its robust
+// normalisation.
+//
+// For every stage, among the nodes whose headroom admits R_need = (1 + rho) R_kv, the largest
+//   S = A - lambda * norm(T_ready) - mu * norm(C_deg),
+//   A = gamma * (1 - norm(RTT(src, node))) + (1 - gamma) * R_need / headroom,
+//   T_ready = T_q + T_act (T_act = 0 when the stage's model is resident),
+// with the class weights (gamma, lambda, mu) of the stage and norm(x) = clamp((x - lo) / (hi - lo),
+// 0, 1) over window bounds (lo, hi) per metric (a degenerate window normalises to 0). The k best
+// (fitness, node) pairs are kept, larger fitness first and the lower index on equal fitness
+// (the strict ">" of Alg. 3).
+//
+// A workgroup takes 256 stages (one per thread) and stages node state chunk by chunk in LDS,
+// with everything that depends on the node alone already normalised: headroom, its float32
+// reciprocal, normalised T_ready with and without activation, normalised C_deg, and
+// 1 - normalised RTT from every source. A pair then costs the feasibility test, one product for
+// the fit and the four products/sums of Eq. 5. Every operation is float32 round-to-nearest in a
+// fixed order (explicit intrinsics, no contraction), so the fitness values are reproducible bit
+// for bit by a sequential evaluation of the same expression.
+//
+// The window bounds are exact order statistics of a sample (no interpolation): one workgroup
+// radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
+#include "internal.h"
+#include "select.h"
+
+namespace maestro {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kChunk = 512;              // nodes staged in LDS at a time
+constexpr int kProxStride = kChunk + 1;  // one-word pad: rows of different sources in different banks
+
+__device__ __forceinline__ float norm_inv(float lo, float hi) {
+  return hi > lo ? __fdiv_rn(1.0f, __fsub_rn(hi, lo)) : 0.0f;
+}
+__device__ __forceinline__ float norm01(float x, float lo, float inv) {
+  float t = __fmul_rn(__fsub_rn(x, lo), inv);
+  if (t < 0.0f) t = 0.0f;
+  if (t > 1.0f) t = 1.0f;
+  return t;
+}
+
+template <int KT>
+__global__ __launch_bounds__(kThreads) void fitness_kernel(
+    int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
+    const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_nodes,
+    int32_t n_src, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
+    const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
+    const float* __restrict__ deg_ms, const float* __restrict__ rtt_ms,
+    const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
+    int32_t* __restrict__ node_idx, float* __restrict__ fitness) {
+  __shared__ double s_free[kChunk];               // KV admission headroom
+  __shared__ float s_inv[kChunk];                 // 1 / fl32(headroom); -1 when that is 0 (fit = 1)
+  __shared__ float s_warm[kChunk];                // norm(T_q): model resident
+  __shared__ float s_cold[kChunk];                // norm(T_q + T_act)
+  __shared__ float s_deg[kChunk];                 // norm(C_deg)
+  __shared__ uint64_t s_mask[kChunk];             // residency bits
+  __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
+
+  const int tid = threadIdx.x;
+  const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
+  const bool valid = stage < n;
+  const float lo_r = bounds[0], lo_t = bounds[2], lo_d = bounds[4];
+  const float inv_r = norm_inv(bounds[0], bounds[1]);
+  const float inv_t = norm_inv(bounds[2], bounds[3]);
+  const float inv_d = norm_inv(bounds[4], bounds[5]);
+
+  double need = INFINITY;   // an invalid lane admits nothing
+  float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
+  uint64_t mbit = 0;
+  int src = 0;
+  if (valid) {
+    need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
+    needf = __double2float_rn(need);
+    const float* wt = class_weights + 3 * class_id[stage];
+    gamma = wt[0];
+    lambda = wt[1];
+    mu = wt[2];
+    omg = __fsub_rn(1.0f, gamma);
+    mbit = (uint64_t)1 << model_id[stage];
+    src = src_id[stage];
+  }
+  const float* prox_row = s_prox + src * kProxStride;
+
+  TopK<KT> best;   // keys are -fitness: the smallest key is the best node
+  best.init();
+  for (int32_t c0 = 0; c0 < n_nodes; c0 += kChunk) {
+    const int cn = min(kChunk, n_nodes - c0);
+    __syncthreads();  // every lane is done with the previous chunk
+    for (int i = tid; i < cn; i += kThreads) {
+      const int32_t j = c0 + i;
+      const double fr = free_bytes[j];
+      const float frf = __double2float_rn(fr);
+      const float q = queue_ms[j];
+      s_free[i] = fr;
+      s_inv[i] = frf > 0.0f ? __fdiv_rn(1.0f, frf) : -1.0f;
+      s_warm[i] = norm01(__fadd_rn(q, 0.0f), lo_t, inv_t);
+      s_cold[i] = norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t);
+      s_deg[i] = norm01(deg_ms[j], lo_d, inv_d);
+      s_mask[i] = resident_mask[j];
+    }
+    for (int e = tid; e < n_src * cn; e += kThreads) {
+      const int r = e / cn, i = e - r * cn;
+      s_prox[r * kProxStride + i] =
+          __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, inv_r));
+    }
+    __syncthreads();
+    for (int i = 0; i < cn; ++i) {
+      if (!(need <= s_free[i])) continue;   // FilterByPolicyAndFeasibility
+      const float inv = s_inv[i];
+      float fit = inv >= 0.0f ? __fmul_rn(needf, inv) : 1.0f;
+      if (fit > 1.0f) fit = 1.0f;
+      const float a = __fadd_rn(__fmul_rn(gamma, prox_row[i]), __fmul_rn(omg, fit));
+      const float nr = (s_mask[i] & mbit) ? s_warm[i] : s_cold[i];
+      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, s_deg[i]));
+      best.push_increasing(-sc, c0 + i);
+    }
+  }
+
+  if (valid) {
+#pragma unroll
+    for (int i = 0; i < KT; ++i) {
+      if (i < k) {
+        const bool some = best.n[i] != kNoNode;
+        node_idx[stage * k + i] = some ? best.n[i] : -1;
+        fitness[stage * k + i] = some ? -best.s[i] : -INFINITY;
+      }
+    }
+  }
+}
+
+// The values of rank r_lo and r_hi (0-based) of v[0 .. m-1] in the total order of float bit
+// patterns (-0 before +0): four passes over the 8-bit digits of the order-preserving image,
+// each narrowing both candidate prefixes by one digit.
+constexpr int kSelectThreads = 1024;
+__global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* __restrict__ v, int64_t m,
+                                                                  int64_t r_lo, int64_t r_hi,
+                                                                  float* __restrict__ out) {
+  __shared__ uint32_t hist[2][256];
+  __shared__ uint32_t s_prefix[2];
+  __shared__ int64_t s_rank[2];
+  const int tid = threadIdx.x;
+  if (tid < 2) {
+    s_prefix[tid] = 0;
+    s_rank[tid] = tid ? r_hi : r_lo;
+  }
+  uint32_t mask = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 512; i += kSelectThreads) (&hist[0][0])[i] = 0;
+    __syncthreads();
+    const uint32_t p0 = s_prefix[0], p1 = s_prefix[1];
+    for (int64_t i = tid; i < m; i += kSelectThreads) {
+      const uint32_t u = float_key(v[i]);
+      const uint32_t dgt = (u >> shift) & 255u;
+      if ((u & mask) == p0) atomicAdd(&hist[0][dgt], 1u);
+      if ((u & mask) == p1) atomicAdd(&hist[1][dgt], 1u);
+    }
+    __syncthreads();
+    if (tid < 2) {
+      int64_t r = s_rank[tid];
+      uint32_t b = 0;
+      for (; b < 255u; ++b) {
+        const uint32_t c = hist[tid][b];
+        if (r < (int64_t)c) break;
+        r -= c;
+      }
+      s_rank[tid] = r;
+      s_prefix[tid] |= b << shift;
+    }
+    mask |= 0xFFu << shift;
+    __syncthreads();
+  }
+  if (tid < 2) out[tid] = key_float(s_prefix[tid]);
+}
+
+}  // namespace
+
+maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
+                                    const int32_t* class_id, const double* kv_bytes,
+                                    int32_t n_nodes, int32_t n_src, const double* free_bytes,
+                                    const float* queue_ms, const float* act_ms,
+                                    const uint64_t* resident_mask, const float* deg_ms,
+                                    const float* rtt_ms, const float* class_weights,
+                                    const float* bounds, double rho, int32_t k, int32_t* node_idx,
+                                    float* fitness, hipStream_t stream) {
+  if (n == 0) return MAESTRO_OK;
+  const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
+#define MAESTRO_FIT_KT(KT)                                                                      \
+  fitness_kernel<KT><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,        \
+                                                 n_nodes, n_src, free_bytes, queue_ms, act_ms,   \
+                                                 resident_mask, deg_ms, rtt_ms, class_weights,   \
+                                                 bounds, rho, k, node_idx, fitness)
+  if (k == 1) MAESTRO_FIT_KT(1);
+  else if (k == 2) MAESTRO_FIT_KT(2);
+  else if (k <= 4) MAESTRO_FIT_KT(4);
+  else if (k <= 8) MAESTRO_FIT_KT(8);
+  else MAESTRO_FIT_KT(16);
+#undef MAESTRO_FIT_KT
+  return launch_status();
+}
+
+maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
+                                hipStream_t stream) {
+  quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(values, m, r_lo, r_hi, out);
+  return launch_status();
+}
+
+}  // namespace maestro

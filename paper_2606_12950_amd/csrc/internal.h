@@ -26,6 +26,20 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
                             size_t workspace_bytes, hipStream_t stream);
 size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);
 
+// Routing by fitness (Eq. 5) and the window bounds of its normalisation.
+constexpr int kMaxFitnessSources = 16;
+constexpr int kMaxFitnessClasses = 16;
+maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
+                                    const int32_t* class_id, const double* kv_bytes,
+                                    int32_t n_nodes, int32_t n_src, const double* free_bytes,
+                                    const float* queue_ms, const float* act_ms,
+                                    const uint64_t* resident_mask, const float* deg_ms,
+                                    const float* rtt_ms, const float* class_weights,
+                                    const float* bounds, double rho, int32_t k, int32_t* node_idx,
+                                    float* fitness, hipStream_t stream);
+maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
+                                hipStream_t stream);
+
 // Prioritisation: chain suffix sums, slack keys, stable radix sort.
 maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
                                  const int64_t* chain_offset, const float* stage_latency_s,

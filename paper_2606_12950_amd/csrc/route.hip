@@ -24,57 +24,13 @@
 #include <type_traits>
 
 #include "internal.h"
+#include "select.h"
 
 namespace maestro {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kNodeChunk = 1024;
-constexpr int32_t kNoNode = INT32_MAX;  // internal "empty slot" index, reported as -1
-
-template <int KT>
-struct TopK {
-  float s[KT];
-  int32_t n[KT];
-
-  __device__ __forceinline__ void init() {
-#pragma unroll
-    for (int i = 0; i < KT; ++i) { s[i] = INFINITY; n[i] = kNoNode; }
-  }
-  // Insert a candidate whose node index is larger than every node already held (nodes are
-  // visited in increasing order within a lane): equal scores stay behind, so comparing
-  // scores strictly gives the lexicographic order.
-  __device__ __forceinline__ void push_increasing(float sc, int32_t node) {
-#pragma unroll
-    for (int i = KT - 1; i >= 0; --i) {
-      const int p = i > 0 ? i - 1 : 0;
-      const bool lt_prev = (i > 0) && sc < s[p];
-      if (sc < s[i]) {
-        if (lt_prev) { s[i] = s[p]; n[i] = n[p]; }
-        else { s[i] = sc; n[i] = node; }
-      }
-    }
-  }
-  // General lexicographic insertion, used when merging lists from other lanes.
-  __device__ __forceinline__ void push_lex(float sc, int32_t node) {
-#pragma unroll
-    for (int i = KT - 1; i >= 0; --i) {
-      const int p = i > 0 ? i - 1 : 0;
-      const bool lt_this = sc < s[i] || (sc == s[i] && node < n[i]);
-      const bool lt_prev = (i > 0) && (sc < s[p] || (sc == s[p] && node < n[p]));
-      if (lt_this) {
-        if (lt_prev) { s[i] = s[p]; n[i] = n[p]; }
-        else { s[i] = sc; n[i] = node; }
-      }
-    }
-  }
-};
-
-template <>
-__device__ __forceinline__ void TopK<1>::push_increasing(float sc, int32_t node) {
-  if (sc < s[0]) { s[0] = sc; n[0] = node; }
-}
-
 template <int KT, bool kMask64>
 __global__ __launch_bounds__(kThreads) void route_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
@@ -186,15 +142,6 @@ struct NodeEntry {                        // 16 bytes: one node in a model's rea
   int32_t node;
   double free;                            // KV admission headroom
 };
-
-// order-preserving map of float bits to unsigned (a < b <=> map(a) < map(b), -0 < +0)
-__device__ __forceinline__ uint32_t float_key(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_float(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
 
 __global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
     int32_t n_nodes, int32_t padded, const float* __restrict__ queue_s, const float* __restrict__ cold_s,

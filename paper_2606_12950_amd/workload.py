@@ -317,6 +317,77 @@ def generate(spec: WorkloadSpec, with_x: bool = True) -> Workload:
                     chain_offset=chain_offset, deadline_us=deadline_us, now_us=now_us)
 
 
+# ---------------------------------------------------------------------------------------------
+# Extra inputs of routing by fitness (Eq. 5), drawn for an existing Workload
+# ---------------------------------------------------------------------------------------------
+
+FITNESS_STREAMS = ("cluster", "src", "class", "rtt", "deg", "rtt_window", "ready_window",
+                   "ready_window_cold", "deg_window")
+
+N_CLUSTERS = 5            # three local and two remote clusters, as in the paper's simulator
+N_LOCAL = 3
+WINDOW = 4096             # recent observations per normalised metric
+
+
+@dataclass
+class FitnessInputs:
+    """Per-stage source and class, per-node metrics in milliseconds, the source x node RTT
+    matrix, per-class weights (gamma, lambda, mu) and windows of recent observations from
+    which the normalisation bounds are taken."""
+    src_id: np.ndarray            # [N] int32 source cluster of each stage
+    class_id: np.ndarray          # [N] int32: 0 interactive, 1 background
+    queue_ms: np.ndarray          # [M] float32 queueing delay T_q
+    act_ms: np.ndarray            # [M] float32 activation latency T_act (model not resident)
+    deg_ms: np.ndarray            # [M] float32 disruption penalty C_deg
+    rtt_ms: np.ndarray            # [N_CLUSTERS][M] float32
+    class_weights: np.ndarray     # [2][3] float32
+    rtt_window: np.ndarray        # [WINDOW] float32
+    ready_window: np.ndarray      # [WINDOW] float32
+    deg_window: np.ndarray        # [WINDOW] float32
+
+
+def _rtt_draw(rng: np.random.Generator, a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """RTT in ms between source cluster a and node cluster b: same cluster U[0.2, 1],
+    both local U[1, 5], across regions U[20, 80]."""
+    same = a == b
+    both_local = (a < N_LOCAL) & (b < N_LOCAL)
+    lo = np.where(same, 0.2, np.where(both_local, 1.0, 20.0))
+    hi = np.where(same, 1.0, np.where(both_local, 5.0, 80.0))
+    return rng.uniform(lo, hi).astype(np.float32)
+
+
+def fitness_inputs(wl: Workload) -> FitnessInputs:
+    """Fitness-routing inputs for the stages and nodes of ``wl`` (seeded by its spec's seed).
+
+    Nodes are spread uniformly over the clusters; 30% of stages are interactive; class weights
+    are (gamma, lambda, mu) = (0.25, 1, 1) for interactive stages -- the paper's latency weight
+    and default lambda = mu = 1 -- and (0.1, 1, 1) for background ones; the queueing delay and
+    activation latency are the workload's own (in ms); 20% of nodes report a disruption penalty
+    U[1, 500] ms. Windows hold recent observations of each metric from the same distributions."""
+    children = np.random.SeedSequence([wl.spec.seed, 0xF17]).spawn(len(FITNESS_STREAMS))
+    r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(FITNESS_STREAMS, children)}
+    M, N = wl.free_bytes.shape[0], wl.n
+    cluster = r["cluster"].integers(0, N_CLUSTERS, M)
+    src = r["src"].integers(0, N_CLUSTERS, N).astype(np.int32)
+    cls = (r["class"].random(N) >= 0.3).astype(np.int32)
+    rtt = _rtt_draw(r["rtt"], np.arange(N_CLUSTERS)[:, None], cluster[None, :])
+    deg = np.where(r["deg"].random(M) < 0.2, r["deg"].uniform(1.0, 500.0, M), 0.0).astype(np.float32)
+    wa = r["rtt_window"].integers(0, N_CLUSTERS, WINDOW)
+    wb = r["rtt_window"].integers(0, N_CLUSTERS, WINDOW)
+    rtt_window = _rtt_draw(r["rtt_window"], wa, wb)
+    ready_window = (r["ready_window"].uniform(0.0, 5000.0, WINDOW)
+                    + np.where(r["ready_window_cold"].random(WINDOW) < 0.7,
+                               r["ready_window_cold"].uniform(2000.0, 20000.0, WINDOW), 0.0)).astype(np.float32)
+    deg_window = np.where(r["deg_window"].random(WINDOW) < 0.2,
+                          r["deg_window"].uniform(1.0, 500.0, WINDOW), 0.0).astype(np.float32)
+    weights = np.array([[0.25, 1.0, 1.0], [0.1, 1.0, 1.0]], np.float32)
+    return FitnessInputs(src_id=src, class_id=cls,
+                         queue_ms=(wl.queue_s * np.float32(1000.0)).astype(np.float32),
+                         act_ms=(wl.cold_s * np.float32(1000.0)).astype(np.float32),
+                         deg_ms=deg, rtt_ms=rtt, class_weights=weights, rtt_window=rtt_window,
+                         ready_window=ready_window, deg_window=deg_window)
+
+
 def workload(name: str, with_x: bool = True, **overrides) -> Workload:
     """Named workload, optionally with fields of its spec replaced (e.g. ``n_stages=5000``)."""
     spec = SPECS[name]

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 8
+    assert len(names) == 10
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -46,7 +46,8 @@ def test_status_strings(lib):
 # below fails validation before any launch.
 _buf = (ctypes.c_double * 64)()
 FAKE = ctypes.c_void_p(ctypes.addressof(_buf))
-MISALIGNED = ctypes.c_void_p(ctypes.addressof(_buf) + 4)
+MISALIGNED = ctypes.c_void_p(ctypes.addressof(_buf) + 4)    # misaligned for 8-byte elements
+MISALIGNED4 = ctypes.c_void_p(ctypes.addressof(_buf) + 2)   # misaligned for 4-byte elements
 
 
 def _pred(dims, dtype, layers):
@@ -103,6 +104,34 @@ def test_route_validation(lib):
     assert call(rho=float("inf")) == INVALID
     assert call(model=None) == INVALID
     assert call(free=MISALIGNED) == INVALID
+
+
+def test_route_fitness_and_quantiles_validation(lib):
+    def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE):
+        return lib.maestro_route_fitness(n, FAKE, src, FAKE, FAKE, n_models, n_nodes, n_src, n_classes,
+                                         FAKE, FAKE, FAKE, FAKE, FAKE, rtt, FAKE, bounds, rho, k, FAKE, FAKE, None)
+    assert call(n=-1) == INVALID
+    assert call(n_models=0) == INVALID
+    assert call(n_models=65) == INVALID
+    assert call(n_nodes=0) == INVALID
+    assert call(n_src=0) == INVALID
+    assert call(n_src=17) == INVALID                                          # at most 16 sources
+    assert call(n_classes=17) == INVALID
+    assert call(k=17) == INVALID
+    assert call(rho=float("nan")) == INVALID
+    assert call(src=None) == INVALID                                          # per-stage input missing
+    assert call(rtt=None) == INVALID
+    assert call(bounds=MISALIGNED4) == INVALID
+    assert call(n=0, src=None) == OK                                          # empty batch: no-op
+    q = lambda m=10, lo=0.05, hi=0.95, v=FAKE, out=FAKE: lib.maestro_quantiles(v, m, lo, hi, out, None)
+    assert q(m=0) == INVALID
+    assert q(lo=0.6, hi=0.5) == INVALID
+    assert q(lo=-0.1) == INVALID
+    assert q(hi=1.5) == INVALID
+    assert q(lo=float("nan")) == INVALID
+    assert q(v=None) == INVALID
+    assert q(out=MISALIGNED4) == INVALID
+    assert q(m=1 << 32) == UNSUPPORTED
 
 
 def test_prioritize_validation_and_workspace(lib):

@@ -1,0 +1,143 @@
+"""Parity of routing by fitness (Eq. 5, Alg. 3) and of the window quantiles between the HIP path
+(through the C-ABI) and the CPU oracle, on seeded inputs.
+
+Bars: quantiles bit-exact; node indices and fitness values bit-exact given the same inputs (both
+sides evaluate the same float32 expression in the same order; the argmax is taken on it).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_12950_amd as M
+from paper_2606_12950_amd import pipeline
+from paper_2606_12950_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+GB = 1e9
+
+
+def _t(a):
+    return pipeline._t(np.ascontiguousarray(a), "cuda")
+
+
+def gpu_quantiles(v, lo=0.05, hi=0.95):
+    out = M.quantiles(_t(np.asarray(v, np.float32)), lo, hi)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def gpu_fitness(model, src, cls, kv, nodes, weights, bounds, k=1, rho=0.0, n_models=64):
+    idx, fit = M.route_fitness(_t(model.astype(np.int32)), _t(src.astype(np.int32)), _t(cls.astype(np.int32)),
+                               _t(kv.astype(np.float64)), _t(nodes["free_bytes"]), _t(nodes["queue_ms"]),
+                               _t(nodes["act_ms"]), _t(nodes["resident_mask"]), _t(nodes["deg_ms"]),
+                               _t(nodes["rtt_ms"]), _t(np.asarray(weights, np.float32).reshape(-1, 3)),
+                               _t(np.asarray(bounds, np.float32)), n_models=n_models, k=k, rho=rho)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), fit.cpu().numpy()
+
+
+def oracle_fitness(model, src, cls, kv, nodes, weights, bounds, k=1, rho=0.0):
+    return oracle.route_fitness(model, src, cls, kv, nodes["free_bytes"], nodes["queue_ms"], nodes["act_ms"],
+                                nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                                np.asarray(weights, np.float32).reshape(-1, 3), np.asarray(bounds, np.float32),
+                                k=k, rho=rho)
+
+
+def assert_same(got, ref):
+    gi, gf = got
+    ri, rf = ref
+    bad = np.flatnonzero((gi != ri).any(axis=1) | (gf.view(np.uint32) != rf.view(np.uint32)).any(axis=1))
+    assert bad.size == 0, f"{bad.size} stages differ, first {bad[:5]}: gpu {gi[bad[0]]} {gf[bad[0]]} " \
+                          f"oracle {ri[bad[0]]} {rf[bad[0]]}"
+
+
+def _nodes(rng, M_, n_src, n_models=16):
+    return dict(
+        free_bytes=rng.uniform(0, 300, M_) * GB,
+        queue_ms=rng.uniform(0, 5000, M_).astype(np.float32),
+        act_ms=rng.uniform(2000, 20000, M_).astype(np.float32),
+        resident_mask=rng.integers(0, 1 << n_models, M_).astype(np.uint64),
+        deg_ms=np.where(rng.random(M_) < 0.3, rng.uniform(0, 500, M_), 0).astype(np.float32),
+        rtt_ms=rng.uniform(0.2, 80, (n_src, M_)).astype(np.float32),
+    )
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 19, 20, 21, 1000, 4096, 100003])
+def test_quantiles_match_oracle(m):
+    rng = np.random.default_rng(m)
+    v = np.round(rng.normal(0, 30, m), 1).astype(np.float32)
+    v[rng.random(m) < 0.05] = -0.0
+    v[rng.random(m) < 0.05] = 0.0
+    for lo, hi in [(0.05, 0.95), (0.0, 1.0), (0.5, 0.5), (0.01, 0.99)]:
+        got = gpu_quantiles(v, lo, hi)
+        ref = oracle.quantiles(v, lo, hi)
+        assert got.view(np.uint32).tolist() == ref.view(np.uint32).tolist(), (lo, hi, got, ref)
+
+
+@pytest.mark.parametrize("n,M_,n_src,k", [(1, 1, 1, 1), (257, 64, 3, 1), (1000, 1300, 5, 3),
+                                          (3000, 512, 16, 16), (700, 2049, 2, 4)])
+def test_fitness_matches_oracle(n, M_, n_src, k):
+    # several 512-node chunks with a ragged tail, every source count, route widths 1..16
+    rng = np.random.default_rng(n * 7 + M_)
+    nodes = _nodes(rng, M_, n_src)
+    model = rng.integers(0, 16, n).astype(np.int32)
+    src = rng.integers(0, n_src, n).astype(np.int32)
+    cls = rng.integers(0, 3, n).astype(np.int32)
+    kv = rng.uniform(0, 250, n) * GB
+    weights = [[0.25, 1, 1], [0.1, 1, 1], [0.6, 0.3, 2.0]]
+    rw, qw = nodes["rtt_ms"].ravel(), (nodes["queue_ms"] + nodes["act_ms"])
+    bounds = [*oracle.quantiles(rw), *oracle.quantiles(qw), *oracle.quantiles(nodes["deg_ms"])]
+    for rho in (0.0, 0.2):
+        got = gpu_fitness(model, src, cls, kv, nodes, weights, bounds, k=k, rho=rho)
+        assert_same(got, oracle_fitness(model, src, cls, kv, nodes, weights, bounds, k=k, rho=rho))
+
+
+def test_fitness_ties_infeasible_and_degenerate_windows():
+    rng = np.random.default_rng(11)
+    M_ = 600
+    nodes = _nodes(rng, M_, 2)
+    # duplicated node states: equal fitness, the lower index must come first
+    for key in nodes:
+        if key == "rtt_ms":
+            nodes[key][:, 300:] = nodes[key][:, :300]
+        else:
+            nodes[key][300:] = nodes[key][:300]
+    n = 2000
+    model = rng.integers(0, 16, n).astype(np.int32)
+    src = rng.integers(0, 2, n).astype(np.int32)
+    cls = np.zeros(n, np.int32)
+    kv = rng.uniform(0, 400, n) * GB          # many stages fit nowhere
+    kv[::50] = 0.0                            # zero demand
+    for bounds in ([0, 100, 0, 30000, 0, 500], [5, 5, 7, 7, 1, 1]):   # normal and degenerate windows
+        got = gpu_fitness(model, src, cls, kv, nodes, [[0.25, 1, 1]], bounds, k=5)
+        ref = oracle_fitness(model, src, cls, kv, nodes, [[0.25, 1, 1]], bounds, k=5)
+        assert_same(got, ref)
+    assert (got[0][:, 0] == -1).any() and (got[0][:, 0] >= 0).any()
+
+
+@pytest.mark.parametrize("name", ["c1", "c3"])
+def test_fitness_workload_full(name):
+    # the GPU's own predictions feed both sides; every stage is compared
+    w = W.workload(name)
+    f = W.fitness_inputs(w)
+    b = pipeline.to_device(w)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    torch.cuda.synchronize()
+    kv = o.kv_bytes.cpu().numpy()
+    nodes = dict(free_bytes=w.free_bytes, queue_ms=f.queue_ms, act_ms=f.act_ms, resident_mask=w.resident_mask,
+                 deg_ms=f.deg_ms, rtt_ms=f.rtt_ms)
+    bounds_g = np.concatenate([gpu_quantiles(f.rtt_window), gpu_quantiles(f.ready_window),
+                               gpu_quantiles(f.deg_window)])
+    bounds_o = np.concatenate([oracle.quantiles(f.rtt_window), oracle.quantiles(f.ready_window),
+                               oracle.quantiles(f.deg_window)])
+    assert bounds_g.view(np.uint32).tolist() == bounds_o.view(np.uint32).tolist()
+    got = gpu_fitness(w.model_id, f.src_id, f.class_id, kv, nodes, f.class_weights, bounds_g, k=w.spec.k,
+                      rho=w.spec.rho, n_models=w.spec.n_models)
+    ref = oracle_fitness(w.model_id, f.src_id, f.class_id, kv, nodes, f.class_weights, bounds_o, k=w.spec.k,
+                         rho=w.spec.rho)
+    assert_same(got, ref)
+    routed = (got[0][:, 0] >= 0).mean()
+    print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes, {routed:.4f} routed, fitness identical")
