@@ -3,6 +3,7 @@
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
 python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for counter calibration)
 python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
+python bench.py --route-fitness        (routing by fitness, Eq. 5, on the workload's predictions)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -28,6 +29,12 @@ METRIC = "stages predicted+routed/sec on 1 MI355X; % of HBM/MFMA roofline"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0
+# non-packed vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+PEAK_VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# operations the fitness definition needs per (stage, node) pair: the feasibility compare and
+# the eight float32 operations of the score (fit product; gamma, (1 - gamma) products and their
+# sum; lambda and mu products and the two differences)
+FITNESS_OPS_PER_PAIR = 9
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "predict_traffic.json")
@@ -162,6 +169,50 @@ def sweep_prioritize(log2_lo: int, log2_hi: int, steps: int, warmup: int):
         torch.cuda.empty_cache()
 
 
+def route_fitness_bench(name: str, steps: int, warmup: int):
+    """Routing by fitness over the workload's stages, on the GPU's own predictions; bounds from
+    the recent-observation windows (maestro_quantiles). One JSON line."""
+    import torch
+    from paper_2606_12950_amd import _native, pipeline
+    from paper_2606_12950_amd import workload as W
+    torch.cuda.set_device(0)
+    wl = W.workload(name)
+    f = W.fitness_inputs(wl)
+    b = pipeline.to_device(wl)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    t = lambda a: pipeline._t(a, "cuda")
+    fd = dict(src=t(f.src_id), cls=t(f.class_id), queue=t(f.queue_ms), act=t(f.act_ms), deg=t(f.deg_ms),
+              rtt=t(f.rtt_ms), weights=t(f.class_weights))
+    bounds = torch.cat([_native.quantiles(t(f.rtt_window)), _native.quantiles(t(f.ready_window)),
+                        _native.quantiles(t(f.deg_window))])
+    n, m = wl.n, wl.spec.n_nodes
+    out = (torch.empty((n, wl.spec.k), dtype=torch.int32, device="cuda"),
+           torch.empty((n, wl.spec.k), dtype=torch.float32, device="cuda"))
+    call = lambda: _native.route_fitness(b.model_id, fd["src"], fd["cls"], o.kv_bytes, b.free_bytes, fd["queue"],
+                                         fd["act"], b.resident_mask, fd["deg"], fd["rtt"], fd["weights"], bounds,
+                                         n_models=wl.spec.n_models, k=wl.spec.k, rho=wl.spec.rho, out=out)
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record()
+        call()
+        e1.record()
+    torch.cuda.synchronize()
+    d = [e0.elapsed_time(e1) for e0, e1 in ev]
+    ms = float(np.mean(d))
+    pairs = n * m
+    achieved = pairs * FITNESS_OPS_PER_PAIR / (ms * 1e-3)
+    print(json.dumps({"route_fitness": name, "n_stages": n, "n_nodes": m, "k": wl.spec.k, "ms": round(ms, 4),
+                      "phase_ms": percentiles(d), "stages_per_s": n / (ms * 1e-3), "pairs_per_s": pairs / (ms * 1e-3),
+                      "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_VALU_LANE_OPS / 1e12,
+                                   "unit": "T lane-ops/s", "frac": round(achieved / PEAK_VALU_LANE_OPS, 4),
+                                   "ops_per_pair": FITNESS_OPS_PER_PAIR},
+                      "routed_frac": float((out[0][:, 0] >= 0).float().mean().item())}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -173,10 +224,15 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--sweep-prioritize", nargs="?", const="17:26", default=None, metavar="LO:HI",
                     help="time the slack ordering alone for W = 2^LO .. 2^HI workflows")
+    ap.add_argument("--route-fitness", action="store_true",
+                    help="time routing by fitness (Eq. 5) on the workload's predictions")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.route_fitness:
+        route_fitness_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
         return
     if args.sweep_prioritize:
         lo, hi = (int(v) for v in args.sweep_prioritize.split(":"))

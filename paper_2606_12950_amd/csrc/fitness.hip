@@ -20,6 +20,8 @@
 //
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
+#include <type_traits>
+
 #include "internal.h"
 #include "select.h"
 
@@ -40,7 +42,7 @@ __device__ __forceinline__ float norm01(float x, float lo, float inv) {
   return t;
 }
 
-template <int KT>
+template <int KT, bool kMask64>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_nodes,
@@ -49,12 +51,15 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     const float* __restrict__ deg_ms, const float* __restrict__ rtt_ms,
     const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
     int32_t* __restrict__ node_idx, float* __restrict__ fitness) {
-  __shared__ double s_free[kChunk];               // KV admission headroom
-  __shared__ float s_inv[kChunk];                 // 1 / fl32(headroom); -1 when that is 0 (fit = 1)
-  __shared__ float s_warm[kChunk];                // norm(T_q): model resident
-  __shared__ float s_cold[kChunk];                // norm(T_q + T_act)
-  __shared__ float s_deg[kChunk];                 // norm(C_deg)
-  __shared__ uint64_t s_mask[kChunk];             // residency bits
+  // per node, two 16-byte records (one LDS read each, the same address for every lane):
+  //   terms: 1 / fl32(headroom) (+inf when that is 0), norm(T_q) (model resident),
+  //          norm(T_q + T_act), norm(C_deg)
+  //   admit: KV admission headroom and the residency bits (the low 32 when no model id
+  //          exceeds 31)
+  typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
+  struct Admit { double free; uint64_t mask; };
+  __shared__ float4 s_terms[kChunk];
+  __shared__ Admit s_admit[kChunk];
   __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
 
   const int tid = threadIdx.x;
@@ -67,7 +72,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 
   double need = INFINITY;   // an invalid lane admits nothing
   float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
-  uint64_t mbit = 0;
+  mask_t mbit = 0;
   int src = 0;
   if (valid) {
     need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
@@ -77,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     lambda = wt[1];
     mu = wt[2];
     omg = __fsub_rn(1.0f, gamma);
-    mbit = (uint64_t)1 << model_id[stage];
+    mbit = (mask_t)1 << model_id[stage];
     src = src_id[stage];
   }
   const float* prox_row = s_prox + src * kProxStride;
@@ -92,12 +97,10 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       const double fr = free_bytes[j];
       const float frf = __double2float_rn(fr);
       const float q = queue_ms[j];
-      s_free[i] = fr;
-      s_inv[i] = frf > 0.0f ? __fdiv_rn(1.0f, frf) : -1.0f;
-      s_warm[i] = norm01(__fadd_rn(q, 0.0f), lo_t, inv_t);
-      s_cold[i] = norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t);
-      s_deg[i] = norm01(deg_ms[j], lo_d, inv_d);
-      s_mask[i] = resident_mask[j];
+      s_terms[i] = make_float4(frf > 0.0f ? __fdiv_rn(1.0f, frf) : INFINITY,
+                               norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
+                               norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t), norm01(deg_ms[j], lo_d, inv_d));
+      s_admit[i] = Admit{fr, resident_mask[j]};
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
@@ -105,15 +108,20 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
           __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, inv_r));
     }
     __syncthreads();
+    // branch-free: every node is scored; an infeasible one offers the key +inf, which never
+    // enters the list (FilterByPolicyAndFeasibility)
+#pragma unroll 4
     for (int i = 0; i < cn; ++i) {
-      if (!(need <= s_free[i])) continue;   // FilterByPolicyAndFeasibility
-      const float inv = s_inv[i];
-      float fit = inv >= 0.0f ? __fmul_rn(needf, inv) : 1.0f;
-      if (fit > 1.0f) fit = 1.0f;
+      const float4 t = s_terms[i];
+      const Admit ad = s_admit[i];
+      // fit = min(1, fl32(need) / fl32(headroom)); with zero headroom only need = 0 is
+      // feasible, and min(0 * inf = NaN, 1) = 1 (IEEE min returns the number), the fit of a
+      // stage that fills the node exactly
+      const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
       const float a = __fadd_rn(__fmul_rn(gamma, prox_row[i]), __fmul_rn(omg, fit));
-      const float nr = (s_mask[i] & mbit) ? s_warm[i] : s_cold[i];
-      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, s_deg[i]));
-      best.push_increasing(-sc, c0 + i);
+      const float nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
+      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, t.w));
+      best.push_increasing(need <= ad.free ? -sc : INFINITY, c0 + i);
     }
   }
 
@@ -176,7 +184,7 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
 }  // namespace
 
 maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
-                                    const int32_t* class_id, const double* kv_bytes,
+                                    const int32_t* class_id, const double* kv_bytes, int32_t n_models,
                                     int32_t n_nodes, int32_t n_src, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* deg_ms,
@@ -185,11 +193,20 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
-#define MAESTRO_FIT_KT(KT)                                                                      \
-  fitness_kernel<KT><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,        \
-                                                 n_nodes, n_src, free_bytes, queue_ms, act_ms,   \
-                                                 resident_mask, deg_ms, rtt_ms, class_weights,   \
-                                                 bounds, rho, k, node_idx, fitness)
+  const bool mask64 = n_models > 32;
+#define MAESTRO_FIT_KT(KT)                                                                                \
+  do {                                                                                                    \
+    if (mask64)                                                                                           \
+      fitness_kernel<KT, true><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,       \
+                                                           n_nodes, n_src, free_bytes, queue_ms, act_ms,  \
+                                                           resident_mask, deg_ms, rtt_ms, class_weights,  \
+                                                           bounds, rho, k, node_idx, fitness);            \
+    else                                                                                                  \
+      fitness_kernel<KT, false><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,      \
+                                                            n_nodes, n_src, free_bytes, queue_ms, act_ms, \
+                                                            resident_mask, deg_ms, rtt_ms, class_weights, \
+                                                            bounds, rho, k, node_idx, fitness);           \
+  } while (0)
   if (k == 1) MAESTRO_FIT_KT(1);
   else if (k == 2) MAESTRO_FIT_KT(2);
   else if (k <= 4) MAESTRO_FIT_KT(4);

@@ -30,7 +30,7 @@ size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32
 constexpr int kMaxFitnessSources = 16;
 constexpr int kMaxFitnessClasses = 16;
 maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
-                                    const int32_t* class_id, const double* kv_bytes,
+                                    const int32_t* class_id, const double* kv_bytes, int32_t n_models,
                                     int32_t n_nodes, int32_t n_src, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* deg_ms,

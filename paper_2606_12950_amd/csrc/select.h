@@ -23,6 +23,7 @@ struct TopK {
   // visited in increasing order within a lane): equal scores stay behind, so comparing
   // scores strictly gives the lexicographic order.
   __device__ __forceinline__ void push_increasing(float sc, int32_t node) {
+    if (!(sc < s[KT - 1])) return;   // cannot enter: the common case once the list is full
 #pragma unroll
     for (int i = KT - 1; i >= 0; --i) {
       const int p = i > 0 ? i - 1 : 0;
