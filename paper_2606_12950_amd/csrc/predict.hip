@@ -153,6 +153,37 @@ __device__ __forceinline__ void mfma_chain(f32x16& acc, const unsigned char* pa,
   }
 }
 
+// Two 32-row blocks of one chunk multiplied together: step f feeds block f % 2 at K-step f / 2
+// (both blocks take the same B operand), so consecutive MFMAs never depend on each other and the
+// chunk has a single chain start. Block lb's fragment of K-step k is read from
+// (k & 4 ? pb[lb] : pa[lb]) + 32k, kLookahead steps ahead; pre() and side(f) as in mfma_chain.
+template <int KS, int NBREG, typename Pre, typename Side>
+__device__ __forceinline__ void mfma_chain_pair(f32x16& acc0, f32x16& acc1, const unsigned char* pa0,
+                                                const unsigned char* pb0, const unsigned char* pa1,
+                                                const unsigned char* pb1, const bf16x8 (&b)[NBREG],
+                                                Pre&& pre, Side&& side) {
+  constexpr int F = 2 * KS;
+  auto frag = [&](int f) {
+    const int k = f >> 1;
+    const unsigned char* base = (f & 1) ? ((k & 4) ? pb1 : pa1) : ((k & 4) ? pb0 : pa0);
+    return *reinterpret_cast<const bf16x8*>(base + k * 32);
+  };
+  bf16x8 fr[F];
+#pragma unroll
+  for (int f = 0; f < kLookahead && f < F; ++f) fr[f] = frag(f);
+  __builtin_amdgcn_sched_barrier(0);
+  pre();
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    if (f + kLookahead < F) fr[f + kLookahead] = frag(f + kLookahead);
+    if (f & 1) acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[f], b[f >> 1], acc1, 0, 0, 0);
+    else acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[f], b[f >> 1], acc0, 0, 0, 0);
+    side(f);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Accumulator of a 32-neuron block initialised with the biases of the neurons lane-half h holds
 // (registers 0-7: neurons 8h .. 8h+7, registers 8-15: neurons 16+8h .. 16+8h+7).
 __device__ __forceinline__ f32x16 bias_acc(const float* __restrict__ b32, int h) {
@@ -407,7 +438,7 @@ void mlp3_bf16_kernel(
     // layer-2 block). The activations live in the accumulation registers, which MFMA reads as
     // its B operand directly, leaving the architectural registers to everything else.
     bf16x8 h1[H1 / 16];
-    f32x16 acc_prev;                      // finished accumulator of the previous block
+    f32x16 prev0, prev1;                  // finished accumulators of the previous chunk
     auto l1_relu = [&](int nb, const f32x16& acc) {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
@@ -419,16 +450,20 @@ void mlp3_bf16_kernel(
     for (int c = 0; c < NC1; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
       const unsigned char* dst = ahead();
-#pragma unroll
-      for (int lb = 0; lb < 2; ++lb) {
-        const int nb = 2 * c + lb;
-        f32x16 acc = bias_acc(s_b1 + nb * 32, h);
-        mfma_chain<KS1, KS1>(
-            acc, buf + l1a[lb], buf + l1b[lb], xf, 0, [&]() { if (nb > 0) l1_relu(nb - 1, acc_prev); },
-            [&](int k) { spread(tile, NX + c + kBufs - 1, dst, KS1 * lb + k); });
-        acc_prev = acc;
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      f32x16 acc0 = bias_acc(s_b1 + (2 * c) * 32, h);
+      f32x16 acc1 = bias_acc(s_b1 + (2 * c + 1) * 32, h);
+      mfma_chain_pair<KS1, KS1>(
+          acc0, acc1, buf + l1a[0], buf + l1b[0], buf + l1a[1], buf + l1b[1], xf,
+          [&]() {
+            if (c > 0) {
+              l1_relu(2 * c - 2, prev0);
+              l1_relu(2 * c - 1, prev1);
+            }
+          },
+          [&](int f) { spread(tile, NX + c + kBufs - 1, dst, f); });
+      prev0 = acc0;
+      prev1 = acc1;
+      __builtin_amdgcn_sched_barrier(0);
       advance();
     }
 
@@ -484,7 +519,10 @@ void mlp3_bf16_kernel(
     constexpr int kSteady = NB2 - kPeel - 1;
     static_assert(kSteady >= 2, "at least one pair of blocks in the steady-state loop");
     auto in_tile = [&](int j, const unsigned char* dst, int k) { spread(tile, NX + NC1 + j, dst, k); };
-    f32x16 carry = l2_block(0, acc_prev, [&](const f32x16& p) { l1_relu(H1 / 32 - 1, p); }, in_tile);
+    f32x16 carry = l2_block(0, prev1, [&](const f32x16& p) {
+      l1_relu(H1 / 32 - 2, prev0);
+      l1_relu(H1 / 32 - 1, p);
+    }, in_tile);
     for (int b = 1; b + 1 <= kSteady; b += 2) {
       const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile);
       carry = l2_block(b + 1, a, l2_epilogue, in_tile);
