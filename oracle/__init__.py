@@ -17,6 +17,9 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
                minimum time-to-start, minimum disruption), clipping at the window bounds and
                degenerate windows, infeasible padding, top-k order and tie-break, per-class
                weights, node-permutation equivariance.
+  degradation_cost - pinned: brute force over priority prefixes (the shortest prefix of the
+               level-sorted engines that frees R), closed forms (R <= 0, one engine, Failure), the
+               interrupt penalty exactly when a level-4/5 engine is in the plan, stable order.
   quantiles  - pinned: numpy's percentile selection ("lower" / "higher" methods).
   prioritize - pinned: closed forms (unit latencies), numpy stable argsort, O(len^2) suffix
                sums, half-even rounding cases, int32 clamping, non-finite latency handling.
@@ -62,7 +65,9 @@ def _load():
     lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
     lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
-                                         f64, i32, P, P, i32]
+                                         f64, i32, P, P, P, P, ctypes.c_float, P, P, i32]
+    lib.oracle_degradation_cost.argtypes = [f64, i32, P, P, P, ctypes.c_float, P]
+    lib.oracle_degradation_cost.restype = ctypes.c_int
     lib.oracle_route_fitness.restype = ctypes.c_int
     lib.oracle_quantiles.argtypes = [P, i64, f64, f64, P]
     lib.oracle_quantiles.restype = ctypes.c_int
@@ -152,10 +157,12 @@ def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s,
 
 def route_fitness(model_id, src_id, class_id, kv_bytes, free_bytes, queue_ms, act_ms, resident_mask,
                   deg_ms, rtt_ms, class_weights, bounds, k: int = 1, rho: float = 0.0, n_models: int = 0,
-                  n_threads: int = 0):
+                  n_threads: int = 0, engines=None):
     """Alg. 3 with the fitness of Eq. 5. rtt_ms [n_src][M]; class_weights [n_classes][3] =
-    (gamma, lambda, mu); bounds [6] = window bounds (lo, hi) of RTT, T_ready, C_deg. Returns
-    (node_idx int32 [N][k], fitness float32 [N][k])."""
+    (gamma, lambda, mu); bounds [6] = window bounds (lo, hi) of RTT, T_ready, C_deg. With
+    ``engines`` = (offset [M+1] int32, level [E] int32, freed [E] float64, cost [E] float32,
+    c_int) the disruption cost is Alg. 2 / Eq. 4's per (stage, node) and ``deg_ms`` is unused.
+    Returns (node_idx int32 [N][k], fitness float32 [N][k])."""
     lib = _load()
     mi = _c(model_id, np.int32)
     n = mi.shape[0]
@@ -168,13 +175,31 @@ def route_fitness(model_id, src_id, class_id, kv_bytes, free_bytes, queue_ms, ac
     M = fr.shape[0]
     idx = np.empty((n, k), np.int32)
     fit = np.empty((n, k), np.float32)
+    if engines is None:
+        eo = el = ef = ec = None
+        c_int = 0.0
+    else:
+        eo, el = _c(engines[0], np.int32), _c(engines[1], np.int32)
+        ef, ec = _c(engines[2], np.float64), _c(engines[3], np.float32)
+        c_int = float(engines[4])
     st = lib.oracle_route_fitness(n, _ptr(mi), _ptr(si), _ptr(ci), _ptr(kv), n_models or 64, M,
                                   rtt.shape[0], cw.shape[0], _ptr(fr), _ptr(q), _ptr(act), _ptr(rm),
                                   _ptr(dg), _ptr(rtt), _ptr(cw), _ptr(bd), float(rho), int(k),
+                                  _ptr(eo), _ptr(el), _ptr(ef), _ptr(ec), c_int,
                                   _ptr(idx), _ptr(fit), n_threads or max_threads())
     if st != 0:
         raise RuntimeError(f"oracle_route_fitness failed with status {st}")
     return idx, fit
+
+
+def degradation_cost(R: float, level, freed, cost, c_int: float):
+    """Alg. 2 + Eq. 4 on one node's engines: the disruption cost of the minimum-impact plan that
+    frees R bytes, or None when no plan frees enough (Failure)."""
+    lib = _load()
+    lv, fr, co = _c(level, np.int32), _c(freed, np.float64), _c(cost, np.float32)
+    out = np.zeros(1, np.float32)
+    st = lib.oracle_degradation_cost(float(R), lv.shape[0], _ptr(lv), _ptr(fr), _ptr(co), float(c_int), _ptr(out))
+    return None if st else float(out[0])
 
 
 def quantiles(values, q_lo: float = 0.05, q_hi: float = 0.95):

@@ -236,6 +236,45 @@ static float norm01(float x, float lo, float inv) {
   return t;
 }
 
+/* Alg. 2 + Eq. 4 on one node: the engines of the node (levels 1..5 = the action taken for each:
+ * idle-running -> sleeping, evict sleeping, stop a pending sleep, swap out an active engine's KV,
+ * abort an active execution) in priority order (SortByPriority: ascending level, lower engine
+ * index first), taken greedily until the freed memory covers R. Returns 0 when the plan meets R
+ * (cost in *c_deg), 1 on Failure. Levels 4 and 5 preempt/abort active work (I_active). */
+typedef struct { int32_t level, idx; } eng_t;
+static int eng_less(eng_t a, eng_t b) { return a.level < b.level || (a.level == b.level && a.idx < b.idx); }
+
+static int degradation_plan(double R, int32_t e0, int32_t e1, const int32_t* level, const double* freed,
+                            const float* cost, float c_int, float* c_deg) {
+  eng_t order[64];
+  int32_t ne = e1 - e0;
+  if (ne > 64) ne = 64;
+  for (int32_t i = 0; i < ne; ++i) {              /* SortByPriority: insertion sort, stable */
+    eng_t e = {level[e0 + i], e0 + i};
+    int32_t j = i;
+    while (j > 0 && eng_less(e, order[j - 1])) { order[j] = order[j - 1]; --j; }
+    order[j] = e;
+  }
+  double m_freed = 0.0;
+  float plan_cost = 0.0f;
+  int interrupt = 0;
+  for (int32_t i = 0; i < ne; ++i) {
+    if (m_freed >= R) break;
+    const int32_t e = order[i].idx;
+    if (order[i].level >= 4) interrupt = 1;       /* Preempt / Abort */
+    m_freed += freed[e];                          /* EstimateFreedMemory */
+    plan_cost += cost[e];                         /* c(e, a) */
+  }
+  if (m_freed < R) return 1;                      /* Failure */
+  *c_deg = plan_cost + (interrupt ? c_int : 0.0f);  /* Eq. 4 */
+  return 0;
+}
+
+int oracle_degradation_cost(double R, int32_t n_engines, const int32_t* level, const double* freed,
+                            const float* cost, float c_int, float* c_deg) {
+  return degradation_plan(R, 0, n_engines, level, freed, cost, c_int, c_deg);
+}
+
 typedef struct { float s; int32_t n; } fcand_t;
 /* larger fitness first; equal fitness: lower node index first (the strict ">" of Alg. 3) */
 static int fcand_better(fcand_t a, fcand_t b) { return a.s > b.s || (a.s == b.s && a.n < b.n); }
@@ -246,6 +285,8 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
                          const double* free_bytes, const float* queue_ms, const float* act_ms,
                          const uint64_t* resident_mask, const float* deg_ms, const float* rtt_ms,
                          const float* class_weights, const float* bounds, double rho, int32_t k,
+                         const int32_t* engine_offset, const int32_t* engine_level,
+                         const double* engine_freed, const float* engine_cost, float c_int,
                          int32_t* node_idx, float* fitness, int32_t n_threads) {
   if (n < 0 || n_nodes < 1 || n_models < 1 || n_models > 64 || n_src < 1 || n_classes < 1 ||
       k < 1 || rho < 0.0)
@@ -277,7 +318,21 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
         const float needf = (float)need;
         int32_t nc = 0;
         for (int32_t nd = 0; nd < n_nodes; ++nd) {
-          if (need > free_bytes[nd]) continue;              /* FilterByPolicyAndFeasibility */
+          /* FilterByPolicyAndFeasibility; C_deg as the runtime reports it: per node, or, with
+           * engine lists, the cost of the minimum-impact plan for the shortfall (Alg. 2, Eq. 4),
+           * 0 when the stage fits, and the node infeasible when no plan frees enough */
+          float c_deg;
+          if (engine_offset) {
+            if (need <= free_bytes[nd]) {
+              c_deg = 0.0f;
+            } else if (degradation_plan(need - free_bytes[nd], engine_offset[nd], engine_offset[nd + 1],
+                                        engine_level, engine_freed, engine_cost, c_int, &c_deg)) {
+              continue;
+            }
+          } else {
+            if (need > free_bytes[nd]) continue;
+            c_deg = deg_ms[nd];
+          }
           /* Affinity: network proximity (decreasing in the normalised RTT) and best fit of
            * R_need to the node's headroom (1 when the stage fills the headroom exactly) */
           const float prox = 1.0f - norm01(rtt_row[nd], bounds[0], inv_rtt);
@@ -289,7 +344,7 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
           const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
           const float ready = queue_ms[nd] + (resident ? 0.0f : act_ms[nd]);
           /* Eq. 5: S = A - lambda * T_ready - mu * C_deg, on normalised metrics */
-          const float s = (a - lambda * norm01(ready, bounds[2], inv_ready)) - mu * norm01(deg_ms[nd], bounds[4], inv_deg);
+          const float s = (a - lambda * norm01(ready, bounds[2], inv_ready)) - mu * norm01(c_deg, bounds[4], inv_deg);
           c[nc].s = s;
           c[nc].n = nd;
           ++nc;

@@ -166,3 +166,81 @@ def test_node_permutation_equivariance():
     ok = idx[:, 0] >= 0
     assert (ok == (idx2[:, 0] >= 0)).all()
     assert (perm[idx2[ok, 0]] == idx[ok, 0]).all() and (fit2 == fit).all()
+
+
+# ---- minimum-impact degradation (Alg. 2) and its cost (Eq. 4) ---------------------------------
+
+def test_degradation_plan_closed_forms():
+    dc = oracle.degradation_cost
+    # one engine: enough frees it alone, too little is a Failure
+    assert dc(5.0, [1], [5.0], [7.5], 100.0) == 7.5            # freed == R suffices (stop at >=)
+    assert dc(5.1, [1], [5.0], [7.5], 100.0) is None
+    # priority order: the level-1 engine (listed second) is taken first and suffices alone
+    assert dc(3.0, [2, 1], [10.0, 4.0], [50.0, 2.0], 100.0) == 2.0
+    # equal levels: lower index first
+    assert dc(3.0, [1, 1], [4.0, 4.0], [2.0, 9.0], 100.0) == 2.0
+    # the check comes before each engine: exactly covered by the first two -> the third is not taken
+    assert dc(6.0, [1, 2, 3], [2.0, 4.0, 8.0], [1.0, 10.0, 100.0], 1000.0) == 11.0
+    # the interrupt penalty is charged only when an active engine (level 4 or 5) is in the plan
+    assert dc(2.0, [1, 4], [2.0, 8.0], [1.0, 3.0], 1000.0) == 1.0
+    assert dc(3.0, [1, 4], [2.0, 8.0], [1.0, 3.0], 1000.0) == 1004.0
+    assert dc(3.0, [1, 5], [2.0, 8.0], [1.0, 3.0], 1000.0) == 1004.0
+    assert dc(3.0, [1, 3], [2.0, 8.0], [1.0, 3.0], 1000.0) == 4.0
+    # nothing required: an empty plan
+    assert dc(0.0, [4], [1.0], [9.0], 1000.0) == 0.0
+    assert dc(-1.0, [], [], [], 1000.0) == 0.0
+    assert dc(1.0, [], [], [], 1000.0) is None
+
+
+def test_degradation_plan_is_the_shortest_sufficient_priority_prefix():
+    rng = np.random.default_rng(8)
+    for _ in range(500):
+        ne = int(rng.integers(0, 9))
+        level = rng.integers(1, 6, ne).astype(np.int32)
+        freed = rng.choice([1.0, 2.0, 3.0, 5.0], ne)             # coarse: many exact coverings
+        cost = rng.uniform(0, 100, ne).astype(np.float32)
+        R = float(rng.choice([0.5, 1.0, 2.0, 3.0, 4.0, 7.0, 11.0, 30.0]))
+        order = sorted(range(ne), key=lambda i: (level[i], i))
+        want = None
+        for j in range(1, ne + 1):                               # shortest prefix freeing R
+            if sum(freed[order[:j]]) >= R:
+                plan = order[:j]
+                c = np.float32(0)
+                for i in plan:
+                    c = np.float32(c + cost[i])
+                want = float(np.float32(c + (np.float32(250) if (level[plan] >= 4).any() else np.float32(0))))
+                break
+        assert oracle.degradation_cost(R, level, freed, cost, 250.0) == want
+
+
+def test_fitness_with_degradation_plans():
+    # node 0 cannot admit the stage and has no plan; node 1 needs a plan; node 2 fits outright
+    nodes = dict(free_bytes=np.array([10, 10, 100], float) * GB,
+                 queue_ms=np.zeros(3, np.float32), act_ms=np.zeros(3, np.float32),
+                 resident_mask=np.zeros(3, np.uint64), deg_ms=np.zeros(3, np.float32),
+                 rtt_ms=np.zeros((1, 3), np.float32))
+    eng = (np.array([0, 0, 2, 2], np.int32), np.array([1, 4], np.int32), np.array([5, 20], float) * GB,
+           np.array([100, 300], np.float32), 1000.0)
+    one = np.zeros(1, np.int32)
+    b = [0, 1, 0, 1, 0, 2000]
+    route = lambda kv, w, k=3: oracle.route_fitness(one, one, one, np.array([kv]), nodes["free_bytes"], nodes["queue_ms"],
+                                                    nodes["act_ms"], nodes["resident_mask"], nodes["deg_ms"],
+                                                    nodes["rtt_ms"], np.array(w, np.float32).reshape(1, 3),
+                                                    np.array(b, np.float32), k=k, engines=eng)
+    # gamma = 1 with equal proximity everywhere: S = 1 - norm(C_deg), C_deg window [0, 2000] ms
+    # 12 GB: node 1 frees 5 GB (level 1, cost 100) -> feasible with C_deg = 100; node 0 infeasible
+    idx, fit = route(12 * GB, [1, 0, 1])
+    assert idx[0].tolist() == [2, 1, -1]
+    assert fit[0, 0] == 1.0 and abs(fit[0, 1] - (1 - 100 / 2000)) < 1e-6
+    # 20 GB: node 1 needs both engines (C_deg = 100 + 300 + interrupt 1000 = 1400)
+    idx, fit = route(20 * GB, [1, 0, 1])
+    assert idx[0].tolist() == [2, 1, -1] and abs(fit[0, 1] - (1 - 1400 / 2000)) < 1e-6
+    # 40 GB: node 1 cannot free enough either; only node 2
+    idx, _ = route(40 * GB, [1, 0, 1])
+    assert idx[0].tolist() == [2, -1, -1]
+    # with mu = 0 feasibility equals "need <= headroom + everything freeable" (node 1: 35 GB)
+    rng = np.random.default_rng(9)
+    for kv in rng.uniform(0, 120, 200) * GB:
+        idx, _ = route(kv, [0, 1, 0])
+        feas = {j for j, cap in enumerate([10, 35, 100]) if kv <= cap * GB}
+        assert {j for j in idx[0] if j >= 0} == feas
