@@ -4,6 +4,7 @@ python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c3] [--no-cpu-ba
 python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for counter calibration)
 python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
 python bench.py --route-fitness        (routing by fitness, Eq. 5, on the workload's predictions)
+python bench.py --route-fitness --plans   (the same with C_deg from degradation plans, Alg. 2)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -169,9 +170,24 @@ def sweep_prioritize(log2_lo: int, log2_hi: int, steps: int, warmup: int):
         torch.cuda.empty_cache()
 
 
-def route_fitness_bench(name: str, steps: int, warmup: int):
+def _time_events(call, steps: int, warmup: int):
+    import torch
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record()
+        call()
+        e1.record()
+    torch.cuda.synchronize()
+    return [e0.elapsed_time(e1) for e0, e1 in ev]
+
+
+def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False):
     """Routing by fitness over the workload's stages, on the GPU's own predictions; bounds from
-    the recent-observation windows (maestro_quantiles). One JSON line."""
+    the recent-observation windows (maestro_quantiles). With ``plans`` C_deg comes from the
+    nodes' degradation plans (built once, timed on their own). One JSON line."""
     import torch
     from paper_2606_12950_amd import _native, pipeline
     from paper_2606_12950_amd import workload as W
@@ -184,25 +200,31 @@ def route_fitness_bench(name: str, steps: int, warmup: int):
     t = lambda a: pipeline._t(a, "cuda")
     fd = dict(src=t(f.src_id), cls=t(f.class_id), queue=t(f.queue_ms), act=t(f.act_ms), deg=t(f.deg_ms),
               rtt=t(f.rtt_ms), weights=t(f.class_weights))
+    extra = {}
+    plan_t = None
+    if plans:
+        e = W.engine_inputs(wl)
+        eng = [t(e.engine_offset), t(e.level), t(e.freed_bytes), t(e.cost_ms)]
+        plan_t = _native.degradation_plans(*eng, e.c_int_ms)
+        dp = _time_events(lambda: _native.degradation_plans(*eng, e.c_int_ms, out=plan_t), steps, warmup)
+        deg_window = e.deg_window
+        extra = {"plans": True, "n_engines": int(e.level.shape[0]), "plan_ms": percentiles(dp)}
+    else:
+        deg_window = f.deg_window
     bounds = torch.cat([_native.quantiles(t(f.rtt_window)), _native.quantiles(t(f.ready_window)),
-                        _native.quantiles(t(f.deg_window))])
+                        _native.quantiles(t(deg_window))])
     n, m = wl.n, wl.spec.n_nodes
     out = (torch.empty((n, wl.spec.k), dtype=torch.int32, device="cuda"),
            torch.empty((n, wl.spec.k), dtype=torch.float32, device="cuda"))
     call = lambda: _native.route_fitness(b.model_id, fd["src"], fd["cls"], o.kv_bytes, b.free_bytes, fd["queue"],
-                                         fd["act"], b.resident_mask, fd["deg"], fd["rtt"], fd["weights"], bounds,
-                                         n_models=wl.spec.n_models, k=wl.spec.k, rho=wl.spec.rho, out=out)
-    for _ in range(warmup):
-        call()
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for e0, e1 in ev:
-        e0.record()
-        call()
-        e1.record()
-    torch.cuda.synchronize()
-    d = [e0.elapsed_time(e1) for e0, e1 in ev]
+                                         fd["act"], b.resident_mask, None if plans else fd["deg"], fd["rtt"],
+                                         fd["weights"], bounds, n_models=wl.spec.n_models, k=wl.spec.k,
+                                         rho=wl.spec.rho, plans=plan_t, out=out)
+    d = _time_events(call, steps, warmup)
     ms = float(np.mean(d))
+    if plans:
+        need = o.kv_bytes.double() * (1.0 + wl.spec.rho)
+        extra["short_pair_frac"] = round(float((need[:, None] > b.free_bytes[None, :]).float().mean().item()), 4)
     pairs = n * m
     achieved = pairs * FITNESS_OPS_PER_PAIR / (ms * 1e-3)
     print(json.dumps({"route_fitness": name, "n_stages": n, "n_nodes": m, "k": wl.spec.k, "ms": round(ms, 4),
@@ -210,7 +232,7 @@ def route_fitness_bench(name: str, steps: int, warmup: int):
                       "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_VALU_LANE_OPS / 1e12,
                                    "unit": "T lane-ops/s", "frac": round(achieved / PEAK_VALU_LANE_OPS, 4),
                                    "ops_per_pair": FITNESS_OPS_PER_PAIR},
-                      "routed_frac": float((out[0][:, 0] >= 0).float().mean().item())}), flush=True)
+                      "routed_frac": float((out[0][:, 0] >= 0).float().mean().item()), **extra}), flush=True)
 
 
 def main():
@@ -226,13 +248,16 @@ def main():
                     help="time the slack ordering alone for W = 2^LO .. 2^HI workflows")
     ap.add_argument("--route-fitness", action="store_true",
                     help="time routing by fitness (Eq. 5) on the workload's predictions")
+    ap.add_argument("--plans", action="store_true",
+                    help="with --route-fitness: C_deg from degradation plans (Alg. 2, Eq. 4)")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
         return
     if args.route_fitness:
-        route_fitness_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
+        route_fitness_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)),
+                            plans=args.plans)
         return
     if args.sweep_prioritize:
         lo, hi = (int(v) for v in args.sweep_prioritize.split(":"))

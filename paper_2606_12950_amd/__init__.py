@@ -5,10 +5,11 @@ include/maestro.h); this package is its thin Python binding plus the seeded work
 generator. PyTorch supplies device memory and streams only.
 """
 from ._native import (LIBRARY_PATH, MaestroError, Predictor, load, make_predictor, predict,
-                      prioritize, prioritize_workspace_bytes, quantiles, route, route_fitness)
+                      degradation_plans, prioritize, prioritize_workspace_bytes, quantiles, route,
+                      route_fitness)
 from .pipeline import DeviceBatch, StepOutputs, run_step, to_device
 
-__all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "load", "make_predictor", "predict",
+__all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "load", "make_predictor", "predict", "degradation_plans",
            "prioritize", "prioritize_workspace_bytes", "quantiles", "route", "route_fitness",
            "DeviceBatch", "StepOutputs",
            "run_step", "to_device"]

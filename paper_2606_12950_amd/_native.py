@@ -22,10 +22,13 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 
 # Every function declared in include/maestro.h.
 EXPORTS = ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
-           "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
+           "maestro_degradation_plans", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
+
+MAX_PLAN_ENGINES = 8
+PLAN_BYTES = 128   # one maestro_deg_plan record: freed f64[8], cost f32[8], n_engines i32, pad
 
 
 class MaestroError(RuntimeError):
@@ -57,8 +60,9 @@ def load():
     lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
-    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
+    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
                                           f64, i32, P, P, P]
+    lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
     for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize"):
@@ -200,16 +204,17 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
 
 def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.Tensor,
                   kv_bytes: torch.Tensor, free_bytes: torch.Tensor, queue_ms: torch.Tensor,
-                  act_ms: torch.Tensor, resident_mask: torch.Tensor, deg_ms: torch.Tensor,
+                  act_ms: torch.Tensor, resident_mask: torch.Tensor, deg_ms: Optional[torch.Tensor],
                   rtt_ms: torch.Tensor, class_weights: torch.Tensor, bounds: torch.Tensor,
-                  n_models: int, k: int = 1, rho: float = 0.0,
+                  n_models: int, k: int = 1, rho: float = 0.0, plans: Optional[torch.Tensor] = None,
                   out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """maestro_route_fitness: returns (node_idx int32 [N][k], fitness float32 [N][k]).
 
     ``rtt_ms`` is [n_src][n_nodes], ``class_weights`` [n_classes][3] = (gamma, lambda, mu),
     ``bounds`` [6] = (lo, hi) of RTT, T_ready, C_deg; ``resident_mask`` is int64 on the torch
-    side (same bits as the C-ABI's uint64)."""
+    side (same bits as the C-ABI's uint64). With ``plans`` (from :func:`degradation_plans`)
+    C_deg comes from the node's degradation plan and ``deg_ms`` may be None."""
     lib = load()
     _dev(model_id, "model_id", torch.int32)
     n = model_id.shape[0]
@@ -217,15 +222,25 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     _dev(class_id, "class_id", torch.int32)
     _dev(kv_bytes, "kv_bytes", torch.float64)
     _dev(free_bytes, "free_bytes", torch.float64)
-    for t, name in ((queue_ms, "queue_ms"), (act_ms, "act_ms"), (deg_ms, "deg_ms"), (rtt_ms, "rtt_ms"),
+    for t, name in ((queue_ms, "queue_ms"), (act_ms, "act_ms"), (rtt_ms, "rtt_ms"),
                     (class_weights, "class_weights"), (bounds, "bounds")):
         _dev(t, name, torch.float32)
     _dev(resident_mask, "resident_mask", torch.int64)
     M = free_bytes.shape[0]
     if src_id.shape[0] != n or class_id.shape[0] != n or kv_bytes.shape[0] != n:
         raise ValueError("per-stage inputs must have the same length")
-    if queue_ms.shape[0] != M or act_ms.shape[0] != M or resident_mask.shape[0] != M or deg_ms.shape[0] != M:
+    if queue_ms.shape[0] != M or act_ms.shape[0] != M or resident_mask.shape[0] != M:
         raise ValueError("per-node inputs must have the same length")
+    if plans is not None:
+        _dev(plans, "plans", torch.uint8)
+        if tuple(plans.shape) != (M, PLAN_BYTES):
+            raise ValueError("plans must be uint8 [n_nodes][128]")
+    if deg_ms is not None:
+        _dev(deg_ms, "deg_ms", torch.float32)
+        if deg_ms.shape[0] != M:
+            raise ValueError("per-node inputs must have the same length")
+    elif plans is None:
+        raise ValueError("deg_ms is required without plans")
     if rtt_ms.dim() != 2 or rtt_ms.shape[1] != M:
         raise ValueError("rtt_ms must be [n_src][n_nodes]")
     if class_weights.dim() != 2 or class_weights.shape[1] != 3 or bounds.numel() != 6:
@@ -239,10 +254,42 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     st = lib.maestro_route_fitness(n, _ptr(model_id), _ptr(src_id), _ptr(class_id), _ptr(kv_bytes),
                                    int(n_models), M, rtt_ms.shape[0], class_weights.shape[0],
                                    _ptr(free_bytes), _ptr(queue_ms), _ptr(act_ms), _ptr(resident_mask),
-                                   _ptr(deg_ms), _ptr(rtt_ms), _ptr(class_weights), _ptr(bounds),
+                                   _ptr(deg_ms) if deg_ms is not None else None,
+                                   _ptr(plans) if plans is not None else None,
+                                   _ptr(rtt_ms), _ptr(class_weights), _ptr(bounds),
                                    float(rho), int(k), _ptr(idx), _ptr(fit), _stream(stream))
     _check("maestro_route_fitness", st)
     return idx, fit
+
+
+def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, engine_freed_bytes: torch.Tensor,
+                      engine_cost_ms: torch.Tensor, c_int_ms: float, out: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """maestro_degradation_plans: uint8 [n_nodes][128] plan records (maestro_deg_plan) from the
+    engines of every node in CSR form (``engine_offset`` int32 [n_nodes + 1], at most 8 engines a
+    node; ``engine_level`` int32, ``engine_freed_bytes`` float64, ``engine_cost_ms`` float32)."""
+    lib = load()
+    _dev(engine_offset, "engine_offset", torch.int32)
+    _dev(engine_level, "engine_level", torch.int32)
+    _dev(engine_freed_bytes, "engine_freed_bytes", torch.float64)
+    _dev(engine_cost_ms, "engine_cost_ms", torch.float32)
+    M = engine_offset.shape[0] - 1
+    if M < 0:
+        raise ValueError("engine_offset holds n_nodes + 1 entries")
+    E = engine_level.shape[0]
+    if engine_freed_bytes.shape[0] != E or engine_cost_ms.shape[0] != E:
+        raise ValueError("per-engine inputs must have the same length")
+    if out is None:
+        out = torch.empty((M, PLAN_BYTES), dtype=torch.uint8, device=engine_offset.device)
+    _dev(out, "plans", torch.uint8)
+    if tuple(out.shape) != (M, PLAN_BYTES):
+        raise ValueError("plans must be uint8 [n_nodes][128]")
+    st = lib.maestro_degradation_plans(M, _ptr(engine_offset), _ptr(engine_level) if E else None,
+                                       _ptr(engine_freed_bytes) if E else None,
+                                       _ptr(engine_cost_ms) if E else None, float(c_int_ms), _ptr(out),
+                                       _stream(stream))
+    _check("maestro_degradation_plans", st)
+    return out
 
 
 def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,

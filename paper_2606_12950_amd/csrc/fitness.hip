@@ -18,6 +18,12 @@
 // fixed order (explicit intrinsics, no contraction), so the fitness values are reproducible bit
 // for bit by a sequential evaluation of the same expression.
 //
+// With degradation plans (Alg. 2, Eq. 4), C_deg is per pair: 0 when the stage fits, else the
+// cost of the shortest priority prefix of the node's engines that frees the shortfall, and the
+// node drops out when no prefix does. The plan records (running freed bytes and costs, one per
+// prefix) are built once per node state and staged in LDS with the other node terms; only lanes
+// whose stage does not fit search them, so a wavefront in which every stage fits skips that.
+//
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
 #include <type_traits>
@@ -29,8 +35,7 @@ namespace maestro {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kChunk = 512;              // nodes staged in LDS at a time
-constexpr int kProxStride = kChunk + 1;  // one-word pad: rows of different sources in different banks
+constexpr int kMaxPlan = MAESTRO_MAX_PLAN_ENGINES;
 
 __device__ __forceinline__ float norm_inv(float lo, float hi) {
   return hi > lo ? __fdiv_rn(1.0f, __fsub_rn(hi, lo)) : 0.0f;
@@ -42,13 +47,69 @@ __device__ __forceinline__ float norm01(float x, float lo, float inv) {
   return t;
 }
 
-template <int KT, bool kMask64>
+// Plan records from the engine lists, one thread per node. SortByPriority orders the engines by
+// ascending level, the lower engine index first (a fixed compare-exchange network over keys
+// level:index); the running sums then follow that order: freed bytes in float64, costs in
+// float32, and c_int added to every prefix that holds an engine of level 4 or 5. The freed
+// column keeps the largest running sum so far, so it never decreases (it is the running sum
+// itself when no action frees a negative amount): the first prefix whose running sum reaches
+// a shortfall is then also the first whose entry does, and a stage finds it by counting the
+// entries below its shortfall. Entries past the node's engines hold +inf.
+__global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const int32_t* __restrict__ engine_offset,
+                                                        const int32_t* __restrict__ engine_level,
+                                                        const double* __restrict__ engine_freed,
+                                                        const float* __restrict__ engine_cost, float c_int,
+                                                        maestro_deg_plan* __restrict__ plans) {
+  const int32_t j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= n_nodes) return;
+  const int32_t e0 = engine_offset[j];
+  int32_t ne = engine_offset[j + 1] - e0;   // at most kMaxPlan by contract; clamped all the same
+  ne = ne < 0 ? 0 : (ne > kMaxPlan ? kMaxPlan : ne);
+  int64_t key[kMaxPlan];
+#pragma unroll
+  for (int i = 0; i < kMaxPlan; ++i)
+    key[i] = i < ne ? ((int64_t)engine_level[e0 + i] << 8 | i) : INT64_MAX;
+#pragma unroll
+  for (int pass = 0; pass < kMaxPlan; ++pass) {
+#pragma unroll
+    for (int q = pass & 1; q + 1 < kMaxPlan; q += 2) {   // odd-even transposition sort
+      const int64_t a = key[q], b = key[q + 1];
+      key[q] = a < b ? a : b;
+      key[q + 1] = a < b ? b : a;
+    }
+  }
+  maestro_deg_plan out;
+  double freed = 0.0, top = 0.0;
+  float cost = 0.0f;
+  bool interrupt = false;
+#pragma unroll
+  for (int i = 0; i < kMaxPlan; ++i) {
+    if (i < ne) {
+      const int32_t e = e0 + (int32_t)(key[i] & 255);
+      interrupt = interrupt || (key[i] >> 8) >= 4;   // Preempt / Abort interrupt active work
+      freed = __dadd_rn(freed, engine_freed[e]);
+      cost = __fadd_rn(cost, engine_cost[e]);
+      top = i == 0 ? freed : fmax(top, freed);
+      out.freed[i] = top;
+      out.cost[i] = __fadd_rn(cost, interrupt ? c_int : 0.0f);
+    } else {
+      out.freed[i] = INFINITY;
+      out.cost[i] = 0.0f;
+    }
+  }
+  out.n_engines = ne;
+#pragma unroll
+  for (int i = 0; i < 7; ++i) out.reserved[i] = 0;
+  plans[j] = out;
+}
+
+template <int KT, bool kMask64, bool kPlans>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_nodes,
     int32_t n_src, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
     const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
-    const float* __restrict__ deg_ms, const float* __restrict__ rtt_ms,
+    const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
     const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
     int32_t* __restrict__ node_idx, float* __restrict__ fitness) {
   // per node, two 16-byte records (one LDS read each, the same address for every lane):
@@ -56,11 +117,15 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   //          norm(T_q + T_act), norm(C_deg)
   //   admit: KV admission headroom and the residency bits (the low 32 when no model id
   //          exceeds 31)
+  // and with plans the node's plan record (norm(C_deg) then depends on the stage).
   typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
+  constexpr int kChunk = kPlans ? 256 : 512;   // nodes staged in LDS at a time
+  constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
   struct Admit { double free; uint64_t mask; };
   __shared__ float4 s_terms[kChunk];
   __shared__ Admit s_admit[kChunk];
   __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
+  __shared__ maestro_deg_plan s_plan[kPlans ? kChunk : 1];
 
   const int tid = threadIdx.x;
   const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
@@ -69,6 +134,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   const float inv_r = norm_inv(bounds[0], bounds[1]);
   const float inv_t = norm_inv(bounds[2], bounds[3]);
   const float inv_d = norm_inv(bounds[4], bounds[5]);
+  const float nd_fits = norm01(0.0f, lo_d, inv_d);   // normalised C_deg of a stage that fits
 
   double need = INFINITY;   // an invalid lane admits nothing
   float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
@@ -99,8 +165,10 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       const float q = queue_ms[j];
       s_terms[i] = make_float4(frf > 0.0f ? __fdiv_rn(1.0f, frf) : INFINITY,
                                norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
-                               norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t), norm01(deg_ms[j], lo_d, inv_d));
+                               norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
+                               kPlans ? nd_fits : norm01(deg_ms[j], lo_d, inv_d));
       s_admit[i] = Admit{fr, resident_mask[j]};
+      if (kPlans) s_plan[i] = plans[j];
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
@@ -108,20 +176,49 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
           __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, inv_r));
     }
     __syncthreads();
-    // branch-free: every node is scored; an infeasible one offers the key +inf, which never
-    // enters the list (FilterByPolicyAndFeasibility)
-#pragma unroll 4
-    for (int i = 0; i < cn; ++i) {
-      const float4 t = s_terms[i];
-      const Admit ad = s_admit[i];
+    // every node is scored; an infeasible one offers the key +inf, which never enters the list
+    // (FilterByPolicyAndFeasibility)
+    auto pair = [&](int i, const float4 t, const Admit ad, float prox) {
       // fit = min(1, fl32(need) / fl32(headroom)); with zero headroom only need = 0 is
       // feasible, and min(0 * inf = NaN, 1) = 1 (IEEE min returns the number), the fit of a
       // stage that fills the node exactly
       const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
-      const float a = __fadd_rn(__fmul_rn(gamma, prox_row[i]), __fmul_rn(omg, fit));
+      const float a = __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
       const float nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
-      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, t.w));
-      best.push_increasing(need <= ad.free ? -sc : INFINITY, c0 + i);
+      bool ok = need <= ad.free;
+      float nd = t.w;
+      if (kPlans && !ok) {   // shortfall: the first prefix of the plan that frees it, if any
+        const maestro_deg_plan& pl = s_plan[i];
+        const double R = __dsub_rn(need, ad.free);
+        int jp = 0;
+#pragma unroll
+        for (int e = 0; e < kMaxPlan; ++e) jp += pl.freed[e] < R ? 1 : 0;
+        ok = jp < pl.n_engines;
+        nd = norm01(pl.cost[ok ? jp : 0], lo_d, inv_d);
+      }
+      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
+      best.push_increasing(ok ? -sc : INFINITY, c0 + i);
+    };
+    if (kPlans) {
+      // the next node's terms are read before this node's shortfall branch, so their LDS
+      // latency overlaps it
+      float4 t = s_terms[0];
+      Admit ad = s_admit[0];
+      float px = prox_row[0];
+#pragma unroll 2
+      for (int i = 0; i < cn; ++i) {
+        const int in = i + 1 < cn ? i + 1 : i;
+        const float4 tn = s_terms[in];
+        const Admit adn = s_admit[in];
+        const float pxn = prox_row[in];
+        pair(i, t, ad, px);
+        t = tn;
+        ad = adn;
+        px = pxn;
+      }
+    } else {
+#pragma unroll 4
+      for (int i = 0; i < cn; ++i) pair(i, s_terms[i], s_admit[i], prox_row[i]);
     }
   }
 
@@ -188,24 +285,25 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     int32_t n_nodes, int32_t n_src, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* deg_ms,
-                                    const float* rtt_ms, const float* class_weights,
+                                    const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,
                                     const float* bounds, double rho, int32_t k, int32_t* node_idx,
                                     float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
   const bool mask64 = n_models > 32;
-#define MAESTRO_FIT_KT(KT)                                                                                \
-  do {                                                                                                    \
-    if (mask64)                                                                                           \
-      fitness_kernel<KT, true><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,       \
-                                                           n_nodes, n_src, free_bytes, queue_ms, act_ms,  \
-                                                           resident_mask, deg_ms, rtt_ms, class_weights,  \
-                                                           bounds, rho, k, node_idx, fitness);            \
-    else                                                                                                  \
-      fitness_kernel<KT, false><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,      \
-                                                            n_nodes, n_src, free_bytes, queue_ms, act_ms, \
-                                                            resident_mask, deg_ms, rtt_ms, class_weights, \
-                                                            bounds, rho, k, node_idx, fitness);           \
+  const bool with_plans = plans != nullptr;
+#define MAESTRO_FIT_LAUNCH(KT, M64, PL)                                                                  \
+  fitness_kernel<KT, M64, PL><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,      \
+                                                          n_nodes, n_src, free_bytes, queue_ms, act_ms, \
+                                                          resident_mask, deg_ms, plans, rtt_ms,         \
+                                                          class_weights, bounds, rho, k, node_idx, fitness)
+#define MAESTRO_FIT_KT(KT)                                                                        \
+  do {                                                                                            \
+    if (with_plans) {                                                                             \
+      if (mask64) MAESTRO_FIT_LAUNCH(KT, true, true); else MAESTRO_FIT_LAUNCH(KT, false, true);   \
+    } else {                                                                                      \
+      if (mask64) MAESTRO_FIT_LAUNCH(KT, true, false); else MAESTRO_FIT_LAUNCH(KT, false, false); \
+    }                                                                                             \
   } while (0)
   if (k == 1) MAESTRO_FIT_KT(1);
   else if (k == 2) MAESTRO_FIT_KT(2);
@@ -213,6 +311,16 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
   else if (k <= 8) MAESTRO_FIT_KT(8);
   else MAESTRO_FIT_KT(16);
 #undef MAESTRO_FIT_KT
+#undef MAESTRO_FIT_LAUNCH
+  return launch_status();
+}
+
+maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_offset, const int32_t* engine_level,
+                                       const double* engine_freed_bytes, const float* engine_cost_ms, float c_int_ms,
+                                       maestro_deg_plan* plans, hipStream_t stream) {
+  if (n_nodes == 0) return MAESTRO_OK;
+  plan_kernel<<<dim3((unsigned)((n_nodes + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream>>>(
+      n_nodes, engine_offset, engine_level, engine_freed_bytes, engine_cost_ms, c_int_ms, plans);
   return launch_status();
 }
 

@@ -388,6 +388,58 @@ def fitness_inputs(wl: Workload) -> FitnessInputs:
                          ready_window=ready_window, deg_window=deg_window)
 
 
+ENGINE_STREAMS = ("count", "level", "size", "kv", "cost", "deg_window")
+# levels of Alg. 2's actions: 1 put an idle-running model to sleep, 2 evict a sleeping model,
+# 3 stop a pending sleep, 4 swap out an active model's KV, 5 abort an active execution
+ENGINE_LEVEL_P = (0.30, 0.20, 0.10, 0.25, 0.15)
+HOST_BW = 25e9           # bytes/s, host <-> GPU reload bandwidth of the stand-in cost model
+C_INT_MS = 2000.0        # interrupt penalty: an interactive SLO threshold (ms)
+
+
+@dataclass
+class EngineInputs:
+    """The resident engines of every node (CSR over nodes) with the action Alg. 2 would take
+    on each, the bytes it frees and its restoration cost, plus c_int and a window of recent
+    C_deg reports."""
+    engine_offset: np.ndarray     # [M + 1] int32
+    level: np.ndarray             # [E] int32 in 1..5
+    freed_bytes: np.ndarray       # [E] float64
+    cost_ms: np.ndarray           # [E] float32
+    c_int_ms: float
+    deg_window: np.ndarray        # [WINDOW] float32
+
+
+def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
+    """Stand-in engine lists for the nodes of ``wl`` (seeded by its spec's seed).
+
+    Each node hosts U{0..max_engines} engines; the action level is drawn with probabilities
+    ENGINE_LEVEL_P. Model sizes are bf16 weights of 0.6B-14B parameters (1.2-28 GB). Freed
+    bytes: the weights for levels 1 and 3, the retained runtime context (194-286 MB, the
+    paper's measured range) for level 2, the KV in use (U[1, 40] GB) for levels 4 and 5. Cost
+    (ms): reloading from host at HOST_BW for levels 1-3 (plus U[0.5, 3] s of context rebuild
+    for level 2), the KV reload at HOST_BW for level 4, and U[1, 10] s of KV regeneration for
+    level 5. The C_deg window is 80% zeros (stages that fit) and 20% U[100, 30000] ms."""
+    children = np.random.SeedSequence([wl.spec.seed, 0xDE6]).spawn(len(ENGINE_STREAMS))
+    r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(ENGINE_STREAMS, children)}
+    M = wl.free_bytes.shape[0]
+    count = r["count"].integers(0, max_engines + 1, M)
+    offset = np.zeros(M + 1, np.int32)
+    np.cumsum(count, out=offset[1:])
+    E = int(offset[-1])
+    level = (r["level"].choice(5, size=E, p=ENGINE_LEVEL_P) + 1).astype(np.int32)
+    weights = r["size"].uniform(0.6e9, 14e9, E) * 2.0
+    ctx = r["size"].uniform(194e6, 286e6, E)
+    kv = r["kv"].uniform(1e9, 40e9, E)
+    freed = np.where((level == 1) | (level == 3), weights, np.where(level == 2, ctx, kv))
+    reload_ms = np.where(level <= 3, weights, kv) / HOST_BW * 1e3
+    extra_ms = np.where(level == 2, r["cost"].uniform(500.0, 3000.0, E), 0.0)
+    cost = np.where(level == 5, r["cost"].uniform(1000.0, 10000.0, E), reload_ms + extra_ms)
+    deg_window = np.where(r["deg_window"].random(WINDOW) < 0.2,
+                          r["deg_window"].uniform(100.0, 30000.0, WINDOW), 0.0).astype(np.float32)
+    return EngineInputs(engine_offset=offset, level=level, freed_bytes=freed.astype(np.float64),
+                        cost_ms=cost.astype(np.float32), c_int_ms=C_INT_MS, deg_window=deg_window)
+
+
 def workload(name: str, with_x: bool = True, **overrides) -> Workload:
     """Named workload, optionally with fields of its spec replaced (e.g. ``n_stages=5000``)."""
     spec = SPECS[name]

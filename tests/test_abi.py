@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -48,6 +48,8 @@ _buf = (ctypes.c_double * 64)()
 FAKE = ctypes.c_void_p(ctypes.addressof(_buf))
 MISALIGNED = ctypes.c_void_p(ctypes.addressof(_buf) + 4)    # misaligned for 8-byte elements
 MISALIGNED4 = ctypes.c_void_p(ctypes.addressof(_buf) + 2)   # misaligned for 4-byte elements
+FAKE16 = ctypes.c_void_p(ctypes.addressof(_buf) + (-ctypes.addressof(_buf) % 16))   # 16-byte aligned
+MISALIGNED16 = ctypes.c_void_p(FAKE16.value + 8)            # 8- but not 16-byte aligned
 
 
 def _pred(dims, dtype, layers):
@@ -107,9 +109,11 @@ def test_route_validation(lib):
 
 
 def test_route_fitness_and_quantiles_validation(lib):
-    def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE):
+    def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE,
+             deg=FAKE, plans=None):
         return lib.maestro_route_fitness(n, FAKE, src, FAKE, FAKE, n_models, n_nodes, n_src, n_classes,
-                                         FAKE, FAKE, FAKE, FAKE, FAKE, rtt, FAKE, bounds, rho, k, FAKE, FAKE, None)
+                                         FAKE, FAKE, FAKE, FAKE, deg, plans, rtt, FAKE, bounds, rho, k, FAKE, FAKE,
+                                         None)
     assert call(n=-1) == INVALID
     assert call(n_models=0) == INVALID
     assert call(n_models=65) == INVALID
@@ -123,6 +127,10 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert call(rtt=None) == INVALID
     assert call(bounds=MISALIGNED4) == INVALID
     assert call(n=0, src=None) == OK                                          # empty batch: no-op
+    assert call(deg=None) == INVALID                                          # C_deg from nowhere
+    assert call(deg=None, plans=MISALIGNED16) == INVALID                      # plan records are 16-aligned
+    assert call(deg=None, plans=FAKE16, rtt=None) == INVALID
+    assert call(n=0, deg=None, plans=FAKE16) == OK                            # plans replace deg_ms
     q = lambda m=10, lo=0.05, hi=0.95, v=FAKE, out=FAKE: lib.maestro_quantiles(v, m, lo, hi, out, None)
     assert q(m=0) == INVALID
     assert q(lo=0.6, hi=0.5) == INVALID
@@ -132,6 +140,20 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert q(v=None) == INVALID
     assert q(out=MISALIGNED4) == INVALID
     assert q(m=1 << 32) == UNSUPPORTED
+
+
+def test_degradation_plans_validation(lib):
+    def call(n_nodes=4, off=FAKE, level=FAKE, freed=FAKE, cost=FAKE, c_int=2000.0, plans=FAKE16):
+        return lib.maestro_degradation_plans(n_nodes, off, level, freed, cost, c_int, plans, None)
+    assert call(n_nodes=-1) == INVALID
+    assert call(c_int=float("nan")) == INVALID
+    assert call(off=None) == INVALID
+    assert call(plans=None) == INVALID
+    assert call(plans=MISALIGNED16) == INVALID
+    assert call(level=MISALIGNED4) == INVALID
+    assert call(freed=MISALIGNED) == INVALID
+    assert call(n_nodes=0, off=None, plans=None) == OK                        # no nodes: no-op
+    assert ctypes.sizeof(ctypes.c_double) * 8 + 4 * 8 + 4 * 8 == _native.PLAN_BYTES
 
 
 def test_prioritize_validation_and_workspace(lib):

@@ -141,3 +141,164 @@ def test_fitness_workload_full(name):
     assert_same(got, ref)
     routed = (got[0][:, 0] >= 0).mean()
     print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes, {routed:.4f} routed, fitness identical")
+
+
+# ---- degradation plans (Alg. 2, Eq. 4) ----------------------------------------------------------
+
+def _engines(rng, M_, max_e=8, level_p=(0.3, 0.2, 0.1, 0.25, 0.15)):
+    count = rng.integers(0, max_e + 1, M_)
+    off = np.zeros(M_ + 1, np.int32)
+    np.cumsum(count, out=off[1:])
+    E = int(off[-1])
+    level = (rng.choice(5, size=E, p=level_p) + 1).astype(np.int32)
+    freed = rng.uniform(0.2, 40, E) * GB
+    freed[rng.random(E) < 0.1] = 0.0                   # an action that frees nothing
+    cost = rng.uniform(1, 5000, E).astype(np.float32)
+    return off, level, freed, cost
+
+
+def gpu_plans(off, level, freed, cost, c_int):
+    p = M.degradation_plans(_t(off), _t(level), _t(freed), _t(cost), c_int)
+    torch.cuda.synchronize()
+    raw = p.cpu().numpy()
+    return (raw[:, :64].copy().view(np.float64), raw[:, 64:96].copy().view(np.float32),
+            raw[:, 96:100].copy().view(np.int32)[:, 0], raw)
+
+
+def _plan_answer(pf, pc, ne, R):
+    """Cost of the shortest prefix with freed >= R, None when none."""
+    for j in range(ne):
+        if pf[j] >= R:
+            return float(pc[j])
+    return None
+
+
+def test_degradation_plans_match_oracle():
+    # every boundary of every node's plan: R at a prefix's freed bytes is met by that prefix,
+    # one ulp above it needs the next one (or fails)
+    rng = np.random.default_rng(5)
+    M_ = 700
+    off, level, freed, cost = _engines(rng, M_)
+    level[off[10]:off[11]] = 4                          # equal levels: engine order decides
+    for c_int in (2000.0, 0.0):
+        pf, pc, ne, raw = gpu_plans(off, level, freed, cost, c_int)
+        assert (ne == np.diff(off)).all()
+        assert not raw[:, 100:].any()                   # reserved words are zero
+        checked = 0
+        for j in range(M_):
+            lv, fr, co = level[off[j]:off[j + 1]], freed[off[j]:off[j + 1]], cost[off[j]:off[j + 1]]
+            Rs = [1.0, 1e12]
+            for e in range(ne[j]):
+                Rs += [pf[j, e], np.nextafter(pf[j, e], np.inf)]
+            for R in Rs:
+                if R <= 0:
+                    continue
+                ref = oracle.degradation_cost(R, lv, fr, co, c_int)
+                got = _plan_answer(pf[j], pc[j], ne[j], R)
+                assert (got is None) == (ref is None), (j, R, got, ref)
+                if ref is not None:
+                    assert np.float32(got).view(np.uint32) == np.float32(ref).view(np.uint32), (j, R, got, ref)
+                checked += 1
+        assert checked > 4 * M_
+
+
+def test_degradation_plans_empty_and_single():
+    off = np.array([0, 0, 1, 1], np.int32)              # nodes with 0, 1 and 0 engines
+    level = np.array([5], np.int32)
+    freed = np.array([3 * GB])
+    cost = np.array([40.0], np.float32)
+    pf, pc, ne, _ = gpu_plans(off, level, freed, cost, 2000.0)
+    assert ne.tolist() == [0, 1, 0]
+    assert pf[1, 0] == 3 * GB and pc[1, 0] == np.float32(2040.0)
+    pf, pc, ne, _ = gpu_plans(np.zeros(3, np.int32), np.zeros(0, np.int32), np.zeros(0), np.zeros(0, np.float32),
+                              10.0)
+    assert ne.tolist() == [0, 0]
+
+
+def gpu_fitness_plans(model, src, cls, kv, nodes, weights, bounds, eng, k=1, rho=0.0, n_models=64):
+    off, level, freed, cost, c_int = eng
+    plans = M.degradation_plans(_t(off), _t(level), _t(freed), _t(cost), c_int)
+    idx, fit = M.route_fitness(_t(model.astype(np.int32)), _t(src.astype(np.int32)), _t(cls.astype(np.int32)),
+                               _t(kv.astype(np.float64)), _t(nodes["free_bytes"]), _t(nodes["queue_ms"]),
+                               _t(nodes["act_ms"]), _t(nodes["resident_mask"]), None,
+                               _t(nodes["rtt_ms"]), _t(np.asarray(weights, np.float32).reshape(-1, 3)),
+                               _t(np.asarray(bounds, np.float32)), n_models=n_models, k=k, rho=rho, plans=plans)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), fit.cpu().numpy()
+
+
+@pytest.mark.parametrize("n,M_,n_src,k", [(1, 1, 1, 1), (300, 255, 2, 1), (1000, 257, 5, 3),
+                                          (2000, 1300, 16, 16), (513, 700, 3, 4)])
+def test_fitness_with_plans_matches_oracle(n, M_, n_src, k):
+    # several 256-node chunks with ragged tails; most stages fall short on many nodes
+    rng = np.random.default_rng(n * 13 + M_)
+    nodes = _nodes(rng, M_, n_src)
+    nodes["free_bytes"] = rng.uniform(0, 60, M_) * GB
+    nodes["free_bytes"][rng.random(M_) < 0.05] = 0.0
+    off, level, freed, cost = _engines(rng, M_)
+    eng = (off, level, freed, cost, 2000.0)
+    model = rng.integers(0, 16, n).astype(np.int32)
+    src = rng.integers(0, n_src, n).astype(np.int32)
+    cls = rng.integers(0, 3, n).astype(np.int32)
+    kv = rng.uniform(0, 120, n) * GB
+    kv[::37] = 0.0
+    weights = [[0.25, 1, 1], [0.1, 1, 1], [1.0, 0.0, 1.0]]
+    bounds = [*oracle.quantiles(nodes["rtt_ms"].ravel()), *oracle.quantiles(nodes["queue_ms"] + nodes["act_ms"]),
+              0.0, 12000.0]
+    for rho in (0.0, 0.2):
+        got = gpu_fitness_plans(model, src, cls, kv, nodes, weights, bounds, eng, k=k, rho=rho)
+        ref = oracle.route_fitness(model, src, cls, kv, nodes["free_bytes"], nodes["queue_ms"], nodes["act_ms"],
+                                   nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                                   np.asarray(weights, np.float32), np.asarray(bounds, np.float32), k=k, rho=rho,
+                                   engines=eng)
+        assert_same(got, ref)
+    if n > 100:   # the shortfall branch is exercised, on most pairs
+        assert (kv[:, None] > nodes["free_bytes"][None, :]).mean() > 0.3
+
+
+def test_fitness_with_plans_exact_shortfall_boundaries():
+    # shortfalls that equal a prefix's freed bytes exactly, and degenerate C_deg window
+    rng = np.random.default_rng(23)
+    M_ = 300
+    nodes = _nodes(rng, M_, 2)
+    nodes["free_bytes"] = np.round(rng.uniform(0, 20, M_)) * GB
+    off, level, freed, cost = _engines(rng, M_)
+    freed = np.round(freed / GB) * GB                   # integral GB: exact sums
+    eng = (off, level, freed, cost, 2000.0)
+    n = 3000
+    kv = np.round(rng.uniform(0, 80, n)) * GB           # shortfalls hit prefix sums exactly
+    model = rng.integers(0, 16, n).astype(np.int32)
+    src = rng.integers(0, 2, n).astype(np.int32)
+    cls = np.zeros(n, np.int32)
+    for bounds in ([0, 100, 0, 30000, 0, 8000], [5, 5, 7, 7, 1, 1]):
+        got = gpu_fitness_plans(model, src, cls, kv, nodes, [[0.25, 1, 1]], bounds, eng, k=4)
+        ref = oracle.route_fitness(model, src, cls, kv, nodes["free_bytes"], nodes["queue_ms"], nodes["act_ms"],
+                                   nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                                   np.asarray([[0.25, 1, 1]], np.float32), np.asarray(bounds, np.float32), k=4,
+                                   engines=eng)
+        assert_same(got, ref)
+
+
+@pytest.mark.parametrize("name", ["c1", "c3"])
+def test_fitness_with_plans_workload_full(name):
+    w = W.workload(name)
+    f = W.fitness_inputs(w)
+    e = W.engine_inputs(w)
+    b = pipeline.to_device(w)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    torch.cuda.synchronize()
+    kv = o.kv_bytes.cpu().numpy()
+    nodes = dict(free_bytes=w.free_bytes, queue_ms=f.queue_ms, act_ms=f.act_ms, resident_mask=w.resident_mask,
+                 deg_ms=f.deg_ms, rtt_ms=f.rtt_ms)
+    bounds = np.concatenate([oracle.quantiles(f.rtt_window), oracle.quantiles(f.ready_window),
+                             oracle.quantiles(e.deg_window)])
+    eng = (e.engine_offset, e.level, e.freed_bytes, e.cost_ms, e.c_int_ms)
+    got = gpu_fitness_plans(w.model_id, f.src_id, f.class_id, kv, nodes, f.class_weights, bounds, eng, k=w.spec.k,
+                            rho=w.spec.rho, n_models=w.spec.n_models)
+    ref = oracle.route_fitness(w.model_id, f.src_id, f.class_id, kv, nodes["free_bytes"], nodes["queue_ms"],
+                               nodes["act_ms"], nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                               f.class_weights, bounds, k=w.spec.k, rho=w.spec.rho, engines=eng)
+    assert_same(got, ref)
+    print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes with plans, "
+          f"{(got[0][:, 0] >= 0).mean():.4f} routed, fitness identical")
