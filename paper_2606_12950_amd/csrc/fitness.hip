@@ -21,8 +21,9 @@
 // With degradation plans (Alg. 2, Eq. 4), C_deg is per pair: 0 when the stage fits, else the
 // cost of the shortest priority prefix of the node's engines that frees the shortfall, and the
 // node drops out when no prefix does. The plan records (running freed bytes and costs, one per
-// prefix) are built once per node state and staged in LDS with the other node terms; only lanes
-// whose stage does not fit search them, so a wavefront in which every stage fits skips that.
+// prefix) are built once per node state and staged in LDS, column by column, with the other
+// node terms. The main loop scores every pair as if it fit and only queues the short ones; a
+// lane then scores its queued nodes against their plans after each chunk.
 //
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
@@ -119,13 +120,21 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   //          exceeds 31)
   // and with plans the node's plan record (norm(C_deg) then depends on the stage).
   typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
-  constexpr int kChunk = kPlans ? 256 : 512;   // nodes staged in LDS at a time
+  // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
+  // workgroups per CU, whose waves hide each other's LDS latency
+  constexpr int kChunk = kPlans ? 128 : 256;
   constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
   struct Admit { double free; uint64_t mask; };
   __shared__ float4 s_terms[kChunk];
   __shared__ Admit s_admit[kChunk];
   __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
-  __shared__ maestro_deg_plan s_plan[kPlans ? kChunk : 1];
+  constexpr int kPC = kPlans ? kChunk : 1;
+  __shared__ double s_pfreed[kMaxPlan][kPC];   // plan columns, node-minor: lanes reading
+  __shared__ float s_pcost[kMaxPlan][kPC];     // different nodes hit different banks
+  __shared__ int32_t s_pn[kPC];
+  constexpr int kQueue = kPlans ? 16 : 1;        // short nodes a lane queues per chunk
+  static_assert(kChunk <= 256 || !kPlans, "queued node offsets are bytes");
+  __shared__ uint8_t s_queue[kQueue * kThreads];
 
   const int tid = threadIdx.x;
   const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
@@ -168,7 +177,15 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
                                norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
                                kPlans ? nd_fits : norm01(deg_ms[j], lo_d, inv_d));
       s_admit[i] = Admit{fr, resident_mask[j]};
-      if (kPlans) s_plan[i] = plans[j];
+      if (kPlans) {
+        const maestro_deg_plan& pl = plans[j];
+#pragma unroll
+        for (int e = 0; e < kMaxPlan; ++e) {
+          s_pfreed[e][i] = pl.freed[e];
+          s_pcost[e][i] = pl.cost[e];
+        }
+        s_pn[i] = pl.n_engines;
+      }
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
@@ -178,47 +195,88 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     __syncthreads();
     // every node is scored; an infeasible one offers the key +inf, which never enters the list
     // (FilterByPolicyAndFeasibility)
-    auto pair = [&](int i, const float4 t, const Admit ad, float prox) {
+    auto score = [&](const float4 t, const Admit ad, float prox, float nd) {
       // fit = min(1, fl32(need) / fl32(headroom)); with zero headroom only need = 0 is
       // feasible, and min(0 * inf = NaN, 1) = 1 (IEEE min returns the number), the fit of a
       // stage that fills the node exactly
       const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
       const float a = __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
       const float nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
-      bool ok = need <= ad.free;
-      float nd = t.w;
-      if (kPlans && !ok) {   // shortfall: the first prefix of the plan that frees it, if any
-        const maestro_deg_plan& pl = s_plan[i];
-        const double R = __dsub_rn(need, ad.free);
-        int jp = 0;
+      return __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
+    };
+    // A stage that falls short of node i's headroom by R takes the first prefix of the node's
+    // plan whose freed bytes reach R, at that prefix's cost; no such prefix leaves the node
+    // infeasible. These pairs are rare, so they leave the main loop: each lane queues its short
+    // nodes and scores them after the chunk (rescanning the chunk when its queue overflowed),
+    // inserting lexicographically since they come after nodes of larger index.
+    auto short_pair = [&](int i) {
+      const float4 t = s_terms[i];
+      const Admit ad = s_admit[i];
+      const double R = __dsub_rn(need, ad.free);
+      int jp = 0;
 #pragma unroll
-        for (int e = 0; e < kMaxPlan; ++e) jp += pl.freed[e] < R ? 1 : 0;
-        ok = jp < pl.n_engines;
-        nd = norm01(pl.cost[ok ? jp : 0], lo_d, inv_d);
-      }
-      const float sc = __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
-      best.push_increasing(ok ? -sc : INFINITY, c0 + i);
+      for (int e = 0; e < kMaxPlan; ++e) jp += s_pfreed[e][i] < R ? 1 : 0;
+      if (jp < s_pn[i])
+        best.push_lex(-score(t, ad, prox_row[i], norm01(s_pcost[jp][i], lo_d, inv_d)), c0 + i);
+    };
+    int n_short = 0;   // queued nodes of this chunk
+    auto queue = [&](int i) {
+      if (n_short < kQueue) s_queue[n_short * kThreads + tid] = (uint8_t)i;
+      ++n_short;
     };
     if (kPlans) {
-      // the next node's terms are read before this node's shortfall branch, so their LDS
-      // latency overlaps it
-      float4 t = s_terms[0];
-      Admit ad = s_admit[0];
-      float px = prox_row[0];
-#pragma unroll 2
-      for (int i = 0; i < cn; ++i) {
-        const int in = i + 1 < cn ? i + 1 : i;
-        const float4 tn = s_terms[in];
-        const Admit adn = s_admit[in];
-        const float pxn = prox_row[in];
-        pair(i, t, ad, px);
-        t = tn;
-        ad = adn;
-        px = pxn;
+      // groups of four nodes: their LDS reads issue together, and one branch per group
+      // queues the short ones
+      int i = 0;
+      for (; i + 4 <= cn; i += 4) {
+        float4 t[4];
+        Admit ad[4];
+        float px[4];
+        bool fits[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          t[u] = s_terms[i + u];
+          ad[u] = s_admit[i + u];
+          px[u] = prox_row[i + u];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          fits[u] = need <= ad[u].free;
+          const float sc = score(t[u], ad[u], px[u], t[u].w);
+          best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u);
+        }
+        if (valid && !(fits[0] && fits[1] && fits[2] && fits[3])) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (!fits[u]) queue(i + u);
+        }
+      }
+      for (; i < cn; ++i) {
+        const float4 t = s_terms[i];
+        const Admit ad = s_admit[i];
+        const bool fits = need <= ad.free;
+        const float sc = score(t, ad, prox_row[i], t.w);
+        best.push_increasing(fits ? -sc : INFINITY, c0 + i);
+        if (valid && !fits) queue(i);
       }
     } else {
 #pragma unroll 4
-      for (int i = 0; i < cn; ++i) pair(i, s_terms[i], s_admit[i], prox_row[i]);
+      for (int i = 0; i < cn; ++i) {
+        const float4 t = s_terms[i];
+        const Admit ad = s_admit[i];
+        const float sc = score(t, ad, prox_row[i], t.w);
+        best.push_increasing(need <= ad.free ? -sc : INFINITY, c0 + i);
+      }
+    }
+    if (kPlans && n_short > 0) {
+      if (n_short <= kQueue) {
+#pragma unroll 1
+        for (int q = 0; q < n_short; ++q) short_pair(s_queue[q * kThreads + tid]);
+      } else {
+#pragma unroll 1
+        for (int i = 0; i < cn; ++i)
+          if (!(need <= s_admit[i].free)) short_pair(i);
+      }
     }
   }
 

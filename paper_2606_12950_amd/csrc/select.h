@@ -34,8 +34,10 @@ struct TopK {
       }
     }
   }
-  // General lexicographic insertion, used when merging lists from other lanes.
+  // General lexicographic insertion, for candidates out of node order (lists merged from other
+  // lanes, nodes visited late).
   __device__ __forceinline__ void push_lex(float sc, int32_t node) {
+    if (!(sc < s[KT - 1] || (sc == s[KT - 1] && node < n[KT - 1]))) return;   // cannot enter
 #pragma unroll
     for (int i = KT - 1; i >= 0; --i) {
       const int p = i > 0 ? i - 1 : 0;
