@@ -294,24 +294,29 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 
 // The values of rank r_lo and r_hi (0-based) of v[0 .. m-1] in the total order of float bit
 // patterns (-0 before +0): four passes over the 8-bit digits of the order-preserving image,
-// each narrowing both candidate prefixes by one digit.
+// each narrowing both candidate prefixes by one digit. Within a pass, the candidates' digits
+// are counted into one 256-bin histogram per rank; eight wavefronts scan the two histograms
+// (64 bins each, cross-lane), and the one bin whose count range holds the rank takes it.
 constexpr int kSelectThreads = 1024;
 __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* __restrict__ v, int64_t m,
                                                                   int64_t r_lo, int64_t r_hi,
                                                                   float* __restrict__ out) {
   __shared__ uint32_t hist[2][256];
-  __shared__ uint32_t s_prefix[2];
-  __shared__ int64_t s_rank[2];
-  const int tid = threadIdx.x;
+  __shared__ uint32_t scan[2][256];   // inclusive prefix within each 64-bin segment
+  __shared__ uint32_t seg[2][4];      // segment totals
+  __shared__ uint32_t s_prefix[2][2];   // [pass parity][rank]: read in one pass, written for the next
+  __shared__ int64_t s_rank[2][2];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (tid < 2) {
-    s_prefix[tid] = 0;
-    s_rank[tid] = tid ? r_hi : r_lo;
+    s_prefix[0][tid] = 0;
+    s_rank[0][tid] = tid ? r_hi : r_lo;
   }
   uint32_t mask = 0;
-  for (int shift = 24; shift >= 0; shift -= 8) {
+  int par = 0;
+  for (int shift = 24; shift >= 0; shift -= 8, par ^= 1) {
     for (int i = tid; i < 512; i += kSelectThreads) (&hist[0][0])[i] = 0;
     __syncthreads();
-    const uint32_t p0 = s_prefix[0], p1 = s_prefix[1];
+    const uint32_t p0 = s_prefix[par][0], p1 = s_prefix[par][1];
     for (int64_t i = tid; i < m; i += kSelectThreads) {
       const uint32_t u = float_key(v[i]);
       const uint32_t dgt = (u >> shift) & 255u;
@@ -319,21 +324,33 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
       if ((u & mask) == p1) atomicAdd(&hist[1][dgt], 1u);
     }
     __syncthreads();
-    if (tid < 2) {
-      int64_t r = s_rank[tid];
-      uint32_t b = 0;
-      for (; b < 255u; ++b) {
-        const uint32_t c = hist[tid][b];
-        if (r < (int64_t)c) break;
-        r -= c;
+    if (wave < 8) {
+      const int h = wave >> 2, b = (wave & 3) * 64 + lane;
+      uint32_t x = hist[h][b];
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
       }
-      s_rank[tid] = r;
-      s_prefix[tid] |= b << shift;
+      scan[h][b] = x;
+      if (lane == 63) seg[h][wave & 3] = x;
+    }
+    __syncthreads();
+    if (tid < 512) {
+      const int h = tid >> 8, b = tid & 255;
+      uint32_t incl = scan[h][b];
+      for (int q = 0; q < (b >> 6); ++q) incl += seg[h][q];
+      const uint32_t c = hist[h][b];
+      const int64_t r = s_rank[par][h];
+      if (r >= (int64_t)(incl - c) && r < (int64_t)incl) {   // exactly one bin per rank
+        s_rank[par ^ 1][h] = r - (int64_t)(incl - c);
+        s_prefix[par ^ 1][h] = s_prefix[par][h] | ((uint32_t)b << shift);
+      }
     }
     mask |= 0xFFu << shift;
     __syncthreads();
   }
-  if (tid < 2) out[tid] = key_float(s_prefix[tid]);
+  if (tid < 2) out[tid] = key_float(s_prefix[par][tid]);
 }
 
 }  // namespace
