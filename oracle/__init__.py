@@ -9,6 +9,11 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
   predict    - pinned: closed forms (zero weights -> mean of bin centres, one-hot bias ->
                that bin's centre), convexity, centre-shift equivariance, Eq. 3 exactly, and a
                float64 PyTorch forward pass with the same rounding points on small shapes.
+  predict_two_phase - pinned (tests/test_oracle_two_phase_pins.py): zero weights give closed
+               forms (sigmoid of the bias through the table, expm1 of the head's bias), no tools
+               gives exactly 0, an identity table leaves the sigmoid unchanged, the table is
+               numpy's interp, role fallback to the shared head, clamps at 0 and max_len, Eq. 3,
+               and the trunk agrees with predict's on the same network.
   route      - pinned: brute force via numpy lexsort on tiny inputs, invariants (feasible,
                sorted, nothing better left out), degenerate cases, node-permutation
                equivariance.
@@ -62,6 +67,9 @@ def _load():
     i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
     lib.oracle_predict.argtypes = [i32, P, i32, P, P, P, i64, P, P, P, P, i32, P, P, i32]
     lib.oracle_predict.restype = ctypes.c_int
+    lib.oracle_predict_two_phase.argtypes = [i32, P, i32, P, P, i32, P, P, i32, P, P, ctypes.c_float, i64, P,
+                                             P, P, P, P, P, i32, P, P, P, i32]
+    lib.oracle_predict_two_phase.restype = ctypes.c_int
     lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
     lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
@@ -133,6 +141,43 @@ def predict(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequence[np.nd
     if st != 0:
         raise RuntimeError(f"oracle_predict failed with status {st}")
     return pred, kv
+
+
+def predict_two_phase(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequence[np.ndarray],
+                      role_head, tool_coef, iso_x, iso_y, max_len: float, prompt_len, model_id, role_id,
+                      tool_avail, kv_bytes_per_token, dtype: str, n_threads: int = 0):
+    """Two-phase predictor: returns (p_tool float32 [N], pred_len float32 [N], kv_bytes float64
+    [N]). The last layer's outputs are the heads: 0 the tool-intent logit, g >= 1 the log(1 + L)
+    regressors (1 the shared one); ``role_head`` [n_roles] maps roles to heads."""
+    lib = _load()
+    dt = 0 if dtype == "f32" else 1
+    store = np.float32 if dt == 0 else np.uint16
+    x = _c(x, store)
+    n = x.shape[0]
+    ws = [_c(w, store) for w in weights]
+    bs = [_c(b, np.float32) for b in biases]
+    L = len(ws)
+    dims = np.array([x.shape[1]] + [w.shape[0] for w in ws], dtype=np.int32)
+    for l, w in enumerate(ws):
+        assert w.shape == (dims[l + 1], dims[l]), "weight shapes must chain [out][in]"
+    wptr = (ctypes.c_void_p * L)(*[w.ctypes.data for w in ws])
+    bptr = (ctypes.c_void_p * L)(*[b.ctypes.data for b in bs])
+    rh, tc = _c(role_head, np.int32), _c(tool_coef, np.float32)
+    kx, ky = _c(iso_x, np.float32), _c(iso_y, np.float32)
+    pl, mi = _c(prompt_len, np.int32), _c(model_id, np.int32)
+    ri, ta = _c(role_id, np.int32), _c(tool_avail, np.int32)
+    alpha = _c(kv_bytes_per_token, np.float32)
+    pt = np.empty(n, np.float32)
+    pred = np.empty(n, np.float32)
+    kv = np.empty(n, np.float64)
+    st = lib.oracle_predict_two_phase(L, _ptr(dims), dt, ctypes.cast(wptr, ctypes.c_void_p),
+                                      ctypes.cast(bptr, ctypes.c_void_p), rh.shape[0], _ptr(rh), _ptr(tc),
+                                      kx.shape[0], _ptr(kx), _ptr(ky), float(max_len), n, _ptr(x), _ptr(pl),
+                                      _ptr(mi), _ptr(ri), _ptr(ta), _ptr(alpha), alpha.shape[0], _ptr(pt),
+                                      _ptr(pred), _ptr(kv), n_threads or max_threads())
+    if st != 0:
+        raise RuntimeError(f"oracle_predict_two_phase failed with status {st}")
+    return pt, pred, kv
 
 
 def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s, cold_s,

@@ -25,6 +25,10 @@
  *                fit = R_need / headroom (best fit), T_ready = T_q + T_act (Eq. 6), each metric
  *                min-max normalised onto [0, 1] with window bounds and clipped; float32 in a
  *                fixed operation order; k best (fitness, lowest index).
+ *   two-phase  : the same network read as heads (Sec. III-B): a tool-intent logit through a
+ *                sigmoid and an isotonic calibration table (Eq. 1), 0 without tools; the
+ *                stage's role regressor (or the shared one) on log(1 + L), fed the calibrated
+ *                probability, inverted with expm1; then Eq. 3.
  *   quantiles  : the window bounds, as exact order statistics of a sample.
  *   prioritize : per-stage latency quantised to integer microseconds, suffix sums along each
  *                workflow chain (Eq. 7 with the future term taken as the sum of the later
@@ -92,6 +96,27 @@ static double stored_value(const void* base, int32_t dtype, int64_t idx) {
 /* predict: Sec. III-B (length predictor stand-in), Eq. 3 (KV demand)                        */
 /* ------------------------------------------------------------------------------------------ */
 
+/* The network's output layer for stage i: z_j = b_j + sum_k W[j][k] h_k (k ascending) layer by
+ * layer from the stage's features, hidden layers through ReLU and stored in dtype. h and z hold
+ * at least the widest layer. */
+static void mlp_forward(int64_t i, int32_t n_layers, const int32_t* dims, int32_t dtype,
+                        const void* const* weight, const float* const* bias, const void* x, double* h,
+                        double* z) {
+  const int32_t D = dims[0];
+  for (int32_t k = 0; k < D; ++k) h[k] = stored_value(x, dtype, i * (int64_t)D + k);
+  for (int l = 0; l < n_layers; ++l) {
+    const int32_t din = dims[l], dout = dims[l + 1];
+    for (int32_t j = 0; j < dout; ++j) {
+      double acc = (double)bias[l][j];
+      for (int32_t k = 0; k < din; ++k) acc += stored_value(weight[l], dtype, (int64_t)j * din + k) * h[k];
+      z[j] = acc;
+    }
+    if (l + 1 < n_layers) {          /* hidden layer: ReLU, stored in dtype */
+      for (int32_t j = 0; j < dout; ++j) h[j] = round_hidden(z[j] > 0.0 ? z[j] : 0.0, dtype);
+    }
+  }
+}
+
 int oracle_predict(int32_t n_layers, const int32_t* dims, int32_t dtype,
                    const void* const* weight, const float* const* bias,
                    const float* bin_centre, int64_t n, const void* x,
@@ -105,7 +130,7 @@ int oracle_predict(int32_t n_layers, const int32_t* dims, int32_t dtype,
     if (dims[l] < 1) return ORACLE_BAD_ARG;
     if (dims[l] > widest) widest = dims[l];
   }
-  const int32_t D = dims[0], B = dims[n_layers];
+  const int32_t B = dims[n_layers];
   int status = ORACLE_OK;
   if (n_threads < 1) n_threads = 1;
 
@@ -119,21 +144,7 @@ int oracle_predict(int32_t n_layers, const int32_t* dims, int32_t dtype,
     } else {
 #pragma omp for schedule(static)
       for (int64_t i = 0; i < n; ++i) {
-        /* input features, converted exactly */
-        for (int32_t k = 0; k < D; ++k) h[k] = stored_value(x, dtype, i * (int64_t)D + k);
-        /* Linear layers: z_j = b_j + sum_k W[j][k] h_k, k ascending */
-        for (int l = 0; l < n_layers; ++l) {
-          const int32_t din = dims[l], dout = dims[l + 1];
-          for (int32_t j = 0; j < dout; ++j) {
-            double acc = (double)bias[l][j];
-            for (int32_t k = 0; k < din; ++k)
-              acc += stored_value(weight[l], dtype, (int64_t)j * din + k) * h[k];
-            z[j] = acc;
-          }
-          if (l + 1 < n_layers) {          /* hidden layer: ReLU, stored in dtype */
-            for (int32_t j = 0; j < dout; ++j) h[j] = round_hidden(z[j] > 0.0 ? z[j] : 0.0, dtype);
-          }
-        }
+        mlp_forward(i, n_layers, dims, dtype, weight, bias, x, h, z);
         /* softmax over bins (max-subtracted), expected length */
         double mu = z[0];
         for (int32_t b = 1; b < B; ++b) if (z[b] > mu) mu = z[b];
@@ -144,6 +155,86 @@ int oracle_predict(int32_t n_layers, const int32_t* dims, int32_t dtype,
         float pred = (float)expect;
         pred_len[i] = pred;
         /* Eq. 3: R_kv = alpha(M(T)) * (P(T) + L(T)) */
+        int32_t m = model_id[i];
+        double alpha = (m >= 0 && m < n_models) ? (double)kv_bytes_per_token[m] : NAN;
+        kv_bytes[i] = ((double)prompt_len[i] + (double)pred) * alpha;
+      }
+    }
+    free(h);
+    free(z);
+  }
+  return status;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* two-phase predict: Sec. III-B (tool intent, Eq. 1; isotonic calibration; per-role         */
+/* log(1+L) regressors), Eq. 3                                                                */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Isotonic calibration map: the piecewise-linear function through the knots (x_j, y_j),
+ * x strictly increasing, constant beyond the first and last knot. */
+static double isotonic(double p, int32_t n_knots, const float* kx, const float* ky) {
+  if (p <= (double)kx[0]) return (double)ky[0];
+  if (p >= (double)kx[n_knots - 1]) return (double)ky[n_knots - 1];
+  int32_t j = 0;                                   /* last knot at or below p */
+  while (j + 1 < n_knots - 1 && (double)kx[j + 1] <= p) ++j;
+  const double x0 = kx[j], x1 = kx[j + 1], y0 = ky[j], y1 = ky[j + 1];
+  return y0 + (p - x0) * (y1 - y0) / (x1 - x0);
+}
+
+/* The network's output layer is read as B heads: output 0 is the tool-intent logit, output g
+ * (1 <= g < B) the log(1 + L) regressor of head g; head 1 is the shared global model. A stage
+ * of role r uses head role_head[r] (r in 0 .. n_roles-1, entry in 1 .. B-1), and the global
+ * head otherwise.
+ *   p_tool = has tools ? isotonic(sigmoid(z_0)) : 0                  (Eq. 1, calibrated)
+ *   y      = z_g + tool_coef[g] * p_tool                               (p_tool feeds the regressor)
+ *   L      = min(expm1(max(y, 0)), max_len)                            (inverse of log(1 + L))
+ *   R_kv   = alpha(M) * (P + L)                                        (Eq. 3) */
+int oracle_predict_two_phase(int32_t n_layers, const int32_t* dims, int32_t dtype,
+                             const void* const* weight, const float* const* bias, int32_t n_roles,
+                             const int32_t* role_head, const float* tool_coef, int32_t n_knots,
+                             const float* iso_x, const float* iso_y, float max_len, int64_t n,
+                             const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                             const int32_t* role_id, const int32_t* tool_avail,
+                             const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
+                             float* pred_len, double* kv_bytes, int32_t n_threads) {
+  if (n_layers < 1 || n_layers > 4 || (dtype != 0 && dtype != 1) || n < 0 || n_models < 1 ||
+      n_roles < 0 || n_knots < 1)
+    return ORACLE_BAD_ARG;
+  int32_t widest = 0;
+  for (int l = 0; l <= n_layers; ++l) {
+    if (dims[l] < 1) return ORACLE_BAD_ARG;
+    if (dims[l] > widest) widest = dims[l];
+  }
+  const int32_t B = dims[n_layers];
+  if (B < 2) return ORACLE_BAD_ARG;
+  int status = ORACLE_OK;
+  if (n_threads < 1) n_threads = 1;
+
+#pragma omp parallel num_threads(n_threads)
+  {
+    double* h = (double*)malloc(sizeof(double) * (size_t)widest);
+    double* z = (double*)malloc(sizeof(double) * (size_t)widest);
+    if (!h || !z) {
+#pragma omp atomic write
+      status = ORACLE_NO_MEM;
+    } else {
+#pragma omp for schedule(static)
+      for (int64_t i = 0; i < n; ++i) {
+        mlp_forward(i, n_layers, dims, dtype, weight, bias, x, h, z);
+        /* phase 1: probability that the stage invokes a tool, calibrated; 0 without tools */
+        double p = 0.0;
+        if (tool_avail[i] != 0) p = isotonic(1.0 / (1.0 + exp(-z[0])), n_knots, iso_x, iso_y);
+        /* phase 2: the role's length regressor (or the shared one) on log(1 + L) */
+        const int32_t r = role_id[i];
+        int32_t g = (r >= 0 && r < n_roles) ? role_head[r] : 1;
+        if (g < 1 || g >= B) g = 1;
+        const double y = z[g] + (double)tool_coef[g] * p;
+        double L = expm1(y > 0.0 ? y : 0.0);
+        if (L > (double)max_len) L = (double)max_len;
+        const float pred = (float)L;
+        p_tool[i] = (float)p;
+        pred_len[i] = pred;
         int32_t m = model_id[i];
         double alpha = (m >= 0 && m < n_models) ? (double)kv_bytes_per_token[m] : NAN;
         kv_bytes[i] = ((double)prompt_len[i] + (double)pred) * alpha;
