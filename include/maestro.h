@@ -5,6 +5,9 @@
  *   maestro_predict    cost prediction (Sec. III-B): predicted output length L of every stage
  *                      from a feature MLP over length bins (stand-in for the paper's trained
  *                      regressor), and its KV demand R_kv = alpha(M) * (P + L) (Eq. 3).
+ *   maestro_predict_two_phase  the paper's two-phase form of the same prediction (Sec. III-B):
+ *                      a calibrated tool-intent probability (Eq. 1), then the stage's role
+ *                      regressor on log(1 + L), fed that probability.
  *   maestro_route      cross-cluster routing (Sec. III-D, Alg. 3): drop nodes whose free KV
  *                      headroom cannot admit R_need = (1 + rho) * R_kv, score the rest by
  *                      expected completion latency T_q + T_act + t_dec(M) * L (Eq. 6 and the
@@ -102,6 +105,50 @@ MAESTRO_API maestro_status maestro_predict(const maestro_predictor* p, int64_t n
                                const float* kv_bytes_per_token, int32_t n_models,
                                float* pred_len, double* kv_bytes,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* The two-phase predictor (Sec. III-B). The network of a maestro_predictor (dims[n_layers] =
+ * B = 64 outputs) is read as heads instead of bins: output 0 is the tool-intent logit z_0,
+ * output g (1 <= g < B) the log(1 + L) regressor of head g; head 1 is the shared global model.
+ *   n_roles     roles 0 .. n_roles-1 that map to a head, 0 <= n_roles <= 64
+ *   role_head   [n_roles] int32 (device, may be NULL when n_roles = 0): the head of each role's
+ *               own regressor; entries outside 1 .. B-1, and roles outside 0 .. n_roles-1,
+ *               use head 1 (the fallback when a role has no regressor of its own)
+ *   tool_coef   [B] float32 (device, 16-byte aligned): weight of the tool probability in each
+ *               length head (entry 0 unused)
+ *   n_knots     2 .. 64 knots of the isotonic calibration map
+ *   iso_x/iso_y [n_knots] float32 (device): knots, iso_x strictly increasing, iso_y
+ *               non-decreasing; the map is piecewise linear through them and constant beyond
+ *               the first and the last
+ *   max_len     upper clamp of the predicted length (tokens), finite and > 0 */
+typedef struct maestro_two_phase {
+  int32_t n_roles;
+  int32_t n_knots;
+  const int32_t* role_head;
+  const float* tool_coef;
+  const float* iso_x;
+  const float* iso_y;
+  float max_len;
+} maestro_two_phase;
+
+/* Two-phase cost prediction for n stages (Sec. III-B: Eq. 1, isotonic calibration, per-role
+ * log(1 + L) regression; Eq. 3). Per stage, with z the network's B outputs (float32):
+ *   p_tool = tool_avail != 0 ? iso(1 / (1 + exp(-z_0))) : 0      (Eq. 1, calibrated)
+ *   g      = the head of the stage's role (see maestro_two_phase)
+ *   L      = min(expm1(max(z_g + tool_coef[g] * p_tool, 0)), max_len)
+ *   R_kv   = ((double)P + (double)L) * (double)alpha(M)            (Eq. 3)
+ * Arguments as maestro_predict, plus
+ *   role_id     [n] int32: the stage's agent role
+ *   tool_avail  [n] int32: nonzero when tools are available to the stage
+ *   p_tool (out)[n] float32, or NULL when not wanted
+ * Built shapes: MAESTRO_BF16, 3 layers, 256 -> 512 -> 512 -> 64 and 256 -> 1024 -> 1024 -> 64
+ * (others return MAESTRO_ERR_UNSUPPORTED). No workspace. Errors: INVALID_ARG for a NULL or
+ * misaligned array, n < 0, n_models outside 1..64, n_roles outside 0..64, n_knots outside
+ * 2..64, or max_len not finite and positive. */
+MAESTRO_API maestro_status maestro_predict_two_phase(const maestro_predictor* p, const maestro_two_phase* tp,
+                             int64_t n, const void* x, const int32_t* prompt_len,
+                             const int32_t* model_id, const int32_t* role_id, const int32_t* tool_avail,
+                             const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
+                             float* pred_len, double* kv_bytes, void* stream);
 
 /* Routing of n stages over n_nodes nodes (Sec. III-D; Alg. 3; Eq. 6; Eq. 2 decode term).
  * Per stage i with model m = model_id[i]:

@@ -4,12 +4,14 @@ The computation lives in libmaestro.so (hand-written HIP kernels behind the C-AB
 include/maestro.h); this package is its thin Python binding plus the seeded workload
 generator. PyTorch supplies device memory and streams only.
 """
-from ._native import (LIBRARY_PATH, MaestroError, Predictor, load, make_predictor, predict,
+from ._native import (LIBRARY_PATH, MaestroError, Predictor, TwoPhase, load, make_predictor, predict,
+                      predict_two_phase,
                       degradation_plans, prioritize, prioritize_workspace_bytes, quantiles, route,
                       route_fitness)
 from .pipeline import DeviceBatch, StepOutputs, run_step, to_device
 
-__all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "load", "make_predictor", "predict", "degradation_plans",
+__all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "TwoPhase", "load", "make_predictor", "predict",
+           "predict_two_phase", "degradation_plans",
            "prioritize", "prioritize_workspace_bytes", "quantiles", "route", "route_fitness",
            "DeviceBatch", "StepOutputs",
            "run_step", "to_device"]

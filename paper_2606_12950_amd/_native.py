@@ -21,7 +21,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
            4: "kernel launch failed"}
 
 # Every function declared in include/maestro.h.
-EXPORTS = ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
+EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
            "maestro_degradation_plans", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
@@ -44,6 +44,13 @@ class Predictor(ctypes.Structure):
                 ("bias", ctypes.c_void_p * 4), ("bin_centre", ctypes.c_void_p)]
 
 
+class TwoPhase(ctypes.Structure):
+    """Mirror of ``maestro_two_phase``."""
+    _fields_ = [("n_roles", ctypes.c_int32), ("n_knots", ctypes.c_int32), ("role_head", ctypes.c_void_p),
+                ("tool_coef", ctypes.c_void_p), ("iso_x", ctypes.c_void_p), ("iso_y", ctypes.c_void_p),
+                ("max_len", ctypes.c_float)]
+
+
 _lib = None
 
 
@@ -58,6 +65,8 @@ def load():
     lib = ctypes.CDLL(LIBRARY_PATH)
     P, i32, i64, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
     lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
+    lib.maestro_predict_two_phase.argtypes = [ctypes.POINTER(Predictor), ctypes.POINTER(TwoPhase), i64, P, P, P,
+                                              P, P, P, i32, P, P, P, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
@@ -103,8 +112,9 @@ def _check(fn: str, status: int):
 
 
 def make_predictor(weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor],
-                   bin_centre: torch.Tensor) -> Predictor:
-    """Describe a predictor held in device tensors (weights [out][in], bf16 or fp32)."""
+                   bin_centre: Optional[torch.Tensor]) -> Predictor:
+    """Describe a predictor held in device tensors (weights [out][in], bf16 or fp32); the two-phase
+    predictor has no bin centres (None)."""
     L = len(weights)
     if not 1 <= L <= 4 or len(biases) != L:
         raise ValueError("1..4 Linear layers with one bias each")
@@ -123,10 +133,11 @@ def make_predictor(weights: Sequence[torch.Tensor], biases: Sequence[torch.Tenso
         p.dims[l + 1] = w.shape[0]
         p.weight[l] = w.data_ptr()
         p.bias[l] = b.data_ptr()
-    _dev(bin_centre, "bin_centre", torch.float32)
-    if bin_centre.shape != (p.dims[L],):
-        raise ValueError("bin_centre must have one entry per output bin")
-    p.bin_centre = bin_centre.data_ptr()
+    if bin_centre is not None:
+        _dev(bin_centre, "bin_centre", torch.float32)
+        if bin_centre.shape != (p.dims[L],):
+            raise ValueError("bin_centre must have one entry per output bin")
+        p.bin_centre = bin_centre.data_ptr()
     return p
 
 
@@ -157,6 +168,53 @@ def predict(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[t
                              _ptr(kv), _ptr(ws), ws_bytes, _stream(stream))
     _check("maestro_predict", st)
     return pred, kv
+
+
+def predict_two_phase(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor],
+                      role_head: torch.Tensor, tool_coef: torch.Tensor, iso_x: torch.Tensor, iso_y: torch.Tensor,
+                      max_len: float, prompt_len: torch.Tensor, model_id: torch.Tensor, role_id: torch.Tensor,
+                      tool_avail: torch.Tensor, kv_bytes_per_token: torch.Tensor,
+                      out: Optional[Tuple[torch.Tensor, torch.Tensor, torch.Tensor]] = None,
+                      stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """maestro_predict_two_phase: returns (p_tool float32 [N], pred_len float32 [N], kv_bytes
+    float64 [N]). The last layer's outputs are heads: 0 the tool-intent logit, g >= 1 the
+    log(1 + L) regressors (1 the shared one); ``role_head`` [n_roles] int32 maps roles to heads."""
+    lib = load()
+    p = make_predictor(weights, biases, None)
+    _dev(x, "x", weights[0].dtype)
+    n = x.shape[0]
+    if x.dim() != 2 or x.shape[1] != p.dims[0]:
+        raise ValueError("x must be [N][D]")
+    for t, name in ((prompt_len, "prompt_len"), (model_id, "model_id"), (role_id, "role_id"),
+                    (tool_avail, "tool_avail"), (role_head, "role_head")):
+        _dev(t, name, torch.int32)
+    for t, name in ((kv_bytes_per_token, "kv_bytes_per_token"), (tool_coef, "tool_coef"), (iso_x, "iso_x"),
+                    (iso_y, "iso_y")):
+        _dev(t, name, torch.float32)
+    if role_id.shape != (n,) or tool_avail.shape != (n,) or prompt_len.shape != (n,) or model_id.shape != (n,):
+        raise ValueError("per-stage inputs must have N entries")
+    if tool_coef.shape != (p.dims[p.n_layers],) or iso_x.shape != iso_y.shape:
+        raise ValueError("tool_coef needs one entry per output; iso_x and iso_y the same length")
+    tp = TwoPhase()
+    tp.n_roles = role_head.shape[0]
+    tp.n_knots = iso_x.shape[0]
+    tp.role_head = role_head.data_ptr() if role_head.numel() else None
+    tp.tool_coef = tool_coef.data_ptr()
+    tp.iso_x = iso_x.data_ptr()
+    tp.iso_y = iso_y.data_ptr()
+    tp.max_len = float(max_len)
+    if out is None:
+        out = (torch.empty(n, dtype=torch.float32, device=x.device), torch.empty(n, dtype=torch.float32, device=x.device),
+               torch.empty(n, dtype=torch.float64, device=x.device))
+    pt, pred, kv = out
+    _dev(pt, "p_tool", torch.float32)
+    _dev(pred, "pred_len", torch.float32)
+    _dev(kv, "kv_bytes", torch.float64)
+    st = lib.maestro_predict_two_phase(ctypes.byref(p), ctypes.byref(tp), n, _ptr(x), _ptr(prompt_len),
+                                       _ptr(model_id), _ptr(role_id), _ptr(tool_avail), _ptr(kv_bytes_per_token),
+                                       kv_bytes_per_token.shape[0], _ptr(pt), _ptr(pred), _ptr(kv), _stream(stream))
+    _check("maestro_predict_two_phase", st)
+    return pt, pred, kv
 
 
 def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,

@@ -66,6 +66,41 @@ maestro_status maestro_predict(const maestro_predictor* p, int64_t n, const void
                                  pred_len, kv_bytes, as_stream(stream));
 }
 
+maestro_status maestro_predict_two_phase(const maestro_predictor* p, const maestro_two_phase* tp, int64_t n,
+                                         const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                         const int32_t* role_id, const int32_t* tool_avail,
+                                         const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
+                                         float* pred_len, double* kv_bytes, void* stream) {
+  if (!p || !tp || n < 0 || n_models < 1 || n_models > 64) return MAESTRO_ERR_INVALID_ARG;
+  if (p->n_layers < 1 || p->n_layers > 4) return MAESTRO_ERR_INVALID_ARG;
+  if (p->dtype != MAESTRO_F32 && p->dtype != MAESTRO_BF16) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l <= p->n_layers; ++l)
+    if (p->dims[l] < 1) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l < p->n_layers; ++l)
+    if (!p->weight[l] || !p->bias[l] || !aligned(p->weight[l], 16) || !aligned(p->bias[l], 16))
+      return MAESTRO_ERR_INVALID_ARG;
+  if (tp->n_roles < 0 || tp->n_roles > 64 || tp->n_knots < 2 || tp->n_knots > 64) return MAESTRO_ERR_INVALID_ARG;
+  if (!(tp->max_len > 0.0f) || !isfinite(tp->max_len)) return MAESTRO_ERR_INVALID_ARG;
+  if (tp->n_roles > 0 && (!tp->role_head || !aligned(tp->role_head, 4))) return MAESTRO_ERR_INVALID_ARG;
+  if (!tp->tool_coef || !aligned(tp->tool_coef, 16) || !tp->iso_x || !tp->iso_y || !aligned(tp->iso_x, 4) ||
+      !aligned(tp->iso_y, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!x || !prompt_len || !model_id || !role_id || !tool_avail || !kv_bytes_per_token || !pred_len ||
+        !kv_bytes)
+      return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(prompt_len, 4) || !aligned(model_id, 4) || !aligned(role_id, 4) ||
+        !aligned(tool_avail, 4) || !aligned(kv_bytes_per_token, 4) || !aligned(pred_len, 4) ||
+        !aligned(kv_bytes, 8) || (p_tool && !aligned(p_tool, 4)))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (!maestro::two_phase_shape_supported(*p)) return MAESTRO_ERR_UNSUPPORTED;
+  if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
+  return maestro::launch_predict_two_phase(*p, *tp, n, x, prompt_len, model_id, role_id, tool_avail,
+                                           kv_bytes_per_token, n_models, p_tool, pred_len, kv_bytes,
+                                           as_stream(stream));
+}
+
 maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float* pred_len,
                                 const double* kv_bytes, const float* decode_s_per_token,
                                 int32_t n_models, int32_t n_nodes, const double* free_bytes,

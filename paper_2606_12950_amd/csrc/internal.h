@@ -15,6 +15,12 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
                               const float* kv_bytes_per_token, int32_t n_models, float* pred_len,
                               double* kv_bytes, hipStream_t stream);
 bool predict_shape_supported(const maestro_predictor& p);
+bool two_phase_shape_supported(const maestro_predictor& p);
+maestro_status launch_predict_two_phase(const maestro_predictor& p, const maestro_two_phase& t, int64_t n,
+                                        const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                        const int32_t* role_id, const int32_t* tool_avail,
+                                        const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
+                                        float* pred_len, double* kv_bytes, hipStream_t stream);
 
 // Routing: feasibility mask, pair scores, lexicographic top-k.
 maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pred_len,

@@ -1,6 +1,8 @@
 // Cost prediction for a batch of stages (Sec. III-B; Eq. 3): the feature MLP over length bins,
 // softmax, expected length, KV bytes -- one fused kernel, logits and hidden layers never leave
-// the chip.
+// the chip. The two-phase form reads the same network's outputs as heads instead (a
+// calibrated tool-intent probability, Eq. 1, then the role's log(1 + L) regressor fed that
+// probability); only the epilogue differs.
 //
 // Layout of the work. Each wavefront owns 32 stages (rows). Every Linear layer is computed
 // transposed, H^T = W * X^T, on 32x32 MFMA tiles: the weights are the A operand (32 output
@@ -85,6 +87,69 @@ __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const
     const float pred = sc / se;
     pred_len[row] = pred;
     kv_bytes[row] = ((double)prompt + (double)pred) * (double)alpha[model];
+  }
+}
+
+// Per-stage inputs and tables of the two-phase predictor (unused by the bins predictor).
+struct TwoPhaseArgs {
+  const int32_t* role_id;
+  const int32_t* tool_avail;
+  const int32_t* role_head;
+  const float* tool_coef;
+  const float* iso_x;
+  const float* iso_y;
+  int32_t n_roles;
+  int32_t n_knots;
+  float max_len;
+  float* p_tool;
+};
+
+// The B = 32*BT outputs of each row read as heads (Sec. III-B): output 0 the tool-intent
+// logit, output g the log(1 + L) regressor of the row's head g (role_head of its role, head 1
+// when the role has none). p_tool = iso(sigmoid(z_0)) (Eq. 1 calibrated; 0 without tools),
+// L = min(expm1(max(z_g + coef_g p_tool, 0)), max_len), then Eq. 3. Lanes r and r + 32 hold
+// complementary halves of row r's outputs; lane r finishes the row.
+template <int BT>
+__device__ __forceinline__ void two_phase_epilogue(const f32x16 (&z)[BT], const float* __restrict__ b_last,
+                                                   const float* __restrict__ coef, const int32_t* __restrict__ head_of,
+                                                   const float* __restrict__ kx, const float* __restrict__ ky,
+                                                   const TwoPhaseArgs& tp, int h, int64_t row, int64_t n,
+                                                   int32_t prompt, int32_t model, int32_t role, int32_t tools,
+                                                   const float* __restrict__ alpha, float* __restrict__ pred_len,
+                                                   double* __restrict__ kv_bytes) {
+  int g = (role >= 0 && role < tp.n_roles) ? head_of[role] : 1;
+  if (g < 1 || g >= 32 * BT) g = 1;
+  float mine = 0.0f;   // output g if this lane-half holds it
+#pragma unroll
+  for (int bt = 0; bt < BT; ++bt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (32 * bt + acc_row(v, h) == g) mine = z[bt][v];
+  const float zg = mine + __shfl_xor(mine, 32);   // exactly one of the two lane-halves holds it
+  if (h == 0 && row < n) {
+    float p = 0.0f;
+    if (tools != 0) {
+      const float s = 1.0f / (1.0f + __expf(-(z[0][0] + b_last[0])));   // output 0: v = 0, h = 0
+      const int K = tp.n_knots;
+      if (!(s > kx[0])) {
+        p = ky[0];
+      } else if (s >= kx[K - 1]) {
+        p = ky[K - 1];
+      } else {   // kx[lo] <= s < kx[hi]: the segment through knots lo and lo + 1
+        int lo = 0, hi = K - 1;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (kx[mid] <= s) lo = mid;
+          else hi = mid;
+        }
+        p = ky[lo] + (s - kx[lo]) * (ky[hi] - ky[lo]) / (kx[hi] - kx[lo]);
+      }
+    }
+    const float y = zg + b_last[g] + coef[g] * p;
+    const float L = fminf(expm1f(fmaxf(y, 0.0f)), tp.max_len);
+    if (tp.p_tool) tp.p_tool[row] = p;
+    pred_len[row] = L;
+    kv_bytes[row] = ((double)prompt + (double)L) * (double)alpha[model];
   }
 }
 
@@ -264,7 +329,7 @@ __device__ __forceinline__ void wait_chunk() {
 
 constexpr int kMaxModels = 64;           // per-model KV bytes staged in LDS
 
-template <int D, int H1, int H2, int B>
+template <int D, int H1, int H2, int B, bool kTwoPhase>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void mlp3_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w1, const uint16_t* __restrict__ w2,
@@ -272,7 +337,7 @@ void mlp3_bf16_kernel(
     const float* __restrict__ b3, const float* __restrict__ centre, int64_t n, int64_t n_tiles,
     const int32_t* __restrict__ prompt_len, const int32_t* __restrict__ model_id,
     const float* __restrict__ alpha, int32_t n_models, float* __restrict__ pred_len,
-    double* __restrict__ kv_bytes) {
+    double* __restrict__ kv_bytes, const TwoPhaseArgs tp) {
   static_assert(D == 256, "feature and layer-1 chunk layouts assume 512-byte rows");
   static_assert(H1 % 512 == 0 && H2 % 32 == 0 && B % 64 == 0, "tile shape");
   constexpr int KS1 = D / 16;             // K-steps of layer 1 (32x32x16 MFMA)
@@ -295,9 +360,14 @@ void mlp3_bf16_kernel(
   __shared__ __attribute__((aligned(16))) float s_b1[H1];
   __shared__ __attribute__((aligned(16))) float s_b2[H2];
   __shared__ __attribute__((aligned(16))) float s_b3[B];
-  __shared__ __attribute__((aligned(16))) float s_c[B];
+  __shared__ __attribute__((aligned(16))) float s_c[B];   // bin centres, or the two-phase tool coefficients
   __shared__ __attribute__((aligned(16))) float s_alpha[kMaxModels];
-  __shared__ __attribute__((aligned(16))) int32_t s_meta[2][2][kRowsPerBlock];  // [tile parity][prompt, model][row]
+  // [tile parity][prompt, model (, role, tool availability)][row]
+  constexpr int kMeta = kTwoPhase ? 4 : 2;
+  __shared__ __attribute__((aligned(16))) int32_t s_meta[2][kMeta][kRowsPerBlock];
+  constexpr int kTab = kTwoPhase ? 64 : 1;   // two-phase tables: role heads, calibration knots
+  __shared__ int32_t s_head[kTab];
+  __shared__ float s_kx[kTab], s_ky[kTab];
 
   const int tid = threadIdx.x;
   // wave index as a scalar: keeps every DMA source row address and LDS destination in SGPRs
@@ -337,6 +407,11 @@ void mlp3_bf16_kernel(
       const int32_t* src = (wave < 2) ? prompt_len : model_id;
       const int parity = (int)(((t - first_tile) / stride) & 1);
       dma4(buffer_rsrc(src + row0, rows * 4), voffm, lds_addr(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
+      if (kTwoPhase) {
+        const int32_t* src2 = (wave < 2) ? tp.role_id : tp.tool_avail;
+        dma4(buffer_rsrc(src2 + row0, rows * 4), voffm,
+             lds_addr(&s_meta[parity][2 + (wave >> 1)][64 * (wave & 1)]));
+      }
     }
   };
   // load q of layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units
@@ -400,7 +475,14 @@ void mlp3_bf16_kernel(
 
   for (int i = tid; i < H1; i += kThreads) s_b1[i] = b1[i];
   for (int i = tid; i < H2; i += kThreads) s_b2[i] = b2[i];
-  for (int i = tid; i < B; i += kThreads) { s_b3[i] = b3[i]; s_c[i] = centre[i]; }
+  for (int i = tid; i < B; i += kThreads) { s_b3[i] = b3[i]; s_c[i] = kTwoPhase ? tp.tool_coef[i] : centre[i]; }
+  if (kTwoPhase) {
+    for (int i = tid; i < kTab; i += kThreads) {
+      s_head[i] = i < tp.n_roles ? tp.role_head[i] : 1;
+      s_kx[i] = i < tp.n_knots ? tp.iso_x[i] : 0.0f;
+      s_ky[i] = i < tp.n_knots ? tp.iso_y[i] : 0.0f;
+    }
+  }
   for (int i = tid; i < kMaxModels; i += kThreads) s_alpha[i] = i < n_models ? alpha[i] : 0.0f;
   __syncthreads();
 
@@ -538,8 +620,13 @@ void mlp3_bf16_kernel(
 
     const int local = wave * kRowsPerWave + r32;
     const int64_t row = tile * kRowsPerBlock + local;
-    length_epilogue<BT>(logit, s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
-                        s_alpha, pred_len, kv_bytes);
+    if constexpr (kTwoPhase)
+      two_phase_epilogue<BT>(logit, s_b3, s_c, s_head, s_kx, s_ky, tp, h, row, n, s_meta[parity][0][local],
+                             s_meta[parity][1][local], s_meta[parity][2][local], s_meta[parity][3][local], s_alpha,
+                             pred_len, kv_bytes);
+    else
+      length_epilogue<BT>(logit, s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
+                          s_alpha, pred_len, kv_bytes);
   }
   wait_chunk<0>();                        // no load into LDS outlives the workgroup
 }
@@ -654,13 +741,44 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
           static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
           static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
           p.bias[0], p.bias[1], p.bias[2], p.bin_centre, n, n_tiles, prompt_len, model_id,
-          kv_bytes_per_token, n_models, pred_len, kv_bytes);
+          kv_bytes_per_token, n_models, pred_len, kv_bytes, TwoPhaseArgs{});
     };
-    if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64>);
-    else args(mlp3_bf16_kernel<256, 1024, 1024, 64>);
+    if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, false>);
+    else args(mlp3_bf16_kernel<256, 1024, 1024, 64, false>);
   } else {
     return MAESTRO_ERR_UNSUPPORTED;
   }
+  return launch_status();
+}
+
+bool two_phase_shape_supported(const maestro_predictor& p) {
+  return dims_are(p, 3, MAESTRO_BF16, kBf16Mid) || dims_are(p, 3, MAESTRO_BF16, kBf16Wide);
+}
+
+maestro_status launch_predict_two_phase(const maestro_predictor& p, const maestro_two_phase& t, int64_t n,
+                                        const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                        const int32_t* role_id, const int32_t* tool_avail,
+                                        const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
+                                        float* pred_len, double* kv_bytes, hipStream_t stream) {
+  if (n == 0) return MAESTRO_OK;
+  if (!two_phase_shape_supported(p)) return MAESTRO_ERR_UNSUPPORTED;
+  const int64_t n_tiles = (n + kRowsPerBlock - 1) / kRowsPerBlock;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return MAESTRO_ERR_LAUNCH;
+  const dim3 pgrid((unsigned)(n_tiles < cus ? n_tiles : cus)), block(kThreads);
+  const TwoPhaseArgs tp{role_id, tool_avail, t.role_head, t.tool_coef, t.iso_x, t.iso_y,
+                        t.n_roles, t.n_knots, t.max_len, p_tool};
+  auto args = [&](auto kernel) {
+    kernel<<<pgrid, block, 0, stream>>>(
+        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
+        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
+        p.bias[0], p.bias[1], p.bias[2], nullptr, n, n_tiles, prompt_len, model_id,
+        kv_bytes_per_token, n_models, pred_len, kv_bytes, tp);
+  };
+  if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, true>);
+  else args(mlp3_bf16_kernel<256, 1024, 1024, 64, true>);
   return launch_status();
 }
 

@@ -440,6 +440,48 @@ def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
                         cost_ms=cost.astype(np.float32), c_int_ms=C_INT_MS, deg_window=deg_window)
 
 
+TWO_PHASE_STREAMS = ("head", "head_bias", "coef", "iso", "tools")
+
+
+@dataclass
+class TwoPhaseInputs:
+    """Stand-in weights of the two-phase predictor's heads (the last layer of the workload's
+    network, read as heads) and its per-stage inputs."""
+    head_weight: np.ndarray       # [B][H] float32 or uint16 (bf16 bits): row 0 tool intent, g >= 1 length heads
+    head_bias: np.ndarray         # [B] float32
+    role_head: np.ndarray         # [n_roles] int32
+    tool_coef: np.ndarray         # [B] float32
+    iso_x: np.ndarray             # [K] float32, strictly increasing
+    iso_y: np.ndarray             # [K] float32, non-decreasing
+    max_len: float
+    tool_avail: np.ndarray        # [N] int32
+
+
+def two_phase_inputs(wl: Workload, n_knots: int = 16, max_len: float = 32768.0) -> TwoPhaseInputs:
+    """Two-phase predictor inputs for ``wl`` (seeded by its spec's seed).
+
+    Heads: row 0 (tool intent) N(0, 1/H) weights and bias 0; rows g >= 1 (log(1 + L)
+    regressors) N(0, 1/H) weights and biases U[4.5, 6.5] (outputs of e^4.5 - e^6.5 tokens
+    before the feature terms). Roles 0, 1, 2 have their own heads (2, 3, 4); the others use the
+    shared head 1. The tool probability shortens the prediction: coefficients U[-2.5, -1.5].
+    The calibration map has n_knots knots from 0 to 1 with sorted uniform values. 60% of stages
+    have tools available."""
+    children = np.random.SeedSequence([wl.spec.seed, 0x2FA5E]).spawn(len(TWO_PHASE_STREAMS))
+    r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(TWO_PHASE_STREAMS, children)}
+    B, H = wl.weights[-1].shape
+    w = r["head"].normal(0.0, H ** -0.5, size=(B, H)).astype(np.float32)
+    bias = np.zeros(B, np.float32)
+    bias[1:] = r["head_bias"].uniform(4.5, 6.5, B - 1)
+    coef = np.zeros(B, np.float32)
+    coef[1:] = r["coef"].uniform(-2.5, -1.5, B - 1)
+    x = np.concatenate([[0.0], np.sort(r["iso"].uniform(0.0, 1.0, n_knots - 2)), [1.0]]).astype(np.float32)
+    y = np.sort(r["iso"].uniform(0.0, 1.0, n_knots)).astype(np.float32)
+    tools = (r["tools"].random(wl.n) < 0.6).astype(np.int32)
+    return TwoPhaseInputs(head_weight=w if wl.spec.dtype == "f32" else f32_to_bf16_bits(w), head_bias=bias,
+                          role_head=np.array([2, 3, 4], np.int32), tool_coef=coef, iso_x=x, iso_y=y,
+                          max_len=max_len, tool_avail=tools)
+
+
 def workload(name: str, with_x: bool = True, **overrides) -> Workload:
     """Named workload, optionally with fields of its spec replaced (e.g. ``n_stages=5000``)."""
     spec = SPECS[name]

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -80,6 +80,38 @@ def test_predict_validation(lib):
     assert call(_pred((256, 384, 512, 64), 1, 3)) == UNSUPPORTED              # not built
     assert call(_pred((64, 128, 32), 1, 2)) == UNSUPPORTED                    # wrong dtype
     assert lib.maestro_predict_workspace(ctypes.byref(_pred((64, 128, 32), 0, 2)), 100) == 0
+
+
+def test_predict_two_phase_validation(lib):
+    def tp(n_roles=3, n_knots=16, max_len=32768.0, coef=FAKE16, head=FAKE, kx=FAKE, ky=FAKE):
+        return M.TwoPhase(n_roles=n_roles, n_knots=n_knots, role_head=head.value if head else None,
+                          tool_coef=coef.value if coef else None, iso_x=kx.value if kx else None,
+                          iso_y=ky.value if ky else None, max_len=max_len)
+
+    def call(p, t, n=10, x=FAKE, role=FAKE, tools=FAKE):
+        return lib.maestro_predict_two_phase(ctypes.byref(p) if p is not None else None,
+                                             ctypes.byref(t) if t is not None else None, n, x, FAKE, FAKE, role,
+                                             tools, FAKE, 4, None, FAKE, FAKE, None)
+    good = _pred((256, 512, 512, 64), 1, 3)
+    assert call(None, tp()) == INVALID
+    assert call(good, None) == INVALID
+    assert call(good, tp(), n=-1) == INVALID
+    assert call(good, tp(n_knots=1)) == INVALID                                 # a map needs two knots
+    assert call(good, tp(n_knots=65)) == INVALID
+    assert call(good, tp(n_roles=65)) == INVALID
+    assert call(good, tp(n_roles=-1)) == INVALID
+    assert call(good, tp(head=None)) == INVALID                                 # roles without a table
+    assert call(good, tp(max_len=0.0)) == INVALID
+    assert call(good, tp(max_len=float("inf"))) == INVALID
+    assert call(good, tp(max_len=float("nan"))) == INVALID
+    assert call(good, tp(coef=None)) == INVALID
+    assert call(good, tp(coef=MISALIGNED16)) == INVALID                         # 16-byte aligned table
+    assert call(good, tp(kx=None)) == INVALID
+    assert call(good, tp(), role=None) == INVALID                              # per-stage roles missing
+    assert call(good, tp(), tools=MISALIGNED4) == INVALID
+    assert call(_pred((64, 128, 32), 0, 2), tp()) == UNSUPPORTED                # float32 network: not built
+    assert call(_pred((256, 384, 512, 64), 1, 3), tp()) == UNSUPPORTED
+    assert call(good, tp(n_roles=0, head=None), n=0, x=None, role=None, tools=None) == OK   # empty batch
 
 
 def test_route_validation(lib):

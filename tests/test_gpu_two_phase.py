@@ -1,0 +1,152 @@
+"""Parity of the two-phase predictor (Sec. III-B: calibrated tool intent, Eq. 1; per-role log(1 + L)
+regressors; Eq. 3) between the HIP path (through the C-ABI) and the CPU oracle, on seeded inputs.
+
+Bars (element by element), from an error bound DZ = 1e-2 on every head's pre-activation z (the
+GPU accumulates in float32, the oracle in float64, and a bfloat16 hidden activation whose two
+pre-activations straddle a rounding boundary differs by one bfloat16 ulp, 2^-7 relative; the
+worst case seen is about 1e-3):
+  p_tool : |dp| <= 0.25 * S * DZ, S the steepest slope of the calibration table (the logistic
+           function's slope is at most 1/4);
+  length : |dL| <= (1 + L) * (DZ + |coef_g| |dp|), since y = z_g + coef_g p and L = expm1(y);
+  kv     : equal, bit for bit, to Eq. 3 on the GPU's own length.
+and, against systematic slips, 99% of stages within 1e-4 in p and 1e-3 in log(1 + L).
+"""
+import ctypes
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_12950_amd as M
+from paper_2606_12950_amd import _native, pipeline
+from paper_2606_12950_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+DZ = 1e-2
+
+
+def _t(a):
+    return pipeline._t(np.ascontiguousarray(a), "cuda")
+
+
+@functools.lru_cache(maxsize=None)
+def _wl(name, n=None):
+    return W.workload(name) if n is None else W.workload(name, n_stages=n)
+
+
+def _inputs(w, **over):
+    tp = W.two_phase_inputs(w)
+    for k, v in over.items():
+        setattr(tp, k, v)
+    return tp
+
+
+def gpu_two_phase(w, tp, rows=None, role=None):
+    sel = slice(None) if rows is None else rows
+    role = w.role[sel] if role is None else role
+    ws = [_t(a) for a in w.weights[:-1]] + [_t(tp.head_weight)]
+    bs = [_t(a) for a in w.biases[:-1]] + [_t(tp.head_bias)]
+    pt, pl, kv = M.predict_two_phase(_t(w.x[sel]), ws, bs, _t(tp.role_head), _t(tp.tool_coef), _t(tp.iso_x),
+                                     _t(tp.iso_y), tp.max_len, _t(w.prompt_len[sel]), _t(w.model_id[sel]),
+                                     _t(role), _t(tp.tool_avail[sel]), _t(w.kv_bytes_per_token))
+    torch.cuda.synchronize()
+    return pt.cpu().numpy(), pl.cpu().numpy(), kv.cpu().numpy()
+
+
+def oracle_two_phase(w, tp, rows=None, role=None):
+    sel = slice(None) if rows is None else rows
+    role = w.role[sel] if role is None else role
+    return oracle.predict_two_phase(w.x[sel], w.weights[:-1] + [tp.head_weight], w.biases[:-1] + [tp.head_bias],
+                                    tp.role_head, tp.tool_coef, tp.iso_x, tp.iso_y, tp.max_len, w.prompt_len[sel],
+                                    w.model_id[sel], role, tp.tool_avail[sel], w.kv_bytes_per_token, w.spec.dtype)
+
+
+def check(w, tp, got, ref, rows=None, role=None):
+    sel = slice(None) if rows is None else rows
+    role = w.role[sel] if role is None else role
+    pg, lg, kg = got
+    po, lo, _ = ref
+    assert np.all(np.isfinite(pg)) and np.all(np.isfinite(lg))
+    slope = (np.diff(tp.iso_y.astype(np.float64)) / np.diff(tp.iso_x.astype(np.float64))).max()
+    dp = np.abs(pg.astype(np.float64) - po)
+    assert dp.max() <= 0.25 * slope * DZ, f"p_tool max err {dp.max():.3e} at {dp.argmax()}"
+    g = np.ones(role.shape[0], np.int64)
+    ok = (role >= 0) & (role < tp.role_head.size)
+    g[ok] = tp.role_head[role[ok]]
+    g[(g < 1) | (g >= tp.tool_coef.size)] = 1
+    dl = np.abs(lg.astype(np.float64) - lo) / (1.0 + lo.astype(np.float64))
+    bound = DZ + np.abs(tp.tool_coef[g].astype(np.float64)) * dp
+    assert np.all(dl <= bound), f"length err {dl.max():.3e} at {dl.argmax()}: {lg[dl.argmax()]} vs {lo[dl.argmax()]}"
+    assert np.quantile(dp, 0.99) <= 1e-4 and np.quantile(dl, 0.99) <= 1e-3
+    assert np.all(pg[tp.tool_avail[sel] == 0] == 0.0)
+    alpha = w.kv_bytes_per_token[w.model_id[sel]].astype(np.float64)
+    assert np.array_equal(kg, (w.prompt_len[sel].astype(np.float64) + lg.astype(np.float64)) * alpha)
+    return dp.max(), dl.max()
+
+
+@pytest.mark.parametrize("name,n", [("c1", 1), ("c1", 129), ("c1", 777), ("c1", None), ("c4", 1000), ("c4", 4097)])
+def test_two_phase_matches_oracle(name, n):
+    # mid (256-512-512-64) and wide (256-1024-1024-64) networks; ragged tiles of 128 rows
+    w = _wl(name, n)
+    tp = _inputs(w)
+    got = gpu_two_phase(w, tp)
+    dp, dl = check(w, tp, got, oracle_two_phase(w, tp))
+    print(f"{name} n={w.n}: max |dp| {dp:.2e}, max |dL|/(1+L) {dl:.2e}, mean L {got[1].mean():.1f}")
+
+
+def test_two_phase_full_size_sampled():
+    # 4,194,304 stages through the wide network in one launch; 20,000 sampled rows against the oracle
+    w = _wl("c4")
+    tp = _inputs(w)
+    got = gpu_two_phase(w, tp)
+    rows = np.sort(np.random.default_rng(5).choice(w.n, 20000, replace=False))
+    check(w, tp, tuple(a[rows] for a in got), oracle_two_phase(w, tp, rows=rows), rows=rows)
+
+
+def test_two_phase_roles_tools_table_and_clamps():
+    w = _wl("c1", 3000)
+    rng = np.random.default_rng(7)
+    role = rng.integers(-3, 70, w.n).astype(np.int32)            # many roles without a head of their own
+    cases = [
+        dict(),                                                  # the workload's own inputs
+        dict(role_head=np.zeros(0, np.int32)),                   # every role uses the shared head
+        dict(role_head=np.array([5, 63, 0, 64, 1, 9, -4], np.int32)),   # heads at and beyond the ends
+        dict(tool_avail=np.zeros(w.n, np.int32)),                # no tools anywhere
+        dict(iso_x=np.array([0.2, 0.8], np.float32), iso_y=np.array([0.1, 0.9], np.float32)),  # two knots
+        dict(max_len=150.0),                                     # the clamp bites
+        dict(tool_coef=np.full(64, 3.0, np.float32)),            # tool probability lengthens outputs
+    ]
+    for over in cases:
+        tp = _inputs(w, **over)
+        check(w, tp, gpu_two_phase(w, tp, role=role), oracle_two_phase(w, tp, role=role), role=role)
+    tp = _inputs(w, max_len=150.0)
+    assert (gpu_two_phase(w, tp, role=role)[1] == np.float32(150.0)).any()
+
+
+def test_two_phase_without_p_tool_output_and_empty():
+    w = _wl("c1", 300)
+    tp = _inputs(w)
+    ref = gpu_two_phase(w, tp)
+    lib = M.load()
+    ws = [_t(a) for a in w.weights[:-1]] + [_t(tp.head_weight)]
+    bs = [_t(a) for a in w.biases[:-1]] + [_t(tp.head_bias)]
+    p = _native.make_predictor(ws, bs, None)
+    keep = [_t(tp.role_head), _t(tp.tool_coef), _t(tp.iso_x), _t(tp.iso_y)]
+    t = _native.TwoPhase(n_roles=3, n_knots=tp.iso_x.size, role_head=keep[0].data_ptr(), tool_coef=keep[1].data_ptr(),
+                         iso_x=keep[2].data_ptr(), iso_y=keep[3].data_ptr(), max_len=tp.max_len)
+    x, P, m, r, ta, a = (_t(w.x), _t(w.prompt_len), _t(w.model_id), _t(w.role), _t(tp.tool_avail),
+                         _t(w.kv_bytes_per_token))
+    pl = torch.empty(w.n, dtype=torch.float32, device="cuda")
+    kv = torch.empty(w.n, dtype=torch.float64, device="cuda")
+    st = lib.maestro_predict_two_phase(ctypes.byref(p), ctypes.byref(t), w.n, x.data_ptr(), P.data_ptr(),
+                                       m.data_ptr(), r.data_ptr(), ta.data_ptr(), a.data_ptr(), a.shape[0], None,
+                                       pl.data_ptr(), kv.data_ptr(), None)
+    torch.cuda.synchronize()
+    assert st == 0
+    assert np.array_equal(pl.cpu().numpy(), ref[1]) and np.array_equal(kv.cpu().numpy(), ref[2])
+    st = lib.maestro_predict_two_phase(ctypes.byref(p), ctypes.byref(t), 0, None, None, None, None, None,
+                                       a.data_ptr(), a.shape[0], None, None, None, None)
+    assert st == 0
