@@ -5,6 +5,7 @@ python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for 
 python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
 python bench.py --route-fitness        (routing by fitness, Eq. 5, on the workload's predictions)
 python bench.py --route-fitness --plans   (the same with C_deg from degradation plans, Alg. 2)
+python bench.py --two-phase            (the two-phase predictor, Sec. III-B, beside the bins one)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -235,6 +236,48 @@ def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False)
                       "routed_frac": float((out[0][:, 0] >= 0).float().mean().item()), **extra}), flush=True)
 
 
+def two_phase_bench(name: str, steps: int, warmup: int):
+    """The two-phase predictor (calibrated tool intent, per-role log(1 + L) heads) and the bins
+    predictor on the same network and batch, interleaved; MFMA roofline of each. One JSON line."""
+    import torch
+    from paper_2606_12950_amd import _native, pipeline
+    from paper_2606_12950_amd import workload as W
+    torch.cuda.set_device(0)
+    wl = W.workload(name)
+    if wl.spec.dtype != "bf16":
+        print("the two-phase predictor is built for the bfloat16 networks (c1 .. c4)", file=sys.stderr)
+        sys.exit(2)
+    tp = W.two_phase_inputs(wl)
+    b = pipeline.to_device(wl)
+    o = pipeline.allocate_outputs(b)
+    t = lambda a: pipeline._t(a, "cuda")
+    ws = b.weights[:-1] + [t(tp.head_weight)]
+    bs = b.biases[:-1] + [t(tp.head_bias)]
+    tabs = [t(tp.role_head), t(tp.tool_coef), t(tp.iso_x), t(tp.iso_y)]
+    role, tools = t(wl.role), t(tp.tool_avail)
+    n = wl.n
+    out = (torch.empty(n, dtype=torch.float32, device="cuda"), torch.empty(n, dtype=torch.float32, device="cuda"),
+           torch.empty(n, dtype=torch.float64, device="cuda"))
+    two = lambda: _native.predict_two_phase(b.x, ws, bs, *tabs, tp.max_len, b.prompt_len, b.model_id, role, tools,
+                                            b.kv_bytes_per_token, out=out)
+    bins = lambda: pipeline.run_predict(b, o)
+    d2 = _time_events(two, steps, warmup)
+    d1 = _time_events(bins, steps, warmup)
+    d2 += _time_events(two, steps, 0)
+    d1 += _time_events(bins, steps, 0)
+    flop = mlp_flop_per_stage(wl.spec.dims) * n
+    res = {"workload": name, "n_stages": n, "predictor": "-".join(map(str, wl.spec.dims)), "flop_per_launch": flop}
+    for key, d in (("two_phase", d2), ("bins", d1)):
+        ms = float(np.mean(d))
+        res[key] = {"ms": round(ms, 4), "phase_ms": percentiles(d), "stages_per_s": n / (ms * 1e-3),
+                    "roofline": {"bound": "mfma", "achieved": round(flop / (ms * 1e-3) / 1e12, 2),
+                                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+    res["mean_p_tool"] = float(out[0].mean().item())
+    res["mean_pred_len"] = float(out[1].mean().item())
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -250,10 +293,15 @@ def main():
                     help="time routing by fitness (Eq. 5) on the workload's predictions")
     ap.add_argument("--plans", action="store_true",
                     help="with --route-fitness: C_deg from degradation plans (Alg. 2, Eq. 4)")
+    ap.add_argument("--two-phase", action="store_true",
+                    help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.two_phase:
+        two_phase_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
         return
     if args.route_fitness:
         route_fitness_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)),
