@@ -122,7 +122,8 @@ def cpu_baseline(wl, n_workflows_sample: int):
     if W_:
         oracle.prioritize(wl.chain_offset[:W_ + 1], sc[:, 0], wl.deadline_us[:W_], wl.now_us)
     dt = time.perf_counter() - t0
-    sample = (f"first {W_} workflows ({S} stages) of the same batch: oracle predict + route + prioritize"
+    which = "all" if W_ == wl.n_workflows else "first"
+    sample = (f"{which} {W_} workflows ({S} stages) of the same batch: oracle predict + route + prioritize"
               if W_ else f"first {S} stages of the same batch: oracle predict + route")
     return {"value": S / dt, "unit": "stages/s", "cores": int(threads), "kind": "oracle",
             "sample": sample, "seconds": round(dt, 3), "cpu_model": cpu_model()}
@@ -284,7 +285,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="c3", choices=["c0", "c1", "c2", "c3", "c4"])
-    ap.add_argument("--cpu-sample-workflows", type=int, default=65536)
+    ap.add_argument("--cpu-sample-workflows", type=int, default=131072)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--sweep-prioritize", nargs="?", const="17:26", default=None, metavar="LO:HI",
