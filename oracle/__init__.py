@@ -25,6 +25,10 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
   degradation_cost - pinned: brute force over priority prefixes (the shortest prefix of the
                level-sorted engines that frees R), closed forms (R <= 0, one engine, Failure), the
                interrupt penalty exactly when a level-4/5 engine is in the plan, stable order.
+  activation_latency - pinned (tests/test_oracle_readiness_pins.py): Running is free, size 0
+               leaves the setup, doubling a bandwidth halves the transfer exactly, tiers past
+               Remote count as Remote; fitness routing with a matrix of {0, act} equals the
+               resident-mask form.
   quantiles  - pinned: numpy's percentile selection ("lower" / "higher" methods).
   prioritize - pinned: closed forms (unit latencies), numpy stable argsort, O(len^2) suffix
                sums, half-even rounding cases, int32 clamping, non-finite latency handling.
@@ -72,8 +76,10 @@ def _load():
     lib.oracle_predict_two_phase.restype = ctypes.c_int
     lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
-    lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
+    lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
                                          f64, i32, P, P, P, P, ctypes.c_float, P, P, i32]
+    lib.oracle_activation_latency.argtypes = [i32, i32, P, P, P, P, P]
+    lib.oracle_activation_latency.restype = ctypes.c_int
     lib.oracle_degradation_cost.argtypes = [f64, i32, P, P, P, ctypes.c_float, P]
     lib.oracle_degradation_cost.restype = ctypes.c_int
     lib.oracle_route_fitness.restype = ctypes.c_int
@@ -202,11 +208,13 @@ def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s,
 
 def route_fitness(model_id, src_id, class_id, kv_bytes, free_bytes, queue_ms, act_ms, resident_mask,
                   deg_ms, rtt_ms, class_weights, bounds, k: int = 1, rho: float = 0.0, n_models: int = 0,
-                  n_threads: int = 0, engines=None):
+                  n_threads: int = 0, engines=None, act_matrix=None):
     """Alg. 3 with the fitness of Eq. 5. rtt_ms [n_src][M]; class_weights [n_classes][3] =
     (gamma, lambda, mu); bounds [6] = window bounds (lo, hi) of RTT, T_ready, C_deg. With
     ``engines`` = (offset [M+1] int32, level [E] int32, freed [E] float64, cost [E] float32,
     c_int) the disruption cost is Alg. 2 / Eq. 4's per (stage, node) and ``deg_ms`` is unused.
+    With ``act_matrix`` [M][n_models] (n_models required) T_act comes from it and ``act_ms`` /
+    ``resident_mask`` are unused.
     Returns (node_idx int32 [N][k], fitness float32 [N][k])."""
     lib = _load()
     mi = _c(model_id, np.int32)
@@ -227,8 +235,14 @@ def route_fitness(model_id, src_id, class_id, kv_bytes, free_bytes, queue_ms, ac
         eo, el = _c(engines[0], np.int32), _c(engines[1], np.int32)
         ef, ec = _c(engines[2], np.float64), _c(engines[3], np.float32)
         c_int = float(engines[4])
+    am = None
+    if act_matrix is not None:
+        if not n_models:
+            raise ValueError("act_matrix needs n_models")
+        am = _c(act_matrix, np.float32)
+        assert am.shape == (M, n_models)
     st = lib.oracle_route_fitness(n, _ptr(mi), _ptr(si), _ptr(ci), _ptr(kv), n_models or 64, M,
-                                  rtt.shape[0], cw.shape[0], _ptr(fr), _ptr(q), _ptr(act), _ptr(rm),
+                                  rtt.shape[0], cw.shape[0], _ptr(fr), _ptr(q), _ptr(act), _ptr(rm), _ptr(am),
                                   _ptr(dg), _ptr(rtt), _ptr(cw), _ptr(bd), float(rho), int(k),
                                   _ptr(eo), _ptr(el), _ptr(ef), _ptr(ec), c_int,
                                   _ptr(idx), _ptr(fit), n_threads or max_threads())
@@ -245,6 +259,21 @@ def degradation_cost(R: float, level, freed, cost, c_int: float):
     out = np.zeros(1, np.float32)
     st = lib.oracle_degradation_cost(float(R), lv.shape[0], _ptr(lv), _ptr(fr), _ptr(co), float(c_int), _ptr(out))
     return None if st else float(out[0])
+
+
+def activation_latency(tier, model_bytes, tier_bw, tier_setup_ms):
+    """T_act [M][K] float32 (ms) of every model on every node from its readiness tier [M][K]
+    (0 Running, 1 Sleeping, 2 CPU, 3 Disk, 4 Remote): Size / BW_tier plus a per-tier setup."""
+    lib = _load()
+    t = _c(tier, np.uint8)
+    M, K = t.shape
+    mb, bw, st_ = _c(model_bytes, np.float64), _c(tier_bw, np.float64), _c(tier_setup_ms, np.float32)
+    assert mb.shape == (K,) and bw.shape == (5,) and st_.shape == (5,)
+    out = np.empty((M, K), np.float32)
+    st = lib.oracle_activation_latency(M, K, _ptr(t), _ptr(mb), _ptr(bw), _ptr(st_), _ptr(out))
+    if st != 0:
+        raise RuntimeError(f"oracle_activation_latency failed with status {st}")
+    return out
 
 
 def quantiles(values, q_lo: float = 0.05, q_hi: float = 0.95):

@@ -317,6 +317,27 @@ int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
 /* route by fitness: Eq. 5 over the feasible nodes, Alg. 3 (argmax with strict ">")            */
 /* ------------------------------------------------------------------------------------------ */
 
+/* Model readiness (Sec. III-C): the activation latency of model m on a node whose copy of m is
+ * in tier t -- 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote (tiers past 4
+ * count as Remote) -- from the profiled bandwidth model T_act = Size / BW_tier, plus a fixed
+ * per-tier setup time: 0 when Running, else setup_ms[t] + (bytes[m] / bw[t]) * 1000 ms,
+ * evaluated in float64 in that order and stored as float32. */
+int oracle_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
+                              const double* model_bytes, const double* tier_bw,
+                              const float* tier_setup_ms, float* act_ms) {
+  if (n_nodes < 0 || n_models < 1) return ORACLE_BAD_ARG;
+  for (int64_t j = 0; j < (int64_t)n_nodes; ++j) {
+    for (int32_t m = 0; m < n_models; ++m) {
+      int t = tier[j * n_models + m];
+      if (t > 4) t = 4;
+      float a = 0.0f;
+      if (t > 0) a = (float)((double)tier_setup_ms[t] + (model_bytes[m] / tier_bw[t]) * 1000.0);
+      act_ms[j * n_models + m] = a;
+    }
+  }
+  return ORACLE_OK;
+}
+
 /* robust min-max normalisation onto [0, 1] with window bounds lo, hi (values outside the
  * bounds clip); a degenerate window (hi <= lo) maps everything to 0. float32 throughout. */
 static float norm_inv(float lo, float hi) { return hi > lo ? 1.0f / (hi - lo) : 0.0f; }
@@ -374,9 +395,9 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
                          const int32_t* class_id, const double* kv_bytes, int32_t n_models,
                          int32_t n_nodes, int32_t n_src, int32_t n_classes,
                          const double* free_bytes, const float* queue_ms, const float* act_ms,
-                         const uint64_t* resident_mask, const float* deg_ms, const float* rtt_ms,
-                         const float* class_weights, const float* bounds, double rho, int32_t k,
-                         const int32_t* engine_offset, const int32_t* engine_level,
+                         const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
+                         const float* rtt_ms, const float* class_weights, const float* bounds, double rho,
+                         int32_t k, const int32_t* engine_offset, const int32_t* engine_level,
                          const double* engine_freed, const float* engine_cost, float c_int,
                          int32_t* node_idx, float* fitness, int32_t n_threads) {
   if (n < 0 || n_nodes < 1 || n_models < 1 || n_models > 64 || n_src < 1 || n_classes < 1 ||
@@ -431,9 +452,16 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
           float fit = freef > 0.0f ? needf * (1.0f / freef) : 1.0f;
           if (fit > 1.0f) fit = 1.0f;
           const float a = gamma * prox + (1.0f - gamma) * fit;
-          /* RuntimeEstimate: T_ready = T_q + T_act (Eq. 6), C_deg as reported */
-          const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
-          const float ready = queue_ms[nd] + (resident ? 0.0f : act_ms[nd]);
+          /* RuntimeEstimate: T_ready = T_q + T_act (Eq. 6): T_act of model m on this node from the
+           * per-(node, model) matrix, or else the node's activation latency unless m is resident */
+          float act;
+          if (act_matrix) {
+            act = act_matrix[(int64_t)nd * n_models + m];
+          } else {
+            const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
+            act = resident ? 0.0f : act_ms[nd];
+          }
+          const float ready = queue_ms[nd] + act;
           /* Eq. 5: S = A - lambda * T_ready - mu * C_deg, on normalised metrics */
           const float s = (a - lambda * norm01(ready, bounds[2], inv_ready)) - mu * norm01(c_deg, bounds[4], inv_deg);
           c[nc].s = s;

@@ -1,0 +1,82 @@
+"""Pins of the oracle's model-readiness inputs (Sec. III-C: five readiness states, T_act from a
+profiled bandwidth model, Size / BW_tier) and their use as T_act(N, M(T)) in Eq. 6 -- no GPU."""
+import numpy as np
+
+import oracle
+
+GB = 1e9
+BW = np.array([1.0, 25.0, 25.0, 3.0, 1.25]) * GB           # bytes/s per tier (tier 0 unused)
+SETUP = np.array([0.0, 150.0, 2500.0, 2500.0, 4000.0], np.float32)
+
+
+def test_activation_latency_closed_forms():
+    rng = np.random.default_rng(1)
+    M, K = 40, 7
+    tier = rng.integers(0, 8, (M, K)).astype(np.uint8)
+    size = rng.uniform(1, 30, K) * GB
+    act = oracle.activation_latency(tier, size, BW, SETUP)
+    assert np.all(act[tier == 0] == 0.0)                    # Running: nothing to activate
+    # tiers past Remote count as Remote
+    assert np.array_equal(act, oracle.activation_latency(np.minimum(tier, 4), size, BW, SETUP))
+    # size 0 leaves the setup; 1 GB over 1 GB/s is 1000 ms exactly
+    z = oracle.activation_latency(tier, np.zeros(K), BW, SETUP)
+    assert np.array_equal(z, np.where(tier == 0, 0.0, SETUP[np.minimum(tier, 4)]).astype(np.float32))
+    one = oracle.activation_latency(np.full((1, 1), 4, np.uint8), np.array([1.25 * GB]), BW, np.zeros(5, np.float32))
+    assert one[0, 0] == 1000.0
+    # without setup, doubling every bandwidth halves every latency exactly (powers of two)
+    a1 = oracle.activation_latency(tier, size, BW, np.zeros(5, np.float32))
+    a2 = oracle.activation_latency(tier, size, 2 * BW, np.zeros(5, np.float32))
+    assert np.array_equal(a1, 2 * a2)
+    # slower tiers of the same model take longer (bandwidths fall, setups rise from tier 1 on)
+    for m in range(K):
+        lat = oracle.activation_latency(np.arange(5, dtype=np.uint8)[:, None].repeat(1, 1), size[m:m + 1], BW, SETUP)
+        assert lat[0, 0] == 0.0 and np.all(np.diff(lat[1:, 0]) > 0)
+
+
+def _fitness_case(rng, n, M, n_models=16):
+    nodes = dict(free_bytes=rng.uniform(0, 300, M) * GB, queue_ms=rng.uniform(0, 5000, M).astype(np.float32),
+                 act_ms=rng.uniform(2000, 20000, M).astype(np.float32),
+                 resident_mask=rng.integers(0, 1 << n_models, M).astype(np.uint64),
+                 deg_ms=rng.uniform(0, 500, M).astype(np.float32), rtt_ms=rng.uniform(0.2, 80, (3, M)).astype(np.float32))
+    stages = dict(model=rng.integers(0, n_models, n).astype(np.int32), src=rng.integers(0, 3, n).astype(np.int32),
+                  cls=rng.integers(0, 2, n).astype(np.int32), kv=rng.uniform(0, 250, n) * GB)
+    return nodes, stages
+
+
+def _route(nodes, st, weights, bounds, k=3, n_models=16, act_matrix=None):
+    return oracle.route_fitness(st["model"], st["src"], st["cls"], st["kv"], nodes["free_bytes"], nodes["queue_ms"],
+                                nodes["act_ms"], nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                                np.asarray(weights, np.float32), np.asarray(bounds, np.float32), k=k,
+                                n_models=n_models, act_matrix=act_matrix)
+
+
+def test_matrix_of_resident_bits_equals_the_mask_form():
+    # T_act(N, m) = 0 where m is resident on N, the node's activation latency otherwise: the same
+    # fitness, bit for bit, as the resident-mask form of Eq. 6
+    rng = np.random.default_rng(2)
+    nodes, st = _fitness_case(rng, 800, 300)
+    bits = (nodes["resident_mask"][:, None] >> np.arange(16, dtype=np.uint64)[None, :]) & np.uint64(1)
+    mat = np.where(bits == 1, 0.0, nodes["act_ms"][:, None]).astype(np.float32)
+    w, b = [[0.25, 1, 1], [0.1, 1, 1]], [0, 80, 0, 25000, 0, 500]
+    i0, f0 = _route(nodes, st, w, b)
+    i1, f1 = _route(nodes, st, w, b, act_matrix=mat)
+    assert np.array_equal(i0, i1) and np.array_equal(f0.view(np.uint32), f1.view(np.uint32))
+
+
+def test_readiness_is_per_model():
+    # two nodes, equal in everything but which model is warm on which: with proximity equal and
+    # lambda = 1, each model's stages go to the node where that model is ready
+    M, n_models = 2, 2
+    nodes = dict(free_bytes=np.full(M, 100 * GB), queue_ms=np.zeros(M, np.float32), act_ms=np.zeros(M, np.float32),
+                 resident_mask=np.zeros(M, np.uint64), deg_ms=np.zeros(M, np.float32),
+                 rtt_ms=np.ones((1, M), np.float32))
+    tier = np.array([[0, 4], [3, 1]], np.uint8)              # node 0: model 0 running; node 1: model 1 sleeping
+    act = oracle.activation_latency(tier, np.array([16 * GB, 16 * GB]), BW, SETUP)
+    st = dict(model=np.array([0, 1, 0, 1], np.int32), src=np.zeros(4, np.int32), cls=np.zeros(4, np.int32),
+              kv=np.full(4, GB))
+    idx, _ = _route(nodes, st, [[1, 1, 0]], [0, 1, 0, 20000, 0, 1], k=1, n_models=n_models, act_matrix=act)
+    assert idx[:, 0].tolist() == [0, 1, 0, 1]
+    # the same stages with the tiers swapped swap nodes
+    act2 = oracle.activation_latency(tier[::-1].copy(), np.array([16 * GB, 16 * GB]), BW, SETUP)
+    idx, _ = _route(nodes, st, [[1, 1, 0]], [0, 1, 0, 20000, 0, 1], k=1, n_models=n_models, act_matrix=act2)
+    assert idx[:, 0].tolist() == [1, 0, 1, 0]
