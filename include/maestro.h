@@ -239,7 +239,8 @@ MAESTRO_API maestro_status maestro_degradation_plans(int32_t n_nodes, const int3
  *   fit   = min(1, fl32(need) * (1 / fl32(free_bytes[j])))   best fit of R_need to the headroom
  *           (1 when fl32(free_bytes[j]) == 0)
  *   A     = gamma * prox + (1 - gamma) * fit               affinity
- *   T_ready = queue_ms[j] + (bit m of resident_mask[j] ? 0 : act_ms[j])
+ *   T_ready = queue_ms[j] + T_act,  T_act = act_matrix[j][m] when given, else
+ *             (bit m of resident_mask[j] ? 0 : act_ms[j])                       (Eq. 6)
  *   S     = (A - lambda * norm_READY(T_ready)) - mu * norm_DEG(C_deg)
  *   every operation float32 round-to-nearest, in exactly this order; output the k feasible
  *   nodes with the largest S, the lower node index first on equal S (the strict ">" of Alg.
@@ -250,6 +251,9 @@ MAESTRO_API maestro_status maestro_degradation_plans(int32_t n_nodes, const int3
  *   free_bytes          [n_nodes] float64: KV admission headroom R_head (bytes)
  *   queue_ms, act_ms    [n_nodes] float32: queueing delay T_q, activation latency T_act (ms)
  *   resident_mask       [n_nodes] uint64: bit m set <=> model m is warm on the node
+ *   act_matrix          [n_nodes][n_models] float32 T_act of each model on each node (ms, e.g.
+ *                       from maestro_activation_latency), or NULL; when given, act_ms and
+ *                       resident_mask are unused (may be NULL)
  *   deg_ms              [n_nodes] float32: disruption penalty C_deg reported by the runtime (ms);
  *                       unused (may be NULL) when plans are given
  *   plans               [n_nodes] maestro_deg_plan from maestro_degradation_plans, or NULL
@@ -264,10 +268,26 @@ MAESTRO_API maestro_status maestro_route_fitness(int64_t n, const int32_t* model
                              const int32_t* class_id, const double* kv_bytes, int32_t n_models,
                              int32_t n_nodes, int32_t n_src, int32_t n_classes,
                              const double* free_bytes, const float* queue_ms, const float* act_ms,
-                             const uint64_t* resident_mask, const float* deg_ms,
+                             const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
                              const maestro_deg_plan* plans, const float* rtt_ms,
                              const float* class_weights, const float* bounds, double rho, int32_t k,
                              int32_t* node_idx, float* fitness, void* stream);
+
+/* Model readiness (Sec. III-C): T_act of every model on every node from the readiness tier of
+ * the node's copy of it -- 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote
+ * (values past 4 count as Remote) -- with the profiled bandwidth model T_act = Size / BW_tier:
+ *   act_ms[j][m] = tier == 0 ? 0 : fl32(tier_setup_ms[t] + (model_bytes[m] / tier_bw[t]) * 1000)
+ * (float64 in that order).
+ *   tier           [n_nodes][n_models] uint8
+ *   model_bytes    [n_models] float64: weight bytes of each model
+ *   tier_bw        [5] float64: bytes/s each tier loads at (entry 0 unused), > 0
+ *   tier_setup_ms  [5] float32: fixed activation overhead of each tier (entry 0 unused)
+ *   act_ms (out)   [n_nodes][n_models] float32, ready for maestro_route_fitness's act_matrix
+ * Device arrays; 1 <= n_models <= 64, n_nodes >= 0 (0: no-op). Errors: INVALID_ARG for a NULL or
+ * misaligned array or a size out of range. */
+MAESTRO_API maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
+                             const double* model_bytes, const double* tier_bw,
+                             const float* tier_setup_ms, float* act_ms, void* stream);
 
 /* Window bounds of the robust normalisation in Eq. 5 (per-metric 5th/95th percentiles of a
  * recent window): out[0] and out[1] (device, float32) receive the values of rank

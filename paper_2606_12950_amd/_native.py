@@ -22,7 +22,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 
 # Every function declared in include/maestro.h.
 EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
-           "maestro_degradation_plans", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
+           "maestro_degradation_plans", "maestro_activation_latency", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
@@ -69,8 +69,9 @@ def load():
                                               P, P, P, i32, P, P, P, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
-    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
+    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P,
                                           f64, i32, P, P, P]
+    lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, P, P]
     lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
@@ -265,6 +266,7 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
                   act_ms: torch.Tensor, resident_mask: torch.Tensor, deg_ms: Optional[torch.Tensor],
                   rtt_ms: torch.Tensor, class_weights: torch.Tensor, bounds: torch.Tensor,
                   n_models: int, k: int = 1, rho: float = 0.0, plans: Optional[torch.Tensor] = None,
+                  act_matrix: Optional[torch.Tensor] = None,
                   out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """maestro_route_fitness: returns (node_idx int32 [N][k], fitness float32 [N][k]).
@@ -272,7 +274,9 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     ``rtt_ms`` is [n_src][n_nodes], ``class_weights`` [n_classes][3] = (gamma, lambda, mu),
     ``bounds`` [6] = (lo, hi) of RTT, T_ready, C_deg; ``resident_mask`` is int64 on the torch
     side (same bits as the C-ABI's uint64). With ``plans`` (from :func:`degradation_plans`)
-    C_deg comes from the node's degradation plan and ``deg_ms`` may be None."""
+    C_deg comes from the node's degradation plan and ``deg_ms`` may be None. With ``act_matrix``
+    [n_nodes][n_models] (from :func:`activation_latency`) T_act comes from it and ``act_ms`` /
+    ``resident_mask`` may be None."""
     lib = load()
     _dev(model_id, "model_id", torch.int32)
     n = model_id.shape[0]
@@ -280,15 +284,23 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     _dev(class_id, "class_id", torch.int32)
     _dev(kv_bytes, "kv_bytes", torch.float64)
     _dev(free_bytes, "free_bytes", torch.float64)
-    for t, name in ((queue_ms, "queue_ms"), (act_ms, "act_ms"), (rtt_ms, "rtt_ms"),
-                    (class_weights, "class_weights"), (bounds, "bounds")):
+    for t, name in ((queue_ms, "queue_ms"), (rtt_ms, "rtt_ms"), (class_weights, "class_weights"),
+                    (bounds, "bounds")):
         _dev(t, name, torch.float32)
-    _dev(resident_mask, "resident_mask", torch.int64)
     M = free_bytes.shape[0]
     if src_id.shape[0] != n or class_id.shape[0] != n or kv_bytes.shape[0] != n:
         raise ValueError("per-stage inputs must have the same length")
-    if queue_ms.shape[0] != M or act_ms.shape[0] != M or resident_mask.shape[0] != M:
+    if queue_ms.shape[0] != M:
         raise ValueError("per-node inputs must have the same length")
+    if act_matrix is not None:
+        _dev(act_matrix, "act_matrix", torch.float32)
+        if tuple(act_matrix.shape) != (M, n_models):
+            raise ValueError("act_matrix must be [n_nodes][n_models]")
+    else:
+        _dev(act_ms, "act_ms", torch.float32)
+        _dev(resident_mask, "resident_mask", torch.int64)
+        if act_ms.shape[0] != M or resident_mask.shape[0] != M:
+            raise ValueError("per-node inputs must have the same length")
     if plans is not None:
         _dev(plans, "plans", torch.uint8)
         if tuple(plans.shape) != (M, PLAN_BYTES):
@@ -312,6 +324,7 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     st = lib.maestro_route_fitness(n, _ptr(model_id), _ptr(src_id), _ptr(class_id), _ptr(kv_bytes),
                                    int(n_models), M, rtt_ms.shape[0], class_weights.shape[0],
                                    _ptr(free_bytes), _ptr(queue_ms), _ptr(act_ms), _ptr(resident_mask),
+                                   _ptr(act_matrix),
                                    _ptr(deg_ms) if deg_ms is not None else None,
                                    _ptr(plans) if plans is not None else None,
                                    _ptr(rtt_ms), _ptr(class_weights), _ptr(bounds),
@@ -347,6 +360,28 @@ def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, e
                                        _ptr(engine_cost_ms) if E else None, float(c_int_ms), _ptr(out),
                                        _stream(stream))
     _check("maestro_degradation_plans", st)
+    return out
+
+
+def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: torch.Tensor,
+                       tier_setup_ms: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """maestro_activation_latency: T_act [n_nodes][n_models] float32 (ms) from the readiness tier
+    [n_nodes][n_models] uint8 (0 Running .. 4 Remote), model sizes [n_models] float64 (bytes),
+    tier bandwidths [5] float64 (bytes/s) and setup times [5] float32 (ms)."""
+    lib = load()
+    _dev(tier, "tier", torch.uint8)
+    _dev(model_bytes, "model_bytes", torch.float64)
+    _dev(tier_bw, "tier_bw", torch.float64)
+    _dev(tier_setup_ms, "tier_setup_ms", torch.float32)
+    if tier.dim() != 2 or model_bytes.shape != (tier.shape[1],) or tier_bw.shape != (5,) or tier_setup_ms.shape != (5,):
+        raise ValueError("tier [n_nodes][n_models], model_bytes [n_models], tier_bw and tier_setup_ms [5]")
+    M, K = tier.shape
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.float32, device=tier.device)
+    _dev(out, "act_ms", torch.float32)
+    st = lib.maestro_activation_latency(M, K, _ptr(tier) if M else None, _ptr(model_bytes), _ptr(tier_bw),
+                                        _ptr(tier_setup_ms), _ptr(out) if M else None, _stream(stream))
+    _check("maestro_activation_latency", st)
     return out
 
 

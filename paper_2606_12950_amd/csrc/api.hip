@@ -150,8 +150,8 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
                                      int32_t n_models, int32_t n_nodes, int32_t n_src,
                                      int32_t n_classes, const double* free_bytes,
                                      const float* queue_ms, const float* act_ms,
-                                     const uint64_t* resident_mask, const float* deg_ms,
-                                     const maestro_deg_plan* plans, const float* rtt_ms,
+                                     const uint64_t* resident_mask, const float* act_matrix,
+                                     const float* deg_ms, const maestro_deg_plan* plans, const float* rtt_ms,
                                      const float* class_weights,
                                      const float* bounds, double rho, int32_t k, int32_t* node_idx,
                                      float* fitness, void* stream) {
@@ -161,11 +161,12 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
       n_classes > maestro::kMaxFitnessClasses)
     return MAESTRO_ERR_INVALID_ARG;
   if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
-  if (!free_bytes || !queue_ms || !act_ms || !resident_mask || !rtt_ms || !class_weights || !bounds)
-    return MAESTRO_ERR_INVALID_ARG;
-  if (!aligned(free_bytes, 8) || !aligned(queue_ms, 4) || !aligned(act_ms, 4) ||
-      !aligned(resident_mask, 8) || !aligned(rtt_ms, 4) || !aligned(class_weights, 4) ||
+  if (!free_bytes || !queue_ms || !rtt_ms || !class_weights || !bounds) return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(free_bytes, 8) || !aligned(queue_ms, 4) || !aligned(rtt_ms, 4) || !aligned(class_weights, 4) ||
       !aligned(bounds, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (act_matrix ? !aligned(act_matrix, 4)
+                 : (!act_ms || !resident_mask || !aligned(act_ms, 4) || !aligned(resident_mask, 8)))
     return MAESTRO_ERR_INVALID_ARG;
   if (plans ? !aligned(plans, 16) : (!deg_ms || !aligned(deg_ms, 4))) return MAESTRO_ERR_INVALID_ARG;
   if (n > 0) {
@@ -177,8 +178,8 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
   }
   if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
   return maestro::launch_route_fitness(n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src,
-                                       free_bytes, queue_ms, act_ms, resident_mask, deg_ms, plans,
-                                       rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,
+                                       free_bytes, queue_ms, act_ms, resident_mask, act_matrix, deg_ms,
+                                       plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,
                                        as_stream(stream));
 }
 
@@ -195,6 +196,18 @@ maestro_status maestro_degradation_plans(int32_t n_nodes, const int32_t* engine_
     return MAESTRO_ERR_INVALID_ARG;
   return maestro::launch_degradation_plans(n_nodes, engine_offset, engine_level, engine_freed_bytes,
                                            engine_cost_ms, c_int_ms, plans, as_stream(stream));
+}
+
+maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
+                                          const double* model_bytes, const double* tier_bw,
+                                          const float* tier_setup_ms, float* act_ms, void* stream) {
+  if (n_nodes < 0 || n_models < 1 || n_models > 64) return MAESTRO_ERR_INVALID_ARG;
+  if (!model_bytes || !tier_bw || !tier_setup_ms || !aligned(model_bytes, 8) || !aligned(tier_bw, 8) ||
+      !aligned(tier_setup_ms, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n_nodes > 0 && (!tier || !act_ms || !aligned(act_ms, 4))) return MAESTRO_ERR_INVALID_ARG;
+  return maestro::launch_activation_latency(n_nodes, n_models, tier, model_bytes, tier_bw, tier_setup_ms, act_ms,
+                                            as_stream(stream));
 }
 
 maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi, float* out,

@@ -104,13 +104,18 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const i
   plans[j] = out;
 }
 
-template <int KT, bool kMask64, bool kPlans>
+// How T_act(N, M(T)) of Eq. 6 reaches the kernel: a node's activation latency unless the
+// stage's model is resident (residency bits in 32 or 64 bits), or a [node][model] matrix.
+enum Ready { kMask32 = 0, kMask64 = 1, kMatrix = 2 };
+constexpr int kMaxMatrixModels = 64;
+
+template <int KT, int kReady, bool kPlans>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
-    const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_nodes,
+    const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_models, int32_t n_nodes,
     int32_t n_src, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
     const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
-    const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
+    const float* __restrict__ act_matrix, const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
     const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
     int32_t* __restrict__ node_idx, float* __restrict__ fitness) {
   // per node, two 16-byte records (one LDS read each, the same address for every lane):
@@ -118,11 +123,13 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   //          norm(T_q + T_act), norm(C_deg)
   //   admit: KV admission headroom and the residency bits (the low 32 when no model id
   //          exceeds 31)
-  // and with plans the node's plan record (norm(C_deg) then depends on the stage).
-  typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
+  // and with plans the node's plan record (norm(C_deg) then depends on the stage). With a
+  // T_act matrix, terms.y holds T_q itself and the node's row of the matrix is staged too.
+  typedef typename std::conditional<kReady == kMask64, uint64_t, uint32_t>::type mask_t;
+  constexpr bool kMat = kReady == kMatrix;
   // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
   // workgroups per CU, whose waves hide each other's LDS latency
-  constexpr int kChunk = kPlans ? 128 : 256;
+  constexpr int kChunk = kMat ? 64 : (kPlans ? 128 : 256);
   constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
   struct Admit { double free; uint64_t mask; };
   __shared__ float4 s_terms[kChunk];
@@ -135,6 +142,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   constexpr int kQueue = kPlans ? 16 : 1;        // short nodes a lane queues per chunk
   static_assert(kChunk <= 256 || !kPlans, "queued node offsets are bytes");
   __shared__ uint8_t s_queue[kQueue * kThreads];
+  __shared__ float s_act[kMat ? kChunk * kMaxMatrixModels : 1];   // [node][model], row stride n_models
 
   const int tid = threadIdx.x;
   const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
@@ -148,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   double need = INFINITY;   // an invalid lane admits nothing
   float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
   mask_t mbit = 0;
-  int src = 0;
+  int src = 0, model = 0;
   if (valid) {
     need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
     needf = __double2float_rn(need);
@@ -157,7 +165,8 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     lambda = wt[1];
     mu = wt[2];
     omg = __fsub_rn(1.0f, gamma);
-    mbit = (mask_t)1 << model_id[stage];
+    model = model_id[stage];
+    mbit = kMat ? 0 : (mask_t)1 << model;
     src = src_id[stage];
   }
   const float* prox_row = s_prox + src * kProxStride;
@@ -173,10 +182,10 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       const float frf = __double2float_rn(fr);
       const float q = queue_ms[j];
       s_terms[i] = make_float4(frf > 0.0f ? __fdiv_rn(1.0f, frf) : INFINITY,
-                               norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
-                               norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
+                               kMat ? q : norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
+                               kMat ? 0.0f : norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
                                kPlans ? nd_fits : norm01(deg_ms[j], lo_d, inv_d));
-      s_admit[i] = Admit{fr, resident_mask[j]};
+      s_admit[i] = Admit{fr, kMat ? 0ull : resident_mask[j]};
       if (kPlans) {
         const maestro_deg_plan& pl = plans[j];
 #pragma unroll
@@ -187,6 +196,10 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         s_pn[i] = pl.n_engines;
       }
     }
+    if (kMat) {   // rows c0 .. c0+cn-1 of the matrix are contiguous
+      const float* src_rows = act_matrix + (size_t)c0 * n_models;
+      for (int e = tid; e < cn * n_models; e += kThreads) s_act[e] = src_rows[e];
+    }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
       s_prox[r * kProxStride + i] =
@@ -195,13 +208,15 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     __syncthreads();
     // every node is scored; an infeasible one offers the key +inf, which never enters the list
     // (FilterByPolicyAndFeasibility)
-    auto score = [&](const float4 t, const Admit ad, float prox, float nd) {
+    auto score = [&](int i, const float4 t, const Admit ad, float prox, float nd) {
       // fit = min(1, fl32(need) / fl32(headroom)); with zero headroom only need = 0 is
       // feasible, and min(0 * inf = NaN, 1) = 1 (IEEE min returns the number), the fit of a
       // stage that fills the node exactly
       const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
       const float a = __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
-      const float nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
+      float nr;
+      if constexpr (kMat) nr = norm01(__fadd_rn(t.y, s_act[i * n_models + model]), lo_t, inv_t);
+      else nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
       return __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
     };
     // A stage that falls short of node i's headroom by R takes the first prefix of the node's
@@ -217,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 #pragma unroll
       for (int e = 0; e < kMaxPlan; ++e) jp += s_pfreed[e][i] < R ? 1 : 0;
       if (jp < s_pn[i])
-        best.push_lex(-score(t, ad, prox_row[i], norm01(s_pcost[jp][i], lo_d, inv_d)), c0 + i);
+        best.push_lex(-score(i, t, ad, prox_row[i], norm01(s_pcost[jp][i], lo_d, inv_d)), c0 + i);
     };
     int n_short = 0;   // queued nodes of this chunk
     auto queue = [&](int i) {
@@ -242,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           fits[u] = need <= ad[u].free;
-          const float sc = score(t[u], ad[u], px[u], t[u].w);
+          const float sc = score(i + u, t[u], ad[u], px[u], t[u].w);
           best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u);
         }
         if (valid && !(fits[0] && fits[1] && fits[2] && fits[3])) {
@@ -255,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         const float4 t = s_terms[i];
         const Admit ad = s_admit[i];
         const bool fits = need <= ad.free;
-        const float sc = score(t, ad, prox_row[i], t.w);
+        const float sc = score(i, t, ad, prox_row[i], t.w);
         best.push_increasing(fits ? -sc : INFINITY, c0 + i);
         if (valid && !fits) queue(i);
       }
@@ -264,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       for (int i = 0; i < cn; ++i) {
         const float4 t = s_terms[i];
         const Admit ad = s_admit[i];
-        const float sc = score(t, ad, prox_row[i], t.w);
+        const float sc = score(i, t, ad, prox_row[i], t.w);
         best.push_increasing(need <= ad.free ? -sc : INFINITY, c0 + i);
       }
     }
@@ -359,26 +374,29 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     const int32_t* class_id, const double* kv_bytes, int32_t n_models,
                                     int32_t n_nodes, int32_t n_src, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
-                                    const uint64_t* resident_mask, const float* deg_ms,
+                                    const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
                                     const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,
                                     const float* bounds, double rho, int32_t k, int32_t* node_idx,
                                     float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
-  const bool mask64 = n_models > 32;
+  const int ready = act_matrix ? kMatrix : (n_models > 32 ? kMask64 : kMask32);
   const bool with_plans = plans != nullptr;
-#define MAESTRO_FIT_LAUNCH(KT, M64, PL)                                                                  \
-  fitness_kernel<KT, M64, PL><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes,      \
-                                                          n_nodes, n_src, free_bytes, queue_ms, act_ms, \
-                                                          resident_mask, deg_ms, plans, rtt_ms,         \
-                                                          class_weights, bounds, rho, k, node_idx, fitness)
-#define MAESTRO_FIT_KT(KT)                                                                        \
-  do {                                                                                            \
-    if (with_plans) {                                                                             \
-      if (mask64) MAESTRO_FIT_LAUNCH(KT, true, true); else MAESTRO_FIT_LAUNCH(KT, false, true);   \
-    } else {                                                                                      \
-      if (mask64) MAESTRO_FIT_LAUNCH(KT, true, false); else MAESTRO_FIT_LAUNCH(KT, false, false); \
-    }                                                                                             \
+#define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                   \
+  fitness_kernel<KT, RD, PL><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes, n_models, \
+                                                         n_nodes, n_src, free_bytes, queue_ms, act_ms,    \
+                                                         resident_mask, act_matrix, deg_ms, plans, rtt_ms, \
+                                                         class_weights, bounds, rho, k, node_idx, fitness)
+#define MAESTRO_FIT_RD(KT, PL)                                       \
+  do {                                                               \
+    if (ready == kMatrix) MAESTRO_FIT_LAUNCH(KT, kMatrix, PL);       \
+    else if (ready == kMask64) MAESTRO_FIT_LAUNCH(KT, kMask64, PL);  \
+    else MAESTRO_FIT_LAUNCH(KT, kMask32, PL);                        \
+  } while (0)
+#define MAESTRO_FIT_KT(KT)                        \
+  do {                                            \
+    if (with_plans) MAESTRO_FIT_RD(KT, true);     \
+    else MAESTRO_FIT_RD(KT, false);               \
   } while (0)
   if (k == 1) MAESTRO_FIT_KT(1);
   else if (k == 2) MAESTRO_FIT_KT(2);
@@ -386,7 +404,39 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
   else if (k <= 8) MAESTRO_FIT_KT(8);
   else MAESTRO_FIT_KT(16);
 #undef MAESTRO_FIT_KT
+#undef MAESTRO_FIT_RD
 #undef MAESTRO_FIT_LAUNCH
+  return launch_status();
+}
+
+// T_act of every (node, model) from its readiness tier (Sec. III-C): 0 when Running, else the
+// tier's setup time plus Size / BW_tier, in float64 in that order, stored as float32.
+__global__ __launch_bounds__(kThreads) void activation_kernel(int64_t total, int32_t n_models,
+                                                              const uint8_t* __restrict__ tier,
+                                                              const double* __restrict__ model_bytes,
+                                                              const double* __restrict__ tier_bw,
+                                                              const float* __restrict__ tier_setup_ms,
+                                                              float* __restrict__ act_ms) {
+  for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (int64_t)gridDim.x * kThreads) {
+    int t = tier[e];
+    t = t > 4 ? 4 : t;   // past Remote counts as Remote
+    const int32_t m = (int32_t)(e % n_models);
+    float a = 0.0f;
+    if (t > 0)
+      a = __double2float_rn(__dadd_rn((double)tier_setup_ms[t],
+                                      __dmul_rn(__ddiv_rn(model_bytes[m], tier_bw[t]), 1000.0)));
+    act_ms[e] = a;
+  }
+}
+
+maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
+                                         const double* model_bytes, const double* tier_bw,
+                                         const float* tier_setup_ms, float* act_ms, hipStream_t stream) {
+  const int64_t total = (int64_t)n_nodes * n_models;
+  if (total == 0) return MAESTRO_OK;
+  const int64_t blocks = (total + kThreads - 1) / kThreads;
+  activation_kernel<<<dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(kThreads), 0, stream>>>(
+      total, n_models, tier, model_bytes, tier_bw, tier_setup_ms, act_ms);
   return launch_status();
 }
 

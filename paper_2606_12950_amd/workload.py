@@ -440,6 +440,39 @@ def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
                         cost_ms=cost.astype(np.float32), c_int_ms=C_INT_MS, deg_window=deg_window)
 
 
+READINESS_STREAMS = ("tier", "size")
+# readiness tiers (Sec. III-C): 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote
+TIER_P = (0.3, 0.3, 0.3, 0.1)               # tiers 1..4 of a model that is not running on a node
+TIER_BW = (1.0, 25e9, 25e9, 3e9, 1.25e9)    # bytes/s: host link, host link, NVMe, network
+TIER_SETUP_MS = (0.0, 150.0, 2500.0, 2500.0, 4000.0)
+
+
+@dataclass
+class ReadinessInputs:
+    """Per-(node, model) readiness tier and the profiled bandwidth model T_act = Size / BW_tier."""
+    tier: np.ndarray              # [M][K] uint8
+    model_bytes: np.ndarray       # [K] float64
+    tier_bw: np.ndarray           # [5] float64
+    tier_setup_ms: np.ndarray     # [5] float32
+
+
+def readiness_inputs(wl: Workload) -> ReadinessInputs:
+    """Readiness tiers for ``wl`` (seeded by its spec's seed): a model resident on a node (the
+    workload's residency bits) is Running there; otherwise Sleeping, CPU-resident, Disk-resident
+    or Remote with probabilities TIER_P. Model sizes are bf16 weights of 0.6B-14B parameters
+    (1.2-28 GB). Tiers load over a 25 GB/s host link (Sleeping keeps its runtime context: 150 ms
+    setup; CPU-resident rebuilds it: 2.5 s), 3 GB/s NVMe (2.5 s) and a 1.25 GB/s network (4 s)."""
+    children = np.random.SeedSequence([wl.spec.seed, 0x7E1]).spawn(len(READINESS_STREAMS))
+    r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(READINESS_STREAMS, children)}
+    M, K = wl.free_bytes.shape[0], wl.spec.n_models
+    bits = (wl.resident_mask[:, None] >> np.arange(K, dtype=np.uint64)[None, :]) & np.uint64(1)
+    cold = (r["tier"].choice(4, size=(M, K), p=TIER_P) + 1).astype(np.uint8)
+    tier = np.where(bits == 1, 0, cold).astype(np.uint8)
+    size = r["size"].uniform(0.6e9, 14e9, K) * 2.0
+    return ReadinessInputs(tier=tier, model_bytes=size, tier_bw=np.array(TIER_BW, np.float64),
+                           tier_setup_ms=np.array(TIER_SETUP_MS, np.float32))
+
+
 TWO_PHASE_STREAMS = ("head", "head_bias", "coef", "iso", "tools")
 
 

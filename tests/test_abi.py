@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -142,10 +142,10 @@ def test_route_validation(lib):
 
 def test_route_fitness_and_quantiles_validation(lib):
     def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE,
-             deg=FAKE, plans=None):
+             deg=FAKE, plans=None, act=FAKE, mask=FAKE, mat=None):
         return lib.maestro_route_fitness(n, FAKE, src, FAKE, FAKE, n_models, n_nodes, n_src, n_classes,
-                                         FAKE, FAKE, FAKE, FAKE, deg, plans, rtt, FAKE, bounds, rho, k, FAKE, FAKE,
-                                         None)
+                                         FAKE, FAKE, act, mask, mat, deg, plans, rtt, FAKE, bounds, rho, k, FAKE,
+                                         FAKE, None)
     assert call(n=-1) == INVALID
     assert call(n_models=0) == INVALID
     assert call(n_models=65) == INVALID
@@ -163,6 +163,10 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert call(deg=None, plans=MISALIGNED16) == INVALID                      # plan records are 16-aligned
     assert call(deg=None, plans=FAKE16, rtt=None) == INVALID
     assert call(n=0, deg=None, plans=FAKE16) == OK                            # plans replace deg_ms
+    assert call(act=None) == INVALID                                          # T_act from nowhere
+    assert call(mask=MISALIGNED) == INVALID
+    assert call(act=None, mask=None, mat=MISALIGNED4) == INVALID
+    assert call(n=0, act=None, mask=None, mat=FAKE) == OK                     # a T_act matrix replaces both
     q = lambda m=10, lo=0.05, hi=0.95, v=FAKE, out=FAKE: lib.maestro_quantiles(v, m, lo, hi, out, None)
     assert q(m=0) == INVALID
     assert q(lo=0.6, hi=0.5) == INVALID
@@ -172,6 +176,19 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert q(v=None) == INVALID
     assert q(out=MISALIGNED4) == INVALID
     assert q(m=1 << 32) == UNSUPPORTED
+
+
+def test_activation_latency_validation(lib):
+    def call(M=4, K=3, tier=FAKE, size=FAKE, bw=FAKE, setup=FAKE, out=FAKE):
+        return lib.maestro_activation_latency(M, K, tier, size, bw, setup, out, None)
+    assert call(M=-1) == INVALID
+    assert call(K=0) == INVALID
+    assert call(K=65) == INVALID
+    assert call(tier=None) == INVALID
+    assert call(size=MISALIGNED) == INVALID
+    assert call(bw=None) == INVALID
+    assert call(out=MISALIGNED4) == INVALID
+    assert call(M=0, tier=None, out=None) == OK                               # no nodes: no-op
 
 
 def test_degradation_plans_validation(lib):

@@ -302,3 +302,122 @@ def test_fitness_with_plans_workload_full(name):
     assert_same(got, ref)
     print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes with plans, "
           f"{(got[0][:, 0] >= 0).mean():.4f} routed, fitness identical")
+
+
+# ---- model readiness tiers (Sec. III-C) as T_act(N, M(T)) of Eq. 6 -------------------------------
+
+TIER_BW = np.array([1.0, 25e9, 25e9, 3e9, 1.25e9])
+TIER_SETUP = np.array([0.0, 150.0, 2500.0, 2500.0, 4000.0], np.float32)
+
+
+def gpu_activation(tier, size, bw=TIER_BW, setup=TIER_SETUP):
+    out = M.activation_latency(_t(tier.astype(np.uint8)), _t(size.astype(np.float64)), _t(bw.astype(np.float64)),
+                               _t(setup.astype(np.float32)))
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def test_activation_latency_matches_oracle():
+    rng = np.random.default_rng(17)
+    for Mn, K in [(1, 1), (513, 16), (3000, 64), (0, 5)]:
+        tier = rng.integers(0, 9, (Mn, K)).astype(np.uint8)      # values past 4 count as Remote
+        size = rng.uniform(0.5, 30, K) * GB
+        size[0] = 0.0
+        got = gpu_activation(tier, size)
+        ref = oracle.activation_latency(tier, size, TIER_BW, TIER_SETUP)
+        assert got.shape == (Mn, K) and np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def gpu_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=1, rho=0.0, eng=None):
+    plans = None
+    if eng is not None:
+        off, level, freed, cost, c_int = eng
+        plans = M.degradation_plans(_t(off), _t(level), _t(freed), _t(cost), c_int)
+    idx, fit = M.route_fitness(_t(model.astype(np.int32)), _t(src.astype(np.int32)), _t(cls.astype(np.int32)),
+                               _t(kv.astype(np.float64)), _t(nodes["free_bytes"]), _t(nodes["queue_ms"]), None, None,
+                               None if eng is not None else _t(nodes["deg_ms"]), _t(nodes["rtt_ms"]),
+                               _t(np.asarray(weights, np.float32).reshape(-1, 3)), _t(np.asarray(bounds, np.float32)),
+                               n_models=n_models, k=k, rho=rho, plans=plans, act_matrix=_t(act))
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), fit.cpu().numpy()
+
+
+def oracle_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=1, rho=0.0, eng=None):
+    return oracle.route_fitness(model, src, cls, kv, nodes["free_bytes"], nodes["queue_ms"], nodes["act_ms"],
+                                nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"],
+                                np.asarray(weights, np.float32).reshape(-1, 3), np.asarray(bounds, np.float32), k=k,
+                                rho=rho, n_models=n_models, engines=eng, act_matrix=act)
+
+
+@pytest.mark.parametrize("n,M_,n_src,k,n_models,plans", [(1, 1, 1, 1, 1, False), (300, 65, 2, 1, 16, False),
+                                                         (1000, 700, 5, 3, 64, False), (777, 129, 16, 16, 33, True),
+                                                         (2000, 1300, 3, 4, 64, True)])
+def test_fitness_with_act_matrix_matches_oracle(n, M_, n_src, k, n_models, plans):
+    # several 64-node chunks with ragged tails, up to 64 models, with and without plans
+    rng = np.random.default_rng(n + 31 * M_)
+    nodes = _nodes(rng, M_, n_src)
+    if plans:
+        nodes["free_bytes"] = rng.uniform(0, 60, M_) * GB
+    tier = rng.integers(0, 5, (M_, n_models)).astype(np.uint8)
+    act = oracle.activation_latency(tier, rng.uniform(1, 28, n_models) * GB, TIER_BW, TIER_SETUP)
+    eng = None
+    if plans:
+        off, level, freed, cost = _engines(rng, M_)
+        eng = (off, level, freed, cost, 2000.0)
+    model = rng.integers(0, n_models, n).astype(np.int32)
+    src = rng.integers(0, n_src, n).astype(np.int32)
+    cls = rng.integers(0, 3, n).astype(np.int32)
+    kv = rng.uniform(0, 120 if plans else 250, n) * GB
+    weights = [[0.25, 1, 1], [0.1, 1, 1], [1.0, 1.0, 0.0]]
+    bounds = [*oracle.quantiles(nodes["rtt_ms"].ravel()), *oracle.quantiles((nodes["queue_ms"][:, None] + act).ravel()),
+              0.0, 12000.0]
+    for rho in (0.0, 0.2):
+        got = gpu_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=k, rho=rho, eng=eng)
+        assert_same(got, oracle_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=k, rho=rho,
+                                            eng=eng))
+
+
+def test_fitness_act_matrix_of_resident_bits_equals_mask_form():
+    # the matrix {0 where resident, act_ms otherwise} routes exactly like the residency bits
+    rng = np.random.default_rng(29)
+    M_, n = 900, 3000
+    nodes = _nodes(rng, M_, 4)
+    bits = (nodes["resident_mask"][:, None] >> np.arange(16, dtype=np.uint64)[None, :]) & np.uint64(1)
+    act = np.where(bits == 1, 0.0, nodes["act_ms"][:, None]).astype(np.float32)
+    model = rng.integers(0, 16, n).astype(np.int32)
+    src = rng.integers(0, 4, n).astype(np.int32)
+    cls = rng.integers(0, 2, n).astype(np.int32)
+    kv = rng.uniform(0, 250, n) * GB
+    w, b = [[0.25, 1, 1], [0.1, 1, 1]], [0, 80, 0, 25000, 0, 500]
+    got = gpu_fitness_act(model, src, cls, kv, nodes, w, b, act, 16, k=4)
+    ref = gpu_fitness(model, src, cls, kv, nodes, w, b, k=4, n_models=16)
+    assert_same(got, ref)
+
+
+@pytest.mark.parametrize("name", ["c1", "c3"])
+def test_fitness_with_readiness_and_plans_workload_full(name):
+    # readiness tiers on the GPU, then fitness with T_act from them and C_deg from plans
+    w = W.workload(name)
+    f = W.fitness_inputs(w)
+    e = W.engine_inputs(w)
+    r = W.readiness_inputs(w)
+    b = pipeline.to_device(w)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    torch.cuda.synchronize()
+    kv = o.kv_bytes.cpu().numpy()
+    act = gpu_activation(r.tier, r.model_bytes, r.tier_bw, r.tier_setup_ms)
+    assert np.array_equal(act.view(np.uint32),
+                          oracle.activation_latency(r.tier, r.model_bytes, r.tier_bw, r.tier_setup_ms).view(np.uint32))
+    nodes = dict(free_bytes=w.free_bytes, queue_ms=f.queue_ms, act_ms=f.act_ms, resident_mask=w.resident_mask,
+                 deg_ms=f.deg_ms, rtt_ms=f.rtt_ms)
+    bounds = np.concatenate([oracle.quantiles(f.rtt_window), oracle.quantiles(f.ready_window),
+                             oracle.quantiles(e.deg_window)])
+    eng = (e.engine_offset, e.level, e.freed_bytes, e.cost_ms, e.c_int_ms)
+    K = w.spec.n_models
+    got = gpu_fitness_act(w.model_id, f.src_id, f.class_id, kv, nodes, f.class_weights, bounds, act, K, k=w.spec.k,
+                          rho=w.spec.rho, eng=eng)
+    ref = oracle_fitness_act(w.model_id, f.src_id, f.class_id, kv, nodes, f.class_weights, bounds, act, K,
+                             k=w.spec.k, rho=w.spec.rho, eng=eng)
+    assert_same(got, ref)
+    print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes, readiness tiers + plans, fitness identical")
