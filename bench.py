@@ -5,6 +5,7 @@ python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for 
 python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
 python bench.py --route-fitness        (routing by fitness, Eq. 5, on the workload's predictions)
 python bench.py --route-fitness --plans   (the same with C_deg from degradation plans, Alg. 2)
+python bench.py --route-fitness --readiness  (T_act per (node, model) from readiness tiers, Sec. III-C)
 python bench.py --two-phase            (the two-phase predictor, Sec. III-B, beside the bins one)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
@@ -186,7 +187,7 @@ def _time_events(call, steps: int, warmup: int):
     return [e0.elapsed_time(e1) for e0, e1 in ev]
 
 
-def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False):
+def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False, readiness: bool = False):
     """Routing by fitness over the workload's stages, on the GPU's own predictions; bounds from
     the recent-observation windows (maestro_quantiles). With ``plans`` C_deg comes from the
     nodes' degradation plans (built once, timed on their own). One JSON line."""
@@ -213,15 +214,23 @@ def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False)
         extra = {"plans": True, "n_engines": int(e.level.shape[0]), "plan_ms": percentiles(dp)}
     else:
         deg_window = f.deg_window
+    act = None
+    if readiness:
+        r = W.readiness_inputs(wl)
+        rin = [t(r.tier), t(r.model_bytes), t(r.tier_bw), t(r.tier_setup_ms)]
+        act = _native.activation_latency(*rin)
+        da = _time_events(lambda: _native.activation_latency(*rin, out=act), steps, warmup)
+        extra.update({"readiness": True, "activation_ms": percentiles(da)})
     bounds = torch.cat([_native.quantiles(t(f.rtt_window)), _native.quantiles(t(f.ready_window)),
                         _native.quantiles(t(deg_window))])
     n, m = wl.n, wl.spec.n_nodes
     out = (torch.empty((n, wl.spec.k), dtype=torch.int32, device="cuda"),
            torch.empty((n, wl.spec.k), dtype=torch.float32, device="cuda"))
     call = lambda: _native.route_fitness(b.model_id, fd["src"], fd["cls"], o.kv_bytes, b.free_bytes, fd["queue"],
-                                         fd["act"], b.resident_mask, None if plans else fd["deg"], fd["rtt"],
-                                         fd["weights"], bounds, n_models=wl.spec.n_models, k=wl.spec.k,
-                                         rho=wl.spec.rho, plans=plan_t, out=out)
+                                         None if readiness else fd["act"], None if readiness else b.resident_mask,
+                                         None if plans else fd["deg"], fd["rtt"], fd["weights"], bounds,
+                                         n_models=wl.spec.n_models, k=wl.spec.k, rho=wl.spec.rho, plans=plan_t,
+                                         act_matrix=act, out=out)
     d = _time_events(call, steps, warmup)
     ms = float(np.mean(d))
     if plans:
@@ -294,6 +303,8 @@ def main():
                     help="time routing by fitness (Eq. 5) on the workload's predictions")
     ap.add_argument("--plans", action="store_true",
                     help="with --route-fitness: C_deg from degradation plans (Alg. 2, Eq. 4)")
+    ap.add_argument("--readiness", action="store_true",
+                    help="with --route-fitness: T_act per (node, model) from readiness tiers (Sec. III-C)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
     args = ap.parse_args()
@@ -306,7 +317,7 @@ def main():
         return
     if args.route_fitness:
         route_fitness_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)),
-                            plans=args.plans)
+                            plans=args.plans, readiness=args.readiness)
         return
     if args.sweep_prioritize:
         lo, hi = (int(v) for v in args.sweep_prioritize.split(":"))

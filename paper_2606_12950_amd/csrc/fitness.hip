@@ -105,9 +105,9 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const i
 }
 
 // How T_act(N, M(T)) of Eq. 6 reaches the kernel: a node's activation latency unless the
-// stage's model is resident (residency bits in 32 or 64 bits), or a [node][model] matrix.
-enum Ready { kMask32 = 0, kMask64 = 1, kMatrix = 2 };
-constexpr int kMaxMatrixModels = 64;
+// stage's model is resident (residency bits in 32 or 64 bits), or a [node][model] matrix (of at
+// most 16 or 64 models: the chunk of node rows staged in LDS shrinks with the row length).
+enum Ready { kMask32 = 0, kMask64 = 1, kMatrix16 = 2, kMatrix64 = 3 };
 
 template <int KT, int kReady, bool kPlans>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
@@ -126,10 +126,11 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   // and with plans the node's plan record (norm(C_deg) then depends on the stage). With a
   // T_act matrix, terms.y holds T_q itself and the node's row of the matrix is staged too.
   typedef typename std::conditional<kReady == kMask64, uint64_t, uint32_t>::type mask_t;
-  constexpr bool kMat = kReady == kMatrix;
+  constexpr bool kMat = kReady >= kMatrix16;
+  constexpr int kMatRow = kReady == kMatrix16 ? 16 : 64;   // largest row the staging area holds
   // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
   // workgroups per CU, whose waves hide each other's LDS latency
-  constexpr int kChunk = kMat ? 64 : (kPlans ? 128 : 256);
+  constexpr int kChunk = kReady == kMatrix64 ? 64 : (kPlans ? 128 : 256);
   constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
   struct Admit { double free; uint64_t mask; };
   __shared__ float4 s_terms[kChunk];
@@ -142,7 +143,9 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   constexpr int kQueue = kPlans ? 16 : 1;        // short nodes a lane queues per chunk
   static_assert(kChunk <= 256 || !kPlans, "queued node offsets are bytes");
   __shared__ uint8_t s_queue[kQueue * kThreads];
-  __shared__ float s_act[kMat ? kChunk * kMaxMatrixModels : 1];   // [node][model], row stride n_models
+  // with a T_act matrix: normalised T_ready = norm(T_q + T_act) of every (node, model) of the
+  // chunk, [node][model] with row stride n_models
+  __shared__ float s_ready[kMat ? kChunk * kMatRow : 1];
 
   const int tid = threadIdx.x;
   const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
@@ -182,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       const float frf = __double2float_rn(fr);
       const float q = queue_ms[j];
       s_terms[i] = make_float4(frf > 0.0f ? __fdiv_rn(1.0f, frf) : INFINITY,
-                               kMat ? q : norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
+                               kMat ? 0.0f : norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
                                kMat ? 0.0f : norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
                                kPlans ? nd_fits : norm01(deg_ms[j], lo_d, inv_d));
       s_admit[i] = Admit{fr, kMat ? 0ull : resident_mask[j]};
@@ -198,7 +201,8 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     }
     if (kMat) {   // rows c0 .. c0+cn-1 of the matrix are contiguous
       const float* src_rows = act_matrix + (size_t)c0 * n_models;
-      for (int e = tid; e < cn * n_models; e += kThreads) s_act[e] = src_rows[e];
+      for (int e = tid; e < cn * n_models; e += kThreads)
+        s_ready[e] = norm01(__fadd_rn(queue_ms[c0 + e / n_models], src_rows[e]), lo_t, inv_t);
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
@@ -215,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
       const float a = __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
       float nr;
-      if constexpr (kMat) nr = norm01(__fadd_rn(t.y, s_act[i * n_models + model]), lo_t, inv_t);
+      if constexpr (kMat) nr = s_ready[i * n_models + model];
       else nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
       return __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
     };
@@ -380,7 +384,7 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
-  const int ready = act_matrix ? kMatrix : (n_models > 32 ? kMask64 : kMask32);
+  const int ready = act_matrix ? (n_models > 16 ? kMatrix64 : kMatrix16) : (n_models > 32 ? kMask64 : kMask32);
   const bool with_plans = plans != nullptr;
 #define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                   \
   fitness_kernel<KT, RD, PL><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes, n_models, \
@@ -389,7 +393,8 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                                          class_weights, bounds, rho, k, node_idx, fitness)
 #define MAESTRO_FIT_RD(KT, PL)                                       \
   do {                                                               \
-    if (ready == kMatrix) MAESTRO_FIT_LAUNCH(KT, kMatrix, PL);       \
+    if (ready == kMatrix16) MAESTRO_FIT_LAUNCH(KT, kMatrix16, PL);   \
+    else if (ready == kMatrix64) MAESTRO_FIT_LAUNCH(KT, kMatrix64, PL); \
     else if (ready == kMask64) MAESTRO_FIT_LAUNCH(KT, kMask64, PL);  \
     else MAESTRO_FIT_LAUNCH(KT, kMask32, PL);                        \
   } while (0)
