@@ -29,6 +29,9 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
                leaves the setup, doubling a bandwidth halves the transfer exactly, tiers past
                Remote count as Remote; fitness routing with a matrix of {0, act} equals the
                resident-mask form.
+  adaptive_rho - pinned (tests/test_oracle_readiness_pins.py): beta = 1 leaves e itself, exact
+               predictions give 0, a constant error gives that constant, the recursion's closed
+               form on geometric inputs, numpy's "higher" percentile of the EWMA values.
   quantiles  - pinned: numpy's percentile selection ("lower" / "higher" methods).
   prioritize - pinned: closed forms (unit latencies), numpy stable argsort, O(len^2) suffix
                sums, half-even rounding cases, int32 clamping, non-finite latency handling.
@@ -79,6 +82,8 @@ def _load():
     lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
                                          f64, i32, P, P, P, P, ctypes.c_float, P, P, i32]
     lib.oracle_activation_latency.argtypes = [i32, i32, P, P, P, P, P]
+    lib.oracle_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P]
+    lib.oracle_adaptive_rho.restype = ctypes.c_int
     lib.oracle_activation_latency.restype = ctypes.c_int
     lib.oracle_degradation_cost.argtypes = [f64, i32, P, P, P, ctypes.c_float, P]
     lib.oracle_degradation_cost.restype = ctypes.c_int
@@ -274,6 +279,19 @@ def activation_latency(tier, model_bytes, tier_bw, tier_setup_ms):
     if st != 0:
         raise RuntimeError(f"oracle_activation_latency failed with status {st}")
     return out
+
+
+def adaptive_rho(kv_actual, kv_pred, beta: float, q: float):
+    """Safety margin from recent prediction errors: returns (ewma float32 [m], rho float32)."""
+    lib = _load()
+    a, p = _c(kv_actual, np.float64), _c(kv_pred, np.float64)
+    m = a.shape[0]
+    ew = np.empty(m, np.float32)
+    rho = np.empty(1, np.float32)
+    st = lib.oracle_adaptive_rho(_ptr(a), _ptr(p), m, float(beta), float(q), _ptr(ew), _ptr(rho))
+    if st != 0:
+        raise RuntimeError(f"oracle_adaptive_rho failed with status {st}")
+    return ew, rho[0]
 
 
 def quantiles(values, q_lo: float = 0.05, q_hi: float = 0.95):

@@ -338,6 +338,35 @@ int oracle_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* 
   return ORACLE_OK;
 }
 
+/* Adaptive safety margin (Sec. III-D): the relative underestimation e = max(0, R_kv / R^_kv - 1)
+ * of each of the last m stages (arrival order), its EWMA e~_i = beta e_i + (1 - beta) e~_(i-1)
+ * starting from e~_0 = e_0 (float64, sequential), stored as float32; rho = the value of rank
+ * ceil(q (m - 1)) (0-based, ascending) among the stored EWMA values. */
+static int f32_cmp(const void* pa, const void* pb) {
+  const float a = *(const float*)pa, b = *(const float*)pb;
+  return (a > b) - (a < b);
+}
+
+int oracle_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta, double q,
+                        float* ewma, float* rho) {
+  if (m < 1 || !(beta > 0.0 && beta <= 1.0) || !(q >= 0.0 && q <= 1.0)) return ORACLE_BAD_ARG;
+  double s = 0.0;
+  for (int64_t i = 0; i < m; ++i) {
+    double e = kv_actual[i] / kv_pred[i] - 1.0;      /* relative underestimation */
+    if (!(e > 0.0)) e = 0.0;
+    s = (i == 0) ? e : beta * e + (1.0 - beta) * s;  /* EWMA */
+    ewma[i] = (float)s;
+  }
+  float* sorted = (float*)malloc(sizeof(float) * (size_t)m);
+  if (!sorted) return ORACLE_NO_MEM;
+  memcpy(sorted, ewma, sizeof(float) * (size_t)m);
+  qsort(sorted, (size_t)m, sizeof(float), f32_cmp);
+  const int64_t r = (int64_t)ceil(q * (double)(m - 1));   /* a high quantile, no interpolation */
+  *rho = sorted[r];
+  free(sorted);
+  return ORACLE_OK;
+}
+
 /* robust min-max normalisation onto [0, 1] with window bounds lo, hi (values outside the
  * bounds clip); a degenerate window (hi <= lo) maps everything to 0. float32 throughout. */
 static float norm_inv(float lo, float hi) { return hi > lo ? 1.0f / (hi - lo) : 0.0f; }

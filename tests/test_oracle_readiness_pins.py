@@ -80,3 +80,42 @@ def test_readiness_is_per_model():
     act2 = oracle.activation_latency(tier[::-1].copy(), np.array([16 * GB, 16 * GB]), BW, SETUP)
     idx, _ = _route(nodes, st, [[1, 1, 0]], [0, 1, 0, 20000, 0, 1], k=1, n_models=n_models, act_matrix=act2)
     assert idx[:, 0].tolist() == [1, 0, 1, 0]
+
+
+# ---- adaptive safety margin (Sec. III-D): EWMA of the relative underestimation, high quantile ----
+
+def test_adaptive_rho_closed_forms():
+    rng = np.random.default_rng(5)
+    m = 2000
+    pred = rng.uniform(1, 100, m) * GB
+    actual = pred * rng.lognormal(0.0, 0.3, m)
+    e = np.maximum(actual / pred - 1.0, 0.0)
+    # beta = 1: no smoothing, the EWMA is e itself; rho its "higher" percentile
+    ew, rho = oracle.adaptive_rho(actual, pred, 1.0, 0.95)
+    assert np.array_equal(ew, e.astype(np.float32))
+    assert rho == np.percentile(ew, 95, method="higher")
+    # exact or over-estimating predictions: no margin
+    ew, rho = oracle.adaptive_rho(pred, pred, 0.2, 0.9)
+    assert not ew.any() and rho == 0.0
+    ew, rho = oracle.adaptive_rho(0.5 * pred, pred, 0.2, 0.9)
+    assert not ew.any() and rho == 0.0
+    # a constant underestimation of 25% is its own average and quantile
+    ew, rho = oracle.adaptive_rho(1.25 * pred, pred, 0.3, 0.9)
+    assert np.all(ew == np.float32(0.25)) and rho == np.float32(0.25)
+
+
+def test_adaptive_rho_recursion_and_window_quantile():
+    # one underestimate followed by exact predictions decays geometrically: e~_i = x (1 - beta)^i
+    m, beta, x = 50, 0.2, 0.8
+    pred = np.full(m, 1e9)
+    actual = pred.copy()
+    actual[0] = (1 + x) * 1e9
+    ew, rho = oracle.adaptive_rho(actual, pred, beta, 0.5)
+    np.testing.assert_allclose(ew, x * (1 - beta) ** np.arange(m), rtol=1e-6)
+    assert rho == np.sort(ew)[int(np.ceil(0.5 * (m - 1)))]
+    # the quantile is over the smoothed values, not the raw errors: alternating errors smooth out
+    pred = np.full(1000, 1e9)
+    actual = np.where(np.arange(1000) % 2 == 0, 2e9, 1e9)          # e alternates 1, 0
+    ew, rho = oracle.adaptive_rho(actual, pred, 0.1, 0.95)
+    assert 0.45 < rho < 0.6                                       # near the mean 0.5, far below 1
+    assert rho == np.percentile(ew, 95, method="higher")
