@@ -7,6 +7,7 @@ python bench.py --route-fitness        (routing by fitness, Eq. 5, on the worklo
 python bench.py --route-fitness --plans   (the same with C_deg from degradation plans, Alg. 2)
 python bench.py --route-fitness --readiness  (T_act per (node, model) from readiness tiers, Sec. III-C)
 python bench.py --two-phase            (the two-phase predictor, Sec. III-B, beside the bins one)
+python bench.py --margin               (the adaptive safety margin rho, Sec. III-D, over windows)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -288,6 +289,23 @@ def two_phase_bench(name: str, steps: int, warmup: int):
     print(json.dumps(res), flush=True)
 
 
+def margin_bench(steps: int, warmup: int):
+    """The adaptive safety margin (EWMA of the relative underestimation, then its high quantile)
+    over windows of recent stages. Latency-bound: one workgroup per kernel. One JSON line."""
+    import torch
+    from paper_2606_12950_amd import _native, pipeline
+    from paper_2606_12950_amd import workload as W
+    torch.cuda.set_device(0)
+    res = {"margin": "adaptive rho", "beta": 0.2, "q": 0.95, "windows": []}
+    for m in (4096, 65536, 1 << 20):
+        actual, pred = W.margin_window(3, m)
+        a, p = pipeline._t(actual, "cuda"), pipeline._t(pred, "cuda")
+        out = _native.adaptive_rho(a, p, 0.2, 0.95)
+        d = _time_events(lambda: _native.adaptive_rho(a, p, 0.2, 0.95, out=out), steps, warmup)
+        res["windows"].append({"m": m, "ms": percentiles(d), "rho": float(out[1].item())})
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -305,12 +323,16 @@ def main():
                     help="with --route-fitness: C_deg from degradation plans (Alg. 2, Eq. 4)")
     ap.add_argument("--readiness", action="store_true",
                     help="with --route-fitness: T_act per (node, model) from readiness tiers (Sec. III-C)")
+    ap.add_argument("--margin", action="store_true", help="time the adaptive safety margin (Sec. III-D)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.margin:
+        margin_bench(steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
         return
     if args.two_phase:
         two_phase_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))

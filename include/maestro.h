@@ -289,6 +289,20 @@ MAESTRO_API maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n
                              const double* model_bytes, const double* tier_bw,
                              const float* tier_setup_ms, float* act_ms, void* stream);
 
+/* Adaptive safety margin rho of R_need = (1 + rho) R_kv (Sec. III-D), from the last m stages
+ * prediction errors in arrival order:
+ *   e_i    = max(0, kv_actual[i] / kv_pred[i] - 1)                 relative underestimation
+ *   s_0 = e_0,  s_i = beta e_i + (1 - beta) s_(i-1)                 EWMA (float64)
+ *   ewma[i] = fl32(s_i)                                             (out, [m] float32)
+ *   rho[0]  = the value of rank ceil(q (m - 1)) (0-based, ascending) among ewma[0 .. m-1]
+ * kv_actual, kv_pred [m] float64 (device; kv_pred > 0, both finite); 0 < beta <= 1; 0 <= q <= 1
+ * (a high quantile, 0.9 - 0.95). ewma doubles as the selection's input. The float64 EWMA is a
+ * parallel scan, so ewma can differ from a sequential evaluation in the last place. Errors:
+ * INVALID_ARG for m < 1, beta or q out of range, a NULL or misaligned array; UNSUPPORTED for
+ * m > 2^32 - 1. */
+MAESTRO_API maestro_status maestro_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m,
+                             double beta, double q, float* ewma, float* rho, void* stream);
+
 /* Window bounds of the robust normalisation in Eq. 5 (per-metric 5th/95th percentiles of a
  * recent window): out[0] and out[1] (device, float32) receive the values of rank
  * floor(q_lo * (m - 1)) and ceil(q_hi * (m - 1)) of values[0 .. m-1] (device, finite), ranks

@@ -6,12 +6,12 @@ generator. PyTorch supplies device memory and streams only.
 """
 from ._native import (LIBRARY_PATH, MaestroError, Predictor, TwoPhase, load, make_predictor, predict,
                       predict_two_phase,
-                      activation_latency, degradation_plans, prioritize, prioritize_workspace_bytes, quantiles, route,
+                      activation_latency, adaptive_rho, degradation_plans, prioritize, prioritize_workspace_bytes, quantiles, route,
                       route_fitness)
 from .pipeline import DeviceBatch, StepOutputs, run_step, to_device
 
 __all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "TwoPhase", "load", "make_predictor", "predict",
-           "predict_two_phase", "activation_latency", "degradation_plans",
+           "predict_two_phase", "activation_latency", "adaptive_rho", "degradation_plans",
            "prioritize", "prioritize_workspace_bytes", "quantiles", "route", "route_fitness",
            "DeviceBatch", "StepOutputs",
            "run_step", "to_device"]

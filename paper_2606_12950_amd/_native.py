@@ -22,7 +22,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 
 # Every function declared in include/maestro.h.
 EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
-           "maestro_degradation_plans", "maestro_activation_latency", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
+           "maestro_degradation_plans", "maestro_activation_latency", "maestro_adaptive_rho", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
@@ -72,6 +72,7 @@ def load():
     lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P,
                                           f64, i32, P, P, P]
     lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, P, P]
+    lib.maestro_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P, P]
     lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
@@ -383,6 +384,27 @@ def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: t
                                         _ptr(tier_setup_ms), _ptr(out) if M else None, _stream(stream))
     _check("maestro_activation_latency", st)
     return out
+
+
+def adaptive_rho(kv_actual: torch.Tensor, kv_pred: torch.Tensor, beta: float, q: float,
+                 out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_adaptive_rho: returns (ewma float32 [m], rho float32 [1]) on the device."""
+    lib = load()
+    _dev(kv_actual, "kv_actual", torch.float64)
+    _dev(kv_pred, "kv_pred", torch.float64)
+    m = kv_actual.shape[0]
+    if kv_pred.shape != (m,):
+        raise ValueError("kv_actual and kv_pred must have the same length")
+    if out is None:
+        out = (torch.empty(m, dtype=torch.float32, device=kv_actual.device),
+               torch.empty(1, dtype=torch.float32, device=kv_actual.device))
+    ew, rho = out
+    _dev(ew, "ewma", torch.float32)
+    _dev(rho, "rho", torch.float32)
+    st = lib.maestro_adaptive_rho(_ptr(kv_actual), _ptr(kv_pred), m, float(beta), float(q), _ptr(ew), _ptr(rho),
+                                  _stream(stream))
+    _check("maestro_adaptive_rho", st)
+    return ew, rho
 
 
 def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,

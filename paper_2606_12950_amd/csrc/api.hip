@@ -210,6 +210,17 @@ maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, con
                                             as_stream(stream));
 }
 
+maestro_status maestro_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
+                                    double q, float* ewma, float* rho, void* stream) {
+  if (m < 1 || !(beta > 0.0 && beta <= 1.0) || !(q >= 0.0 && q <= 1.0)) return MAESTRO_ERR_INVALID_ARG;
+  if (!kv_actual || !kv_pred || !ewma || !rho || !aligned(kv_actual, 8) || !aligned(kv_pred, 8) ||
+      !aligned(ewma, 4) || !aligned(rho, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (m > (int64_t)UINT32_MAX) return MAESTRO_ERR_UNSUPPORTED;
+  const int64_t rank = (int64_t)ceil(q * (double)(m - 1));
+  return maestro::launch_adaptive_rho(kv_actual, kv_pred, m, beta, rank, ewma, rho, as_stream(stream));
+}
+
 maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi, float* out,
                                  void* stream) {
   if (m < 1 || !(q_lo >= 0.0) || !(q_lo <= q_hi) || !(q_hi <= 1.0)) return MAESTRO_ERR_INVALID_ARG;

@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 constexpr int kSelectThreads = 1024;
 __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* __restrict__ v, int64_t m,
                                                                   int64_t r_lo, int64_t r_hi,
-                                                                  float* __restrict__ out) {
+                                                                  float* __restrict__ out, int n_out) {
   __shared__ uint32_t hist[2][256];
   __shared__ uint32_t scan[2][256];   // inclusive prefix within each 64-bin segment
   __shared__ uint32_t seg[2][4];      // segment totals
@@ -369,7 +369,63 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
     mask |= 0xFFu << shift;
     __syncthreads();
   }
-  if (tid < 2) out[tid] = key_float(s_prefix[par][tid]);
+  if (tid < n_out) out[tid] = key_float(s_prefix[par][tid]);
+}
+
+// EWMA of the relative underestimation e_i = max(0, actual_i / pred_i - 1) in arrival order,
+// s_0 = e_0, s_i = beta e_i + (1 - beta) s_(i-1), stored as float32. One workgroup: each thread
+// folds a contiguous segment into an affine map x -> A x + B, a scan of the maps gives every
+// segment its incoming value, and each thread then replays its segment with the recurrence.
+__device__ __forceinline__ double underestimation(double actual, double pred) {
+  const double e = __dsub_rn(__ddiv_rn(actual, pred), 1.0);
+  return e > 0.0 ? e : 0.0;
+}
+
+__global__ __launch_bounds__(kSelectThreads) void ewma_kernel(const double* __restrict__ actual,
+                                                              const double* __restrict__ pred, int64_t m,
+                                                              double beta, float* __restrict__ ewma) {
+  __shared__ double s_a[2][kSelectThreads], s_b[2][kSelectThreads];
+  const int tid = threadIdx.x;
+  const double keep = __dsub_rn(1.0, beta);
+  const int64_t per = (m + kSelectThreads - 1) / kSelectThreads;
+  const int64_t lo = min(m, tid * per), hi = min(m, lo + per);
+  double A = 1.0, B = 0.0;   // identity
+  for (int64_t i = lo; i < hi; ++i) {
+    const double e = underestimation(actual[i], pred[i]);
+    if (i == 0) {
+      A = 0.0;
+      B = e;
+    } else {
+      A = __dmul_rn(keep, A);
+      B = __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, B));
+    }
+  }
+  // inclusive scan of the maps in thread order (Hillis-Steele, double-buffered): the map of
+  // threads p..t applied after the map of earlier threads
+  int buf = 0;
+  s_a[0][tid] = A;
+  s_b[0][tid] = B;
+  __syncthreads();
+  for (int d = 1; d < kSelectThreads; d <<= 1) {
+    double a = s_a[buf][tid], b = s_b[buf][tid];
+    if (tid >= d) {
+      const double pa = s_a[buf][tid - d], pb = s_b[buf][tid - d];
+      b = __dadd_rn(__dmul_rn(a, pb), b);
+      a = __dmul_rn(a, pa);
+    }
+    s_a[buf ^ 1][tid] = a;
+    s_b[buf ^ 1][tid] = b;
+    buf ^= 1;
+    __syncthreads();
+  }
+  // the value entering this segment: the composed map of all earlier threads (which includes
+  // element 0, whose map is constant, so its B is the value itself)
+  double x = tid > 0 ? s_b[buf][tid - 1] : 0.0;
+  for (int64_t i = lo; i < hi; ++i) {
+    const double e = underestimation(actual[i], pred[i]);
+    x = (i == 0) ? e : __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, x));
+    ewma[i] = __double2float_rn(x);
+  }
 }
 
 }  // namespace
@@ -456,7 +512,16 @@ maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_o
 
 maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
                                 hipStream_t stream) {
-  quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(values, m, r_lo, r_hi, out);
+  quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(values, m, r_lo, r_hi, out, 2);
+  return launch_status();
+}
+
+maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
+                                   int64_t rank, float* ewma, float* rho, hipStream_t stream) {
+  ewma_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m, beta, ewma);
+  maestro_status st = launch_status();
+  if (st != MAESTRO_OK) return st;
+  quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(ewma, m, rank, rank, rho, 1);
   return launch_status();
 }
 

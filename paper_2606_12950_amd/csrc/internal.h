@@ -49,6 +49,8 @@ maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_o
 maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                                          const double* model_bytes, const double* tier_bw,
                                          const float* tier_setup_ms, float* act_ms, hipStream_t stream);
+maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
+                                   int64_t rank, float* ewma, float* rho, hipStream_t stream);
 maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
                                 hipStream_t stream);
 

@@ -440,6 +440,16 @@ def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
                         cost_ms=cost.astype(np.float32), c_int_ms=C_INT_MS, deg_window=deg_window)
 
 
+def margin_window(seed: int, m: int = 4096) -> Tuple[np.ndarray, np.ndarray]:
+    """A window of m recent stages' (actual, predicted) KV bytes for the adaptive margin:
+    predictions U[1, 100] GB, actual = prediction x lognormal(-0.05, 0.25) (about 40% of the
+    stages underestimated, by up to ~2x)."""
+    r = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0x4A0])))
+    pred = r.uniform(1.0, 100.0, m) * GB
+    actual = pred * r.lognormal(-0.05, 0.25, m)
+    return actual, pred
+
+
 READINESS_STREAMS = ("tier", "size")
 # readiness tiers (Sec. III-C): 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote
 TIER_P = (0.3, 0.3, 0.3, 0.1)               # tiers 1..4 of a model that is not running on a node

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -189,6 +189,21 @@ def test_activation_latency_validation(lib):
     assert call(bw=None) == INVALID
     assert call(out=MISALIGNED4) == INVALID
     assert call(M=0, tier=None, out=None) == OK                               # no nodes: no-op
+
+
+def test_adaptive_rho_validation(lib):
+    def call(m=100, beta=0.2, q=0.95, a=FAKE, p=FAKE, ew=FAKE, rho=FAKE):
+        return lib.maestro_adaptive_rho(a, p, m, beta, q, ew, rho, None)
+    assert call(m=0) == INVALID
+    assert call(beta=0.0) == INVALID                                          # no weight on new errors
+    assert call(beta=1.5) == INVALID
+    assert call(beta=float("nan")) == INVALID
+    assert call(q=-0.1) == INVALID
+    assert call(q=1.01) == INVALID
+    assert call(a=None) == INVALID
+    assert call(p=MISALIGNED) == INVALID
+    assert call(rho=MISALIGNED4) == INVALID
+    assert call(m=1 << 32) == UNSUPPORTED
 
 
 def test_degradation_plans_validation(lib):

@@ -421,3 +421,37 @@ def test_fitness_with_readiness_and_plans_workload_full(name):
                              k=w.spec.k, rho=w.spec.rho, eng=eng)
     assert_same(got, ref)
     print(f"{name}: {w.n} stages x {w.free_bytes.size} nodes, readiness tiers + plans, fitness identical")
+
+
+# ---- adaptive safety margin (Sec. III-D) ---------------------------------------------------------
+
+def _ulp_close(got, ref):
+    """Within one float32 unit in the last place (the float64 EWMA is a parallel scan on the GPU
+    and a sequential loop in the oracle; rounding to float32 can then differ in the last place)."""
+    got, ref = np.asarray(got, np.float32), np.asarray(ref, np.float32)
+    return np.all(np.abs(got.astype(np.float64) - ref) <= np.spacing(np.abs(ref)).astype(np.float64))
+
+
+@pytest.mark.parametrize("m", [1, 2, 1000, 1023, 1024, 1025, 4096, 100003, 3000000])
+def test_adaptive_rho_matches_oracle(m):
+    actual, pred = W.margin_window(m, m)
+    for beta, q in [(0.2, 0.95), (0.05, 0.9), (1.0, 0.95), (0.5, 1.0), (0.2, 0.0)]:
+        ew, rho = M.adaptive_rho(_t(actual), _t(pred), beta, q)
+        torch.cuda.synchronize()
+        ew, rho = ew.cpu().numpy(), rho.cpu().numpy()[0]
+        ew_o, rho_o = oracle.adaptive_rho(actual, pred, beta, q)
+        assert _ulp_close(ew, ew_o), (beta, q)
+        assert np.mean(ew.view(np.uint32) == ew_o.view(np.uint32)) > 0.999
+        # rho is an order statistic of the GPU's own values, and within an ulp of the oracle's
+        assert rho == np.sort(ew)[int(np.ceil(q * (m - 1)))]
+        assert _ulp_close(rho, rho_o), (beta, q, rho, rho_o)
+        if (beta, q) == (0.2, 0.95):
+            print(f"m={m}: rho(beta 0.2, q 0.95) = {rho:.4f}")
+
+
+def test_adaptive_rho_exact_cases():
+    pred = np.full(5000, 1e9)
+    ew, rho = M.adaptive_rho(_t(pred), _t(pred), 0.2, 0.95)
+    assert not ew.cpu().numpy().any() and rho.item() == 0.0
+    ew, rho = M.adaptive_rho(_t(1.25 * pred), _t(pred), 0.3, 0.9)
+    assert np.all(ew.cpu().numpy() == np.float32(0.25)) and rho.item() == np.float32(0.25)
