@@ -77,11 +77,11 @@ def _load():
     lib.oracle_predict_two_phase.argtypes = [i32, P, i32, P, P, i32, P, P, i32, P, P, ctypes.c_float, i64, P,
                                              P, P, P, P, P, i32, P, P, P, i32]
     lib.oracle_predict_two_phase.restype = ctypes.c_int
-    lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, i32]
+    lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
     lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
                                          f64, i32, P, P, P, P, ctypes.c_float, P, P, i32]
-    lib.oracle_activation_latency.argtypes = [i32, i32, P, P, P, P, P]
+    lib.oracle_activation_latency.argtypes = [i32, i32, P, P, P, P, f64, P]
     lib.oracle_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P]
     lib.oracle_adaptive_rho.restype = ctypes.c_int
     lib.oracle_activation_latency.restype = ctypes.c_int
@@ -192,8 +192,9 @@ def predict_two_phase(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequ
 
 
 def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s, cold_s,
-          resident_mask, k: int = 1, rho: float = 0.0, n_threads: int = 0):
-    """Returns (node_idx int32 [N][k], score float32 [N][k])."""
+          resident_mask, k: int = 1, rho: float = 0.0, n_threads: int = 0, act_matrix=None):
+    """Returns (node_idx int32 [N][k], score float32 [N][k]). With ``act_matrix`` [M][n_models]
+    (seconds) T_act comes from it instead of ``cold_s`` / ``resident_mask``."""
     lib = _load()
     mi = _c(model_id, np.int32)
     n = mi.shape[0]
@@ -201,10 +202,14 @@ def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s,
     dec = _c(decode_s_per_token, np.float32)
     fr, q, cd = _c(free_bytes, np.float64), _c(queue_s, np.float32), _c(cold_s, np.float32)
     rm = _c(resident_mask, np.uint64)
+    am = None
+    if act_matrix is not None:
+        am = _c(act_matrix, np.float32)
+        assert am.shape == (fr.shape[0], dec.shape[0])
     idx = np.empty((n, k), np.int32)
     sc = np.empty((n, k), np.float32)
     st = lib.oracle_route(n, _ptr(mi), _ptr(pr), _ptr(kv), _ptr(dec), dec.shape[0], fr.shape[0],
-                          _ptr(fr), _ptr(q), _ptr(cd), _ptr(rm), float(rho), int(k), _ptr(idx),
+                          _ptr(fr), _ptr(q), _ptr(cd), _ptr(rm), _ptr(am), float(rho), int(k), _ptr(idx),
                           _ptr(sc), n_threads or max_threads())
     if st != 0:
         raise RuntimeError(f"oracle_route failed with status {st}")
@@ -266,16 +271,17 @@ def degradation_cost(R: float, level, freed, cost, c_int: float):
     return None if st else float(out[0])
 
 
-def activation_latency(tier, model_bytes, tier_bw, tier_setup_ms):
-    """T_act [M][K] float32 (ms) of every model on every node from its readiness tier [M][K]
-    (0 Running, 1 Sleeping, 2 CPU, 3 Disk, 4 Remote): Size / BW_tier plus a per-tier setup."""
+def activation_latency(tier, model_bytes, tier_bw, tier_setup_ms, unit: float = 1000.0):
+    """T_act [M][K] float32 of every model on every node from its readiness tier [M][K]
+    (0 Running, 1 Sleeping, 2 CPU, 3 Disk, 4 Remote): Size / BW_tier plus a per-tier setup, in
+    the time unit with ``unit`` counts per second (1000: ms, the default; 1: s)."""
     lib = _load()
     t = _c(tier, np.uint8)
     M, K = t.shape
     mb, bw, st_ = _c(model_bytes, np.float64), _c(tier_bw, np.float64), _c(tier_setup_ms, np.float32)
     assert mb.shape == (K,) and bw.shape == (5,) and st_.shape == (5,)
     out = np.empty((M, K), np.float32)
-    st = lib.oracle_activation_latency(M, K, _ptr(t), _ptr(mb), _ptr(bw), _ptr(st_), _ptr(out))
+    st = lib.oracle_activation_latency(M, K, _ptr(t), _ptr(mb), _ptr(bw), _ptr(st_), float(unit), _ptr(out))
     if st != 0:
         raise RuntimeError(f"oracle_activation_latency failed with status {st}")
     return out

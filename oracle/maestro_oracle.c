@@ -257,8 +257,8 @@ static int cand_less(cand_t a, cand_t b) { return a.s < b.s || (a.s == b.s && a.
 int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
                  const double* kv_bytes, const float* decode_s_per_token, int32_t n_models,
                  int32_t n_nodes, const double* free_bytes, const float* queue_s,
-                 const float* cold_s, const uint64_t* resident_mask, double rho, int32_t k,
-                 int32_t* node_idx, float* score, int32_t n_threads) {
+                 const float* cold_s, const uint64_t* resident_mask, const float* act_matrix,
+                 double rho, int32_t k, int32_t* node_idx, float* score, int32_t n_threads) {
   if (n < 0 || n_nodes < 1 || n_models < 1 || n_models > 64 || k < 1 || rho < 0.0)
     return ORACLE_BAD_ARG;
   int status = ORACLE_OK;
@@ -282,8 +282,13 @@ int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
         int32_t nc = 0;
         for (int32_t nd = 0; nd < n_nodes; ++nd) {
           if (need > free_bytes[nd]) continue;              /* infeasible: not enough headroom */
-          const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
-          const float act = resident ? 0.0f : cold_s[nd];  /* T_act: cold start unless resident */
+          float act;                                        /* T_act of model m on the node */
+          if (act_matrix) {                                 /* from its readiness tier */
+            act = act_matrix[(int64_t)nd * n_models + m];
+          } else {                                          /* cold start unless resident */
+            const int resident = (int)((resident_mask[nd] >> (unsigned)m) & 1u);
+            act = resident ? 0.0f : cold_s[nd];
+          }
           const float ready = queue_s[nd] + act;            /* Eq. 6: T_ready = T_q + T_act */
           const float s = ready + exec_s;                   /* expected completion latency */
           c[nc].s = s;
@@ -320,18 +325,19 @@ int oracle_route(int64_t n, const int32_t* model_id, const float* pred_len,
 /* Model readiness (Sec. III-C): the activation latency of model m on a node whose copy of m is
  * in tier t -- 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote (tiers past 4
  * count as Remote) -- from the profiled bandwidth model T_act = Size / BW_tier, plus a fixed
- * per-tier setup time: 0 when Running, else setup_ms[t] + (bytes[m] / bw[t]) * 1000 ms,
- * evaluated in float64 in that order and stored as float32. */
+ * per-tier setup time: 0 when Running, else setup[t] + (bytes[m] / bw[t]) * unit, in the unit
+ * of time whose count per second is `unit` (1000 for ms, 1 for s), evaluated in float64 in
+ * that order and stored as float32. */
 int oracle_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                               const double* model_bytes, const double* tier_bw,
-                              const float* tier_setup_ms, float* act_ms) {
-  if (n_nodes < 0 || n_models < 1) return ORACLE_BAD_ARG;
+                              const float* tier_setup_ms, double unit, float* act_ms) {
+  if (n_nodes < 0 || n_models < 1 || !(unit > 0.0)) return ORACLE_BAD_ARG;
   for (int64_t j = 0; j < (int64_t)n_nodes; ++j) {
     for (int32_t m = 0; m < n_models; ++m) {
       int t = tier[j * n_models + m];
       if (t > 4) t = 4;
       float a = 0.0f;
-      if (t > 0) a = (float)((double)tier_setup_ms[t] + (model_bytes[m] / tier_bw[t]) * 1000.0);
+      if (t > 0) a = (float)((double)tier_setup_ms[t] + (model_bytes[m] / tier_bw[t]) * unit);
       act_ms[j * n_models + m] = a;
     }
   }

@@ -119,3 +119,35 @@ def test_adaptive_rho_recursion_and_window_quantile():
     ew, rho = oracle.adaptive_rho(actual, pred, 0.1, 0.95)
     assert 0.45 < rho < 0.6                                       # near the mean 0.5, far below 1
     assert rho == np.percentile(ew, 95, method="higher")
+
+
+def test_activation_latency_units_and_latency_routing():
+    # the time unit: 2.5 GB over 1.25 GB/s is 2 s, 2000 ms; setups are taken in the same unit
+    tier = np.array([[4, 0]], np.uint8)
+    size = np.array([2.5 * GB, 7 * GB])
+    assert oracle.activation_latency(tier, size, BW, np.zeros(5, np.float32), unit=1.0)[0].tolist() == [2.0, 0.0]
+    assert oracle.activation_latency(tier, size, BW, np.zeros(5, np.float32))[0].tolist() == [2000.0, 0.0]
+    assert oracle.activation_latency(tier, size, BW, np.full(5, 0.5, np.float32), unit=1.0)[0, 0] == 2.5
+    # latency routing (Alg. 3 with Eq. 6): a {0, cold} matrix in seconds equals the resident-mask form
+    rng = np.random.default_rng(6)
+    M, n, K = 400, 2000, 16
+    free = rng.uniform(0, 300, M) * GB
+    q = rng.uniform(0, 5, M).astype(np.float32)
+    cold = rng.uniform(2, 20, M).astype(np.float32)
+    mask = rng.integers(0, 1 << K, M).astype(np.uint64)
+    model = rng.integers(0, K, n).astype(np.int32)
+    pred = rng.uniform(10, 2000, n).astype(np.float32)
+    kv = rng.uniform(0, 250, n) * GB
+    dec = rng.uniform(0.01, 0.04, K).astype(np.float32)
+    bits = (mask[:, None] >> np.arange(K, dtype=np.uint64)[None, :]) & np.uint64(1)
+    mat = np.where(bits == 1, 0.0, cold[:, None]).astype(np.float32)
+    i0, s0 = oracle.route(model, pred, kv, dec, free, q, cold, mask, k=3)
+    i1, s1 = oracle.route(model, pred, kv, dec, free, q, cold, mask, k=3, act_matrix=mat)
+    assert np.array_equal(i0, i1) and np.array_equal(s0.view(np.uint32), s1.view(np.uint32))
+    # with tiers, a stage goes to the node whose ready time for its own model is least
+    tier = rng.integers(0, 5, (M, K)).astype(np.uint8)
+    act = oracle.activation_latency(tier, rng.uniform(1, 28, K) * GB, BW, SETUP / 1000, unit=1.0)
+    i2, s2 = oracle.route(model, pred, kv, dec, np.full(M, 1e15), q, cold, mask, k=1, act_matrix=act)
+    ready = q[None, :] + act.T[model]
+    best = np.lexsort((np.broadcast_to(np.arange(M), ready.shape), (ready + (pred * dec[model])[:, None]).astype(np.float32)), axis=1)
+    assert np.array_equal(i2[:, 0], best[:, 0])
