@@ -106,6 +106,18 @@ MAESTRO_API maestro_status maestro_predict(const maestro_predictor* p, int64_t n
                                float* pred_len, double* kv_bytes,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* maestro_route_ex with T_act(N, M(T)) of Eq. 6 from readiness tiers: act_s [n_nodes][n_models]
+ * float32 (seconds; maestro_activation_latency with unit = 1) replaces cold_s and
+ * resident_mask, so score = fl32(fl32(queue_s[j] + act_s[j][m]) + fl32(pred_len[i] *
+ * decode_s_per_token[m])). Same algorithms, workspace, outputs and errors as maestro_route_ex
+ * (a NULL act_s is INVALID_ARG). */
+MAESTRO_API maestro_status maestro_route_tiered(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* act_s, double rho, int32_t k, int32_t algo,
+                             int32_t* node_idx, float* score, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
 /* The two-phase predictor (Sec. III-B). The network of a maestro_predictor (dims[n_layers] =
  * B = 64 outputs) is read as heads instead of bins: output 0 is the tool-intent logit z_0,
  * output g (1 <= g < B) the log(1 + L) regressor of head g; head 1 is the shared global model.
@@ -275,19 +287,21 @@ MAESTRO_API maestro_status maestro_route_fitness(int64_t n, const int32_t* model
 
 /* Model readiness (Sec. III-C): T_act of every model on every node from the readiness tier of
  * the node's copy of it -- 0 Running, 1 Sleeping, 2 CPU-resident, 3 Disk-resident, 4 Remote
- * (values past 4 count as Remote) -- with the profiled bandwidth model T_act = Size / BW_tier:
- *   act_ms[j][m] = tier == 0 ? 0 : fl32(tier_setup_ms[t] + (model_bytes[m] / tier_bw[t]) * 1000)
+ * (values past 4 count as Remote) -- with the profiled bandwidth model T_act = Size / BW_tier,
+ * in the time unit that has `unit` counts per second (1000: ms for maestro_route_fitness; 1:
+ * seconds for maestro_route_tiered):
+ *   act[j][m] = tier == 0 ? 0 : fl32(tier_setup[t] + (model_bytes[m] / tier_bw[t]) * unit)
  * (float64 in that order).
- *   tier           [n_nodes][n_models] uint8
- *   model_bytes    [n_models] float64: weight bytes of each model
- *   tier_bw        [5] float64: bytes/s each tier loads at (entry 0 unused), > 0
- *   tier_setup_ms  [5] float32: fixed activation overhead of each tier (entry 0 unused)
- *   act_ms (out)   [n_nodes][n_models] float32, ready for maestro_route_fitness's act_matrix
- * Device arrays; 1 <= n_models <= 64, n_nodes >= 0 (0: no-op). Errors: INVALID_ARG for a NULL or
- * misaligned array or a size out of range. */
+ *   tier         [n_nodes][n_models] uint8
+ *   model_bytes  [n_models] float64: weight bytes of each model
+ *   tier_bw      [5] float64: bytes/s each tier loads at (entry 0 unused), > 0
+ *   tier_setup   [5] float32: fixed activation overhead of each tier, in the output unit
+ *   act (out)    [n_nodes][n_models] float32
+ * Device arrays; 1 <= n_models <= 64, n_nodes >= 0 (0: no-op), unit finite and > 0. Errors:
+ * INVALID_ARG for a NULL or misaligned array or a value out of range. */
 MAESTRO_API maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                              const double* model_bytes, const double* tier_bw,
-                             const float* tier_setup_ms, float* act_ms, void* stream);
+                             const float* tier_setup, double unit, float* act, void* stream);
 
 /* Adaptive safety margin rho of R_need = (1 + rho) R_kv (Sec. III-D), from the last m stages
  * prediction errors in arrival order:

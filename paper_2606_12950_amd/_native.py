@@ -21,7 +21,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
            4: "kernel launch failed"}
 
 # Every function declared in include/maestro.h.
-EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_ex", "maestro_route_fitness",
+EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_tiered", "maestro_route_ex", "maestro_route_fitness",
            "maestro_degradation_plans", "maestro_activation_latency", "maestro_adaptive_rho", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
 
@@ -71,7 +71,8 @@ def load():
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P,
                                           f64, i32, P, P, P]
-    lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, P, P]
+    lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, f64, P, P]
+    lib.maestro_route_tiered.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P, P]
     lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
@@ -221,10 +222,13 @@ def predict_two_phase(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: 
 
 def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,
           decode_s_per_token: torch.Tensor, free_bytes: torch.Tensor, queue_s: torch.Tensor,
-          cold_s: torch.Tensor, resident_mask: torch.Tensor, k: int = 1, rho: float = 0.0,
+          cold_s: Optional[torch.Tensor], resident_mask: Optional[torch.Tensor], k: int = 1, rho: float = 0.0,
           algo: int = ROUTE_AUTO, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
-          workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """maestro_route_ex: returns (node_idx int32 [N][k], score float32 [N][k]).
+          workspace: Optional[torch.Tensor] = None, stream=None,
+          act_s: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_route_ex: returns (node_idx int32 [N][k], score float32 [N][k]); with ``act_s``
+    [n_nodes][n_models] (seconds, from readiness tiers) maestro_route_tiered instead, and
+    ``cold_s`` / ``resident_mask`` may be None.
 
     ``resident_mask`` is int64 on the torch side (same bits as the C-ABI's uint64)."""
     lib = load()
@@ -235,12 +239,20 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
     _dev(decode_s_per_token, "decode_s_per_token", torch.float32)
     _dev(free_bytes, "free_bytes", torch.float64)
     _dev(queue_s, "queue_s", torch.float32)
-    _dev(cold_s, "cold_s", torch.float32)
-    _dev(resident_mask, "resident_mask", torch.int64)
     M = free_bytes.shape[0]
+    K = decode_s_per_token.shape[0]
     if pred_len.shape[0] != n or kv_bytes.shape[0] != n:
         raise ValueError("per-stage inputs must have the same length")
-    if queue_s.shape[0] != M or cold_s.shape[0] != M or resident_mask.shape[0] != M:
+    if act_s is not None:
+        _dev(act_s, "act_s", torch.float32)
+        if tuple(act_s.shape) != (M, K):
+            raise ValueError("act_s must be [n_nodes][n_models]")
+    else:
+        _dev(cold_s, "cold_s", torch.float32)
+        _dev(resident_mask, "resident_mask", torch.int64)
+        if cold_s.shape[0] != M or resident_mask.shape[0] != M:
+            raise ValueError("per-node inputs must have the same length")
+    if queue_s.shape[0] != M:
         raise ValueError("per-node inputs must have the same length")
     if out is None:
         out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
@@ -251,12 +263,17 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
     ws_bytes = route_workspace_bytes(n, decode_s_per_token.shape[0], M, k)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=model_id.device)
+    ws = (_ptr(workspace) if workspace is not None else None, workspace.numel() if workspace is not None else 0)
+    if act_s is not None:
+        st = lib.maestro_route_tiered(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes), _ptr(decode_s_per_token),
+                                      K, M, _ptr(free_bytes), _ptr(queue_s), _ptr(act_s), float(rho), int(k),
+                                      int(algo), _ptr(idx), _ptr(sc), ws[0], ws[1], _stream(stream))
+        _check("maestro_route_tiered", st)
+        return idx, sc
     st = lib.maestro_route_ex(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes),
-                              _ptr(decode_s_per_token), decode_s_per_token.shape[0], M,
+                              _ptr(decode_s_per_token), K, M,
                               _ptr(free_bytes), _ptr(queue_s), _ptr(cold_s), _ptr(resident_mask),
-                              float(rho), int(k), int(algo), _ptr(idx), _ptr(sc),
-                              _ptr(workspace) if workspace is not None else None,
-                              workspace.numel() if workspace is not None else 0,
+                              float(rho), int(k), int(algo), _ptr(idx), _ptr(sc), ws[0], ws[1],
                               _stream(stream))
     _check("maestro_route_ex", st)
     return idx, sc
@@ -365,10 +382,12 @@ def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, e
 
 
 def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: torch.Tensor,
-                       tier_setup_ms: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """maestro_activation_latency: T_act [n_nodes][n_models] float32 (ms) from the readiness tier
+                       tier_setup_ms: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None,
+                       unit: float = 1000.0) -> torch.Tensor:
+    """maestro_activation_latency: T_act [n_nodes][n_models] float32 from the readiness tier
     [n_nodes][n_models] uint8 (0 Running .. 4 Remote), model sizes [n_models] float64 (bytes),
-    tier bandwidths [5] float64 (bytes/s) and setup times [5] float32 (ms)."""
+    tier bandwidths [5] float64 (bytes/s) and setup times [5] float32, in the time unit with
+    ``unit`` counts per second (1000: ms, the default; 1: s)."""
     lib = load()
     _dev(tier, "tier", torch.uint8)
     _dev(model_bytes, "model_bytes", torch.float64)
@@ -381,7 +400,7 @@ def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: t
         out = torch.empty((M, K), dtype=torch.float32, device=tier.device)
     _dev(out, "act_ms", torch.float32)
     st = lib.maestro_activation_latency(M, K, _ptr(tier) if M else None, _ptr(model_bytes), _ptr(tier_bw),
-                                        _ptr(tier_setup_ms), _ptr(out) if M else None, _stream(stream))
+                                        _ptr(tier_setup_ms), float(unit), _ptr(out) if M else None, _stream(stream))
     _check("maestro_activation_latency", st)
     return out
 

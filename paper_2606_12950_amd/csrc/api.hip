@@ -101,22 +101,26 @@ maestro_status maestro_predict_two_phase(const maestro_predictor* p, const maest
                                            as_stream(stream));
 }
 
-maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float* pred_len,
-                                const double* kv_bytes, const float* decode_s_per_token,
-                                int32_t n_models, int32_t n_nodes, const double* free_bytes,
-                                const float* queue_s, const float* cold_s,
-                                const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
-                                int32_t* node_idx, float* score, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+namespace {
+
+// maestro_route_ex and maestro_route_tiered: T_act from (cold_s, resident_mask), or from
+// act_matrix when it is not NULL
+maestro_status route_checked(int64_t n, const int32_t* model_id, const float* pred_len, const double* kv_bytes,
+                             const float* decode_s_per_token, int32_t n_models, int32_t n_nodes,
+                             const double* free_bytes, const float* queue_s, const float* cold_s,
+                             const uint64_t* resident_mask, const float* act_matrix, double rho, int32_t k,
+                             int32_t algo, int32_t* node_idx, float* score, void* workspace,
+                             size_t workspace_bytes, void* stream) {
   if (n < 0 || n_models < 1 || n_models > 64 || n_nodes < 1 || k < 1 || k > 16)
     return MAESTRO_ERR_INVALID_ARG;
   if (algo != MAESTRO_ROUTE_AUTO && algo != MAESTRO_ROUTE_SCAN && algo != MAESTRO_ROUTE_SORTED)
     return MAESTRO_ERR_INVALID_ARG;
   if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
-  if (!decode_s_per_token || !free_bytes || !queue_s || !cold_s || !resident_mask)
+  if (!decode_s_per_token || !free_bytes || !queue_s) return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(decode_s_per_token, 4) || !aligned(free_bytes, 8) || !aligned(queue_s, 4))
     return MAESTRO_ERR_INVALID_ARG;
-  if (!aligned(decode_s_per_token, 4) || !aligned(free_bytes, 8) || !aligned(queue_s, 4) ||
-      !aligned(cold_s, 4) || !aligned(resident_mask, 8))
+  if (act_matrix ? !aligned(act_matrix, 4)
+                 : (!cold_s || !resident_mask || !aligned(cold_s, 4) || !aligned(resident_mask, 8)))
     return MAESTRO_ERR_INVALID_ARG;
   if (n > 0) {
     if (!model_id || !pred_len || !kv_bytes || !node_idx || !score) return MAESTRO_ERR_INVALID_ARG;
@@ -129,8 +133,34 @@ maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float*
   if (algo != MAESTRO_ROUTE_SCAN && (workspace_bytes < need || (need > 0 && !aligned(workspace, 16))))
     return MAESTRO_ERR_WORKSPACE;
   return maestro::launch_route(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models,
-                               n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k, algo,
-                               node_idx, score, workspace, workspace_bytes, as_stream(stream));
+                               n_nodes, free_bytes, queue_s, cold_s, resident_mask, act_matrix, rho, k,
+                               algo, node_idx, score, workspace, workspace_bytes, as_stream(stream));
+}
+
+}  // namespace
+
+maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, const float* pred_len,
+                                const double* kv_bytes, const float* decode_s_per_token,
+                                int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                                const float* queue_s, const float* cold_s,
+                                const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
+                                int32_t* node_idx, float* score, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (!cold_s || !resident_mask) return MAESTRO_ERR_INVALID_ARG;
+  return route_checked(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes, free_bytes,
+                       queue_s, cold_s, resident_mask, nullptr, rho, k, algo, node_idx, score, workspace,
+                       workspace_bytes, stream);
+}
+
+maestro_status maestro_route_tiered(int64_t n, const int32_t* model_id, const float* pred_len,
+                                    const double* kv_bytes, const float* decode_s_per_token, int32_t n_models,
+                                    int32_t n_nodes, const double* free_bytes, const float* queue_s,
+                                    const float* act_s, double rho, int32_t k, int32_t algo, int32_t* node_idx,
+                                    float* score, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!act_s) return MAESTRO_ERR_INVALID_ARG;
+  return route_checked(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes, free_bytes,
+                       queue_s, nullptr, nullptr, act_s, rho, k, algo, node_idx, score, workspace,
+                       workspace_bytes, stream);
 }
 
 maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pred_len,
@@ -200,13 +230,14 @@ maestro_status maestro_degradation_plans(int32_t n_nodes, const int32_t* engine_
 
 maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                                           const double* model_bytes, const double* tier_bw,
-                                          const float* tier_setup_ms, float* act_ms, void* stream) {
-  if (n_nodes < 0 || n_models < 1 || n_models > 64) return MAESTRO_ERR_INVALID_ARG;
-  if (!model_bytes || !tier_bw || !tier_setup_ms || !aligned(model_bytes, 8) || !aligned(tier_bw, 8) ||
-      !aligned(tier_setup_ms, 4))
+                                          const float* tier_setup, double unit, float* act, void* stream) {
+  if (n_nodes < 0 || n_models < 1 || n_models > 64 || !(unit > 0.0) || !isfinite(unit))
     return MAESTRO_ERR_INVALID_ARG;
-  if (n_nodes > 0 && (!tier || !act_ms || !aligned(act_ms, 4))) return MAESTRO_ERR_INVALID_ARG;
-  return maestro::launch_activation_latency(n_nodes, n_models, tier, model_bytes, tier_bw, tier_setup_ms, act_ms,
+  if (!model_bytes || !tier_bw || !tier_setup || !aligned(model_bytes, 8) || !aligned(tier_bw, 8) ||
+      !aligned(tier_setup, 4))
+    return MAESTRO_ERR_INVALID_ARG;
+  if (n_nodes > 0 && (!tier || !act || !aligned(act, 4))) return MAESTRO_ERR_INVALID_ARG;
+  return maestro::launch_activation_latency(n_nodes, n_models, tier, model_bytes, tier_bw, tier_setup, unit, act,
                                             as_stream(stream));
 }
 

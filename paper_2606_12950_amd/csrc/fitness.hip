@@ -471,13 +471,14 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
 }
 
 // T_act of every (node, model) from its readiness tier (Sec. III-C): 0 when Running, else the
-// tier's setup time plus Size / BW_tier, in float64 in that order, stored as float32.
+// tier's setup time plus Size / BW_tier in the caller's time unit (`unit` per second), in
+// float64 in that order, stored as float32.
 __global__ __launch_bounds__(kThreads) void activation_kernel(int64_t total, int32_t n_models,
                                                               const uint8_t* __restrict__ tier,
                                                               const double* __restrict__ model_bytes,
                                                               const double* __restrict__ tier_bw,
                                                               const float* __restrict__ tier_setup_ms,
-                                                              float* __restrict__ act_ms) {
+                                                              double unit, float* __restrict__ act_ms) {
   for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (int64_t)gridDim.x * kThreads) {
     int t = tier[e];
     t = t > 4 ? 4 : t;   // past Remote counts as Remote
@@ -485,19 +486,20 @@ __global__ __launch_bounds__(kThreads) void activation_kernel(int64_t total, int
     float a = 0.0f;
     if (t > 0)
       a = __double2float_rn(__dadd_rn((double)tier_setup_ms[t],
-                                      __dmul_rn(__ddiv_rn(model_bytes[m], tier_bw[t]), 1000.0)));
+                                      __dmul_rn(__ddiv_rn(model_bytes[m], tier_bw[t]), unit)));
     act_ms[e] = a;
   }
 }
 
 maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                                          const double* model_bytes, const double* tier_bw,
-                                         const float* tier_setup_ms, float* act_ms, hipStream_t stream) {
+                                         const float* tier_setup_ms, double unit, float* act_ms,
+                                         hipStream_t stream) {
   const int64_t total = (int64_t)n_nodes * n_models;
   if (total == 0) return MAESTRO_OK;
   const int64_t blocks = (total + kThreads - 1) / kThreads;
   activation_kernel<<<dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(kThreads), 0, stream>>>(
-      total, n_models, tier, model_bytes, tier_bw, tier_setup_ms, act_ms);
+      total, n_models, tier, model_bytes, tier_bw, tier_setup_ms, unit, act_ms);
   return launch_status();
 }
 

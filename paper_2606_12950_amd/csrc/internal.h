@@ -27,8 +27,8 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
                             const double* kv_bytes, const float* decode_s_per_token,
                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
                             const float* queue_s, const float* cold_s,
-                            const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
-                            int32_t* node_idx, float* score, void* workspace,
+                            const uint64_t* resident_mask, const float* act_matrix, double rho, int32_t k,
+                            int32_t algo, int32_t* node_idx, float* score, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
 size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);
 
@@ -48,7 +48,7 @@ maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_o
                                        maestro_deg_plan* plans, hipStream_t stream);
 maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                                          const double* model_bytes, const double* tier_bw,
-                                         const float* tier_setup_ms, float* act_ms, hipStream_t stream);
+                                         const float* tier_setup, double unit, float* act, hipStream_t stream);
 maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
                                    int64_t rank, float* ewma, float* rho, hipStream_t stream);
 maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,

@@ -18,7 +18,9 @@
 // walk is short unless many nodes are infeasible, and never longer than the node count.
 //
 // Arithmetic is the same expression, in the same order and precision, as the definition:
-// score = fl32(fl32(T_q + T_act) + fl32(L * t_dec)), with T_act in {0, cold}. The library is
+// score = fl32(fl32(T_q + T_act) + fl32(L * t_dec)), with T_act in {0, cold} -- or, with
+// readiness tiers, T_act from a [node][model] matrix (then the scan stages fl32(T_q + T_act)
+// of every (node, model) of a smaller node chunk). The library is
 // compiled with -ffp-contract=off and the products/sums below use explicit round-to-nearest
 // intrinsics, so nothing is fused or reassociated.
 #include <type_traits>
@@ -30,19 +32,27 @@ namespace maestro {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kNodeChunk = 1024;
-template <int KT, bool kMask64>
+// T_act: cold start unless resident (residency bits in 32 or 64 bits), or a [node][model] matrix
+enum Ready { kMask32 = 0, kMask64 = 1, kMatrix = 2 };
+constexpr int kMaxMatrixModels = 64;
+
+template <int KT, int kReady>
 __global__ __launch_bounds__(kThreads) void route_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
-    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token,
+    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_models,
     int32_t n_nodes, const double* __restrict__ free_bytes, const float* __restrict__ queue_s,
-    const float* __restrict__ cold_s, const uint64_t* __restrict__ resident_mask, double rho,
-    int32_t k, int g_log2, int32_t* __restrict__ node_idx, float* __restrict__ score) {
-  typedef typename std::conditional<kMask64, uint64_t, uint32_t>::type mask_t;
-  __shared__ float s_warm[kNodeChunk];     // fl32(T_q + 0): ready time when the model is resident
-  __shared__ float s_cold[kNodeChunk];     // fl32(T_q + cold): ready time after a cold start
+    const float* __restrict__ cold_s, const uint64_t* __restrict__ resident_mask,
+    const float* __restrict__ act_matrix, double rho, int32_t k, int g_log2, int32_t* __restrict__ node_idx,
+    float* __restrict__ score) {
+  typedef typename std::conditional<kReady == kMask64, uint64_t, uint32_t>::type mask_t;
+  constexpr bool kMat = kReady == kMatrix;
+  constexpr int kNodeChunk = kMat ? 128 : 1024;
+  constexpr int kM = kMat ? 1 : kNodeChunk;
+  __shared__ float s_warm[kM];             // fl32(T_q + 0): ready time when the model is resident
+  __shared__ float s_cold[kM];             // fl32(T_q + cold): ready time after a cold start
+  __shared__ mask_t s_mask[kM];            // residency bits
   __shared__ double s_free[kNodeChunk];    // KV admission headroom
-  __shared__ mask_t s_mask[kNodeChunk];    // residency bits
+  __shared__ float s_ready[kMat ? kNodeChunk * kMaxMatrixModels : 1];   // fl32(T_q + T_act[j][m])
 
   const int tid = threadIdx.x;
   const int G = 1 << g_log2;
@@ -53,11 +63,12 @@ __global__ __launch_bounds__(kThreads) void route_kernel(
   double need = INFINITY;   // an invalid lane admits nothing
   float exec_s = 0.0f;
   mask_t mbit = 0;
+  int32_t model = 0;
   if (valid) {
-    const int32_t m = model_id[stage];
+    model = model_id[stage];
     need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
-    exec_s = __fmul_rn(pred_len[stage], decode_s_per_token[m]);
-    mbit = (mask_t)1 << m;
+    exec_s = __fmul_rn(pred_len[stage], decode_s_per_token[model]);
+    mbit = kMat ? 0 : (mask_t)1 << model;
   }
 
   TopK<KT> best;
@@ -67,16 +78,24 @@ __global__ __launch_bounds__(kThreads) void route_kernel(
     __syncthreads();  // every lane is done with the previous chunk
     for (int i = tid; i < cn; i += kThreads) {
       const int32_t j = c0 + i;
-      const float q = queue_s[j];
-      s_warm[i] = __fadd_rn(q, 0.0f);
-      s_cold[i] = __fadd_rn(q, cold_s[j]);
       s_free[i] = free_bytes[j];
-      s_mask[i] = (mask_t)resident_mask[j];
+      if constexpr (!kMat) {
+        const float q = queue_s[j];
+        s_warm[i] = __fadd_rn(q, 0.0f);
+        s_cold[i] = __fadd_rn(q, cold_s[j]);
+        s_mask[i] = (mask_t)resident_mask[j];
+      }
+    }
+    if constexpr (kMat) {   // rows c0 .. c0+cn-1 of the matrix are contiguous
+      const float* rows = act_matrix + (size_t)c0 * n_models;
+      for (int e = tid; e < cn * n_models; e += kThreads) s_ready[e] = __fadd_rn(queue_s[c0 + e / n_models], rows[e]);
     }
     __syncthreads();
 #pragma unroll 4
     for (int i = g; i < cn; i += G) {
-      const float ready = (s_mask[i] & mbit) ? s_warm[i] : s_cold[i];
+      float ready;
+      if constexpr (kMat) ready = s_ready[i * n_models + model];
+      else ready = (s_mask[i] & mbit) ? s_warm[i] : s_cold[i];
       const float sc = __fadd_rn(ready, exec_s);
       if (need <= s_free[i]) best.push_increasing(sc, c0 + i);
     }
@@ -108,19 +127,19 @@ __global__ __launch_bounds__(kThreads) void route_kernel(
 }
 
 template <int KT>
-void launch_kt(bool mask64, dim3 grid, hipStream_t stream, int64_t n, const int32_t* model_id,
-               const float* pred_len, const double* kv_bytes, const float* dec, int32_t n_nodes,
+void launch_kt(int ready, dim3 grid, hipStream_t stream, int64_t n, const int32_t* model_id,
+               const float* pred_len, const double* kv_bytes, const float* dec, int32_t n_models, int32_t n_nodes,
                const double* free_bytes, const float* queue_s, const float* cold_s,
-               const uint64_t* mask, double rho, int32_t k, int g_log2, int32_t* node_idx,
+               const uint64_t* mask, const float* act_matrix, double rho, int32_t k, int g_log2, int32_t* node_idx,
                float* score) {
-  if (mask64)
-    route_kernel<KT, true><<<grid, dim3(kThreads), 0, stream>>>(
-        n, model_id, pred_len, kv_bytes, dec, n_nodes, free_bytes, queue_s, cold_s, mask, rho, k,
-        g_log2, node_idx, score);
-  else
-    route_kernel<KT, false><<<grid, dim3(kThreads), 0, stream>>>(
-        n, model_id, pred_len, kv_bytes, dec, n_nodes, free_bytes, queue_s, cold_s, mask, rho, k,
-        g_log2, node_idx, score);
+#define MAESTRO_ROUTE_RD(RD)                                                                               \
+  route_kernel<KT, RD><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes, dec, n_models, \
+                                                           n_nodes, free_bytes, queue_s, cold_s, mask,     \
+                                                           act_matrix, rho, k, g_log2, node_idx, score)
+  if (ready == kMatrix) MAESTRO_ROUTE_RD(kMatrix);
+  else if (ready == kMask64) MAESTRO_ROUTE_RD(kMask64);
+  else MAESTRO_ROUTE_RD(kMask32);
+#undef MAESTRO_ROUTE_RD
 }
 
 // Lanes per stage: enough threads to fill the chip (about 2^18), at least 4 nodes per lane.
@@ -144,16 +163,21 @@ struct NodeEntry {                        // 16 bytes: one node in a model's rea
 };
 
 __global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
-    int32_t n_nodes, int32_t padded, const float* __restrict__ queue_s, const float* __restrict__ cold_s,
-    const uint64_t* __restrict__ resident_mask, const double* __restrict__ free_bytes,
-    NodeEntry* __restrict__ lists) {
+    int32_t n_nodes, int32_t padded, int32_t n_models, const float* __restrict__ queue_s,
+    const float* __restrict__ cold_s, const uint64_t* __restrict__ resident_mask,
+    const float* __restrict__ act_matrix, const double* __restrict__ free_bytes, NodeEntry* __restrict__ lists) {
   __shared__ uint64_t key[kSortMax];
   const int m = blockIdx.x, tid = threadIdx.x;
   for (int i = tid; i < padded; i += kSortThreads) {
     if (i < n_nodes) {
-      const bool res = (resident_mask[i] >> m) & 1u;
       const float q = queue_s[i];
-      const float ready = res ? __fadd_rn(q, 0.0f) : __fadd_rn(q, cold_s[i]);
+      float ready;
+      if (act_matrix) {
+        ready = __fadd_rn(q, act_matrix[(size_t)i * n_models + m]);
+      } else {
+        const bool res = (resident_mask[i] >> m) & 1u;
+        ready = res ? __fadd_rn(q, 0.0f) : __fadd_rn(q, cold_s[i]);
+      }
       key[i] = ((uint64_t)float_key(ready) << 32) | (uint32_t)i;
     } else {
       key[i] = ~0ull;                     // padding sorts last
@@ -235,7 +259,7 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
                             const double* kv_bytes, const float* decode_s_per_token,
                             int32_t n_models, int32_t n_nodes, const double* free_bytes,
                             const float* queue_s, const float* cold_s,
-                            const uint64_t* resident_mask, double rho, int32_t k, int32_t algo,
+                            const uint64_t* resident_mask, const float* act_matrix, double rho, int32_t k, int32_t algo,
                             int32_t* node_idx, float* score, void* workspace,
                             size_t workspace_bytes, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
@@ -250,7 +274,7 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
     int padded = 1;
     while (padded < n_nodes) padded <<= 1;
     sort_nodes_kernel<<<dim3(n_models), dim3(kSortThreads), 0, stream>>>(
-        n_nodes, padded, queue_s, cold_s, resident_mask, free_bytes, lists);
+        n_nodes, padded, n_models, queue_s, cold_s, resident_mask, act_matrix, free_bytes, lists);
     const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
 #define MAESTRO_WALK_KT(KT)                                                                          walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,                                                                  decode_s_per_token, n_nodes, lists, rho,                                                             k, node_idx, score)
     if (k == 1) MAESTRO_WALK_KT(1);
@@ -265,10 +289,10 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
   const int gl = choose_g_log2(n, n_nodes);
   const int64_t stages_per_block = kThreads >> gl;
   const dim3 grid((unsigned)((n + stages_per_block - 1) / stages_per_block));
-  const bool mask64 = n_models > 32;
-#define MAESTRO_ROUTE_KT(KT)                                                                   \
-  launch_kt<KT>(mask64, grid, stream, n, model_id, pred_len, kv_bytes, decode_s_per_token,     \
-                n_nodes, free_bytes, queue_s, cold_s, resident_mask, rho, k, gl, node_idx, score)
+  const int ready = act_matrix ? kMatrix : (n_models > 32 ? kMask64 : kMask32);
+#define MAESTRO_ROUTE_KT(KT)                                                                          \
+  launch_kt<KT>(ready, grid, stream, n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models,   \
+                n_nodes, free_bytes, queue_s, cold_s, resident_mask, act_matrix, rho, k, gl, node_idx, score)
   if (k <= 1) MAESTRO_ROUTE_KT(1);
   else if (k <= 2) MAESTRO_ROUTE_KT(2);
   else if (k <= 4) MAESTRO_ROUTE_KT(4);

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -140,6 +140,18 @@ def test_route_validation(lib):
     assert call(free=MISALIGNED) == INVALID
 
 
+def test_route_tiered_validation(lib):
+    def call(n=10, n_models=8, n_nodes=16, k=1, act=FAKE, algo=0, ws=None, ws_bytes=0):
+        return lib.maestro_route_tiered(n, FAKE, FAKE, FAKE, FAKE, n_models, n_nodes, FAKE, FAKE, act, 0.0, k, algo,
+                                        FAKE, FAKE, ws, ws_bytes, None)
+    assert call(act=None) == INVALID                                          # T_act from nowhere
+    assert call(act=MISALIGNED4) == INVALID
+    assert call(n_models=65) == INVALID
+    assert call(k=17) == INVALID
+    assert call(algo=2) == WORKSPACE                                          # sorted lists need room
+    assert call(n=0, algo=1) == OK                                           # empty batch, scan: no-op
+
+
 def test_route_fitness_and_quantiles_validation(lib):
     def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE,
              deg=FAKE, plans=None, act=FAKE, mask=FAKE, mat=None):
@@ -179,8 +191,8 @@ def test_route_fitness_and_quantiles_validation(lib):
 
 
 def test_activation_latency_validation(lib):
-    def call(M=4, K=3, tier=FAKE, size=FAKE, bw=FAKE, setup=FAKE, out=FAKE):
-        return lib.maestro_activation_latency(M, K, tier, size, bw, setup, out, None)
+    def call(M=4, K=3, tier=FAKE, size=FAKE, bw=FAKE, setup=FAKE, out=FAKE, unit=1000.0):
+        return lib.maestro_activation_latency(M, K, tier, size, bw, setup, unit, out, None)
     assert call(M=-1) == INVALID
     assert call(K=0) == INVALID
     assert call(K=65) == INVALID
@@ -188,6 +200,8 @@ def test_activation_latency_validation(lib):
     assert call(size=MISALIGNED) == INVALID
     assert call(bw=None) == INVALID
     assert call(out=MISALIGNED4) == INVALID
+    assert call(unit=0.0) == INVALID
+    assert call(unit=float("inf")) == INVALID
     assert call(M=0, tier=None, out=None) == OK                               # no nodes: no-op
 
 

@@ -315,6 +315,63 @@ def test_prioritize_adversarial_keys():
             assert np.array_equal(got[2], np.arange(W_))
 
 
+def gpu_route_tiered(w, pred, kv, act_s, k=None, rho=None, free=None, algo=0):
+    t = lambda a: pipeline._t(a, "cuda")
+    k = w.spec.k if k is None else k
+    rho = w.spec.rho if rho is None else rho
+    free = w.free_bytes if free is None else free
+    idx, sc = M.route(t(w.model_id), t(pred), t(kv), t(w.decode_s_per_token), t(free), t(w.queue_s), None, None,
+                      k=k, rho=rho, algo=algo, act_s=t(act_s))
+    torch.cuda.synchronize()
+    ref = oracle.route(w.model_id, pred, kv, w.decode_s_per_token, free, w.queue_s, w.cold_s, w.resident_mask,
+                       k=k, rho=rho, act_matrix=act_s)
+    return (_np(idx), _np(sc)), ref
+
+
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
+@pytest.mark.parametrize("name", ["c1", "c3"])
+def test_route_tiered_full(name, algo):
+    # T_act(N, M(T)) of Eq. 6 from readiness tiers (seconds), both algorithms, every stage
+    w = wl(name)
+    r = W.readiness_inputs(w)
+    act = M.activation_latency(pipeline._t(r.tier, "cuda"), pipeline._t(r.model_bytes, "cuda"),
+                               pipeline._t(r.tier_bw, "cuda"),
+                               pipeline._t((r.tier_setup_ms / np.float32(1000)).astype(np.float32), "cuda"), unit=1.0)
+    torch.cuda.synchronize()
+    act = _np(act)
+    assert np.array_equal(act.view(np.uint32), oracle.activation_latency(
+        r.tier, r.model_bytes, r.tier_bw, (r.tier_setup_ms / np.float32(1000)).astype(np.float32), unit=1.0).view(np.uint32))
+    pred, kv, _, _ = gpu_predict(w)
+    got, ref = gpu_route_tiered(w, pred, kv, act, algo=ALGOS[algo])
+    assert_route_equal(got, ref)
+
+
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
+@pytest.mark.parametrize("n,M_,K,k", [(1, 1, 1, 1), (500, 129, 64, 3), (3000, 1100, 33, 4), (777, 2049, 16, 16)])
+def test_route_tiered_shapes(n, M_, K, k, algo):
+    # ragged node chunks (128 per chunk for the scan), up to 64 models, tie-prone coarse values
+    rng = np.random.default_rng(n + M_ + K)
+    w = wl("c0", n_stages=n, n_nodes=M_, n_models=K)
+    act = np.round(rng.uniform(0, 30, (M_, K)), 0).astype(np.float32)
+    act[rng.random((M_, K)) < 0.3] = 0.0
+    pred, kv, _, _ = gpu_predict(w)
+    got, ref = gpu_route_tiered(w, pred, kv, act, k=k, free=w.free_bytes / 4.0, algo=ALGOS[algo])
+    assert_route_equal(got, ref)
+
+
+def test_route_tiered_of_resident_bits_equals_route():
+    # a {0, cold} matrix routes exactly like the residency bits on the GPU too
+    w = wl("c1")
+    pred, kv, _, _ = gpu_predict(w)
+    K = w.spec.n_models
+    bits = (w.resident_mask[:, None] >> np.arange(K, dtype=np.uint64)[None, :]) & np.uint64(1)
+    act = np.where(bits == 1, 0.0, w.cold_s[:, None]).astype(np.float32)
+    for algo in ALGOS.values():
+        got, _ = gpu_route_tiered(w, pred, kv, act, algo=algo)
+        plain, _ = gpu_route(w, pred, kv, algo=algo)
+        assert_route_equal(got, plain)
+
+
 def test_route_sorted_rejects_too_many_nodes():
     w = wl("c1", n_stages=10, n_nodes=8193, with_x=False)
     pred = np.full(10, 100.0, np.float32)
