@@ -8,6 +8,7 @@ python bench.py --route-fitness --plans   (the same with C_deg from degradation 
 python bench.py --route-fitness --readiness  (T_act per (node, model) from readiness tiers, Sec. III-C)
 python bench.py --two-phase            (the two-phase predictor, Sec. III-B, beside the bins one)
 python bench.py --margin               (the adaptive safety margin rho, Sec. III-D, over windows)
+python bench.py --route-tiered         (latency routing with T_act from readiness tiers beside the plain route)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
 scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
@@ -289,6 +290,37 @@ def two_phase_bench(name: str, steps: int, warmup: int):
     print(json.dumps(res), flush=True)
 
 
+def route_tiered_bench(name: str, steps: int, warmup: int):
+    """Latency routing (Alg. 3, Eq. 6) with T_act per (node, model) from readiness tiers beside the
+    resident-bit route, on the workload's own predictions, interleaved. One JSON line."""
+    import torch
+    from paper_2606_12950_amd import _native, pipeline
+    from paper_2606_12950_amd import workload as W
+    torch.cuda.set_device(0)
+    wl = W.workload(name)
+    r = W.readiness_inputs(wl)
+    b = pipeline.to_device(wl)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    t = lambda a: pipeline._t(a, "cuda")
+    rin = [t(r.tier), t(r.model_bytes), t(r.tier_bw), t((r.tier_setup_ms / np.float32(1000)).astype(np.float32))]
+    act = _native.activation_latency(*rin, unit=1.0)
+    da = _time_events(lambda: _native.activation_latency(*rin, out=act, unit=1.0), steps, warmup)
+    n, k = wl.n, wl.spec.k
+    out = (torch.empty((n, k), dtype=torch.int32, device="cuda"), torch.empty((n, k), dtype=torch.float32, device="cuda"))
+    ws = o.route_workspace
+    tiered = lambda: _native.route(b.model_id, o.pred_len, o.kv_bytes, b.decode_s_per_token, b.free_bytes, b.queue_s,
+                                   None, None, k=k, rho=wl.spec.rho, out=out, workspace=ws, act_s=act)
+    plain = lambda: pipeline.run_route(b, o)
+    d_t = _time_events(tiered, steps, warmup) + _time_events(tiered, steps, 0)
+    d_p = _time_events(plain, steps, warmup) + _time_events(plain, steps, 0)
+    res = {"route_tiered": name, "n_stages": n, "n_nodes": wl.spec.n_nodes, "n_models": wl.spec.n_models, "k": k,
+           "activation_ms": percentiles(da), "tiered_ms": percentiles(d_t), "plain_ms": percentiles(d_p),
+           "tiered_stages_per_s": n / (float(np.mean(d_t)) * 1e-3),
+           "routed_frac": float((out[0][:, 0] >= 0).float().mean().item())}
+    print(json.dumps(res), flush=True)
+
+
 def margin_bench(steps: int, warmup: int):
     """The adaptive safety margin (EWMA of the relative underestimation, then its high quantile)
     over windows of recent stages. Latency-bound: one workgroup per kernel. One JSON line."""
@@ -324,12 +356,17 @@ def main():
     ap.add_argument("--readiness", action="store_true",
                     help="with --route-fitness: T_act per (node, model) from readiness tiers (Sec. III-C)")
     ap.add_argument("--margin", action="store_true", help="time the adaptive safety margin (Sec. III-D)")
+    ap.add_argument("--route-tiered", action="store_true",
+                    help="time latency routing with T_act from readiness tiers (Sec. III-C, Eq. 6)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.route_tiered:
+        route_tiered_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
         return
     if args.margin:
         margin_bench(steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
