@@ -68,10 +68,11 @@ def calibrate_copy(mib: int, reps: int = 5):
     dst = torch.empty_like(src)
     src.fill_(1)
     torch.cuda.synchronize()
-    for _ in range(reps):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    print(json.dumps({"calibration_copy_bytes": mib << 20, "reps": reps}), flush=True)
+    d = _time_events(lambda: dst.copy_(src), reps, 1)
+    ms = float(np.median(d))
+    gbs = 2 * (mib << 20) / (ms * 1e-3) / 1e9   # bytes read + bytes written
+    print(json.dumps({"calibration_copy_bytes": mib << 20, "reps": reps, "copy_ms": round(ms, 4),
+                      "copy_gbs": round(gbs, 1), "of_peak": round(gbs / PEAK_HBM_GBS, 4)}), flush=True)
 
 
 def mlp_flop_per_stage(dims):
