@@ -190,6 +190,16 @@ def _time_events(call, steps: int, warmup: int):
     return [e0.elapsed_time(e1) for e0, e1 in ev]
 
 
+def oracle_timed(fn, units: int, unit: str, sample: str):
+    """The oracle on a bounded sample, timed on the host cores: a cpu_baseline record."""
+    import oracle
+    t0 = time.perf_counter()
+    fn()
+    dt = time.perf_counter() - t0
+    return {"value": units / dt, "unit": unit, "cores": int(oracle.max_threads()), "kind": "oracle",
+            "sample": sample, "seconds": round(dt, 3), "cpu_model": cpu_model()}
+
+
 def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False, readiness: bool = False):
     """Routing by fitness over the workload's stages, on the GPU's own predictions; bounds from
     the recent-observation windows (maestro_quantiles). With ``plans`` C_deg comes from the
@@ -241,6 +251,20 @@ def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False,
         extra["short_pair_frac"] = round(float((need[:, None] > b.free_bytes[None, :]).float().mean().item()), 4)
     pairs = n * m
     achieved = pairs * FITNESS_OPS_PER_PAIR / (ms * 1e-3)
+    import oracle
+    S = min(n, max(256, 10_000_000_000 // m))   # the whole batch up to 10^10 pairs (seconds of oracle work)
+    kv = o.kv_bytes[:S].cpu().numpy()
+    eng = (e.engine_offset, e.level, e.freed_bytes, e.cost_ms, e.c_int_ms) if plans else None
+    am = None
+    if readiness:
+        am = oracle.activation_latency(r.tier, r.model_bytes, r.tier_bw, r.tier_setup_ms)
+    bnd = bounds.cpu().numpy()
+    extra["cpu_baseline"] = oracle_timed(
+        lambda: oracle.route_fitness(wl.model_id[:S], f.src_id[:S], f.class_id[:S], kv, wl.free_bytes, f.queue_ms,
+                                     f.act_ms, wl.resident_mask, f.deg_ms, f.rtt_ms, f.class_weights, bnd,
+                                     k=wl.spec.k, rho=wl.spec.rho, n_models=wl.spec.n_models, engines=eng,
+                                     act_matrix=am),
+        S, "stages/s", (f"all {S} stages" if S == n else f"first {S} stages") + f" x all {m} nodes, same inputs")
     print(json.dumps({"route_fitness": name, "n_stages": n, "n_nodes": m, "k": wl.spec.k, "ms": round(ms, 4),
                       "phase_ms": percentiles(d), "stages_per_s": n / (ms * 1e-3), "pairs_per_s": pairs / (ms * 1e-3),
                       "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_VALU_LANE_OPS / 1e12,
@@ -288,6 +312,14 @@ def two_phase_bench(name: str, steps: int, warmup: int):
                                  "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
     res["mean_p_tool"] = float(out[0].mean().item())
     res["mean_pred_len"] = float(out[1].mean().item())
+    import oracle
+    S = min(n, 65536)
+    res["cpu_baseline"] = oracle_timed(
+        lambda: oracle.predict_two_phase(wl.x[:S], wl.weights[:-1] + [tp.head_weight], wl.biases[:-1] + [tp.head_bias],
+                                         tp.role_head, tp.tool_coef, tp.iso_x, tp.iso_y, tp.max_len, wl.prompt_len[:S],
+                                         wl.model_id[:S], wl.role[:S], tp.tool_avail[:S], wl.kv_bytes_per_token,
+                                         wl.spec.dtype),
+        S, "stages/s", f"first {S} stages, same network and inputs")
     print(json.dumps(res), flush=True)
 
 
@@ -319,6 +351,14 @@ def route_tiered_bench(name: str, steps: int, warmup: int):
            "activation_ms": percentiles(da), "tiered_ms": percentiles(d_t), "plain_ms": percentiles(d_p),
            "tiered_stages_per_s": n / (float(np.mean(d_t)) * 1e-3),
            "routed_frac": float((out[0][:, 0] >= 0).float().mean().item())}
+    import oracle
+    S = min(n, max(256, 10_000_000_000 // wl.spec.n_nodes))
+    act_np = act.cpu().numpy()
+    pred, kv = o.pred_len[:S].cpu().numpy(), o.kv_bytes[:S].cpu().numpy()
+    res["cpu_baseline"] = oracle_timed(
+        lambda: oracle.route(wl.model_id[:S], pred, kv, wl.decode_s_per_token, wl.free_bytes, wl.queue_s, wl.cold_s,
+                             wl.resident_mask, k=k, rho=wl.spec.rho, act_matrix=act_np),
+        S, "stages/s", (f"all {S} stages" if S == n else f"first {S} stages") + f" x all {wl.spec.n_nodes} nodes, same inputs")
     print(json.dumps(res), flush=True)
 
 
@@ -336,6 +376,10 @@ def margin_bench(steps: int, warmup: int):
         out = _native.adaptive_rho(a, p, 0.2, 0.95)
         d = _time_events(lambda: _native.adaptive_rho(a, p, 0.2, 0.95, out=out), steps, warmup)
         res["windows"].append({"m": m, "ms": percentiles(d), "rho": float(out[1].item())})
+    import oracle
+    actual, pred = W.margin_window(3, 1 << 20)
+    res["cpu_baseline"] = oracle_timed(lambda: oracle.adaptive_rho(actual, pred, 0.2, 0.95), 1 << 20,
+                                       "stages/s", "the 2^20-stage window (sequential EWMA and sort)")
     print(json.dumps(res), flush=True)
 
 
