@@ -329,7 +329,47 @@ __device__ __forceinline__ void wait_chunk() {
 
 constexpr int kMaxModels = 64;           // per-model KV bytes staged in LDS
 
-template <int D, int H1, int H2, int B, bool kTwoPhase>
+// acc[g] += sum_k A_k * b[g][k0 + k] for the G row groups of a wavefront: every weight fragment
+// read from LDS feeds G MFMAs, one per group (independent accumulators), so the LDS reads, their
+// waits and the weight traffic per MFMA drop by a factor G. Fragment addressing, pre() and side(k)
+// as in mfma_chain; fragments are read kLookaheadGroups K-steps ahead.
+constexpr int kLookaheadGroups = 2;
+template <int KS, int G, int NBREG, typename Pre, typename Side>
+__device__ __forceinline__ void mfma_chain_groups(f32x16 (&acc)[G], const unsigned char* pa,
+                                                  const unsigned char* pb, const bf16x8 (&b)[G][NBREG], int k0,
+                                                  Pre&& pre, Side&& side) {
+  constexpr int LA = kLookaheadGroups;
+  bf16x8 fr[KS];
+#pragma unroll
+  for (int k = 0; k < LA && k < KS; ++k)
+    fr[k] = *reinterpret_cast<const bf16x8*>(((k & 4) ? pb : pa) + k * 32);
+  __builtin_amdgcn_sched_barrier(0);
+  pre();
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if (k + LA < KS) {
+      const int kk = k + LA;
+      fr[kk] = *reinterpret_cast<const bf16x8*>(((kk & 4) ? pb : pa) + kk * 32);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[k], b[g][k0 + k], acc[g], 0, 0, 0);
+    side(k);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int G>
+struct AccGroups {
+  f32x16 v[G];
+};
+
+// G = number of 32-row groups per wavefront. A tile is kWaves * 32 * G rows; the weights stream
+// through LDS once per tile, so G = 2 halves the weight traffic and the LDS fragment reads per
+// row. G = 2 needs both groups' layer-1 activations in the 256 accumulation registers, which
+// holds for H1 = 512.
+template <int D, int H1, int H2, int B, int G, bool kTwoPhase>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void mlp3_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w1, const uint16_t* __restrict__ w2,
@@ -340,8 +380,10 @@ void mlp3_bf16_kernel(
     double* __restrict__ kv_bytes, const TwoPhaseArgs tp) {
   static_assert(D == 256, "feature and layer-1 chunk layouts assume 512-byte rows");
   static_assert(H1 % 512 == 0 && H2 % 32 == 0 && B % 64 == 0, "tile shape");
+  static_assert(G == 1 || (G == 2 && H1 == 512), "two row groups need H1 = 512 (256 accumulation registers)");
+  constexpr int kTileRows = kWaves * kRowsPerWave * G;
   constexpr int KS1 = D / 16;             // K-steps of layer 1 (32x32x16 MFMA)
-  constexpr int NX = 2;                   // feature chunks per tile
+  constexpr int NX = 2 * G;               // feature chunks per tile (64 rows each)
   constexpr int NC1 = H1 / 64;            // layer-1 chunks (two neuron blocks each)
   constexpr int KP = H1 / 512;            // column parts of a layer-2 block
   constexpr int NB2 = H2 / 32;            // layer-2 neuron blocks
@@ -364,7 +406,7 @@ void mlp3_bf16_kernel(
   __shared__ __attribute__((aligned(16))) float s_alpha[kMaxModels];
   // [tile parity][prompt, model (, role, tool availability)][row]
   constexpr int kMeta = kTwoPhase ? 4 : 2;
-  __shared__ __attribute__((aligned(16))) int32_t s_meta[2][kMeta][kRowsPerBlock];
+  __shared__ __attribute__((aligned(16))) int32_t s_meta[2][kMeta][kTileRows];
   constexpr int kTab = kTwoPhase ? 64 : 1;   // two-phase tables: role heads, calibration knots
   __shared__ int32_t s_head[kTab];
   __shared__ float s_kx[kTab], s_ky[kTab];
@@ -390,28 +432,41 @@ void mlp3_bf16_kernel(
     const int rho = 2 * wave + h + 8 * p;
     voffx[p] = (uint32_t)((2 * wave + h) * D * 2 + (((lane & 31) ^ (rho & 15)) << 4));
   }
-  const uint32_t voffm = (uint32_t)((64 * (wave & 1) + lane) * 4);
-  // feature chunk j of tile t (rows of a partial tile past the last stage, and every row of a
-  // tile past the last, read as zeros and are never stored). Chunk 0 also brings the tile's
-  // prompt lengths (waves 0, 1) and model ids (waves 2, 3), 64 rows each.
-  auto fetch_x = [&](int64_t t, int j, const unsigned char* dst) {
+  // G = 2: feature chunk j is K-slice j instead (columns 64j .. 64j+63 of all 256 tile rows, 128
+  // bytes per row, the 16-byte unit u of row r stored at u ^ ((r / 2) % 8)), so that every
+  // wavefront reads its B operands from every feature chunk. A load brings 8 rows; lane l fills
+  // row l / 8, position l % 8, and since (r / 2) % 8 = 4 (i % 2) + l / 16 for row r = 8i + l / 8
+  // with i = wave + 4q, one offset per lane serves every load of the wavefront.
+  const uint32_t voffk =
+      (uint32_t)((lane >> 3) * D * 2 + (((lane & 7) ^ (4 * (wave & 1) + (lane >> 4))) << 4));
+  // The per-stage inputs (prompt lengths, model ids, and for the two-phase predictor role ids
+  // and tool availability) travel in 64-row pieces with the feature chunks: piece p = 4j + wave
+  // rides on feature chunk j and holds rows 64 (p % R) .. 64 (p % R) + 63 of input p / R
+  // (R = kTileRows / 64 pieces per input).
+  constexpr int kPiecesPerInput = kTileRows / 64;
+  static_assert(kMeta * kPiecesPerInput <= kWaves * NX, "every per-stage piece rides on a feature chunk");
+  // feature chunk j of tile t, whose per-stage inputs go to s_meta[par] (rows of a partial tile
+  // past the last stage, and every row of a tile past the last, read as zeros and are never
+  // stored)
+  auto fetch_x = [&](int64_t t, int par, int j, const unsigned char* dst) {
     const bool live = t < n_tiles;
-    const int64_t row0 = live ? t * kRowsPerBlock : 0;
-    const uint32_t rows = live ? (uint32_t)min<int64_t>(kRowsPerBlock, n - row0) : 0u;
+    const int64_t row0 = live ? t * kTileRows : 0;
+    const uint32_t rows = live ? (uint32_t)min<int64_t>(kTileRows, n - row0) : 0u;
     const i32x4 rs = buffer_rsrc(x + row0 * D, rows * (D * 2));
     const uint32_t base = lds_addr(dst) + wave * 1024;
 #pragma unroll
-    for (int q = 0; q < kDmaPerChunk; ++q)
-      dma16(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
-    if (j == 0) {
-      const int32_t* src = (wave < 2) ? prompt_len : model_id;
-      const int parity = (int)(((t - first_tile) / stride) & 1);
-      dma4(buffer_rsrc(src + row0, rows * 4), voffm, lds_addr(&s_meta[parity][wave >> 1][64 * (wave & 1)]));
-      if (kTwoPhase) {
-        const int32_t* src2 = (wave < 2) ? tp.role_id : tp.tool_avail;
-        dma4(buffer_rsrc(src2 + row0, rows * 4), voffm,
-             lds_addr(&s_meta[parity][2 + (wave >> 1)][64 * (wave & 1)]));
-      }
+    for (int q = 0; q < kDmaPerChunk; ++q) {
+      if constexpr (G == 1)
+        dma16(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
+      else   // rows 8i .. 8i+7, i = wave + 4q, of K-slice j
+        dma16(rs, voffk, (uint32_t)(8 * (wave + 4 * q) * D * 2 + 128 * j), base, q * kWaves * 1024);
+    }
+    const int piece = 4 * j + wave;
+    if (piece < kMeta * kPiecesPerInput) {
+      const int a = piece / kPiecesPerInput, rb = piece % kPiecesPerInput;
+      const int32_t* src = a == 0 ? prompt_len : a == 1 ? model_id : a == 2 ? tp.role_id : tp.tool_avail;
+      dma4(buffer_rsrc(src + row0, rows * 4), (uint32_t)((64 * rb + lane) * 4),
+           lds_addr(&s_meta[par][a][64 * rb]));
     }
   };
   // load q of layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units
@@ -434,9 +489,9 @@ void mlp3_bf16_kernel(
     }
   };
   // chunk c of tile t, all loads at once; c is a compile-time constant at every call site
-  auto fetch = [&](int64_t t, int c, const unsigned char* dst) {
+  auto fetch = [&](int64_t t, int par, int c, const unsigned char* dst) {
     if (c < NX) {
-      fetch_x(t, c, dst);
+      fetch_x(t, par, c, dst);
     } else {
 #pragma unroll
       for (int q = 0; q <= kDmaPerChunk; ++q) {
@@ -450,9 +505,9 @@ void mlp3_bf16_kernel(
   // feature chunk (no multiplications of its own to hide behind) goes out whole at step 0.
   constexpr int kSpread = 3;
   static_assert(kSpread * kDmaPerChunk < 32, "every load of a chunk issues within its 32 steps");
-  auto spread = [&](int64_t t, int c, const unsigned char* dst, int step) {
+  auto spread = [&](int64_t t, int par, int c, const unsigned char* dst, int step) {
     if (c < NX) {
-      if (step == 0) fetch_x(t, c, dst);
+      if (step == 0) fetch_x(t, par, c, dst);
     } else if (step % kSpread == 0 && step / kSpread <= kDmaPerChunk) {
       if (c < NX + NC1) load_l1(c - NX, step / kSpread, dst);
       else load_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, step / kSpread, dst);
@@ -471,7 +526,6 @@ void mlp3_bf16_kernel(
   }
   const int l2 = prow * ROW2 + h * 16;
   const int sw3 = (r32 >> 2) & 3;
-  const int xrow = 32 * (wave & 1) + r32; // this lane's row within its feature chunk
 
   for (int i = tid; i < H1; i += kThreads) s_b1[i] = b1[i];
   for (int i = tid; i < H2; i += kThreads) s_b2[i] = b2[i];
@@ -487,9 +541,9 @@ void mlp3_bf16_kernel(
   __syncthreads();
 
   // chunk g of this workgroup's stream lives in buffer g % kBufs
-  int g = 0;
+  unsigned g = 0;
 #pragma unroll
-  for (int c = 0; c < kBufs - 1; ++c) fetch(first_tile, c, lds + c * CHUNK);
+  for (int c = 0; c < kBufs - 1; ++c) fetch(first_tile, 0, c, lds + c * CHUNK);
   wait_chunk<kDmaPerChunk * (kBufs - 2)>();
 
   auto ahead = [&]() { return lds + ((g + kBufs - 1) % kBufs) * CHUNK; };
@@ -498,135 +552,233 @@ void mlp3_bf16_kernel(
     ++g;
   };
 
-  for (int64_t tile = first_tile; tile < n_tiles; tile += stride) {
-    const int parity = (int)(((tile - first_tile) / stride) & 1);
-
-    // ---- features of this tile: B operand of layer 1, natural K order -------------------
-    bf16x8 xf[KS1];
+  int parity = 0;                         // tiles of this workgroup alternate s_meta halves
+  for (int64_t tile = first_tile; tile < n_tiles; tile += stride, parity ^= 1) {
+    // ---- features of this tile: B operands of layer 1, natural K order; group gr of this
+    // wavefront is tile rows 32 (G wave + gr) .. + 31
+    bf16x8 xf[G][KS1];
 #pragma unroll
     for (int c = 0; c < NX; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      fetch(tile, c + kBufs - 1, ahead());
-      if ((wave >> 1) == c) {
+      fetch(tile, parity, c + kBufs - 1, ahead());
+      if constexpr (G == 1) {
+        if ((wave >> 1) == c) {
+          const int xrow = 32 * (wave & 1) + r32;   // this lane's row within the chunk
 #pragma unroll
-        for (int ks = 0; ks < KS1; ++ks)
-          xf[ks] = *reinterpret_cast<const bf16x8*>(buf + xrow * 512 + (((2 * ks + h) ^ (xrow & 15)) << 4));
+          for (int ks = 0; ks < KS1; ++ks)
+            xf[0][ks] = *reinterpret_cast<const bf16x8*>(buf + xrow * 512 + (((2 * ks + h) ^ (xrow & 15)) << 4));
+        }
+      } else {
+        // K-steps 4c .. 4c+3 of both groups from K-slice c
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr) {
+          const int xrow = (G * wave + gr) * kRowsPerWave + r32;   // this lane's tile row
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk)
+            xf[gr][4 * c + kk] = *reinterpret_cast<const bf16x8*>(
+                buf + xrow * 128 + (((2 * kk + h) ^ ((xrow >> 1) & 7)) << 4));
+        }
       }
       advance();
     }
 
-    // ---- layer 1: H1 = relu(W1 x + b1), kept as the B operand of layer 2 ---------------
-    // Each block's ReLU is deferred into the next block's chain (the last one into the first
-    // layer-2 block). The activations live in the accumulation registers, which MFMA reads as
-    // its B operand directly, leaving the architectural registers to everything else.
-    bf16x8 h1[H1 / 16];
-    f32x16 prev0, prev1;                  // finished accumulators of the previous chunk
-    auto l1_relu = [&](int nb, const f32x16& acc) {
+    f32x16 logit[G][BT];                  // zeroed once layer 1 is done
+    auto zero_logits = [&]() {
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        h1[2 * nb + half] = relu_bf16(acc, half);
-        asm volatile("" : "+a"(h1[2 * nb + half]));
-      }
+      for (int gr = 0; gr < G; ++gr)
+#pragma unroll
+        for (int bt = 0; bt < BT; ++bt) logit[gr][bt] = f32x16{};
     };
-#pragma unroll
-    for (int c = 0; c < NC1; ++c) {
-      const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      const unsigned char* dst = ahead();
-      f32x16 acc0 = bias_acc(s_b1 + (2 * c) * 32, h);
-      f32x16 acc1 = bias_acc(s_b1 + (2 * c + 1) * 32, h);
-      mfma_chain_pair<KS1, KS1>(
-          acc0, acc1, buf + l1a[0], buf + l1b[0], buf + l1a[1], buf + l1b[1], xf,
-          [&]() {
-            if (c > 0) {
-              l1_relu(2 * c - 2, prev0);
-              l1_relu(2 * c - 1, prev1);
-            }
-          },
-          [&](int f) { spread(tile, NX + c + kBufs - 1, dst, f); });
-      prev0 = acc0;
-      prev1 = acc1;
-      __builtin_amdgcn_sched_barrier(0);
-      advance();
-    }
-
-    // ---- layer 2 block by block, each block folded straight into the logits. The last
-    // blocks, whose prefetches reach into the next tile, are peeled off the loop so that its
-    // body only ever fetches layer-2 chunks ---------------------------------------------------
-    // The epilogue of each block -- ReLU and the 2 BT MFMAs that fold its 32 neurons into the
-    // logits -- is deferred into the start of the next block's chain, where it covers the
-    // latency of that chain's first fragment reads; the block's W3 fragments are read into
-    // registers before the barrier that lets its buffer be refilled.
-    f32x16 logit[BT];
-#pragma unroll
-    for (int bt = 0; bt < BT; ++bt) logit[bt] = f32x16{};
-    bf16x8 w3f[BT][2];                    // W3 fragments of the previous block
-    auto l2_epilogue = [&](const f32x16& prev) {
-      bf16x8 h2[2];
-#pragma unroll
-      for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(prev, half);
+    bf16x8 w3f[BT][2];                    // W3 fragments of the previous layer-2 block
+    auto read_w3 = [&](const unsigned char* buf) {
 #pragma unroll
       for (int bt = 0; bt < BT; ++bt)
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
-          logit[bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[bt], 0, 0, 0);
+          w3f[bt][tt] = *reinterpret_cast<const bf16x8*>(
+              buf + W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4));
     };
-    // block b; pre(prev) is the deferred epilogue of the block before it
-    auto l2_block = [&](int b, const f32x16& prev, auto&& pre, auto&& load_ahead) {
-      f32x16 acc = bias_acc(s_b2 + b * 32, h);
+    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied;
+    // the last kPeel blocks, whose prefetches reach into the next tile, are peeled off the loop
+    constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
+    constexpr int kSteady = NB2 - kPeel - 1;
+    static_assert(kSteady >= 2, "at least one pair of blocks in the steady-state loop");
+    auto in_tile = [&](int j, const unsigned char* dst, int k) { spread(tile, parity, NX + NC1 + j, dst, k); };
+    auto wrapping = [&](int j, const unsigned char* dst, int k) {
+      if (j < NB2 * KP) spread(tile, parity, NX + NC1 + j, dst, k);
+      else spread(tile + stride, parity ^ 1, j - NB2 * KP, dst, k);
+    };
+
+    if constexpr (G == 1) {
+      // ---- layer 1: H1 = relu(W1 x + b1), kept as the B operand of layer 2 ---------------
+      // Each block's ReLU is deferred into the next block's chain (the last one into the first
+      // layer-2 block). The activations live in the accumulation registers, which MFMA reads as
+      // its B operand directly, leaving the architectural registers to everything else.
+      bf16x8 h1[H1 / 16];
+      f32x16 prev0, prev1;                  // finished accumulators of the previous chunk
+      auto l1_relu = [&](int nb, const f32x16& acc) {
 #pragma unroll
-      for (int part = 0; part < KP; ++part) {
+        for (int half = 0; half < 2; ++half) {
+          h1[2 * nb + half] = relu_bf16(acc, half);
+          asm volatile("" : "+a"(h1[2 * nb + half]));
+        }
+      };
+#pragma unroll
+      for (int c = 0; c < NC1; ++c) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
         const unsigned char* dst = ahead();
-        mfma_chain<32, H1 / 16>(
-            acc, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(prev); },
-            [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
-        if (part == KP - 1) {
+        f32x16 acc0 = bias_acc(s_b1 + (2 * c) * 32, h);
+        f32x16 acc1 = bias_acc(s_b1 + (2 * c + 1) * 32, h);
+        mfma_chain_pair<KS1, KS1>(
+            acc0, acc1, buf + l1a[0], buf + l1b[0], buf + l1a[1], buf + l1b[1], xf[0],
+            [&]() {
+              if (c > 0) {
+                l1_relu(2 * c - 2, prev0);
+                l1_relu(2 * c - 1, prev1);
+              }
+            },
+            [&](int f) { spread(tile, parity, NX + c + kBufs - 1, dst, f); });
+        prev0 = acc0;
+        prev1 = acc1;
+        __builtin_amdgcn_sched_barrier(0);
+        advance();
+      }
+
+      // ---- layer 2 block by block, each block folded straight into the logits ----------------
+      // The epilogue of each block -- ReLU and the 2 BT MFMAs that fold its 32 neurons into the
+      // logits -- is deferred into the start of the next block's chain, where it covers the
+      // latency of that chain's first fragment reads; the block's W3 fragments are read into
+      // registers before the barrier that lets its buffer be refilled.
+      zero_logits();
+      auto l2_epilogue = [&](const f32x16& prev) {
+        bf16x8 h2[2];
 #pragma unroll
-          for (int bt = 0; bt < BT; ++bt)
+        for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(prev, half);
 #pragma unroll
-            for (int tt = 0; tt < 2; ++tt)
-              w3f[bt][tt] = *reinterpret_cast<const bf16x8*>(
-                  buf + W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4));
+        for (int bt = 0; bt < BT; ++bt)
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt)
+            logit[0][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[0][bt], 0, 0, 0);
+      };
+      // block b; pre(prev) is the deferred epilogue of the block before it
+      auto l2_block = [&](int b, const f32x16& prev, auto&& pre, auto&& load_ahead) {
+        f32x16 acc = bias_acc(s_b2 + b * 32, h);
+#pragma unroll
+        for (int part = 0; part < KP; ++part) {
+          const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+          const unsigned char* dst = ahead();
+          mfma_chain<32, H1 / 16>(
+              acc, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(prev); },
+              [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
+          if (part == KP - 1) read_w3(buf);
+          __builtin_amdgcn_sched_barrier(0);
+          advance();
+        }
+        return acc;
+      };
+      // Block 0 finishes layer 1; blocks 1 .. NB2-kPeel-1 run in a loop over pairs, so that the
+      // two accumulators alternate roles without copies.
+      f32x16 carry = l2_block(0, prev1, [&](const f32x16& p) {
+        l1_relu(H1 / 32 - 2, prev0);
+        l1_relu(H1 / 32 - 1, p);
+      }, in_tile);
+      for (int b = 1; b + 1 <= kSteady; b += 2) {
+        const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile);
+        carry = l2_block(b + 1, a, l2_epilogue, in_tile);
+      }
+      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
+#pragma unroll
+      for (int b = NB2 - kPeel; b < NB2; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping);
+      l2_epilogue(carry);
+    } else {
+      // ---- layer 1, G groups: one 32-neuron block at a time (two per chunk), each block's
+      // ReLU deferred into the next block's chain; activations in the accumulation registers
+      bf16x8 h1[G][H1 / 16];
+      auto l1_relu = [&](int nb, const AccGroups<G>& acc) {
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr)
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            h1[gr][2 * nb + half] = relu_bf16(acc.v[gr], half);
+            asm volatile("" : "+a"(h1[gr][2 * nb + half]));
+          }
+      };
+      AccGroups<G> prev;
+#pragma unroll
+      for (int c = 0; c < NC1; ++c) {
+        const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+        const unsigned char* dst = ahead();
+#pragma unroll
+        for (int lb = 0; lb < 2; ++lb) {
+          const int nb = 2 * c + lb;
+          AccGroups<G> acc;
+#pragma unroll
+          for (int gr = 0; gr < G; ++gr) acc.v[gr] = bias_acc(s_b1 + nb * 32, h);
+          mfma_chain_groups<KS1, G, KS1>(
+              acc.v, buf + l1a[lb], buf + l1b[lb], xf, 0, [&]() { if (nb > 0) l1_relu(nb - 1, prev); },
+              [&](int k) { spread(tile, parity, NX + c + kBufs - 1, dst, KS1 * lb + k); });
+          prev = acc;
         }
         __builtin_amdgcn_sched_barrier(0);
         advance();
       }
-      return acc;
-    };
-    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied.
-    // Block 0 finishes layer 1; blocks 1 .. NB2-kPeel-1 run in a loop over pairs, so that the
-    // two accumulators alternate roles without copies; the last kPeel blocks, whose prefetches
-    // reach into the next tile, are peeled.
-    constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
-    constexpr int kSteady = NB2 - kPeel - 1;
-    static_assert(kSteady >= 2, "at least one pair of blocks in the steady-state loop");
-    auto in_tile = [&](int j, const unsigned char* dst, int k) { spread(tile, NX + NC1 + j, dst, k); };
-    f32x16 carry = l2_block(0, prev1, [&](const f32x16& p) {
-      l1_relu(H1 / 32 - 2, prev0);
-      l1_relu(H1 / 32 - 1, p);
-    }, in_tile);
-    for (int b = 1; b + 1 <= kSteady; b += 2) {
-      const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile);
-      carry = l2_block(b + 1, a, l2_epilogue, in_tile);
-    }
-    if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
-#pragma unroll
-    for (int b = NB2 - kPeel; b < NB2; ++b)
-      carry = l2_block(b, carry, l2_epilogue, [&](int j, const unsigned char* dst, int k) {
-        if (j < NB2 * KP) spread(tile, NX + NC1 + j, dst, k);
-        else spread(tile + stride, j - NB2 * KP, dst, k);
-      });
-    l2_epilogue(carry);
 
-    const int local = wave * kRowsPerWave + r32;
-    const int64_t row = tile * kRowsPerBlock + local;
-    if constexpr (kTwoPhase)
-      two_phase_epilogue<BT>(logit, s_b3, s_c, s_head, s_kx, s_ky, tp, h, row, n, s_meta[parity][0][local],
-                             s_meta[parity][1][local], s_meta[parity][2][local], s_meta[parity][3][local], s_alpha,
-                             pred_len, kv_bytes);
-    else
-      length_epilogue<BT>(logit, s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
-                          s_alpha, pred_len, kv_bytes);
+      // ---- layer 2, G groups; epilogues deferred as for G = 1 --------------------------------
+      zero_logits();
+      auto l2_epilogue = [&](const AccGroups<G>& p) {
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr) {
+          bf16x8 h2[2];
+#pragma unroll
+          for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(p.v[gr], half);
+#pragma unroll
+          for (int bt = 0; bt < BT; ++bt)
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt)
+              logit[gr][bt] =
+                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[gr][bt], 0, 0, 0);
+        }
+      };
+      auto l2_block = [&](int b, const AccGroups<G>& p, auto&& pre, auto&& load_ahead) {
+        AccGroups<G> acc;
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr) acc.v[gr] = bias_acc(s_b2 + b * 32, h);
+#pragma unroll
+        for (int part = 0; part < KP; ++part) {
+          const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+          const unsigned char* dst = ahead();
+          mfma_chain_groups<32, G, H1 / 16>(
+              acc.v, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(p); },
+              [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
+          if (part == KP - 1) read_w3(buf);
+          __builtin_amdgcn_sched_barrier(0);
+          advance();
+        }
+        return acc;
+      };
+      AccGroups<G> carry = l2_block(0, prev, [&](const AccGroups<G>& p) { l1_relu(H1 / 32 - 1, p); }, in_tile);
+      for (int b = 1; b + 1 <= kSteady; b += 2) {
+        const AccGroups<G> a = l2_block(b, carry, l2_epilogue, in_tile);
+        carry = l2_block(b + 1, a, l2_epilogue, in_tile);
+      }
+      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
+#pragma unroll
+      for (int b = NB2 - kPeel; b < NB2; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping);
+      l2_epilogue(carry);
+    }
+
+#pragma unroll
+    for (int gr = 0; gr < G; ++gr) {
+      const int local = (G * wave + gr) * kRowsPerWave + r32;
+      const int64_t row = tile * kTileRows + local;
+      if constexpr (kTwoPhase)
+        two_phase_epilogue<BT>(logit[gr], s_b3, s_c, s_head, s_kx, s_ky, tp, h, row, n, s_meta[parity][0][local],
+                               s_meta[parity][1][local], s_meta[parity][2][local], s_meta[parity][3][local],
+                               s_alpha, pred_len, kv_bytes);
+      else
+        length_epilogue<BT>(logit[gr], s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
+                            s_alpha, pred_len, kv_bytes);
+    }
   }
   wait_chunk<0>();                        // no load into LDS outlives the workgroup
 }
@@ -711,6 +863,35 @@ constexpr int32_t kF32Small[] = {64, 128, 32};
 constexpr int32_t kBf16Mid[] = {256, 512, 512, 64};
 constexpr int32_t kBf16Wide[] = {256, 1024, 1024, 64};
 
+// Row groups per wavefront of the bfloat16 predictor: two for the 512-wide hidden layers (256-row
+// tiles), one for the 1024-wide ones, whose layer-1 activations alone fill the accumulation
+// registers (128-row tiles).
+constexpr int kMidGroups = 2;
+
+template <bool kTwoPhase>
+maestro_status launch_mlp3(const maestro_predictor& p, int64_t n, const void* x, const int32_t* prompt_len,
+                           const int32_t* model_id, const float* kv_bytes_per_token, int32_t n_models,
+                           float* pred_len, double* kv_bytes, const TwoPhaseArgs& tp, hipStream_t stream) {
+  const bool mid = p.dims[1] == 512;
+  const int64_t tile_rows = (int64_t)(mid ? kMidGroups : 1) * kRowsPerBlock;
+  const int64_t n_tiles = (n + tile_rows - 1) / tile_rows;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return MAESTRO_ERR_LAUNCH;
+  const dim3 pgrid((unsigned)(n_tiles < cus ? n_tiles : cus)), block(kThreads);
+  auto args = [&](auto kernel) {
+    kernel<<<pgrid, block, 0, stream>>>(
+        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
+        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
+        p.bias[0], p.bias[1], p.bias[2], kTwoPhase ? nullptr : p.bin_centre, n, n_tiles, prompt_len, model_id,
+        kv_bytes_per_token, n_models, pred_len, kv_bytes, tp);
+  };
+  if (mid) args(mlp3_bf16_kernel<256, 512, 512, 64, kMidGroups, kTwoPhase>);
+  else args(mlp3_bf16_kernel<256, 1024, 1024, 64, 1, kTwoPhase>);
+  return launch_status();
+}
+
 }  // namespace
 
 bool predict_shape_supported(const maestro_predictor& p) {
@@ -730,21 +911,8 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
         static_cast<const float*>(p.weight[1]), p.bias[0], p.bias[1], p.bin_centre, n, prompt_len,
         model_id, kv_bytes_per_token, pred_len, kv_bytes);
   } else if (dims_are(p, 3, MAESTRO_BF16, kBf16Mid) || dims_are(p, 3, MAESTRO_BF16, kBf16Wide)) {
-    const int64_t n_tiles = (n + kRowsPerBlock - 1) / kRowsPerBlock;
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-      return MAESTRO_ERR_LAUNCH;
-    const dim3 pgrid((unsigned)(n_tiles < cus ? n_tiles : cus));
-    auto args = [&](auto kernel) {
-      kernel<<<pgrid, block, 0, stream>>>(
-          static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
-          static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
-          p.bias[0], p.bias[1], p.bias[2], p.bin_centre, n, n_tiles, prompt_len, model_id,
-          kv_bytes_per_token, n_models, pred_len, kv_bytes, TwoPhaseArgs{});
-    };
-    if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, false>);
-    else args(mlp3_bf16_kernel<256, 1024, 1024, 64, false>);
+    return launch_mlp3<false>(p, n, x, prompt_len, model_id, kv_bytes_per_token, n_models, pred_len, kv_bytes,
+                              TwoPhaseArgs{}, stream);
   } else {
     return MAESTRO_ERR_UNSUPPORTED;
   }
@@ -762,24 +930,10 @@ maestro_status launch_predict_two_phase(const maestro_predictor& p, const maestr
                                         float* pred_len, double* kv_bytes, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   if (!two_phase_shape_supported(p)) return MAESTRO_ERR_UNSUPPORTED;
-  const int64_t n_tiles = (n + kRowsPerBlock - 1) / kRowsPerBlock;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-    return MAESTRO_ERR_LAUNCH;
-  const dim3 pgrid((unsigned)(n_tiles < cus ? n_tiles : cus)), block(kThreads);
   const TwoPhaseArgs tp{role_id, tool_avail, t.role_head, t.tool_coef, t.iso_x, t.iso_y,
                         t.n_roles, t.n_knots, t.max_len, p_tool};
-  auto args = [&](auto kernel) {
-    kernel<<<pgrid, block, 0, stream>>>(
-        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
-        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
-        p.bias[0], p.bias[1], p.bias[2], nullptr, n, n_tiles, prompt_len, model_id,
-        kv_bytes_per_token, n_models, pred_len, kv_bytes, tp);
-  };
-  if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, true>);
-  else args(mlp3_bf16_kernel<256, 1024, 1024, 64, true>);
-  return launch_status();
+  return launch_mlp3<true>(p, n, x, prompt_len, model_id, kv_bytes_per_token, n_models, pred_len, kv_bytes, tp,
+                           stream);
 }
 
 }  // namespace maestro

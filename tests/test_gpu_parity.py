@@ -70,7 +70,7 @@ def test_library_is_the_in_tree_build():
 # ----------------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name,n", [("c0", None), ("c0", 1), ("c0", 129), ("c1", 1000),
-                                    ("c1", None), ("c4", 777)])
+                                    ("c1", None), ("c1", 131_149), ("c4", 777)])
 def test_predict_matches_oracle(name, n):
     w = wl(name) if n is None else wl(name, n_stages=n)
     pred_g, kv_g, _, _ = gpu_predict(w)
