@@ -111,50 +111,67 @@ struct TwoPhaseArgs {
 // The B = 32*BT outputs of each row read as heads (Sec. III-B): output 0 the tool-intent
 // logit, output g the log(1 + L) regressor of the row's head g (role_head of its role, head 1
 // when the role has none). p_tool = iso(sigmoid(z_0)) (Eq. 1 calibrated; 0 without tools),
-// L = min(expm1(max(z_g + coef_g p_tool, 0)), max_len), then Eq. 3. Lanes r and r + 32 hold
-// complementary halves of row r's outputs; lane r finishes the row.
+// L = min(expm1(max(z_g + coef_g p_tool, 0)), max_len), then Eq. 3.
+__device__ __forceinline__ int head_of_role(int32_t role, const int32_t* __restrict__ head_of, int32_t n_roles,
+                                            int n_out) {
+  int g = (role >= 0 && role < n_roles) ? head_of[role] : 1;
+  return (g < 1 || g >= n_out) ? 1 : g;
+}
+
+// Output g of a row, summed over its two lane-halves: lane-half h holds the outputs
+// 32 bt + acc_row(v, h), so exactly one half holds output g, as register v = 4 (t / 8) + t % 4
+// of tile bt = g / 32 (t = g % 32) when (t / 4) % 2 == h. A five-level selection tree over the
+// register index picks it; the other half contributes 0.
 template <int BT>
-__device__ __forceinline__ void two_phase_epilogue(const f32x16 (&z)[BT], const float* __restrict__ b_last,
-                                                   const float* __restrict__ coef, const int32_t* __restrict__ head_of,
-                                                   const float* __restrict__ kx, const float* __restrict__ ky,
-                                                   const TwoPhaseArgs& tp, int h, int64_t row, int64_t n,
-                                                   int32_t prompt, int32_t model, int32_t role, int32_t tools,
-                                                   const float* __restrict__ alpha, float* __restrict__ pred_len,
-                                                   double* __restrict__ kv_bytes) {
-  int g = (role >= 0 && role < tp.n_roles) ? head_of[role] : 1;
-  if (g < 1 || g >= 32 * BT) g = 1;
-  float mine = 0.0f;   // output g if this lane-half holds it
+__device__ __forceinline__ float head_output(const f32x16 (&z)[BT], int g, int h) {
+  static_assert(BT == 2, "a 32-entry selection tree");
+  const int t = g & 31;
+  const int idx = (g >> 5) * 16 + (t >> 3) * 4 + (t & 3);
+  float val[32];
 #pragma unroll
   for (int bt = 0; bt < BT; ++bt)
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      if (32 * bt + acc_row(v, h) == g) mine = z[bt][v];
-  const float zg = mine + __shfl_xor(mine, 32);   // exactly one of the two lane-halves holds it
-  if (h == 0 && row < n) {
-    float p = 0.0f;
-    if (tools != 0) {
-      const float s = 1.0f / (1.0f + __expf(-(z[0][0] + b_last[0])));   // output 0: v = 0, h = 0
-      const int K = tp.n_knots;
-      if (!(s > kx[0])) {
-        p = ky[0];
-      } else if (s >= kx[K - 1]) {
-        p = ky[K - 1];
-      } else {   // kx[lo] <= s < kx[hi]: the segment through knots lo and lo + 1
-        int lo = 0, hi = K - 1;
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (kx[mid] <= s) lo = mid;
-          else hi = mid;
-        }
-        p = ky[lo] + (s - kx[lo]) * (ky[hi] - ky[lo]) / (kx[hi] - kx[lo]);
-      }
-    }
-    const float y = zg + b_last[g] + coef[g] * p;
-    const float L = fminf(expm1f(fmaxf(y, 0.0f)), tp.max_len);
-    if (tp.p_tool) tp.p_tool[row] = p;
-    pred_len[row] = L;
-    kv_bytes[row] = ((double)prompt + (double)L) * (double)alpha[model];
+    for (int v = 0; v < 16; ++v) val[16 * bt + v] = z[bt][v];
+#pragma unroll
+  for (int lvl = 0; lvl < 5; ++lvl) {
+    const bool bit = (idx >> lvl) & 1;
+#pragma unroll
+    for (int j = 0; j < (16 >> lvl); ++j) val[j] = bit ? val[2 * j + 1] : val[2 * j];
   }
+  const float mine = (((t >> 2) & 1) == h) ? val[0] : 0.0f;
+  return mine + __shfl_xor(mine, 32);
+}
+
+// The rest of one row from its tool-intent output z0 and head output zg (biases not yet added).
+__device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const float* __restrict__ b_last,
+                                              const float* __restrict__ coef, const float* __restrict__ kx,
+                                              const float* __restrict__ ky, const TwoPhaseArgs& tp, int64_t row,
+                                              int32_t prompt, int32_t model, int32_t tools,
+                                              const float* __restrict__ alpha, float* __restrict__ pred_len,
+                                              double* __restrict__ kv_bytes) {
+  float p = 0.0f;
+  if (tools != 0) {
+    const float s = 1.0f / (1.0f + __expf(-(z0 + b_last[0])));
+    const int K = tp.n_knots;
+    if (!(s > kx[0])) {
+      p = ky[0];
+    } else if (s >= kx[K - 1]) {
+      p = ky[K - 1];
+    } else {   // kx[lo] <= s < kx[hi]: the segment through knots lo and lo + 1
+      int lo = 0, hi = K - 1;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (kx[mid] <= s) lo = mid;
+        else hi = mid;
+      }
+      p = ky[lo] + (s - kx[lo]) * (ky[hi] - ky[lo]) / (kx[hi] - kx[lo]);
+    }
+  }
+  const float y = zg + b_last[g] + coef[g] * p;
+  const float L = fminf(expm1f(fmaxf(y, 0.0f)), tp.max_len);
+  if (tp.p_tool) tp.p_tool[row] = p;
+  pred_len[row] = L;
+  kv_bytes[row] = ((double)prompt + (double)L) * (double)alpha[model];
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -771,17 +788,34 @@ void mlp3_bf16_kernel(
       l2_epilogue(carry);
     }
 
+    if constexpr (kTwoPhase) {
+      // Both lane-halves select each group's head output; then lane-half h finishes row r of
+      // group h (G = 2), or lane-half 0 the wavefront's only group (G = 1), so that the rest
+      // of the row runs once per wavefront.
+      float zg[G], z0[G];
+      int gh[G];
 #pragma unroll
-    for (int gr = 0; gr < G; ++gr) {
-      const int local = (G * wave + gr) * kRowsPerWave + r32;
+      for (int gr = 0; gr < G; ++gr) {
+        const int local = (G * wave + gr) * kRowsPerWave + r32;
+        gh[gr] = head_of_role(s_meta[parity][2][local], s_head, tp.n_roles, B);
+        zg[gr] = head_output<BT>(logit[gr], gh[gr], h);
+        z0[gr] = __shfl(logit[gr][0][0], r32);     // output 0: register 0 of lane-half 0
+      }
+      const int mine = G == 1 ? 0 : h;
+      const int local = (G * wave + mine) * kRowsPerWave + r32;
       const int64_t row = tile * kTileRows + local;
-      if constexpr (kTwoPhase)
-        two_phase_epilogue<BT>(logit[gr], s_b3, s_c, s_head, s_kx, s_ky, tp, h, row, n, s_meta[parity][0][local],
-                               s_meta[parity][1][local], s_meta[parity][2][local], s_meta[parity][3][local],
-                               s_alpha, pred_len, kv_bytes);
-      else
+      if ((G > 1 || h == 0) && row < n)
+        two_phase_row(mine ? z0[G - 1] : z0[0], mine ? zg[G - 1] : zg[0], mine ? gh[G - 1] : gh[0], s_b3, s_c,
+                      s_kx, s_ky, tp, row, s_meta[parity][0][local], s_meta[parity][1][local],
+                      s_meta[parity][3][local], s_alpha, pred_len, kv_bytes);
+    } else {
+#pragma unroll
+      for (int gr = 0; gr < G; ++gr) {
+        const int local = (G * wave + gr) * kRowsPerWave + r32;
+        const int64_t row = tile * kTileRows + local;
         length_epilogue<BT>(logit[gr], s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
                             s_alpha, pred_len, kv_bytes);
+      }
     }
   }
   wait_chunk<0>();                        // no load into LDS outlives the workgroup
