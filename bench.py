@@ -505,8 +505,7 @@ def main():
             "frac": round(achieved / peak, 4), "traffic": measured_traffic(spec.name),
             "flop_per_launch": flop, "avg_ms": round(ms_predict, 4),
         },
-        "step_ms": {"predict": round(ms_predict, 4), "route": round(ms_route, 4),
-                    "prioritize": round(ms_prio, 4)},
+        "step_ms": {"predict": round(ms_predict, 4), "route": round(ms_route, 4)},
         "phase_ms": {"predict": percentiles(d_predict), "route": percentiles(d_route)},
     }
     rb = route_bytes(n, spec.n_nodes, spec.k)
@@ -518,6 +517,7 @@ def main():
     }
     if chained:
         pb = prioritize_bytes(n, wl.n_workflows)
+        line["step_ms"]["prioritize"] = round(ms_prio, 4)
         line["phase_ms"]["prioritize"] = percentiles(d_prio)
         line["prioritize"] = {
             "workflows_per_s": wl.n_workflows / (ms_prio * 1e-3), "algorithmic_bytes": pb,
