@@ -190,6 +190,15 @@ def _time_events(call, steps: int, warmup: int):
     return [e0.elapsed_time(e1) for e0, e1 in ev]
 
 
+def inputs_hash(wl) -> str:
+    """One digest over the sha256 of every generated input array (by field name)."""
+    h = hashlib.sha256()
+    for name, digest in sorted(wl.sha256().items()):
+        h.update(name.encode())
+        h.update(digest.encode())
+    return h.hexdigest()[:16]
+
+
 def oracle_timed(fn, units: int, unit: str, sample: str):
     """The oracle on a bounded sample, timed on the host cores: a cpu_baseline record."""
     import oracle
@@ -498,6 +507,7 @@ def main():
             "workload": f"{spec.name}: {W.DESCRIPTIONS[spec.name]}",
             "n_stages": n, "n_workflows": wl.n_workflows, "n_nodes": spec.n_nodes,
             "n_models": spec.n_models, "predictor": "-".join(map(str, spec.dims)), "route_k": spec.k,
+            "inputs_sha256": inputs_hash(wl),
         },
         "roofline": {
             "bound": "mfma", "kernel": "predict (fused MLP + length epilogue)",

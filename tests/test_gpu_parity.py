@@ -18,6 +18,7 @@ import oracle
 import paper_2606_12950_amd as M
 from paper_2606_12950_amd import pipeline
 from paper_2606_12950_amd import workload as W
+from route_guard import explain_route_differences
 
 pytestmark = pytest.mark.gpu
 
@@ -274,6 +275,32 @@ def test_c3_full_step_matches_oracle():
     ref_p = oracle.prioritize(w.chain_offset, lat, w.deadline_us, w.now_us)
     assert_prio_equal((_np(o.remaining_us), _np(o.slack_key), _np(o.order)), ref_p)
     print(f"c3: W={w.n_workflows} S={w.n}: route + order identical")
+
+
+@pytest.mark.parametrize("name,sample", [("c1", None), ("c2", 20000), ("c3", 20000), ("c4", 3000)])
+def test_end_to_end_match_rate_with_guard_bands(name, sample):
+    # oracle predict -> oracle route against GPU predict -> GPU route. The predictions agree only
+    # to the predictor tolerance, so a node choice may legitimately differ; every difference must
+    # be explained by one of the two ways a prediction enters routing: some node's feasibility
+    # flips between the two predictions (the demand straddles its headroom), or the two choices'
+    # scores under the oracle's prediction tie to within float32 rounding (a prediction adds the
+    # same decode term to every node of the stage, so it can reorder nodes only through rounding)
+    w = wl(name)
+    b = pipeline.to_device(w)
+    o = pipeline.allocate_outputs(b)
+    pipeline.run_predict(b, o)
+    pipeline.run_route(b, o)
+    torch.cuda.synchronize()
+    rows = (np.arange(w.n) if sample is None
+            else np.sort(np.random.default_rng(17).choice(w.n, sample, replace=False)))
+    kv_g = _np(o.kv_bytes)[rows]
+    idx_g = _np(o.node_idx)[rows]
+    pred_o, kv_o = oracle.predict_workload(w, rows=rows)
+    idx_o, _ = oracle.route_workload(w, pred_o, kv_o, rows=rows)
+    rate, flips, ties = explain_route_differences(w, rows, pred_o, kv_o, idx_o, kv_g, idx_g)
+    print(f"{name}: {rows.size} stages, node lists identical for {rate:.5%}; "
+          f"{flips} feasibility flips, {ties} rounding ties")
+    assert rate > 0.99
 
 
 @pytest.mark.parametrize("W_", [1, 5, 1023, 1024, 1025, 4097, 131072, 131073, 300001, 1 << 20, (1 << 22) + 3])
