@@ -315,12 +315,34 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
 // patterns (-0 before +0): four passes over the 8-bit digits of the order-preserving image,
 // each narrowing both candidate prefixes by one digit. Within a pass, the candidates' digits
 // are counted into one 256-bin histogram per rank; eight wavefronts scan the two histograms
-// (64 bins each, cross-lane), and the one bin whose count range holds the rank takes it.
+// (64 bins each, cross-lane), and the one bin whose count range holds the rank takes it. A
+// window's values often share their leading digits, which would serialise the LDS atomics on
+// one bin: a wavefront whose counted lanes all carry the same digit adds their count once, and
+// long inputs count into 64 per-lane copies of each histogram (lane l of every wavefront into
+// copy l; copies 257 words apart, so one bin of different copies sits in different banks), so
+// that no two lanes of one atomic ever add to the same word; the copies are summed per bin.
 constexpr int kSelectThreads = 1024;
+constexpr int kSelectUnroll = 8;          // values per thread per step of the per-lane path
+constexpr int kCopyStride = 257;
+constexpr int64_t kPerLaneMin = 32768;    // inputs at least this long take the per-lane copies
+
+__device__ __forceinline__ void count_digit(uint32_t* hist, bool want, uint32_t dgt, int lane) {
+  const uint64_t act = __ballot(want);
+  if (act == 0) return;
+  const int first = __ffsll((unsigned long long)act) - 1;
+  const uint32_t d0 = __shfl(dgt, first);
+  if (__ballot(want && dgt == d0) == act) {
+    if (lane == first) atomicAdd(&hist[d0], (uint32_t)__popcll(act));
+  } else if (want) {
+    atomicAdd(&hist[dgt], 1u);
+  }
+}
+
 __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* __restrict__ v, int64_t m,
                                                                   int64_t r_lo, int64_t r_hi,
                                                                   float* __restrict__ out, int n_out) {
   __shared__ uint32_t hist[2][256];
+  __shared__ uint32_t hcopy[2][64 * kCopyStride];
   __shared__ uint32_t scan[2][256];   // inclusive prefix within each 64-bin segment
   __shared__ uint32_t seg[2][4];      // segment totals
   __shared__ uint32_t s_prefix[2][2];   // [pass parity][rank]: read in one pass, written for the next
@@ -332,15 +354,47 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
   }
   uint32_t mask = 0;
   int par = 0;
+  const bool per_lane = m >= kPerLaneMin;
+  const int n_hist = n_out > 1 ? 2 : 1;
   for (int shift = 24; shift >= 0; shift -= 8, par ^= 1) {
     for (int i = tid; i < 512; i += kSelectThreads) (&hist[0][0])[i] = 0;
+    if (per_lane)
+      for (int i = tid; i < n_hist * 64 * kCopyStride; i += kSelectThreads) (&hcopy[0][0])[i] = 0;
     __syncthreads();
     const uint32_t p0 = s_prefix[par][0], p1 = s_prefix[par][1];
-    for (int64_t i = tid; i < m; i += kSelectThreads) {
-      const uint32_t u = float_key(v[i]);
-      const uint32_t dgt = (u >> shift) & 255u;
-      if ((u & mask) == p0) atomicAdd(&hist[0][dgt], 1u);
-      if ((u & mask) == p1) atomicAdd(&hist[1][dgt], 1u);
+    if (per_lane) {
+      for (int64_t i0 = 0; i0 < m; i0 += (int64_t)kSelectThreads * kSelectUnroll) {
+        uint32_t u[kSelectUnroll];
+        bool in[kSelectUnroll];
+#pragma unroll
+        for (int q = 0; q < kSelectUnroll; ++q) {   // every load issued before any count
+          const int64_t i = i0 + (int64_t)q * kSelectThreads + tid;
+          in[q] = i < m;
+          u[q] = in[q] ? float_key(v[i]) : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < kSelectUnroll; ++q) {
+          const uint32_t dgt = (u[q] >> shift) & 255u;
+          if (in[q] && (u[q] & mask) == p0) atomicAdd(&hcopy[0][lane * kCopyStride + dgt], 1u);
+          if (n_out > 1 && in[q] && (u[q] & mask) == p1) atomicAdd(&hcopy[1][lane * kCopyStride + dgt], 1u);
+        }
+      }
+      __syncthreads();
+      for (int i = tid; i < n_hist * 256; i += kSelectThreads) {
+        const int h = i >> 8, b = i & 255;
+        uint32_t t = 0;
+        for (int l = 0; l < 64; ++l) t += hcopy[h][l * kCopyStride + b];
+        hist[h][b] = t;
+      }
+    } else {
+      for (int64_t i0 = 0; i0 < m; i0 += kSelectThreads) {   // uniform trip count: whole-wave ballots
+        const int64_t i = i0 + tid;
+        const bool in = i < m;
+        const uint32_t u = in ? float_key(v[i]) : 0u;
+        const uint32_t dgt = (u >> shift) & 255u;
+        count_digit(hist[0], in && (u & mask) == p0, dgt, lane);
+        if (n_out > 1) count_digit(hist[1], in && (u & mask) == p1, dgt, lane);
+      }
     }
     __syncthreads();
     if (wave < 8) {
@@ -373,59 +427,194 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
 }
 
 // EWMA of the relative underestimation e_i = max(0, actual_i / pred_i - 1) in arrival order,
-// s_0 = e_0, s_i = beta e_i + (1 - beta) s_(i-1), stored as float32. One workgroup: each thread
-// folds a contiguous segment into an affine map x -> A x + B, a scan of the maps gives every
-// segment its incoming value, and each thread then replays its segment with the recurrence.
+// s_0 = e_0, s_i = beta e_i + (1 - beta) s_(i-1), stored as float32. The window is cut into
+// tiles of kEwmaTile elements. Within a tile, the errors are computed from coalesced loads into
+// LDS, each thread folds its kEwmaPer consecutive elements into an affine map x -> A x + B, the
+// maps are scanned within each wavefront (cross-lane) and the 16 wavefront totals composed in
+// order by one lane, which gives every thread the value entering its elements; each thread then
+// replays its elements with the recurrence. A map that contains element 0 is constant.
 __device__ __forceinline__ double underestimation(double actual, double pred) {
   const double e = __dsub_rn(__ddiv_rn(actual, pred), 1.0);
   return e > 0.0 ? e : 0.0;
 }
 
+constexpr int kEwmaPer = 8;
+constexpr int kEwmaTile = kSelectThreads * kEwmaPer;
+constexpr int kEwmaWaves = kSelectThreads / 64;
+constexpr int64_t kEwmaOneGroupTiles = 2;   // longer windows take the three-launch path
+
+struct EwmaShared {
+  double e[kEwmaTile];
+  double wa[kEwmaWaves], wb[kEwmaWaves];   // wavefront totals
+  double win[kEwmaWaves + 1];              // value entering each wavefront; [16]: leaving the tile
+};
+
+// Errors of tile t0 into LDS, this thread's map (A, B) scanned inclusively within the
+// wavefront, and the wavefront totals into wa/wb. Ends with a barrier.
+__device__ __forceinline__ void ewma_tile_maps(const double* __restrict__ actual, const double* __restrict__ pred,
+                                               int64_t m, int64_t t0, double beta, double keep, EwmaShared& sh,
+                                               double& A, double& B) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  {
+    double av[kEwmaPer], pv[kEwmaPer];
+#pragma unroll
+    for (int q = 0; q < kEwmaPer; ++q) {
+      const int64_t i = t0 + (int64_t)q * kSelectThreads + tid;
+      av[q] = i < m ? actual[i] : 0.0;
+      pv[q] = i < m ? pred[i] : 1.0;
+    }
+#pragma unroll
+    for (int q = 0; q < kEwmaPer; ++q) sh.e[q * kSelectThreads + tid] = underestimation(av[q], pv[q]);
+  }
+  __syncthreads();
+  const int64_t lo = t0 + (int64_t)tid * kEwmaPer;
+  A = 1.0;
+  B = 0.0;   // identity
+#pragma unroll
+  for (int u = 0; u < kEwmaPer; ++u) {
+    const int64_t i = lo + u;
+    if (i < m) {
+      const double e = sh.e[tid * kEwmaPer + u];
+      if (i == 0) {
+        A = 0.0;
+        B = e;
+      } else {
+        A = __dmul_rn(keep, A);
+        B = __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, B));
+      }
+    }
+  }
+  // the map of lanes p..l applied after the map of earlier lanes
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const double pa = __shfl_up(A, d, 64), pb = __shfl_up(B, d, 64);
+    if (lane >= d) {
+      B = __dadd_rn(__dmul_rn(A, pb), B);
+      A = __dmul_rn(A, pa);
+    }
+  }
+  if (lane == 63) {
+    sh.wa[tid >> 6] = A;
+    sh.wb[tid >> 6] = B;
+  }
+  __syncthreads();
+}
+
+// Values entering each wavefront of the tile given the value x entering the tile (one lane).
+__device__ __forceinline__ void ewma_tile_entries(EwmaShared& sh, double x) {
+  for (int w = 0; w < kEwmaWaves; ++w) {
+    sh.win[w] = x;
+    x = __dadd_rn(__dmul_rn(sh.wa[w], x), sh.wb[w]);
+  }
+  sh.win[kEwmaWaves] = x;
+}
+
+// Replays this thread's elements of tile t0 from the wavefront's entering value.
+__device__ __forceinline__ void ewma_tile_replay(int64_t m, int64_t t0, double beta, double keep, const EwmaShared& sh,
+                                                 double A, double B, float* __restrict__ ewma) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const double xw = sh.win[tid >> 6];
+  const double ea = __shfl_up(A, 1, 64), eb = __shfl_up(B, 1, 64);   // lanes 0 .. lane-1
+  double x = lane > 0 ? __dadd_rn(__dmul_rn(ea, xw), eb) : xw;
+  const int64_t lo = t0 + (int64_t)tid * kEwmaPer;
+#pragma unroll
+  for (int u = 0; u < kEwmaPer; ++u) {
+    const int64_t i = lo + u;
+    if (i < m) {
+      const double e = sh.e[tid * kEwmaPer + u];
+      x = (i == 0) ? e : __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, x));
+      ewma[i] = __double2float_rn(x);
+    }
+  }
+}
+
+// One workgroup walks every tile in order (windows of at most a few tiles: one launch).
 __global__ __launch_bounds__(kSelectThreads) void ewma_kernel(const double* __restrict__ actual,
                                                               const double* __restrict__ pred, int64_t m,
                                                               double beta, float* __restrict__ ewma) {
-  __shared__ double s_a[2][kSelectThreads], s_b[2][kSelectThreads];
-  const int tid = threadIdx.x;
+  __shared__ EwmaShared sh;
   const double keep = __dsub_rn(1.0, beta);
-  const int64_t per = (m + kSelectThreads - 1) / kSelectThreads;
-  const int64_t lo = min(m, tid * per), hi = min(m, lo + per);
-  double A = 1.0, B = 0.0;   // identity
-  for (int64_t i = lo; i < hi; ++i) {
-    const double e = underestimation(actual[i], pred[i]);
-    if (i == 0) {
-      A = 0.0;
-      B = e;
-    } else {
-      A = __dmul_rn(keep, A);
-      B = __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, B));
-    }
-  }
-  // inclusive scan of the maps in thread order (Hillis-Steele, double-buffered): the map of
-  // threads p..t applied after the map of earlier threads
-  int buf = 0;
-  s_a[0][tid] = A;
-  s_b[0][tid] = B;
-  __syncthreads();
-  for (int d = 1; d < kSelectThreads; d <<= 1) {
-    double a = s_a[buf][tid], b = s_b[buf][tid];
-    if (tid >= d) {
-      const double pa = s_a[buf][tid - d], pb = s_b[buf][tid - d];
-      b = __dadd_rn(__dmul_rn(a, pb), b);
-      a = __dmul_rn(a, pa);
-    }
-    s_a[buf ^ 1][tid] = a;
-    s_b[buf ^ 1][tid] = b;
-    buf ^= 1;
+  double carry = 0.0;   // the EWMA just before the tile (unused by the tile holding element 0)
+  for (int64_t t0 = 0; t0 < m; t0 += kEwmaTile) {
+    double A, B;
+    ewma_tile_maps(actual, pred, m, t0, beta, keep, sh, A, B);
+    if (threadIdx.x == 0) ewma_tile_entries(sh, carry);
     __syncthreads();
+    ewma_tile_replay(m, t0, beta, keep, sh, A, B, ewma);
+    carry = sh.win[kEwmaWaves];
+    __syncthreads();   // the next tile rewrites sh
   }
-  // the value entering this segment: the composed map of all earlier threads (which includes
-  // element 0, whose map is constant, so its B is the value itself)
-  double x = tid > 0 ? s_b[buf][tid - 1] : 0.0;
-  for (int64_t i = lo; i < hi; ++i) {
-    const double e = underestimation(actual[i], pred[i]);
-    x = (i == 0) ? e : __dadd_rn(__dmul_rn(beta, e), __dmul_rn(keep, x));
-    ewma[i] = __double2float_rn(x);
+}
+
+// Long windows, one workgroup per tile in three launches. The first 16 bytes of each tile's own
+// output range carry its map (A, B) from the fold to the carry pass, and the first 8 then the
+// value entering the tile from the carry pass to the replay, which reads it before any thread of
+// the tile stores an output. The words are moved as 32-bit halves (the output is 4-byte
+// aligned). The last tile's map is never needed; a last tile of a single element is finished by
+// the carry pass itself.
+__device__ __forceinline__ void slot_store(float* p, int k, double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  uint32_t* w = reinterpret_cast<uint32_t*>(p);
+  w[2 * k] = (uint32_t)u;
+  w[2 * k + 1] = (uint32_t)(u >> 32);
+}
+__device__ __forceinline__ double slot_load(const float* p, int k) {
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(p);
+  return __builtin_bit_cast(double, (uint64_t)w[2 * k] | ((uint64_t)w[2 * k + 1] << 32));
+}
+
+__global__ __launch_bounds__(kSelectThreads) void ewma_fold_kernel(const double* __restrict__ actual,
+                                                                   const double* __restrict__ pred, int64_t m,
+                                                                   double beta, float* __restrict__ ewma) {
+  __shared__ EwmaShared sh;
+  const double keep = __dsub_rn(1.0, beta);
+  const int64_t t0 = (int64_t)blockIdx.x * kEwmaTile;   // never the last tile
+  double A, B;
+  ewma_tile_maps(actual, pred, m, t0, beta, keep, sh, A, B);
+  if (threadIdx.x == 0) {
+    double a = 1.0, b = 0.0;   // compose the wavefront totals in order
+    for (int w = 0; w < kEwmaWaves; ++w) {
+      b = __dadd_rn(__dmul_rn(sh.wa[w], b), sh.wb[w]);
+      a = __dmul_rn(sh.wa[w], a);
+    }
+    slot_store(ewma + t0, 0, a);
+    slot_store(ewma + t0, 1, b);
   }
+}
+
+__global__ __launch_bounds__(64) void ewma_carry_kernel(const double* __restrict__ actual,
+                                                        const double* __restrict__ pred, int64_t m, double beta,
+                                                        int64_t n_tiles, float* __restrict__ ewma) {
+  if (threadIdx.x != 0) return;
+  double x = 0.0;
+  for (int64_t t = 0; t + 1 < n_tiles; ++t) {
+    float* slot = ewma + t * kEwmaTile;
+    const double a = slot_load(slot, 0), b = slot_load(slot, 1);
+    slot_store(slot, 0, x);   // value entering tile t
+    x = __dadd_rn(__dmul_rn(a, x), b);
+  }
+  const int64_t last = (n_tiles - 1) * kEwmaTile;
+  if (m - last >= 2) {
+    slot_store(ewma + last, 0, x);
+  } else {   // a single element: finish it here
+    const double e = underestimation(actual[last], pred[last]);
+    ewma[last] = __double2float_rn(__dadd_rn(__dmul_rn(beta, e), __dmul_rn(__dsub_rn(1.0, beta), x)));
+  }
+}
+
+__global__ __launch_bounds__(kSelectThreads) void ewma_apply_kernel(const double* __restrict__ actual,
+                                                                    const double* __restrict__ pred, int64_t m,
+                                                                    double beta, float* __restrict__ ewma) {
+  __shared__ EwmaShared sh;
+  __shared__ double s_in;
+  const double keep = __dsub_rn(1.0, beta);
+  const int64_t t0 = (int64_t)blockIdx.x * kEwmaTile;
+  if (threadIdx.x == 0) s_in = slot_load(ewma + t0, 0);
+  double A, B;
+  ewma_tile_maps(actual, pred, m, t0, beta, keep, sh, A, B);   // its barriers publish s_in
+  if (threadIdx.x == 0) ewma_tile_entries(sh, s_in);
+  __syncthreads();
+  ewma_tile_replay(m, t0, beta, keep, sh, A, B, ewma);
 }
 
 }  // namespace
@@ -520,7 +709,18 @@ maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, in
 
 maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
                                    int64_t rank, float* ewma, float* rho, hipStream_t stream) {
-  ewma_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m, beta, ewma);
+  const int64_t n_tiles = (m + kEwmaTile - 1) / kEwmaTile;
+  if (n_tiles <= kEwmaOneGroupTiles) {
+    ewma_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m, beta, ewma);
+  } else {
+    const int64_t last_elems = m - (n_tiles - 1) * kEwmaTile;
+    ewma_fold_kernel<<<dim3((unsigned)(n_tiles - 1)), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m,
+                                                                                        beta, ewma);
+    ewma_carry_kernel<<<dim3(1), dim3(64), 0, stream>>>(kv_actual, kv_pred, m, beta, n_tiles, ewma);
+    const int64_t applied = last_elems >= 2 ? n_tiles : n_tiles - 1;
+    ewma_apply_kernel<<<dim3((unsigned)applied), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m, beta,
+                                                                                   ewma);
+  }
   maestro_status st = launch_status();
   if (st != MAESTRO_OK) return st;
   quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(ewma, m, rank, rank, rho, 1);
