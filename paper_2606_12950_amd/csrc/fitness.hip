@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   constexpr int kMatRow = kReady == kMatrix16 ? 16 : 64;   // largest row the staging area holds
   // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
   // workgroups per CU, whose waves hide each other's LDS latency
-  constexpr int kChunk = kReady == kMatrix64 ? 32 : (kPlans ? 128 : 256);
+  constexpr int kChunk = kReady == kMatrix64 ? 32 : 128;
   constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
   struct Admit { double free; uint64_t mask; };
   __shared__ float4 s_terms[kChunk];
