@@ -64,8 +64,9 @@ def _nodes(rng, M_, n_src, n_models=16):
     )
 
 
-@pytest.mark.parametrize("m", [1, 2, 3, 19, 20, 21, 1000, 4096, 100003])
+@pytest.mark.parametrize("m", [1, 2, 3, 19, 20, 21, 1000, 4096, 32767, 32768, 40000, 100003])
 def test_quantiles_match_oracle(m):
+    # 32,768 values and more count into per-lane histogram copies
     rng = np.random.default_rng(m)
     v = np.round(rng.normal(0, 30, m), 1).astype(np.float32)
     v[rng.random(m) < 0.05] = -0.0
@@ -432,8 +433,12 @@ def _ulp_close(got, ref):
     return np.all(np.abs(got.astype(np.float64) - ref) <= np.spacing(np.abs(ref)).astype(np.float64))
 
 
-@pytest.mark.parametrize("m", [1, 2, 1000, 1023, 1024, 1025, 4096, 100003, 3000000])
+@pytest.mark.parametrize("m", [1, 2, 1000, 1023, 1024, 1025, 4096, 8192, 8193, 16384, 16385, 16386, 24576,
+                               24579, 32767, 32768, 100003, 3000000])
 def test_adaptive_rho_matches_oracle(m):
+    # tiles of 8,192 stages: up to two tiles in one workgroup, longer windows in three launches
+    # (16,385 and 24,579 end in a tile of one and three stages; 16,385 is finished by the
+    # composition pass); the selection switches to per-lane histogram copies at 32,768
     actual, pred = W.margin_window(m, m)
     for beta, q in [(0.2, 0.95), (0.05, 0.9), (1.0, 0.95), (0.5, 1.0), (0.2, 0.0)]:
         ew, rho = M.adaptive_rho(_t(actual), _t(pred), beta, q)
