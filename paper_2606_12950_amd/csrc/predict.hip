@@ -844,8 +844,30 @@ __global__ __launch_bounds__(kThreads) void mlp2_f32_kernel(
   const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + wave * kRowsPerWave + r32;
   const int64_t xrow = row < n ? row : n - 1;
 
-  for (int i = tid; i < H * D; i += kThreads) sw1[(i / D) * ROW1 + i % D] = w1[i];
-  for (int i = tid; i < B * H; i += kThreads) sw2[(i / H) * ROW2 + i % H] = w2[i];
+  // weights staged with 16-byte loads, all issued before the first LDS store, so the staging
+  // costs one memory latency rather than one per element
+  static_assert((H * D) % (4 * kThreads) == 0 && (B * H) % (4 * kThreads) == 0 && D % 4 == 0 && H % 4 == 0,
+                "whole float4 staging rounds");
+  {
+    constexpr int N1 = H * D / (4 * kThreads), N2 = B * H / (4 * kThreads);
+    float4 r1[N1], r2[N2];
+#pragma unroll
+    for (int j = 0; j < N1; ++j) r1[j] = reinterpret_cast<const float4*>(w1)[j * kThreads + tid];
+#pragma unroll
+    for (int j = 0; j < N2; ++j) r2[j] = reinterpret_cast<const float4*>(w2)[j * kThreads + tid];
+#pragma unroll
+    for (int j = 0; j < N1; ++j) {
+      const int i = 4 * (j * kThreads + tid);
+      float* d = sw1 + (i / D) * ROW1 + i % D;
+      d[0] = r1[j].x; d[1] = r1[j].y; d[2] = r1[j].z; d[3] = r1[j].w;
+    }
+#pragma unroll
+    for (int j = 0; j < N2; ++j) {
+      const int i = 4 * (j * kThreads + tid);
+      float* d = sw2 + (i / H) * ROW2 + i % H;
+      d[0] = r2[j].x; d[1] = r2[j].y; d[2] = r2[j].z; d[3] = r2[j].w;
+    }
+  }
 
   float xf[KS1];
   {
