@@ -4,9 +4,9 @@
 // calibrated tool-intent probability, Eq. 1, then the role's log(1 + L) regressor fed that
 // probability); only the epilogue differs.
 //
-// Layout of the work. Each wavefront owns 32 stages (rows). Every Linear layer is computed
-// transposed, H^T = W * X^T, on 32x32 MFMA tiles: the weights are the A operand (32 output
-// neurons x K) and the activations the B operand (K x 32 rows). A 32x32 result tile leaves
+// Layout of the work. Each wavefront owns one or two groups of 32 stages (rows). Every Linear
+// layer is computed transposed, H^T = W * X^T, on 32x32 MFMA tiles: the weights are the A
+// operand (32 output neurons x K) and a group's activations the B operand (K x 32 rows). A 32x32 result tile leaves
 // lane (h*32 + r) holding, for row r, the 16 neurons (v/4)*8 + 4h + v%4 (v = 0..15). Those 16
 // values are exactly what the same lane must feed as the B operand of the next layer over a
 // K-slice of 32 inputs, provided the next layer's weight columns are read in the matching
@@ -15,11 +15,11 @@
 // consumed block by block into the logit accumulators without ever being stored whole.
 //
 // Weights stream through LDS: each 32-neuron block of a layer (plus, for the last hidden
-// layer, the matching 32 columns of the logit layer) is copied once per workgroup into a
-// double buffer by direct global->LDS loads (no staging registers) while the previous block
-// is being multiplied, and read by all four wavefronts with 16-byte LDS reads. Weight rows
-// are padded by 16 bytes in LDS so that the 16 rows a half-wavefront reads at one column
-// fall in distinct banks.
+// layer, the matching 32 columns of the logit layer) is copied once per workgroup and tile
+// into a ring of LDS buffers by direct global->LDS loads (no staging registers) while earlier
+// blocks are being multiplied, and read by all four wavefronts with 16-byte LDS reads; with two
+// row groups every fragment read feeds one MFMA per group. Weight rows are padded by 16 bytes
+// in LDS so that the 16 rows a half-wavefront reads at one column fall in distinct banks.
 #include "internal.h"
 
 namespace maestro {
@@ -178,10 +178,11 @@ __device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const f
 // bfloat16, three Linear layers: D -> H1 -> H2 -> B   (D = 256)
 // ---------------------------------------------------------------------------------------------
 //
-// Persistent workgroups (one per compute unit) walk 128-row tiles. Everything a tile reads
-// from global memory arrives as a fixed sequence of LDS "chunks":
-//   feature chunk j (j = 0, 1) : features of tile rows 64j .. 64j+63 (and, with chunk 0, the
-//                                tile's prompt lengths and model ids)
+// Persistent workgroups (one per compute unit) walk tiles of 128 G rows. Everything a tile
+// reads from global memory arrives as a fixed sequence of LDS "chunks":
+//   feature chunk j (j < 2G)   : G = 1: features of tile rows 64j .. 64j+63; G = 2: K-slice j
+//                                (columns 64j .. 64j+63) of all 256 tile rows; with them, in
+//                                64-row pieces, the tile's per-stage inputs
 //   layer-1 chunk j            : W1 rows 64j .. 64j+63 (two 32-neuron blocks), all D columns
 //   layer-2 chunk (b, p)       : W2 rows 32b .. 32b+31, columns 512p .. 512p+511, plus, for
 //                                the last p, W3 columns 32b .. 32b+31 of every bin row
@@ -192,7 +193,8 @@ __device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const f
 // wait ever drains the prefetch.
 //
 // LDS layouts (all 16-byte reads are free of bank conflicts per quarter-wavefront):
-//   feature chunk: 64 rows of 512 bytes, the 16-byte units of row r stored at unit ^ (r % 16)
+//   feature chunk: G = 1: 64 rows of 512 bytes, the 16-byte units of row r stored at
+//                  unit ^ (r % 16); G = 2: 256 rows of 128 bytes, unit u at u ^ ((r / 2) % 8)
 //   layer-1 chunk: row pairs (2i, 2i+1) stored contiguously (1 KB), 16-byte pad per pair; in
 //                  odd rows the 16-byte units are stored with index bit 3 flipped
 //   layer-2 chunk: 32 rows of 1 KB, 16-byte pad per row; then the W3 slice, B rows x 64 bytes
