@@ -70,8 +70,8 @@ def test_library_is_the_in_tree_build():
 # predict
 # ----------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name,n", [("c0", None), ("c0", 1), ("c0", 129), ("c1", 1000),
-                                    ("c1", None), ("c1", 131_149), ("c4", 777)])
+@pytest.mark.parametrize("name,n", [("c0", None), ("c0", 1), ("c0", 129), ("c1", 1), ("c1", 7), ("c1", 257),
+                                    ("c1", 1000), ("c1", None), ("c1", 131_149), ("c4", 1), ("c4", 777)])
 def test_predict_matches_oracle(name, n):
     w = wl(name) if n is None else wl(name, n_stages=n)
     pred_g, kv_g, _, _ = gpu_predict(w)
