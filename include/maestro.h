@@ -310,8 +310,11 @@ MAESTRO_API maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n
  *   ewma[i] = fl32(s_i)                                             (out, [m] float32)
  *   rho[0]  = the value of rank ceil(q (m - 1)) (0-based, ascending) among ewma[0 .. m-1]
  * kv_actual, kv_pred [m] float64 (device; kv_pred > 0, both finite); 0 < beta <= 1; 0 <= q <= 1
- * (a high quantile, 0.9 - 0.95). ewma doubles as the selection's input. The float64 EWMA is a
- * parallel scan, so ewma can differ from a sequential evaluation in the last place. Errors:
+ * (a high quantile, 0.9 - 0.95). ewma doubles as the selection's input, and for windows longer
+ * than 16,384 stages as the call's scratch (per-tile scan state in the first words of each
+ * 8,192-stage range): its contents are defined once the stream reaches the call's end. The
+ * float64 EWMA is a parallel scan, so ewma can differ from a sequential evaluation in the last
+ * place. Errors:
  * INVALID_ARG for m < 1, beta or q out of range, a NULL or misaligned array; UNSUPPORTED for
  * m > 2^32 - 1. */
 MAESTRO_API maestro_status maestro_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m,
