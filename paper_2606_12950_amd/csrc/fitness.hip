@@ -108,8 +108,12 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const i
 // stage's model is resident (residency bits in 32 or 64 bits), or a [node][model] matrix (of at
 // most 16 or 64 models: the chunk of node rows staged in LDS shrinks with the row length).
 enum Ready { kMask32 = 0, kMask64 = 1, kMatrix16 = 2, kMatrix64 = 3 };
+constexpr int64_t kFitnessLanesTarget = 256 * 4 * 64 * 4;   // lanes of four wavefronts per SIMD
 
-template <int KT, int kReady, bool kPlans>
+// kMulti: G = 2^g_log2 lanes share a stage (batches too small to fill the chip); lane g scores
+// nodes g, g + G, g + 2G, ... of every chunk into its own list, and the G lists are merged with
+// xor-shuffles (lexicographic on (key, node)) before lane 0 writes the stage's results.
+template <int KT, int kReady, bool kPlans, bool kMulti>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_models, int32_t n_nodes,
@@ -117,7 +121,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
     const float* __restrict__ act_matrix, const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
     const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
-    int32_t* __restrict__ node_idx, float* __restrict__ fitness) {
+    int32_t* __restrict__ node_idx, float* __restrict__ fitness, int g_log2) {
   // per node, two 16-byte records (one LDS read each, the same address for every lane):
   //   terms: 1 / fl32(headroom) (+inf when that is 0), norm(T_q) (model resident),
   //          norm(T_q + T_act), norm(C_deg)
@@ -148,7 +152,10 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   __shared__ float s_ready[kMat ? kChunk * kMatRow : 1];
 
   const int tid = threadIdx.x;
-  const int64_t stage = (int64_t)blockIdx.x * kThreads + tid;
+  const int G = kMulti ? 1 << g_log2 : 1;
+  const int g = kMulti ? tid & (G - 1) : 0;   // this lane's first node of each chunk
+  const int64_t stage = kMulti ? (int64_t)blockIdx.x * (kThreads >> g_log2) + (tid >> g_log2)
+                               : (int64_t)blockIdx.x * kThreads + tid;
   const bool valid = stage < n;
   const float lo_r = bounds[0], lo_t = bounds[2], lo_d = bounds[4];
   const float inv_r = norm_inv(bounds[0], bounds[1]);
@@ -244,33 +251,33 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       ++n_short;
     };
     if (kPlans) {
-      // groups of four nodes: their LDS reads issue together, and one branch per group
-      // queues the short ones
-      int i = 0;
-      for (; i + 4 <= cn; i += 4) {
+      // groups of four of this lane's nodes: their LDS reads issue together, and one branch
+      // per group queues the short ones
+      int i = g;
+      for (; i + 3 * G < cn; i += 4 * G) {
         float4 t[4];
         Admit ad[4];
         float px[4];
         bool fits[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          t[u] = s_terms[i + u];
-          ad[u] = s_admit[i + u];
-          px[u] = prox_row[i + u];
+          t[u] = s_terms[i + u * G];
+          ad[u] = s_admit[i + u * G];
+          px[u] = prox_row[i + u * G];
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           fits[u] = need <= ad[u].free;
-          const float sc = score(i + u, t[u], ad[u], px[u], t[u].w);
-          best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u);
+          const float sc = score(i + u * G, t[u], ad[u], px[u], t[u].w);
+          best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u * G);
         }
         if (valid && !(fits[0] && fits[1] && fits[2] && fits[3])) {
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            if (!fits[u]) queue(i + u);
+            if (!fits[u]) queue(i + u * G);
         }
       }
-      for (; i < cn; ++i) {
+      for (; i < cn; i += G) {
         const float4 t = s_terms[i];
         const Admit ad = s_admit[i];
         const bool fits = need <= ad.free;
@@ -280,7 +287,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       }
     } else {
 #pragma unroll 4
-      for (int i = 0; i < cn; ++i) {
+      for (int i = g; i < cn; i += G) {
         const float4 t = s_terms[i];
         const Admit ad = s_admit[i];
         const float sc = score(i, t, ad, prox_row[i], t.w);
@@ -293,13 +300,27 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         for (int q = 0; q < n_short; ++q) short_pair(s_queue[q * kThreads + tid]);
       } else {
 #pragma unroll 1
-        for (int i = 0; i < cn; ++i)
+        for (int i = g; i < cn; i += G)
           if (!(need <= s_admit[i].free)) short_pair(i);
       }
     }
   }
 
-  if (valid) {
+  if constexpr (kMulti) {   // lanes g and g ^ o exchange and merge their lists
+    for (int o = 1; o < G; o <<= 1) {
+      float ps[KT];
+      int32_t pn[KT];
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        ps[i] = __shfl_xor(best.s[i], o);
+        pn[i] = __shfl_xor(best.n[i], o);
+      }
+#pragma unroll
+      for (int i = 0; i < KT; ++i) best.push_lex(ps[i], pn[i]);
+    }
+  }
+
+  if (valid && g == 0) {
 #pragma unroll
     for (int i = 0; i < KT; ++i) {
       if (i < k) {
@@ -628,14 +649,27 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     const float* bounds, double rho, int32_t k, int32_t* node_idx,
                                     float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
-  const dim3 grid((unsigned)((n + kThreads - 1) / kThreads)), block(kThreads);
+  // lanes per stage: the smallest power of two (at most 16) that gives the batch about four
+  // wavefronts per SIMD of a 256-CU chip, and never more lanes than a chunk has nodes
+  int g_log2 = 0;
+  while (g_log2 < 4 && n * (2 << g_log2) <= kFitnessLanesTarget && (2 << g_log2) <= n_nodes) ++g_log2;
+  const int64_t per_block = kThreads >> g_log2;
+  const dim3 grid((unsigned)((n + per_block - 1) / per_block)), block(kThreads);
   const int ready = act_matrix ? (n_models > 16 ? kMatrix64 : kMatrix16) : (n_models > 32 ? kMask64 : kMask32);
   const bool with_plans = plans != nullptr;
-#define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                   \
-  fitness_kernel<KT, RD, PL><<<grid, block, 0, stream>>>(n, model_id, src_id, class_id, kv_bytes, n_models, \
-                                                         n_nodes, n_src, free_bytes, queue_ms, act_ms,    \
-                                                         resident_mask, act_matrix, deg_ms, plans, rtt_ms, \
-                                                         class_weights, bounds, rho, k, node_idx, fitness)
+#define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                          \
+  do {                                                                                                          \
+    if (g_log2 > 0)                                                                                             \
+      fitness_kernel<KT, RD, PL, true><<<grid, block, 0, stream>>>(                                             \
+          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, free_bytes, queue_ms, act_ms,      \
+          resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,  \
+          g_log2);                                                                                              \
+    else                                                                                                        \
+      fitness_kernel<KT, RD, PL, false><<<grid, block, 0, stream>>>(                                            \
+          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, free_bytes, queue_ms, act_ms,      \
+          resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,  \
+          0);                                                                                                   \
+  } while (0)
 #define MAESTRO_FIT_RD(KT, PL)                                       \
   do {                                                               \
     if (ready == kMatrix16) MAESTRO_FIT_LAUNCH(KT, kMatrix16, PL);   \
