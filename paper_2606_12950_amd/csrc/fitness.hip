@@ -10,8 +10,9 @@
 // (fitness, node) pairs are kept, larger fitness first and the lower index on equal fitness
 // (the strict ">" of Alg. 3).
 //
-// A workgroup takes 256 stages (one per thread) and stages node state chunk by chunk in LDS,
-// with everything that depends on the node alone already normalised: headroom, its float32
+// A workgroup takes 256 stages (one per thread; 256 / G when a small batch gives each stage G
+// lanes) and stages node state chunk by chunk in LDS, with everything that depends on the node
+// alone already normalised: headroom, its float32
 // reciprocal, normalised T_ready with and without activation, normalised C_deg, and
 // 1 - normalised RTT from every source. A pair then costs the feasibility test, one product for
 // the fit and the four products/sums of Eq. 5. Every operation is float32 round-to-nearest in a
@@ -27,6 +28,8 @@
 //
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
+// The adaptive margin (Sec. III-D) reuses that selection on an EWMA of the window's relative
+// underestimation, computed as a scan of affine maps.
 #include <type_traits>
 
 #include "internal.h"
