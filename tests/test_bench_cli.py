@@ -12,3 +12,16 @@ def test_more_than_one_gpu_exits_with_a_message():
                        text=True, timeout=120, cwd=ROOT)
     assert r.returncode != 0
     assert "GPU" in (r.stdout + r.stderr)
+
+
+def test_committed_traffic_matches_the_current_predictor_source():
+    # the bench line's roofline.traffic is reported only for the kernel source the counters
+    # were taken on; the committed record must be for the current source and workload
+    sys.path.insert(0, ROOT)
+    import bench
+    t = bench.measured_traffic("c3")
+    assert t is not None, "profiles/predict_traffic.json was taken on another predictor source"
+    assert bench.measured_traffic("c1") is None
+    import json
+    rec = json.load(open(bench.TRAFFIC_FILE))
+    assert t == rec["hbm_bytes_per_launch"] > rec["algorithmic_bytes_per_launch"] > 0
