@@ -116,6 +116,8 @@ def test_two_phase_roles_tools_table_and_clamps():
         dict(role_head=np.array([5, 63, 0, 64, 1, 9, -4], np.int32)),   # heads at and beyond the ends
         dict(tool_avail=np.zeros(w.n, np.int32)),                # no tools anywhere
         dict(iso_x=np.array([0.2, 0.8], np.float32), iso_y=np.array([0.1, 0.9], np.float32)),  # two knots
+        dict(iso_x=np.linspace(0.0, 1.0, 64).astype(np.float32),                    # 64 knots (the most),
+             iso_y=np.repeat(np.linspace(0.0, 1.0, 16), 4).astype(np.float32)),   # flat runs of four
         dict(max_len=150.0),                                     # the clamp bites
         dict(tool_coef=np.full(64, 3.0, np.float32)),            # tool probability lengthens outputs
     ]
