@@ -207,22 +207,33 @@ __global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
   }
 }
 
+// The first kWalkHead entries of every model's list are staged in LDS by the whole workgroup
+// (while each thread's own inputs are in flight), so a walk that ends early never waits on a
+// dependent global load.
+constexpr int kWalkHead = 8;
+
 template <int KT>
 __global__ __launch_bounds__(kThreads) void walk_route_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
-    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_nodes,
-    const NodeEntry* __restrict__ lists, double rho, int32_t k, int32_t* __restrict__ node_idx,
+    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_models,
+    int32_t n_nodes, const NodeEntry* __restrict__ lists, double rho, int32_t k, int32_t* __restrict__ node_idx,
     float* __restrict__ score) {
+  __shared__ NodeEntry s_head[kMaxMatrixModels * kWalkHead];
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int head = n_nodes < kWalkHead ? n_nodes : kWalkHead;
+  for (int e = threadIdx.x; e < n_models * head; e += kThreads)
+    s_head[(e / head) * kWalkHead + e % head] = lists[(size_t)(e / head) * n_nodes + e % head];
+  __syncthreads();
   if (i >= n) return;
   const int32_t m = model_id[i];
   const double need = (rho == 0.0) ? kv_bytes[i] : __dmul_rn(kv_bytes[i], 1.0 + rho);
   const float exec_s = __fmul_rn(pred_len[i], decode_s_per_token[m]);
   const NodeEntry* list = lists + (size_t)m * n_nodes;
+  const NodeEntry* lhead = s_head + m * kWalkHead;
   TopK<KT> best;
   best.init();
   for (int32_t j = 0; j < n_nodes; ++j) {
-    const NodeEntry e = list[j];
+    const NodeEntry e = j < head ? lhead[j] : list[j];
     if (!(need <= e.free)) continue;                       // infeasible: skip, keep walking
     const float sc = __fadd_rn(e.ready, exec_s);
     if (best.n[KT - 1] != kNoNode && sc > best.s[KT - 1]) break;   // no later node can enter
@@ -276,7 +287,7 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
     sort_nodes_kernel<<<dim3(n_models), dim3(kSortThreads), 0, stream>>>(
         n_nodes, padded, n_models, queue_s, cold_s, resident_mask, act_matrix, free_bytes, lists);
     const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
-#define MAESTRO_WALK_KT(KT)                                                                          walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,                                                                  decode_s_per_token, n_nodes, lists, rho,                                                             k, node_idx, score)
+#define MAESTRO_WALK_KT(KT)                                                                          walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,                                                                  decode_s_per_token, n_models, n_nodes, lists, rho,                                                             k, node_idx, score)
     if (k == 1) MAESTRO_WALK_KT(1);
     else if (k == 2) MAESTRO_WALK_KT(2);
     else if (k == 3) MAESTRO_WALK_KT(3);
