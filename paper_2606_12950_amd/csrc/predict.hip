@@ -71,16 +71,16 @@ __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const
     }
   }
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  // e^(z - mx) = 2^(z log2(e) - mx log2(e)): one fused multiply-add and the hardware 2^x per
-  // logit; the weighted sum of centres accumulates with fused multiply-adds
+  // e^(z - mx) = 2^((z - mx) log2(e)) with the hardware 2^x; the difference is taken first
+  // (exact when z is near mx), so very large logits lose no accuracy to a rounded mx log2(e).
+  // The weighted sum of centres accumulates with fused multiply-adds.
   constexpr float kLog2e = 1.4426950408889634f;
-  const float off = -mx * kLog2e;
   float se = 0.0f, sc = 0.0f;
 #pragma unroll
   for (int bt = 0; bt < BT; ++bt) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const float e = __builtin_amdgcn_exp2f(fmaf(z[bt][v], kLog2e, off));
+      const float e = __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(z[bt][v], mx), kLog2e));
       se += e;
       sc = fmaf(e, c[bt][v], sc);
     }

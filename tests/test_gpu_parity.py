@@ -90,6 +90,18 @@ def test_predict_full_size_sampled(name, sample):
     print(f"{name}: predict sampled max rel err {err:.2e}")
 
 
+@pytest.mark.parametrize("name,shift", [("c1", 1000.0), ("c1", -1000.0), ("c4", 1000.0), ("c4", -1000.0)])
+def test_predict_shifted_logits(name, shift):
+    # the softmax is invariant to a common shift of the logits; +-1000 on every output bias
+    # overflows (or underflows) float32 e^z unless the row maximum is subtracted first
+    import dataclasses
+    w = wl(name, n_stages=2000)
+    w = dataclasses.replace(w, biases=w.biases[:-1] + [(w.biases[-1] + np.float32(shift)).astype(np.float32)])
+    pred_g, kv_g, _, _ = gpu_predict(w)
+    err = check_pred(w, pred_g, kv_g)
+    print(f"{name} logits {shift:+.0f}: predict max rel err {err:.2e}")
+
+
 @pytest.mark.parametrize("name", ["c0", "c1", "c4"])
 def test_predict_zero_weights_is_exact_mean_centre(name):
     # uniform softmax: the expected length is the mean of the bin centres, exactly
