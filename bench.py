@@ -34,8 +34,10 @@ METRIC = "stages predicted+routed/sec on 1 MI355X; % of HBM/MFMA roofline"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0
-# non-packed vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-PEAK_VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# non-packed float32 vector ALU: 256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.6 T
+# lane-operations/s (the 157.3 TFLOP/s fp32 vector peak counts a multiply-add as two); a probe of
+# independent non-packed v_add_f32 chains sustains about 65 T lane-ops/s on the chip
+PEAK_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 # operations the fitness definition needs per (stage, node) pair: the feasibility compare and
 # the eight float32 operations of the score (fit product; gamma, (1 - gamma) products and their
 # sum; lambda and mu products and the two differences)
