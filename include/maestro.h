@@ -31,8 +31,12 @@
  *   - Host-side checks only (scalars, pointers, alignment, sizes) happen before anything is
  *     enqueued; on failure the call returns MAESTRO_ERR_INVALID_ARG / _UNSUPPORTED /
  *     _WORKSPACE and has no effect. A failed launch returns MAESTRO_ERR_LAUNCH.
- *   - Per-element device data is a precondition, not checked: model ids in [0, n_models),
- *     finite inputs (stage latency excepted), monotone chain offsets.
+ *   - Per-stage ids are checked on the device, stage by stage: a model id outside
+ *     [0, n_models) makes that stage's kv_bytes NaN in maestro_predict(_two_phase) (its length
+ *     is still computed) and gives it no node in the routers (node -1, score +inf, fitness
+ *     -inf), as does a source or class id out of range in maestro_route_fitness; no array is
+ *     indexed out of bounds. Other per-element data is a precondition, not checked: finite
+ *     inputs (stage latency excepted), monotone chain offsets.
  *   - Empty inputs (n = 0, n_workflows = 0) are valid no-ops that return MAESTRO_OK.
  *   - Entry points are re-entrant: the library has no mutable global state.
  */

@@ -109,6 +109,20 @@ def _dev(t: torch.Tensor, name: str, dtype: torch.dtype) -> torch.Tensor:
     return t
 
 
+def _shape(t: torch.Tensor, name: str, shape: Tuple[int, ...]) -> torch.Tensor:
+    """Raise unless ``t`` has exactly ``shape``: the kernels index every array by the sizes the
+    call passes, so a shorter tensor would be read or written past its end."""
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _workspace(t: Optional[torch.Tensor], name: str = "workspace") -> Optional[torch.Tensor]:
+    if t is not None:
+        _dev(t, name, torch.uint8)
+    return t
+
+
 def _check(fn: str, status: int):
     if status != 0:
         raise MaestroError(fn, status)
@@ -155,15 +169,17 @@ def predict(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[t
     n = x.shape[0]
     if x.dim() != 2 or x.shape[1] != p.dims[0]:
         raise ValueError("x must be [N][D]")
-    _dev(prompt_len, "prompt_len", torch.int32)
-    _dev(model_id, "model_id", torch.int32)
+    _shape(_dev(prompt_len, "prompt_len", torch.int32), "prompt_len", (n,))
+    _shape(_dev(model_id, "model_id", torch.int32), "model_id", (n,))
     _dev(kv_bytes_per_token, "kv_bytes_per_token", torch.float32)
+    if kv_bytes_per_token.dim() != 1:
+        raise ValueError("kv_bytes_per_token must be [n_models]")
     if out is None:
         out = (torch.empty(n, dtype=torch.float32, device=x.device),
                torch.empty(n, dtype=torch.float64, device=x.device))
     pred, kv = out
-    _dev(pred, "pred_len", torch.float32)
-    _dev(kv, "kv_bytes", torch.float64)
+    _shape(_dev(pred, "pred_len", torch.float32), "pred_len", (n,))
+    _shape(_dev(kv, "kv_bytes", torch.float64), "kv_bytes", (n,))
     ws_bytes = lib.maestro_predict_workspace(ctypes.byref(p), n)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device) if ws_bytes else None
     st = lib.maestro_predict(ctypes.byref(p), n, _ptr(x), _ptr(prompt_len), _ptr(model_id),
@@ -198,6 +214,8 @@ def predict_two_phase(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: 
         raise ValueError("per-stage inputs must have N entries")
     if tool_coef.shape != (p.dims[p.n_layers],) or iso_x.shape != iso_y.shape:
         raise ValueError("tool_coef needs one entry per output; iso_x and iso_y the same length")
+    if role_head.dim() != 1 or iso_x.dim() != 1 or kv_bytes_per_token.dim() != 1:
+        raise ValueError("role_head, iso_x, iso_y and kv_bytes_per_token must be one-dimensional")
     tp = TwoPhase()
     tp.n_roles = role_head.shape[0]
     tp.n_knots = iso_x.shape[0]
@@ -210,9 +228,10 @@ def predict_two_phase(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: 
         out = (torch.empty(n, dtype=torch.float32, device=x.device), torch.empty(n, dtype=torch.float32, device=x.device),
                torch.empty(n, dtype=torch.float64, device=x.device))
     pt, pred, kv = out
-    _dev(pt, "p_tool", torch.float32)
-    _dev(pred, "pred_len", torch.float32)
-    _dev(kv, "kv_bytes", torch.float64)
+    if pt is not None:
+        _shape(_dev(pt, "p_tool", torch.float32), "p_tool", (n,))
+    _shape(_dev(pred, "pred_len", torch.float32), "pred_len", (n,))
+    _shape(_dev(kv, "kv_bytes", torch.float64), "kv_bytes", (n,))
     st = lib.maestro_predict_two_phase(ctypes.byref(p), ctypes.byref(tp), n, _ptr(x), _ptr(prompt_len),
                                        _ptr(model_id), _ptr(role_id), _ptr(tool_avail), _ptr(kv_bytes_per_token),
                                        kv_bytes_per_token.shape[0], _ptr(pt), _ptr(pred), _ptr(kv), _stream(stream))
@@ -241,7 +260,9 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
     _dev(queue_s, "queue_s", torch.float32)
     M = free_bytes.shape[0]
     K = decode_s_per_token.shape[0]
-    if pred_len.shape[0] != n or kv_bytes.shape[0] != n:
+    if model_id.dim() != 1 or free_bytes.dim() != 1 or decode_s_per_token.dim() != 1:
+        raise ValueError("model_id, free_bytes and decode_s_per_token must be one-dimensional")
+    if pred_len.shape != (n,) or kv_bytes.shape != (n,):
         raise ValueError("per-stage inputs must have the same length")
     if act_s is not None:
         _dev(act_s, "act_s", torch.float32)
@@ -250,16 +271,17 @@ def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor
     else:
         _dev(cold_s, "cold_s", torch.float32)
         _dev(resident_mask, "resident_mask", torch.int64)
-        if cold_s.shape[0] != M or resident_mask.shape[0] != M:
+        if cold_s.shape != (M,) or resident_mask.shape != (M,):
             raise ValueError("per-node inputs must have the same length")
-    if queue_s.shape[0] != M:
+    if queue_s.shape != (M,):
         raise ValueError("per-node inputs must have the same length")
     if out is None:
         out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
                torch.empty((n, k), dtype=torch.float32, device=model_id.device))
     idx, sc = out
-    _dev(idx, "node_idx", torch.int32)
-    _dev(sc, "score", torch.float32)
+    _shape(_dev(idx, "node_idx", torch.int32), "node_idx", (n, k))
+    _shape(_dev(sc, "score", torch.float32), "score", (n, k))
+    _workspace(workspace)
     ws_bytes = route_workspace_bytes(n, decode_s_per_token.shape[0], M, k)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=model_id.device)
@@ -306,9 +328,11 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
                     (bounds, "bounds")):
         _dev(t, name, torch.float32)
     M = free_bytes.shape[0]
-    if src_id.shape[0] != n or class_id.shape[0] != n or kv_bytes.shape[0] != n:
+    if model_id.dim() != 1 or free_bytes.dim() != 1:
+        raise ValueError("model_id and free_bytes must be one-dimensional")
+    if src_id.shape != (n,) or class_id.shape != (n,) or kv_bytes.shape != (n,):
         raise ValueError("per-stage inputs must have the same length")
-    if queue_ms.shape[0] != M:
+    if queue_ms.shape != (M,):
         raise ValueError("per-node inputs must have the same length")
     if act_matrix is not None:
         _dev(act_matrix, "act_matrix", torch.float32)
@@ -317,7 +341,7 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
     else:
         _dev(act_ms, "act_ms", torch.float32)
         _dev(resident_mask, "resident_mask", torch.int64)
-        if act_ms.shape[0] != M or resident_mask.shape[0] != M:
+        if act_ms.shape != (M,) or resident_mask.shape != (M,):
             raise ValueError("per-node inputs must have the same length")
     if plans is not None:
         _dev(plans, "plans", torch.uint8)
@@ -325,7 +349,7 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
             raise ValueError("plans must be uint8 [n_nodes][128]")
     if deg_ms is not None:
         _dev(deg_ms, "deg_ms", torch.float32)
-        if deg_ms.shape[0] != M:
+        if deg_ms.shape != (M,):
             raise ValueError("per-node inputs must have the same length")
     elif plans is None:
         raise ValueError("deg_ms is required without plans")
@@ -337,8 +361,8 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
         out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
                torch.empty((n, k), dtype=torch.float32, device=model_id.device))
     idx, fit = out
-    _dev(idx, "node_idx", torch.int32)
-    _dev(fit, "fitness", torch.float32)
+    _shape(_dev(idx, "node_idx", torch.int32), "node_idx", (n, k))
+    _shape(_dev(fit, "fitness", torch.float32), "fitness", (n, k))
     st = lib.maestro_route_fitness(n, _ptr(model_id), _ptr(src_id), _ptr(class_id), _ptr(kv_bytes),
                                    int(n_models), M, rtt_ms.shape[0], class_weights.shape[0],
                                    _ptr(free_bytes), _ptr(queue_ms), _ptr(act_ms), _ptr(resident_mask),
@@ -366,7 +390,9 @@ def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, e
     if M < 0:
         raise ValueError("engine_offset holds n_nodes + 1 entries")
     E = engine_level.shape[0]
-    if engine_freed_bytes.shape[0] != E or engine_cost_ms.shape[0] != E:
+    if engine_offset.dim() != 1 or engine_level.dim() != 1:
+        raise ValueError("engine_offset and engine_level must be one-dimensional")
+    if engine_freed_bytes.shape != (E,) or engine_cost_ms.shape != (E,):
         raise ValueError("per-engine inputs must have the same length")
     if out is None:
         out = torch.empty((M, PLAN_BYTES), dtype=torch.uint8, device=engine_offset.device)
@@ -398,7 +424,7 @@ def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: t
     M, K = tier.shape
     if out is None:
         out = torch.empty((M, K), dtype=torch.float32, device=tier.device)
-    _dev(out, "act_ms", torch.float32)
+    _shape(_dev(out, "act_ms", torch.float32), "act_ms", (M, K))
     st = lib.maestro_activation_latency(M, K, _ptr(tier) if M else None, _ptr(model_bytes), _ptr(tier_bw),
                                         _ptr(tier_setup_ms), float(unit), _ptr(out) if M else None, _stream(stream))
     _check("maestro_activation_latency", st)
@@ -412,14 +438,14 @@ def adaptive_rho(kv_actual: torch.Tensor, kv_pred: torch.Tensor, beta: float, q:
     _dev(kv_actual, "kv_actual", torch.float64)
     _dev(kv_pred, "kv_pred", torch.float64)
     m = kv_actual.shape[0]
-    if kv_pred.shape != (m,):
+    if kv_actual.dim() != 1 or kv_pred.shape != (m,):
         raise ValueError("kv_actual and kv_pred must have the same length")
     if out is None:
         out = (torch.empty(m, dtype=torch.float32, device=kv_actual.device),
                torch.empty(1, dtype=torch.float32, device=kv_actual.device))
     ew, rho = out
-    _dev(ew, "ewma", torch.float32)
-    _dev(rho, "rho", torch.float32)
+    _shape(_dev(ew, "ewma", torch.float32), "ewma", (m,))
+    _shape(_dev(rho, "rho", torch.float32), "rho", (1,))
     st = lib.maestro_adaptive_rho(_ptr(kv_actual), _ptr(kv_pred), m, float(beta), float(q), _ptr(ew), _ptr(rho),
                                   _stream(stream))
     _check("maestro_adaptive_rho", st)
@@ -434,7 +460,7 @@ def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,
     _dev(values, "values", torch.float32)
     if out is None:
         out = torch.empty(2, dtype=torch.float32, device=values.device)
-    _dev(out, "out", torch.float32)
+    _shape(_dev(out, "out", torch.float32), "out", (2,))
     st = lib.maestro_quantiles(_ptr(values), values.numel(), float(q_lo), float(q_hi), _ptr(out),
                                _stream(stream))
     _check("maestro_quantiles", st)
@@ -461,11 +487,13 @@ def prioritize(chain_offset: torch.Tensor, stage_latency_s: torch.Tensor, deadli
     _dev(deadline_us, "deadline_us", torch.int64)
     W = chain_offset.shape[0] - 1
     S = stage_latency_s.shape[0]
-    if deadline_us.shape[0] != W:
+    if chain_offset.dim() != 1 or W < 0 or stage_latency_s.dim() != 1:
+        raise ValueError("chain_offset [W + 1] and stage_latency_s [S] must be one-dimensional")
+    if deadline_us.shape != (W,):
         raise ValueError("one deadline per workflow")
     if cursor is not None:
         _dev(cursor, "cursor", torch.int32)
-        if cursor.shape[0] != W:
+        if cursor.shape != (W,):
             raise ValueError("one cursor per workflow")
     dev = chain_offset.device
     if out is None:
@@ -473,6 +501,11 @@ def prioritize(chain_offset: torch.Tensor, stage_latency_s: torch.Tensor, deadli
                torch.empty(W, dtype=torch.int32, device=dev),
                torch.empty(W, dtype=torch.int32, device=dev))
     rem, key, order = out
+    if rem is not None:
+        _shape(_dev(rem, "remaining_us", torch.int64), "remaining_us", (S,))
+    _shape(_dev(key, "slack_key", torch.int32), "slack_key", (W,))
+    _shape(_dev(order, "order", torch.int32), "order", (W,))
+    _workspace(workspace)
     ws_bytes = prioritize_workspace_bytes(W, S)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)

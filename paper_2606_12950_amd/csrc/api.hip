@@ -207,7 +207,7 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
       return MAESTRO_ERR_INVALID_ARG;
   }
   if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
-  return maestro::launch_route_fitness(n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src,
+  return maestro::launch_route_fitness(n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes,
                                        free_bytes, queue_ms, act_ms, resident_mask, act_matrix, deg_ms,
                                        plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,
                                        as_stream(stream));

@@ -120,7 +120,7 @@ template <int KT, int kReady, bool kPlans, bool kMulti>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_models, int32_t n_nodes,
-    int32_t n_src, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
+    int32_t n_src, int32_t n_classes, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
     const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
     const float* __restrict__ act_matrix, const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
     const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
@@ -170,17 +170,24 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
   mask_t mbit = 0;
   int src = 0, model = 0;
+  bool ok = false;          // a stage whose model, source and class ids are in range
   if (valid) {
-    need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
-    needf = __double2float_rn(need);
-    const float* wt = class_weights + 3 * class_id[stage];
-    gamma = wt[0];
-    lambda = wt[1];
-    mu = wt[2];
-    omg = __fsub_rn(1.0f, gamma);
-    model = model_id[stage];
-    mbit = kMat ? 0 : (mask_t)1 << model;
-    src = src_id[stage];
+    const int32_t m = model_id[stage], s = src_id[stage], c = class_id[stage];
+    ok = (uint32_t)m < (uint32_t)n_models && (uint32_t)s < (uint32_t)n_src && (uint32_t)c < (uint32_t)n_classes;
+    if (ok) {
+      need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
+      needf = __double2float_rn(need);
+      const float* wt = class_weights + 3 * c;
+      gamma = wt[0];
+      lambda = wt[1];
+      mu = wt[2];
+      omg = __fsub_rn(1.0f, gamma);
+      model = m;
+      mbit = kMat ? 0 : (mask_t)1 << model;
+      src = s;
+    } else {
+      need = NAN;             // an id out of range: no node admits the stage, no plan is tried
+    }
   }
   const float* prox_row = s_prox + src * kProxStride;
 
@@ -274,7 +281,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
           const float sc = score(i + u * G, t[u], ad[u], px[u], t[u].w);
           best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u * G);
         }
-        if (valid && !(fits[0] && fits[1] && fits[2] && fits[3])) {
+        if (ok && !(fits[0] && fits[1] && fits[2] && fits[3])) {
 #pragma unroll
           for (int u = 0; u < 4; ++u)
             if (!fits[u]) queue(i + u * G);
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         const bool fits = need <= ad.free;
         const float sc = score(i, t, ad, prox_row[i], t.w);
         best.push_increasing(fits ? -sc : INFINITY, c0 + i);
-        if (valid && !fits) queue(i);
+        if (ok && !fits) queue(i);
       }
     } else {
 #pragma unroll 4
@@ -645,7 +652,7 @@ __global__ __launch_bounds__(kSelectThreads) void ewma_apply_kernel(const double
 
 maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
                                     const int32_t* class_id, const double* kv_bytes, int32_t n_models,
-                                    int32_t n_nodes, int32_t n_src, const double* free_bytes,
+                                    int32_t n_nodes, int32_t n_src, int32_t n_classes, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
                                     const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,
@@ -664,14 +671,14 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
   do {                                                                                                          \
     if (g_log2 > 0)                                                                                             \
       fitness_kernel<KT, RD, PL, true><<<grid, block, 0, stream>>>(                                             \
-          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, free_bytes, queue_ms, act_ms,      \
-          resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,  \
-          g_log2);                                                                                              \
+          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
+          act_ms, resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx,   \
+          fitness, g_log2);                                                                                     \
     else                                                                                                        \
       fitness_kernel<KT, RD, PL, false><<<grid, block, 0, stream>>>(                                            \
-          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, free_bytes, queue_ms, act_ms,      \
-          resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,  \
-          0);                                                                                                   \
+          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
+          act_ms, resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx,   \
+          fitness, 0);                                                                                          \
   } while (0)
 #define MAESTRO_FIT_RD(KT, PL)                                       \
   do {                                                               \

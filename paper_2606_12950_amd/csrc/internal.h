@@ -37,7 +37,7 @@ constexpr int kMaxFitnessSources = 16;
 constexpr int kMaxFitnessClasses = 16;
 maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
                                     const int32_t* class_id, const double* kv_bytes, int32_t n_models,
-                                    int32_t n_nodes, int32_t n_src, const double* free_bytes,
+                                    int32_t n_nodes, int32_t n_src, int32_t n_classes, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
                                     const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,

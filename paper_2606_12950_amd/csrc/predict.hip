@@ -50,13 +50,20 @@ __device__ __forceinline__ void load_acc_layout(const float* __restrict__ src, i
   }
 }
 
+// alpha(M) of a stage's model, as float64; a model id outside [0, n_models) gives NaN, so that
+// stage's KV demand is NaN and no node admits it.
+__device__ __forceinline__ double alpha_of(const float* __restrict__ alpha, int32_t model, int32_t n_models) {
+  return (uint32_t)model < (uint32_t)n_models ? (double)alpha[model] : (double)NAN;
+}
+
 // Softmax over the B = 32*BT logits of each row, expected length, Eq. 3 KV bytes.
 // Lanes r and r + 32 hold complementary halves of row r's logits.
 template <int BT>
 __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const float* __restrict__ b_last,
                                                 const float* __restrict__ centre, int h, int64_t row, int64_t n,
                                                 int32_t prompt, int32_t model, const float* __restrict__ alpha,
-                                                float* __restrict__ pred_len, double* __restrict__ kv_bytes) {
+                                                int32_t n_models, float* __restrict__ pred_len,
+                                                double* __restrict__ kv_bytes) {
   float z[BT][16], c[BT][16];
   float mx = -INFINITY;
 #pragma unroll
@@ -90,7 +97,7 @@ __device__ __forceinline__ void length_epilogue(const f32x16 (&logit)[BT], const
   if (h == 0 && row < n) {
     const float pred = sc / se;
     pred_len[row] = pred;
-    kv_bytes[row] = ((double)prompt + (double)pred) * (double)alpha[model];
+    kv_bytes[row] = ((double)prompt + (double)pred) * alpha_of(alpha, model, n_models);
   }
 }
 
@@ -147,8 +154,8 @@ __device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const f
                                               const float* __restrict__ coef, const float* __restrict__ kx,
                                               const float* __restrict__ ky, const TwoPhaseArgs& tp, int64_t row,
                                               int32_t prompt, int32_t model, int32_t tools,
-                                              const float* __restrict__ alpha, float* __restrict__ pred_len,
-                                              double* __restrict__ kv_bytes) {
+                                              const float* __restrict__ alpha, int32_t n_models,
+                                              float* __restrict__ pred_len, double* __restrict__ kv_bytes) {
   float p = 0.0f;
   if (tools != 0) {
     const float s = 1.0f / (1.0f + __expf(-(z0 + b_last[0])));
@@ -171,7 +178,7 @@ __device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const f
   const float L = fminf(expm1f(fmaxf(y, 0.0f)), tp.max_len);
   if (tp.p_tool) tp.p_tool[row] = p;
   pred_len[row] = L;
-  kv_bytes[row] = ((double)prompt + (double)L) * (double)alpha[model];
+  kv_bytes[row] = ((double)prompt + (double)L) * alpha_of(alpha, model, n_models);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -809,14 +816,14 @@ void mlp3_bf16_kernel(
       if ((G > 1 || h == 0) && row < n)
         two_phase_row(mine ? z0[G - 1] : z0[0], mine ? zg[G - 1] : zg[0], mine ? gh[G - 1] : gh[0], s_b3, s_c,
                       s_kx, s_ky, tp, row, s_meta[parity][0][local], s_meta[parity][1][local],
-                      s_meta[parity][3][local], s_alpha, pred_len, kv_bytes);
+                      s_meta[parity][3][local], s_alpha, n_models, pred_len, kv_bytes);
     } else {
 #pragma unroll
       for (int gr = 0; gr < G; ++gr) {
         const int local = (G * wave + gr) * kRowsPerWave + r32;
         const int64_t row = tile * kTileRows + local;
         length_epilogue<BT>(logit[gr], s_b3, s_c, h, row, n, s_meta[parity][0][local], s_meta[parity][1][local],
-                            s_alpha, pred_len, kv_bytes);
+                            s_alpha, n_models, pred_len, kv_bytes);
       }
     }
   }
@@ -831,7 +838,8 @@ __global__ __launch_bounds__(kThreads) void mlp2_f32_kernel(
     const float* __restrict__ x, const float* __restrict__ w1, const float* __restrict__ w2,
     const float* __restrict__ b1, const float* __restrict__ b2, const float* __restrict__ centre,
     int64_t n, const int32_t* __restrict__ prompt_len, const int32_t* __restrict__ model_id,
-    const float* __restrict__ alpha, float* __restrict__ pred_len, double* __restrict__ kv_bytes) {
+    const float* __restrict__ alpha, int32_t n_models, float* __restrict__ pred_len,
+    double* __restrict__ kv_bytes) {
   static_assert(D % 8 == 0 && H % 32 == 0 && B % 32 == 0, "tile shape");
   constexpr int KS1 = D / 2;         // K-steps of layer 1; lane-half h covers inputs [h*KS1, (h+1)*KS1)
   constexpr int NB1 = H / 32;
@@ -911,7 +919,7 @@ __global__ __launch_bounds__(kThreads) void mlp2_f32_kernel(
 
   const int32_t prompt = row < n ? prompt_len[row] : 0;
   const int32_t model = row < n ? model_id[row] : 0;
-  length_epilogue<BT>(logit, b2, centre, h, row, n, prompt, model, alpha, pred_len, kv_bytes);
+  length_epilogue<BT>(logit, b2, centre, h, row, n, prompt, model, alpha, n_models, pred_len, kv_bytes);
 }
 
 bool dims_are(const maestro_predictor& p, int32_t layers, int32_t dtype, const int32_t* d) {
@@ -971,7 +979,7 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
     mlp2_f32_kernel<64, 128, 32><<<grid, block, 0, stream>>>(
         static_cast<const float*>(x), static_cast<const float*>(p.weight[0]),
         static_cast<const float*>(p.weight[1]), p.bias[0], p.bias[1], p.bin_centre, n, prompt_len,
-        model_id, kv_bytes_per_token, pred_len, kv_bytes);
+        model_id, kv_bytes_per_token, n_models, pred_len, kv_bytes);
   } else if (dims_are(p, 3, MAESTRO_BF16, kBf16Mid) || dims_are(p, 3, MAESTRO_BF16, kBf16Wide)) {
     return launch_mlp3<false>(p, n, x, prompt_len, model_id, kv_bytes_per_token, n_models, pred_len, kv_bytes,
                               TwoPhaseArgs{}, stream);

@@ -65,10 +65,15 @@ __global__ __launch_bounds__(kThreads) void route_kernel(
   mask_t mbit = 0;
   int32_t model = 0;
   if (valid) {
-    model = model_id[stage];
-    need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
-    exec_s = __fmul_rn(pred_len[stage], decode_s_per_token[model]);
-    mbit = kMat ? 0 : (mask_t)1 << model;
+    const int32_t m = model_id[stage];
+    if ((uint32_t)m < (uint32_t)n_models) {
+      model = m;
+      need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
+      exec_s = __fmul_rn(pred_len[stage], decode_s_per_token[model]);
+      mbit = kMat ? 0 : (mask_t)1 << model;
+    } else {
+      need = NAN;             // a model id out of range: no node admits the stage (NaN <= x is false)
+    }
   }
 
   TopK<KT> best;
@@ -226,6 +231,13 @@ __global__ __launch_bounds__(kThreads) void walk_route_kernel(
   __syncthreads();
   if (i >= n) return;
   const int32_t m = model_id[i];
+  if ((uint32_t)m >= (uint32_t)n_models) {   // a model id out of range: no node
+    for (int t = 0; t < k; ++t) {
+      node_idx[i * k + t] = -1;
+      score[i * k + t] = INFINITY;
+    }
+    return;
+  }
   const double need = (rho == 0.0) ? kv_bytes[i] : __dmul_rn(kv_bytes[i], 1.0 + rho);
   const float exec_s = __fmul_rn(pred_len[i], decode_s_per_token[m]);
   const NodeEntry* list = lists + (size_t)m * n_nodes;
