@@ -11,7 +11,8 @@ import oracle
 import paper_2606_12950_amd as M
 from paper_2606_12950_amd import pipeline
 from paper_2606_12950_amd import workload as W
-from test_gpu_fitness import GB, _engines, _nodes, assert_same, gpu_fitness, gpu_fitness_plans
+from test_gpu_fitness import (GB, _engines, _nodes, assert_same, gpu_fitness, gpu_fitness_act, gpu_fitness_plans,
+                              oracle_fitness_act)
 from test_gpu_parity import ALGOS, assert_route_equal
 
 pytestmark = pytest.mark.gpu
@@ -114,4 +115,27 @@ def test_fitness_flags_out_of_range_ids(which, plans):
                                nodes["queue_ms"], nodes["act_ms"], nodes["resident_mask"], nodes["deg_ms"],
                                nodes["rtt_ms"], np.asarray(weights, np.float32), np.asarray(bounds, np.float32), k=k,
                                engines=eng if plans else None)
+    assert_same((gi[ok], gf[ok]), ref)
+
+
+@pytest.mark.parametrize("n_models", [16, 40])
+@pytest.mark.parametrize("which", ["model", "src", "cls"])
+def test_fitness_with_act_matrix_flags_out_of_range_ids(which, n_models):
+    # T_act from a [node][model] matrix (both chunk classes: up to 16 and up to 64 models), plans
+    rng = np.random.default_rng(15 + n_models)
+    n, M_, n_src, k = 1200, 200, 4, 3
+    nodes = _nodes(rng, M_, n_src)
+    ids = dict(model=rng.integers(0, n_models, n).astype(np.int32), src=rng.integers(0, n_src, n).astype(np.int32),
+               cls=rng.integers(0, 2, n).astype(np.int32))
+    ids[which], bad = _spoil(rng, ids[which], dict(model=n_models, src=n_src, cls=2)[which])
+    kv = rng.uniform(0, 250, n) * GB
+    act = rng.uniform(0, 20000, (M_, n_models)).astype(np.float32)
+    weights, bounds = [[0.25, 1, 1], [0.1, 1, 1]], [0, 80, 0, 25000, 0, 500]
+    eng = (*_engines(rng, M_), 2000.0)
+    gi, gf = gpu_fitness_act(ids["model"], ids["src"], ids["cls"], kv, nodes, weights, bounds, act, n_models, k=k,
+                             eng=eng)
+    assert bad.any() and np.all(gi[bad] == -1) and np.all(gf[bad] == -np.inf)
+    ok = ~bad
+    ref = oracle_fitness_act(ids["model"][ok], ids["src"][ok], ids["cls"][ok], kv[ok], nodes, weights, bounds, act,
+                             n_models, k=k, eng=eng)
     assert_same((gi[ok], gf[ok]), ref)
