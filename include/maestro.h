@@ -204,25 +204,34 @@ MAESTRO_API maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, 
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Minimum-impact degradation plans of a node (Alg. 2) and their disruption cost (Eq. 4), for
- * every possible shortfall: the node's engines (at most MAESTRO_MAX_PLAN_ENGINES) in priority
- * order -- ascending level, lower engine index first -- with, for the plan made of the first
- * j + 1 of them, the bytes it frees and its cost. */
-#define MAESTRO_MAX_PLAN_ENGINES 8
+ * every possible shortfall. Alg. 2 takes the node's engines in priority order -- ascending
+ * action level, the lower engine index first on equal levels -- and stops before the first
+ * engine once the freed memory reaches the shortfall R, so its plan for R is the shortest prefix
+ * of that order whose freed bytes reach R. A step p of a node describes the prefix made of its
+ * first p + 1 engines in that order. */
+typedef struct maestro_plan_step {
+  double freed;      /* bytes freed by the prefix: the running sum in order (float64), kept
+                        non-decreasing (the largest sum so far; the sum itself when no action
+                        frees a negative amount)                                              */
+  float cost;        /* its cost: the running sum of c(e, a) in order (float32), + c_int when
+                        the prefix holds an engine of level 4 or 5                             */
+  int32_t engine;    /* the engine taken at this step (index into the engine arrays)           */
+} maestro_plan_step;
+
+/* Per node, the first MAESTRO_PLAN_RECORD_STEPS steps in one 128-byte record (what the fitness
+ * router stages on chip); a node with more engines continues in the step array. */
+#define MAESTRO_PLAN_RECORD_STEPS 8
 typedef struct maestro_deg_plan {
-  double freed[MAESTRO_MAX_PLAN_ENGINES];  /* running sum of freed bytes, float64, in order;
-                                              kept non-decreasing (the largest sum so far, the
-                                              sum itself for non-negative frees); +inf past
-                                              n_engines                                       */
-  float cost[MAESTRO_MAX_PLAN_ENGINES];    /* running sum of costs (float32, in order) + c_int
-                                              when an engine of level 4 or 5 is in the plan;
-                                              0 past n_engines                                */
-  int32_t n_engines;                       /* 0 .. MAESTRO_MAX_PLAN_ENGINES                   */
-  int32_t reserved[7];                     /* 128-byte record                                 */
+  double freed[MAESTRO_PLAN_RECORD_STEPS];  /* steps 0..7: freed; +inf past n_engines          */
+  float cost[MAESTRO_PLAN_RECORD_STEPS];    /* steps 0..7: cost; 0 past n_engines              */
+  int32_t n_engines;                        /* the node's engine count (any number >= 0)        */
+  int32_t first_step;                       /* index of the node's step 0 in the step array    */
+  int32_t reserved[6];                      /* 128-byte record                                 */
 } maestro_deg_plan;
 
-/* Plan records of n_nodes nodes from their engine lists (CSR):
+/* Plan records and steps of n_nodes nodes from their engine lists (CSR):
  *   engine_offset       [n_nodes + 1] int32, non-decreasing, engine_offset[0] = 0; node j owns
- *                       engines [engine_offset[j], engine_offset[j+1]), at most 8 of them
+ *                       engines [engine_offset[j], engine_offset[j+1]), any number of them
  *   engine_level        [E] int32 in 1..5: the action Alg. 2 takes for the engine -- 1 an
  *                       idle-running model goes to sleep, 2 a sleeping model is evicted, 3 a
  *                       pending sleep is stopped, 4 an active model's KV is swapped out, 5 an
@@ -231,16 +240,18 @@ typedef struct maestro_deg_plan {
  *   engine_cost_ms      [E] float32: restoration latency of the action, c(e, a)
  *   c_int_ms            the interrupt penalty of Eq. 4 (the SLO violation threshold)
  *   plans (out)         [n_nodes] maestro_deg_plan, 16-byte aligned
- * A shortfall R > 0 is met by the shortest prefix with freed[j] >= R (Alg. 2 checks before each
- * engine); its cost is cost[j]; no such prefix means the plan fails. Device pointers, no
- * workspace; n_nodes == 0 launches nothing. The engine arrays may be NULL when E == 0.
- * Errors: INVALID_ARG for n_nodes < 0, a NaN c_int_ms, a NULL or misaligned offset/plan array,
- * or a misaligned engine array. A node with more than MAESTRO_MAX_PLAN_ENGINES engines breaks
- * the contract (only its first MAESTRO_MAX_PLAN_ENGINES are used). */
+ *   steps (out)         [E] maestro_plan_step, 16-byte aligned, E = engine_offset[n_nodes]:
+ *                       node j's steps at [engine_offset[j], engine_offset[j+1]), in order
+ * A shortfall R > 0 is met by the first step with freed >= R, at that step's cost; no such step
+ * means the plan fails (the node cannot admit the stage). One thread per node: a node of up to
+ * 8 engines is sorted in registers, a larger one by counting ranks (time quadratic in its
+ * engine count). Device pointers, no workspace; n_nodes == 0 launches nothing. The engine
+ * arrays may be NULL when E == 0. Errors: INVALID_ARG for n_nodes < 0, a NaN c_int_ms, a NULL
+ * or misaligned offset, plan or step array, or a misaligned engine array. */
 MAESTRO_API maestro_status maestro_degradation_plans(int32_t n_nodes, const int32_t* engine_offset,
                              const int32_t* engine_level, const double* engine_freed_bytes,
                              const float* engine_cost_ms, float c_int_ms, maestro_deg_plan* plans,
-                             void* stream);
+                             maestro_plan_step* steps, void* stream);
 
 /* Routing by fitness (Sec. III-D: Eq. 5 with T_ready of Eq. 6; Alg. 3). Per stage i with
  * model m = model_id[i], source s = src_id[i] and weights (gamma, lambda, mu) =
@@ -249,15 +260,15 @@ MAESTRO_API maestro_status maestro_degradation_plans(int32_t n_nodes, const int3
  *   node j is feasible iff need <= free_bytes[j]                     (equality admits)
  *                      or, with plans, its plan meets the shortfall R = need - free_bytes[j]
  *   C_deg = deg_ms[j], or with plans: 0 when need <= free_bytes[j], else the plan's cost
- *   norm_X(x) = clamp((x - lo_X) * inv_X, 0, 1), inv_X = hi_X > lo_X ? 1 / (hi_X - lo_X) : 0,
- *               with (lo_X, hi_X) the window bounds of metric X (see maestro_quantiles)
+ *   norm_X(x) = clamp((x - lo_X) / (hi_X - lo_X), 0, 1), or 0 when hi_X <= lo_X, with
+ *               (lo_X, hi_X) the window bounds of metric X (see maestro_quantiles)
  *   prox  = 1 - norm_RTT(rtt_ms[s][j])                    network proximity
- *   fit   = min(1, fl32(need) * (1 / fl32(free_bytes[j])))   best fit of R_need to the headroom
- *           (1 when fl32(free_bytes[j]) == 0)
+ *   fit   = fl32(need) / fl32(free_bytes[j])      best fit of R_need to the headroom, <= 1 on
+ *           a feasible node (0 when fl32(free_bytes[j]) <= 0)
  *   A     = gamma * prox + (1 - gamma) * fit               affinity
  *   T_ready = queue_ms[j] + T_act,  T_act = act_matrix[j][m] when given, else
  *             (bit m of resident_mask[j] ? 0 : act_ms[j])                       (Eq. 6)
- *   S     = (A - lambda * norm_READY(T_ready)) - mu * norm_DEG(C_deg)
+ *   S     = A - (lambda * norm_READY(T_ready) + mu * norm_DEG(C_deg))
  *   every operation float32 round-to-nearest, in exactly this order; output the k feasible
  *   nodes with the largest S, the lower node index first on equal S (the strict ">" of Alg.
  *   3); when fewer than k nodes are feasible the tail is padded with node -1 and -inf.
@@ -272,8 +283,9 @@ MAESTRO_API maestro_status maestro_degradation_plans(int32_t n_nodes, const int3
  *                       resident_mask are unused (may be NULL)
  *   deg_ms              [n_nodes] float32: disruption penalty C_deg reported by the runtime (ms);
  *                       unused (may be NULL) when plans are given
- *   plans               [n_nodes] maestro_deg_plan from maestro_degradation_plans, or NULL
- *                       (16-byte aligned); the byte counts must be finite
+ *   plans, plan_steps   [n_nodes] maestro_deg_plan and [E] maestro_plan_step from
+ *                       maestro_degradation_plans (16-byte aligned), or both NULL; the byte
+ *                       counts must be finite
  *   rtt_ms              [n_src][n_nodes] float32: round-trip time from each source (ms)
  *   class_weights       [n_classes][3] float32: (gamma, lambda, mu) per stage class
  *   bounds              [6] float32: (lo, hi) of RTT, T_ready, C_deg, in that order
@@ -285,7 +297,8 @@ MAESTRO_API maestro_status maestro_route_fitness(int64_t n, const int32_t* model
                              int32_t n_nodes, int32_t n_src, int32_t n_classes,
                              const double* free_bytes, const float* queue_ms, const float* act_ms,
                              const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
-                             const maestro_deg_plan* plans, const float* rtt_ms,
+                             const maestro_deg_plan* plans, const maestro_plan_step* plan_steps,
+                             const float* rtt_ms,
                              const float* class_weights, const float* bounds, double rho, int32_t k,
                              int32_t* node_idx, float* fitness, void* stream);
 

@@ -21,10 +21,13 @@
  *                smallest (score, node index) pairs in lexicographic order. The strict ">" of
  *                Alg. 3 keeps the first of equal scores, i.e. the lowest index.
  *   fitness    : Alg. 3 with the fitness of Eq. 5: among the feasible nodes, the largest
- *                S = A - lambda T_ready - mu C_deg, A = gamma (1 - norm RTT) + (1 - gamma) fit,
+ *                S = A - (lambda T_ready + mu C_deg), A = gamma (1 - norm RTT) + (1 - gamma) fit,
  *                fit = R_need / headroom (best fit), T_ready = T_q + T_act (Eq. 6), each metric
- *                min-max normalised onto [0, 1] with window bounds and clipped; float32 in a
- *                fixed operation order; k best (fitness, lowest index).
+ *                min-max normalised onto [0, 1] with window bounds, (x - lo) / (hi - lo), and
+ *                clipped; float32 (every operation rounded to nearest) in that order; k best
+ *                (fitness, lowest index). C_deg from engine lists is the cost (Eq. 4) of the
+ *                shortest priority-ordered prefix of the node's engines that frees the
+ *                shortfall (Alg. 2), any number of engines.
  *   two-phase  : the same network read as heads (Sec. III-B): a tool-intent logit through a
  *                sigmoid and an isotonic calibration table (Eq. 1), 0 without tools; the
  *                stage's role regressor (or the shared one) on log(1 + L), fed the calibrated
@@ -373,48 +376,63 @@ int oracle_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t 
   return ORACLE_OK;
 }
 
-/* robust min-max normalisation onto [0, 1] with window bounds lo, hi (values outside the
- * bounds clip); a degenerate window (hi <= lo) maps everything to 0. float32 throughout. */
-static float norm_inv(float lo, float hi) { return hi > lo ? 1.0f / (hi - lo) : 0.0f; }
-static float norm01(float x, float lo, float inv) {
-  float t = (x - lo) * inv;
+/* Robust min-max normalisation (Sec. III-D): (x - lo) / (hi - lo) clipped to [0, 1], with the
+ * window bounds lo, hi of the metric; a degenerate window (hi <= lo) maps everything to 0.
+ * float32 subtraction and division, each rounded to nearest. */
+static float norm01(float x, float lo, float hi) {
+  if (!(hi > lo)) return 0.0f;
+  float t = (x - lo) / (hi - lo);
   if (t < 0.0f) t = 0.0f;
   if (t > 1.0f) t = 1.0f;
   return t;
 }
 
-/* Alg. 2 + Eq. 4 on one node: the engines of the node (levels 1..5 = the action taken for each:
- * idle-running -> sleeping, evict sleeping, stop a pending sleep, swap out an active engine's KV,
- * abort an active execution) in priority order (SortByPriority: ascending level, lower engine
- * index first), taken greedily until the freed memory covers R. Returns 0 when the plan meets R
- * (cost in *c_deg), 1 on Failure. Levels 4 and 5 preempt/abort active work (I_active). */
+/* The minimum-impact plan of Alg. 2 and its cost, Eq. 4, on one node. The greedy loop of Alg. 2
+ * takes engines in priority order (SortByPriority: ascending action level 1..5, the lower engine
+ * index first on equal levels) and stops before the first engine once the freed memory reaches
+ * R, so the plan it returns is the shortest prefix of that order whose freed bytes (summed in
+ * float64, in order) reach R -- the empty prefix when R <= 0 -- and it fails when even the whole
+ * order frees less. The plan's cost is the float32 sum, in order, of its engines' restoration
+ * latencies c(e, a), plus c_int when it holds an engine of level 4 or 5 (the active work of that
+ * engine is preempted or aborted). Returns 0 with the cost in *c_deg, or 1 on Failure. */
 typedef struct { int32_t level, idx; } eng_t;
-static int eng_less(eng_t a, eng_t b) { return a.level < b.level || (a.level == b.level && a.idx < b.idx); }
+static int eng_cmp(const void* pa, const void* pb) {
+  const eng_t* a = (const eng_t*)pa;
+  const eng_t* b = (const eng_t*)pb;
+  if (a->level != b->level) return a->level < b->level ? -1 : 1;
+  return (a->idx > b->idx) - (a->idx < b->idx);
+}
 
 static int degradation_plan(double R, int32_t e0, int32_t e1, const int32_t* level, const double* freed,
                             const float* cost, float c_int, float* c_deg) {
-  eng_t order[64];
-  int32_t ne = e1 - e0;
-  if (ne > 64) ne = 64;
-  for (int32_t i = 0; i < ne; ++i) {              /* SortByPriority: insertion sort, stable */
-    eng_t e = {level[e0 + i], e0 + i};
-    int32_t j = i;
-    while (j > 0 && eng_less(e, order[j - 1])) { order[j] = order[j - 1]; --j; }
-    order[j] = e;
-  }
-  double m_freed = 0.0;
-  float plan_cost = 0.0f;
-  int interrupt = 0;
+  const int32_t ne = e1 > e0 ? e1 - e0 : 0;
+  eng_t* order = (eng_t*)malloc(sizeof(eng_t) * (size_t)(ne > 0 ? ne : 1));
+  double* sum = (double*)malloc(sizeof(double) * (size_t)(ne + 1));
+  if (!order || !sum) abort();
   for (int32_t i = 0; i < ne; ++i) {
-    if (m_freed >= R) break;
-    const int32_t e = order[i].idx;
-    if (order[i].level >= 4) interrupt = 1;       /* Preempt / Abort */
-    m_freed += freed[e];                          /* EstimateFreedMemory */
-    plan_cost += cost[e];                         /* c(e, a) */
+    order[i].level = level[e0 + i];
+    order[i].idx = e0 + i;
   }
-  if (m_freed < R) return 1;                      /* Failure */
-  *c_deg = plan_cost + (interrupt ? c_int : 0.0f);  /* Eq. 4 */
-  return 0;
+  qsort(order, (size_t)ne, sizeof(eng_t), eng_cmp);     /* priority order */
+  sum[0] = 0.0;                                         /* freed bytes of the first p engines */
+  for (int32_t p = 1; p <= ne; ++p) sum[p] = sum[p - 1] + freed[order[p - 1].idx];
+  int32_t len = -1;                                     /* the shortest prefix reaching R */
+  for (int32_t p = 0; p <= ne && len < 0; ++p)
+    if (sum[p] >= R) len = p;
+  int status = 1;                                       /* Failure */
+  if (len >= 0) {
+    float total = 0.0f;
+    int interrupt = 0;
+    for (int32_t p = 0; p < len; ++p) {
+      total += cost[order[p].idx];
+      if (order[p].level >= 4) interrupt = 1;
+    }
+    *c_deg = total + (interrupt ? c_int : 0.0f);
+    status = 0;
+  }
+  free(order);
+  free(sum);
+  return status;
 }
 
 int oracle_degradation_cost(double R, int32_t n_engines, const int32_t* level, const double* freed,
@@ -440,10 +458,8 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
     return ORACLE_BAD_ARG;
   int status = ORACLE_OK;
   if (n_threads < 1) n_threads = 1;
-  /* window bounds of the three normalised metrics: RTT, T_ready, C_deg (milliseconds) */
-  const float inv_rtt = norm_inv(bounds[0], bounds[1]);
-  const float inv_ready = norm_inv(bounds[2], bounds[3]);
-  const float inv_deg = norm_inv(bounds[4], bounds[5]);
+  /* window bounds (lo, hi) of the three normalised metrics: RTT, T_ready, C_deg (milliseconds)
+   * are bounds[0..1], bounds[2..3], bounds[4..5] */
 
 #pragma omp parallel num_threads(n_threads)
   {
@@ -481,11 +497,12 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
             c_deg = deg_ms[nd];
           }
           /* Affinity: network proximity (decreasing in the normalised RTT) and best fit of
-           * R_need to the node's headroom (1 when the stage fills the headroom exactly) */
-          const float prox = 1.0f - norm01(rtt_row[nd], bounds[0], inv_rtt);
+           * R_need to the node's headroom, R_need / headroom (1 when the stage fills the
+           * headroom, at most 1 on a feasible node; a node without headroom admits only an
+           * empty demand and gets 0) */
+          const float prox = 1.0f - norm01(rtt_row[nd], bounds[0], bounds[1]);
           const float freef = (float)free_bytes[nd];
-          float fit = freef > 0.0f ? needf * (1.0f / freef) : 1.0f;
-          if (fit > 1.0f) fit = 1.0f;
+          const float fit = freef > 0.0f ? needf / freef : 0.0f;
           const float a = gamma * prox + (1.0f - gamma) * fit;
           /* RuntimeEstimate: T_ready = T_q + T_act (Eq. 6): T_act of model m on this node from the
            * per-(node, model) matrix, or else the node's activation latency unless m is resident */
@@ -497,8 +514,11 @@ int oracle_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_
             act = resident ? 0.0f : act_ms[nd];
           }
           const float ready = queue_ms[nd] + act;
-          /* Eq. 5: S = A - lambda * T_ready - mu * C_deg, on normalised metrics */
-          const float s = (a - lambda * norm01(ready, bounds[2], inv_ready)) - mu * norm01(c_deg, bounds[4], inv_deg);
+          /* Eq. 5 on normalised metrics: S = A - (lambda * T_ready + mu * C_deg), the two
+           * penalties summed before they are taken from the affinity */
+          const float penalty =
+              lambda * norm01(ready, bounds[2], bounds[3]) + mu * norm01(c_deg, bounds[4], bounds[5]);
+          const float s = a - penalty;
           c[nc].s = s;
           c[nc].n = nd;
           ++nc;

@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Sequence, Tuple
+from typing import NamedTuple, Optional, Sequence, Tuple
 
 import torch
 
@@ -27,8 +27,17 @@ EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "mae
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
 
-MAX_PLAN_ENGINES = 8
-PLAN_BYTES = 128   # one maestro_deg_plan record: freed f64[8], cost f32[8], n_engines i32, pad
+PLAN_RECORD_STEPS = 8   # steps held in a node's record; more engines continue in the step array
+PLAN_BYTES = 128   # one maestro_deg_plan record: freed f64[8], cost f32[8], n_engines, first_step, pad
+STEP_BYTES = 16    # one maestro_plan_step: freed f64, cost f32, engine i32
+
+
+class DegradationPlans(NamedTuple):
+    """Output of maestro_degradation_plans: ``records`` uint8 [n_nodes][128] (maestro_deg_plan)
+    and ``steps`` uint8 [max(E, 1)][16] (maestro_plan_step, node j's at [engine_offset[j],
+    engine_offset[j+1]))."""
+    records: torch.Tensor
+    steps: torch.Tensor
 
 
 class MaestroError(RuntimeError):
@@ -69,12 +78,12 @@ def load():
                                               P, P, P, i32, P, P, P, P]
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
-    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P,
+    lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P, P,
                                           f64, i32, P, P, P]
     lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, f64, P, P]
     lib.maestro_route_tiered.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P, P]
-    lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P]
+    lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
     for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize"):
@@ -305,7 +314,7 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
                   kv_bytes: torch.Tensor, free_bytes: torch.Tensor, queue_ms: torch.Tensor,
                   act_ms: torch.Tensor, resident_mask: torch.Tensor, deg_ms: Optional[torch.Tensor],
                   rtt_ms: torch.Tensor, class_weights: torch.Tensor, bounds: torch.Tensor,
-                  n_models: int, k: int = 1, rho: float = 0.0, plans: Optional[torch.Tensor] = None,
+                  n_models: int, k: int = 1, rho: float = 0.0, plans: Optional[DegradationPlans] = None,
                   act_matrix: Optional[torch.Tensor] = None,
                   out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
@@ -344,9 +353,12 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
         if act_ms.shape != (M,) or resident_mask.shape != (M,):
             raise ValueError("per-node inputs must have the same length")
     if plans is not None:
-        _dev(plans, "plans", torch.uint8)
-        if tuple(plans.shape) != (M, PLAN_BYTES):
-            raise ValueError("plans must be uint8 [n_nodes][128]")
+        _dev(plans.records, "plans.records", torch.uint8)
+        _dev(plans.steps, "plans.steps", torch.uint8)
+        if tuple(plans.records.shape) != (M, PLAN_BYTES):
+            raise ValueError("plans.records must be uint8 [n_nodes][128]")
+        if plans.steps.dim() != 2 or plans.steps.shape[1] != STEP_BYTES:
+            raise ValueError("plans.steps must be uint8 [E][16]")
     if deg_ms is not None:
         _dev(deg_ms, "deg_ms", torch.float32)
         if deg_ms.shape != (M,):
@@ -368,7 +380,8 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
                                    _ptr(free_bytes), _ptr(queue_ms), _ptr(act_ms), _ptr(resident_mask),
                                    _ptr(act_matrix),
                                    _ptr(deg_ms) if deg_ms is not None else None,
-                                   _ptr(plans) if plans is not None else None,
+                                   _ptr(plans.records) if plans is not None else None,
+                                   _ptr(plans.steps) if plans is not None else None,
                                    _ptr(rtt_ms), _ptr(class_weights), _ptr(bounds),
                                    float(rho), int(k), _ptr(idx), _ptr(fit), _stream(stream))
     _check("maestro_route_fitness", st)
@@ -376,11 +389,12 @@ def route_fitness(model_id: torch.Tensor, src_id: torch.Tensor, class_id: torch.
 
 
 def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, engine_freed_bytes: torch.Tensor,
-                      engine_cost_ms: torch.Tensor, c_int_ms: float, out: Optional[torch.Tensor] = None,
-                      stream=None) -> torch.Tensor:
-    """maestro_degradation_plans: uint8 [n_nodes][128] plan records (maestro_deg_plan) from the
-    engines of every node in CSR form (``engine_offset`` int32 [n_nodes + 1], at most 8 engines a
-    node; ``engine_level`` int32, ``engine_freed_bytes`` float64, ``engine_cost_ms`` float32)."""
+                      engine_cost_ms: torch.Tensor, c_int_ms: float, out: Optional[DegradationPlans] = None,
+                      stream=None) -> DegradationPlans:
+    """maestro_degradation_plans: the plan records and steps (:class:`DegradationPlans`) of every
+    node from its engines in CSR form (``engine_offset`` int32 [n_nodes + 1], any number of
+    engines a node; ``engine_level`` int32, ``engine_freed_bytes`` float64, ``engine_cost_ms``
+    float32)."""
     lib = load()
     _dev(engine_offset, "engine_offset", torch.int32)
     _dev(engine_level, "engine_level", torch.int32)
@@ -395,14 +409,18 @@ def degradation_plans(engine_offset: torch.Tensor, engine_level: torch.Tensor, e
     if engine_freed_bytes.shape != (E,) or engine_cost_ms.shape != (E,):
         raise ValueError("per-engine inputs must have the same length")
     if out is None:
-        out = torch.empty((M, PLAN_BYTES), dtype=torch.uint8, device=engine_offset.device)
-    _dev(out, "plans", torch.uint8)
-    if tuple(out.shape) != (M, PLAN_BYTES):
-        raise ValueError("plans must be uint8 [n_nodes][128]")
+        out = DegradationPlans(torch.empty((M, PLAN_BYTES), dtype=torch.uint8, device=engine_offset.device),
+                               torch.empty((max(E, 1), STEP_BYTES), dtype=torch.uint8, device=engine_offset.device))
+    _dev(out.records, "plans.records", torch.uint8)
+    _dev(out.steps, "plans.steps", torch.uint8)
+    if tuple(out.records.shape) != (M, PLAN_BYTES):
+        raise ValueError("plans.records must be uint8 [n_nodes][128]")
+    if out.steps.dim() != 2 or out.steps.shape[1] != STEP_BYTES or out.steps.shape[0] < E:
+        raise ValueError("plans.steps must be uint8 [>= E][16]")
     st = lib.maestro_degradation_plans(M, _ptr(engine_offset), _ptr(engine_level) if E else None,
                                        _ptr(engine_freed_bytes) if E else None,
-                                       _ptr(engine_cost_ms) if E else None, float(c_int_ms), _ptr(out),
-                                       _stream(stream))
+                                       _ptr(engine_cost_ms) if E else None, float(c_int_ms), _ptr(out.records),
+                                       _ptr(out.steps), _stream(stream))
     _check("maestro_degradation_plans", st)
     return out
 

@@ -8,6 +8,7 @@ namespace {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 static_assert(sizeof(maestro_deg_plan) == 128, "plan record layout");
+static_assert(sizeof(maestro_plan_step) == 16, "plan step layout");
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
@@ -181,7 +182,8 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
                                      int32_t n_classes, const double* free_bytes,
                                      const float* queue_ms, const float* act_ms,
                                      const uint64_t* resident_mask, const float* act_matrix,
-                                     const float* deg_ms, const maestro_deg_plan* plans, const float* rtt_ms,
+                                     const float* deg_ms, const maestro_deg_plan* plans,
+                                     const maestro_plan_step* plan_steps, const float* rtt_ms,
                                      const float* class_weights,
                                      const float* bounds, double rho, int32_t k, int32_t* node_idx,
                                      float* fitness, void* stream) {
@@ -198,7 +200,8 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
   if (act_matrix ? !aligned(act_matrix, 4)
                  : (!act_ms || !resident_mask || !aligned(act_ms, 4) || !aligned(resident_mask, 8)))
     return MAESTRO_ERR_INVALID_ARG;
-  if (plans ? !aligned(plans, 16) : (!deg_ms || !aligned(deg_ms, 4))) return MAESTRO_ERR_INVALID_ARG;
+  if (plans ? (!aligned(plans, 16) || !plan_steps || !aligned(plan_steps, 16)) : (!deg_ms || !aligned(deg_ms, 4)))
+    return MAESTRO_ERR_INVALID_ARG;
   if (n > 0) {
     if (!model_id || !src_id || !class_id || !kv_bytes || !node_idx || !fitness)
       return MAESTRO_ERR_INVALID_ARG;
@@ -209,23 +212,24 @@ maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const i
   if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
   return maestro::launch_route_fitness(n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes,
                                        free_bytes, queue_ms, act_ms, resident_mask, act_matrix, deg_ms,
-                                       plans, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,
+                                       plans, plan_steps, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness,
                                        as_stream(stream));
 }
 
 maestro_status maestro_degradation_plans(int32_t n_nodes, const int32_t* engine_offset,
                                          const int32_t* engine_level, const double* engine_freed_bytes,
                                          const float* engine_cost_ms, float c_int_ms, maestro_deg_plan* plans,
-                                         void* stream) {
+                                         maestro_plan_step* steps, void* stream) {
   if (n_nodes < 0 || !(c_int_ms == c_int_ms)) return MAESTRO_ERR_INVALID_ARG;
   if (n_nodes == 0) return MAESTRO_OK;
-  if (!engine_offset || !plans || !aligned(engine_offset, 4) || !aligned(plans, 16))
+  if (!engine_offset || !plans || !steps || !aligned(engine_offset, 4) || !aligned(plans, 16) ||
+      !aligned(steps, 16))
     return MAESTRO_ERR_INVALID_ARG;
   // the engine arrays may be empty (no node has an engine), then they may be NULL
   if (!aligned(engine_level, 4) || !aligned(engine_freed_bytes, 8) || !aligned(engine_cost_ms, 4))
     return MAESTRO_ERR_INVALID_ARG;
   return maestro::launch_degradation_plans(n_nodes, engine_offset, engine_level, engine_freed_bytes,
-                                           engine_cost_ms, c_int_ms, plans, as_stream(stream));
+                                           engine_cost_ms, c_int_ms, plans, steps, as_stream(stream));
 }
 
 maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,

@@ -2,29 +2,38 @@
 // normalisation.
 //
 // For every stage, among the nodes whose headroom admits R_need = (1 + rho) R_kv, the largest
-//   S = A - lambda * norm(T_ready) - mu * norm(C_deg),
-//   A = gamma * (1 - norm(RTT(src, node))) + (1 - gamma) * R_need / headroom,
+//   S = A - (lambda * norm(T_ready) + mu * norm(C_deg)),
+//   A = gamma * (1 - norm(RTT(src, node))) + (1 - gamma) * fit,  fit = R_need / headroom,
 //   T_ready = T_q + T_act (T_act = 0 when the stage's model is resident),
 // with the class weights (gamma, lambda, mu) of the stage and norm(x) = clamp((x - lo) / (hi - lo),
 // 0, 1) over window bounds (lo, hi) per metric (a degenerate window normalises to 0). The k best
 // (fitness, node) pairs are kept, larger fitness first and the lower index on equal fitness
-// (the strict ">" of Alg. 3).
+// (the strict ">" of Alg. 3). Every operation is float32 rounded to nearest, in that order.
 //
 // A workgroup takes 256 stages (one per thread; 256 / G when a small batch gives each stage G
 // lanes) and stages node state chunk by chunk in LDS, with everything that depends on the node
-// alone already normalised: headroom, its float32
-// reciprocal, normalised T_ready with and without activation, normalised C_deg, and
-// 1 - normalised RTT from every source. A pair then costs the feasibility test, one product for
-// the fit and the four products/sums of Eq. 5. Every operation is float32 round-to-nearest in a
-// fixed order (explicit intrinsics, no contraction), so the fitness values are reproducible bit
-// for bit by a sequential evaluation of the same expression.
+// alone already evaluated: the normalised metrics (true divisions, once per node), the
+// headroom and its float64 reciprocal, 1 - norm(RTT) from every source and, with residency
+// bits, the penalty lambda * norm(T_ready) + mu * norm(C_deg) of every stage class for both
+// residency states. A pair then costs the feasibility test, the fit, the affinity and one
+// subtraction.
+//
+// The fit is fl32(fl32(R_need) / fl32(headroom)) -- at most 1 on a feasible node, since R_need <=
+// headroom survives the rounding to float32; 0 on a node without headroom -- computed as the
+// float64 product of fl32(R_need)
+// with the float64 reciprocal of fl32(headroom), rounded once to float32. For float32 operands
+// a and b that product is within 2^-52 (relative) of a / b, while a / b lies at least 2^-49
+// (relative) away from every float32 rounding boundary (a midpoint has a 25-bit significand, so
+// a - midpoint * b, a nonzero multiple of the operands' least significant bits, cannot vanish),
+// hence the rounding gives the correctly rounded float32 quotient -- the division itself.
 //
 // With degradation plans (Alg. 2, Eq. 4), C_deg is per pair: 0 when the stage fits, else the
 // cost of the shortest priority prefix of the node's engines that frees the shortfall, and the
-// node drops out when no prefix does. The plan records (running freed bytes and costs, one per
-// prefix) are built once per node state and staged in LDS, column by column, with the other
-// node terms. The main loop scores every pair as if it fit and only queues the short ones; a
-// lane then scores its queued nodes against their plans after each chunk.
+// node drops out when no prefix does. The first eight steps of each node's plan are staged in
+// LDS, column by column, with the other node terms; a node with more engines continues in the
+// step array in global memory (binary search). The main loop scores every pair as if it fit and
+// only queues the short ones; a lane then scores its queued nodes against their plans after
+// each chunk.
 //
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
@@ -39,71 +48,100 @@ namespace maestro {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxPlan = MAESTRO_MAX_PLAN_ENGINES;
+constexpr int kRecSteps = MAESTRO_PLAN_RECORD_STEPS;
 
-__device__ __forceinline__ float norm_inv(float lo, float hi) {
-  return hi > lo ? __fdiv_rn(1.0f, __fsub_rn(hi, lo)) : 0.0f;
-}
-__device__ __forceinline__ float norm01(float x, float lo, float inv) {
-  float t = __fmul_rn(__fsub_rn(x, lo), inv);
+// (x - lo) / (hi - lo) clipped to [0, 1]; 0 for a degenerate window
+__device__ __forceinline__ float norm01(float x, float lo, float hi) {
+  if (!(hi > lo)) return 0.0f;
+  float t = __fdiv_rn(__fsub_rn(x, lo), __fsub_rn(hi, lo));
   if (t < 0.0f) t = 0.0f;
   if (t > 1.0f) t = 1.0f;
   return t;
 }
 
-// Plan records from the engine lists, one thread per node. SortByPriority orders the engines by
-// ascending level, the lower engine index first (a fixed compare-exchange network over keys
-// level:index); the running sums then follow that order: freed bytes in float64, costs in
-// float32, and c_int added to every prefix that holds an engine of level 4 or 5. The freed
-// column keeps the largest running sum so far, so it never decreases (it is the running sum
-// itself when no action frees a negative amount): the first prefix whose running sum reaches
-// a shortfall is then also the first whose entry does, and a stage finds it by counting the
-// entries below its shortfall. Entries past the node's engines hold +inf.
+// Plan steps and records from the engine lists, one thread per node. SortByPriority orders the
+// engines by ascending level, the lower engine index first: up to eight engines with a fixed
+// compare-exchange network over keys level:index in registers, more by counting each engine's
+// rank among the node's keys (the keys are distinct). The running sums then follow that order:
+// freed bytes in float64, costs in float32, and c_int added to every prefix that holds an engine
+// of level 4 or 5. The freed column keeps the largest running sum so far, so it never decreases
+// (it is the running sum itself when no action frees a negative amount): the first prefix whose
+// running sum reaches a shortfall is then also the first whose entry does, which a stage finds
+// by counting (record) or by binary search (steps). Record entries past the node's engines hold
+// +inf.
+__device__ __forceinline__ int64_t engine_key(int32_t level, int32_t i) {
+  return (int64_t)level * ((int64_t)1 << 32) + (int64_t)(uint32_t)i;
+}
+
 __global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const int32_t* __restrict__ engine_offset,
                                                         const int32_t* __restrict__ engine_level,
                                                         const double* __restrict__ engine_freed,
                                                         const float* __restrict__ engine_cost, float c_int,
-                                                        maestro_deg_plan* __restrict__ plans) {
+                                                        maestro_deg_plan* __restrict__ plans,
+                                                        maestro_plan_step* __restrict__ steps) {
   const int32_t j = blockIdx.x * kThreads + threadIdx.x;
   if (j >= n_nodes) return;
   const int32_t e0 = engine_offset[j];
-  int32_t ne = engine_offset[j + 1] - e0;   // at most kMaxPlan by contract; clamped all the same
-  ne = ne < 0 ? 0 : (ne > kMaxPlan ? kMaxPlan : ne);
-  int64_t key[kMaxPlan];
-#pragma unroll
-  for (int i = 0; i < kMaxPlan; ++i)
-    key[i] = i < ne ? ((int64_t)engine_level[e0 + i] << 8 | i) : INT64_MAX;
-#pragma unroll
-  for (int pass = 0; pass < kMaxPlan; ++pass) {
-#pragma unroll
-    for (int q = pass & 1; q + 1 < kMaxPlan; q += 2) {   // odd-even transposition sort
-      const int64_t a = key[q], b = key[q + 1];
-      key[q] = a < b ? a : b;
-      key[q + 1] = a < b ? b : a;
-    }
-  }
+  int32_t ne = engine_offset[j + 1] - e0;
+  ne = ne < 0 ? 0 : ne;
   maestro_deg_plan out;
   double freed = 0.0, top = 0.0;
   float cost = 0.0f;
   bool interrupt = false;
+  // one step of the running sums: engine e (global index) of level lv at position p
+  auto step = [&](int32_t p, int32_t e, int32_t lv) {
+    interrupt = interrupt || lv >= 4;   // Preempt / Abort interrupt active work
+    freed = __dadd_rn(freed, engine_freed[e]);
+    cost = __fadd_rn(cost, engine_cost[e]);
+    top = p == 0 ? freed : fmax(top, freed);
+    const float c = __fadd_rn(cost, interrupt ? c_int : 0.0f);
+    steps[e0 + p] = maestro_plan_step{top, c, e};
+    if (p < kRecSteps) {
+      out.freed[p] = top;
+      out.cost[p] = c;
+    }
+  };
+  if (ne <= kRecSteps) {
+    int64_t key[kRecSteps];
 #pragma unroll
-  for (int i = 0; i < kMaxPlan; ++i) {
-    if (i < ne) {
-      const int32_t e = e0 + (int32_t)(key[i] & 255);
-      interrupt = interrupt || (key[i] >> 8) >= 4;   // Preempt / Abort interrupt active work
-      freed = __dadd_rn(freed, engine_freed[e]);
-      cost = __fadd_rn(cost, engine_cost[e]);
-      top = i == 0 ? freed : fmax(top, freed);
-      out.freed[i] = top;
-      out.cost[i] = __fadd_rn(cost, interrupt ? c_int : 0.0f);
-    } else {
-      out.freed[i] = INFINITY;
-      out.cost[i] = 0.0f;
+    for (int i = 0; i < kRecSteps; ++i) key[i] = i < ne ? engine_key(engine_level[e0 + i], i) : INT64_MAX;
+#pragma unroll
+    for (int pass = 0; pass < kRecSteps; ++pass) {
+#pragma unroll
+      for (int q = pass & 1; q + 1 < kRecSteps; q += 2) {   // odd-even transposition sort
+        const int64_t a = key[q], b = key[q + 1];
+        key[q] = a < b ? a : b;
+        key[q + 1] = a < b ? b : a;
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < kRecSteps; ++p)
+      if (p < ne) step(p, e0 + (int32_t)(uint32_t)key[p], (int32_t)(key[p] >> 32));
+  } else {
+    // the rank of engine i among the node's keys is its position in priority order; the step
+    // array holds the order (engine of each position) before the running sums overwrite it
+    for (int32_t i = 0; i < ne; ++i) {
+      const int64_t ki = engine_key(engine_level[e0 + i], i);
+      int32_t rank = 0;
+      for (int32_t q = 0; q < ne; ++q) rank += engine_key(engine_level[e0 + q], q) < ki ? 1 : 0;
+      steps[e0 + rank].engine = e0 + i;
+    }
+    for (int32_t p = 0; p < ne; ++p) {
+      const int32_t e = steps[e0 + p].engine;
+      step(p, e, engine_level[e]);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < kRecSteps; ++p) {
+    if (p >= ne) {
+      out.freed[p] = INFINITY;
+      out.cost[p] = 0.0f;
     }
   }
   out.n_engines = ne;
+  out.first_step = e0;
 #pragma unroll
-  for (int i = 0; i < 7; ++i) out.reserved[i] = 0;
+  for (int i = 0; i < 6; ++i) out.reserved[i] = 0;
   plans[j] = out;
 }
 
@@ -113,46 +151,55 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(int32_t n_nodes, const i
 enum Ready { kMask32 = 0, kMask64 = 1, kMatrix16 = 2, kMatrix64 = 3 };
 constexpr int64_t kFitnessLanesTarget = 256 * 4 * 64 * 4;   // lanes of four wavefronts per SIMD
 
+template <int kReady>
+struct FitnessChunk {
+  static constexpr int value = kReady == kMatrix64 ? 32 : 128;
+};
+
 // kMulti: G = 2^g_log2 lanes share a stage (batches too small to fill the chip); lane g scores
 // nodes g, g + G, g + 2G, ... of every chunk into its own list, and the G lists are merged with
 // xor-shuffles (lexicographic on (key, node)) before lane 0 writes the stage's results.
+// Dynamic LDS: with residency bits, the per-class penalties, n_classes * chunk float2.
 template <int KT, int kReady, bool kPlans, bool kMulti>
 __global__ __launch_bounds__(kThreads) void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_models, int32_t n_nodes,
     int32_t n_src, int32_t n_classes, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
     const float* __restrict__ act_ms, const uint64_t* __restrict__ resident_mask,
-    const float* __restrict__ act_matrix, const float* __restrict__ deg_ms, const maestro_deg_plan* __restrict__ plans, const float* __restrict__ rtt_ms,
-    const float* __restrict__ class_weights, const float* __restrict__ bounds, double rho, int32_t k,
-    int32_t* __restrict__ node_idx, float* __restrict__ fitness, int g_log2) {
-  // per node, two 16-byte records (one LDS read each, the same address for every lane):
-  //   terms: 1 / fl32(headroom) (+inf when that is 0), norm(T_q) (model resident),
-  //          norm(T_q + T_act), norm(C_deg)
-  //   admit: KV admission headroom and the residency bits (the low 32 when no model id
-  //          exceeds 31)
-  // and with plans the node's plan record (norm(C_deg) then depends on the stage). With a
-  // T_act matrix, terms.y holds T_q itself and the node's row of the matrix is staged too.
+    const float* __restrict__ act_matrix, const float* __restrict__ deg_ms,
+    const maestro_deg_plan* __restrict__ plans, const maestro_plan_step* __restrict__ plan_steps,
+    const float* __restrict__ rtt_ms, const float* __restrict__ class_weights, const float* __restrict__ bounds,
+    double rho, int32_t k, int32_t* __restrict__ node_idx, float* __restrict__ fitness, int g_log2) {
+  // per node: {headroom, 1 / fl32(headroom)} (one 16-byte LDS read, the same address for every
+  // lane), the residency bits, and per source row 1 - norm(RTT). With residency bits, the
+  // penalty of each class for both states (model resident or not) and, for the short pairs of
+  // plans, the two normalised ready times; with a T_act matrix, norm(T_q + T_act) of every
+  // (node, model) and the node's normalised C_deg.
   typedef typename std::conditional<kReady == kMask64, uint64_t, uint32_t>::type mask_t;
   constexpr bool kMat = kReady >= kMatrix16;
   constexpr int kMatRow = kReady == kMatrix16 ? 16 : 64;   // largest row the staging area holds
   // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
   // workgroups per CU, whose waves hide each other's LDS latency
-  constexpr int kChunk = kReady == kMatrix64 ? 32 : 128;
+  constexpr int kChunk = FitnessChunk<kReady>::value;
   constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
-  struct Admit { double free; uint64_t mask; };
-  __shared__ float4 s_terms[kChunk];
-  __shared__ Admit s_admit[kChunk];
+  struct Node { double free, recip; };
+  __shared__ Node s_node[kChunk];
+  __shared__ mask_t s_mask[kMat ? 1 : kChunk];
+  __shared__ float2 s_tr[kMat || !kPlans ? 1 : kChunk];   // norm(T_q), norm(T_q + T_act)
+  __shared__ float s_nd[kMat ? kChunk : 1];                // norm(C_deg) (T_act matrix)
   __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
+  __shared__ float s_w[3 * kMaxFitnessClasses];           // (gamma, lambda, mu) per class
   constexpr int kPC = kPlans ? kChunk : 1;
-  __shared__ double s_pfreed[kMaxPlan][kPC];   // plan columns, node-minor: lanes reading
-  __shared__ float s_pcost[kMaxPlan][kPC];     // different nodes hit different banks
-  __shared__ int32_t s_pn[kPC];
+  __shared__ double s_pfreed[kRecSteps][kPC];   // plan columns, node-minor: lanes reading
+  __shared__ float s_pcost[kRecSteps][kPC];     // different nodes hit different banks
+  __shared__ int32_t s_pn[kPC], s_pfirst[kPC];
   constexpr int kQueue = kPlans ? 16 : 1;        // short nodes a lane queues per chunk
   static_assert(kChunk <= 256 || !kPlans, "queued node offsets are bytes");
   __shared__ uint8_t s_queue[kQueue * kThreads];
   // with a T_act matrix: normalised T_ready = norm(T_q + T_act) of every (node, model) of the
   // chunk, [node][model] with row stride n_models
   __shared__ float s_ready[kMat ? kChunk * kMatRow : 1];
+  extern __shared__ float2 s_pen[];              // [class][node]: penalty resident, not resident
 
   const int tid = threadIdx.x;
   const int G = kMulti ? 1 << g_log2 : 1;
@@ -160,23 +207,23 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   const int64_t stage = kMulti ? (int64_t)blockIdx.x * (kThreads >> g_log2) + (tid >> g_log2)
                                : (int64_t)blockIdx.x * kThreads + tid;
   const bool valid = stage < n;
-  const float lo_r = bounds[0], lo_t = bounds[2], lo_d = bounds[4];
-  const float inv_r = norm_inv(bounds[0], bounds[1]);
-  const float inv_t = norm_inv(bounds[2], bounds[3]);
-  const float inv_d = norm_inv(bounds[4], bounds[5]);
-  const float nd_fits = norm01(0.0f, lo_d, inv_d);   // normalised C_deg of a stage that fits
+  const float lo_r = bounds[0], hi_r = bounds[1], lo_t = bounds[2], hi_t = bounds[3];
+  const float lo_d = bounds[4], hi_d = bounds[5];
+  const float nd_fits = norm01(0.0f, lo_d, hi_d);   // normalised C_deg of a stage that fits
+  for (int e = tid; e < 3 * n_classes; e += kThreads) s_w[e] = class_weights[e];
 
   double need = INFINITY;   // an invalid lane admits nothing
-  float needf = 0.0f, gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
+  double needd = 0.0;       // fl32(R_need), widened
+  float gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
   mask_t mbit = 0;
-  int src = 0, model = 0;
+  int src = 0, model = 0, cls = 0;
   bool ok = false;          // a stage whose model, source and class ids are in range
   if (valid) {
     const int32_t m = model_id[stage], s = src_id[stage], c = class_id[stage];
     ok = (uint32_t)m < (uint32_t)n_models && (uint32_t)s < (uint32_t)n_src && (uint32_t)c < (uint32_t)n_classes;
     if (ok) {
       need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
-      needf = __double2float_rn(need);
+      needd = (double)__double2float_rn(need);
       const float* wt = class_weights + 3 * c;
       gamma = wt[0];
       lambda = wt[1];
@@ -185,124 +232,158 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       model = m;
       mbit = kMat ? 0 : (mask_t)1 << model;
       src = s;
+      cls = c;
     } else {
       need = NAN;             // an id out of range: no node admits the stage, no plan is tried
     }
   }
   const float* prox_row = s_prox + src * kProxStride;
+  const float2* pen_row = s_pen + cls * kChunk;
 
   TopK<KT> best;   // keys are -fitness: the smallest key is the best node
   best.init();
   for (int32_t c0 = 0; c0 < n_nodes; c0 += kChunk) {
     const int cn = min(kChunk, n_nodes - c0);
-    __syncthreads();  // every lane is done with the previous chunk
+    __syncthreads();  // every lane is done with the previous chunk (and s_w is written)
     for (int i = tid; i < cn; i += kThreads) {
       const int32_t j = c0 + i;
       const double fr = free_bytes[j];
       const float frf = __double2float_rn(fr);
-      const float q = queue_ms[j];
-      s_terms[i] = make_float4(frf > 0.0f ? __fdiv_rn(1.0f, frf) : INFINITY,
-                               kMat ? 0.0f : norm01(__fadd_rn(q, 0.0f), lo_t, inv_t),
-                               kMat ? 0.0f : norm01(__fadd_rn(q, act_ms[j]), lo_t, inv_t),
-                               kPlans ? nd_fits : norm01(deg_ms[j], lo_d, inv_d));
-      s_admit[i] = Admit{fr, kMat ? 0ull : resident_mask[j]};
-      if (kPlans) {
+      // a node without headroom admits only an empty demand: its fit is 0
+      s_node[i] = Node{fr, frf > 0.0f ? __ddiv_rn(1.0, (double)frf) : 0.0};
+      const float nd = kPlans ? nd_fits : norm01(deg_ms[j], lo_d, hi_d);
+      if constexpr (kMat) {
+        s_nd[i] = nd;
+      } else {
+        const float q = queue_ms[j];
+        const float tr0 = norm01(__fadd_rn(q, 0.0f), lo_t, hi_t);
+        const float tr1 = norm01(__fadd_rn(q, act_ms[j]), lo_t, hi_t);
+        s_mask[i] = (mask_t)resident_mask[j];
+        if constexpr (kPlans) s_tr[i] = make_float2(tr0, tr1);
+        for (int c = 0; c < n_classes; ++c) {
+          const float l = s_w[3 * c + 1], u = s_w[3 * c + 2];
+          const float pd = __fmul_rn(u, nd);
+          s_pen[c * kChunk + i] =
+              make_float2(__fadd_rn(__fmul_rn(l, tr0), pd), __fadd_rn(__fmul_rn(l, tr1), pd));
+        }
+      }
+      if constexpr (kPlans) {
         const maestro_deg_plan& pl = plans[j];
 #pragma unroll
-        for (int e = 0; e < kMaxPlan; ++e) {
+        for (int e = 0; e < kRecSteps; ++e) {
           s_pfreed[e][i] = pl.freed[e];
           s_pcost[e][i] = pl.cost[e];
         }
         s_pn[i] = pl.n_engines;
+        s_pfirst[i] = pl.first_step;
       }
     }
-    if (kMat) {   // rows c0 .. c0+cn-1 of the matrix are contiguous
+    if constexpr (kMat) {   // rows c0 .. c0+cn-1 of the matrix are contiguous
       const float* src_rows = act_matrix + (size_t)c0 * n_models;
       for (int e = tid; e < cn * n_models; e += kThreads)
-        s_ready[e] = norm01(__fadd_rn(queue_ms[c0 + e / n_models], src_rows[e]), lo_t, inv_t);
+        s_ready[e] = norm01(__fadd_rn(queue_ms[c0 + e / n_models], src_rows[e]), lo_t, hi_t);
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
-      s_prox[r * kProxStride + i] =
-          __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, inv_r));
+      s_prox[r * kProxStride + i] = __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, hi_r));
     }
     __syncthreads();
-    // every node is scored; an infeasible one offers the key +inf, which never enters the list
-    // (FilterByPolicyAndFeasibility)
-    auto score = [&](int i, const float4 t, const Admit ad, float prox, float nd) {
-      // fit = min(1, fl32(need) / fl32(headroom)); with zero headroom only need = 0 is
-      // feasible, and min(0 * inf = NaN, 1) = 1 (IEEE min returns the number), the fit of a
-      // stage that fills the node exactly
-      const float fit = fminf(__fmul_rn(needf, t.x), 1.0f);
-      const float a = __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
-      float nr;
-      if constexpr (kMat) nr = s_ready[i * n_models + model];
-      else nr = ((mask_t)ad.mask & mbit) ? t.y : t.z;
-      return __fsub_rn(__fsub_rn(a, __fmul_rn(lambda, nr)), __fmul_rn(mu, nd));
+    // A = gamma * prox + (1 - gamma) * fit with fit = fl32(fl32(R_need) * (1 / fl32(headroom)))
+    auto affinity = [&](const Node nd, float prox) {
+      const float fit = __double2float_rn(__dmul_rn(needd, nd.recip));
+      return __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
     };
-    // A stage that falls short of node i's headroom by R takes the first prefix of the node's
-    // plan whose freed bytes reach R, at that prefix's cost; no such prefix leaves the node
+    // the penalty lambda * norm(T_ready) + mu * nd of node i
+    auto penalty = [&](int i, float nd) {
+      float tr;
+      if constexpr (kMat) {
+        tr = s_ready[i * n_models + model];
+      } else {
+        const float2 t = s_tr[i];
+        tr = (s_mask[i] & mbit) ? t.x : t.y;
+      }
+      return __fadd_rn(__fmul_rn(lambda, tr), __fmul_rn(mu, nd));
+    };
+    // A stage that falls short of node i's headroom by R takes the first step of the node's
+    // plan whose freed bytes reach R, at that step's cost; no such step leaves the node
     // infeasible. These pairs are rare, so they leave the main loop: each lane queues its short
     // nodes and scores them after the chunk (rescanning the chunk when its queue overflowed),
     // inserting lexicographically since they come after nodes of larger index.
     auto short_pair = [&](int i) {
-      const float4 t = s_terms[i];
-      const Admit ad = s_admit[i];
-      const double R = __dsub_rn(need, ad.free);
+      const Node nd = s_node[i];
+      const double R = __dsub_rn(need, nd.free);
+      const int ne = s_pn[i];
       int jp = 0;
 #pragma unroll
-      for (int e = 0; e < kMaxPlan; ++e) jp += s_pfreed[e][i] < R ? 1 : 0;
-      if (jp < s_pn[i])
-        best.push_lex(-score(i, t, ad, prox_row[i], norm01(s_pcost[jp][i], lo_d, inv_d)), c0 + i);
+      for (int e = 0; e < kRecSteps; ++e) jp += s_pfreed[e][i] < R ? 1 : 0;
+      float c = 0.0f;
+      bool found = jp < ne && jp < kRecSteps;
+      if (found) {
+        c = s_pcost[jp][i];
+      } else if (ne > kRecSteps) {   // the steps past the record: the first freed >= R
+        const maestro_plan_step* st = plan_steps + s_pfirst[i];
+        int lo = kRecSteps, hi = ne;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (st[mid].freed < R) lo = mid + 1;
+          else hi = mid;
+        }
+        found = lo < ne;
+        if (found) c = st[lo].cost;
+      }
+      if (found) {
+        const float a = affinity(nd, prox_row[i]);
+        best.push_lex(-__fsub_rn(a, penalty(i, norm01(c, lo_d, hi_d))), c0 + i);
+      }
     };
     int n_short = 0;   // queued nodes of this chunk
     auto queue = [&](int i) {
       if (n_short < kQueue) s_queue[n_short * kThreads + tid] = (uint8_t)i;
       ++n_short;
     };
-    if (kPlans) {
-      // groups of four of this lane's nodes: their LDS reads issue together, and one branch
-      // per group queues the short ones
-      int i = g;
-      for (; i + 3 * G < cn; i += 4 * G) {
-        float4 t[4];
-        Admit ad[4];
-        float px[4];
-        bool fits[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          t[u] = s_terms[i + u * G];
-          ad[u] = s_admit[i + u * G];
-          px[u] = prox_row[i + u * G];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          fits[u] = need <= ad[u].free;
-          const float sc = score(i + u * G, t[u], ad[u], px[u], t[u].w);
-          best.push_increasing(fits[u] ? -sc : INFINITY, c0 + i + u * G);
-        }
-        if (ok && !(fits[0] && fits[1] && fits[2] && fits[3])) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (!fits[u]) queue(i + u * G);
-        }
+    // the pair's fitness when the stage fits (C_deg = the node's, or 0 with plans)
+    auto fits_score = [&](int i, const Node nd, float prox) {
+      const float a = affinity(nd, prox);
+      float pen;
+      if constexpr (kMat) {
+        pen = __fadd_rn(__fmul_rn(lambda, s_ready[i * n_models + model]), __fmul_rn(mu, s_nd[i]));
+      } else {
+        const float2 p = pen_row[i];
+        pen = (s_mask[i] & mbit) ? p.x : p.y;
       }
-      for (; i < cn; i += G) {
-        const float4 t = s_terms[i];
-        const Admit ad = s_admit[i];
-        const bool fits = need <= ad.free;
-        const float sc = score(i, t, ad, prox_row[i], t.w);
-        best.push_increasing(fits ? -sc : INFINITY, c0 + i);
-        if (ok && !fits) queue(i);
+      return __fsub_rn(a, pen);
+    };
+    // groups of four of this lane's nodes: their LDS reads issue together, the four scores are
+    // computed before any of them enters the list, and with plans one branch per group queues
+    // the short ones
+    int i = g;
+    for (; i + 3 * G < cn; i += 4 * G) {
+      Node nd[4];
+      float px[4], sc[4];
+      bool fits[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        nd[u] = s_node[i + u * G];
+        px[u] = prox_row[i + u * G];
       }
-    } else {
-#pragma unroll 4
-      for (int i = g; i < cn; i += G) {
-        const float4 t = s_terms[i];
-        const Admit ad = s_admit[i];
-        const float sc = score(i, t, ad, prox_row[i], t.w);
-        best.push_increasing(need <= ad.free ? -sc : INFINITY, c0 + i);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        fits[u] = need <= nd[u].free;
+        sc[u] = fits_score(i + u * G, nd[u], px[u]);
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) best.push_increasing_if(fits[u], -sc[u], c0 + i + u * G);
+      if (kPlans && ok && !(fits[0] && fits[1] && fits[2] && fits[3])) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (!fits[u]) queue(i + u * G);
+      }
+    }
+    for (; i < cn; i += G) {
+      const Node nd = s_node[i];
+      const bool fits = need <= nd.free;
+      best.push_increasing_if(fits, -fits_score(i, nd, prox_row[i]), c0 + i);
+      if (kPlans && ok && !fits) queue(i);
     }
     if (kPlans && n_short > 0) {
       if (n_short <= kQueue) {
@@ -311,7 +392,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       } else {
 #pragma unroll 1
         for (int i = g; i < cn; i += G)
-          if (!(need <= s_admit[i].free)) short_pair(i);
+          if (!(need <= s_node[i].free)) short_pair(i);
       }
     }
   }
@@ -655,9 +736,9 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     int32_t n_nodes, int32_t n_src, int32_t n_classes, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
-                                    const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,
-                                    const float* bounds, double rho, int32_t k, int32_t* node_idx,
-                                    float* fitness, hipStream_t stream) {
+                                    const maestro_deg_plan* plans, const maestro_plan_step* plan_steps,
+                                    const float* rtt_ms, const float* class_weights, const float* bounds, double rho,
+                                    int32_t k, int32_t* node_idx, float* fitness, hipStream_t stream) {
   if (n == 0) return MAESTRO_OK;
   // lanes per stage: the smallest power of two (at most 16) that gives the batch about four
   // wavefronts per SIMD of a 256-CU chip, and never more lanes than a chunk has nodes
@@ -667,18 +748,21 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
   const dim3 grid((unsigned)((n + per_block - 1) / per_block)), block(kThreads);
   const int ready = act_matrix ? (n_models > 16 ? kMatrix64 : kMatrix16) : (n_models > 32 ? kMask64 : kMask32);
   const bool with_plans = plans != nullptr;
+  // per-class penalties of a chunk (residency-bit forms only)
+  const size_t pen_bytes =
+      act_matrix ? 0 : (size_t)n_classes * (size_t)FitnessChunk<kMask32>::value * sizeof(float2);
 #define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                          \
   do {                                                                                                          \
     if (g_log2 > 0)                                                                                             \
-      fitness_kernel<KT, RD, PL, true><<<grid, block, 0, stream>>>(                                             \
+      fitness_kernel<KT, RD, PL, true><<<grid, block, pen_bytes, stream>>>(                                     \
           n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
-          act_ms, resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx,   \
-          fitness, g_log2);                                                                                     \
+          act_ms, resident_mask, act_matrix, deg_ms, plans, plan_steps, rtt_ms, class_weights, bounds, rho, k,  \
+          node_idx, fitness, g_log2);                                                                           \
     else                                                                                                        \
-      fitness_kernel<KT, RD, PL, false><<<grid, block, 0, stream>>>(                                            \
+      fitness_kernel<KT, RD, PL, false><<<grid, block, pen_bytes, stream>>>(                                    \
           n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
-          act_ms, resident_mask, act_matrix, deg_ms, plans, rtt_ms, class_weights, bounds, rho, k, node_idx,   \
-          fitness, 0);                                                                                          \
+          act_ms, resident_mask, act_matrix, deg_ms, plans, plan_steps, rtt_ms, class_weights, bounds, rho, k,  \
+          node_idx, fitness, 0);                                                                                \
   } while (0)
 #define MAESTRO_FIT_RD(KT, PL)                                       \
   do {                                                               \
@@ -738,10 +822,10 @@ maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, cons
 
 maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_offset, const int32_t* engine_level,
                                        const double* engine_freed_bytes, const float* engine_cost_ms, float c_int_ms,
-                                       maestro_deg_plan* plans, hipStream_t stream) {
+                                       maestro_deg_plan* plans, maestro_plan_step* steps, hipStream_t stream) {
   if (n_nodes == 0) return MAESTRO_OK;
   plan_kernel<<<dim3((unsigned)((n_nodes + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream>>>(
-      n_nodes, engine_offset, engine_level, engine_freed_bytes, engine_cost_ms, c_int_ms, plans);
+      n_nodes, engine_offset, engine_level, engine_freed_bytes, engine_cost_ms, c_int_ms, plans, steps);
   return launch_status();
 }
 

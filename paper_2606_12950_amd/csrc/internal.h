@@ -40,12 +40,12 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
                                     int32_t n_nodes, int32_t n_src, int32_t n_classes, const double* free_bytes,
                                     const float* queue_ms, const float* act_ms,
                                     const uint64_t* resident_mask, const float* act_matrix, const float* deg_ms,
-                                    const maestro_deg_plan* plans, const float* rtt_ms, const float* class_weights,
-                                    const float* bounds, double rho, int32_t k, int32_t* node_idx,
-                                    float* fitness, hipStream_t stream);
+                                    const maestro_deg_plan* plans, const maestro_plan_step* plan_steps,
+                                    const float* rtt_ms, const float* class_weights, const float* bounds, double rho,
+                                    int32_t k, int32_t* node_idx, float* fitness, hipStream_t stream);
 maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_offset, const int32_t* engine_level,
                                        const double* engine_freed_bytes, const float* engine_cost_ms, float c_int_ms,
-                                       maestro_deg_plan* plans, hipStream_t stream);
+                                       maestro_deg_plan* plans, maestro_plan_step* steps, hipStream_t stream);
 maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, const uint8_t* tier,
                                          const double* model_bytes, const double* tier_bw,
                                          const float* tier_setup, double unit, float* act, hipStream_t stream);

@@ -34,6 +34,20 @@ struct TopK {
       }
     }
   }
+  // push_increasing for a candidate that may be absent (ok == false): the presence test joins
+  // the entry test, so an absent candidate costs no select of its own
+  __device__ __forceinline__ void push_increasing_if(bool ok, float sc, int32_t node) {
+    if (!(ok && sc < s[KT - 1])) return;
+#pragma unroll
+    for (int i = KT - 1; i >= 0; --i) {
+      const int p = i > 0 ? i - 1 : 0;
+      const bool lt_prev = (i > 0) && sc < s[p];
+      if (sc < s[i]) {
+        if (lt_prev) { s[i] = s[p]; n[i] = n[p]; }
+        else { s[i] = sc; n[i] = node; }
+      }
+    }
+  }
   // General lexicographic insertion, for candidates out of node order (lists merged from other
   // lanes, nodes visited late).
   __device__ __forceinline__ void push_lex(float sc, int32_t node) {
@@ -54,6 +68,10 @@ struct TopK {
 template <>
 __device__ __forceinline__ void TopK<1>::push_increasing(float sc, int32_t node) {
   if (sc < s[0]) { s[0] = sc; n[0] = node; }
+}
+template <>
+__device__ __forceinline__ void TopK<1>::push_increasing_if(bool ok, float sc, int32_t node) {
+  if (ok && sc < s[0]) { s[0] = sc; n[0] = node; }
 }
 
 // order-preserving map of float bits to unsigned (a < b <=> map(a) < map(b), -0 < +0)

@@ -409,10 +409,12 @@ class EngineInputs:
     deg_window: np.ndarray        # [WINDOW] float32
 
 
-def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
+def engine_inputs(wl: Workload, max_engines: int = 8, crowded: float = 0.1, max_crowded: int = 20) -> EngineInputs:
     """Stand-in engine lists for the nodes of ``wl`` (seeded by its spec's seed).
 
-    Each node hosts U{0..max_engines} engines; the action level is drawn with probabilities
+    Each node hosts U{0..max_engines} engines, except a fraction ``crowded`` of nodes packed
+    with many small models, which host U{max_engines+1..max_crowded}; the action level is drawn
+    with probabilities
     ENGINE_LEVEL_P. Model sizes are bf16 weights of 0.6B-14B parameters (1.2-28 GB). Freed
     bytes: the weights for levels 1 and 3, the retained runtime context (194-286 MB, the
     paper's measured range) for level 2, the KV in use (U[1, 40] GB) for levels 4 and 5. Cost
@@ -422,7 +424,8 @@ def engine_inputs(wl: Workload, max_engines: int = 8) -> EngineInputs:
     children = np.random.SeedSequence([wl.spec.seed, 0xDE6]).spawn(len(ENGINE_STREAMS))
     r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(ENGINE_STREAMS, children)}
     M = wl.free_bytes.shape[0]
-    count = r["count"].integers(0, max_engines + 1, M)
+    count = np.where(r["count"].random(M) < crowded, r["count"].integers(max_engines + 1, max_crowded + 1, M),
+                     r["count"].integers(0, max_engines + 1, M))
     offset = np.zeros(M + 1, np.int32)
     np.cumsum(count, out=offset[1:])
     E = int(offset[-1])

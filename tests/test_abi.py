@@ -154,10 +154,10 @@ def test_route_tiered_validation(lib):
 
 def test_route_fitness_and_quantiles_validation(lib):
     def call(n=10, n_models=8, n_nodes=16, n_src=2, n_classes=2, k=1, rho=0.0, src=FAKE, rtt=FAKE, bounds=FAKE,
-             deg=FAKE, plans=None, act=FAKE, mask=FAKE, mat=None):
+             deg=FAKE, plans=None, steps=None, act=FAKE, mask=FAKE, mat=None):
         return lib.maestro_route_fitness(n, FAKE, src, FAKE, FAKE, n_models, n_nodes, n_src, n_classes,
-                                         FAKE, FAKE, act, mask, mat, deg, plans, rtt, FAKE, bounds, rho, k, FAKE,
-                                         FAKE, None)
+                                         FAKE, FAKE, act, mask, mat, deg, plans, steps, rtt, FAKE, bounds, rho, k,
+                                         FAKE, FAKE, None)
     assert call(n=-1) == INVALID
     assert call(n_models=0) == INVALID
     assert call(n_models=65) == INVALID
@@ -172,9 +172,11 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert call(bounds=MISALIGNED4) == INVALID
     assert call(n=0, src=None) == OK                                          # empty batch: no-op
     assert call(deg=None) == INVALID                                          # C_deg from nowhere
-    assert call(deg=None, plans=MISALIGNED16) == INVALID                      # plan records are 16-aligned
-    assert call(deg=None, plans=FAKE16, rtt=None) == INVALID
-    assert call(n=0, deg=None, plans=FAKE16) == OK                            # plans replace deg_ms
+    assert call(deg=None, plans=MISALIGNED16, steps=FAKE16) == INVALID        # plan records are 16-aligned
+    assert call(deg=None, plans=FAKE16, steps=None) == INVALID                # records need their steps
+    assert call(deg=None, plans=FAKE16, steps=MISALIGNED16) == INVALID
+    assert call(deg=None, plans=FAKE16, steps=FAKE16, rtt=None) == INVALID
+    assert call(n=0, deg=None, plans=FAKE16, steps=FAKE16) == OK              # plans replace deg_ms
     assert call(act=None) == INVALID                                          # T_act from nowhere
     assert call(mask=MISALIGNED) == INVALID
     assert call(act=None, mask=None, mat=MISALIGNED4) == INVALID
@@ -221,17 +223,20 @@ def test_adaptive_rho_validation(lib):
 
 
 def test_degradation_plans_validation(lib):
-    def call(n_nodes=4, off=FAKE, level=FAKE, freed=FAKE, cost=FAKE, c_int=2000.0, plans=FAKE16):
-        return lib.maestro_degradation_plans(n_nodes, off, level, freed, cost, c_int, plans, None)
+    def call(n_nodes=4, off=FAKE, level=FAKE, freed=FAKE, cost=FAKE, c_int=2000.0, plans=FAKE16, steps=FAKE16):
+        return lib.maestro_degradation_plans(n_nodes, off, level, freed, cost, c_int, plans, steps, None)
     assert call(n_nodes=-1) == INVALID
     assert call(c_int=float("nan")) == INVALID
     assert call(off=None) == INVALID
     assert call(plans=None) == INVALID
     assert call(plans=MISALIGNED16) == INVALID
+    assert call(steps=None) == INVALID
+    assert call(steps=MISALIGNED16) == INVALID
     assert call(level=MISALIGNED4) == INVALID
     assert call(freed=MISALIGNED) == INVALID
-    assert call(n_nodes=0, off=None, plans=None) == OK                        # no nodes: no-op
+    assert call(n_nodes=0, off=None, plans=None, steps=None) == OK            # no nodes: no-op
     assert ctypes.sizeof(ctypes.c_double) * 8 + 4 * 8 + 4 * 8 == _native.PLAN_BYTES
+    assert ctypes.sizeof(ctypes.c_double) + 4 + 4 == _native.STEP_BYTES
 
 
 def test_prioritize_validation_and_workspace(lib):

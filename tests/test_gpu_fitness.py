@@ -58,7 +58,8 @@ def _nodes(rng, M_, n_src, n_models=16):
         free_bytes=rng.uniform(0, 300, M_) * GB,
         queue_ms=rng.uniform(0, 5000, M_).astype(np.float32),
         act_ms=rng.uniform(2000, 20000, M_).astype(np.float32),
-        resident_mask=rng.integers(0, 1 << n_models, M_).astype(np.uint64),
+        # residency over all 64 bits (models past n_models never ask for theirs)
+        resident_mask=rng.integers(0, 2 ** 64, M_, dtype=np.uint64),
         deg_ms=np.where(rng.random(M_) < 0.3, rng.uniform(0, 500, M_), 0).astype(np.float32),
         rtt_ms=rng.uniform(0.2, 80, (n_src, M_)).astype(np.float32),
     )
@@ -159,11 +160,15 @@ def _engines(rng, M_, max_e=8, level_p=(0.3, 0.2, 0.1, 0.25, 0.15)):
 
 
 def gpu_plans(off, level, freed, cost, c_int):
+    """(record freed [M][8], record cost [M][8], n_engines [M], raw records, step freed [E],
+    step cost [E], step engine [E])"""
     p = M.degradation_plans(_t(off), _t(level), _t(freed), _t(cost), c_int)
     torch.cuda.synchronize()
-    raw = p.cpu().numpy()
+    raw = p.records.cpu().numpy()
+    st = p.steps.cpu().numpy()[: int(off[-1])]
     return (raw[:, :64].copy().view(np.float64), raw[:, 64:96].copy().view(np.float32),
-            raw[:, 96:100].copy().view(np.int32)[:, 0], raw)
+            raw[:, 96:100].copy().view(np.int32)[:, 0], raw, st[:, :8].copy().view(np.float64)[:, 0],
+            st[:, 8:12].copy().view(np.float32)[:, 0], st[:, 12:16].copy().view(np.int32)[:, 0])
 
 
 def _plan_answer(pf, pc, ne, R):
@@ -174,33 +179,46 @@ def _plan_answer(pf, pc, ne, R):
     return None
 
 
-def test_degradation_plans_match_oracle():
+@pytest.mark.parametrize("max_e", [8, 40])
+def test_degradation_plans_match_oracle(max_e):
     # every boundary of every node's plan: R at a prefix's freed bytes is met by that prefix,
-    # one ulp above it needs the next one (or fails)
-    rng = np.random.default_rng(5)
+    # one ulp above it needs the next one (or fails). Up to 40 engines a node: nodes past the
+    # record's eight steps are sorted by rank counting and continue in the step array.
+    rng = np.random.default_rng(5 + max_e)
     M_ = 700
-    off, level, freed, cost = _engines(rng, M_)
+    off, level, freed, cost = _engines(rng, M_, max_e=max_e)
     level[off[10]:off[11]] = 4                          # equal levels: engine order decides
     for c_int in (2000.0, 0.0):
-        pf, pc, ne, raw = gpu_plans(off, level, freed, cost, c_int)
+        pf, pc, ne, raw, sf, sc, se = gpu_plans(off, level, freed, cost, c_int)
         assert (ne == np.diff(off)).all()
-        assert not raw[:, 100:].any()                   # reserved words are zero
+        assert (raw[:, 100:104].copy().view(np.int32)[:, 0] == off[:-1]).all()   # first step
+        assert not raw[:, 104:].any()                   # reserved words are zero
         checked = 0
         for j in range(M_):
             lv, fr, co = level[off[j]:off[j + 1]], freed[off[j]:off[j + 1]], cost[off[j]:off[j + 1]]
-            Rs = [1.0, 1e12]
+            jf, jc, je = sf[off[j]:off[j + 1]], sc[off[j]:off[j + 1]], se[off[j]:off[j + 1]]
+            # the steps take every engine once, in (level, index) order
+            assert je.tolist() == sorted(range(off[j], off[j + 1]), key=lambda e: (level[e], e))
+            # the record holds the first eight steps, +inf and 0 past the node's engines
+            h = min(ne[j], 8)
+            assert np.array_equal(pf[j, :h], jf[:h]) and np.array_equal(pc[j, :h].view(np.uint32),
+                                                                        jc[:h].view(np.uint32))
+            assert np.isposinf(pf[j, h:]).all() and (pc[j, h:] == 0).all()
+            Rs = [1.0, 1e13]
             for e in range(ne[j]):
-                Rs += [pf[j, e], np.nextafter(pf[j, e], np.inf)]
+                Rs += [jf[e], np.nextafter(jf[e], np.inf)]
             for R in Rs:
                 if R <= 0:
                     continue
                 ref = oracle.degradation_cost(R, lv, fr, co, c_int)
-                got = _plan_answer(pf[j], pc[j], ne[j], R)
+                got = _plan_answer(jf, jc, ne[j], R)
                 assert (got is None) == (ref is None), (j, R, got, ref)
                 if ref is not None:
                     assert np.float32(got).view(np.uint32) == np.float32(ref).view(np.uint32), (j, R, got, ref)
                 checked += 1
         assert checked > 4 * M_
+        if max_e > 8:
+            assert (ne > 8).sum() > 100
 
 
 def test_degradation_plans_empty_and_single():
@@ -208,11 +226,11 @@ def test_degradation_plans_empty_and_single():
     level = np.array([5], np.int32)
     freed = np.array([3 * GB])
     cost = np.array([40.0], np.float32)
-    pf, pc, ne, _ = gpu_plans(off, level, freed, cost, 2000.0)
+    pf, pc, ne = gpu_plans(off, level, freed, cost, 2000.0)[:3]
     assert ne.tolist() == [0, 1, 0]
     assert pf[1, 0] == 3 * GB and pc[1, 0] == np.float32(2040.0)
-    pf, pc, ne, _ = gpu_plans(np.zeros(3, np.int32), np.zeros(0, np.int32), np.zeros(0), np.zeros(0, np.float32),
-                              10.0)
+    pf, pc, ne = gpu_plans(np.zeros(3, np.int32), np.zeros(0, np.int32), np.zeros(0), np.zeros(0, np.float32),
+                           10.0)[:3]
     assert ne.tolist() == [0, 0]
 
 
@@ -228,15 +246,19 @@ def gpu_fitness_plans(model, src, cls, kv, nodes, weights, bounds, eng, k=1, rho
     return idx.cpu().numpy(), fit.cpu().numpy()
 
 
-@pytest.mark.parametrize("n,M_,n_src,k", [(1, 1, 1, 1), (300, 255, 2, 1), (1000, 257, 5, 3),
-                                          (2000, 1300, 16, 16), (513, 700, 3, 4)])
-def test_fitness_with_plans_matches_oracle(n, M_, n_src, k):
-    # several 256-node chunks with ragged tails; most stages fall short on many nodes
-    rng = np.random.default_rng(n * 13 + M_)
+@pytest.mark.parametrize("n,M_,n_src,k,max_e", [(1, 1, 1, 1, 8), (300, 255, 2, 1, 8), (1000, 257, 5, 3, 8),
+                                                (2000, 1300, 16, 16, 8), (513, 700, 3, 4, 8), (1000, 300, 4, 1, 30),
+                                                (777, 1100, 3, 4, 30)])
+def test_fitness_with_plans_matches_oracle(n, M_, n_src, k, max_e):
+    # several 128-node chunks with ragged tails; most stages fall short on many nodes; with up to
+    # 30 engines a node, shortfalls beyond a record's eight steps search the step array
+    rng = np.random.default_rng(n * 13 + M_ + max_e)
     nodes = _nodes(rng, M_, n_src)
     nodes["free_bytes"] = rng.uniform(0, 60, M_) * GB
     nodes["free_bytes"][rng.random(M_) < 0.05] = 0.0
-    off, level, freed, cost = _engines(rng, M_)
+    off, level, freed, cost = _engines(rng, M_, max_e=max_e)
+    if max_e > 8:
+        freed = freed * 0.2                               # small actions: long plans on big nodes
     eng = (off, level, freed, cost, 2000.0)
     model = rng.integers(0, 16, n).astype(np.int32)
     src = rng.integers(0, n_src, n).astype(np.int32)

@@ -1,14 +1,20 @@
 """Parity of the two-phase predictor (Sec. III-B: calibrated tool intent, Eq. 1; per-role log(1 + L)
 regressors; Eq. 3) between the HIP path (through the C-ABI) and the CPU oracle, on seeded inputs.
 
-Bars (element by element), from an error bound DZ = 1e-2 on every head's pre-activation z (the
-GPU accumulates in float32, the oracle in float64, and a bfloat16 hidden activation whose two
-pre-activations straddle a rounding boundary differs by one bfloat16 ulp, 2^-7 relative; the
-worst case seen is about 1e-3):
-  p_tool : |dp| <= 0.25 * S * DZ, S the steepest slope of the calibration table (the logistic
-           function's slope is at most 1/4);
-  length : |dL| <= (1 + L) * (DZ + |coef_g| |dp|), since y = z_g + coef_g p and L = expm1(y);
-  kv     : equal, bit for bit, to Eq. 3 on the GPU's own length.
+Bars (element by element):
+  every stage   : |dp| <= 1e-3 and |dL| <= 1e-2 max(L, 1) (the bfloat16 predictor's relative
+                  tolerance), with at most one stage in a thousand allowed the derived bound below
+                  instead;
+  derived bound : from DZ = 2e-3 on every head's pre-activation z (the GPU accumulates in float32,
+                  the oracle in float64, and a bfloat16 hidden activation whose two pre-activations
+                  straddle a rounding boundary differs by one bfloat16 ulp, 2^-8 to 2^-7 relative; the worst
+                  implied error seen is about 1e-3): |dp| <= 0.25 * S * DZ, S the steepest slope of
+                  the calibration table (the logistic function's slope is at most 1/4), and
+                  |dL| <= (1 + L) * (DZ + |coef_g| |dp|), since y = z_g + coef_g p and L = expm1(y).
+                  A steep calibration segment multiplies the pre-activation error of z_0 by up to
+                  S / 4 (S is 12-16 in the workloads' tables), so a stage whose z_0 moved by a
+                  hidden-rounding flip can leave the 1e-3 bar on p while its z stays within DZ;
+  kv            : equal, bit for bit, to Eq. 3 on the GPU's own length;
 and, against systematic slips, 99% of stages within 1e-4 in p and 1e-3 in log(1 + L).
 """
 import ctypes
@@ -25,7 +31,9 @@ from paper_2606_12950_amd import workload as W
 
 pytestmark = pytest.mark.gpu
 
-DZ = 1e-2
+DZ = 2e-3
+TIGHT_P, TIGHT_L = 1e-3, 1e-2
+MAX_DERIVED = 1e-3      # fraction of stages that may need the derived bound
 
 
 def _t(a):
@@ -72,15 +80,26 @@ def check(w, tp, got, ref, rows=None, role=None):
     assert np.all(np.isfinite(pg)) and np.all(np.isfinite(lg))
     slope = (np.diff(tp.iso_y.astype(np.float64)) / np.diff(tp.iso_x.astype(np.float64))).max()
     dp = np.abs(pg.astype(np.float64) - po)
-    assert dp.max() <= 0.25 * slope * DZ, f"p_tool max err {dp.max():.3e} at {dp.argmax()}"
     g = np.ones(role.shape[0], np.int64)
     ok = (role >= 0) & (role < tp.role_head.size)
     g[ok] = tp.role_head[role[ok]]
     g[(g < 1) | (g >= tp.tool_coef.size)] = 1
-    dl = np.abs(lg.astype(np.float64) - lo) / (1.0 + lo.astype(np.float64))
+    lo64 = lo.astype(np.float64)
+    rel = np.abs(lg.astype(np.float64) - lo64) / np.maximum(lo64, 1.0)
+    tight = (dp <= TIGHT_P) & (rel <= TIGHT_L)
+    derived = np.flatnonzero(~tight)
+    assert derived.size <= MAX_DERIVED * max(tight.size, 1000), \
+        f"{derived.size} stages outside |dp| <= 1e-3, |dL| <= 1e-2 L, first {derived[:5]}"
+    dl = np.abs(lg.astype(np.float64) - lo64) / (1.0 + lo64)
+    assert np.all(dp[derived] <= 0.25 * slope * DZ), f"p_tool max err {dp.max():.3e} at {dp.argmax()}"
     bound = DZ + np.abs(tp.tool_coef[g].astype(np.float64)) * dp
-    assert np.all(dl <= bound), f"length err {dl.max():.3e} at {dl.argmax()}: {lg[dl.argmax()]} vs {lo[dl.argmax()]}"
+    assert np.all(dl[derived] <= bound[derived]), \
+        f"length err {dl.max():.3e} at {dl.argmax()}: {lg[dl.argmax()]} vs {lo[dl.argmax()]}"
     assert np.quantile(dp, 0.99) <= 1e-4 and np.quantile(dl, 0.99) <= 1e-3
+    # the pre-activation error the lengths imply: dy = dz_g + coef_g dp
+    dz = np.abs(np.log1p(lg.astype(np.float64)) - np.log1p(lo64))
+    print(f"  two-phase: {derived.size} of {tight.size} stages on the derived bound; max |dp| {dp.max():.2e}, "
+          f"max rel dL {rel.max():.2e}, max |dy| {dz.max():.2e}", flush=True)
     assert np.all(pg[tp.tool_avail[sel] == 0] == 0.0)
     alpha = w.kv_bytes_per_token[w.model_id[sel]].astype(np.float64)
     assert np.array_equal(kg, (w.prompt_len[sel].astype(np.float64) + lg.astype(np.float64)) * alpha)

@@ -193,13 +193,14 @@ def test_degradation_plan_closed_forms():
 
 
 def test_degradation_plan_is_the_shortest_sufficient_priority_prefix():
+    # any number of engines: the definition has no cap
     rng = np.random.default_rng(8)
-    for _ in range(500):
-        ne = int(rng.integers(0, 9))
+    for t in range(600):
+        ne = int(rng.integers(0, 9)) if t < 400 else int(rng.integers(9, 80))
         level = rng.integers(1, 6, ne).astype(np.int32)
         freed = rng.choice([1.0, 2.0, 3.0, 5.0], ne)             # coarse: many exact coverings
         cost = rng.uniform(0, 100, ne).astype(np.float32)
-        R = float(rng.choice([0.5, 1.0, 2.0, 3.0, 4.0, 7.0, 11.0, 30.0]))
+        R = float(rng.choice([0.5, 1.0, 2.0, 3.0, 4.0, 7.0, 11.0, 30.0, 60.0, 150.0]))
         order = sorted(range(ne), key=lambda i: (level[i], i))
         want = None
         for j in range(1, ne + 1):                               # shortest prefix freeing R
@@ -211,6 +212,74 @@ def test_degradation_plan_is_the_shortest_sufficient_priority_prefix():
                 want = float(np.float32(c + (np.float32(250) if (level[plan] >= 4).any() else np.float32(0))))
                 break
         assert oracle.degradation_cost(R, level, freed, cost, 250.0) == want
+
+
+def test_late_low_level_engine_is_taken_first():
+    # a ninth, tenth ... engine of the lowest level comes first in priority order: a plan that
+    # truncated the list at eight engines would miss it
+    level = np.array([3] * 12 + [1], np.int32)
+    freed = np.array([1.0] * 12 + [50.0])
+    cost = np.array([10.0] * 12 + [7.0], np.float32)
+    assert oracle.degradation_cost(40.0, level, freed, cost, 1000.0) == 7.0
+    assert oracle.degradation_cost(52.0, level, freed, cost, 1000.0) == 27.0     # 1-level, then two 3s
+    assert oracle.degradation_cost(63.0, level, freed, cost, 1000.0) is None
+
+
+def _quotient_pairs(rng, n):
+    """float32 pairs (a, b), 0 < a <= b, whose correctly rounded quotient a / b differs from the
+    product of a with the rounded reciprocal of b"""
+    a = rng.uniform(1e8, 3e11, 20 * n).astype(np.float32)
+    b = (a * rng.uniform(1.0, 8.0, a.size)).astype(np.float32)
+    with np.errstate(all="ignore"):
+        q = a / b
+        r = a * (np.float32(1) / b)
+    sel = np.flatnonzero(q != r)[:n]
+    assert sel.size == n
+    return a[sel], b[sel], q[sel]
+
+
+def test_fit_is_the_float32_quotient():
+    # gamma = lambda = mu = 0: the fitness is the fit alone, R_need / headroom rounded once
+    rng = np.random.default_rng(21)
+    a, b, q = _quotient_pairs(rng, 200)
+    for ai, bi, qi in zip(a, b, q):
+        nodes = dict(free_bytes=np.array([float(bi)]), queue_ms=np.zeros(1, np.float32),
+                     act_ms=np.zeros(1, np.float32), resident_mask=np.zeros(1, np.uint64),
+                     deg_ms=np.zeros(1, np.float32), rtt_ms=np.zeros((1, 1), np.float32))
+        one = np.zeros(1, np.int32)
+        idx, fit = _route(nodes, one, one, one, np.array([float(ai)]), [0, 0, 0], [0, 1, 0, 1, 0, 1])
+        assert idx[0, 0] == 0 and fit[0, 0].view(np.uint32) == qi.view(np.uint32)
+
+
+def test_normalisation_is_the_float32_quotient():
+    # gamma = 1, lambda = mu = 0: the fitness is 1 - norm(RTT), norm = (x - lo) / (hi - lo)
+    rng = np.random.default_rng(22)
+    lo = np.float32(0.0)
+    a, b, q = _quotient_pairs(rng, 100)
+    for ai, bi, qi in zip(a, b, q):
+        # x - lo = ai and hi - lo = bi exactly (lo = 0), inside the window
+        nodes = dict(free_bytes=np.array([1e12]), queue_ms=np.zeros(1, np.float32),
+                     act_ms=np.zeros(1, np.float32), resident_mask=np.zeros(1, np.uint64),
+                     deg_ms=np.zeros(1, np.float32), rtt_ms=np.array([[ai]], np.float32))
+        one = np.zeros(1, np.int32)
+        _, fit = _route(nodes, one, one, one, np.array([1.0]), [1, 0, 0], [lo, bi, 0, 1, 0, 1])
+        assert fit[0, 0].view(np.uint32) == (np.float32(1) - qi).view(np.uint32)
+
+
+def test_penalties_add_before_they_leave_the_affinity():
+    # S = A - (lambda T + mu C): with A = 0 (gamma = 1, RTT at the window top) the fitness is the
+    # negated float32 sum of the two weighted penalties
+    rng = np.random.default_rng(23)
+    for _ in range(200):
+        t, c = rng.uniform(0, 1, 2).astype(np.float32)
+        lam, mu = rng.uniform(0.1, 3, 2).astype(np.float32)
+        nodes = dict(free_bytes=np.array([1e12]), queue_ms=np.array([t], np.float32),
+                     act_ms=np.zeros(1, np.float32), resident_mask=np.ones(1, np.uint64),
+                     deg_ms=np.array([c], np.float32), rtt_ms=np.array([[5.0]], np.float32))
+        one = np.zeros(1, np.int32)
+        _, fit = _route(nodes, one, one, one, np.array([1.0]), [1, lam, mu], [0, 5, 0, 1, 0, 1])
+        want = -(np.float32(lam * t) + np.float32(mu * c))
+        assert fit[0, 0].view(np.uint32) == np.float32(want).view(np.uint32)
 
 
 def test_fitness_with_degradation_plans():
