@@ -38,7 +38,9 @@
  *     indexed out of bounds. Other per-element data is a precondition, not checked: finite
  *     inputs (stage latency excepted), monotone chain offsets.
  *   - Empty inputs (n = 0, n_workflows = 0) are valid no-ops that return MAESTRO_OK.
- *   - Entry points are re-entrant: the library has no mutable global state.
+ *   - Entry points are re-entrant: the library has no mutable global state beyond the
+ *     per-device address of maestro_prioritize_noalloc's static scratch (resolved once under
+ *     a lock).
  */
 #ifndef MAESTRO_H
 #define MAESTRO_H
@@ -372,6 +374,25 @@ MAESTRO_API maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_sta
                                   int64_t now_us, int64_t* remaining_us, int32_t* slack_key,
                                   int32_t* order, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/* maestro_prioritize for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same computation, outputs
+ * and errors, with the radix sort's scratch in a static device array of
+ * MAESTRO_PRIORITIZE_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on until
+ * the process ends, so the call takes no workspace and allocates nothing. Batches of up to
+ * MAESTRO_PRIORITIZE_NOALLOC_MAX_WORKFLOWS workflows; larger ones return MAESTRO_ERR_WORKSPACE
+ * before anything is enqueued. The stream must belong to the current device; the first call with
+ * a device current resolves that device's copy of the array (and returns MAESTRO_ERR_LAUNCH if
+ * it cannot). Every call on one GPU shares that GPU's array and leaves its contents behind:
+ * calls that overlap in time on one GPU (two streams, two host threads) race and give undefined
+ * results; calls ordered on one stream do not. */
+#define MAESTRO_PRIORITIZE_NOALLOC_MAX_WORKFLOWS (1 << 20)
+#define MAESTRO_PRIORITIZE_NOALLOC_SCRATCH_BYTES ((size_t)17 << 20)
+MAESTRO_API maestro_status maestro_prioritize_noalloc(int32_t n_workflows, int64_t n_stages,
+                                  const int64_t* chain_offset, const float* stage_latency_s,
+                                  const int32_t* cursor, const int64_t* deadline_us,
+                                  int64_t now_us, int64_t* remaining_us, int32_t* slack_key,
+                                  int32_t* order, void* stream);
 
 /* Workspace sizes in bytes (0 = none needed). */
 MAESTRO_API size_t maestro_predict_workspace(const maestro_predictor* p, int64_t n);

@@ -23,7 +23,10 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 # Every function declared in include/maestro.h.
 EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_tiered", "maestro_route_ex", "maestro_route_fitness",
            "maestro_degradation_plans", "maestro_activation_latency", "maestro_adaptive_rho", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
-           "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string")
+           "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string",
+           "maestro_prioritize_noalloc")
+
+PRIORITIZE_NOALLOC_MAX_WORKFLOWS = 1 << 20
 
 ROUTE_AUTO, ROUTE_SCAN, ROUTE_SORTED = 0, 1, 2
 
@@ -86,7 +89,9 @@ def load():
     lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P, P]
     lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
-    for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize"):
+    lib.maestro_prioritize_noalloc.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P]
+    for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize",
+              "maestro_prioritize_noalloc"):
         getattr(lib, f).restype = ctypes.c_int
     lib.maestro_predict_workspace.argtypes = [ctypes.POINTER(Predictor), i64]
     lib.maestro_route_workspace.argtypes = [i64, i32, i32, i32]
@@ -496,9 +501,12 @@ def prioritize_workspace_bytes(n_workflows: int, n_stages: int) -> int:
 def prioritize(chain_offset: torch.Tensor, stage_latency_s: torch.Tensor, deadline_us: torch.Tensor,
                now_us: int, cursor: Optional[torch.Tensor] = None, want_remaining: bool = True,
                out: Optional[Tuple[Optional[torch.Tensor], torch.Tensor, torch.Tensor]] = None,
-               workspace: Optional[torch.Tensor] = None, stream=None):
+               workspace: Optional[torch.Tensor] = None, stream=None, noalloc: bool = False):
     """maestro_prioritize: returns (remaining_us int64 [S] or None, slack_key int32 [W],
-    order int32 [W])."""
+    order int32 [W]). With ``noalloc`` maestro_prioritize_noalloc instead: the library's static
+    scratch replaces the workspace (at most PRIORITIZE_NOALLOC_MAX_WORKFLOWS workflows; calls
+    that overlap in time on one GPU race), so ``out`` preallocated makes the call allocate
+    nothing."""
     lib = load()
     _dev(chain_offset, "chain_offset", torch.int64)
     _dev(stage_latency_s, "stage_latency_s", torch.float32)
@@ -523,6 +531,14 @@ def prioritize(chain_offset: torch.Tensor, stage_latency_s: torch.Tensor, deadli
         _shape(_dev(rem, "remaining_us", torch.int64), "remaining_us", (S,))
     _shape(_dev(key, "slack_key", torch.int32), "slack_key", (W,))
     _shape(_dev(order, "order", torch.int32), "order", (W,))
+    if noalloc:
+        if workspace is not None:
+            raise ValueError("the allocation-free call takes no workspace")
+        st = lib.maestro_prioritize_noalloc(W, S, _ptr(chain_offset), _ptr(stage_latency_s), _ptr(cursor),
+                                            _ptr(deadline_us), int(now_us), _ptr(rem), _ptr(key), _ptr(order),
+                                            _stream(stream))
+        _check("maestro_prioritize_noalloc", st)
+        return rem, key, order
     _workspace(workspace)
     ws_bytes = prioritize_workspace_bytes(W, S)
     if workspace is None:

@@ -287,4 +287,27 @@ maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,
                                     workspace, workspace_bytes, as_stream(stream));
 }
 
+maestro_status maestro_prioritize_noalloc(int32_t n_workflows, int64_t n_stages, const int64_t* chain_offset,
+                                          const float* stage_latency_s, const int32_t* cursor,
+                                          const int64_t* deadline_us, int64_t now_us, int64_t* remaining_us,
+                                          int32_t* slack_key, int32_t* order, void* stream) {
+  if (n_workflows < 0 || n_stages < 0) return MAESTRO_ERR_INVALID_ARG;
+  if (n_workflows == 0) return MAESTRO_OK;
+  if (n_workflows > MAESTRO_PRIORITIZE_NOALLOC_MAX_WORKFLOWS) return MAESTRO_ERR_WORKSPACE;
+  const size_t need = maestro::prioritize_workspace_bytes(n_workflows, n_stages);
+  if (need > MAESTRO_PRIORITIZE_NOALLOC_SCRATCH_BYTES) return MAESTRO_ERR_WORKSPACE;
+  if (!chain_offset || !deadline_us || !slack_key || !order) return MAESTRO_ERR_INVALID_ARG;
+  if (n_stages > 0 && !stage_latency_s) return MAESTRO_ERR_INVALID_ARG;
+  if (!aligned(chain_offset, 8) || !aligned(deadline_us, 8) || !aligned(slack_key, 4) ||
+      !aligned(order, 4) || !aligned(stage_latency_s, 4) || !aligned(cursor, 4) ||
+      !aligned(remaining_us, 8))
+    return MAESTRO_ERR_INVALID_ARG;
+  void* scratch = nullptr;
+  const maestro_status st = maestro::static_prioritize_scratch(&scratch);
+  if (st != MAESTRO_OK) return st;
+  return maestro::launch_prioritize(n_workflows, n_stages, chain_offset, stage_latency_s, cursor, deadline_us,
+                                    now_us, remaining_us, slack_key, order, scratch,
+                                    MAESTRO_PRIORITIZE_NOALLOC_SCRATCH_BYTES, as_stream(stream));
+}
+
 }  // extern "C"

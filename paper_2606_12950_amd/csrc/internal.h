@@ -62,6 +62,8 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
                                  int32_t* order, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 size_t prioritize_workspace_bytes(int32_t n_workflows, int64_t n_stages);
+// the static scratch of maestro_prioritize_noalloc on the current device
+maestro_status static_prioritize_scratch(void** out);
 
 inline maestro_status launch_status() {
   return hipGetLastError() == hipSuccess ? MAESTRO_OK : MAESTRO_ERR_LAUNCH;

@@ -21,7 +21,15 @@
 //     relative order.
 //     The key array is padded to whole tiles with all-ones keys, which always sort last and
 //     never reach the caller's output.
+#include <mutex>
+
 #include "internal.h"
+
+// Scratch of maestro_prioritize_noalloc: the radix key/value buffers and count tables of the
+// largest batch it takes, in static device memory that every GPU the library runs on holds
+// until the process ends. Host code never names it: kernels get the address resolved per device
+// by hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[MAESTRO_PRIORITIZE_NOALLOC_SCRATCH_BYTES];
 
 namespace maestro {
 namespace {
@@ -404,6 +412,28 @@ PrioLayout prio_layout(int32_t n_workflows) {
 
 size_t prioritize_workspace_bytes(int32_t n_workflows, int64_t) {
   return n_workflows > 0 ? prio_layout(n_workflows).total : 0;
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of the static scratch on the current device, resolved on the first call made
+// with that device current and kept for later calls.
+maestro_status static_prioritize_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MAESTRO_ERR_LAUNCH;
+  if (dev < 0 || dev >= kMaxDevices) return MAESTRO_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MAESTRO_ERR_LAUNCH;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MAESTRO_OK;
 }
 
 maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,

@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -258,6 +258,17 @@ def test_prioritize_validation_and_workspace(lib):
     assert call(off=None) == INVALID
     assert call(ws_bytes=100) == WORKSPACE
     assert call(ws=None) == WORKSPACE
+    assert call(W=0) == OK                                                   # empty: no-op
+
+
+def test_prioritize_noalloc_validation(lib):
+    call = lambda W=4, S=8, off=FAKE, key=FAKE: lib.maestro_prioritize_noalloc(
+        W, S, off, FAKE, None, FAKE, 0, None, key, FAKE, None)
+    assert call(W=-1) == INVALID
+    assert call(S=-1) == INVALID
+    assert call(off=None) == INVALID
+    assert call(key=MISALIGNED4) == INVALID
+    assert call(W=_native.PRIORITIZE_NOALLOC_MAX_WORKFLOWS + 1) == WORKSPACE   # beyond the static scratch
     assert call(W=0) == OK                                                   # empty: no-op
 
 
