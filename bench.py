@@ -1,6 +1,6 @@
 """Throughput of the batched predict -> route -> prioritize step on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--no-cpu-baseline] [--no-chained]
 python bench.py --calibrate-copy MIB   (plain device copy of MIB mebibytes, for counter calibration)
 python bench.py --sweep-prioritize     (slack ordering alone, W = 2^17 .. 2^26 workflows)
 python bench.py --route-fitness        (routing by fitness, Eq. 5, on the workload's predictions)
@@ -11,10 +11,12 @@ python bench.py --margin               (the adaptive safety margin rho, Sec. III
 python bench.py --route-tiered         (latency routing with T_act from readiness tiers beside the plain route)
 
 One step = predict (fused MLP + softmax + expected length + KV bytes) -> route (feasibility,
-scores, best node) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
-whose inputs are already resident in device memory. The default workload is the chained
-batch: 131,072 workflows of 3..8 stages (719,712 stages), 512 nodes, 16 models, predictor
-256-512-512-64 in bfloat16. Prints one JSON line.
+scores, best nodes) -> prioritize (chain suffix sums, slack keys, stable sort) over one batch
+whose inputs are already resident in device memory. The default workload is the largest one:
+4,194,304 stages, 4,096 nodes, 64 models, predictor 256-1024-1024-64 in bfloat16, top-4 routes.
+It has no workflow chains, so its step is predict -> route; the chained batch (131,072
+workflows of 3..8 stages, 719,712 stages, 512 nodes, predictor 256-512-512-64) is timed in the
+same run as the full three-phase step and reported under "chained_step". Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -59,9 +61,9 @@ def measured_traffic(workload: str):
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if rec.get("predict_source_sha256_16") != predict_source_hash() or rec.get("workload") != workload:
+    if rec.get("predict_source_sha256_16") != predict_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("records", {}).get(workload, {}).get("hbm_bytes_per_launch")
 
 
 def calibrate_copy(mib: int, reps: int = 5):
@@ -82,6 +84,21 @@ def mlp_flop_per_stage(dims):
 
 
 def cpu_model() -> str:
+    """The host CPU as lscpu names it (model name, sockets x cores, threads), else /proc/cpuinfo."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        f = {}
+        for line in out.splitlines():
+            if ":" in line:
+                k, v = line.split(":", 1)
+                f[k.strip()] = v.strip()
+        name = f.get("Model name", "unknown")
+        return (f"{name}; {f.get('Socket(s)', '?')} socket(s) x {f.get('Core(s) per socket', '?')} cores x "
+                f"{f.get('Thread(s) per core', '?')} threads; family {f.get('CPU family', '?')} model "
+                f"{f.get('Model', '?')} stepping {f.get('Stepping', '?')}; {f.get('CPU(s)', '?')} CPUs visible")
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
@@ -104,6 +121,38 @@ def route_bytes(n, m, k):
     return n * (16 + 8 * k) + 24 * m
 
 
+def walk_entries(wl, pred, kv, rows, chunk=2048):
+    """Mean number of list entries the sorted-walk route visits per stage, over ``rows``: the
+    walk goes through its model's nodes in (ready time, index) order, skips nodes whose headroom
+    cannot admit the stage, and stops at the first admitting node whose score exceeds its k-th
+    best once it holds k nodes. Counted on the host from the same inputs (the kernel keeps no
+    counter)."""
+    n_nodes, k = wl.spec.n_nodes, wl.spec.k
+    assert pred.shape == kv.shape == (wl.n,), "pred and kv of every stage of the batch"
+    need = kv.astype(np.float64) * (1.0 + wl.spec.rho) if wl.spec.rho else kv.astype(np.float64)
+    exec_s = (pred.astype(np.float32) * wl.decode_s_per_token[wl.model_id]).astype(np.float32)
+    bits = (wl.resident_mask[:, None] >> np.arange(wl.spec.n_models, dtype=np.uint64)[None, :]) & np.uint64(1)
+    total = 0
+    for m in range(wl.spec.n_models):
+        ready = np.where(bits[:, m] == 1, wl.queue_s + np.float32(0), wl.queue_s + wl.cold_s).astype(np.float32)
+        order = np.lexsort((np.arange(n_nodes), ready))
+        r_sorted, f_sorted = ready[order], wl.free_bytes[order]
+        sel = rows[wl.model_id[rows] == m]
+        for c in range(0, sel.size, chunk):
+            s = sel[c:c + chunk]
+            feas = need[s][:, None] <= f_sorted[None, :]
+            sc = (r_sorted[None, :] + exec_s[s][:, None]).astype(np.float32)
+            cnt = np.cumsum(feas, axis=1)
+            full = cnt[:, -1] >= k
+            kth_pos = np.argmax(cnt >= k, axis=1)
+            kth = sc[np.arange(s.size), kth_pos]
+            stop = feas & (sc > kth[:, None]) & (np.arange(n_nodes)[None, :] > kth_pos[:, None])
+            has_stop = stop.any(axis=1) & full
+            visited = np.where(has_stop, np.argmax(stop, axis=1) + 1, n_nodes)
+            total += int(visited.sum())
+    return total / max(rows.size, 1)
+
+
 def prioritize_bytes(n_stages, n_workflows, passes=4):
     """Algorithmic HBM bytes of the slack ordering: per stage the latency in (4 B) and the
     remaining time out (8 B); per workflow chain offsets, deadline in and key out (16 + 4 B),
@@ -111,15 +160,15 @@ def prioritize_bytes(n_stages, n_workflows, passes=4):
     return n_stages * 12 + n_workflows * (20 + passes * 16 + 4)
 
 
-def cpu_baseline(wl, n_workflows_sample: int):
-    """Oracle (C, OpenMP over stages) on the first workflows of the batch: predict -> route ->
-    prioritize, timed on the host cores."""
+def cpu_baseline(wl, n_workflows_sample: int, n_stages_sample: int):
+    """Oracle (C, OpenMP over stages) on the first workflows (chained batch) or the first stages
+    of the batch: predict -> route (-> prioritize), timed on the host cores."""
     import oracle
     W_ = min(n_workflows_sample, wl.n_workflows) if wl.n_workflows else 0
     if W_:
         S = int(wl.chain_offset[W_])
     else:
-        S = min(wl.n, n_workflows_sample * 5)
+        S = min(wl.n, n_stages_sample)
     rows = np.arange(S)
     threads = oracle.max_threads()
     t0 = time.perf_counter()
@@ -130,7 +179,8 @@ def cpu_baseline(wl, n_workflows_sample: int):
     dt = time.perf_counter() - t0
     which = "all" if W_ == wl.n_workflows else "first"
     sample = (f"{which} {W_} workflows ({S} stages) of the same batch: oracle predict + route + prioritize"
-              if W_ else f"first {S} stages of the same batch: oracle predict + route")
+              if W_ else f"first {S} of {wl.n} stages of the same batch (a deterministic prefix; every node): "
+                         f"oracle predict + route")
     return {"value": S / dt, "unit": "stages/s", "cores": int(threads), "kind": "oracle",
             "sample": sample, "seconds": round(dt, 3), "cpu_model": cpu_model()}
 
@@ -397,10 +447,15 @@ def margin_bench(steps: int, warmup: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c3", choices=["c0", "c1", "c2", "c3", "c4"])
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c4", choices=["c0", "c1", "c2", "c3", "c4"])
     ap.add_argument("--cpu-sample-workflows", type=int, default=131072)
+    ap.add_argument("--cpu-sample-stages", type=int, default=262144,
+                    help="stages of a batch without chains that the oracle baseline runs (a prefix)")
+    ap.add_argument("--no-chained", action="store_true",
+                    help="skip the chained batch's three-phase step after a batch without chains")
+    ap.add_argument("--chained-steps", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--sweep-prioritize", nargs="?", const="17:26", default=None, metavar="LO:HI",
@@ -454,20 +509,48 @@ def main():
     torch.cuda.set_device(0)
 
     wl = W.workload(args.workload)
-    spec = wl.spec
+    step = time_step(wl, args.steps, args.warmup)
+    line = step_record(wl, step, args.steps)
+    line.update({"metric": METRIC, "value": line.pop("stages_per_s"), "unit": "stages/s", "n_gpus": 1,
+                 "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
+                 "vs_baseline": None, "dtype": wl.spec.dtype, "data": "synthetic"})
+    order = ["metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better", "scaling",
+             "vs_baseline", "dtype", "data", "config", "roofline"]
+    line = {**{key: line[key] for key in order}, **{key: v for key, v in line.items() if key not in order}}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_workflows, args.cpu_sample_stages)
+        if line["route"]["algorithm"] == "sorted walk":
+            rows = np.arange(min(wl.n, args.cpu_sample_stages))
+            line["route"]["walk_entries_per_stage"] = round(walk_entries(wl, step["pred"], step["kv"], rows), 3)
+            line["route"]["walk_sample"] = f"first {rows.size} stages, host count of the walk's stopping rule"
+    if wl.n_workflows == 0 and not args.no_chained:
+        del step, wl
+        torch.cuda.empty_cache()
+        cw = W.workload("c3")
+        cs = time_step(cw, args.chained_steps, args.warmup)
+        rec = step_record(cw, cs, args.chained_steps)
+        line["chained_step"] = {key: rec[key] for key in ("stages_per_s", "ms_per_step", "config", "roofline",
+                                                          "step_ms", "phase_ms", "route", "prioritize")}
+        line["chained_step"]["steps"] = args.chained_steps
+    print(json.dumps(line), flush=True)
+
+
+def time_step(wl, steps: int, warmup: int):
+    """Times ``steps`` passes of predict -> route (-> prioritize for chained batches) with the
+    batch resident on the GPU: the wall clock of the whole run, bracketed by synchronisation, and
+    HIP events on the launch stream around each phase."""
+    import torch
+    from paper_2606_12950_amd import pipeline
     b = pipeline.to_device(wl)
     o = pipeline.allocate_outputs(b)
     chained = b.chain_offset is not None
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         pipeline.run_step(b, o)
     torch.cuda.synchronize()
-
-    K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(K):
+    for i in range(steps):
         e = ev[i]
         e[0].record()
         pipeline.run_predict(b, o)
@@ -479,32 +562,29 @@ def main():
         e[3].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    res = {"wall": t1 - t0, "chained": chained,
+           "predict": [e[0].elapsed_time(e[1]) for e in ev], "route": [e[1].elapsed_time(e[2]) for e in ev],
+           "prioritize": [e[2].elapsed_time(e[3]) for e in ev],
+           "pred": o.pred_len.cpu().numpy(), "kv": o.kv_bytes.cpu().numpy()}
+    del b, o
+    torch.cuda.empty_cache()
+    return res
 
-    wall = t1 - t0
-    d_predict = [e[0].elapsed_time(e[1]) for e in ev]
-    d_route = [e[1].elapsed_time(e[2]) for e in ev]
-    d_prio = [e[2].elapsed_time(e[3]) for e in ev]
-    ms_predict = float(np.mean(d_predict))
-    ms_route = float(np.mean(d_route))
-    ms_prio = float(np.mean(d_prio))
 
-    n = wl.n
+def step_record(wl, step, steps: int):
+    """The measured figures of one timed run: throughput, per-phase event times, the predictor's
+    MFMA roofline, route and prioritize bytes."""
+    from paper_2606_12950_amd import workload as W
+    spec, n = wl.spec, wl.n
+    ms_predict = float(np.mean(step["predict"]))
+    ms_route = float(np.mean(step["route"]))
+    ms_prio = float(np.mean(step["prioritize"]))
     flop = mlp_flop_per_stage(spec.dims) * n
     peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = flop / (ms_predict * 1e-3) / 1e12
     line = {
-        "metric": METRIC,
-        "value": n * K / wall,
-        "unit": "stages/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": wall / K * 1e3,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": spec.dtype,
-        "data": "synthetic",
+        "stages_per_s": n * steps / step["wall"],
+        "ms_per_step": step["wall"] / steps * 1e3,
         "config": {
             "workload": f"{spec.name}: {W.DESCRIPTIONS[spec.name]}",
             "n_stages": n, "n_workflows": wl.n_workflows, "n_nodes": spec.n_nodes,
@@ -518,26 +598,27 @@ def main():
             "flop_per_launch": flop, "avg_ms": round(ms_predict, 4),
         },
         "step_ms": {"predict": round(ms_predict, 4), "route": round(ms_route, 4)},
-        "phase_ms": {"predict": percentiles(d_predict), "route": percentiles(d_route)},
+        "phase_ms": {"predict": percentiles(step["predict"]), "route": percentiles(step["route"])},
     }
     rb = route_bytes(n, spec.n_nodes, spec.k)
     line["route"] = {
         "algorithm": "sorted walk" if spec.n_nodes <= 8192 and n >= 4 * spec.n_models else "scan",
         "stages_per_s": n / (ms_route * 1e-3), "algorithmic_bytes": rb,
-        "achieved_gbs": round(rb / (ms_route * 1e-3) / 1e9, 2), "hbm_frac": round(rb / (ms_route * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-        "pairs_per_s": n * spec.n_nodes / (ms_route * 1e-3),
+        "achieved_gbs": round(rb / (ms_route * 1e-3) / 1e9, 2),
+        "hbm_frac": round(rb / (ms_route * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
     }
-    if chained:
+    if step["chained"]:
         pb = prioritize_bytes(n, wl.n_workflows)
         line["step_ms"]["prioritize"] = round(ms_prio, 4)
-        line["phase_ms"]["prioritize"] = percentiles(d_prio)
+        line["phase_ms"]["prioritize"] = percentiles(step["prioritize"])
         line["prioritize"] = {
             "workflows_per_s": wl.n_workflows / (ms_prio * 1e-3), "algorithmic_bytes": pb,
-            "achieved_gbs": round(pb / (ms_prio * 1e-3) / 1e9, 2), "hbm_frac": round(pb / (ms_prio * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "achieved_gbs": round(pb / (ms_prio * 1e-3) / 1e9, 2),
+            "hbm_frac": round(pb / (ms_prio * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_workflows)
-    print(json.dumps(line), flush=True)
+    else:
+        line["prioritize"] = None
+    return line
 
 
 if __name__ == "__main__":

@@ -335,13 +335,21 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const lds_uchar*)(p);
 }
+// kStream marks the load non-temporal (nt): data read once (features, per-stage inputs) is
+// then a candidate for early eviction and does not push the weights, which every tile re-reads,
+// out of the L2 cache.
+template <bool kStream = false>
 __device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t soff, uint32_t lds_base,
                                       int lds_off) {
-  asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
-               ::"s"(lds_base), "i"(lds_off), "v"(voff), "s"(rsrc), "s"(soff) : "m0", "scc");
+  if constexpr (kStream)
+    asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen nt lds"
+                 ::"s"(lds_base), "i"(lds_off), "v"(voff), "s"(rsrc), "s"(soff) : "m0", "scc");
+  else
+    asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
+                 ::"s"(lds_base), "i"(lds_off), "v"(voff), "s"(rsrc), "s"(soff) : "m0", "scc");
 }
 __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen nt lds"
                ::"s"(lds_base), "v"(voff), "s"(rsrc) : "m0");
 }
 
@@ -487,9 +495,9 @@ void mlp3_bf16_kernel(
 #pragma unroll
     for (int q = 0; q < kDmaPerChunk; ++q) {
       if constexpr (G == 1)
-        dma16(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
+        dma16<true>(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
       else   // rows 8i .. 8i+7, i = wave + 4q, of K-slice j
-        dma16(rs, voffk, (uint32_t)(8 * (wave + 4 * q) * D * 2 + 128 * j), base, q * kWaves * 1024);
+        dma16<true>(rs, voffk, (uint32_t)(8 * (wave + 4 * q) * D * 2 + 128 * j), base, q * kWaves * 1024);
     }
     const int piece = 4 * j + wave;
     if (piece < kMeta * kPiecesPerInput) {
