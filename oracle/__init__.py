@@ -14,6 +14,11 @@ Parity status of each function (what pins it, see tests/test_oracle_pins.py):
                gives exactly 0, an identity table leaves the sigmoid unchanged, the table is
                numpy's interp, role fallback to the shared head, clamps at 0 and max_len, Eq. 3,
                and the trunk agrees with predict's on the same network.
+  predict_role_lengths - pinned (tests/test_oracle_role_pins.py): zero-weight regressors give
+               expm1 of the bias plus the tool term, in closed form; a regressor equal to a bins
+               network recovers that network's output 0 through the pinned predict (two-bin
+               softmax identity); roles without a regressor keep their inputs bit for bit; the
+               stacking offset of each regressor's layers; clamps at 0 and max_len; Eq. 3.
   route      - pinned: brute force via numpy lexsort on tiny inputs, invariants (feasible,
                sorted, nothing better left out), degenerate cases, node-permutation
                equivariance.
@@ -77,6 +82,9 @@ def _load():
     lib.oracle_predict_two_phase.argtypes = [i32, P, i32, P, P, i32, P, P, i32, P, P, ctypes.c_float, i64, P,
                                              P, P, P, P, P, i32, P, P, P, i32]
     lib.oracle_predict_two_phase.restype = ctypes.c_int
+    lib.oracle_predict_role_lengths.argtypes = [i32, P, i32, i32, P, P, i32, P, P, ctypes.c_float, i64, P, P, P,
+                                                P, P, P, i32, P, P, i32]
+    lib.oracle_predict_role_lengths.restype = ctypes.c_int
     lib.oracle_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, P, f64, i32, P, P, i32]
     lib.oracle_route.restype = ctypes.c_int
     lib.oracle_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P,
@@ -189,6 +197,46 @@ def predict_two_phase(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequ
     if st != 0:
         raise RuntimeError(f"oracle_predict_two_phase failed with status {st}")
     return pt, pred, kv
+
+
+def predict_role_lengths(x: np.ndarray, weights: Sequence[np.ndarray], biases: Sequence[np.ndarray],
+                         role_group, tool_coef, max_len: float, prompt_len, model_id, role_id, p_tool,
+                         kv_bytes_per_token, dtype: str, pred_len, kv_bytes, n_threads: int = 0):
+    """Per-role regressors: ``weights[l]`` [G][out][in] and ``biases[l]`` [G][out] stack the
+    layers of the G regressor networks; ``role_group`` [n_roles] maps a role to its regressor
+    (-1: none); ``p_tool`` is the first phase's calibrated tool probability. Returns copies of
+    (pred_len float32 [N], kv_bytes float64 [N]) with the stages of roles that have a regressor
+    predicted by it and every other stage as given."""
+    lib = _load()
+    dt = 0 if dtype == "f32" else 1
+    store = np.float32 if dt == 0 else np.uint16
+    x = _c(x, store)
+    n = x.shape[0]
+    ws = [_c(w, store) for w in weights]
+    bs = [_c(b, np.float32) for b in biases]
+    L = len(ws)
+    G = ws[0].shape[0]
+    dims = np.array([x.shape[1]] + [w.shape[1] for w in ws], dtype=np.int32)
+    for l, w in enumerate(ws):
+        assert w.shape == (G, dims[l + 1], dims[l]), "weight shapes must chain [G][out][in]"
+        assert bs[l].shape == (G, dims[l + 1])
+    wptr = (ctypes.c_void_p * L)(*[w.ctypes.data for w in ws])
+    bptr = (ctypes.c_void_p * L)(*[b.ctypes.data for b in bs])
+    rg, tc = _c(role_group, np.int32), _c(tool_coef, np.float32)
+    pl, mi, ri = _c(prompt_len, np.int32), _c(model_id, np.int32), _c(role_id, np.int32)
+    pt = _c(p_tool, np.float32)
+    alpha = _c(kv_bytes_per_token, np.float32)
+    pred = np.array(pred_len, np.float32, copy=True)
+    kv = np.array(kv_bytes, np.float64, copy=True)
+    assert tc.shape == (G,) and pt.shape == pred.shape == kv.shape == (n,)
+    st = lib.oracle_predict_role_lengths(L, _ptr(dims), dt, G, ctypes.cast(wptr, ctypes.c_void_p),
+                                         ctypes.cast(bptr, ctypes.c_void_p), rg.shape[0], _ptr(rg), _ptr(tc),
+                                         float(max_len), n, _ptr(x), _ptr(pl), _ptr(mi), _ptr(ri), _ptr(pt),
+                                         _ptr(alpha), alpha.shape[0], _ptr(pred), _ptr(kv),
+                                         n_threads or max_threads())
+    if st != 0:
+        raise RuntimeError(f"oracle_predict_role_lengths failed with status {st}")
+    return pred, kv
 
 
 def route(model_id, pred_len, kv_bytes, decode_s_per_token, free_bytes, queue_s, cold_s,

@@ -30,8 +30,12 @@
  *                shortfall (Alg. 2), any number of engines.
  *   two-phase  : the same network read as heads (Sec. III-B): a tool-intent logit through a
  *                sigmoid and an isotonic calibration table (Eq. 1), 0 without tools; the
- *                stage's role regressor (or the shared one) on log(1 + L), fed the calibrated
+ *                stage's role head (or the shared one) on log(1 + L), fed the calibrated
  *                probability, inverted with expm1; then Eq. 3.
+ *   role regr. : per-role regressors with weights of their own (Sec. III-B): the stage's role
+ *                network, output 0 on log(1 + L) plus the calibrated tool probability's term,
+ *                inverted with expm1; then Eq. 3; stages of roles without one keep the shared
+ *                model's prediction.
  *   quantiles  : the window bounds, as exact order statistics of a sample.
  *   prioritize : per-stage latency quantised to integer microseconds, suffix sums along each
  *                workflow chain (Eq. 7 with the future term taken as the sum of the later
@@ -240,6 +244,70 @@ int oracle_predict_two_phase(int32_t n_layers, const int32_t* dims, int32_t dtyp
         pred_len[i] = pred;
         int32_t m = model_id[i];
         double alpha = (m >= 0 && m < n_models) ? (double)kv_bytes_per_token[m] : NAN;
+        kv_bytes[i] = ((double)prompt_len[i] + (double)pred) * alpha;
+      }
+    }
+    free(h);
+    free(z);
+  }
+  return status;
+}
+
+/* Per-role length regressors (Sec. III-B: a regressor per role where the role has training
+ * data, the shared global model otherwise). Regressor g is a network of its own, the shape of
+ * the predictor, with its weights stored after those of regressors 0 .. g-1 (layer l of
+ * regressor g at weight[l] + g * dims[l+1] * dims[l], bias[l] + g * dims[l+1]). A stage of role
+ * r with 0 <= role_group[r] < n_groups (r in 0 .. n_roles-1) is predicted by that regressor:
+ *   y      = z_0 + tool_coef[g] * p_tool      (output 0 regresses log(1 + L); the calibrated tool
+ *                                               probability of the first phase is an input)
+ *   L      = min(expm1(max(y, 0)), max_len)
+ *   R_kv   = alpha(M) * (P + L)                (Eq. 3)
+ * Every other stage keeps pred_len and kv_bytes as they came in (the shared model's). */
+int oracle_predict_role_lengths(int32_t n_layers, const int32_t* dims, int32_t dtype, int32_t n_groups,
+                                const void* const* weight, const float* const* bias, int32_t n_roles,
+                                const int32_t* role_group, const float* tool_coef, float max_len, int64_t n,
+                                const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                const int32_t* role_id, const float* p_tool, const float* kv_bytes_per_token,
+                                int32_t n_models, float* pred_len, double* kv_bytes, int32_t n_threads) {
+  if (n_layers < 1 || n_layers > 4 || (dtype != 0 && dtype != 1) || n < 0 || n_models < 1 || n_groups < 1 ||
+      n_roles < 0)
+    return ORACLE_BAD_ARG;
+  int32_t widest = 0;
+  for (int l = 0; l <= n_layers; ++l) {
+    if (dims[l] < 1) return ORACLE_BAD_ARG;
+    if (dims[l] > widest) widest = dims[l];
+  }
+  const size_t esize = dtype == 0 ? sizeof(float) : sizeof(uint16_t);
+  int status = ORACLE_OK;
+  if (n_threads < 1) n_threads = 1;
+
+#pragma omp parallel num_threads(n_threads)
+  {
+    double* h = (double*)malloc(sizeof(double) * (size_t)widest);
+    double* z = (double*)malloc(sizeof(double) * (size_t)widest);
+    if (!h || !z) {
+#pragma omp atomic write
+      status = ORACLE_NO_MEM;
+    } else {
+#pragma omp for schedule(static)
+      for (int64_t i = 0; i < n; ++i) {
+        const int32_t r = role_id[i];
+        const int32_t g = (r >= 0 && r < n_roles) ? role_group[r] : -1;
+        if (g < 0 || g >= n_groups) continue;             /* the shared model's prediction stands */
+        const void* wg[4];
+        const float* bg[4];
+        for (int l = 0; l < n_layers; ++l) {               /* regressor g's own layers */
+          wg[l] = (const char*)weight[l] + (size_t)g * (size_t)dims[l + 1] * (size_t)dims[l] * esize;
+          bg[l] = bias[l] + (size_t)g * (size_t)dims[l + 1];
+        }
+        mlp_forward(i, n_layers, dims, dtype, wg, bg, x, h, z);
+        const double y = z[0] + (double)tool_coef[g] * (double)p_tool[i];
+        double L = expm1(y > 0.0 ? y : 0.0);
+        if (L > (double)max_len) L = (double)max_len;
+        const float pred = (float)L;
+        pred_len[i] = pred;
+        const int32_t m = model_id[i];
+        const double alpha = (m >= 0 && m < n_models) ? (double)kv_bytes_per_token[m] : NAN;
         kv_bytes[i] = ((double)prompt_len[i] + (double)pred) * alpha;
       }
     }

@@ -528,6 +528,46 @@ def two_phase_inputs(wl: Workload, n_knots: int = 16, max_len: float = 32768.0) 
                           max_len=max_len, tool_avail=tools)
 
 
+ROLE_STREAMS = ("w1", "w2", "w3", "bias", "coef")
+
+
+@dataclass
+class RoleRegressorInputs:
+    """Stand-in weights of per-role length regressors: G networks of the workload predictor's
+    shape, stacked [G][out][in], and the role -> regressor map."""
+    weights: list                 # per layer [G][out][in], float32 or uint16 (bf16 bits)
+    biases: list                  # per layer [G][out] float32
+    role_group: np.ndarray        # [n_roles] int32, -1 = the shared model
+    tool_coef: np.ndarray         # [G] float32
+    max_len: float
+
+
+def role_regressor_inputs(wl: Workload, max_len: float = 32768.0) -> RoleRegressorInputs:
+    """Per-role regressors for ``wl`` (seeded by its spec's seed): roles 0, 1 and 2 of the five
+    have regressors of their own (0, 1, 2); roles 3 and 4 keep the shared model. Each regressor
+    is a network of the predictor's shape with N(0, 1/fan_in) weights and zero hidden biases;
+    output 0 regresses log(1 + L) (bias U[4.5, 6.5], e^4.5 - e^6.5 tokens before the feature
+    terms) and the other outputs are zero. Tool coefficients U[-2.5, -1.5]: tool-invoking stages
+    produce short structured outputs (Sec. III-B)."""
+    children = np.random.SeedSequence([wl.spec.seed, 0x201E5]).spawn(len(ROLE_STREAMS))
+    r = {name: np.random.Generator(np.random.PCG64(c)) for name, c in zip(ROLE_STREAMS, children)}
+    G = 3
+    dims = wl.spec.dims
+    ws, bs = [], []
+    for l, key in enumerate(("w1", "w2", "w3")):
+        din, dout = dims[l], dims[l + 1]
+        w = r[key].normal(0.0, din ** -0.5, size=(G, dout, din)).astype(np.float32)
+        b = np.zeros((G, dout), np.float32)
+        if l == len(dims) - 2:
+            w[:, 1:, :] = 0.0
+            b[:, 0] = r["bias"].uniform(4.5, 6.5, G)
+        ws.append(w if wl.spec.dtype == "f32" else f32_to_bf16_bits(w))
+        bs.append(b)
+    coef = r["coef"].uniform(-2.5, -1.5, G).astype(np.float32)
+    return RoleRegressorInputs(weights=ws, biases=bs, role_group=np.array([0, 1, 2, -1, -1], np.int32),
+                               tool_coef=coef, max_len=max_len)
+
+
 def workload(name: str, with_x: bool = True, **overrides) -> Workload:
     """Named workload, optionally with fields of its spec replaced (e.g. ``n_stages=5000``)."""
     spec = SPECS[name]
