@@ -335,8 +335,10 @@ def route_fitness_bench(name: str, steps: int, warmup: int, plans: bool = False,
 
 
 def two_phase_bench(name: str, steps: int, warmup: int):
-    """The two-phase predictor (calibrated tool intent, per-role log(1 + L) heads) and the bins
-    predictor on the same network and batch, interleaved; MFMA roofline of each. One JSON line."""
+    """The two-phase predictor (calibrated tool intent, per-role log(1 + L) heads), the per-role
+    regressors with weights of their own (grouped GEMM over the stages bucketed by role), and the
+    bins predictor on the same network and batch, interleaved; MFMA roofline of each. One JSON
+    line."""
     import torch
     from paper_2606_12950_amd import _native, pipeline
     from paper_2606_12950_amd import workload as W
@@ -359,18 +361,37 @@ def two_phase_bench(name: str, steps: int, warmup: int):
     two = lambda: _native.predict_two_phase(b.x, ws, bs, *tabs, tp.max_len, b.prompt_len, b.model_id, role, tools,
                                             b.kv_bytes_per_token, out=out)
     bins = lambda: pipeline.run_predict(b, o)
+    # the per-role regressors (second phase, grouped GEMM) on the two-phase outputs; they rewrite
+    # the lengths of their stages in place, which every call does identically
+    rr = W.role_regressor_inputs(wl)
+    rw, rb = [t(a) for a in rr.weights], [t(a) for a in rr.biases]
+    rg, rc = t(rr.role_group), t(rr.tool_coef)
+    rws = torch.empty(max(256, _native.load().maestro_role_lengths_workspace(n, rr.tool_coef.size)), dtype=torch.uint8,
+                      device="cuda")
+    two()
+    torch.cuda.synchronize()
+    roles = lambda: _native.predict_role_lengths(b.x, rw, rb, rg, rc, rr.max_len, b.prompt_len, b.model_id, role,
+                                                 out[0], b.kv_bytes_per_token, out[1], out[2], workspace=rws)
     d2 = _time_events(two, steps, warmup)
     d1 = _time_events(bins, steps, warmup)
+    dr = _time_events(roles, steps, warmup)
     d2 += _time_events(two, steps, 0)
     d1 += _time_events(bins, steps, 0)
+    dr += _time_events(roles, steps, 0)
     flop = mlp_flop_per_stage(wl.spec.dims) * n
-    res = {"workload": name, "n_stages": n, "predictor": "-".join(map(str, wl.spec.dims)), "flop_per_launch": flop}
-    for key, d in (("two_phase", d2), ("bins", d1)):
+    g = np.where((wl.role >= 0) & (wl.role < rr.role_group.size), rr.role_group[np.clip(wl.role, 0, rr.role_group.size - 1)], -1)
+    n_roles = int(((g >= 0) & (g < rr.tool_coef.size)).sum())
+    flop_roles = mlp_flop_per_stage(wl.spec.dims) * n_roles
+    res = {"workload": name, "n_stages": n, "predictor": "-".join(map(str, wl.spec.dims)), "flop_per_launch": flop,
+           "role_stages": n_roles, "role_flop_per_launch": flop_roles}
+    for key, d, f in (("two_phase", d2, flop), ("bins", d1, flop), ("role_regressors", dr, flop_roles)):
         ms = float(np.mean(d))
-        res[key] = {"ms": round(ms, 4), "phase_ms": percentiles(d), "stages_per_s": n / (ms * 1e-3),
-                    "roofline": {"bound": "mfma", "achieved": round(flop / (ms * 1e-3) / 1e12, 2),
+        res[key] = {"ms": round(ms, 4), "phase_ms": percentiles(d), "stages_per_s": (n_roles if f == flop_roles else n) / (ms * 1e-3),
+                    "roofline": {"bound": "mfma", "achieved": round(f / (ms * 1e-3) / 1e12, 2),
                                  "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                                 "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+                                 "frac": round(f / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+    res["role_regressors"]["note"] = ("bucketing (count, plan, scatter) and the grouped GEMM over the stages of "
+                                      "roles with a regressor; FLOP counted for those stages only")
     res["mean_p_tool"] = float(out[0].mean().item())
     res["mean_pred_len"] = float(out[1].mean().item())
     import oracle

@@ -7,7 +7,9 @@
  *                      regressor), and its KV demand R_kv = alpha(M) * (P + L) (Eq. 3).
  *   maestro_predict_two_phase  the paper's two-phase form of the same prediction (Sec. III-B):
  *                      a calibrated tool-intent probability (Eq. 1), then the stage's role
- *                      regressor on log(1 + L), fed that probability.
+ *                      head or the shared model on log(1 + L), fed that probability.
+ *   maestro_predict_role_lengths  the per-role regressors with weights of their own, as one
+ *                      grouped GEMM over the stages bucketed by role (Sec. III-B).
  *   maestro_route      cross-cluster routing (Sec. III-D, Alg. 3): drop nodes whose free KV
  *                      headroom cannot admit R_need = (1 + rho) * R_kv, score the rest by
  *                      expected completion latency T_q + T_act + t_dec(M) * L (Eq. 6 and the
@@ -167,6 +169,53 @@ MAESTRO_API maestro_status maestro_predict_two_phase(const maestro_predictor* p,
                              const int32_t* model_id, const int32_t* role_id, const int32_t* tool_avail,
                              const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
                              float* pred_len, double* kv_bytes, void* stream);
+
+/* Per-role length regressors (Sec. III-B: a regressor of its own for each role with training
+ * data, the shared global model for the others). Regressor g (0 <= g < n_regressors) is a
+ * network of the predictor's shape with weights of its own; its output 0 regresses log(1 + L).
+ *   n_regressors     1 .. MAESTRO_MAX_ROLE_REGRESSORS
+ *   n_roles          0 .. 64 entries of role_regressor
+ *   role_regressor   [n_roles] int32 (device; may be NULL when n_roles = 0): the regressor of
+ *                    each role; entries outside 0 .. n_regressors-1, and roles outside
+ *                    0 .. n_roles-1, mean none (the shared model's prediction stands)
+ *   tool_coef        [n_regressors] float32 (device): weight of the tool probability
+ *   max_len          upper clamp of the predicted length (tokens), finite and > 0 */
+#define MAESTRO_MAX_ROLE_REGRESSORS 16
+typedef struct maestro_role_regressors {
+  int32_t n_regressors;
+  int32_t n_roles;
+  const int32_t* role_regressor;
+  const float* tool_coef;
+  float max_len;
+} maestro_role_regressors;
+
+/* The second phase's per-role regressors over n stages (Sec. III-B; Eq. 3), after
+ * maestro_predict_two_phase has produced the calibrated tool probability and the shared model's
+ * prediction of every stage. For each stage whose role has a regressor g:
+ *   z      = regressor g's network on the stage's features (float32 outputs)
+ *   L      = min(expm1(max(z_0 + tool_coef[g] * p_tool, 0)), max_len)
+ *   R_kv   = ((double)P + (double)L) * (double)alpha(M)                    (Eq. 3)
+ * written to pred_len and kv_bytes; every other stage's entries are left untouched.
+ *   p                  the regressors' shape and weights: n_layers = 3, dtype MAESTRO_BF16, dims
+ *                      256 -> 512 -> 512 -> 64 or 256 -> 1024 -> 1024 -> 64; weight[l] points at
+ *                      the n_regressors networks' layer l stacked [g][dims[l+1]][dims[l]], bias[l]
+ *                      at [g][dims[l+1]] (bin_centre unused)
+ *   x, prompt_len, model_id, kv_bytes_per_token, n_models   as maestro_predict
+ *   role_id            [n] int32: the stage's agent role
+ *   p_tool             [n] float32: calibrated tool probability (from maestro_predict_two_phase)
+ *   pred_len, kv_bytes [n] float32 / float64, in and out
+ * The stages are bucketed by regressor on the device (a stable counting sort) and predicted as one
+ * grouped GEMM: tiles of 128 stages of one regressor, feature rows gathered. Workspace:
+ * maestro_role_lengths_workspace(n, n_regressors) bytes. Errors: INVALID_ARG for a NULL or
+ * misaligned array, n < 0, n_models outside 1..64, n_regressors outside 1..16, n_roles outside
+ * 0..64, max_len not finite and positive; UNSUPPORTED for another shape or n > 2^22 (the feature
+ * rows are addressed with 31-bit offsets); WORKSPACE for a short workspace. */
+MAESTRO_API maestro_status maestro_predict_role_lengths(const maestro_predictor* p, const maestro_role_regressors* r,
+                             int64_t n, const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                             const int32_t* role_id, const float* p_tool, const float* kv_bytes_per_token,
+                             int32_t n_models, float* pred_len, double* kv_bytes, void* workspace,
+                             size_t workspace_bytes, void* stream);
+MAESTRO_API size_t maestro_role_lengths_workspace(int64_t n, int32_t n_regressors);
 
 /* Routing of n stages over n_nodes nodes (Sec. III-D; Alg. 3; Eq. 6; Eq. 2 decode term).
  * Per stage i with model m = model_id[i]:

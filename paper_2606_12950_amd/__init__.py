@@ -5,13 +5,13 @@ include/maestro.h); this package is its thin Python binding plus the seeded work
 generator. PyTorch supplies device memory and streams only.
 """
 from ._native import (LIBRARY_PATH, MaestroError, Predictor, TwoPhase, load, make_predictor, predict,
-                      predict_two_phase,
+                      predict_two_phase, predict_role_lengths,
                       activation_latency, adaptive_rho, degradation_plans, prioritize, prioritize_workspace_bytes, quantiles, route,
                       route_fitness)
 from .pipeline import DeviceBatch, StepOutputs, run_step, to_device
 
 __all__ = ["LIBRARY_PATH", "MaestroError", "Predictor", "TwoPhase", "load", "make_predictor", "predict",
-           "predict_two_phase", "activation_latency", "adaptive_rho", "degradation_plans",
+           "predict_two_phase", "predict_role_lengths", "activation_latency", "adaptive_rho", "degradation_plans",
            "prioritize", "prioritize_workspace_bytes", "quantiles", "route", "route_fitness",
            "DeviceBatch", "StepOutputs",
            "run_step", "to_device"]

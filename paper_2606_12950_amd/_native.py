@@ -24,7 +24,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_tiered", "maestro_route_ex", "maestro_route_fitness",
            "maestro_degradation_plans", "maestro_activation_latency", "maestro_adaptive_rho", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string",
-           "maestro_prioritize_noalloc")
+           "maestro_prioritize_noalloc", "maestro_predict_role_lengths", "maestro_role_lengths_workspace")
 
 PRIORITIZE_NOALLOC_MAX_WORKFLOWS = 1 << 20
 
@@ -56,6 +56,12 @@ class Predictor(ctypes.Structure):
                 ("bias", ctypes.c_void_p * 4), ("bin_centre", ctypes.c_void_p)]
 
 
+class RoleRegressors(ctypes.Structure):
+    """Mirror of ``maestro_role_regressors``."""
+    _fields_ = [("n_regressors", ctypes.c_int32), ("n_roles", ctypes.c_int32), ("role_regressor", ctypes.c_void_p),
+                ("tool_coef", ctypes.c_void_p), ("max_len", ctypes.c_float)]
+
+
 class TwoPhase(ctypes.Structure):
     """Mirror of ``maestro_two_phase``."""
     _fields_ = [("n_roles", ctypes.c_int32), ("n_knots", ctypes.c_int32), ("role_head", ctypes.c_void_p),
@@ -79,6 +85,11 @@ def load():
     lib.maestro_predict.argtypes = [ctypes.POINTER(Predictor), i64, P, P, P, P, i32, P, P, P, sz, P]
     lib.maestro_predict_two_phase.argtypes = [ctypes.POINTER(Predictor), ctypes.POINTER(TwoPhase), i64, P, P, P,
                                               P, P, P, i32, P, P, P, P]
+    lib.maestro_predict_role_lengths.argtypes = [ctypes.POINTER(Predictor), ctypes.POINTER(RoleRegressors), i64, P,
+                                                 P, P, P, P, P, i32, P, P, P, sz, P]
+    lib.maestro_predict_role_lengths.restype = ctypes.c_int
+    lib.maestro_role_lengths_workspace.argtypes = [i64, i32]
+    lib.maestro_role_lengths_workspace.restype = sz
     lib.maestro_route.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, P, P, P, sz, P]
     lib.maestro_route_ex.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, P, f64, i32, i32, P, P, P, sz, P]
     lib.maestro_route_fitness.argtypes = [i64, P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P, P, P,
@@ -251,6 +262,67 @@ def predict_two_phase(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: 
                                        kv_bytes_per_token.shape[0], _ptr(pt), _ptr(pred), _ptr(kv), _stream(stream))
     _check("maestro_predict_two_phase", st)
     return pt, pred, kv
+
+
+def predict_role_lengths(x: torch.Tensor, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor],
+                         role_regressor: torch.Tensor, tool_coef: torch.Tensor, max_len: float,
+                         prompt_len: torch.Tensor, model_id: torch.Tensor, role_id: torch.Tensor, p_tool: torch.Tensor,
+                         kv_bytes_per_token: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,
+                         workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_predict_role_lengths: the per-role regressors over the stages whose role has one,
+    written into ``pred_len`` / ``kv_bytes`` in place (returned). ``weights[l]`` [G][out][in] and
+    ``biases[l]`` [G][out] stack the G regressors' layers; ``role_regressor`` [n_roles] int32 maps
+    a role to its regressor (-1: none); ``p_tool`` is the first phase's calibrated probability."""
+    lib = load()
+    L = len(weights)
+    if not 1 <= L <= 4 or len(biases) != L:
+        raise ValueError("1..4 Linear layers with one bias each")
+    dt = weights[0].dtype
+    G = weights[0].shape[0]
+    p = Predictor()
+    p.n_layers = L
+    p.dtype = MAESTRO_F32 if dt == torch.float32 else MAESTRO_BF16
+    p.dims[0] = weights[0].shape[2]
+    for l, (w, b) in enumerate(zip(weights, biases)):
+        _dev(w, f"weight[{l}]", dt)
+        _dev(b, f"bias[{l}]", torch.float32)
+        if w.dim() != 3 or w.shape[0] != G or w.shape[2] != p.dims[l] or tuple(b.shape) != (G, w.shape[1]):
+            raise ValueError(f"layer {l}: weight must be [G][out][in] chaining the previous layer, bias [G][out]")
+        p.dims[l + 1] = w.shape[1]
+        p.weight[l] = w.data_ptr()
+        p.bias[l] = b.data_ptr()
+    _dev(x, "x", dt)
+    n = x.shape[0]
+    if x.dim() != 2 or x.shape[1] != p.dims[0]:
+        raise ValueError("x must be [N][D]")
+    for t, name in ((prompt_len, "prompt_len"), (model_id, "model_id"), (role_id, "role_id"),
+                    (role_regressor, "role_regressor")):
+        _dev(t, name, torch.int32)
+    for t, name in ((kv_bytes_per_token, "kv_bytes_per_token"), (tool_coef, "tool_coef"), (p_tool, "p_tool")):
+        _dev(t, name, torch.float32)
+    for t, name in ((prompt_len, "prompt_len"), (model_id, "model_id"), (role_id, "role_id"), (p_tool, "p_tool")):
+        _shape(t, name, (n,))
+    _shape(_dev(pred_len, "pred_len", torch.float32), "pred_len", (n,))
+    _shape(_dev(kv_bytes, "kv_bytes", torch.float64), "kv_bytes", (n,))
+    _shape(tool_coef, "tool_coef", (G,))
+    if role_regressor.dim() != 1 or kv_bytes_per_token.dim() != 1:
+        raise ValueError("role_regressor and kv_bytes_per_token must be one-dimensional")
+    r = RoleRegressors()
+    r.n_regressors = G
+    r.n_roles = role_regressor.shape[0]
+    r.role_regressor = role_regressor.data_ptr() if role_regressor.numel() else None
+    r.tool_coef = tool_coef.data_ptr()
+    r.max_len = float(max_len)
+    need = lib.maestro_role_lengths_workspace(n, G)
+    _workspace(workspace)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+    st = lib.maestro_predict_role_lengths(ctypes.byref(p), ctypes.byref(r), n, _ptr(x), _ptr(prompt_len),
+                                          _ptr(model_id), _ptr(role_id), _ptr(p_tool), _ptr(kv_bytes_per_token),
+                                          kv_bytes_per_token.shape[0], _ptr(pred_len), _ptr(kv_bytes),
+                                          _ptr(workspace), workspace.numel(), _stream(stream))
+    _check("maestro_predict_role_lengths", st)
+    return pred_len, kv_bytes
 
 
 def route(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,

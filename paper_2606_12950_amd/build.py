@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmaestro.so")
-SOURCES = ("api.hip", "predict.hip", "route.hip", "fitness.hip", "prioritize.hip")
+SOURCES = ("api.hip", "predict.hip", "roles.hip", "route.hip", "fitness.hip", "prioritize.hip")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

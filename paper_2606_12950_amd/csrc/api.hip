@@ -102,6 +102,45 @@ maestro_status maestro_predict_two_phase(const maestro_predictor* p, const maest
                                            as_stream(stream));
 }
 
+size_t maestro_role_lengths_workspace(int64_t n, int32_t n_regressors) {
+  if (n < 0 || n_regressors < 1 || n_regressors > MAESTRO_MAX_ROLE_REGRESSORS) return 0;
+  return maestro::role_lengths_workspace_bytes(n, n_regressors);
+}
+
+maestro_status maestro_predict_role_lengths(const maestro_predictor* p, const maestro_role_regressors* r, int64_t n,
+                                            const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                            const int32_t* role_id, const float* p_tool,
+                                            const float* kv_bytes_per_token, int32_t n_models, float* pred_len,
+                                            double* kv_bytes, void* workspace, size_t workspace_bytes,
+                                            void* stream) {
+  if (!p || !r || n < 0 || n_models < 1 || n_models > 64) return MAESTRO_ERR_INVALID_ARG;
+  if (p->n_layers < 1 || p->n_layers > 4) return MAESTRO_ERR_INVALID_ARG;
+  if (p->dtype != MAESTRO_F32 && p->dtype != MAESTRO_BF16) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l <= p->n_layers; ++l)
+    if (p->dims[l] < 1) return MAESTRO_ERR_INVALID_ARG;
+  for (int l = 0; l < p->n_layers; ++l)
+    if (!p->weight[l] || !p->bias[l] || !aligned(p->weight[l], 16) || !aligned(p->bias[l], 16))
+      return MAESTRO_ERR_INVALID_ARG;
+  if (r->n_regressors < 1 || r->n_regressors > MAESTRO_MAX_ROLE_REGRESSORS || r->n_roles < 0 || r->n_roles > 64)
+    return MAESTRO_ERR_INVALID_ARG;
+  if (!(r->max_len > 0.0f) || !isfinite(r->max_len)) return MAESTRO_ERR_INVALID_ARG;
+  if (r->n_roles > 0 && (!r->role_regressor || !aligned(r->role_regressor, 4))) return MAESTRO_ERR_INVALID_ARG;
+  if (!r->tool_coef || !aligned(r->tool_coef, 4)) return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!x || !prompt_len || !model_id || !role_id || !p_tool || !kv_bytes_per_token || !pred_len || !kv_bytes)
+      return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(prompt_len, 4) || !aligned(model_id, 4) || !aligned(role_id, 4) ||
+        !aligned(p_tool, 4) || !aligned(kv_bytes_per_token, 4) || !aligned(pred_len, 4) || !aligned(kv_bytes, 8))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (!maestro::two_phase_shape_supported(*p)) return MAESTRO_ERR_UNSUPPORTED;
+  if (n > ((int64_t)1 << 22)) return MAESTRO_ERR_UNSUPPORTED;
+  const size_t need = maestro::role_lengths_workspace_bytes(n, r->n_regressors);
+  if (workspace_bytes < need || (need > 0 && (!workspace || !aligned(workspace, 256)))) return MAESTRO_ERR_WORKSPACE;
+  return maestro::launch_role_lengths(*p, *r, n, x, prompt_len, model_id, role_id, p_tool, kv_bytes_per_token,
+                                      n_models, pred_len, kv_bytes, workspace, as_stream(stream));
+}
+
 namespace {
 
 // maestro_route_ex and maestro_route_tiered: T_act from (cold_s, resident_mask), or from

@@ -22,6 +22,19 @@ maestro_status launch_predict_two_phase(const maestro_predictor& p, const maestr
                                         const float* kv_bytes_per_token, int32_t n_models, float* p_tool,
                                         float* pred_len, double* kv_bytes, hipStream_t stream);
 
+// Per-role regressors: bucketing by regressor, then the fused predictor as a grouped GEMM.
+maestro_status launch_role_lengths(const maestro_predictor& p, const maestro_role_regressors& r, int64_t n,
+                                   const void* x, const int32_t* prompt_len, const int32_t* model_id,
+                                   const int32_t* role_id, const float* p_tool, const float* kv_bytes_per_token,
+                                   int32_t n_models, float* pred_len, double* kv_bytes, void* workspace,
+                                   hipStream_t stream);
+size_t role_lengths_workspace_bytes(int64_t n, int32_t n_groups);
+maestro_status launch_role_regressors(const maestro_predictor& p, int64_t n, const void* x, const float* coef,
+                                      float max_len, const int32_t* tile_group, const int32_t* perm,
+                                      const int32_t* prompt_p, const int32_t* model_p, const int32_t* p_bits,
+                                      const int32_t* n_tiles, int64_t max_tiles, const float* kv_bytes_per_token,
+                                      int32_t n_models, float* pred_len, double* kv_bytes, hipStream_t stream);
+
 // Routing: feasibility mask, pair scores, lexicographic top-k.
 maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pred_len,
                             const double* kv_bytes, const float* decode_s_per_token,

@@ -181,6 +181,21 @@ __device__ __forceinline__ void two_phase_row(float z0, float zg, int g, const f
   kv_bytes[row] = ((double)prompt + (double)L) * alpha_of(alpha, model, n_models);
 }
 
+// Per-role regressors (Sec. III-B): a stage whose role has a regressor of its own is predicted by
+// that regressor's network; output 0 regresses log(1 + L), fed the first phase's calibrated tool
+// probability p: L = min(expm1(max(z_0 + coef p, 0)), max_len), then Eq. 3. Stages reach the
+// kernel bucketed by regressor (every tile belongs to one), in tile-row order, with their stage
+// index, prompt length, model id and p carried alongside; padding rows have stage -1.
+__device__ __forceinline__ void role_row(float z0, float b0, float coef, float p, float max_len, int32_t stage,
+                                         int32_t prompt, int32_t model, const float* __restrict__ alpha,
+                                         int32_t n_models, float* __restrict__ pred_len,
+                                         double* __restrict__ kv_bytes) {
+  const float y = z0 + b0 + coef * p;
+  const float L = fminf(expm1f(fmaxf(y, 0.0f)), max_len);
+  pred_len[stage] = L;
+  kv_bytes[stage] = ((double)prompt + (double)L) * alpha_of(alpha, model, n_models);
+}
+
 // ---------------------------------------------------------------------------------------------
 // bfloat16, three Linear layers: D -> H1 -> H2 -> B   (D = 256)
 // ---------------------------------------------------------------------------------------------
@@ -353,6 +368,16 @@ __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t 
                ::"s"(lds_base), "v"(voff), "s"(rsrc) : "m0");
 }
 
+// Two consecutive int32 at a wavefront-uniform, 8-byte aligned address, through the scalar data
+// cache and waited for here: a scalar load is counted apart from the vector-memory operations, so
+// fetching it never waits for the LDS-DMA prefetches in flight (a vector load's wait would).
+__device__ __forceinline__ void scalar_load2(const int32_t* p, int32_t& a, int32_t& b) {
+  uint64_t v;
+  asm volatile("s_load_dwordx2 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+  a = (int32_t)(uint32_t)v;
+  b = (int32_t)(uint32_t)(v >> 32);
+}
+
 // Wait until at most N vector-memory operations of this wavefront are outstanding and all of
 // its LDS operations are done (gfx9 s_waitcnt encoding), then the workgroup barrier. The
 // empty asm statements keep the compiler from moving LDS accesses across.
@@ -407,16 +432,26 @@ struct AccGroups {
 // through LDS once per tile, so G = 2 halves the weight traffic and the LDS fragment reads per
 // row. G = 2 needs both groups' layer-1 activations in the 256 accumulation registers, which
 // holds for H1 = 512.
-template <int D, int H1, int H2, int B, int G, bool kTwoPhase>
+//
+// kRoles: the per-role regressors as one grouped GEMM. Tile t belongs to regressor
+// tile_group[t] (bucketed by role_bucket_kernels); its weights are regressor g's layers, stacked
+// after those of regressors 0 .. g-1, and its rows are the stages perm[128 t ...] (feature rows
+// gathered through the permutation; padding rows, stage -1, read as zeros). The tile count is
+// read from device memory (n_tiles_dev). The biases are restaged whenever a workgroup's tile
+// moves to another regressor (tiles of one regressor are contiguous, so rarely).
+template <int D, int H1, int H2, int B, int G, bool kTwoPhase, bool kRoles = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void mlp3_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w1, const uint16_t* __restrict__ w2,
     const uint16_t* __restrict__ w3, const float* __restrict__ b1, const float* __restrict__ b2,
-    const float* __restrict__ b3, const float* __restrict__ centre, int64_t n, int64_t n_tiles,
+    const float* __restrict__ b3, const float* __restrict__ centre, int64_t n, int64_t n_tiles_arg,
     const int32_t* __restrict__ prompt_len, const int32_t* __restrict__ model_id,
     const float* __restrict__ alpha, int32_t n_models, float* __restrict__ pred_len,
-    double* __restrict__ kv_bytes, const TwoPhaseArgs tp) {
+    double* __restrict__ kv_bytes, const TwoPhaseArgs tp, const int32_t* __restrict__ tile_group,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ p_bits, const int32_t* __restrict__ n_tiles_dev,
+    const float* __restrict__ role_coef, float role_max_len) {
   static_assert(D == 256, "feature and layer-1 chunk layouts assume 512-byte rows");
+  static_assert(!kRoles || (!kTwoPhase && G == 1), "role regressors: one row group, output 0 only");
   static_assert(H1 % 512 == 0 && H2 % 32 == 0 && B % 64 == 0, "tile shape");
   static_assert(G == 1 || (G == 2 && H1 == 512), "two row groups need H1 = 512 (256 accumulation registers)");
   constexpr int kTileRows = kWaves * kRowsPerWave * G;
@@ -443,7 +478,7 @@ void mlp3_bf16_kernel(
   __shared__ __attribute__((aligned(16))) float s_c[B];   // bin centres, or the two-phase tool coefficients
   __shared__ __attribute__((aligned(16))) float s_alpha[kMaxModels];
   // [tile parity][prompt, model (, role, tool availability)][row]
-  constexpr int kMeta = kTwoPhase ? 4 : 2;
+  constexpr int kMeta = (kTwoPhase || kRoles) ? 4 : 2;
   __shared__ __attribute__((aligned(16))) int32_t s_meta[2][kMeta][kTileRows];
   constexpr int kTab = kTwoPhase ? 64 : 1;   // two-phase tables: role heads, calibration knots
   __shared__ int32_t s_head[kTab];
@@ -456,9 +491,17 @@ void mlp3_bf16_kernel(
   const int64_t first_tile = blockIdx.x, stride = gridDim.x;
 
   // ---- chunk fetchers, each issuing at least kDmaPerChunk direct loads per wavefront
-  const i32x4 rs_w1 = buffer_rsrc(w1, (uint32_t)(H1 * D * 2));
-  const i32x4 rs_w2 = buffer_rsrc(w2, (uint32_t)(H2 * H1 * 2));
-  const i32x4 rs_w3 = buffer_rsrc(w3, (uint32_t)(B * H2 * 2));
+  // tiles to walk: from the launch, or (role regressors) from the bucketing pass
+  const int64_t n_tiles = kRoles ? (int64_t)n_tiles_dev[0] : n_tiles_arg;
+  // the regressor of tile t (0 past the last tile) and its weights' buffer resources
+  auto group_of = [&](int64_t t) -> int { return (kRoles && t < n_tiles) ? tile_group[t] : 0; };
+  auto rsrc_w1 = [&](int grp) { return buffer_rsrc(w1 + (size_t)grp * (H1 * D), (uint32_t)(H1 * D * 2)); };
+  auto rsrc_w2 = [&](int grp) { return buffer_rsrc(w2 + (size_t)grp * (H2 * H1), (uint32_t)(H2 * H1 * 2)); };
+  auto rsrc_w3 = [&](int grp) { return buffer_rsrc(w3 + (size_t)grp * (B * H2), (uint32_t)(B * H2 * 2)); };
+  int grp_cur = group_of(first_tile);
+  i32x4 rs_w1 = rsrc_w1(grp_cur), rs_w2 = rsrc_w2(grp_cur), rs_w3 = rsrc_w3(grp_cur);
+  i32x4 rs_w1_next = rs_w1;               // W1 of the next tile, whose first chunks this tile prefetches
+  int64_t cur_tile = first_tile;
   const uint32_t voff1 = (uint32_t)(((lane >> 5) * D + (((lane & 31) ^ ((lane >> 5) << 3)) * 8)) * 2);
   const uint32_t voff2 = (uint32_t)(lane * 16);
   const uint32_t voff3 = (uint32_t)(((lane >> 2) * H2 + (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
@@ -489,29 +532,47 @@ void mlp3_bf16_kernel(
   auto fetch_x = [&](int64_t t, int par, int j, const unsigned char* dst) {
     const bool live = t < n_tiles;
     const int64_t row0 = live ? t * kTileRows : 0;
-    const uint32_t rows = live ? (uint32_t)min<int64_t>(kTileRows, n - row0) : 0u;
-    const i32x4 rs = buffer_rsrc(x + row0 * D, rows * (D * 2));
+    const uint32_t rows = live ? (kRoles ? (uint32_t)kTileRows : (uint32_t)min<int64_t>(kTileRows, n - row0)) : 0u;
     const uint32_t base = lds_addr(dst) + wave * 1024;
+    if constexpr (kRoles) {
+      // rows gathered through the permutation: load q brings tile rows rho0 = 64j + 2 wave + 8q
+      // (lanes 0-31) and rho0 + 1 (lanes 32-63); a padding row (stage -1) gets an offset past the
+      // buffer and reads zeros. The feature array spans at most 2^31 bytes.
+      const i32x4 rs = buffer_rsrc(x, (uint32_t)(n * (D * 2)));
 #pragma unroll
-    for (int q = 0; q < kDmaPerChunk; ++q) {
-      if constexpr (G == 1)
-        dma16<true>(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
-      else   // rows 8i .. 8i+7, i = wave + 4q, of K-slice j
-        dma16<true>(rs, voffk, (uint32_t)(8 * (wave + 4 * q) * D * 2 + 128 * j), base, q * kWaves * 1024);
+      for (int q = 0; q < kDmaPerChunk; ++q) {
+        const int rho0 = 64 * j + 2 * wave + 8 * q;
+        int32_t s0 = -1, s1 = -1;
+        if (live) scalar_load2(perm + row0 + rho0, s0, s1);
+        const int32_t st = h ? s1 : s0;
+        const uint32_t unit = (uint32_t)(((lane & 31) ^ ((rho0 + h) & 15)) << 4);
+        const uint32_t voff = st >= 0 ? (uint32_t)st * (uint32_t)(D * 2) + unit : 0x80000000u;
+        dma16<true>(rs, voff, 0u, base, q * kWaves * 1024);
+      }
+    } else {
+      const i32x4 rs = buffer_rsrc(x + row0 * D, rows * (D * 2));
+#pragma unroll
+      for (int q = 0; q < kDmaPerChunk; ++q) {
+        if constexpr (G == 1)
+          dma16<true>(rs, voffx[q & 1] + (uint32_t)((64 * j + 8 * q) * D * 2), 0u, base, q * kWaves * 1024);
+        else   // rows 8i .. 8i+7, i = wave + 4q, of K-slice j
+          dma16<true>(rs, voffk, (uint32_t)(8 * (wave + 4 * q) * D * 2 + 128 * j), base, q * kWaves * 1024);
+      }
     }
     const int piece = 4 * j + wave;
     if (piece < kMeta * kPiecesPerInput) {
       const int a = piece / kPiecesPerInput, rb = piece % kPiecesPerInput;
-      const int32_t* src = a == 0 ? prompt_len : a == 1 ? model_id : a == 2 ? tp.role_id : tp.tool_avail;
+      const int32_t* src = kRoles ? (a == 0 ? prompt_len : a == 1 ? model_id : a == 2 ? p_bits : perm)
+                                  : (a == 0 ? prompt_len : a == 1 ? model_id : a == 2 ? tp.role_id : tp.tool_avail);
       dma4(buffer_rsrc(src + row0, rows * 4), (uint32_t)((64 * rb + lane) * 4),
            lds_addr(&s_meta[par][a][64 * rb]));
     }
   };
   // load q of layer-1 chunk j: rows 64j + 2i (lanes 0-31) and 64j + 2i + 1 (lanes 32-63, units
   // with bit 3 flipped), i = wave + 4q; q = kDmaPerChunk issues nothing
-  auto load_l1 = [&](int j, int q, const unsigned char* dst) {
+  auto load_l1 = [&](int j, int q, const unsigned char* dst, const i32x4& r1) {
     if (q < kDmaPerChunk)
-      dma16(rs_w1, voff1, (uint32_t)((64 * j + 2 * wave + 8 * q) * D * 2), lds_addr(dst) + wave * PAIR,
+      dma16(r1, voff1, (uint32_t)((64 * j + 2 * wave + 8 * q) * D * 2), lds_addr(dst) + wave * PAIR,
             q * kWaves * PAIR);
   };
   // load q of layer-2 chunk (b, part): W2 rows 32b + r, r = wave + 4q; load kDmaPerChunk of the
@@ -533,7 +594,7 @@ void mlp3_bf16_kernel(
     } else {
 #pragma unroll
       for (int q = 0; q <= kDmaPerChunk; ++q) {
-        if (c < NX + NC1) load_l1(c - NX, q, dst);
+        if (c < NX + NC1) load_l1(c - NX, q, dst, (!kRoles || t == cur_tile) ? rs_w1 : rs_w1_next);
         else load_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, q, dst);
       }
     }
@@ -547,7 +608,7 @@ void mlp3_bf16_kernel(
     if (c < NX) {
       if (step == 0) fetch_x(t, par, c, dst);
     } else if (step % kSpread == 0 && step / kSpread <= kDmaPerChunk) {
-      if (c < NX + NC1) load_l1(c - NX, step / kSpread, dst);
+      if (c < NX + NC1) load_l1(c - NX, step / kSpread, dst, (!kRoles || t == cur_tile) ? rs_w1 : rs_w1_next);
       else load_l2((c - NX - NC1) / KP, (c - NX - NC1) % KP, step / kSpread, dst);
     }
   };
@@ -565,9 +626,15 @@ void mlp3_bf16_kernel(
   const int l2 = prow * ROW2 + h * 16;
   const int sw3 = (r32 >> 2) & 3;
 
-  for (int i = tid; i < H1; i += kThreads) s_b1[i] = b1[i];
-  for (int i = tid; i < H2; i += kThreads) s_b2[i] = b2[i];
-  for (int i = tid; i < B; i += kThreads) { s_b3[i] = b3[i]; s_c[i] = kTwoPhase ? tp.tool_coef[i] : centre[i]; }
+  auto stage_biases = [&](int grp) {   // the biases of regressor grp (of the network when !kRoles)
+    for (int i = tid; i < H1; i += kThreads) s_b1[i] = b1[(size_t)grp * H1 + i];
+    for (int i = tid; i < H2; i += kThreads) s_b2[i] = b2[(size_t)grp * H2 + i];
+    for (int i = tid; i < B; i += kThreads) s_b3[i] = b3[(size_t)grp * B + i];
+  };
+  stage_biases(grp_cur);
+  if constexpr (!kRoles)
+    for (int i = tid; i < B; i += kThreads) s_c[i] = kTwoPhase ? tp.tool_coef[i] : centre[i];
+  float coef_cur = kRoles ? role_coef[grp_cur] : 0.0f;
   if (kTwoPhase) {
     for (int i = tid; i < kTab; i += kThreads) {
       s_head[i] = i < tp.n_roles ? tp.role_head[i] : 1;
@@ -592,6 +659,24 @@ void mlp3_bf16_kernel(
 
   int parity = 0;                         // tiles of this workgroup alternate s_meta halves
   for (int64_t tile = first_tile; tile < n_tiles; tile += stride, parity ^= 1) {
+    if constexpr (kRoles) {
+      // this tile's regressor: its W2 and W3 for this tile's layer-2 chunks, its W1 (already
+      // prefetched for the first layer-1 chunk) for the rest, and the next tile's W1 for the
+      // layer-1 chunk that this tile prefetches; biases restaged when the regressor changes
+      const int gc = group_of(tile), gn = group_of(tile + stride);
+      rs_w1 = rsrc_w1(gc);
+      rs_w2 = rsrc_w2(gc);
+      rs_w3 = rsrc_w3(gc);
+      rs_w1_next = rsrc_w1(gn);
+      cur_tile = tile;
+      if (gc != grp_cur) {
+        __syncthreads();   // every wavefront is done with the previous regressor's biases
+        stage_biases(gc);
+        __syncthreads();
+        grp_cur = gc;
+        coef_cur = role_coef[gc];
+      }
+    }
     // ---- features of this tile: B operands of layer 1, natural K order; group gr of this
     // wavefront is tile rows 32 (G wave + gr) .. + 31
     bf16x8 xf[G][KS1];
@@ -805,7 +890,14 @@ void mlp3_bf16_kernel(
       l2_epilogue(carry);
     }
 
-    if constexpr (kTwoPhase) {
+    if constexpr (kRoles) {
+      // output 0 of row r32 sits in register 0 of lane-half 0
+      const int local = wave * kRowsPerWave + r32;
+      const int32_t stage = s_meta[parity][3][local];
+      if (h == 0 && stage >= 0)
+        role_row(logit[0][0][0], s_b3[0], coef_cur, __int_as_float(s_meta[parity][2][local]), role_max_len, stage,
+                 s_meta[parity][0][local], s_meta[parity][1][local], s_alpha, n_models, pred_len, kv_bytes);
+    } else if constexpr (kTwoPhase) {
       // Both lane-halves select each group's head output; then lane-half h finishes row r of
       // group h (G = 2), or lane-half 0 the wavefront's only group (G = 1), so that the rest
       // of the row runs once per wavefront.
@@ -963,7 +1055,7 @@ maestro_status launch_mlp3(const maestro_predictor& p, int64_t n, const void* x,
         static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
         static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]),
         p.bias[0], p.bias[1], p.bias[2], kTwoPhase ? nullptr : p.bin_centre, n, n_tiles, prompt_len, model_id,
-        kv_bytes_per_token, n_models, pred_len, kv_bytes, tp);
+        kv_bytes_per_token, n_models, pred_len, kv_bytes, tp, nullptr, nullptr, nullptr, nullptr, nullptr, 0.0f);
   };
   if (mid) args(mlp3_bf16_kernel<256, 512, 512, 64, kMidGroups, kTwoPhase>);
   else args(mlp3_bf16_kernel<256, 1024, 1024, 64, 1, kTwoPhase>);
@@ -994,6 +1086,30 @@ maestro_status launch_predict(const maestro_predictor& p, int64_t n, const void*
   } else {
     return MAESTRO_ERR_UNSUPPORTED;
   }
+  return launch_status();
+}
+
+// The regressors' grouped GEMM: one persistent workgroup per compute unit (at most one per
+// possible tile), the tile count read on the device.
+maestro_status launch_role_regressors(const maestro_predictor& p, int64_t n, const void* x, const float* coef,
+                                      float max_len, const int32_t* tile_group, const int32_t* perm,
+                                      const int32_t* prompt_p, const int32_t* model_p, const int32_t* p_bits,
+                                      const int32_t* n_tiles, int64_t max_tiles, const float* kv_bytes_per_token,
+                                      int32_t n_models, float* pred_len, double* kv_bytes, hipStream_t stream) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return MAESTRO_ERR_LAUNCH;
+  const dim3 pgrid((unsigned)(max_tiles < cus ? max_tiles : cus)), block(kThreads);
+  auto args = [&](auto kernel) {
+    kernel<<<pgrid, block, 0, stream>>>(
+        static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(p.weight[0]),
+        static_cast<const uint16_t*>(p.weight[1]), static_cast<const uint16_t*>(p.weight[2]), p.bias[0],
+        p.bias[1], p.bias[2], nullptr, n, 0, prompt_p, model_p, kv_bytes_per_token, n_models, pred_len, kv_bytes,
+        TwoPhaseArgs{}, tile_group, perm, p_bits, n_tiles, coef, max_len);
+  };
+  if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, 1, false, true>);
+  else args(mlp3_bf16_kernel<256, 1024, 1024, 64, 1, false, true>);
   return launch_status();
 }
 

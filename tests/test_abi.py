@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 18
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
