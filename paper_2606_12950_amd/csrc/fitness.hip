@@ -10,13 +10,13 @@
 // (fitness, node) pairs are kept, larger fitness first and the lower index on equal fitness
 // (the strict ">" of Alg. 3). Every operation is float32 rounded to nearest, in that order.
 //
-// A workgroup takes 256 stages (one per thread; 256 / G when a small batch gives each stage G
-// lanes) and stages node state chunk by chunk in LDS, with everything that depends on the node
-// alone already evaluated: the normalised metrics (true divisions, once per node), the
-// headroom and its float64 reciprocal, 1 - norm(RTT) from every source and, with residency
-// bits, the penalty lambda * norm(T_ready) + mu * norm(C_deg) of every stage class for both
-// residency states. A pair then costs the feasibility test, the fit, the affinity and one
-// subtraction.
+// A workgroup takes 256 stages (one per thread), 512 for large batches (two per thread, which
+// then share every node read), or 256 / G when a small batch gives each stage G lanes. It
+// stages node state chunk by chunk in LDS, with everything that depends on the node alone
+// already evaluated: the normalised metrics (true divisions, once per node), the headroom and
+// its float64 reciprocal, 1 - norm(RTT) from every source and, with residency bits, the penalty
+// lambda * norm(T_ready) + mu * norm(C_deg) of every stage class for both residency states. A
+// pair then costs the feasibility test, the fit, the affinity and one subtraction.
 //
 // The fit is fl32(fl32(R_need) / fl32(headroom)) -- at most 1 on a feasible node, since R_need <=
 // headroom survives the rounding to float32; 0 on a node without headroom -- computed as the
@@ -33,7 +33,8 @@
 // LDS, column by column, with the other node terms; a node with more engines continues in the
 // step array in global memory (binary search). The main loop scores every pair as if it fit and
 // only queues the short ones; a lane then scores its queued nodes against their plans after
-// each chunk.
+// each chunk. A short pair whose fitness bound (its score with C_deg normalised to 0) cannot
+// enter the stage's top-k is dropped without a plan lookup.
 //
 // The window bounds are exact order statistics of a sample (no interpolation): one workgroup
 // radix-selects both ranks at once, 8 bits per pass over the order-preserving integer image.
@@ -159,9 +160,15 @@ struct FitnessChunk {
 // kMulti: G = 2^g_log2 lanes share a stage (batches too small to fill the chip); lane g scores
 // nodes g, g + G, g + 2G, ... of every chunk into its own list, and the G lists are merged with
 // xor-shuffles (lexicographic on (key, node)) before lane 0 writes the stage's results.
-// Dynamic LDS: with residency bits, the per-class penalties, n_classes * chunk float2.
-template <int KT, int kReady, bool kPlans, bool kMulti>
-__global__ __launch_bounds__(kThreads) void fitness_kernel(
+// kS: stages per lane (1 or 2; 1 with kMulti). The loop over pairs is bound by the bytes the
+// lanes read from LDS (a read that every lane shares costs as much as any other), and the node
+// terms a lane reads serve all of its stages: a second stage per lane cuts the bytes per pair
+// by a third.
+// Dynamic LDS: with residency bits, the per-class penalties, n_classes rows of chunk + 1 float2
+// (the pad puts one node's entries of different classes in different banks).
+template <int KT, int kReady, bool kPlans, bool kMulti, int kS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kPlans || KT * kS == 1 ? 1 : (kS == 2 ? 6 : 8), 8)))
+void fitness_kernel(
     int64_t n, const int32_t* __restrict__ model_id, const int32_t* __restrict__ src_id,
     const int32_t* __restrict__ class_id, const double* __restrict__ kv_bytes, int32_t n_models, int32_t n_nodes,
     int32_t n_src, int32_t n_classes, const double* __restrict__ free_bytes, const float* __restrict__ queue_ms,
@@ -170,31 +177,32 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     const maestro_deg_plan* __restrict__ plans, const maestro_plan_step* __restrict__ plan_steps,
     const float* __restrict__ rtt_ms, const float* __restrict__ class_weights, const float* __restrict__ bounds,
     double rho, int32_t k, int32_t* __restrict__ node_idx, float* __restrict__ fitness, int g_log2) {
-  // per node: {headroom, 1 / fl32(headroom)} (one 16-byte LDS read, the same address for every
-  // lane), the residency bits, and per source row 1 - norm(RTT). With residency bits, the
-  // penalty of each class for both states (model resident or not) and, for the short pairs of
-  // plans, the two normalised ready times; with a T_act matrix, norm(T_q + T_act) of every
-  // (node, model) and the node's normalised C_deg.
+  // per node: {headroom, 1 / fl32(headroom)} and the residency bits (reads that every lane
+  // shares), and per source row 1 - norm(RTT). With residency bits, the penalty of each class
+  // for both states (model resident or not) and, for the short pairs of plans, the two
+  // normalised ready times; with a T_act matrix, norm(T_q + T_act) of every (node, model) and
+  // the node's normalised C_deg.
   typedef typename std::conditional<kReady == kMask64, uint64_t, uint32_t>::type mask_t;
+  static_assert(kS == 1 || (kS == 2 && !kMulti), "lanes that share a stage take one stage each");
   constexpr bool kMat = kReady >= kMatrix16;
   constexpr int kMatRow = kReady == kMatrix16 ? 16 : 64;   // largest row the staging area holds
   // nodes staged in LDS at a time: small chunks keep the LDS footprint low enough for several
   // workgroups per CU, whose waves hide each other's LDS latency
   constexpr int kChunk = FitnessChunk<kReady>::value;
-  constexpr int kProxStride = kChunk + 1;      // one-word pad: rows of different sources in different banks
+  constexpr int kRowStride = kChunk + 1;   // one-entry pad: rows of different sources / classes in different banks
   struct Node { double free, recip; };
   __shared__ Node s_node[kChunk];
   __shared__ mask_t s_mask[kMat ? 1 : kChunk];
   __shared__ float2 s_tr[kMat || !kPlans ? 1 : kChunk];   // norm(T_q), norm(T_q + T_act)
   __shared__ float s_nd[kMat ? kChunk : 1];                // norm(C_deg) (T_act matrix)
-  __shared__ float s_prox[kMaxFitnessSources * kProxStride];   // 1 - norm(RTT), per source row
+  __shared__ float s_prox[kMaxFitnessSources * kRowStride];   // 1 - norm(RTT), per source row
   __shared__ float s_w[3 * kMaxFitnessClasses];           // (gamma, lambda, mu) per class
   constexpr int kPC = kPlans ? kChunk : 1;
   __shared__ double s_pfreed[kRecSteps][kPC];   // plan columns, node-minor: lanes reading
   __shared__ float s_pcost[kRecSteps][kPC];     // different nodes hit different banks
   __shared__ int32_t s_pn[kPC], s_pfirst[kPC];
-  constexpr int kQueue = kPlans ? 16 : 1;        // short nodes a lane queues per chunk
-  static_assert(kChunk <= 256 || !kPlans, "queued node offsets are bytes");
+  constexpr int kQueue = kPlans ? 16 : 1;   // short pairs a lane queues per chunk
+  static_assert(kChunk * kS <= 256 || !kPlans, "a queued pair (node offset, stage) is a byte");
   __shared__ uint8_t s_queue[kQueue * kThreads];
   // with a T_act matrix: normalised T_ready = norm(T_q + T_act) of every (node, model) of the
   // chunk, [node][model] with row stride n_models
@@ -204,44 +212,70 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
   const int tid = threadIdx.x;
   const int G = kMulti ? 1 << g_log2 : 1;
   const int g = kMulti ? tid & (G - 1) : 0;   // this lane's first node of each chunk
-  const int64_t stage = kMulti ? (int64_t)blockIdx.x * (kThreads >> g_log2) + (tid >> g_log2)
-                               : (int64_t)blockIdx.x * kThreads + tid;
-  const bool valid = stage < n;
   const float lo_r = bounds[0], hi_r = bounds[1], lo_t = bounds[2], hi_t = bounds[3];
   const float lo_d = bounds[4], hi_d = bounds[5];
   const float nd_fits = norm01(0.0f, lo_d, hi_d);   // normalised C_deg of a stage that fits
   for (int e = tid; e < 3 * n_classes; e += kThreads) s_w[e] = class_weights[e];
 
-  double need = INFINITY;   // an invalid lane admits nothing
-  double needd = 0.0;       // fl32(R_need), widened
-  float gamma = 0.0f, omg = 0.0f, lambda = 0.0f, mu = 0.0f;
-  mask_t mbit = 0;
-  int src = 0, model = 0, cls = 0;
-  bool ok = false;          // a stage whose model, source and class ids are in range
-  if (valid) {
-    const int32_t m = model_id[stage], s = src_id[stage], c = class_id[stage];
-    ok = (uint32_t)m < (uint32_t)n_models && (uint32_t)s < (uint32_t)n_src && (uint32_t)c < (uint32_t)n_classes;
-    if (ok) {
-      need = (rho == 0.0) ? kv_bytes[stage] : __dmul_rn(kv_bytes[stage], 1.0 + rho);
-      needd = (double)__double2float_rn(need);
-      const float* wt = class_weights + 3 * c;
-      gamma = wt[0];
-      lambda = wt[1];
-      mu = wt[2];
-      omg = __fsub_rn(1.0f, gamma);
-      model = m;
-      mbit = kMat ? 0 : (mask_t)1 << model;
-      src = s;
-      cls = c;
-    } else {
-      need = NAN;             // an id out of range: no node admits the stage, no plan is tried
+  // the stages of this lane: consecutive lanes take consecutive stages, 256 * kS per workgroup
+  struct Lane {
+    int64_t stage;
+    double need;    // R_need; +inf without a stage (admits nothing), NaN for ids out of range
+    double needd;   // fl32(R_need), widened
+    float gamma, omg, lambda, mu;
+    mask_t mbit;
+    int model;
+    bool ok;        // a stage whose model, source and class ids are in range
+    const float* prox;    // 1 - norm(RTT) from the stage's source, per node of the chunk
+    const float2* pen;    // the stage class's penalties, per node of the chunk
+  };
+  Lane L[kS];
+  TopK<KT> best[kS];   // keys are -fitness: the smallest key is the best node
+#pragma unroll
+  for (int s = 0; s < kS; ++s) {
+    Lane& l = L[s];
+    l.stage = kMulti ? (int64_t)blockIdx.x * (kThreads >> g_log2) + (tid >> g_log2)
+                     : ((int64_t)blockIdx.x * kS + s) * kThreads + tid;
+    l.need = INFINITY;
+    l.needd = 0.0;
+    l.gamma = l.omg = l.lambda = l.mu = 0.0f;
+    l.mbit = 0;
+    l.model = 0;
+    l.ok = false;
+    int src = 0, cls = 0;
+    if (l.stage < n) {
+      const int32_t m = model_id[l.stage], sid = src_id[l.stage], c = class_id[l.stage];
+      l.ok = (uint32_t)m < (uint32_t)n_models && (uint32_t)sid < (uint32_t)n_src &&
+             (uint32_t)c < (uint32_t)n_classes;
+      if (l.ok) {
+        l.need = (rho == 0.0) ? kv_bytes[l.stage] : __dmul_rn(kv_bytes[l.stage], 1.0 + rho);
+        l.needd = (double)__double2float_rn(l.need);
+        const float* wt = class_weights + 3 * c;
+        l.gamma = wt[0];
+        l.lambda = wt[1];
+        l.mu = wt[2];
+        l.omg = __fsub_rn(1.0f, l.gamma);
+        l.model = m;
+        l.mbit = kMat ? 0 : (mask_t)1 << m;
+        src = sid;
+        cls = c;
+      } else {
+        l.need = NAN;   // an id out of range: no node admits the stage, no plan is tried
+      }
     }
+    l.prox = s_prox + src * kRowStride;
+    l.pen = s_pen + cls * kRowStride;
+    best[s].init();
   }
-  const float* prox_row = s_prox + src * kProxStride;
-  const float2* pen_row = s_pen + cls * kChunk;
+  // A short pair's fitness is at most its score with C_deg normalised to 0 when mu >= 0: norm()
+  // is never below 0, the penalty cannot fall as C_deg grows, and every float32 operation is
+  // monotone. When a stage that fits normalises to 0 as well (nd_fits == 0), that bound is the
+  // score the main loop computes for the pair as if it fit, so a short pair whose bound cannot
+  // enter the lane's list (which only improves) is dropped there, before its plan is looked up.
+  bool prefilter[kS];
+#pragma unroll
+  for (int s = 0; s < kS; ++s) prefilter[s] = kPlans && nd_fits == 0.0f && L[s].mu >= 0.0f;
 
-  TopK<KT> best;   // keys are -fitness: the smallest key is the best node
-  best.init();
   for (int32_t c0 = 0; c0 < n_nodes; c0 += kChunk) {
     const int cn = min(kChunk, n_nodes - c0);
     __syncthreads();  // every lane is done with the previous chunk (and s_w is written)
@@ -263,7 +297,7 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         for (int c = 0; c < n_classes; ++c) {
           const float l = s_w[3 * c + 1], u = s_w[3 * c + 2];
           const float pd = __fmul_rn(u, nd);
-          s_pen[c * kChunk + i] =
+          s_pen[c * kRowStride + i] =
               make_float2(__fadd_rn(__fmul_rn(l, tr0), pd), __fadd_rn(__fmul_rn(l, tr1), pd));
         }
       }
@@ -285,33 +319,51 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
     }
     for (int e = tid; e < n_src * cn; e += kThreads) {
       const int r = e / cn, i = e - r * cn;
-      s_prox[r * kProxStride + i] = __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, hi_r));
+      s_prox[r * kRowStride + i] = __fsub_rn(1.0f, norm01(rtt_ms[(size_t)r * n_nodes + c0 + i], lo_r, hi_r));
     }
     __syncthreads();
     // A = gamma * prox + (1 - gamma) * fit with fit = fl32(fl32(R_need) * (1 / fl32(headroom)))
-    auto affinity = [&](const Node nd, float prox) {
-      const float fit = __double2float_rn(__dmul_rn(needd, nd.recip));
-      return __fadd_rn(__fmul_rn(gamma, prox), __fmul_rn(omg, fit));
+    auto affinity = [&](const Lane& l, const Node nd, float prox) {
+      const float fit = __double2float_rn(__dmul_rn(l.needd, nd.recip));
+      return __fadd_rn(__fmul_rn(l.gamma, prox), __fmul_rn(l.omg, fit));
     };
     // the penalty lambda * norm(T_ready) + mu * nd of node i
-    auto penalty = [&](int i, float nd) {
+    auto penalty = [&](const Lane& l, int i, float nd) {
       float tr;
       if constexpr (kMat) {
-        tr = s_ready[i * n_models + model];
+        tr = s_ready[i * n_models + l.model];
       } else {
         const float2 t = s_tr[i];
-        tr = (s_mask[i] & mbit) ? t.x : t.y;
+        tr = (s_mask[i] & l.mbit) ? t.x : t.y;
       }
-      return __fadd_rn(__fmul_rn(lambda, tr), __fmul_rn(mu, nd));
+      return __fadd_rn(__fmul_rn(l.lambda, tr), __fmul_rn(l.mu, nd));
+    };
+    // the pair's fitness when the stage fits (C_deg = the node's, or 0 with plans); mk is the
+    // node's residency bits
+    auto fits_score = [&](const Lane& l, int i, const Node nd, mask_t mk) {
+      const float a = affinity(l, nd, l.prox[i]);
+      float pen;
+      if constexpr (kMat) {
+        pen = __fadd_rn(__fmul_rn(l.lambda, s_ready[i * n_models + l.model]), __fmul_rn(l.mu, s_nd[i]));
+      } else {
+        const float2 p = l.pen[i];
+        pen = (mk & l.mbit) ? p.x : p.y;
+      }
+      return __fsub_rn(a, pen);
     };
     // A stage that falls short of node i's headroom by R takes the first step of the node's
     // plan whose freed bytes reach R, at that step's cost; no such step leaves the node
     // infeasible. These pairs are rare, so they leave the main loop: each lane queues its short
-    // nodes and scores them after the chunk (rescanning the chunk when its queue overflowed),
-    // inserting lexicographically since they come after nodes of larger index.
-    auto short_pair = [&](int i) {
+    // pairs and scores them after the chunk (rescanning the chunk when its queue overflowed),
+    // inserting lexicographically since they come after nodes of larger index. The stage is a
+    // compile-time index (std::integral_constant), so the lane state stays in registers.
+    auto short_pair = [&](int i, auto stage_index) {
+      constexpr int s = decltype(stage_index)::value;
+      const Lane& l = L[s];
       const Node nd = s_node[i];
-      const double R = __dsub_rn(need, nd.free);
+      const float a = affinity(l, nd, l.prox[i]);
+      if (l.mu >= 0.0f && -__fsub_rn(a, penalty(l, i, 0.0f)) > best[s].s[KT - 1]) return;   // cannot enter
+      const double R = __dsub_rn(l.need, nd.free);
       const int ne = s_pn[i];
       int jp = 0;
 #pragma unroll
@@ -331,68 +383,100 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
         found = lo < ne;
         if (found) c = st[lo].cost;
       }
-      if (found) {
-        const float a = affinity(nd, prox_row[i]);
-        best.push_lex(-__fsub_rn(a, penalty(i, norm01(c, lo_d, hi_d))), c0 + i);
-      }
+      if (found) best[s].push_lex(-__fsub_rn(a, penalty(l, i, norm01(c, lo_d, hi_d))), c0 + i);
     };
-    int n_short = 0;   // queued nodes of this chunk
-    auto queue = [&](int i) {
-      if (n_short < kQueue) s_queue[n_short * kThreads + tid] = (uint8_t)i;
+    auto short_pair_of = [&](int i, int s) {
+      if (kS == 1 || s == 0) short_pair(i, std::integral_constant<int, 0>{});
+      else short_pair(i, std::integral_constant<int, kS - 1>{});
+    };
+    int n_short = 0;   // queued pairs of this chunk
+    auto queue = [&](int code) {
+      if (n_short < kQueue) s_queue[n_short * kThreads + tid] = (uint8_t)code;
       ++n_short;
     };
-    // the pair's fitness when the stage fits (C_deg = the node's, or 0 with plans)
-    auto fits_score = [&](int i, const Node nd, float prox) {
-      const float a = affinity(nd, prox);
-      float pen;
-      if constexpr (kMat) {
-        pen = __fadd_rn(__fmul_rn(lambda, s_ready[i * n_models + model]), __fmul_rn(mu, s_nd[i]));
-      } else {
-        const float2 p = pen_row[i];
-        pen = (s_mask[i] & mbit) ? p.x : p.y;
-      }
-      return __fsub_rn(a, pen);
+    auto node_mask = [&](int i) -> mask_t {
+      if constexpr (kMat) return 0;
+      else return s_mask[i];
     };
-    // groups of four of this lane's nodes: their LDS reads issue together, the four scores are
-    // computed before any of them enters the list, and with plans one branch per group queues
-    // the short ones
-    int i = g;
-    for (; i + 3 * G < cn; i += 4 * G) {
-      Node nd[4];
-      float px[4], sc[4];
-      bool fits[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        nd[u] = s_node[i + u * G];
-        px[u] = prox_row[i + u * G];
+    if constexpr (kS == 1 && !kPlans) {
+      // one node at a time, unrolled by four: few registers in flight, so that many
+      // wavefronts per SIMD hide the LDS latency
+#pragma unroll 4
+      for (int i = g; i < cn; i += G) {
+        const Node nd = s_node[i];
+        best[0].push_increasing_if(L[0].need <= nd.free, -fits_score(L[0], i, nd, node_mask(i)), c0 + i);
       }
+    } else if constexpr (kS == 1) {
+      // groups of four of this lane's nodes: their LDS reads issue together, the four scores
+      // are computed before any of them enters the list, and one branch per group queues the
+      // short ones
+      int i = g;
+      for (; i + 3 * G < cn; i += 4 * G) {
+        Node nd[4];
+        bool fits[4];
+        float sc[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        fits[u] = need <= nd[u].free;
-        sc[u] = fits_score(i + u * G, nd[u], px[u]);
+        for (int u = 0; u < 4; ++u) nd[u] = s_node[i + u * G];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          fits[u] = L[0].need <= nd[u].free;
+          sc[u] = fits_score(L[0], i + u * G, nd[u], node_mask(i + u * G));
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) best[0].push_increasing_if(fits[u], -sc[u], c0 + i + u * G);
+        if (L[0].ok && !(fits[0] && fits[1] && fits[2] && fits[3])) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (!fits[u] && !(prefilter[0] && -sc[u] > best[0].s[KT - 1])) queue(i + u * G);
+        }
       }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) best.push_increasing_if(fits[u], -sc[u], c0 + i + u * G);
-      if (kPlans && ok && !(fits[0] && fits[1] && fits[2] && fits[3])) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (!fits[u]) queue(i + u * G);
+      for (; i < cn; i += G) {
+        const Node nd = s_node[i];
+        const bool fits = L[0].need <= nd.free;
+        const float key = -fits_score(L[0], i, nd, node_mask(i));
+        best[0].push_increasing_if(fits, key, c0 + i);
+        if (L[0].ok && !fits && !(prefilter[0] && key > best[0].s[KT - 1])) queue(i);
       }
-    }
-    for (; i < cn; i += G) {
-      const Node nd = s_node[i];
-      const bool fits = need <= nd.free;
-      best.push_increasing_if(fits, -fits_score(i, nd, prox_row[i]), c0 + i);
-      if (kPlans && ok && !fits) queue(i);
+    } else {
+      // every node once for the lane's stages: one read of its shared terms, then per stage
+      // the stage's own source and class entries; with plans one branch per node queues the
+      // short pairs
+#pragma unroll 2
+      for (int i = 0; i < cn; ++i) {
+        const Node nd = s_node[i];
+        const mask_t mk = node_mask(i);
+        bool fits[kS];
+        float key[kS];
+#pragma unroll
+        for (int s = 0; s < kS; ++s) {
+          fits[s] = L[s].need <= nd.free;
+          key[s] = -fits_score(L[s], i, nd, mk);
+          best[s].push_increasing_if(fits[s], key[s], c0 + i);
+        }
+        if constexpr (kPlans) {
+          if (!(fits[0] && fits[kS - 1])) {
+#pragma unroll
+            for (int s = 0; s < kS; ++s)
+              if (L[s].ok && !fits[s] && !(prefilter[s] && key[s] > best[s].s[KT - 1])) queue(i + s * kChunk);
+          }
+        }
+      }
     }
     if (kPlans && n_short > 0) {
       if (n_short <= kQueue) {
 #pragma unroll 1
-        for (int q = 0; q < n_short; ++q) short_pair(s_queue[q * kThreads + tid]);
+        for (int q = 0; q < n_short; ++q) {
+          const int code = s_queue[q * kThreads + tid];
+          short_pair_of(code % kChunk, code / kChunk);
+        }
       } else {
 #pragma unroll 1
-        for (int i = g; i < cn; i += G)
-          if (!(need <= s_node[i].free)) short_pair(i);
+        for (int i = g; i < cn; i += G) {
+          const double fr = s_node[i].free;
+#pragma unroll
+          for (int s = 0; s < kS; ++s)
+            if (L[s].ok && !(L[s].need <= fr)) short_pair_of(i, s);
+        }
       }
     }
   }
@@ -403,21 +487,25 @@ __global__ __launch_bounds__(kThreads) void fitness_kernel(
       int32_t pn[KT];
 #pragma unroll
       for (int i = 0; i < KT; ++i) {
-        ps[i] = __shfl_xor(best.s[i], o);
-        pn[i] = __shfl_xor(best.n[i], o);
+        ps[i] = __shfl_xor(best[0].s[i], o);
+        pn[i] = __shfl_xor(best[0].n[i], o);
       }
 #pragma unroll
-      for (int i = 0; i < KT; ++i) best.push_lex(ps[i], pn[i]);
+      for (int i = 0; i < KT; ++i) best[0].push_lex(ps[i], pn[i]);
     }
   }
 
-  if (valid && g == 0) {
 #pragma unroll
-    for (int i = 0; i < KT; ++i) {
-      if (i < k) {
-        const bool some = best.n[i] != kNoNode;
-        node_idx[stage * k + i] = some ? best.n[i] : -1;
-        fitness[stage * k + i] = some ? -best.s[i] : -INFINITY;
+  for (int s = 0; s < kS; ++s) {
+    const int64_t stage = L[s].stage;
+    if (stage < n && g == 0) {
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        if (i < k) {
+          const bool some = best[s].n[i] != kNoNode;
+          node_idx[stage * k + i] = some ? best[s].n[i] : -1;
+          fitness[stage * k + i] = some ? -best[s].s[i] : -INFINITY;
+        }
       }
     }
   }
@@ -744,25 +832,30 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
   // wavefronts per SIMD of a 256-CU chip, and never more lanes than a chunk has nodes
   int g_log2 = 0;
   while (g_log2 < 4 && n * (2 << g_log2) <= kFitnessLanesTarget && (2 << g_log2) <= n_nodes) ++g_log2;
-  const int64_t per_block = kThreads >> g_log2;
+  // stages per lane: two when the batch still gives the chip that many wavefronts with two (and
+  // the lists are short enough to keep both stages' state in registers), else one. With plans
+  // (more registers and LDS per workgroup, so fewer resident workgroups) two only from twice
+  // that size on: a grid just above one round of resident workgroups would run a second, nearly
+  // empty round.
+  const bool with_plans = plans != nullptr;
+  const bool two = g_log2 == 0 && k <= 4 && n >= (with_plans ? 4 : 2) * kFitnessLanesTarget;
+  const int64_t per_block = two ? 2 * kThreads : kThreads >> g_log2;
   const dim3 grid((unsigned)((n + per_block - 1) / per_block)), block(kThreads);
   const int ready = act_matrix ? (n_models > 16 ? kMatrix64 : kMatrix16) : (n_models > 32 ? kMask64 : kMask32);
-  const bool with_plans = plans != nullptr;
-  // per-class penalties of a chunk (residency-bit forms only)
+  // per-class penalties of a chunk (residency-bit forms only), rows of chunk + 1 entries
   const size_t pen_bytes =
-      act_matrix ? 0 : (size_t)n_classes * (size_t)FitnessChunk<kMask32>::value * sizeof(float2);
-#define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                          \
-  do {                                                                                                          \
-    if (g_log2 > 0)                                                                                             \
-      fitness_kernel<KT, RD, PL, true><<<grid, block, pen_bytes, stream>>>(                                     \
-          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
-          act_ms, resident_mask, act_matrix, deg_ms, plans, plan_steps, rtt_ms, class_weights, bounds, rho, k,  \
-          node_idx, fitness, g_log2);                                                                           \
-    else                                                                                                        \
-      fitness_kernel<KT, RD, PL, false><<<grid, block, pen_bytes, stream>>>(                                    \
-          n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms,   \
-          act_ms, resident_mask, act_matrix, deg_ms, plans, plan_steps, rtt_ms, class_weights, bounds, rho, k,  \
-          node_idx, fitness, 0);                                                                                \
+      act_matrix ? 0 : (size_t)n_classes * (size_t)(FitnessChunk<kMask32>::value + 1) * sizeof(float2);
+#define MAESTRO_FIT_ARGS                                                                                         \
+  n, model_id, src_id, class_id, kv_bytes, n_models, n_nodes, n_src, n_classes, free_bytes, queue_ms, act_ms,    \
+      resident_mask, act_matrix, deg_ms, plans, plan_steps, rtt_ms, class_weights, bounds, rho, k, node_idx, fitness
+#define MAESTRO_FIT_LAUNCH(KT, RD, PL)                                                                            \
+  do {                                                                                                            \
+    if (g_log2 > 0)                                                                                               \
+      fitness_kernel<KT, RD, PL, true, 1><<<grid, block, pen_bytes, stream>>>(MAESTRO_FIT_ARGS, g_log2);          \
+    else if (two)                                                                                                 \
+      fitness_kernel<KT, RD, PL, false, (KT <= 4 ? 2 : 1)><<<grid, block, pen_bytes, stream>>>(MAESTRO_FIT_ARGS, 0); \
+    else                                                                                                          \
+      fitness_kernel<KT, RD, PL, false, 1><<<grid, block, pen_bytes, stream>>>(MAESTRO_FIT_ARGS, 0);              \
   } while (0)
 #define MAESTRO_FIT_RD(KT, PL)                                       \
   do {                                                               \
@@ -784,6 +877,7 @@ maestro_status launch_route_fitness(int64_t n, const int32_t* model_id, const in
 #undef MAESTRO_FIT_KT
 #undef MAESTRO_FIT_RD
 #undef MAESTRO_FIT_LAUNCH
+#undef MAESTRO_FIT_ARGS
   return launch_status();
 }
 
