@@ -446,18 +446,25 @@ def route_tiered_bench(name: str, steps: int, warmup: int):
 
 def margin_bench(steps: int, warmup: int):
     """The adaptive safety margin (EWMA of the relative underestimation, then its high quantile)
-    over windows of recent stages. Latency-bound: one workgroup per kernel. One JSON line."""
+    over windows of recent stages, and the window bounds (maestro_quantiles) over the same
+    lengths. Windows of 32,768 values or more select over 256 workgroups in a workspace,
+    preallocated here. One JSON line."""
     import torch
     from paper_2606_12950_amd import _native, pipeline
     from paper_2606_12950_amd import workload as W
     torch.cuda.set_device(0)
     res = {"margin": "adaptive rho", "beta": 0.2, "q": 0.95, "windows": []}
-    for m in (4096, 65536, 1 << 20):
+    for m in (4096, 65536, 1 << 20, 1 << 22):
         actual, pred = W.margin_window(3, m)
         a, p = pipeline._t(actual, "cuda"), pipeline._t(pred, "cuda")
-        out = _native.adaptive_rho(a, p, 0.2, 0.95)
-        d = _time_events(lambda: _native.adaptive_rho(a, p, 0.2, 0.95, out=out), steps, warmup)
-        res["windows"].append({"m": m, "ms": percentiles(d), "rho": float(out[1].item())})
+        ws = torch.empty(max(_native.quantiles_workspace_bytes(m), 16), dtype=torch.uint8, device="cuda")
+        out = _native.adaptive_rho(a, p, 0.2, 0.95, workspace=ws)
+        d = _time_events(lambda: _native.adaptive_rho(a, p, 0.2, 0.95, out=out, workspace=ws), steps, warmup)
+        qv = out[0].clone()
+        qo = _native.quantiles(qv, workspace=ws)
+        dq = _time_events(lambda: _native.quantiles(qv, out=qo, workspace=ws), steps, warmup)
+        res["windows"].append({"m": m, "ms": percentiles(d), "quantiles_ms": percentiles(dq),
+                               "rho": float(out[1].item())})
     import oracle
     actual, pred = W.margin_window(3, 1 << 20)
     res["cpu_baseline"] = oracle_timed(lambda: oracle.adaptive_rho(actual, pred, 0.2, 0.95), 1 << 20,

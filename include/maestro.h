@@ -254,6 +254,29 @@ MAESTRO_API maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, 
                              int32_t* node_idx, float* score,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/* The two halves of MAESTRO_ROUTE_SORTED (Sec. III-D; Alg. 3; Eq. 6), for callers that route
+ * several batches against one node state, or that run the node half beside other work on a
+ * second stream of the same priority and join it before the walk.
+ * maestro_route_sort_nodes writes, for every model m, its n_nodes nodes in ascending order of
+ * (ready time, node index), ready = fl32(queue_s[j] + act) with act as in maestro_route (0 when
+ * bit m of resident_mask[j] is set, else cold_s[j]) or, when act_s is not NULL, act_s[j][m] as in
+ * maestro_route_tiered (cold_s and resident_mask are then not read), each with its headroom
+ * free_bytes[j]. `lists` is device memory of at least maestro_route_lists_bytes(n_models,
+ * n_nodes) bytes, 16-byte aligned, owned by the caller, valid until the node state changes.
+ * maestro_route_walk then gives every stage exactly the result of maestro_route_ex (or
+ * maestro_route_tiered) with MAESTRO_ROUTE_SORTED on that node state; it reads only `lists` of
+ * the node state. n_nodes <= 8192 (else MAESTRO_ERR_UNSUPPORTED; maestro_route_lists_bytes is
+ * then 0); lists_bytes too small is MAESTRO_ERR_WORKSPACE; other arguments and errors as
+ * maestro_route_ex. */
+MAESTRO_API size_t maestro_route_lists_bytes(int32_t n_models, int32_t n_nodes);
+MAESTRO_API maestro_status maestro_route_sort_nodes(int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                             const float* queue_s, const float* cold_s, const uint64_t* resident_mask,
+                             const float* act_s, void* lists, size_t lists_bytes, void* stream);
+MAESTRO_API maestro_status maestro_route_walk(int64_t n, const int32_t* model_id, const float* pred_len,
+                             const double* kv_bytes, const float* decode_s_per_token,
+                             int32_t n_models, int32_t n_nodes, const void* lists, size_t lists_bytes,
+                             double rho, int32_t k, int32_t* node_idx, float* score, void* stream);
+
 /* Minimum-impact degradation plans of a node (Alg. 2) and their disruption cost (Eq. 4), for
  * every possible shortfall. Alg. 2 takes the node's engines in priority order -- ascending
  * action level, the lower engine index first on equal levels -- and stops before the first
@@ -382,20 +405,26 @@ MAESTRO_API maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n
  * than 16,384 stages as the call's scratch (per-tile scan state in the first words of each
  * 8,192-stage range): its contents are defined once the stream reaches the call's end. The
  * float64 EWMA is a parallel scan, so ewma can differ from a sequential evaluation in the last
- * place. Errors:
- * INVALID_ARG for m < 1, beta or q out of range, a NULL or misaligned array; UNSUPPORTED for
- * m > 2^32 - 1. */
+ * place. Workspace: maestro_quantiles_workspace(m) bytes (0 below 32,768 stages; NULL allowed
+ * then). Errors: INVALID_ARG for m < 1, beta or q out of range, a NULL or misaligned array;
+ * WORKSPACE for a workspace that is too small; UNSUPPORTED for m > 2^32 - 1. */
 MAESTRO_API maestro_status maestro_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m,
-                             double beta, double q, float* ewma, float* rho, void* stream);
+                             double beta, double q, float* ewma, float* rho, void* workspace,
+                             size_t workspace_bytes, void* stream);
 
 /* Window bounds of the robust normalisation in Eq. 5 (per-metric 5th/95th percentiles of a
  * recent window): out[0] and out[1] (device, float32) receive the values of rank
  * floor(q_lo * (m - 1)) and ceil(q_hi * (m - 1)) of values[0 .. m-1] (device, finite), ranks
  * counted from 0 in ascending order of the float values (-0 before +0); no interpolation.
- * 0 <= q_lo <= q_hi <= 1, 1 <= m < 2^32. One workgroup; meant for windows of up to a few
- * million values. No workspace. */
+ * 0 <= q_lo <= q_hi <= 1, 1 <= m < 2^32. Below 32,768 values one workgroup selects (no
+ * workspace); from there on 256 workgroups count each 8-bit digit pass into histograms of
+ * their own in the workspace (maestro_quantiles_workspace(m) bytes) and one workgroup picks
+ * the bins, eight launches in all. WORKSPACE for a workspace that is too small. */
 MAESTRO_API maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi,
-                             float* out, void* stream);
+                             float* out, void* workspace, size_t workspace_bytes, void* stream);
+/* Workspace bytes of maestro_quantiles and maestro_adaptive_rho over m values (0 when none is
+ * needed, and for m outside 1 .. 2^32 - 1). */
+MAESTRO_API size_t maestro_quantiles_workspace(int64_t m);
 
 /* Slack ordering of n_workflows workflow chains over n_stages stages (Sec. III-D, Eq. 7).
  *   chain_offset        [n_workflows + 1] int64, chain_offset[0] = 0, non-decreasing,

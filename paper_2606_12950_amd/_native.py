@@ -24,7 +24,9 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace
 EXPORTS = ("maestro_predict", "maestro_predict_two_phase", "maestro_route", "maestro_route_tiered", "maestro_route_ex", "maestro_route_fitness",
            "maestro_degradation_plans", "maestro_activation_latency", "maestro_adaptive_rho", "maestro_quantiles", "maestro_prioritize", "maestro_predict_workspace",
            "maestro_route_workspace", "maestro_prioritize_workspace", "maestro_status_string",
-           "maestro_prioritize_noalloc", "maestro_predict_role_lengths", "maestro_role_lengths_workspace")
+           "maestro_prioritize_noalloc", "maestro_predict_role_lengths", "maestro_role_lengths_workspace",
+           "maestro_route_lists_bytes", "maestro_route_sort_nodes", "maestro_route_walk",
+           "maestro_quantiles_workspace")
 
 PRIORITIZE_NOALLOC_MAX_WORKFLOWS = 1 << 20
 
@@ -96,11 +98,19 @@ def load():
                                           f64, i32, P, P, P]
     lib.maestro_activation_latency.argtypes = [i32, i32, P, P, P, P, f64, P, P]
     lib.maestro_route_tiered.argtypes = [i64, P, P, P, P, i32, i32, P, P, P, f64, i32, i32, P, P, P, sz, P]
-    lib.maestro_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P, P]
+    lib.maestro_adaptive_rho.argtypes = [P, P, i64, f64, f64, P, P, P, sz, P]
     lib.maestro_degradation_plans.argtypes = [i32, P, P, P, P, ctypes.c_float, P, P, P]
-    lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P]
+    lib.maestro_quantiles.argtypes = [P, i64, f64, f64, P, P, sz, P]
+    lib.maestro_quantiles_workspace.argtypes = [i64]
+    lib.maestro_quantiles_workspace.restype = sz
     lib.maestro_prioritize.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, sz, P]
     lib.maestro_prioritize_noalloc.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P]
+    lib.maestro_route_sort_nodes.argtypes = [i32, i32, P, P, P, P, P, P, sz, P]
+    lib.maestro_route_sort_nodes.restype = ctypes.c_int
+    lib.maestro_route_walk.argtypes = [i64, P, P, P, P, i32, i32, P, sz, f64, i32, P, P, P]
+    lib.maestro_route_walk.restype = ctypes.c_int
+    lib.maestro_route_lists_bytes.argtypes = [i32, i32]
+    lib.maestro_route_lists_bytes.restype = sz
     for f in ("maestro_predict", "maestro_route", "maestro_route_ex", "maestro_prioritize",
               "maestro_prioritize_noalloc"):
         getattr(lib, f).restype = ctypes.c_int
@@ -526,9 +536,23 @@ def activation_latency(tier: torch.Tensor, model_bytes: torch.Tensor, tier_bw: t
     return out
 
 
+def quantiles_workspace_bytes(m: int) -> int:
+    return int(load().maestro_quantiles_workspace(m))
+
+
+def _select_workspace(m: int, workspace: Optional[torch.Tensor], device) -> Tuple[Optional[int], int]:
+    _workspace(workspace)
+    need = quantiles_workspace_bytes(m)
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    return (_ptr(workspace), workspace.numel()) if workspace is not None else (None, 0)
+
+
 def adaptive_rho(kv_actual: torch.Tensor, kv_pred: torch.Tensor, beta: float, q: float,
-                 out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """maestro_adaptive_rho: returns (ewma float32 [m], rho float32 [1]) on the device."""
+                 out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, workspace: Optional[torch.Tensor] = None,
+                 stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_adaptive_rho: returns (ewma float32 [m], rho float32 [1]) on the device; the
+    workspace (quantiles_workspace_bytes(m), uint8) is allocated when needed and not given."""
     lib = load()
     _dev(kv_actual, "kv_actual", torch.float64)
     _dev(kv_pred, "kv_pred", torch.float64)
@@ -541,22 +565,26 @@ def adaptive_rho(kv_actual: torch.Tensor, kv_pred: torch.Tensor, beta: float, q:
     ew, rho = out
     _shape(_dev(ew, "ewma", torch.float32), "ewma", (m,))
     _shape(_dev(rho, "rho", torch.float32), "rho", (1,))
+    ws = _select_workspace(m, workspace, kv_actual.device)
     st = lib.maestro_adaptive_rho(_ptr(kv_actual), _ptr(kv_pred), m, float(beta), float(q), _ptr(ew), _ptr(rho),
-                                  _stream(stream))
+                                  ws[0], ws[1], _stream(stream))
     _check("maestro_adaptive_rho", st)
     return ew, rho
 
 
 def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,
-              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+              out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
     """maestro_quantiles: float32 [2] on the device = the order statistics of rank
-    floor(q_lo (m-1)) and ceil(q_hi (m-1)) of ``values``."""
+    floor(q_lo (m-1)) and ceil(q_hi (m-1)) of ``values``; the workspace
+    (quantiles_workspace_bytes(m), uint8) is allocated when needed and not given."""
     lib = load()
     _dev(values, "values", torch.float32)
     if out is None:
         out = torch.empty(2, dtype=torch.float32, device=values.device)
     _shape(_dev(out, "out", torch.float32), "out", (2,))
-    st = lib.maestro_quantiles(_ptr(values), values.numel(), float(q_lo), float(q_hi), _ptr(out),
+    ws = _select_workspace(values.numel(), workspace, values.device)
+    st = lib.maestro_quantiles(_ptr(values), values.numel(), float(q_lo), float(q_hi), _ptr(out), ws[0], ws[1],
                                _stream(stream))
     _check("maestro_quantiles", st)
     return out
@@ -564,6 +592,73 @@ def quantiles(values: torch.Tensor, q_lo: float = 0.05, q_hi: float = 0.95,
 
 def route_workspace_bytes(n: int, n_models: int, n_nodes: int, k: int) -> int:
     return int(load().maestro_route_workspace(n, n_models, n_nodes, k))
+
+
+def route_lists_bytes(n_models: int, n_nodes: int) -> int:
+    """maestro_route_lists_bytes: device bytes of the per-model node lists (0 past 8,192 nodes)."""
+    return int(load().maestro_route_lists_bytes(n_models, n_nodes))
+
+
+def route_sort_nodes(free_bytes: torch.Tensor, queue_s: torch.Tensor, cold_s: Optional[torch.Tensor],
+                     resident_mask: Optional[torch.Tensor], n_models: int, act_s: Optional[torch.Tensor] = None,
+                     lists: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """maestro_route_sort_nodes: every model's nodes in (ready time, index) order with their
+    headroom, into ``lists`` (uint8, route_lists_bytes(n_models, n_nodes) bytes; allocated when
+    None) -- the node half of the sorted route. With ``act_s`` [n_nodes][n_models] (seconds)
+    the readiness-tier form; ``cold_s`` / ``resident_mask`` may then be None."""
+    lib = load()
+    _dev(free_bytes, "free_bytes", torch.float64)
+    _dev(queue_s, "queue_s", torch.float32)
+    M = free_bytes.shape[0]
+    if free_bytes.dim() != 1 or queue_s.shape != (M,):
+        raise ValueError("per-node inputs must be one-dimensional and of the same length")
+    if act_s is not None:
+        _dev(act_s, "act_s", torch.float32)
+        if tuple(act_s.shape) != (M, n_models):
+            raise ValueError("act_s must be [n_nodes][n_models]")
+    else:
+        _dev(cold_s, "cold_s", torch.float32)
+        _dev(resident_mask, "resident_mask", torch.int64)
+        if cold_s.shape != (M,) or resident_mask.shape != (M,):
+            raise ValueError("per-node inputs must have the same length")
+    need = route_lists_bytes(n_models, M)
+    if lists is None:
+        lists = torch.empty(max(need, 16), dtype=torch.uint8, device=free_bytes.device)
+    _workspace(lists)
+    st = lib.maestro_route_sort_nodes(n_models, M, _ptr(free_bytes), _ptr(queue_s),
+                                      _ptr(cold_s) if act_s is None else None,
+                                      _ptr(resident_mask) if act_s is None else None,
+                                      _ptr(act_s) if act_s is not None else None, _ptr(lists), lists.numel(),
+                                      _stream(stream))
+    _check("maestro_route_sort_nodes", st)
+    return lists
+
+
+def route_walk(model_id: torch.Tensor, pred_len: torch.Tensor, kv_bytes: torch.Tensor,
+               decode_s_per_token: torch.Tensor, n_nodes: int, lists: torch.Tensor, k: int = 1, rho: float = 0.0,
+               out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """maestro_route_walk: the stage half of the sorted route over lists from route_sort_nodes;
+    returns (node_idx int32 [N][k], score float32 [N][k])."""
+    lib = load()
+    _dev(model_id, "model_id", torch.int32)
+    n = model_id.shape[0]
+    _dev(pred_len, "pred_len", torch.float32)
+    _dev(kv_bytes, "kv_bytes", torch.float64)
+    _dev(decode_s_per_token, "decode_s_per_token", torch.float32)
+    if model_id.dim() != 1 or decode_s_per_token.dim() != 1 or pred_len.shape != (n,) or kv_bytes.shape != (n,):
+        raise ValueError("per-stage inputs must be one-dimensional and of the same length")
+    _workspace(lists)
+    if out is None:
+        out = (torch.empty((n, k), dtype=torch.int32, device=model_id.device),
+               torch.empty((n, k), dtype=torch.float32, device=model_id.device))
+    idx, sc = out
+    _shape(_dev(idx, "node_idx", torch.int32), "node_idx", (n, k))
+    _shape(_dev(sc, "score", torch.float32), "score", (n, k))
+    st = lib.maestro_route_walk(n, _ptr(model_id), _ptr(pred_len), _ptr(kv_bytes), _ptr(decode_s_per_token),
+                                decode_s_per_token.shape[0], int(n_nodes), _ptr(lists), lists.numel(), float(rho),
+                                int(k), _ptr(idx), _ptr(sc), _stream(stream))
+    _check("maestro_route_walk", st)
+    return idx, sc
 
 
 def prioritize_workspace_bytes(n_workflows: int, n_stages: int) -> int:

@@ -215,6 +215,47 @@ maestro_status maestro_route(int64_t n, const int32_t* model_id, const float* pr
                           node_idx, score, workspace, workspace_bytes, stream);
 }
 
+size_t maestro_route_lists_bytes(int32_t n_models, int32_t n_nodes) {
+  if (n_models < 1 || n_models > 64 || n_nodes < 1) return 0;
+  return maestro::route_lists_bytes(n_models, n_nodes);
+}
+
+maestro_status maestro_route_sort_nodes(int32_t n_models, int32_t n_nodes, const double* free_bytes,
+                                        const float* queue_s, const float* cold_s, const uint64_t* resident_mask,
+                                        const float* act_s, void* lists, size_t lists_bytes, void* stream) {
+  if (n_models < 1 || n_models > 64 || n_nodes < 1) return MAESTRO_ERR_INVALID_ARG;
+  if (!free_bytes || !queue_s || !aligned(free_bytes, 8) || !aligned(queue_s, 4)) return MAESTRO_ERR_INVALID_ARG;
+  if (act_s ? !aligned(act_s, 4)
+            : (!cold_s || !resident_mask || !aligned(cold_s, 4) || !aligned(resident_mask, 8)))
+    return MAESTRO_ERR_INVALID_ARG;
+  const size_t need = maestro::route_lists_bytes(n_models, n_nodes);
+  if (need == 0) return MAESTRO_ERR_UNSUPPORTED;
+  if (!lists || !aligned(lists, 16) || lists_bytes < need) return MAESTRO_ERR_WORKSPACE;
+  return maestro::launch_sort_nodes(n_models, n_nodes, free_bytes, queue_s, cold_s, resident_mask, act_s, lists,
+                                    as_stream(stream));
+}
+
+maestro_status maestro_route_walk(int64_t n, const int32_t* model_id, const float* pred_len, const double* kv_bytes,
+                                  const float* decode_s_per_token, int32_t n_models, int32_t n_nodes,
+                                  const void* lists, size_t lists_bytes, double rho, int32_t k, int32_t* node_idx,
+                                  float* score, void* stream) {
+  if (n < 0 || n_models < 1 || n_models > 64 || n_nodes < 1 || k < 1 || k > 16) return MAESTRO_ERR_INVALID_ARG;
+  if (!(rho >= 0.0) || rho == INFINITY) return MAESTRO_ERR_INVALID_ARG;
+  if (!decode_s_per_token || !aligned(decode_s_per_token, 4)) return MAESTRO_ERR_INVALID_ARG;
+  if (n > 0) {
+    if (!model_id || !pred_len || !kv_bytes || !node_idx || !score) return MAESTRO_ERR_INVALID_ARG;
+    if (!aligned(model_id, 4) || !aligned(pred_len, 4) || !aligned(kv_bytes, 8) || !aligned(node_idx, 4) ||
+        !aligned(score, 4))
+      return MAESTRO_ERR_INVALID_ARG;
+  }
+  if (n > (int64_t)1 << 37) return MAESTRO_ERR_UNSUPPORTED;
+  const size_t need = maestro::route_lists_bytes(n_models, n_nodes);
+  if (need == 0) return MAESTRO_ERR_UNSUPPORTED;
+  if (!lists || !aligned(lists, 16) || lists_bytes < need) return MAESTRO_ERR_WORKSPACE;
+  return maestro::launch_route_walk(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes, lists,
+                                    rho, k, node_idx, score, as_stream(stream));
+}
+
 maestro_status maestro_route_fitness(int64_t n, const int32_t* model_id, const int32_t* src_id,
                                      const int32_t* class_id, const double* kv_bytes,
                                      int32_t n_models, int32_t n_nodes, int32_t n_src,
@@ -284,25 +325,34 @@ maestro_status maestro_activation_latency(int32_t n_nodes, int32_t n_models, con
                                             as_stream(stream));
 }
 
+size_t maestro_quantiles_workspace(int64_t m) {
+  return (m >= 1 && m <= (int64_t)UINT32_MAX) ? maestro::quantiles_workspace_bytes(m) : 0;
+}
+
 maestro_status maestro_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
-                                    double q, float* ewma, float* rho, void* stream) {
+                                    double q, float* ewma, float* rho, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
   if (m < 1 || !(beta > 0.0 && beta <= 1.0) || !(q >= 0.0 && q <= 1.0)) return MAESTRO_ERR_INVALID_ARG;
   if (!kv_actual || !kv_pred || !ewma || !rho || !aligned(kv_actual, 8) || !aligned(kv_pred, 8) ||
       !aligned(ewma, 4) || !aligned(rho, 4))
     return MAESTRO_ERR_INVALID_ARG;
   if (m > (int64_t)UINT32_MAX) return MAESTRO_ERR_UNSUPPORTED;
+  const size_t need = maestro::quantiles_workspace_bytes(m);
+  if (need > 0 && (!workspace || !aligned(workspace, 16) || workspace_bytes < need)) return MAESTRO_ERR_WORKSPACE;
   const int64_t rank = (int64_t)ceil(q * (double)(m - 1));
-  return maestro::launch_adaptive_rho(kv_actual, kv_pred, m, beta, rank, ewma, rho, as_stream(stream));
+  return maestro::launch_adaptive_rho(kv_actual, kv_pred, m, beta, rank, ewma, rho, workspace, as_stream(stream));
 }
 
 maestro_status maestro_quantiles(const float* values, int64_t m, double q_lo, double q_hi, float* out,
-                                 void* stream) {
+                                 void* workspace, size_t workspace_bytes, void* stream) {
   if (m < 1 || !(q_lo >= 0.0) || !(q_lo <= q_hi) || !(q_hi <= 1.0)) return MAESTRO_ERR_INVALID_ARG;
   if (!values || !out || !aligned(values, 4) || !aligned(out, 4)) return MAESTRO_ERR_INVALID_ARG;
   if (m > (int64_t)UINT32_MAX) return MAESTRO_ERR_UNSUPPORTED;
+  const size_t need = maestro::quantiles_workspace_bytes(m);
+  if (need > 0 && (!workspace || !aligned(workspace, 16) || workspace_bytes < need)) return MAESTRO_ERR_WORKSPACE;
   const int64_t r_lo = (int64_t)floor(q_lo * (double)(m - 1));
   const int64_t r_hi = (int64_t)ceil(q_hi * (double)(m - 1));
-  return maestro::launch_quantiles(values, m, r_lo, r_hi, out, as_stream(stream));
+  return maestro::launch_quantiles(values, m, r_lo, r_hi, out, workspace, as_stream(stream));
 }
 
 maestro_status maestro_prioritize(int32_t n_workflows, int64_t n_stages,

@@ -517,14 +517,9 @@ void fitness_kernel(
 // are counted into one 256-bin histogram per rank; eight wavefronts scan the two histograms
 // (64 bins each, cross-lane), and the one bin whose count range holds the rank takes it. A
 // window's values often share their leading digits, which would serialise the LDS atomics on
-// one bin: a wavefront whose counted lanes all carry the same digit adds their count once, and
-// long inputs count into 64 per-lane copies of each histogram (lane l of every wavefront into
-// copy l; copies 257 words apart, so one bin of different copies sits in different banks), so
-// that no two lanes of one atomic ever add to the same word; the copies are summed per bin.
+// one bin: a wavefront whose counted lanes all carry the same digit adds their count once.
+// Short inputs: one workgroup does every pass. Long ones: below.
 constexpr int kSelectThreads = 1024;
-constexpr int kSelectUnroll = 8;          // values per thread per step of the per-lane path
-constexpr int kCopyStride = 257;
-constexpr int64_t kPerLaneMin = 32768;    // inputs at least this long take the per-lane copies
 
 __device__ __forceinline__ void count_digit(uint32_t* hist, bool want, uint32_t dgt, int lane) {
   const uint64_t act = __ballot(want);
@@ -542,7 +537,6 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
                                                                   int64_t r_lo, int64_t r_hi,
                                                                   float* __restrict__ out, int n_out) {
   __shared__ uint32_t hist[2][256];
-  __shared__ uint32_t hcopy[2][64 * kCopyStride];
   __shared__ uint32_t scan[2][256];   // inclusive prefix within each 64-bin segment
   __shared__ uint32_t seg[2][4];      // segment totals
   __shared__ uint32_t s_prefix[2][2];   // [pass parity][rank]: read in one pass, written for the next
@@ -554,47 +548,17 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
   }
   uint32_t mask = 0;
   int par = 0;
-  const bool per_lane = m >= kPerLaneMin;
-  const int n_hist = n_out > 1 ? 2 : 1;
   for (int shift = 24; shift >= 0; shift -= 8, par ^= 1) {
     for (int i = tid; i < 512; i += kSelectThreads) (&hist[0][0])[i] = 0;
-    if (per_lane)
-      for (int i = tid; i < n_hist * 64 * kCopyStride; i += kSelectThreads) (&hcopy[0][0])[i] = 0;
     __syncthreads();
     const uint32_t p0 = s_prefix[par][0], p1 = s_prefix[par][1];
-    if (per_lane) {
-      for (int64_t i0 = 0; i0 < m; i0 += (int64_t)kSelectThreads * kSelectUnroll) {
-        uint32_t u[kSelectUnroll];
-        bool in[kSelectUnroll];
-#pragma unroll
-        for (int q = 0; q < kSelectUnroll; ++q) {   // every load issued before any count
-          const int64_t i = i0 + (int64_t)q * kSelectThreads + tid;
-          in[q] = i < m;
-          u[q] = in[q] ? float_key(v[i]) : 0u;
-        }
-#pragma unroll
-        for (int q = 0; q < kSelectUnroll; ++q) {
-          const uint32_t dgt = (u[q] >> shift) & 255u;
-          if (in[q] && (u[q] & mask) == p0) atomicAdd(&hcopy[0][lane * kCopyStride + dgt], 1u);
-          if (n_out > 1 && in[q] && (u[q] & mask) == p1) atomicAdd(&hcopy[1][lane * kCopyStride + dgt], 1u);
-        }
-      }
-      __syncthreads();
-      for (int i = tid; i < n_hist * 256; i += kSelectThreads) {
-        const int h = i >> 8, b = i & 255;
-        uint32_t t = 0;
-        for (int l = 0; l < 64; ++l) t += hcopy[h][l * kCopyStride + b];
-        hist[h][b] = t;
-      }
-    } else {
-      for (int64_t i0 = 0; i0 < m; i0 += kSelectThreads) {   // uniform trip count: whole-wave ballots
-        const int64_t i = i0 + tid;
-        const bool in = i < m;
-        const uint32_t u = in ? float_key(v[i]) : 0u;
-        const uint32_t dgt = (u >> shift) & 255u;
-        count_digit(hist[0], in && (u & mask) == p0, dgt, lane);
-        if (n_out > 1) count_digit(hist[1], in && (u & mask) == p1, dgt, lane);
-      }
+    for (int64_t i0 = 0; i0 < m; i0 += kSelectThreads) {   // uniform trip count: whole-wave ballots
+      const int64_t i = i0 + tid;
+      const bool in = i < m;
+      const uint32_t u = in ? float_key(v[i]) : 0u;
+      const uint32_t dgt = (u >> shift) & 255u;
+      count_digit(hist[0], in && (u & mask) == p0, dgt, lane);
+      if (n_out > 1) count_digit(hist[1], in && (u & mask) == p1, dgt, lane);
     }
     __syncthreads();
     if (wave < 8) {
@@ -624,6 +588,118 @@ __global__ __launch_bounds__(kSelectThreads) void quantile_kernel(const float* _
     __syncthreads();
   }
   if (tid < n_out) out[tid] = key_float(s_prefix[par][tid]);
+}
+
+// Long inputs: the same four 8-bit passes over several workgroups. Per pass, kSelBlocks
+// workgroups each count the digits of the candidates (the values that match a rank's prefix so
+// far) of a contiguous range into histograms of their own in the workspace, and one workgroup
+// sums them per bin, finds the bin that holds each rank and narrows the rank's prefix for the
+// next pass (state in the workspace). No atomics outside LDS and no waiting across workgroups.
+constexpr int kSelBlocks = 256;
+constexpr int64_t kMultiSelectMin = 32768;   // inputs at least this long take the multi-workgroup passes
+struct SelectState {
+  uint32_t prefix[2];
+  int64_t rank[2];
+};
+
+size_t select_workspace_bytes(int64_t m) {
+  return m >= kMultiSelectMin ? (size_t)kSelBlocks * 512 * sizeof(uint32_t) + 256 : 0;
+}
+
+__device__ __forceinline__ uint32_t select_mask(int shift) {
+  return shift == 24 ? 0u : ~((1u << (shift + 8)) - 1u);
+}
+
+__global__ __launch_bounds__(kSelectThreads) void select_hist_kernel(const float* __restrict__ v, int64_t m,
+                                                                     int shift, int n_hist,
+                                                                     const SelectState* __restrict__ st,
+                                                                     uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[2][256];
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int i = tid; i < 512; i += kSelectThreads) (&h[0][0])[i] = 0;
+  __syncthreads();
+  const uint32_t mask = select_mask(shift);
+  const uint32_t p0 = shift == 24 ? 0u : st->prefix[0], p1 = shift == 24 ? 0u : st->prefix[1];
+  const int64_t per = (m + gridDim.x - 1) / gridDim.x;
+  const int64_t b0 = (int64_t)blockIdx.x * per, b1 = min(m, b0 + per);
+  for (int64_t i0 = b0; i0 < b1; i0 += kSelectThreads) {   // workgroup-uniform trip count: whole-wave ballots
+    const int64_t i = i0 + tid;
+    const bool in = i < b1;
+    const uint32_t u = in ? float_key(v[i]) : 0u;
+    const uint32_t dgt = (u >> shift) & 255u;
+    count_digit(h[0], in && (u & mask) == p0, dgt, lane);
+    if (n_hist > 1) count_digit(h[1], in && (u & mask) == p1, dgt, lane);
+  }
+  __syncthreads();
+  for (int i = tid; i < 512; i += kSelectThreads) hist[(int64_t)blockIdx.x * 512 + i] = (&h[0][0])[i];
+}
+
+// one workgroup: bin totals over the kSelBlocks histograms, the bin of each rank, the state for
+// the next pass; after the last pass (shift 0) the selected values
+__global__ __launch_bounds__(kSelectThreads) void select_pick_kernel(const uint32_t* __restrict__ hist, int shift,
+                                                                     int n_out, int64_t r_lo, int64_t r_hi,
+                                                                     SelectState* __restrict__ st,
+                                                                     float* __restrict__ out) {
+  __shared__ uint32_t tot[2][2][256];   // [half of the workgroups][histogram][bin]
+  __shared__ uint32_t scan[2][256];
+  __shared__ uint32_t seg[2][4];
+  __shared__ uint32_t s_prefix[2];
+  __shared__ int64_t s_rank[2];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (tid < 2) {
+    s_prefix[tid] = shift == 24 ? 0u : st->prefix[tid];
+    s_rank[tid] = shift == 24 ? (tid ? r_hi : r_lo) : st->rank[tid];
+  }
+  {   // thread (half, histogram, bin): the sum over its half of the workgroups, loads in batches
+    const int half = tid >> 9, hb = tid & 511;
+    uint32_t t = 0;
+    for (int b = half * (kSelBlocks / 2); b < (half + 1) * (kSelBlocks / 2); b += 16) {
+      uint32_t c[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) c[u] = hist[(int64_t)(b + u) * 512 + hb];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) t += c[u];
+    }
+    (&tot[half][0][0])[hb] = t;
+  }
+  __syncthreads();
+  if (wave < 8) {
+    const int hh = wave >> 2, b = (wave & 3) * 64 + lane;
+    uint32_t x = tot[0][hh][b] + tot[1][hh][b];
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    scan[hh][b] = x;
+    if (lane == 63) seg[hh][wave & 3] = x;
+  }
+  __syncthreads();
+  if (tid < 512) {
+    const int hh = tid >> 8, b = tid & 255;
+    const int hsrc = n_out > 1 ? hh : 0;   // one rank: both slots follow histogram 0
+    uint32_t incl = scan[hsrc][b];
+    for (int q = 0; q < (b >> 6); ++q) incl += seg[hsrc][q];
+    const uint32_t c = tot[0][hsrc][b] + tot[1][hsrc][b];
+    const int64_t r = s_rank[hh];
+    if (r >= (int64_t)(incl - c) && r < (int64_t)incl) {   // exactly one bin per rank
+      st->rank[hh] = r - (int64_t)(incl - c);
+      st->prefix[hh] = s_prefix[hh] | ((uint32_t)b << shift);
+      if (shift == 0 && hh < n_out) out[hh] = key_float(s_prefix[hh] | (uint32_t)b);
+    }
+  }
+}
+
+maestro_status launch_select(const float* v, int64_t m, int64_t r_lo, int64_t r_hi, float* out, int n_out,
+                             void* workspace, hipStream_t stream) {
+  uint32_t* hist = static_cast<uint32_t*>(workspace);
+  SelectState* st = reinterpret_cast<SelectState*>(static_cast<unsigned char*>(workspace) +
+                                                   (size_t)kSelBlocks * 512 * sizeof(uint32_t));
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    select_hist_kernel<<<dim3(kSelBlocks), dim3(kSelectThreads), 0, stream>>>(v, m, shift, n_out, st, hist);
+    select_pick_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(hist, shift, n_out, r_lo, r_hi, st, out);
+  }
+  return launch_status();
 }
 
 // EWMA of the relative underestimation e_i = max(0, actual_i / pred_i - 1) in arrival order,
@@ -923,14 +999,17 @@ maestro_status launch_degradation_plans(int32_t n_nodes, const int32_t* engine_o
   return launch_status();
 }
 
+size_t quantiles_workspace_bytes(int64_t m) { return select_workspace_bytes(m); }
+
 maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
-                                hipStream_t stream) {
+                                void* workspace, hipStream_t stream) {
+  if (m >= kMultiSelectMin) return launch_select(values, m, r_lo, r_hi, out, 2, workspace, stream);
   quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(values, m, r_lo, r_hi, out, 2);
   return launch_status();
 }
 
 maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
-                                   int64_t rank, float* ewma, float* rho, hipStream_t stream) {
+                                   int64_t rank, float* ewma, float* rho, void* workspace, hipStream_t stream) {
   const int64_t n_tiles = (m + kEwmaTile - 1) / kEwmaTile;
   if (n_tiles <= kEwmaOneGroupTiles) {
     ewma_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(kv_actual, kv_pred, m, beta, ewma);
@@ -945,6 +1024,7 @@ maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pre
   }
   maestro_status st = launch_status();
   if (st != MAESTRO_OK) return st;
+  if (m >= kMultiSelectMin) return launch_select(ewma, m, rank, rank, rho, 1, workspace, stream);
   quantile_kernel<<<dim3(1), dim3(kSelectThreads), 0, stream>>>(ewma, m, rank, rank, rho, 1);
   return launch_status();
 }

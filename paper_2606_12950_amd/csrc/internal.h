@@ -44,6 +44,15 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
                             int32_t algo, int32_t* node_idx, float* score, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
 size_t route_workspace_bytes(int64_t n, int32_t n_models, int32_t n_nodes, int32_t k);
+// the sorted route in two halves: per-model node lists, then the walk of every stage
+size_t route_lists_bytes(int32_t n_models, int32_t n_nodes);
+maestro_status launch_sort_nodes(int32_t n_models, int32_t n_nodes, const double* free_bytes, const float* queue_s,
+                                 const float* cold_s, const uint64_t* resident_mask, const float* act_matrix,
+                                 void* lists, hipStream_t stream);
+maestro_status launch_route_walk(int64_t n, const int32_t* model_id, const float* pred_len, const double* kv_bytes,
+                                 const float* decode_s_per_token, int32_t n_models, int32_t n_nodes,
+                                 const void* lists, double rho, int32_t k, int32_t* node_idx, float* score,
+                                 hipStream_t stream);
 
 // Routing by fitness (Eq. 5) and the window bounds of its normalisation.
 constexpr int kMaxFitnessSources = 16;
@@ -63,9 +72,10 @@ maestro_status launch_activation_latency(int32_t n_nodes, int32_t n_models, cons
                                          const double* model_bytes, const double* tier_bw,
                                          const float* tier_setup, double unit, float* act, hipStream_t stream);
 maestro_status launch_adaptive_rho(const double* kv_actual, const double* kv_pred, int64_t m, double beta,
-                                   int64_t rank, float* ewma, float* rho, hipStream_t stream);
+                                   int64_t rank, float* ewma, float* rho, void* workspace, hipStream_t stream);
 maestro_status launch_quantiles(const float* values, int64_t m, int64_t r_lo, int64_t r_hi, float* out,
-                                hipStream_t stream);
+                                void* workspace, hipStream_t stream);
+size_t quantiles_workspace_bytes(int64_t m);
 
 // Prioritisation: chain suffix sums, slack keys, stable radix sort.
 maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,

@@ -158,22 +158,51 @@ int choose_g_log2(int64_t n, int32_t n_nodes) {
 // sorted per-model node lists + early-exit walk
 // ---------------------------------------------------------------------------------------------
 
-constexpr int kSortMax = 8192;            // nodes sortable in one workgroup's LDS (64 KB of keys)
-constexpr int kSortThreads = 1024;
+constexpr int kSortMax = 8192;            // nodes sortable in one workgroup (64 KB of keys in LDS)
 
-struct NodeEntry {                        // 16 bytes: one node in a model's ready-time order
+struct __align__(16) NodeEntry {          // 16 bytes: one node in a model's ready-time order
   float ready;                            // fl32(T_q + T_act) for this model
   int32_t node;
   double free;                            // KV admission headroom
 };
 
-__global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  const int lo = __shfl_xor((int)(uint32_t)v, mask), hi = __shfl_xor((int)(uint32_t)(v >> 32), mask);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// compare-exchange of a thread's keys j and j + S (S < IPT) in a bitonic stage of block `size`
+template <int IPT, int S>
+__device__ __forceinline__ void sort_in_thread(uint64_t (&key)[IPT], int base, int size) {
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    if ((j & S) == 0) {
+      const bool up = ((base + j) & size) == 0;
+      const uint64_t a = key[j], b = key[j + S];
+      const bool swap = (a > b) == up;
+      key[j] = swap ? b : a;
+      key[j + S] = swap ? a : b;
+    }
+  }
+}
+
+// One workgroup per model sorts the keys (ready time, node) of every node -- bitonic network
+// over `padded` (a power of two, 64 .. 8192) keys, IPT consecutive keys per thread. Compare-
+// exchange stages whose partners are a thread's own keys run in registers, those within a
+// wavefront through cross-lane shuffles, and only strides that cross wavefronts go through LDS
+// with a barrier per stage (10 of the 78 stages for 4,096 nodes). LDS: `padded` keys, dynamic.
+template <int IPT>
+__global__ __launch_bounds__(1024) void sort_nodes_kernel(
     int32_t n_nodes, int32_t padded, int32_t n_models, const float* __restrict__ queue_s,
     const float* __restrict__ cold_s, const uint64_t* __restrict__ resident_mask,
     const float* __restrict__ act_matrix, const double* __restrict__ free_bytes, NodeEntry* __restrict__ lists) {
-  __shared__ uint64_t key[kSortMax];
-  const int m = blockIdx.x, tid = threadIdx.x;
-  for (int i = tid; i < padded; i += kSortThreads) {
+  extern __shared__ uint64_t s_key[];
+  const int m = blockIdx.x, t = threadIdx.x, nt = blockDim.x;
+  const int base = t * IPT;   // position of this thread's first key
+  uint64_t key[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int i = base + j;
     if (i < n_nodes) {
       const float q = queue_s[i];
       float ready;
@@ -183,53 +212,75 @@ __global__ __launch_bounds__(kSortThreads) void sort_nodes_kernel(
         const bool res = (resident_mask[i] >> m) & 1u;
         ready = res ? __fadd_rn(q, 0.0f) : __fadd_rn(q, cold_s[i]);
       }
-      key[i] = ((uint64_t)float_key(ready) << 32) | (uint32_t)i;
+      key[j] = ((uint64_t)float_key(ready) << 32) | (uint32_t)i;
     } else {
-      key[i] = ~0ull;                     // padding sorts last
+      key[j] = ~0ull;                     // padding sorts last
     }
   }
-  __syncthreads();
-  // bitonic sort, ascending
   for (int size = 2; size <= padded; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < padded / 2; i += kSortThreads) {
-        const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
-        const bool up = (lo & size) == 0;
-        const uint64_t a = key[lo], b = key[hi];
-        if ((a > b) == up) { key[lo] = b; key[hi] = a; }
-      }
+    int stride = size >> 1;
+    if (stride >= IPT * 64) {   // partners in other wavefronts: through LDS
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) s_key[base + j] = key[j];
       __syncthreads();
+      for (; stride >= IPT * 64; stride >>= 1) {
+        for (int q = t; q < padded / 2; q += nt) {
+          const int lo = 2 * q - (q & (stride - 1)), hi = lo + stride;
+          const bool up = (lo & size) == 0;
+          const uint64_t a = s_key[lo], b = s_key[hi];
+          if ((a > b) == up) {
+            s_key[lo] = b;
+            s_key[hi] = a;
+          }
+        }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) key[j] = s_key[base + j];
+      __syncthreads();   // every thread has its keys back before the LDS is written again
     }
+    for (; stride >= IPT; stride >>= 1) {   // partner: the same slot of lane ^ (stride / IPT)
+      const int lx = stride / IPT;
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) {
+        const uint64_t other = shfl_xor_u64(key[j], lx);
+        const int p = base + j;
+        const bool keep_min = ((p & stride) == 0) == ((p & size) == 0);
+        key[j] = keep_min ? (key[j] < other ? key[j] : other) : (key[j] < other ? other : key[j]);
+      }
+    }
+    if (IPT >= 8 && stride == 4) { sort_in_thread<IPT, (IPT >= 8 ? 4 : 0)>(key, base, size); stride = 2; }
+    if (IPT >= 4 && stride == 2) { sort_in_thread<IPT, (IPT >= 4 ? 2 : 0)>(key, base, size); stride = 1; }
+    if (IPT >= 2 && stride == 1) sort_in_thread<IPT, (IPT >= 2 ? 1 : 0)>(key, base, size);
   }
   NodeEntry* out = lists + (size_t)m * n_nodes;
-  for (int j = tid; j < n_nodes; j += kSortThreads) {
-    const uint64_t k = key[j];
-    NodeEntry e;
-    e.ready = key_float((uint32_t)(k >> 32));
-    e.node = (int32_t)(uint32_t)k;
-    e.free = free_bytes[e.node];
-    out[j] = e;
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int p = base + j;
+    if (p < n_nodes) {
+      NodeEntry e;
+      e.ready = key_float((uint32_t)(key[j] >> 32));
+      e.node = (int32_t)(uint32_t)key[j];
+      e.free = free_bytes[e.node];
+      out[p] = e;
+    }
   }
 }
 
 // The first kWalkHead entries of every model's list are staged in LDS by the whole workgroup
 // (while each thread's own inputs are in flight), so a walk that ends early never waits on a
-// dependent global load.
+// dependent global load. One workgroup per 256 stages: a persistent grid that staged the heads
+// once per workgroup, and a walk split into a loop over the head and one over the rest of the
+// list, were both slower (120 and 110 us against 94 us per c4 route call on one box).
 constexpr int kWalkHead = 8;
 
+// one stage's walk down its model's list
 template <int KT>
-__global__ __launch_bounds__(kThreads) void walk_route_kernel(
-    int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
+__device__ __forceinline__ void walk_stage(
+    int64_t i, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
     const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_models,
-    int32_t n_nodes, const NodeEntry* __restrict__ lists, double rho, int32_t k, int32_t* __restrict__ node_idx,
-    float* __restrict__ score) {
-  __shared__ NodeEntry s_head[kMaxMatrixModels * kWalkHead];
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int head = n_nodes < kWalkHead ? n_nodes : kWalkHead;
-  for (int e = threadIdx.x; e < n_models * head; e += kThreads)
-    s_head[(e / head) * kWalkHead + e % head] = lists[(size_t)(e / head) * n_nodes + e % head];
-  __syncthreads();
-  if (i >= n) return;
+    int32_t n_nodes, const NodeEntry* __restrict__ lists, const NodeEntry* s_head, int head, double rho, int32_t k,
+    int32_t* __restrict__ node_idx, float* __restrict__ score) {
   const int32_t m = model_id[i];
   if ((uint32_t)m >= (uint32_t)n_models) {   // a model id out of range: no node
     for (int t = 0; t < k; ++t) {
@@ -240,25 +291,62 @@ __global__ __launch_bounds__(kThreads) void walk_route_kernel(
   }
   const double need = (rho == 0.0) ? kv_bytes[i] : __dmul_rn(kv_bytes[i], 1.0 + rho);
   const float exec_s = __fmul_rn(pred_len[i], decode_s_per_token[m]);
-  const NodeEntry* list = lists + (size_t)m * n_nodes;
-  const NodeEntry* lhead = s_head + m * kWalkHead;
   TopK<KT> best;
   best.init();
-  for (int32_t j = 0; j < n_nodes; ++j) {
-    const NodeEntry e = j < head ? lhead[j] : list[j];
-    if (!(need <= e.free)) continue;                       // infeasible: skip, keep walking
+  // one list entry; true when the walk stops there
+  auto visit = [&](const NodeEntry& e) {
+    if (!(need <= e.free)) return false;                   // infeasible: skip, keep walking
     const float sc = __fadd_rn(e.ready, exec_s);
-    if (best.n[KT - 1] != kNoNode && sc > best.s[KT - 1]) break;   // no later node can enter
+    if (best.n[KT - 1] != kNoNode && sc > best.s[KT - 1]) return true;   // no later node can enter
     best.push_lex(sc, e.node);
+    return false;
+  };
+  const NodeEntry* lhead = s_head + m * kWalkHead;
+  const NodeEntry* list = lists + (size_t)m * n_nodes;
+  for (int32_t j = 0; j < n_nodes; ++j)
+    if (visit(j < head ? lhead[j] : list[j])) break;
+  int32_t outn[KT];
+  float outs[KT];
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    const bool some = best.n[t] != kNoNode;
+    outn[t] = some ? best.n[t] : -1;
+    outs[t] = some ? best.s[t] : INFINITY;
+  }
+  if ((KT == 2 || KT == 4) && k == KT && ((uintptr_t)(node_idx + i * k) % (4 * KT)) == 0 &&
+      ((uintptr_t)(score + i * k) % (4 * KT)) == 0) {   // whole rows as one vector store each
+    if constexpr (KT == 4) {
+      *reinterpret_cast<int4*>(node_idx + i * k) = make_int4(outn[0], outn[1], outn[2], outn[3]);
+      *reinterpret_cast<float4*>(score + i * k) = make_float4(outs[0], outs[1], outs[2], outs[3]);
+    } else if constexpr (KT == 2) {
+      *reinterpret_cast<int2*>(node_idx + i * k) = make_int2(outn[0], outn[1]);
+      *reinterpret_cast<float2*>(score + i * k) = make_float2(outs[0], outs[1]);
+    }
+    return;
   }
 #pragma unroll
   for (int t = 0; t < KT; ++t) {
     if (t < k) {
-      const bool some = best.n[t] != kNoNode;
-      node_idx[i * k + t] = some ? best.n[t] : -1;
-      score[i * k + t] = some ? best.s[t] : INFINITY;
+      node_idx[i * k + t] = outn[t];
+      score[i * k + t] = outs[t];
     }
   }
+}
+
+template <int KT>
+__global__ __launch_bounds__(kThreads) void walk_route_kernel(
+    int64_t n, const int32_t* __restrict__ model_id, const float* __restrict__ pred_len,
+    const double* __restrict__ kv_bytes, const float* __restrict__ decode_s_per_token, int32_t n_models,
+    int32_t n_nodes, const NodeEntry* __restrict__ lists, double rho, int32_t k, int32_t* __restrict__ node_idx,
+    float* __restrict__ score) {
+  __shared__ NodeEntry s_head[kMaxMatrixModels * kWalkHead];
+  const int head = n_nodes < kWalkHead ? n_nodes : kWalkHead;
+  for (int e = threadIdx.x; e < n_models * head; e += kThreads)
+    s_head[(e / head) * kWalkHead + e % head] = lists[(size_t)(e / head) * n_nodes + e % head];
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) walk_stage<KT>(i, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes, lists, s_head,
+                            head, rho, k, node_idx, score);
 }
 
 size_t sorted_lists_bytes(int32_t n_models, int32_t n_nodes) {
@@ -273,6 +361,53 @@ bool prefer_sorted(int64_t n, int32_t n_models, int32_t n_nodes) {
 }
 
 }  // namespace
+
+size_t route_lists_bytes(int32_t n_models, int32_t n_nodes) {
+  return sorted_possible(n_nodes) ? sorted_lists_bytes(n_models, n_nodes) : 0;
+}
+
+maestro_status launch_sort_nodes(int32_t n_models, int32_t n_nodes, const double* free_bytes, const float* queue_s,
+                                 const float* cold_s, const uint64_t* resident_mask, const float* act_matrix,
+                                 void* lists, hipStream_t stream) {
+  if (!sorted_possible(n_nodes)) return MAESTRO_ERR_UNSUPPORTED;
+  int padded = 64;
+  while (padded < n_nodes) padded <<= 1;
+  const int threads = padded < 1024 ? padded : 1024;   // a multiple of 64
+  const int ipt = padded / threads;                    // 1, 2, 4 or 8 keys per thread
+  const size_t lds = (size_t)padded * sizeof(uint64_t);
+  NodeEntry* out = static_cast<NodeEntry*>(lists);
+#define MAESTRO_SORT(IPT)                                                                                       \
+  sort_nodes_kernel<IPT><<<dim3(n_models), dim3(threads), lds, stream>>>(n_nodes, padded, n_models, queue_s, \
+                                                                         cold_s, resident_mask, act_matrix,  \
+                                                                         free_bytes, out)
+  if (ipt == 1) MAESTRO_SORT(1);
+  else if (ipt == 2) MAESTRO_SORT(2);
+  else if (ipt == 4) MAESTRO_SORT(4);
+  else MAESTRO_SORT(8);
+#undef MAESTRO_SORT
+  return launch_status();
+}
+
+maestro_status launch_route_walk(int64_t n, const int32_t* model_id, const float* pred_len, const double* kv_bytes,
+                                 const float* decode_s_per_token, int32_t n_models, int32_t n_nodes,
+                                 const void* lists, double rho, int32_t k, int32_t* node_idx, float* score,
+                                 hipStream_t stream) {
+  if (n == 0) return MAESTRO_OK;
+  const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
+  const NodeEntry* l = static_cast<const NodeEntry*>(lists);
+#define MAESTRO_WALK_KT(KT)                                                                                  \
+  walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,               \
+                                                             decode_s_per_token, n_models, n_nodes, l, rho, \
+                                                             k, node_idx, score)
+  if (k == 1) MAESTRO_WALK_KT(1);
+  else if (k == 2) MAESTRO_WALK_KT(2);
+  else if (k == 3) MAESTRO_WALK_KT(3);
+  else if (k == 4) MAESTRO_WALK_KT(4);
+  else if (k <= 8) MAESTRO_WALK_KT(8);
+  else MAESTRO_WALK_KT(16);
+#undef MAESTRO_WALK_KT
+  return launch_status();
+}
 
 size_t route_workspace_bytes(int64_t, int32_t n_models, int32_t n_nodes, int32_t) {
   return sorted_possible(n_nodes) ? sorted_lists_bytes(n_models, n_nodes) : 0;
@@ -293,21 +428,11 @@ maestro_status launch_route(int64_t n, const int32_t* model_id, const float* pre
   if (sorted) {
     if (!sorted_possible(n_nodes)) return MAESTRO_ERR_UNSUPPORTED;
     if (!workspace || workspace_bytes < sorted_lists_bytes(n_models, n_nodes)) return MAESTRO_ERR_WORKSPACE;
-    NodeEntry* lists = static_cast<NodeEntry*>(workspace);
-    int padded = 1;
-    while (padded < n_nodes) padded <<= 1;
-    sort_nodes_kernel<<<dim3(n_models), dim3(kSortThreads), 0, stream>>>(
-        n_nodes, padded, n_models, queue_s, cold_s, resident_mask, act_matrix, free_bytes, lists);
-    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
-#define MAESTRO_WALK_KT(KT)                                                                          walk_route_kernel<KT><<<grid, dim3(kThreads), 0, stream>>>(n, model_id, pred_len, kv_bytes,                                                                  decode_s_per_token, n_models, n_nodes, lists, rho,                                                             k, node_idx, score)
-    if (k == 1) MAESTRO_WALK_KT(1);
-    else if (k == 2) MAESTRO_WALK_KT(2);
-    else if (k == 3) MAESTRO_WALK_KT(3);
-    else if (k == 4) MAESTRO_WALK_KT(4);
-    else if (k <= 8) MAESTRO_WALK_KT(8);
-    else MAESTRO_WALK_KT(16);
-#undef MAESTRO_WALK_KT
-    return launch_status();
+    const maestro_status st = launch_sort_nodes(n_models, n_nodes, free_bytes, queue_s, cold_s, resident_mask,
+                                                act_matrix, workspace, stream);
+    if (st != MAESTRO_OK) return st;
+    return launch_route_walk(n, model_id, pred_len, kv_bytes, decode_s_per_token, n_models, n_nodes, workspace,
+                             rho, k, node_idx, score, stream);
   }
   const int gl = choose_g_log2(n, n_nodes);
   const int64_t stages_per_block = kThreads >> gl;

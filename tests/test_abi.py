@@ -30,7 +30,7 @@ def lib():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 22
     assert sorted(_native.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -140,6 +140,37 @@ def test_route_validation(lib):
     assert call(free=MISALIGNED) == INVALID
 
 
+def test_route_split_validation(lib):
+    # the node half and the stage half of the sorted route, rejected before any launch
+    assert lib.maestro_route_lists_bytes(8, 16) == 8 * 16 * 16
+    assert lib.maestro_route_lists_bytes(64, 8192) == 64 * 8192 * 16
+    assert lib.maestro_route_lists_bytes(8, 8193) == 0
+    assert lib.maestro_route_lists_bytes(0, 16) == 0 and lib.maestro_route_lists_bytes(65, 16) == 0
+    need = 8 * 16 * 16
+
+    def sort(n_models=8, n_nodes=16, free=FAKE, queue=FAKE, cold=FAKE, mask=FAKE, act=None, lists=FAKE16,
+             nbytes=need):
+        return lib.maestro_route_sort_nodes(n_models, n_nodes, free, queue, cold, mask, act, lists, nbytes, None)
+    assert sort(n_models=0) == INVALID and sort(n_models=65) == INVALID and sort(n_nodes=0) == INVALID
+    assert sort(free=None) == INVALID and sort(free=MISALIGNED) == INVALID and sort(queue=MISALIGNED4) == INVALID
+    assert sort(cold=None) == INVALID and sort(mask=MISALIGNED) == INVALID    # residency form incomplete
+    assert sort(lists=None) == WORKSPACE and sort(lists=MISALIGNED16) == WORKSPACE
+    assert sort(nbytes=need - 1) == WORKSPACE
+    assert sort(n_nodes=8193, nbytes=1 << 30) == UNSUPPORTED
+    assert sort(cold=None, mask=None, act=MISALIGNED4) == INVALID            # readiness form misaligned
+
+    def walk(n=10, n_models=8, n_nodes=16, k=1, rho=0.0, model=FAKE, lists=FAKE16, nbytes=need, dec=FAKE):
+        return lib.maestro_route_walk(n, model, FAKE, FAKE, dec, n_models, n_nodes, lists, nbytes, rho, k, FAKE,
+                                      FAKE, None)
+    assert walk(n=-1) == INVALID and walk(n_models=0) == INVALID and walk(n_nodes=0) == INVALID
+    assert walk(k=0) == INVALID and walk(k=17) == INVALID
+    assert walk(rho=-1.0) == INVALID and walk(rho=float("nan")) == INVALID
+    assert walk(model=None) == INVALID and walk(model=MISALIGNED4) == INVALID and walk(dec=None) == INVALID
+    assert walk(lists=None) == WORKSPACE and walk(nbytes=need - 16) == WORKSPACE
+    assert walk(n_nodes=9000, nbytes=1 << 30) == UNSUPPORTED
+    assert walk(n=1 << 38, nbytes=need) == UNSUPPORTED
+
+
 def test_route_tiered_validation(lib):
     def call(n=10, n_models=8, n_nodes=16, k=1, act=FAKE, algo=0, ws=None, ws_bytes=0):
         return lib.maestro_route_tiered(n, FAKE, FAKE, FAKE, FAKE, n_models, n_nodes, FAKE, FAKE, act, 0.0, k, algo,
@@ -181,7 +212,8 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert call(mask=MISALIGNED) == INVALID
     assert call(act=None, mask=None, mat=MISALIGNED4) == INVALID
     assert call(n=0, act=None, mask=None, mat=FAKE) == OK                     # a T_act matrix replaces both
-    q = lambda m=10, lo=0.05, hi=0.95, v=FAKE, out=FAKE: lib.maestro_quantiles(v, m, lo, hi, out, None)
+    q = lambda m=10, lo=0.05, hi=0.95, v=FAKE, out=FAKE, ws=None, wb=0: lib.maestro_quantiles(v, m, lo, hi, out, ws,
+                                                                                              wb, None)
     assert q(m=0) == INVALID
     assert q(lo=0.6, hi=0.5) == INVALID
     assert q(lo=-0.1) == INVALID
@@ -190,6 +222,13 @@ def test_route_fitness_and_quantiles_validation(lib):
     assert q(v=None) == INVALID
     assert q(out=MISALIGNED4) == INVALID
     assert q(m=1 << 32) == UNSUPPORTED
+    # long windows select over several workgroups in a workspace: 256 histograms of 512 words
+    need = lib.maestro_quantiles_workspace(32768)
+    assert lib.maestro_quantiles_workspace(32767) == 0 and need >= 256 * 512 * 4
+    assert lib.maestro_quantiles_workspace(0) == 0 and lib.maestro_quantiles_workspace(1 << 32) == 0
+    assert q(m=32768) == WORKSPACE
+    assert q(m=32768, ws=FAKE16, wb=need - 1) == WORKSPACE
+    assert q(m=32768, ws=MISALIGNED16, wb=need) == WORKSPACE
 
 
 def test_activation_latency_validation(lib):
@@ -208,8 +247,8 @@ def test_activation_latency_validation(lib):
 
 
 def test_adaptive_rho_validation(lib):
-    def call(m=100, beta=0.2, q=0.95, a=FAKE, p=FAKE, ew=FAKE, rho=FAKE):
-        return lib.maestro_adaptive_rho(a, p, m, beta, q, ew, rho, None)
+    def call(m=100, beta=0.2, q=0.95, a=FAKE, p=FAKE, ew=FAKE, rho=FAKE, ws=None, wb=0):
+        return lib.maestro_adaptive_rho(a, p, m, beta, q, ew, rho, ws, wb, None)
     assert call(m=0) == INVALID
     assert call(beta=0.0) == INVALID                                          # no weight on new errors
     assert call(beta=1.5) == INVALID
@@ -220,6 +259,8 @@ def test_adaptive_rho_validation(lib):
     assert call(p=MISALIGNED) == INVALID
     assert call(rho=MISALIGNED4) == INVALID
     assert call(m=1 << 32) == UNSUPPORTED
+    assert call(m=1 << 20) == WORKSPACE                                       # long windows need one
+    assert call(m=1 << 20, ws=FAKE16, wb=lib.maestro_quantiles_workspace(1 << 20) - 16) == WORKSPACE
 
 
 def test_degradation_plans_validation(lib):

@@ -78,6 +78,26 @@ def test_quantiles_match_oracle(m):
         assert got.view(np.uint32).tolist() == ref.view(np.uint32).tolist(), (lo, hi, got, ref)
 
 
+@pytest.mark.parametrize("m", [32768, 32769, (1 << 20) + 7])
+@pytest.mark.parametrize("kind", ["equal", "two", "zeros", "spread"])
+def test_quantiles_long_windows_degenerate(m, kind):
+    # windows of 32,768 values and more select over 256 workgroups: every pass with all
+    # candidates in one bin, two values, signed zeros, and a wide spread
+    rng = np.random.default_rng(m + len(kind))
+    if kind == "equal":
+        v = np.full(m, 3.25, np.float32)
+    elif kind == "two":
+        v = rng.choice(np.array([-1.5, 7.0], np.float32), m)
+    elif kind == "zeros":
+        v = rng.choice(np.array([-0.0, 0.0, 1e-30, -1e-30], np.float32), m)
+    else:
+        v = (rng.standard_normal(m) * 10.0 ** rng.integers(-20, 20, m)).astype(np.float32)
+    for lo, hi in [(0.05, 0.95), (0.0, 1.0), (0.5, 0.5)]:
+        got = gpu_quantiles(v, lo, hi)
+        ref = oracle.quantiles(v, lo, hi)
+        assert got.view(np.uint32).tolist() == ref.view(np.uint32).tolist(), (lo, hi, got, ref)
+
+
 @pytest.mark.parametrize("n,M_,n_src,k", [(1, 1, 1, 1), (257, 64, 3, 1), (1000, 1300, 5, 3),
                                           (3000, 512, 16, 16), (700, 2049, 2, 4)])
 def test_fitness_matches_oracle(n, M_, n_src, k):
