@@ -4,7 +4,10 @@
 //     workflow's chain from the last stage backwards, quantising every stage latency to integer
 //     microseconds (round half to even) and accumulating the suffix sums in int64 -- the
 //     remaining predicted time from each stage to the end of the chain. The stage latencies
-//     are loaded eight at a time, so a chain costs one memory round trip per eight stages. The
+//     are loaded eight at a time, so a chain costs one memory round trip per eight stages.
+//     Chains of more than 1,024 stages are instead scanned by the whole block, one after the
+//     other: 1,024-stage chunks from the end backwards, a block-wide exclusive scan of
+//     saturating sums per chunk plus the carry of the chunks after it. The
 //     remaining time at the workflow's cursor gives slack = deadline - now - remaining,
 //     clamped to int32. Integer sums are exact, so the result does not depend on the
 //     summation order. The block also counts the first radix digit of its tile.
@@ -64,6 +67,92 @@ __device__ __forceinline__ int64_t sat_sub(int64_t a, int64_t b) {
 }
 
 constexpr int kChainBatch = 8;                     // stage latencies loaded per round trip
+constexpr int64_t kLongChain = 1024;               // longer chains: the whole block scans them
+constexpr int kLongItems = 1;                      // stages per thread per chunk of a long chain (more
+                                                   // cost registers that every chain pays for)
+
+__device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int d) {
+  const int lo = __shfl_up((int)(uint32_t)v, d, 64), hi = __shfl_up((int)(uint32_t)((uint64_t)v >> 32), d, 64);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// exclusive scan of saturating int64 sums over the block's threads in thread order (sat_add is
+// associative: +inf absorbs, and no finite sum of a chain can overflow); returns the sum over
+// the threads before this one and, in *total, the block's. Uses wtot; consecutive calls must be
+// separated by a barrier.
+__device__ __forceinline__ int64_t block_exclusive_sat(int64_t x, int64_t* wtot, int64_t* total) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int64_t incl = x;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = shfl_up_i64(incl, d);
+    if (lane >= d) incl = sat_add(y, incl);
+  }
+  const int64_t prev = shfl_up_i64(incl, 1);
+  const int64_t excl = lane > 0 ? prev : 0;   // within the wavefront
+  if (lane == 63) wtot[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    int64_t t = lane < kTile / 64 ? wtot[lane] : 0;
+#pragma unroll
+    for (int d = 1; d < kTile / 64; d <<= 1) {
+      const int64_t y = shfl_up_i64(t, d);
+      if (lane >= d) t = sat_add(y, t);
+    }
+    if (lane < kTile / 64) wtot[lane] = t;   // inclusive over wavefronts
+  }
+  __syncthreads();
+  *total = wtot[kTile / 64 - 1];
+  return sat_add(wave > 0 ? wtot[wave - 1] : 0, excl);
+}
+
+// Suffix sums of one long chain [first, end) by the whole block: chunks of kTile * kLongItems
+// stages from the end backwards, thread t taking the chunk's stages from its end in reverse, so
+// that an inclusive scan in thread order gives each stage the sum of the stages at and after it
+// within the chunk; the chunks after it add their total (carry). kStaged: the quantised
+// latencies are read from LDS (stage_us, indexed from s_lo) and the suffix sums written back
+// there; otherwise stage_latency_s is quantised and the sums go to remaining_us (when given).
+// Returns, in every thread, the suffix sum at `head` (0 when head is past the chain).
+template <bool kStaged>
+__device__ int64_t long_chain_suffix(int64_t first, int64_t end, int64_t head, int64_t s_lo, int64_t* stage_us,
+                                     const float* __restrict__ stage_latency_s, int64_t* __restrict__ remaining_us,
+                                     int64_t* wtot, int64_t* s_head) {
+  const int tid = threadIdx.x;
+  if (tid == 0) *s_head = 0;
+  int64_t carry = 0;
+  for (int64_t cend = end; cend > first; cend -= (int64_t)kTile * kLongItems) {
+    int64_t v[kLongItems];
+    int64_t run = 0;
+#pragma unroll
+    for (int u = 0; u < kLongItems; ++u) {
+      const int64_t j = cend - 1 - ((int64_t)tid * kLongItems + u);
+      int64_t lat = 0;
+      if (j >= first) {
+        if constexpr (kStaged) lat = stage_us[j - s_lo];
+        else lat = latency_us(stage_latency_s[j]);
+      }
+      run = sat_add(lat, run);
+      v[u] = run;   // this thread's stages from its first (latest) one down to j
+    }
+    int64_t chunk_total;
+    const int64_t before = sat_add(carry, block_exclusive_sat(run, wtot, &chunk_total));   // later stages
+#pragma unroll
+    for (int u = 0; u < kLongItems; ++u) {
+      const int64_t j = cend - 1 - ((int64_t)tid * kLongItems + u);
+      if (j >= first) {
+        const int64_t suf = sat_add(before, v[u]);
+        if constexpr (kStaged) stage_us[j - s_lo] = suf;
+        else if (remaining_us) remaining_us[j] = suf;
+        if (j == head) *s_head = suf;
+      }
+    }
+    carry = sat_add(carry, chunk_total);
+    __syncthreads();   // wtot is reused by the next chunk; *s_head is final after the last one
+  }
+  const int64_t r = *s_head;
+  __syncthreads();   // every thread has read it before the next long chain resets it
+  return r;
+}
 
 // One block per sort tile, one workflow per thread; also writes the tile's counts of the
 // first digit. When the block's workflows span at most kStageCap stages (the usual case), the
@@ -92,13 +181,19 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
   }
   __syncthreads();
   uint32_t ukey = 0xFFFFFFFFu;   // tile padding: largest key, sorts after every real workflow
+  uint32_t long_mark = 0;        // top bit of vals[w]: a chain long_chain_kernel scans
   if (w < n_workflows) {
     const int64_t first = chain_offset[w], end = chain_offset[w + 1];
     int64_t cur = cursor ? (int64_t)cursor[w] : 0;
     if (cur < 0) cur = 0;
     const int64_t head = first + cur;
     int64_t suffix = 0, rem_head = 0;
-    if (staged) {
+    if (end - first > kLongChain) {
+      long_mark = 0x80000000u;   // left to long_chain_kernel, which replaces the placeholder key (rem_head 0)
+    } else if (staged) {
+      // not unrolled: chains are a few stages long, and the unrolled form's set-up (64-bit
+      // addresses of eight stages) costs more than the loop itself
+#pragma unroll 1
       for (int64_t j = end - 1; j >= first; --j) {
         suffix = sat_add(stage_us[j - s_lo], suffix);
         stage_us[j - s_lo] = suffix;
@@ -132,12 +227,86 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
     ukey = (uint32_t)key ^ 0x80000000u;   // order-preserving unsigned image
   }
   keys[w] = ukey;
-  vals[w] = (uint32_t)w;
+  vals[w] = (uint32_t)w | long_mark;
   atomicAdd(&hist[ukey & (kBuckets - 1)], 1u);
   __syncthreads();
   if (counts && tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
   if (staged && remaining_us) {
     for (int64_t j = s_lo + tid; j < s_hi; j += kTile) remaining_us[j] = stage_us[j - s_lo];
+  }
+}
+
+// The chains of more than kLongChain stages, after the chain kernel (which leaves them a
+// placeholder key and marks them in the top bit of their index in vals -- indices are below
+// 2^31): persistent workgroups take the chain kernel's 1024-workflow tiles in turn, find the
+// marked chains of a tile (clearing the mark), scan each with all their threads (long_chain_suffix;
+// remaining times written over whatever the chain kernel's LDS write-back left there), and give
+// the workflow its slack key; with small tiles they also move the tile's first-digit count
+// from the placeholder to the real key (one workgroup owns a tile, so no other touches those
+// counts). Kept out of the chain kernel: the registers of the scan there slowed every chain (by
+// half at 2^24 workflows); persistent, since one short-lived workgroup per tile cost more in
+// scheduling than the check itself.
+constexpr int kLongChainBlocks = 512;
+constexpr int kLongChainTilesPerCheck = 8;   // at most this many tiles' marks per barrier
+__global__ __launch_bounds__(kTile) void long_chain_kernel(
+    int32_t n_workflows, const int64_t* __restrict__ chain_offset, const float* __restrict__ stage_latency_s,
+    const int32_t* __restrict__ cursor, const int64_t* __restrict__ deadline_us, int64_t now_us,
+    int64_t* __restrict__ remaining_us, int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys,
+    uint32_t* __restrict__ vals, uint32_t* __restrict__ counts, int tiles_per_check) {
+  __shared__ int64_t wtot[kTile / 64];
+  __shared__ int64_t s_head_rem;
+  __shared__ int32_t s_long[kTile];
+  __shared__ int32_t s_n_long;
+  const int tid = threadIdx.x;
+  const int64_t n_tiles = ((int64_t)n_workflows + kTile - 1) / kTile;
+  const int kT = tiles_per_check;   // 1 .. kLongChainTilesPerCheck
+  for (int64_t t0 = (int64_t)blockIdx.x * kT; t0 < n_tiles; t0 += (int64_t)gridDim.x * kT) {   // workgroup-uniform
+    uint32_t marks = 0;   // bit i: this thread's workflow of tile t0 + i is marked
+#pragma unroll
+    for (int i = 0; i < kLongChainTilesPerCheck; ++i) {
+      const int64_t wi = (t0 + i) * kTile + tid;
+      if (i < kT && wi < n_workflows && (vals[wi] & 0x80000000u)) marks |= 1u << i;
+    }
+    if (__syncthreads_count(marks != 0) == 0) continue;   // the usual case: none in these tiles
+    for (int64_t tile = t0; tile < t0 + kT && tile < n_tiles; ++tile) {   // workgroup-uniform
+      const int64_t w = tile * kTile + tid;
+      const bool is_long = (marks >> (tile - t0)) & 1u;
+      if (tid == 0) s_n_long = 0;
+      if (__syncthreads_count(is_long) == 0) continue;
+      if (is_long) s_long[atomicAdd(&s_n_long, 1)] = tid;
+      __syncthreads();
+      const int n_long = s_n_long;
+      int64_t rem_head = 0;
+      for (int q = 0; q < n_long; ++q) {   // workgroup-uniform trip count
+        const int t = s_long[q];
+        const int64_t wl = tile * kTile + t;
+        const int64_t first = chain_offset[wl], end = chain_offset[wl + 1];
+        int64_t cur = cursor ? (int64_t)cursor[wl] : 0;
+        if (cur < 0) cur = 0;
+        const int64_t r = long_chain_suffix<false>(first, end, first + cur, 0, nullptr, stage_latency_s, remaining_us,
+                                                   wtot, &s_head_rem);
+        if (tid == t) rem_head = r;
+      }
+      if (is_long) {
+        int32_t key;
+        if (rem_head == kLatSat) {
+          key = INT32_MIN;
+        } else {
+          const int64_t slack = sat_sub(sat_sub(deadline_us[w], now_us), rem_head);
+          key = slack > INT32_MAX ? INT32_MAX : (slack < INT32_MIN ? INT32_MIN : (int32_t)slack);
+        }
+        slack_key[w] = key;
+        const uint32_t ukey = (uint32_t)key ^ 0x80000000u;
+        const uint32_t placeholder = keys[w];
+        keys[w] = ukey;
+        vals[w] = (uint32_t)w;
+        if (counts) {
+          atomicSub(&counts[tile * kBuckets + (placeholder & (kBuckets - 1))], 1u);
+          atomicAdd(&counts[tile * kBuckets + (ukey & (kBuckets - 1))], 1u);
+        }
+      }
+      __syncthreads();   // s_long and s_n_long are reused by the next tile
+    }
   }
 }
 
@@ -456,6 +625,16 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
   chain_kernel<<<dim3((unsigned)(L.padded / kTile)), dim3(kTile), 0, stream>>>(
       n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us,
       slack_key, keys[0], vals[0], L.fused ? counts : nullptr);
+  // one tile per workgroup while that fits kLongChainBlocks workgroups, more per barrier beyond
+  const int64_t chain_tiles = (n_workflows + (int64_t)kTile - 1) / kTile;
+  int tiles_per_check = 1;
+  while (tiles_per_check < kLongChainTilesPerCheck && chain_tiles > (int64_t)tiles_per_check * kLongChainBlocks)
+    tiles_per_check *= 2;
+  const int64_t chain_steps = (chain_tiles + tiles_per_check - 1) / tiles_per_check;
+  long_chain_kernel<<<dim3((unsigned)(chain_steps < kLongChainBlocks ? chain_steps : kLongChainBlocks)), dim3(kTile),
+                      0, stream>>>(
+      n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us, slack_key, keys[0],
+      vals[0], L.fused ? counts : nullptr, tiles_per_check);
   for (int pass = 0; pass < kPasses; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     const int shift = pass * kRadixBits;

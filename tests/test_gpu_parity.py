@@ -445,6 +445,40 @@ def test_prioritize_mixed_staging():
     assert_prio_equal(got, oracle.prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur))
 
 
+@pytest.mark.parametrize("case", ["staged", "unstaged", "cursors_inf", "mixed_blocks", "very_long"])
+def test_prioritize_block_scanned_long_chains(case):
+    # chains of more than 1,024 stages are scanned by the whole block (1,024-stage chunks from
+    # the end, saturating sums): inside a block staged in LDS, in one walking global memory,
+    # with cursors anywhere (also past the end) and infinite latencies at chunk edges, several
+    # in one block beside short ones, and one chain of 2^22 stages
+    rng = np.random.default_rng(len(case))
+    if case == "staged":            # 1,025 + 3,000 + short: the block's 8,192-stage range is staged
+        lens = np.concatenate([[1025, 3000], np.full(1022, 3)])
+    elif case == "unstaged":
+        lens = np.concatenate([[1024, 1025, 2047, 2048, 2049, 9000], rng.integers(0, 9, 1018)])
+    elif case == "cursors_inf":
+        lens = np.concatenate([[5000, 4097, 1536], rng.integers(0, 6, 2000)])
+    elif case == "mixed_blocks":
+        lens = np.concatenate([rng.integers(0, 9, 1500), [3000], rng.integers(0, 9, 600), [1100, 1100]])
+    else:
+        lens = np.array([1 << 22, 5, 0, 7])
+    lens = lens.astype(np.int64)
+    W_ = lens.size
+    off = np.zeros(W_ + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    S = int(off[-1])
+    lat = rng.uniform(0.0, 30.0, S).astype(np.float32)
+    cur = None
+    if case == "cursors_inf":
+        for j in (off[0] + 5000 - 1024, off[0] + 5000 - 1025, off[1] + 7, off[2] + 1535):
+            lat[j] = np.inf         # at chunk edges and inside
+        cur = rng.integers(0, 6000, W_).astype(np.int32)
+        cur[:3] = [1000, 4097, 0]   # inside, exactly at the end, at the start
+    dl = rng.integers(0, 10 ** 12, W_).astype(np.int64)
+    got = gpu_prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur)
+    assert_prio_equal(got, oracle.prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur))
+
+
 def test_prioritize_long_chain_and_empty():
     # one chain spanning every stage, then an empty batch
     S = 100000
