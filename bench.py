@@ -472,6 +472,63 @@ def margin_bench(steps: int, warmup: int):
     print(json.dumps(res), flush=True)
 
 
+def library_gemm_bench(name: str, steps: int, warmup: int):
+    """The vendor GEMM library (hipBLASLt through torch.mm, bfloat16) beside the fused predictor on
+    the same box: a large square GEMM, the predictor's three layers as separate library GEMMs on
+    the workload's batch, and the unfused three-layer network (library GEMMs with bias, ReLU by
+    torch, no length epilogue). It says how far the chip's MFMA throughput goes under its power
+    limit for plain dense products; the fused kernel is timed last, on the workload's own inputs.
+    One JSON line."""
+    import torch
+    import torch.nn.functional as F
+    from paper_2606_12950_amd import workload as W
+    torch.cuda.set_device(0)
+    torch.manual_seed(0)
+    wl = W.workload(name)
+    spec, n = wl.spec, wl.n
+    if spec.dtype != "bf16" or len(spec.dims) != 4:
+        raise SystemExit("--library-gemm compares the bfloat16 three-layer predictor (c1 .. c4)")
+    d0, d1, d2, d3 = spec.dims
+    res = {"library": "hipBLASLt via torch.mm, bf16", "workload": name, "gemms": []}
+
+    def rec(label, m, k, nn, fn):
+        ms = percentiles(_time_events(fn, steps, warmup))
+        fl = 2.0 * m * k * nn
+        res["gemms"].append({"shape": label, "m": m, "k": k, "n": nn, "ms": ms,
+                             "tflops": round(fl / (ms["mean"] * 1e-3) / 1e12, 1),
+                             "frac": round(fl / (ms["mean"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
+
+    a = torch.randn(16384, 16384, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(16384, 16384, device="cuda", dtype=torch.bfloat16)
+    rec("square 16384^3", 16384, 16384, 16384, lambda: torch.mm(a, b))
+    del a, b
+    x = torch.randn(n, d0, device="cuda", dtype=torch.bfloat16)
+    ws = [torch.randn(o, i, device="cuda", dtype=torch.bfloat16) * (1.0 / i) ** 0.5
+          for i, o in ((d0, d1), (d1, d2), (d2, d3))]
+    bs = [torch.zeros(o, device="cuda", dtype=torch.bfloat16) for o in (d1, d2, d3)]
+    h1 = F.relu(F.linear(x, ws[0], bs[0]))
+    h2 = F.relu(F.linear(h1, ws[1], bs[1]))
+    rec(f"layer 1 ({d0}->{d1})", n, d0, d1, lambda: F.linear(x, ws[0], bs[0]))
+    rec(f"layer 2 ({d1}->{d2})", n, d1, d2, lambda: F.linear(h1, ws[1], bs[1]))
+    rec(f"layer 3 ({d2}->{d3})", n, d2, d3, lambda: F.linear(h2, ws[2], bs[2]))
+    del h1, h2
+
+    def mlp():
+        h = F.relu(F.linear(x, ws[0], bs[0]))
+        h = F.relu(F.linear(h, ws[1], bs[1]))
+        return F.linear(h, ws[2], bs[2])
+    flop = mlp_flop_per_stage(spec.dims) * n
+    ms = percentiles(_time_events(mlp, max(1, steps // 2), warmup))
+    res["unfused_network"] = {"ms": ms, "frac": round(flop / (ms["mean"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    del x, ws, bs
+    torch.cuda.empty_cache()
+    st = time_step(wl, steps, warmup)
+    mp = float(np.mean(st["predict"]))
+    res["fused_predictor"] = {"ms": percentiles(st["predict"]),
+                              "frac": round(flop / (mp * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -499,10 +556,16 @@ def main():
                     help="time latency routing with T_act from readiness tiers (Sec. III-C, Eq. 6)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="time the vendor GEMM library (square and per-layer bf16 GEMMs, the unfused network) "
+                         "beside the fused predictor")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.library_gemm:
+        library_gemm_bench(args.workload, steps=max(2, min(args.steps, 20)), warmup=max(1, min(args.warmup, 3)))
         return
     if args.route_tiered:
         route_tiered_bench(args.workload, steps=max(1, min(args.steps, 50)), warmup=max(1, min(args.warmup, 5)))
