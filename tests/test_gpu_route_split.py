@@ -5,8 +5,8 @@ maestro_route_walk (each stage's k best feasible nodes from its model's list).
 Bars: the lists bit-exact against numpy's stable lexicographic sort of the definition's ready
 times fl32(T_q + T_act); the walk's node indices and score bits identical to the oracle's route
 and to maestro_route_ex with the sorted algorithm, also when one set of lists serves two batches.
-Node counts cover every keys-per-thread width of the sort (64 .. 8,192 keys padded to a power of
-two: 1, 2, 4 and 8 keys per thread) and non-powers of two.
+Node counts cover every launch shape of the sort (256 .. 8,192 positions, a power of two: 256, 512
+or 1,024 threads with 1 key each, then 2, 4 and 8 keys per thread) and non-powers of two.
 """
 import numpy as np
 import pytest
