@@ -472,6 +472,43 @@ def margin_bench(steps: int, warmup: int):
     print(json.dumps(res), flush=True)
 
 
+def mfma_ceiling_bench(steps: int, warmup: int, rounds: int = 20000):
+    """The chip's matrix-core ceilings: nothing but bfloat16 32x32x16 MFMAs on pseudo-random
+    operands, one wavefront per SIMD as the predictor runs, from the measurement-only
+    libmaestro_calibrate.so -- both operands in registers (a dependent accumulation chain, and four
+    independent accumulators), then the A operand read from LDS for every MFMA (the predictor's
+    LDS traffic with one row group) or for every second MFMA (two row groups). What the power limit
+    leaves of the 2.5 PFLOP/s datasheet figure with no global memory traffic or synchronisation.
+    One JSON line."""
+    import ctypes
+    import torch
+    from paper_2606_12950_amd import build as B
+    if not os.path.exists(B.CALIBRATE_LIB):
+        raise SystemExit(f"{B.CALIBRATE_LIB} is not built (python -m paper_2606_12950_amd.build)")
+    lib = ctypes.CDLL(B.CALIBRATE_LIB)
+    lib.maestro_calibrate_mfma.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_uint32, ctypes.c_void_p]
+    lib.maestro_calibrate_mfma.restype = ctypes.c_int
+    lib.maestro_calibrate_mfma_count.argtypes = [ctypes.c_int]
+    lib.maestro_calibrate_mfma_count.restype = ctypes.c_int64
+    torch.cuda.set_device(0)
+    out = torch.empty(lib.maestro_calibrate_mfma_outputs(), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    flop = lib.maestro_calibrate_mfma_count(rounds) * 32768.0
+    res = {"mfma_ceiling": "bf16 32x32x16, register operands, one wavefront per SIMD", "rounds": rounds,
+           "flop_per_launch": flop, "variants": []}
+    for n_acc, lds_every in ((1, 0), (4, 0), (1, 1), (1, 2)):
+        def call(n_acc=n_acc, lds_every=lds_every):
+            if lib.maestro_calibrate_mfma(ctypes.c_void_p(out.data_ptr()), rounds, n_acc, lds_every, 1, stream) != 0:
+                raise RuntimeError("maestro_calibrate_mfma failed")
+        ms = percentiles(_time_events(call, steps, warmup))
+        tf = flop / (ms["mean"] * 1e-3) / 1e12
+        res["variants"].append({"accumulators": n_acc,
+                                "a_operand": "registers" if lds_every == 0 else f"LDS, one read per {lds_every} MFMA",
+                                "ms": ms, "tflops": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4)})
+    print(json.dumps(res), flush=True)
+
+
 def library_gemm_bench(name: str, steps: int, warmup: int):
     """The vendor GEMM library (hipBLASLt through torch.mm, bfloat16) beside the fused predictor on
     the same box: a large square GEMM, the predictor's three layers as separate library GEMMs on
@@ -559,10 +596,15 @@ def main():
     ap.add_argument("--library-gemm", action="store_true",
                     help="time the vendor GEMM library (square and per-layer bf16 GEMMs, the unfused network) "
                          "beside the fused predictor")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="time the matrix-core ceiling kernel (register-only bf16 MFMAs)")
     args = ap.parse_args()
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.mfma_ceiling:
+        mfma_ceiling_bench(steps=max(2, min(args.steps, 20)), warmup=max(1, min(args.warmup, 3)))
         return
     if args.library_gemm:
         library_gemm_bench(args.workload, steps=max(2, min(args.steps, 20)), warmup=max(1, min(args.warmup, 3)))

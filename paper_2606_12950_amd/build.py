@@ -1,4 +1,5 @@
-"""Build libmaestro.so (gfx950) in-tree with hipcc.
+"""Build libmaestro.so (gfx950) in-tree with hipcc, and beside it libmaestro_calibrate.so, the
+measurement-only matrix-core ceiling kernel that bench.py --mfma-ceiling times.
 
 Usage: python -m paper_2606_12950_amd.build [-v]
 """
@@ -17,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmaestro.so")
 SOURCES = ("api.hip", "predict.hip", "roles.hip", "route.hip", "fitness.hip", "prioritize.hip")
+CALIBRATE_LIB = os.path.join(PKG, "libmaestro_calibrate.so")
+CALIBRATE_SOURCE = "calibrate.hip"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -57,15 +60,16 @@ def build(verbose: bool = False) -> str:
     if not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     with tempfile.TemporaryDirectory(prefix="maestro_build_") as tmp:
-        with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-            objs = list(ex.map(lambda s: _compile(s, tmp, verbose), SOURCES))
-        out = os.path.join(tmp, "libmaestro.so")
-        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out]
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True)
-        shutil.copyfile(out, LIB + ".tmp")
-        os.replace(LIB + ".tmp", LIB)
+        with ThreadPoolExecutor(max_workers=len(SOURCES) + 1) as ex:
+            objs = list(ex.map(lambda s: _compile(s, tmp, verbose), SOURCES + (CALIBRATE_SOURCE,)))
+        for lib, lib_objs in ((LIB, objs[:-1]), (CALIBRATE_LIB, objs[-1:])):
+            out = os.path.join(tmp, os.path.basename(lib))
+            cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *lib_objs, "-o", out]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            subprocess.run(cmd, check=True)
+            shutil.copyfile(out, lib + ".tmp")
+            os.replace(lib + ".tmp", lib)
     return LIB
 
 

@@ -20,6 +20,8 @@
 // blocks are being multiplied, and read by all four wavefronts with 16-byte LDS reads; with two
 // row groups every fragment read feeds one MFMA per group. Weight rows are padded by 16 bytes
 // in LDS so that the 16 rows a half-wavefront reads at one column fall in distinct banks.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace maestro {
@@ -208,11 +210,14 @@ __device__ __forceinline__ void role_row(float z0, float b0, float coef, float p
 //   layer-1 chunk j            : W1 rows 64j .. 64j+63 (two 32-neuron blocks), all D columns
 //   layer-2 chunk (b, p)       : W2 rows 32b .. 32b+31, columns 512p .. 512p+511, plus, for
 //                                the last p, W3 columns 32b .. 32b+31 of every bin row
-// Chunks rotate through kBufs LDS buffers and are fetched kBufs-1 chunks ahead (across tile
+// Chunks rotate through kBufs LDS buffers and are fetched kAhead chunks ahead (across tile
 // boundaries) by direct global->LDS loads, so every fetch overlaps the multiplication of
 // earlier chunks. Each wavefront waits only for the loads of the chunk needed next (counted
 // vmcnt), then the workgroup barrier publishes it. No other global load is in flight, so no
-// wait ever drains the prefetch.
+// wait ever drains the prefetch. With one row group the barrier sits inside the chain of MFMAs
+// (mfma_chain_handover) and the prefetch distance is 2, so that the buffer being refilled is two
+// chunks old and no wavefront can still be reading it; with two row groups the barrier follows
+// each chunk's MFMAs and the distance is 3.
 //
 // LDS layouts (all 16-byte reads are free of bank conflicts per quarter-wavefront):
 //   feature chunk: G = 1: 64 rows of 512 bytes, the 16-byte units of row r stored at
@@ -234,63 +239,49 @@ __device__ __forceinline__ int tile_row_neuron(int i) {
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// acc += sum_k A_k * B[k0 + k], A_k the 16-byte LDS fragment at (k & 4 ? pb : pa) + 32k (the
-// two bases absorb the layer-1 unit swizzle; pass pa == pb elsewhere). Fragments are read
-// kLookahead steps ahead of their MFMA. pre() -- the deferred epilogue of the previous block --
-// runs after the first fragment reads are issued, so that it fills their latency; side(k) is
-// issued right after MFMA k, while the matrix core is busy. The scheduling barriers keep
-// exactly this order.
-constexpr int kLookahead = 3;
-template <int KS, int NBREG, typename Pre, typename Side>
-__device__ __forceinline__ void mfma_chain(f32x16& acc, const unsigned char* pa, const unsigned char* pb,
-                                           const bf16x8 (&b)[NBREG], int k0, Pre&& pre, Side&& side) {
-  bf16x8 fr[KS];
-#pragma unroll
-  for (int k = 0; k < kLookahead && k < KS; ++k)
-    fr[k] = *reinterpret_cast<const bf16x8*>(((k & 4) ? pb : pa) + k * 32);
-  __builtin_amdgcn_sched_barrier(0);
-  pre();
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int k = 0; k < KS; ++k) {
-    if (k + kLookahead < KS) {
-      const int kk = k + kLookahead;
-      fr[kk] = *reinterpret_cast<const bf16x8*>(((kk & 4) ? pb : pa) + kk * 32);
-    }
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[k], b[k0 + k], acc, 0, 0, 0);
-    side(k);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
+constexpr int kLookahead = 3;            // fragment reads ahead of their MFMA (one row group)
 
-// Two 32-row blocks of one chunk multiplied together: step f feeds block f % 2 at K-step f / 2
-// (both blocks take the same B operand), so consecutive MFMAs never depend on each other and the
-// chunk has a single chain start. Block lb's fragment of K-step k is read from
-// (k & 4 ? pb[lb] : pa[lb]) + 32k, kLookahead steps ahead; pre() and side(f) as in mfma_chain.
-template <int KS, int NBREG, typename Pre, typename Side>
-__device__ __forceinline__ void mfma_chain_pair(f32x16& acc0, f32x16& acc1, const unsigned char* pa0,
-                                                const unsigned char* pb0, const unsigned char* pa1,
-                                                const unsigned char* pb1, const bf16x8 (&b)[NBREG],
-                                                Pre&& pre, Side&& side) {
-  constexpr int F = 2 * KS;
-  auto frag = [&](int f) {
-    const int k = f >> 1;
-    const unsigned char* base = (f & 1) ? ((k & 4) ? pb1 : pa1) : ((k & 4) ? pb0 : pa0);
-    return *reinterpret_cast<const bf16x8*>(base + k * 32);
-  };
-  bf16x8 fr[F];
+// One row group's chain of F MFMA steps over one LDS chunk, with the hand-over to the next chunk
+// folded in. fr holds the fragments (16-byte A operands) of steps 0 .. kLookahead-1 on entry
+// (read by the chain before, or by the caller); step f's fragment is cur(f), read kLookahead
+// steps ahead. At step F - kLookahead every fragment of this chunk has been requested: release()
+// lets the next chunk in (its loads waited for, the workgroup barrier crossed), and the remaining
+// lookahead reads fetch the next chain's first fragments through next(i), left in fr on return
+// (kNext). The barrier then overlaps the last MFMAs of this chain, and the next chain starts with
+// its first fragments already in flight. mma(f, fragment) issues step f's MFMA; pre() runs before
+// the first one, side(f) right after MFMA f, while the matrix core is busy (weight loads, the
+// pieces of the previous block's deferred epilogue); the scheduling barriers keep this order.
+// Measured on 4,194,304 stages (256-1024-1024-64): 8.45 against 8.57 ms with a barrier (and a
+// wait for the wavefront's own LDS reads) between the chains, outputs bit for bit the same;
+// reading 4 or 5 steps ahead instead of 3 changed nothing.
+template <int F, bool kNext, typename Cur, typename Next, typename Mma, typename Pre, typename Side,
+          typename Release>
+__device__ __forceinline__ void mfma_chain_handover(bf16x8 (&fr)[kLookahead], Cur&& cur, Next&& next, Mma&& mma,
+                                                    Pre&& pre, Side&& side, Release&& release) {
+  constexpr int LA = kLookahead;
+  static_assert(F > LA, "the hand-over lies inside the chain");
+  bf16x8 ring[F + LA];
 #pragma unroll
-  for (int f = 0; f < kLookahead && f < F; ++f) fr[f] = frag(f);
+  for (int f = 0; f < LA; ++f) ring[f] = fr[f];
   __builtin_amdgcn_sched_barrier(0);
   pre();
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int f = 0; f < F; ++f) {
-    if (f + kLookahead < F) fr[f + kLookahead] = frag(f + kLookahead);
-    if (f & 1) acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[f], b[f >> 1], acc1, 0, 0, 0);
-    else acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[f], b[f >> 1], acc0, 0, 0, 0);
+    if (f == F - LA) {
+      release();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int ff = f + LA;
+    if (ff < F) ring[ff] = cur(ff);
+    else if (kNext) ring[ff] = next(ff - F);
+    mma(f, ring[f]);
     side(f);
     __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (kNext) {
+#pragma unroll
+    for (int f = 0; f < LA; ++f) fr[f] = ring[F + f];
   }
 }
 
@@ -322,7 +313,7 @@ __device__ __forceinline__ bf16x8 relu_bf16(const f32x16& acc, int half) {
   return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
 }
 
-constexpr int kBufs = 4;                 // LDS chunk buffers (prefetch distance kBufs - 1)
+constexpr int kBufs = 4;                 // LDS chunk buffers
 constexpr int kDmaPerChunk = 8;          // direct loads per wavefront per chunk (at least)
 
 // Direct global->LDS loads through a raw buffer resource: lane l's 16 (or 4) bytes at byte offset
@@ -390,12 +381,27 @@ __device__ __forceinline__ void wait_chunk() {
   asm volatile("" ::: "memory");
 }
 
+// Wait until at most N vector-memory operations of this wavefront are outstanding (its own loads
+// of the chunk needed next have landed), then the workgroup barrier -- without waiting for this
+// wavefront's LDS reads, so that fragment reads issued ahead stay in flight across it.
+template <int N>
+__device__ __forceinline__ void release_chunk() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 constexpr int kMaxModels = 64;           // per-model KV bytes staged in LDS
 
 // acc[g] += sum_k A_k * b[g][k0 + k] for the G row groups of a wavefront: every weight fragment
 // read from LDS feeds G MFMAs, one per group (independent accumulators), so the LDS reads, their
-// waits and the weight traffic per MFMA drop by a factor G. Fragment addressing, pre() and side(k)
-// as in mfma_chain; fragments are read kLookaheadGroups K-steps ahead.
+// waits and the weight traffic per MFMA drop by a factor G. A_k is the 16-byte LDS fragment at
+// (k & 4 ? pb : pa) + 32k (the two bases absorb the layer-1 unit swizzle; pa == pb elsewhere),
+// read kLookaheadGroups K-steps ahead; pre() -- the deferred epilogue of the previous block --
+// runs after the first fragment reads are issued, so that it fills their latency, and side(k)
+// right after the MFMAs of step k; the scheduling barriers keep this order.
 constexpr int kLookaheadGroups = 2;
 template <int KS, int G, int NBREG, typename Pre, typename Side>
 __device__ __forceinline__ void mfma_chain_groups(f32x16 (&acc)[G], const unsigned char* pa,
@@ -466,10 +472,16 @@ void mlp3_bf16_kernel(
   constexpr int ROW2 = 1024 + 16;         // layer-2 chunk: bytes per row
   constexpr int W3OFF = 32 * ROW2;
   constexpr int CHUNK = cmax(cmax(64 * 512, 32 * PAIR), W3OFF + B * 64);
-  static_assert(NC >= kBufs - 1, "prologue fetches whole chunks of the first tile");
-  static_assert(NX + NC1 + kBufs - 1 <= NC, "feature and layer-1 prefetches stay within the tile");
+  // Prefetch distance in chunks. One row group hands each chunk over inside the chain (the
+  // barrier before the last MFMAs, no wait for its own LDS reads), so the buffer a new prefetch
+  // fills must be two chunks old: distance 2 of the 4 buffers. Two groups wait for their reads
+  // at the barrier after the chain, and prefetch 3 ahead.
+  constexpr int kAhead = G == 1 ? 2 : kBufs - 1;
+  static_assert(kAhead + 2 <= kBufs || G != 1, "the chunk a prefetch overwrites is two chunks old");
+  static_assert(NC >= kAhead, "prologue fetches whole chunks of the first tile");
+  static_assert(NX + NC1 + kAhead <= NC, "feature and layer-1 prefetches stay within the tile");
   static_assert(2 * KS1 == 32, "a layer-1 chunk is 32 MFMA steps");
-  static_assert(NB2 * KP >= kBufs - 1, "the peeled layer-2 blocks cover every wrapping prefetch");
+  static_assert(NB2 * KP >= kAhead, "the peeled layer-2 blocks cover every wrapping prefetch");
 
   __shared__ __attribute__((aligned(16))) unsigned char lds[kBufs * CHUNK];
   __shared__ __attribute__((aligned(16))) float s_b1[H1];
@@ -648,12 +660,17 @@ void mlp3_bf16_kernel(
   // chunk g of this workgroup's stream lives in buffer g % kBufs
   unsigned g = 0;
 #pragma unroll
-  for (int c = 0; c < kBufs - 1; ++c) fetch(first_tile, 0, c, lds + c * CHUNK);
-  wait_chunk<kDmaPerChunk * (kBufs - 2)>();
+  for (int c = 0; c < kAhead; ++c) fetch(first_tile, 0, c, lds + c * CHUNK);
+  wait_chunk<kDmaPerChunk * (kAhead - 1)>();
 
-  auto ahead = [&]() { return lds + ((g + kBufs - 1) % kBufs) * CHUNK; };
+  auto ahead = [&]() { return lds + ((g + kAhead) % kBufs) * CHUNK; };
   auto advance = [&]() {
-    wait_chunk<kDmaPerChunk * (kBufs - 2)>();
+    wait_chunk<kDmaPerChunk * (kAhead - 1)>();
+    ++g;
+  };
+  // the hand-over inside a chain (one row group)
+  auto release = [&]() {
+    release_chunk<kDmaPerChunk * (kAhead - 1)>();
     ++g;
   };
 
@@ -683,7 +700,7 @@ void mlp3_bf16_kernel(
 #pragma unroll
     for (int c = 0; c < NX; ++c) {
       const unsigned char* buf = lds + (g % kBufs) * CHUNK;
-      fetch(tile, parity, c + kBufs - 1, ahead());
+      fetch(tile, parity, c + kAhead, ahead());
       if constexpr (G == 1) {
         if ((wave >> 1) == c) {
           const int xrow = 32 * (wave & 1) + r32;   // this lane's row within the chunk
@@ -721,9 +738,9 @@ void mlp3_bf16_kernel(
           w3f[bt][tt] = *reinterpret_cast<const bf16x8*>(
               buf + W3OFF + (bt * 32 + r32) * 64 + ((((2 * tt) | h) ^ sw3) << 4));
     };
-    // layer-2 chunk j = b * KP + part is prefetched while chunk j - (kBufs - 1) is multiplied;
-    // the last kPeel blocks, whose prefetches reach into the next tile, are peeled off the loop
-    constexpr int kPeel = (kBufs - 1 + KP - 1) / KP;
+    // layer-2 chunk j = b * KP + part is prefetched while chunk j - kAhead is multiplied; the
+    // last kPeel blocks, whose prefetches reach into the next tile, are peeled off the loop
+    constexpr int kPeel = (kAhead + KP - 1) / KP;
     constexpr int kSteady = NB2 - kPeel - 1;
     static_assert(kSteady >= 2, "at least one pair of blocks in the steady-state loop");
     auto in_tile = [&](int j, const unsigned char* dst, int k) { spread(tile, parity, NX + NC1 + j, dst, k); };
@@ -746,73 +763,129 @@ void mlp3_bf16_kernel(
           asm volatile("" : "+a"(h1[2 * nb + half]));
         }
       };
+      // Fragment f of a layer-1 chain (block f % 2, K-step f / 2) and K-step k of a layer-2 chunk.
+      auto l1_frag = [&](const unsigned char* buf, int f) {
+        const int k = f >> 1, lb = f & 1;
+        return *reinterpret_cast<const bf16x8*>(buf + ((k & 4) ? l1b[lb] : l1a[lb]) + k * 32);
+      };
+      auto l2_frag = [&](const unsigned char* buf, int k) {
+        return *reinterpret_cast<const bf16x8*>(buf + l2 + k * 32);
+      };
+      // The chains hand the chunks over to each other (mfma_chain_handover); the first layer-1
+      // chain follows the feature chunks, which have none, so its first fragments are read here.
+      // Like the first fragments, the biases that start the next chain's accumulators are read
+      // during the chain before it (step kBiasStep), and the deferred ReLU of the previous
+      // chunk's blocks runs one half-block per MFMA step (steps 1 .. 4), in the shadow of the
+      // matrix core, so that no chain waits on LDS or vector-ALU work before its first MFMA.
+      constexpr int kBiasStep = 8;
+      bf16x8 fr[kLookahead];
+      f32x16 nb0, nb1;                      // biases of the next chain's blocks
+#pragma unroll
+      for (int f = 0; f < kLookahead; ++f) fr[f] = l1_frag(lds + (g % kBufs) * CHUNK, f);
+      nb0 = bias_acc(s_b1, h);
+      nb1 = bias_acc(s_b1 + 32, h);
+      auto l1_relu_half = [&](int nb, const f32x16& acc, int half) {
+        h1[2 * nb + half] = relu_bf16(acc, half);
+        asm volatile("" : "+a"(h1[2 * nb + half]));
+      };
 #pragma unroll
       for (int c = 0; c < NC1; ++c) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+        const unsigned char* nbuf = lds + ((g + 1) % kBufs) * CHUNK;
         const unsigned char* dst = ahead();
-        f32x16 acc0 = bias_acc(s_b1 + (2 * c) * 32, h);
-        f32x16 acc1 = bias_acc(s_b1 + (2 * c + 1) * 32, h);
-        mfma_chain_pair<KS1, KS1>(
-            acc0, acc1, buf + l1a[0], buf + l1b[0], buf + l1a[1], buf + l1b[1], xf[0],
-            [&]() {
-              if (c > 0) {
-                l1_relu(2 * c - 2, prev0);
-                l1_relu(2 * c - 1, prev1);
+        f32x16 acc0 = nb0;
+        f32x16 acc1 = nb1;
+        mfma_chain_handover<2 * KS1, true>(
+            fr, [&](int f) { return l1_frag(buf, f); },
+            [&](int i) { return c + 1 < NC1 ? l1_frag(nbuf, i) : l2_frag(nbuf, i); },
+            [&](int f, const bf16x8& a) {
+              if (f & 1) acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xf[0][f >> 1], acc1, 0, 0, 0);
+              else acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xf[0][f >> 1], acc0, 0, 0, 0);
+            },
+            [&]() {},
+            [&](int f) {
+              spread(tile, parity, NX + c + kAhead, dst, f);
+              if (c > 0 && f >= 1 && f <= 4) l1_relu_half(2 * c - 2 + ((f - 1) >> 1), (f - 1) >> 1 ? prev1 : prev0, (f - 1) & 1);
+              if (f == kBiasStep) {
+                if (c + 1 < NC1) {
+                  nb0 = bias_acc(s_b1 + (2 * c + 2) * 32, h);
+                  nb1 = bias_acc(s_b1 + (2 * c + 3) * 32, h);
+                } else {
+                  nb0 = bias_acc(s_b2, h);   // the first layer-2 block's
+                }
               }
             },
-            [&](int f) { spread(tile, parity, NX + c + kBufs - 1, dst, f); });
+            release);
         prev0 = acc0;
         prev1 = acc1;
         __builtin_amdgcn_sched_barrier(0);
-        advance();
       }
 
       // ---- layer 2 block by block, each block folded straight into the logits ----------------
       // The epilogue of each block -- ReLU and the 2 BT MFMAs that fold its 32 neurons into the
-      // logits -- is deferred into the start of the next block's chain, where it covers the
-      // latency of that chain's first fragment reads; the block's W3 fragments are read into
-      // registers before the barrier that lets its buffer be refilled.
+      // logits -- is deferred into the start of the next block's chain; the block's W3 fragments
+      // are read into registers after its chain, two chunks before its buffer is refilled.
       zero_logits();
-      auto l2_epilogue = [&](const f32x16& prev) {
-        bf16x8 h2[2];
+      // the deferred epilogue of the previous block, in pieces over the first steps of the next
+      // block's first chain (step k; k < 0: all at once, after the tile's last block)
+      bf16x8 h2[2];
+      auto l2_epilogue = [&](const f32x16& prev, int k) {
+        if (k < 0 || k == 1) {
 #pragma unroll
-        for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(prev, half);
+          for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(prev, half);
+        }
 #pragma unroll
         for (int bt = 0; bt < BT; ++bt)
+          if (k < 0 || k == 2 + bt) {
 #pragma unroll
-          for (int tt = 0; tt < 2; ++tt)
-            logit[0][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[0][bt], 0, 0, 0);
+            for (int tt = 0; tt < 2; ++tt)
+              logit[0][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[0][bt], 0, 0, 0);
+          }
       };
-      // block b; pre(prev) is the deferred epilogue of the block before it
-      auto l2_block = [&](int b, const f32x16& prev, auto&& pre, auto&& load_ahead) {
-        f32x16 acc = bias_acc(s_b2 + b * 32, h);
+      // block b; pre(prev) is the deferred epilogue of the block before it; kLast: the tile's
+      // last block, whose last chain hands over to the next tile's feature chunk (no fragments)
+      auto l2_block = [&](int b, const f32x16& prev, auto&& pre, auto&& load_ahead, auto last) {
+        f32x16 acc = nb0;
 #pragma unroll
         for (int part = 0; part < KP; ++part) {
           const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+          const unsigned char* nbuf = lds + ((g + 1) % kBufs) * CHUNK;
           const unsigned char* dst = ahead();
-          mfma_chain<32, H1 / 16>(
-              acc, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(prev); },
-              [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
+          auto chain = [&](auto next_exists) {
+            mfma_chain_handover<32, decltype(next_exists)::value>(
+                fr, [&](int k) { return l2_frag(buf, k); }, [&](int i) { return l2_frag(nbuf, i); },
+                [&](int k, const bf16x8& a) {
+                  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, h1[part * 32 + k], acc, 0, 0, 0);
+                },
+                [&]() {},
+                [&](int k) {
+                  load_ahead(b * KP + part + kAhead, dst, k);
+                  if (part == 0) pre(prev, k);
+                  if (part == KP - 1 && k == kBiasStep && !decltype(last)::value) nb0 = bias_acc(s_b2 + (b + 1) * 32, h);
+                },
+                release);
+          };
+          if (decltype(last)::value && part == KP - 1) chain(std::false_type{});
+          else chain(std::true_type{});
           if (part == KP - 1) read_w3(buf);
           __builtin_amdgcn_sched_barrier(0);
-          advance();
         }
         return acc;
       };
       // Block 0 finishes layer 1; blocks 1 .. NB2-kPeel-1 run in a loop over pairs, so that the
       // two accumulators alternate roles without copies.
-      f32x16 carry = l2_block(0, prev1, [&](const f32x16& p) {
-        l1_relu(H1 / 32 - 2, prev0);
-        l1_relu(H1 / 32 - 1, p);
-      }, in_tile);
+      f32x16 carry = l2_block(0, prev1, [&](const f32x16& p, int k) {
+        if (k >= 1 && k <= 4) l1_relu_half(H1 / 32 - 2 + ((k - 1) >> 1), (k - 1) >> 1 ? p : prev0, (k - 1) & 1);
+      }, in_tile, std::false_type{});
       for (int b = 1; b + 1 <= kSteady; b += 2) {
-        const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile);
-        carry = l2_block(b + 1, a, l2_epilogue, in_tile);
+        const f32x16 a = l2_block(b, carry, l2_epilogue, in_tile, std::false_type{});
+        carry = l2_block(b + 1, a, l2_epilogue, in_tile, std::false_type{});
       }
-      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
+      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile, std::false_type{});
 #pragma unroll
-      for (int b = NB2 - kPeel; b < NB2; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping);
-      l2_epilogue(carry);
+      for (int b = NB2 - kPeel; b < NB2 - 1; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping, std::false_type{});
+      carry = l2_block(NB2 - 1, carry, l2_epilogue, wrapping, std::true_type{});
+      l2_epilogue(carry, -1);
     } else {
       // ---- layer 1, G groups: one 32-neuron block at a time (two per chunk), each block's
       // ReLU deferred into the next block's chain; activations in the accumulation registers
@@ -839,7 +912,7 @@ void mlp3_bf16_kernel(
           for (int gr = 0; gr < G; ++gr) acc.v[gr] = bias_acc(s_b1 + nb * 32, h);
           mfma_chain_groups<KS1, G, KS1>(
               acc.v, buf + l1a[lb], buf + l1b[lb], xf, 0, [&]() { if (nb > 0) l1_relu(nb - 1, prev); },
-              [&](int k) { spread(tile, parity, NX + c + kBufs - 1, dst, KS1 * lb + k); });
+              [&](int k) { spread(tile, parity, NX + c + kAhead, dst, KS1 * lb + k); });
           prev = acc;
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -872,7 +945,7 @@ void mlp3_bf16_kernel(
           const unsigned char* dst = ahead();
           mfma_chain_groups<32, G, H1 / 16>(
               acc.v, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(p); },
-              [&](int k) { load_ahead(b * KP + part + kBufs - 1, dst, k); });
+              [&](int k) { load_ahead(b * KP + part + kAhead, dst, k); });
           if (part == KP - 1) read_w3(buf);
           __builtin_amdgcn_sched_barrier(0);
           advance();
