@@ -214,10 +214,9 @@ __device__ __forceinline__ void role_row(float z0, float b0, float coef, float p
 // boundaries) by direct global->LDS loads, so every fetch overlaps the multiplication of
 // earlier chunks. Each wavefront waits only for the loads of the chunk needed next (counted
 // vmcnt), then the workgroup barrier publishes it. No other global load is in flight, so no
-// wait ever drains the prefetch. With one row group the barrier sits inside the chain of MFMAs
+// wait ever drains the prefetch. The barrier sits inside the chain of MFMAs
 // (mfma_chain_handover) and the prefetch distance is 2, so that the buffer being refilled is two
-// chunks old and no wavefront can still be reading it; with two row groups the barrier follows
-// each chunk's MFMAs and the distance is 3.
+// chunks old and no wavefront can still be reading it.
 //
 // LDS layouts (all 16-byte reads are free of bank conflicts per quarter-wavefront):
 //   feature chunk: G = 1: 64 rows of 512 bytes, the 16-byte units of row r stored at
@@ -241,24 +240,25 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kLookahead = 3;            // fragment reads ahead of their MFMA (one row group)
 
-// One row group's chain of F MFMA steps over one LDS chunk, with the hand-over to the next chunk
-// folded in. fr holds the fragments (16-byte A operands) of steps 0 .. kLookahead-1 on entry
-// (read by the chain before, or by the caller); step f's fragment is cur(f), read kLookahead
-// steps ahead. At step F - kLookahead every fragment of this chunk has been requested: release()
-// lets the next chunk in (its loads waited for, the workgroup barrier crossed), and the remaining
-// lookahead reads fetch the next chain's first fragments through next(i), left in fr on return
-// (kNext). The barrier then overlaps the last MFMAs of this chain, and the next chain starts with
-// its first fragments already in flight. mma(f, fragment) issues step f's MFMA; pre() runs before
-// the first one, side(f) right after MFMA f, while the matrix core is busy (weight loads, the
-// pieces of the previous block's deferred epilogue); the scheduling barriers keep this order.
-// Measured on 4,194,304 stages (256-1024-1024-64): 8.45 against 8.57 ms with a barrier (and a
-// wait for the wavefront's own LDS reads) between the chains, outputs bit for bit the same;
-// reading 4 or 5 steps ahead instead of 3 changed nothing.
-template <int F, bool kNext, typename Cur, typename Next, typename Mma, typename Pre, typename Side,
-          typename Release>
-__device__ __forceinline__ void mfma_chain_handover(bf16x8 (&fr)[kLookahead], Cur&& cur, Next&& next, Mma&& mma,
-                                                    Pre&& pre, Side&& side, Release&& release) {
-  constexpr int LA = kLookahead;
+// A chain of F MFMA steps over one LDS chunk, with the hand-over to the next chunk folded in. fr
+// holds the fragments (16-byte A operands) of steps 0 .. LA-1 on entry (read by the chain before,
+// or by the caller); step f's fragment is cur(f), read LA steps ahead. At step F - LA every
+// fragment of this chunk has been requested: release() lets the next chunk in (its loads waited
+// for, the workgroup barrier crossed), and the remaining lookahead reads fetch the next chain's
+// first fragments through next(i), left in fr on return (kNext). The barrier then overlaps the
+// last MFMAs of this chain, and the next chain starts with its first fragments already in
+// flight. mma(f, fragment) issues step f's MFMAs (one per row group the fragment feeds); pre()
+// runs before the first step, side(f) right after step f, while the matrix core is busy (weight
+// loads, the pieces of the previous block's deferred epilogue); the scheduling barriers keep
+// this order.
+// Measured against a barrier (and a wait for the wavefront's own LDS reads) between the chains,
+// outputs bit for bit the same: 8.45 against 8.57 ms on 4,194,304 stages (256-1024-1024-64, one
+// row group; reading 4 or 5 steps ahead instead of 3 changed nothing), 0.443 against 0.454 ms
+// on 719,712 stages (256-512-512-64, two row groups).
+template <int F, bool kNext, int LA = kLookahead, typename Cur, typename Next, typename Mma, typename Pre,
+          typename Side, typename Release>
+__device__ __forceinline__ void mfma_chain_handover(bf16x8 (&fr)[LA], Cur&& cur, Next&& next, Mma&& mma, Pre&& pre,
+                                                    Side&& side, Release&& release) {
   static_assert(F > LA, "the hand-over lies inside the chain");
   bf16x8 ring[F + LA];
 #pragma unroll
@@ -395,39 +395,10 @@ __device__ __forceinline__ void release_chunk() {
 
 constexpr int kMaxModels = 64;           // per-model KV bytes staged in LDS
 
-// acc[g] += sum_k A_k * b[g][k0 + k] for the G row groups of a wavefront: every weight fragment
-// read from LDS feeds G MFMAs, one per group (independent accumulators), so the LDS reads, their
-// waits and the weight traffic per MFMA drop by a factor G. A_k is the 16-byte LDS fragment at
-// (k & 4 ? pb : pa) + 32k (the two bases absorb the layer-1 unit swizzle; pa == pb elsewhere),
-// read kLookaheadGroups K-steps ahead; pre() -- the deferred epilogue of the previous block --
-// runs after the first fragment reads are issued, so that it fills their latency, and side(k)
-// right after the MFMAs of step k; the scheduling barriers keep this order.
+// Fragment lookahead with two row groups (K-steps; each fragment read from LDS feeds one MFMA
+// per group into independent accumulators, so the LDS fragment reads, their waits and the weight
+// traffic per MFMA are half those of one group).
 constexpr int kLookaheadGroups = 2;
-template <int KS, int G, int NBREG, typename Pre, typename Side>
-__device__ __forceinline__ void mfma_chain_groups(f32x16 (&acc)[G], const unsigned char* pa,
-                                                  const unsigned char* pb, const bf16x8 (&b)[G][NBREG], int k0,
-                                                  Pre&& pre, Side&& side) {
-  constexpr int LA = kLookaheadGroups;
-  bf16x8 fr[KS];
-#pragma unroll
-  for (int k = 0; k < LA && k < KS; ++k)
-    fr[k] = *reinterpret_cast<const bf16x8*>(((k & 4) ? pb : pa) + k * 32);
-  __builtin_amdgcn_sched_barrier(0);
-  pre();
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int k = 0; k < KS; ++k) {
-    if (k + LA < KS) {
-      const int kk = k + LA;
-      fr[kk] = *reinterpret_cast<const bf16x8*>(((kk & 4) ? pb : pa) + kk * 32);
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[k], b[g][k0 + k], acc[g], 0, 0, 0);
-    side(k);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
 
 template <int G>
 struct AccGroups {
@@ -472,12 +443,11 @@ void mlp3_bf16_kernel(
   constexpr int ROW2 = 1024 + 16;         // layer-2 chunk: bytes per row
   constexpr int W3OFF = 32 * ROW2;
   constexpr int CHUNK = cmax(cmax(64 * 512, 32 * PAIR), W3OFF + B * 64);
-  // Prefetch distance in chunks. One row group hands each chunk over inside the chain (the
-  // barrier before the last MFMAs, no wait for its own LDS reads), so the buffer a new prefetch
-  // fills must be two chunks old: distance 2 of the 4 buffers. Two groups wait for their reads
-  // at the barrier after the chain, and prefetch 3 ahead.
-  constexpr int kAhead = G == 1 ? 2 : kBufs - 1;
-  static_assert(kAhead + 2 <= kBufs || G != 1, "the chunk a prefetch overwrites is two chunks old");
+  // Prefetch distance in chunks. Each chunk is handed over inside the chain of MFMAs (the
+  // barrier before the last MFMAs, no wait for the wavefront's own LDS reads), so the buffer a
+  // new prefetch fills must be two chunks old: distance 2 of the 4 buffers.
+  constexpr int kAhead = 2;
+  static_assert(kAhead + 2 <= kBufs, "the chunk a prefetch overwrites is two chunks old");
   static_assert(NC >= kAhead, "prologue fetches whole chunks of the first tile");
   static_assert(NX + NC1 + kAhead <= NC, "feature and layer-1 prefetches stay within the tile");
   static_assert(2 * KS1 == 32, "a layer-1 chunk is 32 MFMA steps");
@@ -899,68 +869,128 @@ void mlp3_bf16_kernel(
             asm volatile("" : "+a"(h1[gr][2 * nb + half]));
           }
       };
+      // The chains hand over as with one group (mfma_chain_handover, kLookaheadGroups K-steps
+      // ahead): the first block of a layer-1 chunk to the second within the same chunk (no
+      // barrier), the second to the next chunk; the next block's biases are read mid-chain and
+      // the previous block's deferred ReLU runs one piece per step.
+      constexpr int LA = kLookaheadGroups;
+      constexpr int kBiasStep = 8;
+      auto l1_frag = [&](const unsigned char* buf, int lb, int k) {
+        return *reinterpret_cast<const bf16x8*>(buf + ((k & 4) ? l1b[lb] : l1a[lb]) + k * 32);
+      };
+      auto l2_frag = [&](const unsigned char* buf, int k) {
+        return *reinterpret_cast<const bf16x8*>(buf + l2 + k * 32);
+      };
+      auto l1_relu_piece = [&](int nb, const AccGroups<G>& acc, int piece) {   // piece = 2 gr + half
+        const int gr = piece >> 1, half = piece & 1;
+        h1[gr][2 * nb + half] = relu_bf16(acc.v[gr], half);
+        asm volatile("" : "+a"(h1[gr][2 * nb + half]));
+      };
+      auto no_release = [&]() {};
+      bf16x8 fr[LA];
+#pragma unroll
+      for (int k = 0; k < LA; ++k) fr[k] = l1_frag(lds + (g % kBufs) * CHUNK, 0, k);
+      f32x16 nb = bias_acc(s_b1, h);          // biases of the next chain's block
       AccGroups<G> prev;
 #pragma unroll
       for (int c = 0; c < NC1; ++c) {
         const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+        const unsigned char* nbuf = lds + ((g + 1) % kBufs) * CHUNK;
         const unsigned char* dst = ahead();
 #pragma unroll
         for (int lb = 0; lb < 2; ++lb) {
-          const int nb = 2 * c + lb;
+          const int blk = 2 * c + lb;
           AccGroups<G> acc;
 #pragma unroll
-          for (int gr = 0; gr < G; ++gr) acc.v[gr] = bias_acc(s_b1 + nb * 32, h);
-          mfma_chain_groups<KS1, G, KS1>(
-              acc.v, buf + l1a[lb], buf + l1b[lb], xf, 0, [&]() { if (nb > 0) l1_relu(nb - 1, prev); },
-              [&](int k) { spread(tile, parity, NX + c + kAhead, dst, KS1 * lb + k); });
+          for (int gr = 0; gr < G; ++gr) acc.v[gr] = nb;
+          auto mma = [&](int k, const bf16x8& a) {
+#pragma unroll
+            for (int gr = 0; gr < G; ++gr)
+              acc.v[gr] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xf[gr][k], acc.v[gr], 0, 0, 0);
+          };
+          auto side = [&](int k) {
+            spread(tile, parity, NX + c + kAhead, dst, KS1 * lb + k);
+            if (blk > 0 && k >= 1 && k <= 2 * G) l1_relu_piece(blk - 1, prev, k - 1);
+            if (k == kBiasStep) nb = blk + 1 < H1 / 32 ? bias_acc(s_b1 + (blk + 1) * 32, h) : bias_acc(s_b2, h);
+          };
+          if (lb == 0)
+            mfma_chain_handover<KS1, true, LA>(
+                fr, [&](int k) { return l1_frag(buf, 0, k); }, [&](int i) { return l1_frag(buf, 1, i); }, mma,
+                [&]() {}, side, no_release);
+          else
+            mfma_chain_handover<KS1, true, LA>(
+                fr, [&](int k) { return l1_frag(buf, 1, k); },
+                [&](int i) { return c + 1 < NC1 ? l1_frag(nbuf, 0, i) : l2_frag(nbuf, i); }, mma, [&]() {}, side,
+                release);
           prev = acc;
         }
         __builtin_amdgcn_sched_barrier(0);
-        advance();
       }
 
-      // ---- layer 2, G groups; epilogues deferred as for G = 1 --------------------------------
+      // ---- layer 2, G groups; epilogues deferred as for G = 1, in pieces over the first steps
       zero_logits();
-      auto l2_epilogue = [&](const AccGroups<G>& p) {
+      bf16x8 h2[2];
+      auto l2_epilogue = [&](const AccGroups<G>& p, int k) {   // k < 0: all at once
 #pragma unroll
         for (int gr = 0; gr < G; ++gr) {
-          bf16x8 h2[2];
+          if (k < 0 || k == 1 + 3 * gr) {
 #pragma unroll
-          for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(p.v[gr], half);
+            for (int half = 0; half < 2; ++half) h2[half] = relu_bf16(p.v[gr], half);
+          }
 #pragma unroll
           for (int bt = 0; bt < BT; ++bt)
+            if (k < 0 || k == 2 + 3 * gr + bt) {
 #pragma unroll
-            for (int tt = 0; tt < 2; ++tt)
-              logit[gr][bt] =
-                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[gr][bt], 0, 0, 0);
+              for (int tt = 0; tt < 2; ++tt)
+                logit[gr][bt] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(w3f[bt][tt], h2[tt], logit[gr][bt], 0, 0, 0);
+            }
         }
       };
-      auto l2_block = [&](int b, const AccGroups<G>& p, auto&& pre, auto&& load_ahead) {
+      auto l2_block = [&](int b, const AccGroups<G>& p, auto&& pre, auto&& load_ahead, auto last) {
         AccGroups<G> acc;
 #pragma unroll
-        for (int gr = 0; gr < G; ++gr) acc.v[gr] = bias_acc(s_b2 + b * 32, h);
+        for (int gr = 0; gr < G; ++gr) acc.v[gr] = nb;
 #pragma unroll
         for (int part = 0; part < KP; ++part) {
           const unsigned char* buf = lds + (g % kBufs) * CHUNK;
+          const unsigned char* nbuf = lds + ((g + 1) % kBufs) * CHUNK;
           const unsigned char* dst = ahead();
-          mfma_chain_groups<32, G, H1 / 16>(
-              acc.v, buf + l2, buf + l2, h1, part * 32, [&]() { if (part == 0) pre(p); },
-              [&](int k) { load_ahead(b * KP + part + kAhead, dst, k); });
+          auto chain = [&](auto next_exists) {
+            mfma_chain_handover<32, decltype(next_exists)::value, LA>(
+                fr, [&](int k) { return l2_frag(buf, k); }, [&](int i) { return l2_frag(nbuf, i); },
+                [&](int k, const bf16x8& a) {
+#pragma unroll
+                  for (int gr = 0; gr < G; ++gr)
+                    acc.v[gr] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, h1[gr][part * 32 + k], acc.v[gr], 0, 0, 0);
+                },
+                [&]() {},
+                [&](int k) {
+                  load_ahead(b * KP + part + kAhead, dst, k);
+                  if (part == 0) pre(p, k);
+                  if (part == KP - 1 && k == kBiasStep && !decltype(last)::value) nb = bias_acc(s_b2 + (b + 1) * 32, h);
+                },
+                release);
+          };
+          if (decltype(last)::value && part == KP - 1) chain(std::false_type{});
+          else chain(std::true_type{});
           if (part == KP - 1) read_w3(buf);
           __builtin_amdgcn_sched_barrier(0);
-          advance();
         }
         return acc;
       };
-      AccGroups<G> carry = l2_block(0, prev, [&](const AccGroups<G>& p) { l1_relu(H1 / 32 - 1, p); }, in_tile);
+      AccGroups<G> carry = l2_block(0, prev, [&](const AccGroups<G>& q, int k) {
+        if (k >= 1 && k <= 2 * G) l1_relu_piece(H1 / 32 - 1, q, k - 1);
+      }, in_tile, std::false_type{});
       for (int b = 1; b + 1 <= kSteady; b += 2) {
-        const AccGroups<G> a = l2_block(b, carry, l2_epilogue, in_tile);
-        carry = l2_block(b + 1, a, l2_epilogue, in_tile);
+        const AccGroups<G> a = l2_block(b, carry, l2_epilogue, in_tile, std::false_type{});
+        carry = l2_block(b + 1, a, l2_epilogue, in_tile, std::false_type{});
       }
-      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile);
+      if constexpr (kSteady % 2 == 1) carry = l2_block(kSteady, carry, l2_epilogue, in_tile, std::false_type{});
 #pragma unroll
-      for (int b = NB2 - kPeel; b < NB2; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping);
-      l2_epilogue(carry);
+      for (int b = NB2 - kPeel; b < NB2 - 1; ++b) carry = l2_block(b, carry, l2_epilogue, wrapping, std::false_type{});
+      carry = l2_block(NB2 - 1, carry, l2_epilogue, wrapping, std::true_type{});
+      l2_epilogue(carry, -1);
     }
 
     if constexpr (kRoles) {
