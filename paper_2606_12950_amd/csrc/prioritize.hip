@@ -5,9 +5,9 @@
 //     microseconds (round half to even) and accumulating the suffix sums in int64 -- the
 //     remaining predicted time from each stage to the end of the chain. The stage latencies
 //     are loaded eight at a time, so a chain costs one memory round trip per eight stages.
-//     Chains of more than 1,024 stages are instead scanned by the whole block, one after the
-//     other: 1,024-stage chunks from the end backwards, a block-wide exclusive scan of
-//     saturating sums per chunk plus the carry of the chunks after it. The
+//     Chains of more than 1,024 stages are left to a second kernel, whose workgroups scan them
+//     one after the other: 1,024-stage chunks from the end backwards, a block-wide exclusive
+//     scan of saturating sums per chunk plus the carry of the chunks after it. The
 //     remaining time at the workflow's cursor gives slack = deadline - now - remaining,
 //     clamped to int32. Integer sums are exact, so the result does not depend on the
 //     summation order. The block also counts the first radix digit of its tile.
@@ -17,13 +17,14 @@
 //     kernel); the global offset of every (digit, tile), i.e. the exclusive scan of the count
 //     table in digit-major order, which each scatter block derives itself from the table when
 //     there are few tiles (four threads per digit read it, one memory round trip); with many
-//     tiles a group scan (prefix of each digit within groups of 256 tiles, in place, plus the
-//     group totals) and a one-block scan over the group totals and the digits prepare it, and
+//     tiles a group scan (prefix of each digit within groups of 16 .. 256 tiles, in place, plus
+//     the group totals) and a one-block scan over the group totals and the digits prepare it, and
 //     the scatter adds two table entries; and a scatter in which each wavefront ranks its keys
 //     digit by digit with ballots (wave multisplit) in input order, so equal digits keep their
 //     relative order.
 //     The key array is padded to whole tiles with all-ones keys, which always sort last and
 //     never reach the caller's output.
+#include <atomic>
 #include <mutex>
 
 #include "internal.h"
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
     const float* __restrict__ stage_latency_s, const int32_t* __restrict__ cursor,
     const int64_t* __restrict__ deadline_us, int64_t now_us, int64_t* __restrict__ remaining_us,
     int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
-    uint32_t* __restrict__ counts) {
+    uint32_t* __restrict__ counts, uint32_t* __restrict__ long_flag, uint32_t epoch) {
   __shared__ uint32_t hist[kBuckets];
   __shared__ int64_t stage_us[kStageCap];
   const int tid = threadIdx.x, tile = blockIdx.x;
@@ -190,6 +191,7 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
     int64_t suffix = 0, rem_head = 0;
     if (end - first > kLongChain) {
       long_mark = 0x80000000u;   // left to long_chain_kernel, which replaces the placeholder key (rem_head 0)
+      *long_flag = epoch;        // this call has a long chain (every writer stores the same value)
     } else if (staged) {
       // not unrolled: chains are a few stages long, and the unrolled form's set-up (64-bit
       // addresses of eight stages) costs more than the loop itself
@@ -245,14 +247,17 @@ __global__ __launch_bounds__(kTile) void chain_kernel(
 // from the placeholder to the real key (one workgroup owns a tile, so no other touches those
 // counts). Kept out of the chain kernel: the registers of the scan there slowed every chain (by
 // half at 2^24 workflows); persistent, since one short-lived workgroup per tile cost more in
-// scheduling than the check itself.
+// scheduling than the check itself. A call without long chains (the chain kernel's flag word does
+// not hold this call's number) returns at once instead of reading every mark (41 us at 2^24
+// workflows).
 constexpr int kLongChainBlocks = 512;
 constexpr int kLongChainTilesPerCheck = 8;   // at most this many tiles' marks per barrier
 __global__ __launch_bounds__(kTile) void long_chain_kernel(
     int32_t n_workflows, const int64_t* __restrict__ chain_offset, const float* __restrict__ stage_latency_s,
     const int32_t* __restrict__ cursor, const int64_t* __restrict__ deadline_us, int64_t now_us,
     int64_t* __restrict__ remaining_us, int32_t* __restrict__ slack_key, uint32_t* __restrict__ keys,
-    uint32_t* __restrict__ vals, uint32_t* __restrict__ counts, int tiles_per_check) {
+    uint32_t* __restrict__ vals, uint32_t* __restrict__ counts, int tiles_per_check,
+    const uint32_t* __restrict__ long_flag, uint32_t epoch) {
   __shared__ int64_t wtot[kTile / 64];
   __shared__ int64_t s_head_rem;
   __shared__ int32_t s_long[kTile];
@@ -260,6 +265,7 @@ __global__ __launch_bounds__(kTile) void long_chain_kernel(
   const int tid = threadIdx.x;
   const int64_t n_tiles = ((int64_t)n_workflows + kTile - 1) / kTile;
   const int kT = tiles_per_check;   // 1 .. kLongChainTilesPerCheck
+  if (*long_flag != epoch) return;  // the usual case: no chain of this call is long
   for (int64_t t0 = (int64_t)blockIdx.x * kT; t0 < n_tiles; t0 += (int64_t)gridDim.x * kT) {   // workgroup-uniform
     uint32_t marks = 0;   // bit i: this thread's workflow of tile t0 + i is marked
 #pragma unroll
@@ -327,11 +333,13 @@ __global__ __launch_bounds__(kTile) void radix_count_kernel(const uint32_t* __re
   if (tid < kBuckets) counts[(int64_t)tile * kBuckets + tid] = hist[tid];
 }
 
-// Many tiles, step 1: one block per group of kGroup tiles. In place, counts[t][d] becomes the
-// number of keys with digit d in the tiles of t's group before t; gsum[group][d] gets the
-// group's total. Thread (q, d) runs over the tiles q*kGroup/4 .. of the group for digit d (for
-// a fixed tile, a wavefront's 64 digits are consecutive words).
-constexpr int kGroup = 256;
+// Many tiles, step 1: one block per group of group_tiles tiles (a power of two, 16 .. 256, so
+// that there are at most 64 groups up to 2^26 keys: the group scans spread over as many
+// workgroups as that allows, and the one-workgroup top scan stays short). In place, counts[t][d]
+// becomes the number of keys with digit d in the tiles of t's group before t; gsum[group][d]
+// gets the group's total. Thread (q, d) runs over the tiles q*group_tiles/4 .. of the group for
+// digit d (for a fixed tile, a wavefront's 64 digits are consecutive words).
+constexpr int kMinGroupTiles = 16, kMaxGroupTiles = 256, kTargetGroups = 64;
 constexpr int kBatch = 16;                         // independent loads in flight per thread
 
 // Exclusive prefix, in place, of the column entries t0 .. t1-1 (row stride kBuckets words) of a
@@ -366,11 +374,11 @@ __device__ __forceinline__ uint32_t column_sum(const uint32_t* __restrict__ tabl
 }
 
 __global__ __launch_bounds__(1024) void radix_group_scan_kernel(uint32_t* __restrict__ counts, int n_tiles,
-                                                                uint32_t* __restrict__ gsum) {
+                                                                int group_tiles, uint32_t* __restrict__ gsum) {
   __shared__ uint32_t part[4][kBuckets];
   const int tid = threadIdx.x, d = tid & (kBuckets - 1), q = tid >> 8;
-  const int t0 = min(n_tiles, blockIdx.x * kGroup + q * (kGroup / 4));
-  const int t1 = min(n_tiles, t0 + kGroup / 4);
+  const int t0 = min(n_tiles, blockIdx.x * group_tiles + q * (group_tiles / 4));
+  const int t1 = min(n_tiles, t0 + group_tiles / 4);
   part[q][d] = column_sum(counts, t0, t1, d);
   __syncthreads();
   uint32_t before = 0;
@@ -417,8 +425,8 @@ constexpr int kFusedScanMaxTiles = 128;
 template <bool kFusedScan, int ITEMS>
 __global__ __launch_bounds__(kTile) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, int shift, int n_tiles,
-    const uint32_t* __restrict__ table, const uint32_t* __restrict__ gtable, uint32_t* __restrict__ out_keys,
-    uint32_t* __restrict__ out_vals, int64_t out_limit) {
+    const uint32_t* __restrict__ table, const uint32_t* __restrict__ gtable, int group_tiles,
+    uint32_t* __restrict__ out_keys, uint32_t* __restrict__ out_vals, int64_t out_limit) {
   static_assert(!kFusedScan || ITEMS == 1, "the fused offsets path handles one key per thread");
   constexpr int TK = kTile * ITEMS;
   constexpr int kStage = kFusedScan ? 1 : TK;
@@ -473,7 +481,7 @@ __global__ __launch_bounds__(kTile) void radix_scatter_kernel(
     }
   } else {
     if (tid < kBuckets)
-      base[tid] = gtable[(int64_t)(tile / kGroup) * kBuckets + tid] + table[(int64_t)tile * kBuckets + tid];
+      base[tid] = gtable[(int64_t)(tile / group_tiles) * kBuckets + tid] + table[(int64_t)tile * kBuckets + tid];
   }
   __syncthreads();
 
@@ -554,8 +562,8 @@ size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 // fused into the scatter. More: tiles of kTile * kBigItems keys and the group/top scans.
 struct PrioLayout {
   bool fused;
-  int64_t tile_keys, n_tiles, n_groups, padded;
-  size_t keys_a, vals_a, keys_b, vals_b, counts, gsum, total;
+  int64_t tile_keys, n_tiles, group_tiles, n_groups, padded;
+  size_t keys_a, vals_a, keys_b, vals_b, counts, gsum, flag, total;
 };
 
 PrioLayout prio_layout(int32_t n_workflows) {
@@ -566,14 +574,17 @@ PrioLayout prio_layout(int32_t n_workflows) {
   L.padded = L.n_tiles * L.tile_keys;
   const size_t kb = align256(sizeof(uint32_t) * (size_t)L.padded);
   const size_t cb = align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_tiles);
-  L.n_groups = (L.n_tiles + kGroup - 1) / kGroup;
+  L.group_tiles = kMinGroupTiles;
+  while (L.group_tiles < kMaxGroupTiles && L.n_tiles > (int64_t)kTargetGroups * L.group_tiles) L.group_tiles *= 2;
+  L.n_groups = (L.n_tiles + L.group_tiles - 1) / L.group_tiles;
   L.keys_a = 0;
   L.vals_a = L.keys_a + kb;
   L.keys_b = L.vals_a + kb;
   L.vals_b = L.keys_b + kb;
   L.counts = L.vals_b + kb;
   L.gsum = L.counts + cb;
-  L.total = L.gsum + (L.fused ? 0 : align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_groups));
+  L.flag = L.gsum + (L.fused ? 0 : align256(sizeof(uint32_t) * kBuckets * (size_t)L.n_groups));
+  L.total = L.flag + 256;
   return L;
 }
 
@@ -618,13 +629,21 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
   uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(ws + L.vals_a), reinterpret_cast<uint32_t*>(ws + L.vals_b)};
   uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.counts);
   uint32_t* gsum = reinterpret_cast<uint32_t*>(ws + L.gsum);
+  // Whether any chain of this call is long: the chain kernel stores this call's number in the
+  // workspace word when it meets one, and the long-chain kernel returns at once unless it finds
+  // it there. A stale or uninitialised word equal to the number only costs that kernel a scan
+  // that finds no marks, so the word needs no clearing (and a captured graph, which replays one
+  // number, stays correct).
+  static std::atomic<uint32_t> call_counter{0};
+  const uint32_t epoch = call_counter.fetch_add(1, std::memory_order_relaxed) + 1;
+  uint32_t* long_flag = reinterpret_cast<uint32_t*>(ws + L.flag);
 
   const int nt = (int)L.n_tiles;
   // the chain kernel covers the padded range in blocks of kTile workflows; with small tiles
   // (block = tile) it also counts the first digit
   chain_kernel<<<dim3((unsigned)(L.padded / kTile)), dim3(kTile), 0, stream>>>(
       n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us,
-      slack_key, keys[0], vals[0], L.fused ? counts : nullptr);
+      slack_key, keys[0], vals[0], L.fused ? counts : nullptr, long_flag, epoch);
   // one tile per workgroup while that fits kLongChainBlocks workgroups, more per barrier beyond
   const int64_t chain_tiles = (n_workflows + (int64_t)kTile - 1) / kTile;
   int tiles_per_check = 1;
@@ -634,7 +653,7 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
   long_chain_kernel<<<dim3((unsigned)(chain_steps < kLongChainBlocks ? chain_steps : kLongChainBlocks)), dim3(kTile),
                       0, stream>>>(
       n_workflows, chain_offset, stage_latency_s, cursor, deadline_us, now_us, remaining_us, slack_key, keys[0],
-      vals[0], L.fused ? counts : nullptr, tiles_per_check);
+      vals[0], L.fused ? counts : nullptr, tiles_per_check, long_flag, epoch);
   for (int pass = 0; pass < kPasses; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     const int shift = pass * kRadixBits;
@@ -646,14 +665,14 @@ maestro_status launch_prioritize(int32_t n_workflows, int64_t n_stages,
       if (pass > 0)
         radix_count_kernel<1><<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
       radix_scatter_kernel<true, 1><<<dim3(nt), dim3(kTile), 0, stream>>>(
-          keys[src], vals[src], shift, nt, counts, nullptr, out_k, out_v, limit);
+          keys[src], vals[src], shift, nt, counts, nullptr, 0, out_k, out_v, limit);
     } else {
       const int ng = (int)L.n_groups;
       radix_count_kernel<kBigItems><<<dim3(nt), dim3(kTile), 0, stream>>>(keys[src], shift, counts);
-      radix_group_scan_kernel<<<dim3(ng), dim3(1024), 0, stream>>>(counts, nt, gsum);
+      radix_group_scan_kernel<<<dim3(ng), dim3(1024), 0, stream>>>(counts, nt, (int)L.group_tiles, gsum);
       radix_top_scan_kernel<<<dim3(1), dim3(1024), 0, stream>>>(gsum, ng);
       radix_scatter_kernel<false, kBigItems><<<dim3(nt), dim3(kTile), 0, stream>>>(
-          keys[src], vals[src], shift, nt, counts, gsum, out_k, out_v, limit);
+          keys[src], vals[src], shift, nt, counts, gsum, (int)L.group_tiles, out_k, out_v, limit);
     }
   }
   return launch_status();
