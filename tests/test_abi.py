@@ -282,16 +282,18 @@ def test_degradation_plans_validation(lib):
 
 def test_prioritize_validation_and_workspace(lib):
     ws = lib.maestro_prioritize_workspace(131072, 720000)
-    # four key/value arrays padded to 1024-key tiles plus a 256-entry count table per tile
+    # four key/value arrays padded to 1024-key tiles plus a 256-entry count table per tile, and
+    # 256 bytes for the word that tells whether a call has long chains
     tiles = 131072 // 1024
-    assert ws == 4 * 4 * tiles * 1024 + 4 * 256 * tiles
+    assert ws == 4 * 4 * tiles * 1024 + 4 * 256 * tiles + 256
     assert lib.maestro_prioritize_workspace(0, 0) == 0
-    assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 1024 + 4 * 256
-    # beyond 128 such tiles: 4096-key tiles, plus a 256-entry offset table per group of 256 tiles
+    assert lib.maestro_prioritize_workspace(1, 3) == 4 * 4 * 1024 + 4 * 256 + 256
+    # beyond 128 such tiles: 4096-key tiles, plus a 256-entry offset table per group of tiles
+    # (16 .. 256 tiles, a power of two, at most 64 groups up to 2^26 keys)
     tiles = (200000 + 4095) // 4096
-    assert lib.maestro_prioritize_workspace(200000, 10**6) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256
+    assert lib.maestro_prioritize_workspace(200000, 10**6) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256 * 4 + 256
     tiles = (1 << 26) // 4096
-    assert lib.maestro_prioritize_workspace(1 << 26, 0) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256 * (tiles // 256)
+    assert lib.maestro_prioritize_workspace(1 << 26, 0) == 4 * 4 * tiles * 4096 + 4 * 256 * tiles + 4 * 256 * 64 + 256
     call = lambda W=4, S=8, off=FAKE, ws=FAKE, ws_bytes=1 << 20: lib.maestro_prioritize(
         W, S, off, FAKE, None, FAKE, 0, None, FAKE, FAKE, ws, ws_bytes, None)
     assert call(W=-1) == INVALID

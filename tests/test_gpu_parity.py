@@ -479,6 +479,41 @@ def test_prioritize_block_scanned_long_chains(case):
     assert_prio_equal(got, oracle.prioritize(off, lat, dl, 600 * 10 ** 6, cursor=cur))
 
 
+def test_prioritize_long_chain_flag_with_a_reused_workspace():
+    # whether a call has chains of more than 1,024 stages is told to the long-chain kernel through a
+    # word of the workspace holding the call's number; one workspace serves calls with and without
+    # long chains in turn (a stale word from an earlier call must neither skip a long chain nor
+    # disturb a call without any), then the same through the static scratch of the allocation-free
+    # entry point, and a workspace filled with ones (any stale word) serves one of each
+    rng = np.random.default_rng(17)
+    t = lambda a: pipeline._t(a, "cuda")
+
+    def batch(long):
+        lens = rng.integers(0, 9, 3000)
+        if long:
+            lens[[7, 1500, 2999]] = [1025, 4000, 2048]
+        off = np.zeros(lens.size + 1, np.int64)
+        off[1:] = np.cumsum(lens)
+        lat = rng.uniform(0.0, 30.0, int(off[-1])).astype(np.float32)
+        dl = rng.integers(0, 10 ** 12, lens.size).astype(np.int64)
+        return off, lat, dl
+
+    batches = [batch(x) for x in (True, False, True, True, False, False, True)]
+    need = max(M.prioritize_workspace_bytes(b[0].size - 1, b[1].size) for b in batches)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    for noalloc in (False, True):
+        for off, lat, dl in batches:
+            got = M.prioritize(t(off), t(lat), t(dl), 600 * 10 ** 6, workspace=None if noalloc else ws,
+                               noalloc=noalloc)
+            torch.cuda.synchronize()
+            assert_prio_equal(tuple(_np(x) for x in got), oracle.prioritize(off, lat, dl, 600 * 10 ** 6))
+    ws.fill_(255)
+    for off, lat, dl in batches[:2]:
+        got = M.prioritize(t(off), t(lat), t(dl), 600 * 10 ** 6, workspace=ws)
+        torch.cuda.synchronize()
+        assert_prio_equal(tuple(_np(x) for x in got), oracle.prioritize(off, lat, dl, 600 * 10 ** 6))
+
+
 def test_prioritize_long_chain_and_empty():
     # one chain spanning every stage, then an empty batch
     S = 100000
