@@ -456,13 +456,14 @@ static float norm01(float x, float lo, float hi) {
 }
 
 /* The minimum-impact plan of Alg. 2 and its cost, Eq. 4, on one node. The greedy loop of Alg. 2
- * takes engines in priority order (SortByPriority: ascending action level 1..5, the lower engine
- * index first on equal levels) and stops before the first engine once the freed memory reaches
+ * takes engines in priority order (ascending action level 1..5, the lower engine index first on
+ * equal levels) and stops before the first engine once the freed memory reaches
  * R, so the plan it returns is the shortest prefix of that order whose freed bytes (summed in
  * float64, in order) reach R -- the empty prefix when R <= 0 -- and it fails when even the whole
  * order frees less. The plan's cost is the float32 sum, in order, of its engines' restoration
  * latencies c(e, a), plus c_int when it holds an engine of level 4 or 5 (the active work of that
- * engine is preempted or aborted). Returns 0 with the cost in *c_deg, or 1 on Failure. */
+ * engine is preempted or aborted). Returns 0 with the cost in *c_deg, or 1 when no prefix frees
+ * enough. */
 typedef struct { int32_t level, idx; } eng_t;
 static int eng_cmp(const void* pa, const void* pb) {
   const eng_t* a = (const eng_t*)pa;
@@ -487,7 +488,7 @@ static int degradation_plan(double R, int32_t e0, int32_t e1, const int32_t* lev
   int32_t len = -1;                                     /* the shortest prefix reaching R */
   for (int32_t p = 0; p <= ne && len < 0; ++p)
     if (sum[p] >= R) len = p;
-  int status = 1;                                       /* Failure */
+  int status = 1;                                       /* no plan */
   if (len >= 0) {
     float total = 0.0f;
     int interrupt = 0;
