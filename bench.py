@@ -593,6 +593,8 @@ def main():
                     help="time latency routing with T_act from readiness tiers (Sec. III-C, Eq. 6)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
+    ap.add_argument("--free-scale", type=float, default=1.0, metavar="S",
+                    help="divide every node's free HBM by S (S = 48 on c4: most stage-node pairs infeasible)")
     ap.add_argument("--library-gemm", action="store_true",
                     help="time the vendor GEMM library (square and per-layer bf16 GEMMs, the unfused network) "
                          "beside the fused predictor")
@@ -642,8 +644,15 @@ def main():
     torch.cuda.set_device(0)
 
     wl = W.workload(args.workload)
+    if args.free_scale != 1.0:
+        wl.free_bytes = wl.free_bytes / args.free_scale
     step = time_step(wl, args.steps, args.warmup)
     line = step_record(wl, step, args.steps)
+    if args.free_scale != 1.0:
+        line["config"]["free_scale"] = args.free_scale
+        rows = np.arange(min(wl.n, 16384))
+        need = step["kv"][rows][:, None] * (1.0 + wl.spec.rho)
+        line["config"]["infeasible_pair_fraction"] = round(float((need > wl.free_bytes[None, :]).mean()), 4)
     line.update({"metric": METRIC, "value": line.pop("stages_per_s"), "unit": "stages/s", "n_gpus": 1,
                  "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
                  "vs_baseline": None, "dtype": wl.spec.dtype, "data": "synthetic"})

@@ -261,7 +261,9 @@ MAESTRO_API maestro_status maestro_route_ex(int64_t n, const int32_t* model_id, 
  * (ready time, node index), ready = fl32(queue_s[j] + act) with act as in maestro_route (0 when
  * bit m of resident_mask[j] is set, else cold_s[j]) or, when act_s is not NULL, act_s[j][m] as in
  * maestro_route_tiered (cold_s and resident_mask are then not read), each with its headroom
- * free_bytes[j]. `lists` is device memory of at least maestro_route_lists_bytes(n_models,
+ * free_bytes[j], and after the lists, per model, the largest headroom of every block of 8, 64 and
+ * 512 consecutive entries (rounded up to float32), which lets the walk skip nodes that cannot
+ * admit its stage. `lists` is device memory of at least maestro_route_lists_bytes(n_models,
  * n_nodes) bytes, 16-byte aligned, owned by the caller, valid until the node state changes.
  * maestro_route_walk then gives every stage exactly the result of maestro_route_ex (or
  * maestro_route_tiered) with MAESTRO_ROUTE_SORTED on that node state; it reads only `lists` of

@@ -166,6 +166,23 @@ struct __align__(16) NodeEntry {          // 16 bytes: one node in a model's rea
   double free;                            // KV admission headroom
 };
 
+// After the lists, per model, the largest headroom of every block of 8, 64 and 512 consecutive
+// list entries, rounded up to float32 (-inf past the last node): past its first kPlainWalk
+// entries a walk skips every block whose largest headroom cannot admit its stage, so a stage that
+// fits few nodes, or none, does not visit every infeasible node. Rounding up keeps the test exact:
+// a block is skipped only when its true largest headroom is below the demand too. Measured on c4
+// (one box): with every headroom divided by 48 (59% of the pairs infeasible, 922 list entries per
+// stage) the route call takes 0.44 instead of 9.26 ms; on c4 itself 77.5 instead of 73.4 us (the
+// tables cost the sort 1 us, their test the walk 3 us). Gating the walk on the whole list's largest
+// headroom, or testing the tables from the first entry past the staged head, cost the c4 walk 3-13
+// us more.
+__host__ __device__ constexpr int32_t skip_blocks(int32_t n_nodes, int shift) {
+  return (n_nodes + (1 << shift) - 1) >> shift;
+}
+__host__ __device__ constexpr int64_t skip_per_model(int32_t n_nodes) {
+  return (int64_t)skip_blocks(n_nodes, 3) + skip_blocks(n_nodes, 6) + skip_blocks(n_nodes, 9);
+}
+
 // One workgroup per model puts every node in (ready time, node index) order: a stable LSD radix
 // sort of the 32-bit order-preserving image of the ready time (float_key) in four 8-bit passes,
 // starting from index order, so equal ready times keep increasing indices. Wavefront w holds
@@ -278,16 +295,40 @@ __global__ __launch_bounds__(1024) void sort_nodes_kernel(
     __syncthreads();   // every thread has its keys and the counts are read before the next pass
   }
   NodeEntry* out = lists + (size_t)m * n_nodes;
+  float* max8 = reinterpret_cast<float*>(lists + (size_t)n_models * n_nodes) + (size_t)m * skip_per_model(n_nodes);
+  float* max64 = max8 + skip_blocks(n_nodes, 3);
+  float* max512 = max64 + skip_blocks(n_nodes, 6);
+  __shared__ float s_max64[kSortMax / 64];
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
     const int p = (IPT * wave + j) * 64 + lane;
+    float f = -INFINITY;
     if (p < n_nodes) {
       NodeEntry e;
       e.ready = key_float(key[j]);
       e.node = (int32_t)idx[j];
       e.free = free_bytes[e.node];
       out[p] = e;
+      f = __double2float_ru(e.free);
     }
+    // the 64 positions of item j are lanes 0 .. 63 in order: blocks of 8 are lane octets
+    f = fmaxf(f, __shfl_xor(f, 1));
+    f = fmaxf(f, __shfl_xor(f, 2));
+    f = fmaxf(f, __shfl_xor(f, 4));
+    if ((lane & 7) == 0 && p < n_nodes) max8[p >> 3] = f;
+    f = fmaxf(f, __shfl_xor(f, 8));
+    f = fmaxf(f, __shfl_xor(f, 16));
+    f = fmaxf(f, __shfl_xor(f, 32));
+    if (lane == 0) {
+      if (p < n_nodes) max64[p >> 6] = f;
+      s_max64[IPT * wave + j] = f;
+    }
+  }
+  __syncthreads();
+  for (int b = t; b < skip_blocks(n_nodes, 9); b += (int)blockDim.x) {
+    float f = -INFINITY;
+    for (int r = 8 * b; r < 8 * b + 8 && r < padded / 64; ++r) f = fmaxf(f, s_max64[r]);
+    max512[b] = f;
   }
 }
 
@@ -297,6 +338,7 @@ __global__ __launch_bounds__(1024) void sort_nodes_kernel(
 // once per workgroup, and a walk split into a loop over the head and one over the rest of the
 // list, were both slower (120 and 110 us against 94 us per c4 route call on one box).
 constexpr int kWalkHead = 8;
+constexpr int kPlainWalk = 32;            // entries visited before the skip tables are consulted
 
 // one stage's walk down its model's list
 template <int KT>
@@ -327,8 +369,25 @@ __device__ __forceinline__ void walk_stage(
   };
   const NodeEntry* lhead = s_head + m * kWalkHead;
   const NodeEntry* list = lists + (size_t)m * n_nodes;
-  for (int32_t j = 0; j < n_nodes; ++j)
-    if (visit(j < head ? lhead[j] : list[j])) break;
+  const float* max8 = reinterpret_cast<const float*>(lists + (size_t)n_models * n_nodes) +
+                      (size_t)m * skip_per_model(n_nodes);
+  const float* max64 = max8 + skip_blocks(n_nodes, 3);
+  const float* max512 = max64 + skip_blocks(n_nodes, 6);
+  bool done = false;
+  int32_t j = 0;
+#pragma unroll 1
+  for (; j < n_nodes && j < kPlainWalk; ++j)
+    if (visit(j < head ? lhead[j] : list[j])) {
+      done = true;
+      break;
+    }
+  while (!done && j < n_nodes) {   // skip blocks whose largest headroom admits nothing
+    if ((j & 511) == 0 && !(need <= (double)max512[j >> 9])) { j += 512; continue; }
+    if ((j & 63) == 0 && !(need <= (double)max64[j >> 6])) { j += 64; continue; }
+    if ((j & 7) == 0 && !(need <= (double)max8[j >> 3])) { j += 8; continue; }
+    done = visit(list[j]);
+    ++j;
+  }
   int32_t outn[KT];
   float outs[KT];
 #pragma unroll
@@ -374,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void walk_route_kernel(
 }
 
 size_t sorted_lists_bytes(int32_t n_models, int32_t n_nodes) {
-  return (size_t)n_models * (size_t)n_nodes * sizeof(NodeEntry);
+  return (size_t)n_models * ((size_t)n_nodes * sizeof(NodeEntry) + (size_t)skip_per_model(n_nodes) * sizeof(float));
 }
 
 bool sorted_possible(int32_t n_nodes) { return n_nodes <= kSortMax; }

@@ -203,6 +203,27 @@ def test_route_c4_top4_sampled_stages(algo):
 
 
 @pytest.mark.parametrize("algo", ["scan", "sorted"])
+def test_route_c4_contended_sampled_stages(algo):
+    # c4 with every node's headroom divided by 48 (U[0, 0.625] GB): most stage-node pairs are
+    # infeasible, so the sorted walk skips many nodes per stage and some stages have fewer than k
+    # feasible nodes; full launch on the GPU, the oracle on a stage sample
+    w = wl("c4")
+    pred, kv, b, o = gpu_predict(w)
+    free = w.free_bytes / 48.0
+    idx, sc = M.route(b.model_id, o.pred_len, o.kv_bytes, b.decode_s_per_token, pipeline._t(free, "cuda"),
+                      b.queue_s, b.cold_s, b.resident_mask, k=4, rho=w.spec.rho, algo=ALGOS[algo])
+    torch.cuda.synchronize()
+    gi, gs = _np(idx), _np(sc)
+    rows = np.sort(np.random.default_rng(11).choice(w.n, 20000, replace=False))
+    rows = np.unique(np.concatenate([rows, [0, w.n - 1]]))
+    assert (kv[rows][:, None] > free[None, :]).mean() > 0.5
+    assert (gi[rows] < 0).any()             # some sampled stages fit fewer than 4 nodes
+    ref = oracle.route(w.model_id[rows], pred[rows], kv[rows], w.decode_s_per_token, free,
+                       w.queue_s, w.cold_s, w.resident_mask, k=4)
+    assert_route_equal((gi[rows], gs[rows]), ref)
+
+
+@pytest.mark.parametrize("algo", ["scan", "sorted"])
 @pytest.mark.parametrize("k", [1, 3, 4, 16])
 @pytest.mark.parametrize("n,M_", [(1, 1), (7, 3), (300, 64), (2500, 1500), (40000, 37), (3000, 8192)])
 def test_route_shapes_and_widths(n, M_, k, algo):

@@ -65,12 +65,25 @@ def test_sorted_lists_match_definition(M_, K):
         free, q, cold, mask = _nodes(rng, M_, K, coarse)
         lists = M.route_sort_nodes(_t(free), _t(q), _t(cold), _t(mask), K)
         torch.cuda.synchronize()
-        assert lists.numel() >= M.route_lists_bytes(K, M_) == K * M_ * 16
+        # largest headroom per 8 / 64 / 512 entries, rounded up to float32
+        blocks = sum((M_ + (1 << b) - 1) >> b for b in (3, 6, 9))
+        assert lists.numel() >= M.route_lists_bytes(K, M_) == K * (M_ * 16 + blocks * 4)
+        skip = lists[K * M_ * 16: K * (M_ * 16 + blocks * 4)].cpu().numpy().view(np.float32).reshape(K, blocks)
         got = _lists(lists, K, M_)
         for m, (ready, node, fr) in enumerate(_expected_lists(free, q, cold, mask, K)):
             assert np.array_equal(got["ready"][m].view(np.uint32), ready.view(np.uint32)), (m, coarse)
             assert np.array_equal(got["node"][m], node), (m, coarse)
             assert np.array_equal(got["free"][m], fr), (m, coarse)
+            for b, off in ((3, 0), (6, (M_ + 7) >> 3), (9, ((M_ + 7) >> 3) + ((M_ + 63) >> 6))):
+                nb = (M_ + (1 << b) - 1) >> b
+                padded = np.full(nb << b, -np.inf)
+                padded[:M_] = fr
+                want = padded.reshape(nb, 1 << b).max(axis=1)
+                got_b = skip[m, off: off + nb].astype(np.float64)
+                # the float32 value at or above the float64 block maximum, and the nearest such
+                assert np.all(got_b >= want), (m, b)
+                assert np.all((want == -np.inf) | (np.nextafter(got_b.astype(np.float32), np.float32(-np.inf))
+                                                   .astype(np.float64) < want)), (m, b)
 
 
 def test_sorted_lists_readiness_form():
@@ -117,3 +130,30 @@ def test_walk_rejects_lists_of_the_wrong_size():
         M.route_walk(one, torch.ones(1, device="cuda"), torch.ones(1, dtype=torch.float64, device="cuda"),
                      torch.ones(K, device="cuda"), M_, lists)
     assert e.value.status == 3
+
+
+@pytest.mark.parametrize("M_,K,k", [(9, 3, 4), (520, 8, 4), (4100, 16, 3), (8192, 4, 16)])
+def test_walk_with_few_admitting_nodes(M_, K, k):
+    # most nodes admit almost no stage: the walk skips blocks of 8 / 64 / 512 entries whose largest
+    # headroom is below the stage's demand; stages that fit nowhere, in one or two nodes only (at
+    # any list position, block edges included), and the usual ones; against the oracle and the scan
+    rng = np.random.default_rng(M_ + 3 * K + k)
+    free, q, cold, mask = _nodes(rng, M_, K)
+    free = rng.uniform(0, 1, M_) * GB
+    big = rng.choice(M_, min(M_, 5), replace=False)
+    free[big] = rng.uniform(40, 80, big.size) * GB
+    n = 6000
+    model = rng.integers(0, K, n).astype(np.int32)
+    pred = rng.uniform(32, 4064, n).astype(np.float32)
+    kv = rng.choice(np.array([0.5, 10.0, 60.0, 90.0]), n) * GB      # fits many, a few, one or two, none
+    dec = rng.choice(np.array([0.015625, 0.03125, 0.02], np.float32), K)
+    lists = M.route_sort_nodes(_t(free), _t(q), _t(cold), _t(mask), K)
+    gi, gs = M.route_walk(_t(model), _t(pred), _t(kv), _t(dec), M_, lists, k=k)
+    si, ss = M.route(_t(model), _t(pred), _t(kv), _t(dec), _t(free), _t(q), _t(cold), _t(mask), k=k,
+                     algo=M._native.ROUTE_SCAN)
+    torch.cuda.synchronize()
+    ri, rs = oracle.route(model, pred, kv, dec, free, q, cold, mask, k=k)
+    gi, gs = gi.cpu().numpy(), gs.cpu().numpy()
+    assert (gi[:, 0] < 0).any() and (gi[:, 0] >= 0).any()
+    assert np.array_equal(gi, ri) and np.array_equal(gs.view(np.uint32), rs.view(np.uint32))
+    assert np.array_equal(gi, si.cpu().numpy()) and np.array_equal(gs.view(np.uint32), ss.cpu().numpy().view(np.uint32))
