@@ -125,7 +125,8 @@ def test_route_validation(lib):
     assert call_ex(-1) == INVALID
     assert call_ex(2) == WORKSPACE                                            # sorted lists need space
     # sorted lists: one 16-byte entry per (model, node); none beyond 8192 nodes
-    assert lib.maestro_route_workspace(10, 8, 16, 1) == 8 * 16 * 16
+    # per model: 16 bytes per node, then the float32 largest headroom of every 8 / 64 / 512 nodes
+    assert lib.maestro_route_workspace(10, 8, 16, 1) == 8 * (16 * 16 + 4 * (2 + 1 + 1))
     assert lib.maestro_route_workspace(10, 8, 8193, 1) == 0
     assert call(n=-1) == INVALID
     assert call(n_models=0) == INVALID
@@ -142,8 +143,8 @@ def test_route_validation(lib):
 
 def test_route_split_validation(lib):
     # the node half and the stage half of the sorted route, rejected before any launch
-    assert lib.maestro_route_lists_bytes(8, 16) == 8 * 16 * 16
-    assert lib.maestro_route_lists_bytes(64, 8192) == 64 * 8192 * 16
+    assert lib.maestro_route_lists_bytes(8, 16) == 8 * (16 * 16 + 4 * (2 + 1 + 1))
+    assert lib.maestro_route_lists_bytes(64, 8192) == 64 * (8192 * 16 + 4 * (1024 + 128 + 16))
     assert lib.maestro_route_lists_bytes(8, 8193) == 0
     assert lib.maestro_route_lists_bytes(0, 16) == 0 and lib.maestro_route_lists_bytes(65, 16) == 0
     need = 8 * 16 * 16
