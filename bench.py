@@ -511,7 +511,7 @@ def mfma_ceiling_bench(steps: int, warmup: int, rounds: int = 20000):
 
 def library_gemm_bench(name: str, steps: int, warmup: int):
     """The vendor GEMM library (hipBLASLt through torch.mm, bfloat16) beside the fused predictor on
-    the same box: a large square GEMM, the predictor's three layers as separate library GEMMs on
+    the same GPU: a large square GEMM, the predictor's three layers as separate library GEMMs on
     the workload's batch, and the unfused three-layer network (library GEMMs with bias, ReLU by
     torch, no length epilogue). It says how far the chip's MFMA throughput goes under its power
     limit for plain dense products; the fused kernel is timed last, on the workload's own inputs.

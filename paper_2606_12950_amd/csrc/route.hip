@@ -171,7 +171,7 @@ struct __align__(16) NodeEntry {          // 16 bytes: one node in a model's rea
 // entries a walk skips every block whose largest headroom cannot admit its stage, so a stage that
 // fits few nodes, or none, does not visit every infeasible node. Rounding up keeps the test exact:
 // a block is skipped only when its true largest headroom is below the demand too. Measured on c4
-// (one box): with every headroom divided by 48 (59% of the pairs infeasible, 922 list entries per
+// (one GPU): with every headroom divided by 48 (59% of the pairs infeasible, 922 list entries per
 // stage) the route call takes 0.44 instead of 9.26 ms; on c4 itself 77.5 instead of 73.4 us (the
 // tables cost the sort 1 us, their test the walk 3 us). Gating the walk on the whole list's largest
 // headroom, or testing the tables from the first entry past the staged head, cost the c4 walk 3-13
@@ -194,7 +194,7 @@ __host__ __device__ constexpr int64_t skip_per_model(int32_t n_nodes) {
 // and indices at their new positions in LDS: five barriers per pass. A bitonic network over the
 // 64-bit keys (ready, index), with in-register and cross-lane stages and a barrier per cross-
 // wavefront stage, took 35 us on 64 models x 4,096 nodes against 20 us for this sort (calls back
-// to back, one box); taking the digit-count loads of the scan out of its loop (21.3 us), a scan
+// to back, one GPU); taking the digit-count loads of the scan out of its loop (21.3 us), a scan
 // spread over all threads plus one wavefront (21.5 us) and 512 threads of 8 keys (23.1 us) were
 // slower. LDS: `padded` keys and indices (dynamic), 16 x 256 digit counts.
 constexpr int kSortWaves = 16;
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(1024) void sort_nodes_kernel(
 // (while each thread's own inputs are in flight), so a walk that ends early never waits on a
 // dependent global load. One workgroup per 256 stages: a persistent grid that staged the heads
 // once per workgroup, and a walk split into a loop over the head and one over the rest of the
-// list, were both slower (120 and 110 us against 94 us per c4 route call on one box).
+// list, were both slower (120 and 110 us against 94 us per c4 route call on one GPU).
 constexpr int kWalkHead = 8;
 constexpr int kPlainWalk = 32;            // entries visited before the skip tables are consulted
 
