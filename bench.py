@@ -593,6 +593,10 @@ def main():
                     help="time latency routing with T_act from readiness tiers (Sec. III-C, Eq. 6)")
     ap.add_argument("--two-phase", action="store_true",
                     help="time the two-phase predictor (Sec. III-B) beside the bins predictor")
+    ap.add_argument("--n-stages", type=int, default=0, metavar="N",
+                    help="replace the workload's stage count (one GPU's share of a batch sharded by stage)")
+    ap.add_argument("--n-nodes", type=int, default=0, metavar="M",
+                    help="replace the workload's node count (one GPU's share of a batch sharded by node)")
     ap.add_argument("--free-scale", type=float, default=1.0, metavar="S",
                     help="divide every node's free HBM by S (S = 48 on c4: most stage-node pairs infeasible)")
     ap.add_argument("--library-gemm", action="store_true",
@@ -643,11 +647,14 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
 
-    wl = W.workload(args.workload)
+    overrides = {key: v for key, v in (("n_stages", args.n_stages), ("n_nodes", args.n_nodes)) if v}
+    wl = W.workload(args.workload, **overrides)
     if args.free_scale != 1.0:
         wl.free_bytes = wl.free_bytes / args.free_scale
     step = time_step(wl, args.steps, args.warmup)
     line = step_record(wl, step, args.steps)
+    if overrides:
+        line["config"]["overrides"] = overrides
     if args.free_scale != 1.0:
         line["config"]["free_scale"] = args.free_scale
         rows = np.arange(min(wl.n, 16384))
