@@ -224,6 +224,8 @@ void fitness_kernel(
     double needd;   // fl32(R_need), widened
     float gamma, omg, lambda, mu;
     mask_t mbit;
+    const uint32_t* mword;   // 64-bit residency bits: the 32-bit half of s_mask[0] holding mbit
+    uint32_t mbit32;         // mbit within that half
     int model;
     bool ok;        // a stage whose model, source and class ids are in range
     const float* prox;    // 1 - norm(RTT) from the stage's source, per node of the chunk
@@ -240,6 +242,8 @@ void fitness_kernel(
     l.needd = 0.0;
     l.gamma = l.omg = l.lambda = l.mu = 0.0f;
     l.mbit = 0;
+    l.mword = reinterpret_cast<const uint32_t*>(s_mask);
+    l.mbit32 = 0;
     l.model = 0;
     l.ok = false;
     int src = 0, cls = 0;
@@ -257,6 +261,10 @@ void fitness_kernel(
         l.omg = __fsub_rn(1.0f, l.gamma);
         l.model = m;
         l.mbit = kMat ? 0 : (mask_t)1 << m;
+        if constexpr (kReady == kMask64) {
+          l.mword = reinterpret_cast<const uint32_t*>(s_mask) + (m >> 5);
+          l.mbit32 = 1u << (m & 31);
+        }
         src = sid;
         cls = c;
       } else {
@@ -338,6 +346,15 @@ void fitness_kernel(
       }
       return __fadd_rn(__fmul_rn(l.lambda, tr), __fmul_rn(l.mu, nd));
     };
+    // whether the lane's model is resident on node i: with 64-bit residency bits each stage
+    // reads the one 32-bit half that holds its bit (a 32-bit AND and compare per pair instead of
+    // a 64-bit pair of each; c4, 64 models, with the plain node loop below unrolled by four:
+    // 5.04-5.22 against 5.42-5.48 ms on two boxes, with plans 7.47-7.61 against 7.63-7.65), else
+    // from mk, the node's bits read once for all the lane's stages
+    auto resident = [&](const Lane& l, int i, mask_t mk) -> bool {
+      if constexpr (kReady == kMask64) return (l.mword[2 * i] & l.mbit32) != 0u;
+      else return (mk & l.mbit) != 0;
+    };
     // the pair's fitness when the stage fits (C_deg = the node's, or 0 with plans); mk is the
     // node's residency bits
     auto fits_score = [&](const Lane& l, int i, const Node nd, mask_t mk) {
@@ -347,7 +364,7 @@ void fitness_kernel(
         pen = __fadd_rn(__fmul_rn(l.lambda, s_ready[i * n_models + l.model]), __fmul_rn(l.mu, s_nd[i]));
       } else {
         const float2 p = l.pen[i];
-        pen = (mk & l.mbit) ? p.x : p.y;
+        pen = resident(l, i, mk) ? p.x : p.y;
       }
       return __fsub_rn(a, pen);
     };
@@ -443,9 +460,9 @@ void fitness_kernel(
       // short pairs, and nodes go two at a time: all their LDS reads and scores come before the
       // first insertion, whose branches would otherwise hold back the next node's reads (c4 with
       // plans 7.58 against 8.06 ms). Without plans there are fewer branches and one node at a
-      // time unrolled by two stays: grouping there measured 5.48 against 5.44 ms.
+      // time unrolled by four stays: grouping there measured 5.48 against 5.44 ms.
       if constexpr (!kPlans) {
-#pragma unroll 2
+#pragma unroll 4
         for (int i = 0; i < cn; ++i) {
           const Node nd = s_node[i];
           const mask_t mk = node_mask(i);
