@@ -460,9 +460,12 @@ void fitness_kernel(
       // short pairs, and nodes go two at a time: all their LDS reads and scores come before the
       // first insertion, whose branches would otherwise hold back the next node's reads (c4 with
       // plans 7.58 against 8.06 ms). Without plans there are fewer branches and one node at a
-      // time unrolled by four stays: grouping there measured 5.48 against 5.44 ms.
+      // time stays (grouping there measured 5.48 against 5.44 ms), unrolled by four, or by two
+      // with T_act rows of up to 16 models (c3: 0.160 against 0.171 ms; c4, 64 models, by four:
+      // 6.98 against 7.17 ms).
       if constexpr (!kPlans) {
-#pragma unroll 4
+        constexpr int kNodeUnroll = kReady == kMatrix16 ? 2 : 4;
+#pragma unroll kNodeUnroll
         for (int i = 0; i < cn; ++i) {
           const Node nd = s_node[i];
           const mask_t mk = node_mask(i);
