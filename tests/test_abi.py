@@ -321,3 +321,26 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_native, "LIBRARY_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         _native.load()
+
+
+def test_calibrate_library_sizes_and_argument_checks():
+    """The measurement-only matrix-core probe (libmaestro_calibrate.so, timed by bench.py
+    --mfma-ceiling): its sizing calls, and argument checks that return -1 before any launch."""
+    from paper_2606_12950_amd import build as B
+    if not os.path.exists(B.CALIBRATE_LIB):
+        pytest.fail("libmaestro_calibrate.so is not built (python -m paper_2606_12950_amd.build)")
+    c = ctypes.CDLL(B.CALIBRATE_LIB)
+    c.maestro_calibrate_mfma.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_uint32, ctypes.c_void_p]
+    c.maestro_calibrate_mfma.restype = ctypes.c_int
+    c.maestro_calibrate_mfma_outputs.restype = ctypes.c_int
+    c.maestro_calibrate_mfma_count.argtypes = [ctypes.c_int]
+    c.maestro_calibrate_mfma_count.restype = ctypes.c_int64
+    assert c.maestro_calibrate_mfma_outputs() == 256 * 256          # one float per thread
+    assert c.maestro_calibrate_mfma_count(1000) == 16 * 1000 * 4 * 256   # per wavefront x 4 x 256 workgroups
+    buf = ctypes.c_void_p(FAKE16.value)
+    assert c.maestro_calibrate_mfma(None, 10, 1, 0, 1, None) == -1
+    assert c.maestro_calibrate_mfma(buf, 0, 1, 0, 1, None) == -1
+    assert c.maestro_calibrate_mfma(buf, 10, 2, 0, 1, None) == -1
+    assert c.maestro_calibrate_mfma(buf, 10, 1, 3, 1, None) == -1
+    assert c.maestro_calibrate_mfma(buf, 10, 1, -1, 1, None) == -1
