@@ -104,7 +104,8 @@ def test_fitness_matches_oracle(n, M_, n_src, k):
     # several 512-node chunks with a ragged tail, every source count, route widths 1..16
     rng = np.random.default_rng(n * 7 + M_)
     nodes = _nodes(rng, M_, n_src)
-    model = rng.integers(0, 16, n).astype(np.int32)
+    # 64 models: residency bits in both halves of the 64-bit mask
+    model = rng.integers(0, 64, n).astype(np.int32)
     src = rng.integers(0, n_src, n).astype(np.int32)
     cls = rng.integers(0, 3, n).astype(np.int32)
     kv = rng.uniform(0, 250, n) * GB
@@ -280,7 +281,7 @@ def test_fitness_with_plans_matches_oracle(n, M_, n_src, k, max_e):
     if max_e > 8:
         freed = freed * 0.2                               # small actions: long plans on big nodes
     eng = (off, level, freed, cost, 2000.0)
-    model = rng.integers(0, 16, n).astype(np.int32)
+    model = rng.integers(0, 64, n).astype(np.int32)
     src = rng.integers(0, n_src, n).astype(np.int32)
     cls = rng.integers(0, 3, n).astype(np.int32)
     kv = rng.uniform(0, 120, n) * GB
