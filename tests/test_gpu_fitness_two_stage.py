@@ -8,6 +8,10 @@ widths 1..4 all take two stages per lane. With plans, one stage class has mu < 0
 window starts below 0: there the bound that drops short pairs before their plan lookup does not
 hold and must not be applied.
 
+Between the split-lane sizes and those, each lane takes one stage of its own (and at any size
+when the list is longer than four); those launches, with 64-bit residency masks, are compared
+here as well.
+
 Bars: node indices and fitness values bit-exact (both sides evaluate the same float32
 expression in the same order).
 """
@@ -22,6 +26,8 @@ pytestmark = pytest.mark.gpu
 
 N_DEG = (1 << 19) + 333      # two stages per lane without plans
 N_PLANS = (1 << 20) + 777    # two stages per lane with plans
+N_ONE = 200_003              # one lane, one stage (above 2^17, below 2^19)
+N_ONE_PLANS = 600_011        # one lane, one stage with plans (below 2^20)
 
 
 def _stages(rng, n, n_models, n_src, n_cls, kv_gb):
@@ -93,3 +99,35 @@ def test_two_stage_fitness_with_act_matrix_matches_oracle(n_models, plans):
     k = 4 if plans else 2
     got = gpu_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=k, eng=eng)
     assert_same(got, oracle_fitness_act(model, src, cls, kv, nodes, weights, bounds, act, n_models, k=k, eng=eng))
+
+
+@pytest.mark.parametrize("k,n_models", [(1, 64), (4, 64), (8, 33)])
+def test_one_stage_per_lane_fitness_matches_oracle(k, n_models):
+    rng = np.random.default_rng(400 + 10 * k + n_models)
+    M_, n_src = 300, 5
+    nodes = _nodes(rng, M_, n_src)
+    model, src, cls, kv = _stages(rng, N_ONE, n_models, n_src, 3, 250)
+    weights = [[0.25, 1, 1], [0.1, 1, 1], [0.6, 0.3, 2.0]]
+    bounds = [*oracle.quantiles(nodes["rtt_ms"].ravel()), *oracle.quantiles(nodes["queue_ms"] + nodes["act_ms"]),
+              *oracle.quantiles(nodes["deg_ms"])]
+    got = gpu_fitness(model, src, cls, kv, nodes, weights, bounds, k=k, n_models=n_models)
+    assert_same(got, oracle_fitness(model, src, cls, kv, nodes, weights, bounds, k=k))
+
+
+@pytest.mark.parametrize("k", [1, 4])
+def test_one_stage_per_lane_fitness_with_plans_matches_oracle(k):
+    rng = np.random.default_rng(500 + k)
+    M_, n_src = 200, 4
+    nodes = _nodes(rng, M_, n_src)
+    nodes["free_bytes"] = rng.uniform(0, 60, M_) * GB
+    off, level, freed, cost = _engines(rng, M_, max_e=30)
+    eng = (off, level, freed * 0.2, cost, 2000.0)
+    model, src, cls, kv = _stages(rng, N_ONE_PLANS, 64, n_src, 3, 120)
+    weights = [[0.25, 1, 1], [0.1, 1, 1], [0.5, 0.5, -1.0]]
+    bounds = [*oracle.quantiles(nodes["rtt_ms"].ravel()), *oracle.quantiles(nodes["queue_ms"] + nodes["act_ms"]),
+              0.0, 12000.0]
+    got = gpu_fitness_plans(model, src, cls, kv, nodes, weights, bounds, eng, k=k)
+    ref = oracle.route_fitness(model, src, cls, kv, nodes["free_bytes"], nodes["queue_ms"], nodes["act_ms"],
+                               nodes["resident_mask"], nodes["deg_ms"], nodes["rtt_ms"], np.asarray(weights, np.float32),
+                               np.asarray(bounds, np.float32), k=k, engines=eng)
+    assert_same(got, ref)
