@@ -347,8 +347,8 @@ void fitness_kernel(
       return __fadd_rn(__fmul_rn(l.lambda, tr), __fmul_rn(l.mu, nd));
     };
     // whether the lane's model is resident on node i: with 64-bit residency bits each stage
-    // reads the one 32-bit half that holds its bit (a 32-bit AND and compare per pair instead of
-    // a 64-bit pair of each; c4, 64 models, with the plain node loop below unrolled by four:
+    // reads the one 32-bit half that holds its bit (one 32-bit AND and compare per pair instead of
+    // two ANDs and a 64-bit compare; c4, 64 models, with the plain node loop below unrolled by four:
     // 5.04-5.22 against 5.42-5.48 ms on two boxes, with plans 7.47-7.61 against 7.63-7.65), else
     // from mk, the node's bits read once for all the lane's stages
     auto resident = [&](const Lane& l, int i, mask_t mk) -> bool {
