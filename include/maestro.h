@@ -205,7 +205,8 @@ typedef struct maestro_role_regressors {
  *   p_tool             [n] float32: calibrated tool probability (from maestro_predict_two_phase)
  *   pred_len, kv_bytes [n] float32 / float64, in and out
  * The stages are bucketed by regressor on the device (a stable counting sort) and predicted as one
- * grouped GEMM: tiles of 128 stages of one regressor, feature rows gathered. Workspace:
+ * grouped GEMM: tiles of 128 stages of one regressor (256 for the 256-512-512-64 network),
+ * feature rows gathered. Workspace:
  * maestro_role_lengths_workspace(n, n_regressors) bytes. Errors: INVALID_ARG for a NULL or
  * misaligned array, n < 0, n_models outside 1..64, n_regressors outside 1..16, n_roles outside
  * 0..64, max_len not finite and positive; UNSUPPORTED for another shape or n > 2^22 (the feature

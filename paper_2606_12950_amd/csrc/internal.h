@@ -29,6 +29,8 @@ maestro_status launch_role_lengths(const maestro_predictor& p, const maestro_rol
                                    int32_t n_models, float* pred_len, double* kv_bytes, void* workspace,
                                    hipStream_t stream);
 size_t role_lengths_workspace_bytes(int64_t n, int32_t n_groups);
+// rows of one tile of the role regressors' grouped launch for the predictor's shape
+int32_t role_tile_rows(const maestro_predictor& p);
 maestro_status launch_role_regressors(const maestro_predictor& p, int64_t n, const void* x, const float* coef,
                                       float max_len, const int32_t* tile_group, const int32_t* perm,
                                       const int32_t* prompt_p, const int32_t* model_p, const int32_t* p_bits,

@@ -368,6 +368,17 @@ __device__ __forceinline__ void scalar_load2(const int32_t* p, int32_t& a, int32
   a = (int32_t)(uint32_t)v;
   b = (int32_t)(uint32_t)(v >> 32);
 }
+// Eight consecutive int32 at a wavefront-uniform, 32-byte aligned address the same way; returns
+// entry r (r in 0..7, per lane).
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ int32_t scalar_load8_pick(const int32_t* p, int r) {
+  i32x8 v;
+  asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+  int32_t x = v[0];
+#pragma unroll
+  for (int k = 1; k < 8; ++k) x = r == k ? v[k] : x;
+  return x;
+}
 
 // Wait until at most N vector-memory operations of this wavefront are outstanding and all of
 // its LDS operations are done (gfx9 s_waitcnt encoding), then the workgroup barrier. The
@@ -411,9 +422,9 @@ struct AccGroups {
 // holds for H1 = 512.
 //
 // kRoles: the per-role regressors as one grouped GEMM. Tile t belongs to regressor
-// tile_group[t] (bucketed by role_bucket_kernels); its weights are regressor g's layers, stacked
-// after those of regressors 0 .. g-1, and its rows are the stages perm[128 t ...] (feature rows
-// gathered through the permutation; padding rows, stage -1, read as zeros). The tile count is
+// tile_group[t] (bucketed by the role_*_kernel launches); its weights are regressor g's layers, stacked
+// after those of regressors 0 .. g-1, and its rows are the stages perm[kTileRows t ...] (feature
+// rows gathered through the permutation; padding rows, stage -1, read as zeros). The tile count is
 // read from device memory (n_tiles_dev). The biases are restaged whenever a workgroup's tile
 // moves to another regressor (tiles of one regressor are contiguous, so rarely).
 template <int D, int H1, int H2, int B, int G, bool kTwoPhase, bool kRoles = false>
@@ -428,7 +439,7 @@ void mlp3_bf16_kernel(
     const int32_t* __restrict__ perm, const int32_t* __restrict__ p_bits, const int32_t* __restrict__ n_tiles_dev,
     const float* __restrict__ role_coef, float role_max_len) {
   static_assert(D == 256, "feature and layer-1 chunk layouts assume 512-byte rows");
-  static_assert(!kRoles || (!kTwoPhase && G == 1), "role regressors: one row group, output 0 only");
+  static_assert(!kRoles || !kTwoPhase, "role regressors: output 0 only");
   static_assert(H1 % 512 == 0 && H2 % 32 == 0 && B % 64 == 0, "tile shape");
   static_assert(G == 1 || (G == 2 && H1 == 512), "two row groups need H1 = 512 (256 accumulation registers)");
   constexpr int kTileRows = kWaves * kRowsPerWave * G;
@@ -521,15 +532,28 @@ void mlp3_bf16_kernel(
       // (lanes 0-31) and rho0 + 1 (lanes 32-63); a padding row (stage -1) gets an offset past the
       // buffer and reads zeros. The feature array spans at most 2^31 bytes.
       const i32x4 rs = buffer_rsrc(x, (uint32_t)(n * (D * 2)));
+      if constexpr (G == 1) {
 #pragma unroll
-      for (int q = 0; q < kDmaPerChunk; ++q) {
-        const int rho0 = 64 * j + 2 * wave + 8 * q;
-        int32_t s0 = -1, s1 = -1;
-        if (live) scalar_load2(perm + row0 + rho0, s0, s1);
-        const int32_t st = h ? s1 : s0;
-        const uint32_t unit = (uint32_t)(((lane & 31) ^ ((rho0 + h) & 15)) << 4);
-        const uint32_t voff = st >= 0 ? (uint32_t)st * (uint32_t)(D * 2) + unit : 0x80000000u;
-        dma16<true>(rs, voff, 0u, base, q * kWaves * 1024);
+        for (int q = 0; q < kDmaPerChunk; ++q) {
+          const int rho0 = 64 * j + 2 * wave + 8 * q;
+          int32_t s0 = -1, s1 = -1;
+          if (live) scalar_load2(perm + row0 + rho0, s0, s1);
+          const int32_t st = h ? s1 : s0;
+          const uint32_t unit = (uint32_t)(((lane & 31) ^ ((rho0 + h) & 15)) << 4);
+          const uint32_t voff = st >= 0 ? (uint32_t)st * (uint32_t)(D * 2) + unit : 0x80000000u;
+          dma16<true>(rs, voff, 0u, base, q * kWaves * 1024);
+        }
+      } else {
+        // K-slice j of tile rows 8i .. 8i+7 (i = wave + 4q) as in the contiguous layout, each
+        // lane's row (8i + lane / 8) gathered: one scalar load brings the load's eight stages
+        const uint32_t unit = (uint32_t)((((lane & 7) ^ (4 * (wave & 1) + (lane >> 4))) << 4) + 128 * j);
+#pragma unroll
+        for (int q = 0; q < kDmaPerChunk; ++q) {
+          int32_t st = -1;
+          if (live) st = scalar_load8_pick(perm + row0 + 8 * (wave + 4 * q), lane >> 3);
+          const uint32_t voff = st >= 0 ? (uint32_t)st * (uint32_t)(D * 2) + unit : 0x80000000u;
+          dma16<true>(rs, voff, 0u, base, q * kWaves * 1024);
+        }
       }
     } else {
       const i32x4 rs = buffer_rsrc(x + row0 * D, rows * (D * 2));
@@ -994,12 +1018,17 @@ void mlp3_bf16_kernel(
     }
 
     if constexpr (kRoles) {
-      // output 0 of row r32 sits in register 0 of lane-half 0
-      const int local = wave * kRowsPerWave + r32;
+      // output 0 of each group's row r32 sits in register 0 of lane-half 0; lane-half h finishes
+      // the row of group h (G = 2), lane-half 0 that of the only group (G = 1)
+      float z0[G];
+#pragma unroll
+      for (int gr = 0; gr < G; ++gr) z0[gr] = G == 1 ? logit[0][0][0] : __shfl(logit[gr][0][0], r32);
+      const int mine = G == 1 ? 0 : h;
+      const int local = (G * wave + mine) * kRowsPerWave + r32;
       const int32_t stage = s_meta[parity][3][local];
-      if (h == 0 && stage >= 0)
-        role_row(logit[0][0][0], s_b3[0], coef_cur, __int_as_float(s_meta[parity][2][local]), role_max_len, stage,
-                 s_meta[parity][0][local], s_meta[parity][1][local], s_alpha, n_models, pred_len, kv_bytes);
+      if ((G > 1 || h == 0) && stage >= 0)
+        role_row(mine ? z0[G - 1] : z0[0], s_b3[0], coef_cur, __int_as_float(s_meta[parity][2][local]), role_max_len,
+                 stage, s_meta[parity][0][local], s_meta[parity][1][local], s_alpha, n_models, pred_len, kv_bytes);
     } else if constexpr (kTwoPhase) {
       // Both lane-halves select each group's head output; then lane-half h finishes row r of
       // group h (G = 2), or lane-half 0 the wavefront's only group (G = 1), so that the rest
@@ -1211,9 +1240,13 @@ maestro_status launch_role_regressors(const maestro_predictor& p, int64_t n, con
         p.bias[1], p.bias[2], nullptr, n, 0, prompt_p, model_p, kv_bytes_per_token, n_models, pred_len, kv_bytes,
         TwoPhaseArgs{}, tile_group, perm, p_bits, n_tiles, coef, max_len);
   };
-  if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, 1, false, true>);
+  if (p.dims[1] == 512) args(mlp3_bf16_kernel<256, 512, 512, 64, kMidGroups, false, true>);
   else args(mlp3_bf16_kernel<256, 1024, 1024, 64, 1, false, true>);
   return launch_status();
+}
+
+int32_t role_tile_rows(const maestro_predictor& p) {
+  return (p.dims[1] == 512 ? kMidGroups : 1) * kRowsPerBlock;
 }
 
 bool two_phase_shape_supported(const maestro_predictor& p) {

@@ -7,7 +7,8 @@
 // regressor. To form such tiles the stages are bucketed by regressor, stably (a counting sort):
 //
 //   1. role_count_kernel   per 1024-stage block, the number of stages of each regressor;
-//   2. role_plan_kernel    one workgroup: each regressor's rows padded to whole 128-row tiles
+//   2. role_plan_kernel    one workgroup: each regressor's rows padded to whole tiles of the
+//                          predictor (128 rows, 256 for the 512-wide network's two row groups)
 //                          and laid out one regressor after another; the start of every
 //                          (block, regressor) run, the regressor of every tile, the padding
 //                          rows (stage -1) and the tile count;
@@ -25,7 +26,8 @@ namespace {
 constexpr int kBlock = 1024;
 constexpr int kWavesPerBlock = kBlock / 64;
 constexpr int kMaxGroups = MAESTRO_MAX_ROLE_REGRESSORS;
-constexpr int kRoleTileRows = 128;       // rows of one tile of the fused predictor (one row group)
+constexpr int kRoleTileMin = 128;        // rows of a tile of the fused predictor: one row group,
+constexpr int kRoleTileMax = 256;        // or two
 
 __device__ __forceinline__ int regressor_of(int32_t role, const int32_t* __restrict__ role_regressor,
                                             int32_t n_roles, int32_t n_groups) {
@@ -75,7 +77,7 @@ __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t* tota
   return before + x - v;
 }
 
-__global__ __launch_bounds__(kBlock) void role_plan_kernel(int32_t n_blocks, int32_t n_groups,
+__global__ __launch_bounds__(kBlock) void role_plan_kernel(int32_t n_blocks, int32_t n_groups, int32_t tile_rows,
                                                            const int32_t* __restrict__ counts,
                                                            int32_t* __restrict__ offsets,
                                                            int32_t* __restrict__ tile_group, int32_t* __restrict__ perm,
@@ -94,17 +96,17 @@ __global__ __launch_bounds__(kBlock) void role_plan_kernel(int32_t n_blocks, int
       offsets[(size_t)b * kMaxGroups + g] = run;
       run += counts[(size_t)b * kMaxGroups + g];
     }
-    const int32_t padded = (total + kRoleTileRows - 1) / kRoleTileRows * kRoleTileRows;
+    const int32_t padded = (total + tile_rows - 1) / tile_rows * tile_rows;
     for (int32_t r = base + total + t; r < base + padded; r += kBlock) {   // padding rows
       perm[r] = -1;
       prompt_p[r] = 0;
       model_p[r] = 0;
       p_bits[r] = 0;
     }
-    for (int32_t tt = base / kRoleTileRows + t; tt < (base + padded) / kRoleTileRows; tt += kBlock) tile_group[tt] = g;
+    for (int32_t tt = base / tile_rows + t; tt < (base + padded) / tile_rows; tt += kBlock) tile_group[tt] = g;
     base += padded;
   }
-  if (t == 0) n_tiles[0] = base / kRoleTileRows;
+  if (t == 0) n_tiles[0] = base / tile_rows;
 }
 
 __global__ __launch_bounds__(kBlock) void role_scatter_kernel(
@@ -148,12 +150,13 @@ struct RoleLayout {
   size_t perm, prompt, model, pbits, counts, offsets, tile_group, n_tiles, total;
 };
 
+// sized for either tile height: rows padded to the taller tiles, tiles counted at the shorter
 RoleLayout role_layout(int64_t n, int32_t n_groups) {
   RoleLayout L{};
-  L.rows_max = n + (int64_t)n_groups * (kRoleTileRows - 1);
-  L.tiles_max = (L.rows_max + kRoleTileRows - 1) / kRoleTileRows;
+  L.rows_max = n + (int64_t)n_groups * (kRoleTileMax - 1);
+  L.tiles_max = (L.rows_max + kRoleTileMin - 1) / kRoleTileMin;
   L.n_blocks = (n + kBlock - 1) / kBlock;
-  const size_t rb = align256(sizeof(int32_t) * (size_t)(L.tiles_max * kRoleTileRows));
+  const size_t rb = align256(sizeof(int32_t) * (size_t)(L.tiles_max * kRoleTileMin));
   const size_t cb = align256(sizeof(int32_t) * (size_t)(L.n_blocks * kMaxGroups));
   L.perm = 0;
   L.prompt = L.perm + rb;
@@ -189,16 +192,18 @@ maestro_status launch_role_lengths(const maestro_predictor& p, const maestro_rol
   int32_t* offsets = reinterpret_cast<int32_t*>(ws + L.offsets);
   int32_t* tile_group = reinterpret_cast<int32_t*>(ws + L.tile_group);
   int32_t* n_tiles = reinterpret_cast<int32_t*>(ws + L.n_tiles);
+  const int32_t tile_rows = role_tile_rows(p);
+  const int64_t tiles_max = (L.rows_max + tile_rows - 1) / tile_rows;
   const dim3 grid((unsigned)L.n_blocks), block(kBlock);
   role_count_kernel<<<grid, block, 0, stream>>>(n, role_id, r.n_roles, r.role_regressor, r.n_regressors, counts);
-  role_plan_kernel<<<dim3(1), block, 0, stream>>>((int32_t)L.n_blocks, r.n_regressors, counts, offsets, tile_group,
-                                                 perm, prompt_p, model_p, p_bits, n_tiles);
+  role_plan_kernel<<<dim3(1), block, 0, stream>>>((int32_t)L.n_blocks, r.n_regressors, tile_rows, counts, offsets,
+                                                 tile_group, perm, prompt_p, model_p, p_bits, n_tiles);
   role_scatter_kernel<<<grid, block, 0, stream>>>(n, role_id, r.n_roles, r.role_regressor, r.n_regressors, offsets,
                                                   prompt_len, model_id, p_tool, perm, prompt_p, model_p, p_bits);
   const maestro_status st = launch_status();
   if (st != MAESTRO_OK) return st;
   return launch_role_regressors(p, n, x, r.tool_coef, r.max_len, tile_group, perm, prompt_p, model_p, p_bits, n_tiles,
-                                L.tiles_max, kv_bytes_per_token, n_models, pred_len, kv_bytes, stream);
+                                tiles_max, kv_bytes_per_token, n_models, pred_len, kv_bytes, stream);
 }
 
 }  // namespace maestro
