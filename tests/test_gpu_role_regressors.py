@@ -77,7 +77,8 @@ def check(w, rr, role, pt, pl_in, kv_in, got, ref, rows=None, role_regressor=Non
 @pytest.mark.parametrize("name,n", [("c1", 1), ("c1", 7), ("c1", 129), ("c1", 1000), ("c1", None), ("c4", 1000),
                                     ("c4", 4097)])
 def test_role_regressors_match_oracle(name, n):
-    # mid (256-512-512-64) and wide (256-1024-1024-64) regressors; ragged 128-row tiles per regressor
+    # mid (256-512-512-64) and wide (256-1024-1024-64) regressors; ragged tiles per regressor (256 rows
+    # with the two row groups of the mid network, 128 with the one of the wide)
     w = W.workload(name) if n is None else W.workload(name, n_stages=n)
     tp, rr = W.two_phase_inputs(w), W.role_regressor_inputs(w)
     pt, pl, kv = _first_phase(w, tp)
