@@ -132,6 +132,25 @@ def test_role_map_edge_cases():
     assert (got[0] == pl).all()                      # role 2 has no regressor: nothing changes
 
 
+@pytest.mark.parametrize("n", [255, 256, 257, 512])
+def test_role_tiles_at_tile_boundaries(n):
+    # every stage on one regressor (role 0's), so its rows fill whole 256-row tiles of the mid
+    # network's two row groups exactly (256, 512) or leave one padding row (255) or one row on a
+    # tile of its own (257)
+    w = W.workload("c1", n_stages=n)
+    rr = W.role_regressor_inputs(w)
+    assert rr.role_group[0] >= 0
+    tp = W.two_phase_inputs(w)
+    pt, pl, kv = (a.cpu().numpy() for a in _first_phase(w, tp))
+    role = np.zeros(n, np.int32)
+    got = gpu_roles(w.x, rr, w.prompt_len, w.model_id, role, pt, w.kv_bytes_per_token, pl, kv)
+    ref = oracle.predict_role_lengths(w.x, rr.weights, rr.biases, rr.role_group, rr.tool_coef, rr.max_len,
+                                      w.prompt_len, w.model_id, role, pt, w.kv_bytes_per_token, w.spec.dtype,
+                                      pl, kv)
+    own = check(w, rr, role, pt, pl, kv, got, ref)
+    assert own.all()
+
+
 def test_two_phase_with_role_regressors_end_to_end():
     # oracle two-phase -> oracle regressors against GPU two-phase -> GPU regressors: the lengths
     # of stages with a regressor within the bar (p_tool now also differs within its own bar)
